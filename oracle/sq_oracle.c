@@ -1,0 +1,325 @@
+/*
+ * ShiftQuant backward path: CPU ORACLE.  TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, single-threaded C implementation of what the GPU path
+ * computes, written from "Towards Accurate and Efficient Sub-8-Bit Integer
+ * Training" (arXiv 2411.10948).  Only the tests, the smoke check and the
+ * benchmark's CPU-baseline leg may load it; the product library never does.
+ * It shares no code, header or table with the HIP sources.
+ *
+ * Floating point: IEEE binary32, round-to-nearest-even, no contraction
+ * (built with -ffp-contract=off -fno-fast-math), denormals kept.
+ * Integer GEMMs accumulate in int64 and are range-checked against int32.
+ *
+ * Readings of the paper that these functions follow (the paper is silent,
+ * ambiguous or self-inconsistent on each):
+ *  R1 thresholds decrease from tau_0 = r_max: tau_g = r_max * 2^-g and the
+ *     0-indexed group g holds channel ranges in (tau_{g+1}, tau_g]; the last
+ *     group also takes everything down to 0 (Sec. 3.1 grouping objective
+ *     constraints and the power-of-two threshold equation).
+ *  R2 the range of a channel is its absolute maximum and the zero point is 0
+ *     (symmetric quantization; Eq. dq_mm_f has no zero-point term).
+ *  R3 b-bit codes take values in [-Q, Q] with Q = 2^(b-1) - 1.
+ *  R4 group 0 (the one that holds r_max) uses the step r_max / Q and group g
+ *     the step (r_max / Q) * 2^-g (App. D per-group formula, 0-indexed).
+ *  R5 scaling multiplies by the scale s = fl(Q / r_max) * 2^g, as App. B
+ *     writes SR(X S) S^-1; the dequantization factor is fl(r_max / Q).
+ *  R6 deterministic rounding is round-half-to-even; stochastic rounding draws
+ *     its uniform from Philox4x32-10 (see sqo_quantize_grad).
+ *  R7 codes are clamped to [-Q, Q] after rounding.
+ *  R8 the dgrad accumulator is the left-shift form of App. D (each group's
+ *     product shifted left by N_G-1-g); the wgrad accumulator is unshifted and
+ *     its group scale is applied per output row.
+ *  R9 a tensor whose absolute maximum is NaN/Inf is flagged NONFINITE, one
+ *     whose maximum is below 2^-96 (including 0) is flagged ZERO; both give
+ *     all-zero codes, every channel in the last group and zero scales.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define SQO_OK 0
+#define SQO_ERR_ARG 1
+#define SQO_ERR_RANGE 2
+
+#define SQO_FLAG_NONFINITE 1u
+#define SQO_FLAG_ZERO 2u
+
+typedef struct {
+    float r_max;   /* tau_0: absolute maximum of the tensor               */
+    float inv0;    /* s_{G_B} = fl(Q / r_max): scale of group 0            */
+    float d0;      /* s_{G_B}^-1 = fl(r_max / Q): step of group 0          */
+    uint32_t flags;
+} sqo_scale;
+
+static uint32_t f2u(float f) { uint32_t u; memcpy(&u, &f, 4); return u; }
+static float u2f(uint32_t u) { float f; memcpy(&f, &u, 4); return f; }
+
+/* 2^k as a float, exact for -126 <= k <= 127 (built from its bit pattern). */
+static float pow2f(int k) { return u2f((uint32_t)(k + 127) << 23); }
+
+static int32_t qmax_of(int bits) { return (1 << (bits - 1)) - 1; }
+
+/* ---------------------------------------------------------------------------
+ * Philox4x32-10, Salmon, Moraes, Dror and Shaw, "Parallel random numbers: as
+ * easy as 1, 2, 3", SC'11.  One round maps the counter (x0,x1,x2,x3) with key
+ * (k0,k1) through two 32x32->64-bit products with the multipliers
+ * 0xD2511F53 and 0xCD9E8D57; the key is bumped by the Weyl constants
+ * 0x9E3779B9 and 0xBB67AE85 between rounds.
+ * ------------------------------------------------------------------------- */
+void sqo_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    uint32_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; ++round) {
+        uint64_t p0 = (uint64_t)0xD2511F53u * x0;
+        uint64_t p1 = (uint64_t)0xCD9E8D57u * x2;
+        uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        uint32_t y0 = hi1 ^ x1 ^ k0;
+        uint32_t y1 = lo1;
+        uint32_t y2 = hi0 ^ x3 ^ k1;
+        uint32_t y3 = lo0;
+        x0 = y0; x1 = y1; x2 = y2; x3 = y3;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
+}
+
+/* The 24-bit uniform integer that stochastic rounding compares against for
+ * the element with logical index idx = m * C + c: counter = (idx / 4 split
+ * into two words, offset split into two words), key = seed split into two
+ * words, word idx % 4 of the output, top 24 bits. */
+uint32_t sqo_sr_uniform24(uint64_t idx, uint64_t seed, uint64_t offset)
+{
+    uint64_t blk = idx >> 2;
+    uint32_t ctr[4] = {(uint32_t)blk, (uint32_t)(blk >> 32), (uint32_t)offset, (uint32_t)(offset >> 32)};
+    uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t w[4];
+    sqo_philox4x32_10(ctr, key, w);
+    return w[idx & 3u] >> 8;
+}
+
+/* ---------------------------------------------------------------------------
+ * Sec. 3.1: r_i is the range of channel i (R2: its absolute maximum).
+ * The absolute value is taken on the bit pattern (sign bit cleared) and the
+ * maximum on the unsigned pattern, which orders every non-NaN float by value
+ * and places NaN above +Inf.  nonfinite is set when any element is NaN/Inf.
+ * ------------------------------------------------------------------------- */
+int sqo_channel_range(const float* x, int64_t M, int64_t C, int64_t ld, float* r, int* nonfinite)
+{
+    if (!x || !r || M < 0 || C < 0 || ld < C) return SQO_ERR_ARG;
+    int nf = 0;
+    for (int64_t c = 0; c < C; ++c) {
+        uint32_t best = 0;
+        for (int64_t m = 0; m < M; ++m) {
+            uint32_t a = f2u(x[m * ld + c]) & 0x7FFFFFFFu;
+            if (a >= 0x7F800000u) nf = 1;
+            if (a > best) best = a;
+        }
+        r[c] = u2f(best);
+    }
+    if (nonfinite) *nonfinite = nf;
+    return SQO_OK;
+}
+
+/* Sec. 3.1, power-of-two grouping (R1): group g of channel c is the first g
+ * whose lower threshold tau_{g+1} = r_max * 2^-(g+1) lies strictly below r_c;
+ * the last group N_G-1 takes the rest (tau_{N_G} = 0). */
+int sqo_group_of(float r_c, float r_max, int num_groups)
+{
+    for (int g = 0; g < num_groups - 1; ++g) {
+        float tau_next = r_max * pow2f(-(g + 1));
+        if (r_c > tau_next) return g;
+    }
+    return num_groups - 1;
+}
+
+static int check_qparams(int bits, int num_groups)
+{
+    return (bits >= 2 && bits <= 8 && num_groups >= 1 && num_groups <= 8) ? SQO_OK : SQO_ERR_ARG;
+}
+
+/* ---------------------------------------------------------------------------
+ * ShiftQuant of the output gradient G_B = dY [M, C] (App. D, App. B Eq. sq).
+ *   Q = 2^(bits-1) - 1, s = fl(Q / r_max), d = fl(r_max / Q)     (R3, R5)
+ *   channel c in group g_c uses the scale s * 2^{g_c}              (R4)
+ *   v = fl(x * (s * 2^{g_c}))
+ *   round_mode 0: q = clamp(round_half_even(v), -Q, Q)             (R6, R7)
+ *   round_mode 1: l = floor(v), f = fl(v - l);  q = l + 1 with probability
+ *     f (App. B Eq. sq), realised as [u24 < f * 2^24] with u24 from
+ *     sqo_sr_uniform24(m * C + c, seed, offset); then clamp.
+ * Outputs q [M, C] (row stride C), g [C], *scale.
+ * ------------------------------------------------------------------------- */
+int sqo_quantize_grad(const float* dY, int64_t M, int64_t C, int64_t ld, int bits, int num_groups,
+                      int round_mode, uint64_t seed, uint64_t offset,
+                      int8_t* q, uint8_t* g, float* r_out, sqo_scale* scale)
+{
+    if (!dY || !q || !g || !scale || M < 0 || C < 0 || ld < C) return SQO_ERR_ARG;
+    if (check_qparams(bits, num_groups) || (round_mode != 0 && round_mode != 1)) return SQO_ERR_ARG;
+    const int32_t Q = qmax_of(bits);
+
+    /* channel ranges r_c and the tensor range tau_0 = r_max */
+    float* r = r_out ? r_out : (float*)malloc(sizeof(float) * (size_t)(C > 0 ? C : 1));
+    if (!r) return SQO_ERR_ARG;
+    int nonfinite = 0;
+    sqo_channel_range(dY, M, C, ld, r, &nonfinite);
+    uint32_t rmax_bits = 0;
+    for (int64_t c = 0; c < C; ++c)
+        if (f2u(r[c]) > rmax_bits) rmax_bits = f2u(r[c]);
+    float r_max = u2f(rmax_bits);
+    scale->r_max = r_max;
+    scale->flags = 0;
+    if (nonfinite) scale->flags = SQO_FLAG_NONFINITE;
+    else if (r_max < pow2f(-96)) scale->flags = SQO_FLAG_ZERO;
+    if (scale->flags) {
+        scale->inv0 = 0.0f;
+        scale->d0 = 0.0f;
+        for (int64_t c = 0; c < C; ++c) g[c] = (uint8_t)(num_groups - 1);
+        memset(q, 0, (size_t)(M * C));
+        if (!r_out) free(r);
+        return SQO_OK;
+    }
+    scale->inv0 = (float)Q / r_max;
+    scale->d0 = r_max / (float)Q;
+
+    /* group of each channel */
+    for (int64_t c = 0; c < C; ++c) g[c] = (uint8_t)sqo_group_of(r[c], r_max, num_groups);
+    if (!r_out) free(r);
+
+    const float two24 = pow2f(24);
+    for (int64_t m = 0; m < M; ++m) {
+        for (int64_t c = 0; c < C; ++c) {
+            float s_c = scale->inv0 * pow2f(g[c]);
+            float v = dY[m * ld + c] * s_c;
+            float qf;
+            if (round_mode == 0) {
+                qf = rintf(v);
+            } else {
+                float l = floorf(v);
+                float f = v - l;
+                uint32_t u = sqo_sr_uniform24((uint64_t)(m * C + c), seed, offset);
+                qf = ((float)u < f * two24) ? l + 1.0f : l;
+            }
+            if (qf > (float)Q) qf = (float)Q;
+            if (qf < (float)-Q) qf = (float)-Q;
+            q[m * C + c] = (int8_t)(int32_t)qf;
+        }
+    }
+    return SQO_OK;
+}
+
+/* Per-tensor symmetric quantization of W or X: the paper's INT8 baseline
+ * quantizes weights, activations and gradients per tensor (Sec. 5.1).
+ *   a = max |T|, s = fl(Q / a), d = fl(a / Q), t = clamp(rint(fl(T * s)), -Q, Q)
+ * Same flag rules as the gradient quantizer (R9).  Output q [rows, cols]. */
+int sqo_quantize_tensor(const float* T, int64_t rows, int64_t cols, int64_t ld, int bits,
+                        int8_t* q, sqo_scale* scale)
+{
+    if (!T || !q || !scale || rows < 0 || cols < 0 || ld < cols || bits < 2 || bits > 8) return SQO_ERR_ARG;
+    const int32_t Q = qmax_of(bits);
+    uint32_t amax = 0;
+    int nonfinite = 0;
+    for (int64_t i = 0; i < rows; ++i)
+        for (int64_t j = 0; j < cols; ++j) {
+            uint32_t a = f2u(T[i * ld + j]) & 0x7FFFFFFFu;
+            if (a >= 0x7F800000u) nonfinite = 1;
+            if (a > amax) amax = a;
+        }
+    float a = u2f(amax);
+    scale->r_max = a;
+    scale->flags = nonfinite ? SQO_FLAG_NONFINITE : (a < pow2f(-96) ? SQO_FLAG_ZERO : 0u);
+    if (scale->flags) {
+        scale->inv0 = 0.0f;
+        scale->d0 = 0.0f;
+        memset(q, 0, (size_t)(rows * cols));
+        return SQO_OK;
+    }
+    scale->inv0 = (float)Q / a;
+    scale->d0 = a / (float)Q;
+    for (int64_t i = 0; i < rows; ++i)
+        for (int64_t j = 0; j < cols; ++j) {
+            float v = rintf(T[i * ld + j] * scale->inv0);
+            if (v > (float)Q) v = (float)Q;
+            if (v < (float)-Q) v = (float)-Q;
+            q[i * cols + j] = (int8_t)(int32_t)v;
+        }
+    return SQO_OK;
+}
+
+/* ---------------------------------------------------------------------------
+ * Loss propagation (Eq. dq_mm_f and App. D, left-shift form, R8):
+ *   A[n, k] = sum_c  (q[n, c] * wq[c, k]) << (N_G - 1 - g_c)
+ * ShiftMM (Sec. 3.2) shifts each product before it is accumulated; that is
+ * what this loop does, in int64.  q [M, C_out], wq [C_out, C_in] (W in the
+ * PyTorch layout, so dX = dY . W).  Only the rows listed in `rows` (or all
+ * rows when rows == NULL) are computed, into A [n_rows, C_in].
+ * ------------------------------------------------------------------------- */
+int sqo_dgrad(const int8_t* q, int64_t M, int64_t C_out, const uint8_t* g, int num_groups,
+              const int8_t* wq, int64_t C_in, const int64_t* rows, int64_t n_rows, int32_t* A)
+{
+    if (!q || !g || !wq || !A || num_groups < 1 || num_groups > 8) return SQO_ERR_ARG;
+    int64_t nr = rows ? n_rows : M;
+    for (int64_t i = 0; i < nr; ++i) {
+        int64_t n = rows ? rows[i] : i;
+        if (n < 0 || n >= M) return SQO_ERR_ARG;
+        for (int64_t k = 0; k < C_in; ++k) {
+            int64_t acc = 0;
+            for (int64_t c = 0; c < C_out; ++c) {
+                int shift = num_groups - 1 - (int)g[c];
+                int64_t prod = (int64_t)q[n * C_out + c] * (int64_t)wq[c * C_in + k];
+                acc += prod * ((int64_t)1 << shift);
+            }
+            if (acc > INT32_MAX || acc < INT32_MIN) return SQO_ERR_RANGE;
+            A[i * C_in + k] = (int32_t)acc;
+        }
+    }
+    return SQO_OK;
+}
+
+/* Weight gradient (the third training GEMM, Fig. "MMs"): inner dimension is
+ * the token index, so each output row c lies in one gradient group:
+ *   B[c, k] = sum_m q[m, c] * xq[m, k]            (unshifted, R8)
+ * q [M, C_out], xq [M, C_in]; rows lists output channels c (NULL = all). */
+int sqo_wgrad(const int8_t* q, int64_t M, int64_t C_out, const int8_t* xq, int64_t C_in,
+              const int64_t* rows, int64_t n_rows, int32_t* B)
+{
+    if (!q || !xq || !B) return SQO_ERR_ARG;
+    int64_t nr = rows ? n_rows : C_out;
+    for (int64_t i = 0; i < nr; ++i) {
+        int64_t c = rows ? rows[i] : i;
+        if (c < 0 || c >= C_out) return SQO_ERR_ARG;
+        for (int64_t k = 0; k < C_in; ++k) {
+            int64_t acc = 0;
+            for (int64_t m = 0; m < M; ++m)
+                acc += (int64_t)q[m * C_out + c] * (int64_t)xq[m * C_in + k];
+            if (acc > INT32_MAX || acc < INT32_MIN) return SQO_ERR_RANGE;
+            B[i * C_in + k] = (int32_t)acc;
+        }
+    }
+    return SQO_OK;
+}
+
+/* Dequantization of the dgrad accumulator (Eq. dq_mm_f: the product of the two
+ * inverse scales stays outside the integer sum; App. D left-shift form adds
+ * 2^-(N_G-1) for the 0-indexed groups):
+ *   alpha = fl(fl(d_G * d_W) * 2^-(N_G-1)),   dX = fl(float(A) * alpha). */
+void sqo_dequant_dgrad(const int32_t* A, int64_t n, float d_grad, float d_w, int num_groups, float* out)
+{
+    float alpha = (d_grad * d_w) * pow2f(-(num_groups - 1));
+    for (int64_t i = 0; i < n; ++i) out[i] = (float)A[i] * alpha;
+}
+
+/* Dequantization of the wgrad accumulator: output row c carries its group's
+ * step d_G * 2^-g_c times the activation step d_X:
+ *   beta_c = fl(fl(d_G * d_X) * 2^-g_c),      dW[c, k] = fl(float(B[c, k]) * beta_c). */
+void sqo_dequant_wgrad(const int32_t* B, int64_t n_rows, int64_t C_in, const uint8_t* g_rows,
+                       float d_grad, float d_x, float* out)
+{
+    for (int64_t i = 0; i < n_rows; ++i) {
+        float beta = (d_grad * d_x) * pow2f(-(int)g_rows[i]);
+        for (int64_t k = 0; k < C_in; ++k) out[i * C_in + k] = (float)B[i * C_in + k] * beta;
+    }
+}

@@ -1,0 +1,443 @@
+"""Pins for the CPU oracle: each test ties the oracle to something other than
+itself -- published known answers, closed forms from the paper, invariants,
+library routines on special cases, or brute force.
+
+The paper's passages are cited by section and equation name.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2411_10948_amd import workloads
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _qmax(bits):
+    return (1 << (bits - 1)) - 1
+
+
+def _load_rows(name):
+    rows = []
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                rows.append(line.split())
+    return rows
+
+
+# --------------------------------------------------------------------------
+# Philox4x32-10 (the counter-based generator behind stochastic rounding)
+# --------------------------------------------------------------------------
+def test_philox_known_answers():
+    rows = _load_rows("philox4x32_10_kat.txt")
+    assert len(rows) == 3
+    for r in rows:
+        vals = [int(v, 16) for v in r]
+        out = oracle.philox4x32_10(vals[0:4], vals[4:6])
+        assert [int(x) for x in out] == vals[6:10]
+
+
+def test_sr_uniform_is_uniform_and_keyed():
+    # chi-square of the 24-bit draws over 64 equal bins (top 6 bits)
+    n = 1 << 16
+    u = np.array([oracle.sr_uniform24(i, 7, 3) for i in range(n)], dtype=np.uint32)
+    assert u.max() < (1 << 24)
+    counts = np.bincount(u >> 18, minlength=64)
+    exp = n / 64
+    chi2 = float(((counts - exp) ** 2 / exp).sum())
+    # 63 degrees of freedom: p = 1e-4 quantile is about 113
+    assert chi2 < 113, chi2
+    # the four words of one Philox block feed four consecutive indices
+    w = oracle.philox4x32_10([5, 0, 3, 0], [7, 0])
+    assert [oracle.sr_uniform24(20 + j, 7, 3) for j in range(4)] == [int(x) >> 8 for x in w]
+    # different seed / offset give different streams
+    assert oracle.sr_uniform24(123, 7, 3) != oracle.sr_uniform24(123, 8, 3)
+    assert oracle.sr_uniform24(123, 7, 3) != oracle.sr_uniform24(123, 7, 4)
+
+
+# --------------------------------------------------------------------------
+# Channel range (Sec. 3.1: r_i is the range of channel i; reading: abs-max)
+# --------------------------------------------------------------------------
+def test_channel_range_matches_numpy():
+    rng = np.random.default_rng(1)
+    x = (rng.standard_normal((37, 19)) * rng.lognormal(0, 2, 19)).astype(np.float32)
+    x[3, 4] = -1e30
+    r, nf = oracle.channel_range(x)
+    np.testing.assert_array_equal(r, np.abs(x).max(axis=0))
+    assert not nf
+    x[5, 7] = np.nan
+    _, nf = oracle.channel_range(x)
+    assert nf
+    x[5, 7] = -np.inf
+    r, nf = oracle.channel_range(x)
+    assert nf and np.isinf(r[7])
+
+
+# --------------------------------------------------------------------------
+# Power-of-two grouping (Sec. 3.1)
+# --------------------------------------------------------------------------
+def test_grouping_hand_table():
+    for r_c, g in _load_rows("grouping_rmax8_ng4.txt"):
+        assert oracle.group_of(np.float32(float(r_c)), 8.0, 4) == int(g), r_c
+
+
+def _group_closed_form(r_c, r_max, num_groups):
+    # group g holds (r_max 2^-(g+1), r_max 2^-g]  <=>  g = ceil(log2(r_max / r_c)) - 1
+    if r_c == 0:
+        return num_groups - 1
+    return min(num_groups - 1, max(0, math.ceil(math.log2(r_max / r_c)) - 1))
+
+
+@pytest.mark.parametrize("num_groups", [1, 2, 3, 4, 6, 8])
+def test_grouping_closed_form_random(num_groups):
+    rng = np.random.default_rng(num_groups)
+    r_max = np.float32(rng.lognormal(0, 3))
+    r = (r_max * np.exp2(-rng.uniform(0, num_groups + 2, 4000))).astype(np.float32)
+    r = np.minimum(r, r_max)
+    for rc in r:
+        lg = math.log2(float(r_max) / float(rc))
+        if abs(lg - round(lg)) < 1e-9:      # boundaries are pinned separately
+            continue
+        assert oracle.group_of(rc, r_max, num_groups) == _group_closed_form(float(rc), float(r_max), num_groups)
+
+
+@pytest.mark.parametrize("num_groups", [2, 4, 8])
+def test_grouping_boundaries_exact(num_groups):
+    # r_c exactly on a threshold belongs to the group below it (interval closed above)
+    for r_max in [np.float32(1.0), np.float32(3.0), np.float32(1e-20), np.float32(7e30)]:
+        for j in range(0, num_groups + 1):
+            t = np.float32(np.ldexp(np.float64(r_max), -j))
+            up = np.nextafter(t, np.float32(np.inf))
+            dn = np.nextafter(t, np.float32(0))
+            exp_t = min(j, num_groups - 1)          # (tau_{j+1}, tau_j] holds t
+            assert oracle.group_of(t, r_max, num_groups) == exp_t
+            if j >= 1:
+                assert oracle.group_of(up, r_max, num_groups) == min(j - 1, num_groups - 1)
+            assert oracle.group_of(dn, r_max, num_groups) == min(j, num_groups - 1)
+
+
+# --------------------------------------------------------------------------
+# Quantizer: range, step and error invariants (App. B, App. D)
+# --------------------------------------------------------------------------
+def _grad(M=64, C=48, seed=0, s=2.0):
+    return workloads.make_grad(M, C, seed=seed, sigma_s=s, outlier_frac=0.05, outlier_factor=100.0)
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4, 5, 6, 7, 8])
+@pytest.mark.parametrize("num_groups", [1, 2, 4, 6])
+@pytest.mark.parametrize("round_mode", [0, 1])
+def test_codes_in_range_and_top_maps_to_Q(bits, num_groups, round_mode):
+    x = _grad(seed=bits * 10 + num_groups)
+    q, g, s, r = oracle.quantize_grad(x, bits, num_groups, round_mode, seed=1, offset=2)
+    Q = _qmax(bits)
+    assert np.abs(q.astype(np.int32)).max() == Q
+    assert q.min() >= -Q and q.max() <= Q
+    # the element that sets r_max sits in group 0 and maps to +-Q
+    m, c = np.unravel_index(np.argmax(np.abs(x)), x.shape)
+    assert g[c] == 0
+    assert abs(int(q[m, c])) == Q
+    assert s["flags"] == 0
+    assert s["r_max"] == np.abs(x).max()
+
+
+@pytest.mark.parametrize("bits", [2, 4, 6, 8])
+@pytest.mark.parametrize("num_groups", [1, 3, 4, 8])
+def test_rtn_half_step_error_bound(bits, num_groups):
+    # App. D: each group is quantized with step Delta_g = (r_max / Q) * 2^-g; with
+    # round-to-nearest every element is within Delta_g / 2 of its code's value.
+    x = _grad(M=96, C=40, seed=bits + 100 * num_groups, s=2.5)
+    q, g, s, _ = oracle.quantize_grad(x, bits, num_groups, 0)
+    Q = _qmax(bits)
+    step = (np.float64(s["r_max"]) / Q) * np.exp2(-g.astype(np.float64))
+    err = np.abs(q.astype(np.float64) * step[None, :] - x.astype(np.float64))
+    # slack: the fp32 scale and product each round once (<= 2^-23 relative of |x|)
+    slack = step[None, :] * 0.5 * (1 + 1e-6) + np.abs(x) * 2.0 ** -22
+    assert np.all(err <= slack)
+    # the step is the one App. D prescribes, not a coarser one
+    for c in range(x.shape[1]):
+        r_c = np.abs(x[:, c]).max()
+        if r_c > 0:
+            assert r_c <= step[c] * Q * (1 + 1e-6)          # no clamping needed
+            if g[c] < num_groups - 1:
+                assert r_c > step[c] * Q / 2 * (1 - 1e-6)  # channel fills at least half its range
+
+
+def test_scale_invariance_power_of_two():
+    # Sec. 3.1 worked example: tau_p = 2 tau_q and r_i = 2 r_j give the same
+    # grouping loss, so scaling the tensor by 2^k changes no group and no code.
+    x = _grad(M=50, C=33, seed=5)
+    for mode in [0, 1]:
+        q0, g0, s0, _ = oracle.quantize_grad(x, 4, 4, mode, seed=9, offset=1)
+        for k in [-20, -3, 1, 7, 30]:
+            xs = (x.astype(np.float64) * 2.0 ** k).astype(np.float32)
+            q1, g1, s1, _ = oracle.quantize_grad(xs, 4, 4, mode, seed=9, offset=1)
+            np.testing.assert_array_equal(g0, g1)
+            np.testing.assert_array_equal(q0, q1)
+            assert np.float64(s1["d0"]) == np.float64(s0["d0"]) * 2.0 ** k
+            assert np.float64(s1["inv0"]) == np.float64(s0["inv0"]) * 2.0 ** -k
+
+
+@pytest.mark.parametrize("bits", [2, 4, 6, 8])
+def test_single_group_is_per_tensor_symmetric(bits):
+    # With N_G = 1 ShiftQuant reduces to per-tensor symmetric quantization, the
+    # paper's INT8 baseline (Sec. 5.1).  Independent textbook version:
+    x = _grad(M=70, C=21, seed=bits)
+    Q = _qmax(bits)
+    amax = np.float32(np.abs(x).max())
+    scale = np.float32(np.float32(Q) / amax)
+    ref = np.clip(np.rint(x * scale), -Q, Q).astype(np.int8)
+    q, g, s, _ = oracle.quantize_grad(x, bits, 1, 0)
+    np.testing.assert_array_equal(q, ref)
+    assert np.all(g == 0)
+    qt, st = oracle.quantize_tensor(x, bits)
+    np.testing.assert_array_equal(qt, ref)
+    assert st["d0"] == np.float32(amax / np.float32(Q))
+
+
+def test_round_half_to_even_ties():
+    # r_max = Q * 2^k makes the scale an exact power of two, so x = (n + 1/2) 2^k
+    # scales to an exact tie; reading R6 rounds ties to even.
+    Q = 7
+    k = -3
+    x = np.zeros((1, 8), np.float32)
+    x[0, 0] = Q * 2.0 ** k
+    x[0, 1:] = np.array([0.5, 1.5, 2.5, -0.5, -1.5, -2.5, 3.5], np.float32) * 2.0 ** k
+    q, g, s, _ = oracle.quantize_grad(x, 4, 1, 0)
+    assert s["inv0"] == np.float32(2.0 ** -k)
+    assert q[0].tolist() == [7, 0, 2, 2, 0, -2, -2, 4]
+
+
+# --------------------------------------------------------------------------
+# Stochastic rounding (App. B Eq. sq, unbiasedness, Eq. varianceq / varup)
+# --------------------------------------------------------------------------
+def test_stochastic_rounding_unbiased_and_variance():
+    x = _grad(M=8, C=32, seed=11)
+    bits, ng = 4, 4
+    S = 1500
+    q0, g, s, _ = oracle.quantize_grad(x, bits, ng, 1, seed=3, offset=0)
+    step = (np.float64(s["r_max"]) / _qmax(bits)) * np.exp2(-g.astype(np.float64))
+    acc = np.zeros(x.shape)
+    acc2 = np.zeros(x.shape)
+    for off in range(S):
+        q, g2, _, _ = oracle.quantize_grad(x, bits, ng, 1, seed=3, offset=off)
+        assert np.array_equal(g, g2)
+        deq = q.astype(np.float64) * step[None, :]
+        acc += deq
+        acc2 += deq * deq
+    mean = acc / S
+    var_emp = acc2 / S - mean ** 2
+    v = x.astype(np.float64) / step[None, :]
+    lo = np.floor(v)
+    var_cf = (v - lo) * (lo + 1 - v) * step[None, :] ** 2        # (x - l)(u - x)
+    assert np.all(var_cf <= step[None, :] ** 2 / 4 * (1 + 1e-12))  # Eq. varup
+    # unbiased: |mean - x| within 5 standard errors (+ the 2^-24 step bias bound)
+    se = np.sqrt(var_cf / S)
+    assert np.all(np.abs(mean - x) <= 5 * se + step[None, :] * (2.0 ** -23) + 1e-30)
+    # variance matches the closed form: in aggregate (sum over 256 elements of
+    # Bernoulli variances, relative standard error about 1.2% at S = 1500)
+    tot_emp = float((var_emp / step[None, :] ** 2).sum())
+    tot_cf = float((var_cf / step[None, :] ** 2).sum())
+    assert abs(tot_emp - tot_cf) / tot_cf < 0.05, (tot_emp, tot_cf)
+    # and per element where p(1-p) is not tiny, within 6 standard errors
+    p = v - lo
+    pv = p * (1 - p)
+    sel = pv > 0.1
+    se_var = np.sqrt(np.maximum(pv * (1 - 4 * pv), 1e-4) / S)
+    assert np.all(np.abs(var_emp / step[None, :] ** 2 - pv)[sel] <= 6 * se_var[sel] + 0.01)
+    # each draw is one of the two neighbouring levels
+    assert np.all((q0 == lo) | (q0 == lo + 1) | (np.abs(q0) == _qmax(bits)))
+
+
+def test_stochastic_rounding_reproducible():
+    x = _grad(M=16, C=24, seed=12)
+    a = oracle.quantize_grad(x, 6, 4, 1, seed=5, offset=77)[0]
+    b = oracle.quantize_grad(x, 6, 4, 1, seed=5, offset=77)[0]
+    c = oracle.quantize_grad(x, 6, 4, 1, seed=5, offset=78)[0]
+    np.testing.assert_array_equal(a, b)
+    assert np.any(a != c)
+
+
+@pytest.mark.parametrize("num_groups", [1, 2, 3, 4, 6])
+def test_shiftquant_variance_bound(num_groups):
+    # App. B: U_dq <= 4 U_fq + 2^(-2 N_G + 2) U_cq, with U_fq the variance bound
+    # of per-channel (fine-grained) and U_cq of per-tensor (coarse) quantization.
+    # The SR variance of every element is known in closed form (Eq. varianceq).
+    bits = 4
+    Q = _qmax(bits)
+    for seed in range(5):
+        x = _grad(M=64, C=64, seed=seed + 50, s=2.0)
+        q, g, s, r = oracle.quantize_grad(x, bits, num_groups, 1, seed=1)
+        step = (np.float64(s["r_max"]) / Q) * np.exp2(-g.astype(np.float64))
+        v = x.astype(np.float64) / step[None, :]
+        lo = np.floor(v)
+        U_dq = float(((v - lo) * (lo + 1 - v) * step[None, :] ** 2).sum())
+        N, D = x.shape
+        r64 = r.astype(np.float64)
+        U_fq = N / 4 * float(((r64 / Q) ** 2).sum())
+        U_cq = N * D / 4 * (float(s["r_max"]) / Q) ** 2
+        assert U_dq <= 4 * U_fq + 2.0 ** (-2 * num_groups + 2) * U_cq
+
+
+# --------------------------------------------------------------------------
+# Flags for degenerate tensors (reading R9)
+# --------------------------------------------------------------------------
+def test_flags_zero_tiny_nonfinite():
+    z = np.zeros((5, 9), np.float32)
+    q, g, s, _ = oracle.quantize_grad(z, 4, 4)
+    assert s["flags"] == oracle.FLAG_ZERO and not q.any() and np.all(g == 3) and s["d0"] == 0
+    t = np.full((5, 9), 2.0 ** -100, np.float32)
+    assert oracle.quantize_grad(t, 4, 4)[2]["flags"] == oracle.FLAG_ZERO
+    t = np.full((5, 9), 2.0 ** -96, np.float32)
+    q, g, s, _ = oracle.quantize_grad(t, 4, 4)
+    assert s["flags"] == 0 and np.all(q == 7)
+    x = _grad(M=5, C=9)
+    x[2, 3] = np.nan
+    q, g, s, _ = oracle.quantize_grad(x, 4, 4)
+    assert s["flags"] == oracle.FLAG_NONFINITE and not q.any() and s["inv0"] == 0
+    x[2, 3] = np.inf
+    assert oracle.quantize_grad(x, 4, 4)[2]["flags"] == oracle.FLAG_NONFINITE
+    e = np.zeros((0, 4), np.float32)
+    q, g, s, _ = oracle.quantize_grad(e, 4, 4)
+    assert s["flags"] == oracle.FLAG_ZERO and q.shape == (0, 4)
+
+
+# --------------------------------------------------------------------------
+# dgrad: ShiftMM (Sec. 3.2) = GEMM-based ShiftQuant (Sec. 3.2) = dequantized product
+# --------------------------------------------------------------------------
+def _close_to_product(out32, exact, abs_product):
+    # fp32 result of an exact integer sum: float(acc) and the scale product each
+    # round once (<= 3 * 2^-24 relative); the fp64 reference GEMM adds a few
+    # ulps of the absolute-value product.
+    err = np.abs(out32.astype(np.float64) - exact)
+    assert np.all(err <= 2e-7 * np.abs(exact) + 1e-13 * abs_product)
+
+
+def _layer(M, C_out, C_in, bits, ng, seed, mode=0):
+    x = _grad(M=M, C=C_out, seed=seed, s=2.0)
+    rng = np.random.default_rng(seed + 1000)
+    W = (rng.standard_normal((C_out, C_in)) * 0.02).astype(np.float32)
+    X = rng.standard_normal((M, C_in)).astype(np.float32)
+    return x, W, X
+
+
+@pytest.mark.parametrize("bits,ng", [(4, 4), (6, 4), (8, 3), (2, 8), (5, 1)])
+def test_dgrad_equals_shifted_matmul_and_group_gemms(bits, ng):
+    x, W, X = _layer(45, 70, 33, bits, ng, seed=bits * 7 + ng)
+    q, g, s, _ = oracle.quantize_grad(x, bits, ng)
+    wq, ws = oracle.quantize_tensor(W, 8)
+    A = oracle.dgrad(q, g, ng, wq)
+    sh = (ng - 1 - g.astype(np.int64))
+    # numpy int64 matmul of the left-shifted codes (App. D left-shift form)
+    ref = (q.astype(np.int64) << sh[None, :]) @ wq.astype(np.int64)
+    np.testing.assert_array_equal(A, ref)
+    # GEMM-based implementation (Sec. 3.2): one sub-GEMM per group after
+    # gathering its channels, then shift and sum
+    acc = np.zeros_like(ref)
+    for grp in range(ng):
+        idx = np.nonzero(g == grp)[0]
+        if idx.size:
+            part = q[:, idx].astype(np.int64) @ wq[idx, :].astype(np.int64)
+            acc += part << (ng - 1 - grp)
+    np.testing.assert_array_equal(A, acc)
+    # row subset gives the same rows
+    rows = np.array([44, 0, 17])
+    np.testing.assert_array_equal(oracle.dgrad(q, g, ng, wq, rows), ref[rows])
+
+
+@pytest.mark.parametrize("bits,ng", [(4, 4), (6, 4), (8, 6)])
+def test_dgrad_dequant_equals_dequantized_product(bits, ng):
+    # App. D: s_G^-1 s_W^-1 2^-(N_G-1) sum_g [Gq^g Wq^g << (N_G-1-g)] equals the
+    # product of the dequantized operands.
+    x, W, X = _layer(40, 64, 24, bits, ng, seed=3 + bits)
+    q, g, s, _ = oracle.quantize_grad(x, bits, ng)
+    wq, ws = oracle.quantize_tensor(W, 8)
+    A = oracle.dgrad(q, g, ng, wq)
+    Q = _qmax(bits)
+    step_g = np.float64(s["d0"]) * np.exp2(-g.astype(np.float64))
+    exact = (q.astype(np.float64) * step_g[None, :]) @ (wq.astype(np.float64) * np.float64(ws["d0"]))
+    alpha = np.float64(s["d0"]) * np.float64(ws["d0"]) * 2.0 ** -(ng - 1)
+    # fp64 GEMM error bound: a few ulps of the product of absolute values
+    bound = (np.abs(q.astype(np.float64)) * step_g[None, :]) @ (np.abs(wq.astype(np.float64)) * np.float64(ws["d0"]))
+    assert np.all(np.abs(A.astype(np.float64) * alpha - exact) <= 1e-13 * bound)
+    dX = oracle.dequant_dgrad(A, s["d0"], ws["d0"], ng)
+    assert np.all(np.abs(dX.astype(np.float64) - exact) <= 2e-7 * np.abs(exact) + 1e-13 * bound)
+    assert Q > 0
+
+
+def test_wgrad_equals_int64_matmul_and_dequantized_product():
+    x, W, X = _layer(77, 30, 21, 6, 4, seed=21)
+    q, g, s, _ = oracle.quantize_grad(x, 6, 4)
+    xq, xs = oracle.quantize_tensor(X, 8)
+    B = oracle.wgrad(q, xq)
+    np.testing.assert_array_equal(B, q.astype(np.int64).T @ xq.astype(np.int64))
+    step_g = np.float64(s["d0"]) * np.exp2(-g.astype(np.float64))
+    exact = (q.astype(np.float64) * step_g[None, :]).T @ (xq.astype(np.float64) * np.float64(xs["d0"]))
+    dW = oracle.dequant_wgrad(B, g, s["d0"], xs["d0"])
+    qd = np.abs(q.astype(np.float64) * step_g[None, :])
+    _close_to_product(dW, exact, qd.T @ (np.abs(xq.astype(np.float64)) * np.float64(xs["d0"])))
+    rows = np.array([29, 3])
+    np.testing.assert_array_equal(oracle.wgrad(q, xq, rows), B[rows])
+
+
+def test_gemm_brute_force_tiny():
+    # pure-Python loops on tiny shapes
+    rng = np.random.default_rng(4)
+    for trial in range(20):
+        M, C_out, C_in = rng.integers(1, 6, 3)
+        ng = int(rng.integers(1, 5))
+        q = rng.integers(-7, 8, (M, C_out)).astype(np.int8)
+        g = rng.integers(0, ng, C_out).astype(np.uint8)
+        wq = rng.integers(-127, 128, (C_out, C_in)).astype(np.int8)
+        xq = rng.integers(-127, 128, (M, C_in)).astype(np.int8)
+        A = oracle.dgrad(q, g, ng, wq)
+        B = oracle.wgrad(q, xq)
+        for n in range(M):
+            for k in range(C_in):
+                assert A[n, k] == sum(int(q[n, c]) * int(wq[c, k]) * 2 ** (ng - 1 - int(g[c]))
+                                      for c in range(C_out))
+        for c in range(C_out):
+            for k in range(C_in):
+                assert B[c, k] == sum(int(q[m, c]) * int(xq[m, k]) for m in range(M))
+
+
+def test_int32_range_is_enforced():
+    C_out = 1100
+    q = np.full((1, C_out), 127, np.int8)
+    g = np.zeros(C_out, np.uint8)
+    wq = np.full((C_out, 1), 127, np.int8)
+    with pytest.raises(oracle.RangeError):
+        oracle.dgrad(q, g, 8, wq)        # 1100 * 127 * 127 * 2^7 > 2^31
+    A = oracle.dgrad(q[:, :1000], g[:1000], 8, wq[:1000])
+    assert A[0, 0] == 1000 * 127 * 127 * 128
+
+
+def test_dequant_wgrad_row_scale_direction():
+    # a channel in group g has the finer step 2^-g: its dequantized weight
+    # gradient carries 2^-g (Eq. dq_mm_f applied to the token-inner GEMM).
+    B = np.array([[1000, -3], [1000, 5]], np.int32)
+    out = oracle.dequant_wgrad(B, np.array([0, 3], np.uint8), np.float32(0.5), np.float32(0.25))
+    assert out[0, 0] == np.float32(1000 * 0.125)
+    assert out[1, 0] == np.float32(1000 * 0.125 / 8)
+    out = oracle.dequant_dgrad(np.array([[8]], np.int32), np.float32(0.5), np.float32(0.25), 4)
+    assert out[0, 0] == np.float32(8 * 0.125 / 8)
+
+
+def test_full_small_workload_consistency():
+    d = workloads.make_inputs("linear_256")
+    res = oracle.backward(d["dY"], d["W"], d["X"], 4, 4)
+    assert res["gscale"]["flags"] == 0
+    counts = np.bincount(res["g"], minlength=4)
+    assert counts.sum() == 256 and counts[0] >= 1
+    # whole-layer fp64 check of both gradients
+    g = res["g"]
+    step_g = np.float64(res["gscale"]["d0"]) * np.exp2(-g.astype(np.float64))
+    dq = res["q"].astype(np.float64) * step_g[None, :]
+    wd = res["wq"].astype(np.float64) * np.float64(res["wscale"]["d0"])
+    xd = res["xq"].astype(np.float64) * np.float64(res["xscale"]["d0"])
+    _close_to_product(res["dX"], dq @ wd, np.abs(dq) @ np.abs(wd))
+    _close_to_product(res["dW"], dq.T @ xd, np.abs(dq).T @ np.abs(xd))
