@@ -1,0 +1,197 @@
+#!/usr/bin/env python3
+"""Benchmark of the ShiftQuant backward step on one MI355X.
+
+One step = sq_quantize_grad (dY -> codes, groups, scale) -> sq_gemm_dgrad
+(fp32 dX) -> sq_gemm_wgrad (fp32 dW) on one stream, inputs resident in HBM.
+W and X are quantized once, untimed: in training their codes come from the
+forward pass.
+
+Prints ONE JSON line.  `value` is whole-step throughput in TOPS, counting the
+two integer GEMMs as 4 * M * C_out * C_in ops (quantizer element work is not
+counted as ops).  `roofline` describes the step's dominant kernel, timed with
+HIP events on the launch stream inside the timed region; `cpu_baseline` times
+the CPU oracle on a bounded slice of the same workload.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
+PEAK_INT8_TOPS = 5000.0      # MI355X dense int8 matrix-core peak
+DEFAULT_WORKLOAD = "resnet18_conv3x3"
+KERNEL_SOURCES = ["paper_2411_10948_amd/csrc/sq_gemm.hip", "paper_2411_10948_amd/csrc/sq_quant.hip",
+                  "paper_2411_10948_amd/csrc/sq_internal.h"]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+        ent = rec.get(workload, {}).get(kernel)
+        if not ent or ent.get("kernel_source_hash") != kernel_source_hash():
+            return None
+        return ent.get("hbm_bytes_per_launch")
+    except (OSError, ValueError):
+        return None
+
+
+def cpu_baseline(inputs, wl, budget_s: float = 10.0):
+    """The CPU oracle (single-threaded C) on the first rows of the same layer."""
+    import oracle
+    dY, W, X = inputs["dY"], inputs["W"], inputs["X"]
+    M = dY.shape[0]
+
+    def run(rows):
+        t0 = time.perf_counter()
+        oracle.backward(dY[:rows], W, X[:rows], wl.bits, wl.num_groups, wl.round_mode, wl.sr_seed, wl.sr_offset)
+        return time.perf_counter() - t0
+
+    rows = max(1, min(M, M // 256))
+    t = run(rows)
+    rows = int(min(M, max(rows, rows * budget_s / max(t, 1e-3))))
+    t = run(rows)
+    ops = 4 * rows * wl.C_out * wl.C_in
+    return {"value": ops / t / 1e12, "unit": "TOPS", "cores": 1, "kind": "oracle",
+            "sample": f"oracle quantize+dgrad+wgrad+dequant on the first {rows} of {M} token rows "
+                      f"({ops / 1e9:.2f} Gop in {t:.2f} s, 1 thread)"}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the ShiftQuant path is single-GPU, see DESIGN.md for how it would shard)", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2411_10948_amd import shiftquant as sq
+    from paper_2411_10948_amd import workloads
+
+    if not os.path.exists(sq.LIB_PATH):
+        from paper_2411_10948_amd import build
+        build.build()
+    sq.load()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    wl = workloads.WORKLOADS[args.workload]
+    inputs = workloads.make_inputs(args.workload)
+    M, C_out, C_in = inputs["M"], wl.C_out, wl.C_in
+    print(f"[bench] {args.workload}: M={M} C_out={C_out} C_in={C_in} b={wl.bits} N_G={wl.num_groups} "
+          f"round={'SR' if wl.round_mode else 'RTN'}", file=sys.stderr, flush=True)
+
+    dev = torch.device("cuda:0")
+    dY = torch.from_numpy(inputs["dY"]).to(dev)
+    W = torch.from_numpy(inputs["W"]).to(dev)
+    X = torch.from_numpy(inputs["X"]).to(dev)
+    params = sq.Params.make(wl.bits, wl.num_groups, wl.round_mode, wl.sr_seed, wl.sr_offset)
+    wq_t, ws = sq.quantize_tensor(W, 8, transpose=True)
+    xq_t, xs = sq.quantize_tensor(X, 8, transpose=True)
+    del W, X
+    plan = sq.BackwardPlan(M, C_out, C_in, params, device=dev)
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        plan.run(dY, wq_t, ws, xq_t, xs, stream)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for k in range(K):
+        e = ev[k]
+        e[0].record(stream)
+        plan.quantize(dY, stream)
+        e[1].record(stream)
+        plan.dgrad(wq_t, ws, stream)
+        e[2].record(stream)
+        plan.wgrad(xq_t, xs, stream)
+        e[3].record(stream)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    t_quant = sum(e[0].elapsed_time(e[1]) for e in ev) / K
+    t_dgrad = sum(e[1].elapsed_time(e[2]) for e in ev) / K
+    t_wgrad = sum(e[2].elapsed_time(e[3]) for e in ev) / K
+    ms_step = total_ms / K
+    ops = 4 * M * C_out * C_in
+    value = ops / (ms_step * 1e-3) / 1e12
+
+    # algorithmic bytes / ops per launch (int8 operands read once, outputs written once)
+    parts = {
+        "sq_quantize_grad": {"ms": t_quant, "bytes": 5 * M * C_out, "ops": 0},
+        "sq_gemm_dgrad": {"ms": t_dgrad, "bytes": M * C_out + C_out * C_in + 4 * M * C_in,
+                          "ops": 2 * M * C_out * C_in},
+        "sq_gemm_wgrad": {"ms": t_wgrad, "bytes": M * C_out + M * C_in + 4 * C_out * C_in,
+                          "ops": 2 * M * C_out * C_in},
+    }
+    dom = max(parts, key=lambda k: parts[k]["ms"])
+    d = parts[dom]
+    balance = PEAK_INT8_TOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if d["ops"] and d["ops"] / d["bytes"] > balance:
+        achieved = d["ops"] / (d["ms"] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_INT8_TOPS, "unit": "TOPS"}
+    else:
+        achieved = d["bytes"] / (d["ms"] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = measured_traffic(args.workload, dom)
+    roof["kernel"] = dom
+    roof["algorithmic_bytes"] = d["bytes"]
+    roof["algorithmic_ops"] = d["ops"]
+    roof["avg_ms"] = d["ms"]
+
+    out = {
+        "metric": "ShiftQuant backward TOPS (quantize+dgrad+wgrad) and % of int8 MFMA peak",
+        "value": value,
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "M": M, "C_out": C_out, "C_in": C_in, "bits": wl.bits,
+                   "num_groups": wl.num_groups, "rounding": "stochastic" if wl.round_mode else "nearest-even",
+                   "parallelism": "none"},
+        "pct_int8_peak": 100.0 * value / PEAK_INT8_TOPS,
+        "breakdown_ms": {k: v["ms"] for k, v in parts.items()},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a slice of the workload", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(inputs, wl)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

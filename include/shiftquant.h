@@ -1,0 +1,245 @@
+/*
+ * shiftquant.h -- C ABI of libshiftquant, the ShiftQuant backward path for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * ShiftQuant ("Towards Accurate and Efficient Sub-8-Bit Integer Training",
+ * arXiv 2411.10948) quantizes the output gradient G_B = dY [M, C_out] of a
+ * linear (or im2col'd conv) layer to b-bit integers whose channels fall into
+ * N_G groups with power-of-two scales (Sec. 3.1), so that both backward GEMMs
+ *     dX = dY . W      (loss propagation, inner dimension C_out)
+ *     dW = dY^T . X    (weight gradient,  inner dimension M)
+ * run as plain integer GEMMs with the group scales applied as bit shifts
+ * (Sec. 3.2, "ShiftMM"; App. D).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every array argument is a DEVICE pointer owned by the caller.  The
+ *    library never allocates device memory, never frees caller memory and
+ *    never synchronizes the host: all work is enqueued on `stream` (a
+ *    hipStream_t passed as void*, NULL = the default stream) and completes
+ *    in stream order.  Scratch memory is passed in as `workspace`; its size
+ *    comes from the matching *_workspace_size query.
+ *  - Matrices are row-major with a leading dimension `ld` in elements;
+ *    a buffer [rows, ld] must hold rows * ld elements.
+ *  - int8 code matrices (q_fold, q_t, wq_t, xq_t) and the workspace must be
+ *    16-byte aligned with ld a multiple of 16.  fp32/int32 arrays must be
+ *    4-byte aligned.
+ *  - Arguments are validated synchronously before anything is launched; on
+ *    failure nothing is enqueued and a status other than SQ_OK is returned.
+ *    sq_last_error() then describes the failure (thread-local).
+ *  - Data-dependent anomalies cannot be seen on the host: they are reported
+ *    in the `flags` word of the device-resident sq_scale and the codes are
+ *    then all 0 (see SQ_FLAG_*).
+ *  - Calls that share a workspace, layout or output buffer must not overlap
+ *    in time (enqueue them on one stream, or synchronize between them).
+ */
+#ifndef SHIFTQUANT_H
+#define SHIFTQUANT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SQ_OK = 0,
+    SQ_ERR_INVALID_ARGUMENT = 1,   /* null pointer, bad size, stride or alignment  */
+    SQ_ERR_OVERFLOW_RISK = 2,      /* the worst-case int32 accumulator would overflow */
+    SQ_ERR_UNSUPPORTED = 3,        /* valid request outside what this build supports */
+    SQ_ERR_WORKSPACE_TOO_SMALL = 4,
+    SQ_ERR_HIP = 5                 /* a HIP runtime call or kernel launch failed     */
+} sq_status;
+
+/* Rounding of the gradient codes. */
+enum {
+    SQ_ROUND_NEAREST_EVEN = 0,     /* round(.) of App. D, ties to even                 */
+    SQ_ROUND_STOCHASTIC = 1        /* SR of App. B, Eq. "sq", Philox4x32-10 uniforms   */
+};
+
+/* Bits of sq_scale.flags.  When either is set every code is 0, every channel
+ * is in the last group and inv = step = 0. */
+enum {
+    SQ_FLAG_NONFINITE = 1u,        /* the tensor holds NaN or +-Inf                     */
+    SQ_FLAG_ZERO = 2u              /* max |x| < 2^-96 (all-zero, tiny or empty tensor)  */
+};
+
+/* Quantizer parameters (host memory, read during the call only). */
+typedef struct {
+    int32_t bits;         /* b in [2, 8]: codes lie in [-Q, Q], Q = 2^(b-1) - 1            */
+    int32_t num_groups;   /* N_G in [1, 8] (the paper's default is 4, Sec. 5.1)            */
+    int32_t round_mode;   /* SQ_ROUND_*                                                    */
+    int32_t reserved;     /* must be 0                                                     */
+    uint64_t seed;        /* stochastic rounding: Philox key                               */
+    uint64_t offset;      /* stochastic rounding: stream offset (e.g. the training step)   */
+} sq_quant_params;
+
+/* Device-resident scale of a quantized tensor (written by the quantizers,
+ * read by the GEMMs and sq_dequant).
+ *   r_max : tau_0, the tensor's absolute maximum (Sec. 3.1)
+ *   inv   : s = fl(Q / r_max), the scale of group 0 (App. B writes SR(X S) S^-1)
+ *   step  : s^-1 = fl(r_max / Q), the quantization step of group 0
+ *   flags : SQ_FLAG_* */
+typedef struct {
+    float r_max;
+    float inv;
+    float step;
+    uint32_t flags;
+} sq_scale;
+
+/* ---------------------------------------------------------------------------
+ * Size queries (host only, no device work).
+ * ------------------------------------------------------------------------- */
+
+/* Layout descriptor of the shift-folded dgrad operand produced by
+ * sq_quantize_grad and consumed by sq_gemm_dgrad.
+ *   *layout_bytes : size of the device buffer `layout`
+ *   *min_ld_fold  : smallest admissible ld_fold for q_fold (a multiple of 16);
+ *                   q_fold rows hold C_out main columns followed, from column
+ *                   roundup(C_out, 64), by the appended columns of the fold. */
+sq_status sq_grad_layout_size(int64_t C_out, const sq_quant_params* p,
+                              size_t* layout_bytes, int64_t* min_ld_fold);
+
+sq_status sq_quantize_grad_workspace_size(int64_t M, int64_t C_out, const sq_quant_params* p,
+                                          size_t* bytes);
+sq_status sq_quantize_tensor_workspace_size(int64_t rows, int64_t cols, size_t* bytes);
+sq_status sq_gemm_dgrad_workspace_size(int64_t M, int64_t C_out, int64_t C_in,
+                                       const sq_quant_params* p, size_t* bytes);
+sq_status sq_gemm_wgrad_workspace_size(int64_t M, int64_t C_out, int64_t C_in,
+                                       const sq_quant_params* p, size_t* bytes);
+
+/* ---------------------------------------------------------------------------
+ * sq_quantize_grad -- ShiftQuant of the output gradient.
+ *
+ * Follows Sec. 3.1 (channel ranges r_c, power-of-two thresholds
+ * tau_g = r_max 2^-g), App. D (group g quantized with step
+ * (r_max / Q) 2^-g) and App. B Eq. "sq" (stochastic rounding):
+ *   r_c   = max_m |dY[m, c]|,  r_max = max_c r_c
+ *   g_c   = the group whose interval (r_max 2^-(g+1), r_max 2^-g] holds r_c,
+ *           the last group N_G - 1 also holding everything below
+ *   v     = fl(dY[m, c] * fl(inv * 2^g_c)),  inv = fl(Q / r_max)
+ *   code  = clamp(round(v), -Q, Q), round = ties-to-even or stochastic:
+ *           floor(v) + [u24 < fl(v - floor(v)) * 2^24] with u24 the top 24
+ *           bits of word (i mod 4) of Philox4x32-10(counter = (i / 4 as two
+ *           32-bit words, offset as two words), key = seed as two words),
+ *           i = m * C_out + c.
+ *
+ * Inputs : dY [M, ld_dY] fp32 (M >= 0, C_out >= 0, ld_dY >= C_out).
+ * Outputs (any of q_fold / q_t may be NULL to skip it):
+ *   q_fold [M, ld_fold] int8, the dgrad operand with the shifts of
+ *          ShiftMM folded in: column c holds code * 2^t_c with
+ *          t_c = min(N_G - 1 - g_c, T), T the largest shift with Q 2^T <= 127.
+ *          When some channel needs more than T (b >= 6 at N_G = 4), its
+ *          column is appended again after column roundup(C_out, 64), as
+ *          described by `layout`; sq_gemm_dgrad adds those columns with
+ *          the remaining powers of two.  Columns in [C_out, roundup(C_out,
+ *          64)) and beyond the appended ones are left unwritten.
+ *   q_t    [C_out, ld_t] int8 (ld_t >= M), the codes themselves, transposed:
+ *          q_t[c, m] = code(m, c); this is the wgrad operand.
+ *   group  [C_out] uint8, g_c.
+ *   scale  one sq_scale (r_max, inv, step, flags).
+ *   layout [layout_bytes], the fold descriptor for sq_gemm_dgrad.
+ * Workspace: sq_quantize_grad_workspace_size bytes.
+ * Errors: SQ_ERR_INVALID_ARGUMENT, SQ_ERR_WORKSPACE_TOO_SMALL, SQ_ERR_HIP.
+ * ------------------------------------------------------------------------- */
+sq_status sq_quantize_grad(const float* dY, int64_t M, int64_t C_out, int64_t ld_dY,
+                           const sq_quant_params* p,
+                           int8_t* q_fold, int64_t ld_fold,
+                           int8_t* q_t, int64_t ld_t,
+                           uint8_t* group, sq_scale* scale, int32_t* layout,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * sq_quantize_tensor -- per-tensor symmetric quantization of W or X.
+ *
+ * The paper's INT8 baseline quantizes weights, activations and gradients per
+ * tensor (Sec. 5.1); it is ShiftQuant with a single group:
+ *   a = max |T|,  inv = fl(Q / a),  step = fl(a / Q),
+ *   code = clamp(round_half_even(fl(T * inv)), -Q, Q),  Q = 2^(bits-1) - 1.
+ * Input : T [rows, ld] fp32 (ld >= cols).
+ * Output: transpose == 0: q [rows, ld_q] int8 (ld_q >= cols)
+ *         transpose == 1: q [cols, ld_q] int8 (ld_q >= rows), q[j, i] = code(i, j)
+ *         (sq_gemm_dgrad takes W^T codes and sq_gemm_wgrad X^T codes, i.e.
+ *         W [C_out, C_in] and X [M, C_in] quantized with transpose = 1).
+ *         scale: one sq_scale.
+ * Errors: SQ_ERR_INVALID_ARGUMENT, SQ_ERR_WORKSPACE_TOO_SMALL, SQ_ERR_HIP.
+ * ------------------------------------------------------------------------- */
+sq_status sq_quantize_tensor(const float* T, int64_t rows, int64_t cols, int64_t ld, int32_t bits,
+                             int32_t transpose, int8_t* q, int64_t ld_q, sq_scale* scale,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * sq_gemm_dgrad -- loss propagation dX = dY . W as ShiftMM.
+ *
+ * Eq. "dq_mm_f" and App. D (left-shift form): with 0-indexed groups,
+ *   acc[n, k] = sum_c (code(n, c) * wq[c, k]) << (N_G - 1 - g_c)      (int32)
+ *   dX[n, k]  = fl(float(acc[n, k]) * alpha),
+ *   alpha     = fl(fl(gscale.step * wscale.step) * 2^-(N_G - 1)).
+ * Sec. 3.2 shifts every product before it is accumulated; here the shift of
+ * each inner index c is folded into the int8 operand (q_fold), and shifts
+ * beyond int8 range are added through the appended columns of `layout`.
+ * Inputs : q_fold, ld_fold, layout, group, gscale from sq_quantize_grad with
+ *          the same M, C_out and p; wq_t [C_in, ld_w] int8 = W^T codes
+ *          (ld_w >= C_out); wscale its sq_scale.
+ * Outputs (either may be NULL, not both): acc [M, ld_acc] int32,
+ *          dX [M, ld_dX] fp32.
+ * Errors: SQ_ERR_INVALID_ARGUMENT; SQ_ERR_OVERFLOW_RISK when
+ *         C_out * Q * 2^(N_G-1) * 128 >= 2^31; SQ_ERR_WORKSPACE_TOO_SMALL;
+ *         SQ_ERR_HIP.
+ * ------------------------------------------------------------------------- */
+sq_status sq_gemm_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* layout,
+                        const uint8_t* group, const sq_scale* gscale,
+                        const int8_t* wq_t, int64_t ld_w, const sq_scale* wscale,
+                        int64_t M, int64_t C_out, int64_t C_in, const sq_quant_params* p,
+                        int32_t* acc, int64_t ld_acc, float* dX, int64_t ld_dX,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * sq_gemm_wgrad -- weight gradient dW = dY^T . X.
+ *
+ * The third training GEMM (Fig. "MMs"); its inner dimension is the token
+ * index, so every output row c lies in one gradient group and the group
+ * scale is a per-row factor (Eq. "dq_mm_f" applied to this product):
+ *   acc[c, k] = sum_m code(m, c) * xq[m, k]                             (int32)
+ *   dW[c, k]  = fl(float(acc[c, k]) * beta_c),
+ *   beta_c    = fl(fl(gscale.step * xscale.step) * 2^-g_c).
+ * Inputs : q_t [C_out, ld_t] int8 and group, gscale from sq_quantize_grad;
+ *          xq_t [C_in, ld_x] int8 = X^T codes (ld_x >= M); xscale its scale.
+ * Outputs (either may be NULL, not both): acc [C_out, ld_acc] int32,
+ *          dW [C_out, ld_dW] fp32.
+ * Errors: SQ_ERR_INVALID_ARGUMENT; SQ_ERR_OVERFLOW_RISK when
+ *         M * Q * 128 >= 2^31; SQ_ERR_WORKSPACE_TOO_SMALL; SQ_ERR_HIP.
+ * ------------------------------------------------------------------------- */
+sq_status sq_gemm_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, const sq_scale* gscale,
+                        const int8_t* xq_t, int64_t ld_x, const sq_scale* xscale,
+                        int64_t M, int64_t C_out, int64_t C_in, const sq_quant_params* p,
+                        int32_t* acc, int64_t ld_acc, float* dW, int64_t ld_dW,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * sq_dequant -- int32 accumulator to fp32 (Eq. "dq_mm_f": the inverse
+ * scales multiply the integer sum once, outside the accumulation).
+ *   kind 0 (dgrad): out = fl(float(acc) * alpha), alpha as in sq_gemm_dgrad
+ *   kind 1 (wgrad): out[r, :] = fl(float(acc[r, :]) * beta_r), beta_r as in
+ *                   sq_gemm_wgrad with g_r = group[r]
+ * Inputs : acc [rows, ld_acc] int32; group [rows] (kind 1 only); gscale and
+ *          oscale (the W scale for kind 0, the X scale for kind 1).
+ * Output : out [rows, ld_out] fp32.
+ * Errors: SQ_ERR_INVALID_ARGUMENT, SQ_ERR_HIP.
+ * ------------------------------------------------------------------------- */
+sq_status sq_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_t ld_acc, int32_t kind,
+                     const uint8_t* group, const sq_scale* gscale, const sq_scale* oscale,
+                     int32_t num_groups, float* out, int64_t ld_out, void* stream);
+
+/* Static description of a status code. */
+const char* sq_status_string(sq_status s);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* sq_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SHIFTQUANT_H */

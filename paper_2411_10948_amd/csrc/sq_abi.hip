@@ -1,0 +1,349 @@
+// extern "C" entry points of libshiftquant: synchronous argument checks,
+// workspace carving and stream-ordered kernel launches.  The semantics of
+// every call are documented in include/shiftquant.h.
+#include <cstdint>
+#include <cstring>
+#include <string>
+
+#include "sq_internal.h"
+
+namespace sq {
+
+QuantCfg make_cfg(const sq_quant_params& p) {
+    QuantCfg c;
+    c.bits = p.bits;
+    c.Q = (1 << (p.bits - 1)) - 1;
+    c.num_groups = p.num_groups;
+    int T = 0;
+    while (c.Q * (1 << (T + 1)) <= 127) ++T;
+    c.T = T;
+    c.E_max = p.num_groups - 1 - T > 0 ? p.num_groups - 1 - T : 0;
+    c.round_mode = p.round_mode;
+    c.seed = p.seed;
+    c.offset = p.offset;
+    return c;
+}
+
+int64_t fold_ext_max(int64_t C, const QuantCfg& c) { return (int64_t)c.E_max * round_up(C, kFoldPad); }
+
+}  // namespace sq
+
+namespace {
+
+using namespace sq;
+
+thread_local std::string g_last_error;
+
+constexpr int64_t kMaxRows = (int64_t)1 << 31;      // rows of any operand
+constexpr int64_t kMaxChannels = (int64_t)1 << 20;  // C_out, C_in, cols
+
+sq_status fail(sq_status s, const std::string& msg) {
+    g_last_error = msg;
+    return s;
+}
+
+sq_status hip_status(hipError_t e, const char* what) {
+    if (e == hipSuccess) return SQ_OK;
+    return fail(SQ_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+sq_status check_params(const sq_quant_params* p) {
+    if (!p) return fail(SQ_ERR_INVALID_ARGUMENT, "params is NULL");
+    if (p->bits < 2 || p->bits > 8) return fail(SQ_ERR_INVALID_ARGUMENT, "bits must be in [2, 8]");
+    if (p->num_groups < 1 || p->num_groups > 8)
+        return fail(SQ_ERR_INVALID_ARGUMENT, "num_groups must be in [1, 8]");
+    if (p->round_mode != SQ_ROUND_NEAREST_EVEN && p->round_mode != SQ_ROUND_STOCHASTIC)
+        return fail(SQ_ERR_INVALID_ARGUMENT, "round_mode must be SQ_ROUND_NEAREST_EVEN or SQ_ROUND_STOCHASTIC");
+    if (p->reserved != 0) return fail(SQ_ERR_INVALID_ARGUMENT, "reserved must be 0");
+    return SQ_OK;
+}
+
+// int8 code matrix [rows, ld] with ld >= min_ld, 16-byte aligned, ld % 16 == 0
+sq_status check_codes(const void* q, int64_t ld, int64_t min_ld, const char* name) {
+    if (!q) return fail(SQ_ERR_INVALID_ARGUMENT, std::string(name) + " is NULL");
+    if (!aligned(q, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, std::string(name) + " must be 16-byte aligned");
+    if (ld < min_ld || ld % 16 != 0)
+        return fail(SQ_ERR_INVALID_ARGUMENT, std::string("ld of ") + name + " must be a multiple of 16 and >= " +
+                                                 std::to_string(min_ld));
+    return SQ_OK;
+}
+
+sq_status check_f32(const void* p, int64_t ld, int64_t min_ld, const char* name) {
+    if (!p) return fail(SQ_ERR_INVALID_ARGUMENT, std::string(name) + " is NULL");
+    if (!aligned(p, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, std::string(name) + " must be 4-byte aligned");
+    if (ld < min_ld) return fail(SQ_ERR_INVALID_ARGUMENT, std::string("ld of ") + name + " is smaller than its row");
+    return SQ_OK;
+}
+
+sq_status check_dims(int64_t rows, int64_t cols, const char* what) {
+    if (rows < 0 || cols < 0 || rows >= kMaxRows || cols >= kMaxChannels)
+        return fail(SQ_ERR_INVALID_ARGUMENT, std::string("dimensions of ") + what + " out of range");
+    return SQ_OK;
+}
+
+size_t rbits_bytes(int64_t C) { return (size_t)round_up(C > 0 ? C * 4 : 4, 256); }
+
+#define SQ_TRY(expr)                      \
+    do {                                  \
+        const sq_status st__ = (expr);    \
+        if (st__ != SQ_OK) return st__;   \
+    } while (0)
+
+}  // namespace
+
+using namespace sq;
+
+extern "C" {
+
+const char* sq_status_string(sq_status s) {
+    switch (s) {
+        case SQ_OK: return "SQ_OK";
+        case SQ_ERR_INVALID_ARGUMENT: return "SQ_ERR_INVALID_ARGUMENT";
+        case SQ_ERR_OVERFLOW_RISK: return "SQ_ERR_OVERFLOW_RISK";
+        case SQ_ERR_UNSUPPORTED: return "SQ_ERR_UNSUPPORTED";
+        case SQ_ERR_WORKSPACE_TOO_SMALL: return "SQ_ERR_WORKSPACE_TOO_SMALL";
+        case SQ_ERR_HIP: return "SQ_ERR_HIP";
+    }
+    return "SQ_ERR_UNKNOWN";
+}
+
+const char* sq_last_error(void) { return g_last_error.c_str(); }
+
+sq_status sq_grad_layout_size(int64_t C_out, const sq_quant_params* p, size_t* layout_bytes, int64_t* min_ld_fold) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_dims(0, C_out, "gradient"));
+    if (!layout_bytes || !min_ld_fold) return fail(SQ_ERR_INVALID_ARGUMENT, "output pointer is NULL");
+    const QuantCfg cfg = make_cfg(*p);
+    const int64_t ext = fold_ext_max(C_out, cfg);
+    *layout_bytes = (size_t)(kLayoutHeader + ext) * sizeof(int32_t);
+    *min_ld_fold = ext > 0 ? fold_ext_base(C_out) + ext : round_up(C_out > 0 ? C_out : 1, 16);
+    return SQ_OK;
+}
+
+sq_status sq_quantize_grad_workspace_size(int64_t M, int64_t C_out, const sq_quant_params* p, size_t* bytes) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_dims(M, C_out, "gradient"));
+    if (!bytes) return fail(SQ_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    *bytes = rbits_bytes(C_out);
+    return SQ_OK;
+}
+
+sq_status sq_quantize_tensor_workspace_size(int64_t rows, int64_t cols, size_t* bytes) {
+    SQ_TRY(check_dims(rows, cols, "tensor"));
+    if (!bytes) return fail(SQ_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    *bytes = rbits_bytes(cols);
+    return SQ_OK;
+}
+
+sq_status sq_gemm_dgrad_workspace_size(int64_t M, int64_t C_out, int64_t C_in, const sq_quant_params* p,
+                                       size_t* bytes) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_dims(M, C_out, "gradient"));
+    SQ_TRY(check_dims(C_in, C_in, "weight"));
+    if (!bytes) return fail(SQ_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    const QuantCfg cfg = make_cfg(*p);
+    *bytes = (size_t)round_up(C_in * fold_ext_max(C_out, cfg), 256);
+    return SQ_OK;
+}
+
+sq_status sq_gemm_wgrad_workspace_size(int64_t M, int64_t C_out, int64_t C_in, const sq_quant_params* p,
+                                       size_t* bytes) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_dims(M, C_out, "gradient"));
+    SQ_TRY(check_dims(C_in, C_in, "activation"));
+    if (!bytes) return fail(SQ_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    const int splits = (M > 0 && C_out > 0 && C_in > 0) ? wgrad_splits(M, C_out, C_in) : 1;
+    *bytes = splits > 1 ? (size_t)round_up(C_out * C_in * 4, 256) : 0;
+    return SQ_OK;
+}
+
+sq_status sq_quantize_grad(const float* dY, int64_t M, int64_t C_out, int64_t ld_dY, const sq_quant_params* p,
+                           int8_t* q_fold, int64_t ld_fold, int8_t* q_t, int64_t ld_t, uint8_t* group,
+                           sq_scale* scale, int32_t* layout, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_dims(M, C_out, "dY"));
+    if (M > 0 && C_out > 0) SQ_TRY(check_f32(dY, ld_dY, C_out, "dY"));
+    if (!scale || !aligned(scale, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "scale is NULL or misaligned");
+    if (!layout || !aligned(layout, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "layout is NULL or misaligned");
+    if (C_out > 0 && !group) return fail(SQ_ERR_INVALID_ARGUMENT, "group is NULL");
+    size_t lay_bytes = 0;
+    int64_t min_ld_fold = 0;
+    SQ_TRY(sq_grad_layout_size(C_out, p, &lay_bytes, &min_ld_fold));
+    if (q_fold && M > 0) SQ_TRY(check_codes(q_fold, ld_fold, min_ld_fold, "q_fold"));
+    if (q_t && C_out > 0) SQ_TRY(check_codes(q_t, ld_t, M > 0 ? M : 1, "q_t"));
+    if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
+    if (workspace_bytes < rbits_bytes(C_out)) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+
+    const QuantCfg cfg = make_cfg(*p);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    uint32_t* rbits = static_cast<uint32_t*>(workspace);
+    SQ_TRY(hip_status(launch_fill_u32(rbits, C_out, 0u, s), "fill"));
+    SQ_TRY(hip_status(launch_colmax(dY, M, C_out, ld_dY, rbits, s), "colmax"));
+    SQ_TRY(hip_status(launch_finalize_grad(rbits, C_out, cfg, group, scale, layout, s), "finalize"));
+    SQ_TRY(hip_status(launch_quantize(dY, M, C_out, ld_dY, group, scale, cfg, q_fold, ld_fold, q_t, ld_t,
+                                      layout, s),
+                      "quantize"));
+    return SQ_OK;
+}
+
+sq_status sq_quantize_tensor(const float* T, int64_t rows, int64_t cols, int64_t ld, int32_t bits, int32_t transpose,
+                             int8_t* q, int64_t ld_q, sq_scale* scale, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+    SQ_TRY(check_dims(rows, cols, "tensor"));
+    if (bits < 2 || bits > 8) return fail(SQ_ERR_INVALID_ARGUMENT, "bits must be in [2, 8]");
+    if (transpose != 0 && transpose != 1) return fail(SQ_ERR_INVALID_ARGUMENT, "transpose must be 0 or 1");
+    if (rows > 0 && cols > 0) {
+        SQ_TRY(check_f32(T, ld, cols, "T"));
+        SQ_TRY(check_codes(q, ld_q, transpose ? rows : cols, "q"));
+    }
+    if (!scale || !aligned(scale, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "scale is NULL or misaligned");
+    if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
+    if (workspace_bytes < rbits_bytes(cols)) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+
+    sq_quant_params p{};
+    p.bits = bits;
+    p.num_groups = 1;
+    p.round_mode = SQ_ROUND_NEAREST_EVEN;
+    const QuantCfg cfg = make_cfg(p);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    uint32_t* rbits = static_cast<uint32_t*>(workspace);
+    SQ_TRY(hip_status(launch_fill_u32(rbits, cols, 0u, s), "fill"));
+    SQ_TRY(hip_status(launch_colmax(T, rows, cols, ld, rbits, s), "colmax"));
+    SQ_TRY(hip_status(launch_finalize_tensor(rbits, cols, cfg.Q, scale, s), "finalize"));
+    SQ_TRY(hip_status(launch_quantize(T, rows, cols, ld, nullptr, scale, cfg, transpose ? nullptr : q, ld_q,
+                                      transpose ? q : nullptr, ld_q, nullptr, s),
+                      "quantize"));
+    return SQ_OK;
+}
+
+sq_status sq_gemm_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* layout, const uint8_t* group,
+                        const sq_scale* gscale, const int8_t* wq_t, int64_t ld_w, const sq_scale* wscale, int64_t M,
+                        int64_t C_out, int64_t C_in, const sq_quant_params* p, int32_t* acc, int64_t ld_acc,
+                        float* dX, int64_t ld_dX, void* workspace, size_t workspace_bytes, void* stream) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_dims(M, C_out, "gradient codes"));
+    SQ_TRY(check_dims(C_in, C_in, "weight codes"));
+    if (!acc && !dX) return fail(SQ_ERR_INVALID_ARGUMENT, "acc and dX are both NULL");
+    if (!layout || !gscale || !wscale) return fail(SQ_ERR_INVALID_ARGUMENT, "layout or a scale is NULL");
+    const QuantCfg cfg = make_cfg(*p);
+    // worst case |acc| = C_out * Q * 2^(N_G-1) * 128 must stay below 2^31
+    const double bound = (double)C_out * cfg.Q * (double)(1 << (cfg.num_groups - 1)) * 128.0;
+    if (bound >= 2147483648.0)
+        return fail(SQ_ERR_OVERFLOW_RISK, "C_out * Q * 2^(N_G-1) * 128 reaches 2^31: the int32 accumulator could overflow");
+    if (M == 0 || C_in == 0) return SQ_OK;
+    size_t lay_bytes = 0;
+    int64_t min_ld_fold = 0;
+    SQ_TRY(sq_grad_layout_size(C_out, p, &lay_bytes, &min_ld_fold));
+    SQ_TRY(check_codes(q_fold, ld_fold, min_ld_fold, "q_fold"));
+    SQ_TRY(check_codes(wq_t, ld_w, C_out > 0 ? C_out : 1, "wq_t"));
+    if (acc) SQ_TRY(check_f32(acc, ld_acc, C_in, "acc"));
+    if (dX) SQ_TRY(check_f32(dX, ld_dX, C_in, "dX"));
+    const int64_t ext_max = fold_ext_max(C_out, cfg);
+    size_t need = 0;
+    SQ_TRY(sq_gemm_dgrad_workspace_size(M, C_out, C_in, p, &need));
+    if (need > 0) {
+        if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
+        if (workspace_bytes < need) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+
+    GemmArgs a{};
+    a.Mg = M; a.Ng = C_in;
+    a.A = q_fold; a.lda = ld_fold;
+    a.B = wq_t; a.ldb = ld_w;
+    a.K = C_out;
+    if (ext_max > 0) {
+        int8_t* wext = static_cast<int8_t*>(workspace);
+        SQ_TRY(hip_status(launch_gather_ext(wq_t, ld_w, C_in, layout, wext, ext_max, ext_max, s), "gather"));
+        a.extA = q_fold + fold_ext_base(C_out); a.ld_extA = ld_fold;
+        a.extB = wext; a.ld_extB = ext_max;
+        a.layout = layout;
+    }
+    a.splits = 1;
+    a.acc = acc; a.ld_acc = ld_acc;
+    a.out = dX; a.ld_out = ld_dX;
+    a.atomic_acc = 0;
+    a.epi_mode = 0;
+    a.gs = gscale; a.os = wscale; a.group = group; a.num_groups = cfg.num_groups;
+    return hip_status(launch_gemm(a, s), "gemm_dgrad");
+}
+
+sq_status sq_gemm_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, const sq_scale* gscale,
+                        const int8_t* xq_t, int64_t ld_x, const sq_scale* xscale, int64_t M, int64_t C_out,
+                        int64_t C_in, const sq_quant_params* p, int32_t* acc, int64_t ld_acc, float* dW,
+                        int64_t ld_dW, void* workspace, size_t workspace_bytes, void* stream) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_dims(M, C_out, "gradient codes"));
+    SQ_TRY(check_dims(C_in, C_in, "activation codes"));
+    if (!acc && !dW) return fail(SQ_ERR_INVALID_ARGUMENT, "acc and dW are both NULL");
+    if (!gscale || !xscale) return fail(SQ_ERR_INVALID_ARGUMENT, "a scale is NULL");
+    const QuantCfg cfg = make_cfg(*p);
+    const double bound = (double)M * cfg.Q * 128.0;
+    if (bound >= 2147483648.0)
+        return fail(SQ_ERR_OVERFLOW_RISK, "M * Q * 128 reaches 2^31: the int32 accumulator could overflow");
+    if (C_out == 0 || C_in == 0) return SQ_OK;
+    if (!group) return fail(SQ_ERR_INVALID_ARGUMENT, "group is NULL");
+    if (M > 0) {
+        SQ_TRY(check_codes(q_t, ld_t, M, "q_t"));
+        SQ_TRY(check_codes(xq_t, ld_x, M, "xq_t"));
+    }
+    if (acc) SQ_TRY(check_f32(acc, ld_acc, C_in, "acc"));
+    if (dW) SQ_TRY(check_f32(dW, ld_dW, C_in, "dW"));
+    size_t need = 0;
+    SQ_TRY(sq_gemm_wgrad_workspace_size(M, C_out, C_in, p, &need));
+    const int splits = (M > 0) ? wgrad_splits(M, C_out, C_in) : 1;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+
+    GemmArgs a{};
+    a.Mg = C_out; a.Ng = C_in;
+    a.A = q_t; a.lda = ld_t;
+    a.B = xq_t; a.ldb = ld_x;
+    a.K = M;
+    a.gs = gscale; a.os = xscale; a.group = group; a.num_groups = cfg.num_groups;
+    a.epi_mode = 1;
+    if (splits <= 1) {
+        a.splits = 1;
+        a.acc = acc; a.ld_acc = ld_acc;
+        a.out = dW; a.ld_out = ld_dW;
+        return hip_status(launch_gemm(a, s), "gemm_wgrad");
+    }
+    int32_t* target = acc;
+    int64_t ld_target = ld_acc;
+    if (!target) {
+        if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
+        if (workspace_bytes < need) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+        target = static_cast<int32_t*>(workspace);
+        ld_target = C_in;
+    }
+    SQ_TRY(hip_status(launch_zero_i32(target, C_out, C_in, ld_target, s), "zero"));
+    a.splits = splits;
+    a.acc = target; a.ld_acc = ld_target;
+    a.atomic_acc = 1;
+    SQ_TRY(hip_status(launch_gemm(a, s), "gemm_wgrad"));
+    if (dW)
+        SQ_TRY(hip_status(launch_dequant(target, C_out, C_in, ld_target, 1, group, gscale, xscale, cfg.num_groups, dW,
+                                         ld_dW, s),
+                          "dequant"));
+    return SQ_OK;
+}
+
+sq_status sq_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_t ld_acc, int32_t kind,
+                     const uint8_t* group, const sq_scale* gscale, const sq_scale* oscale, int32_t num_groups,
+                     float* out, int64_t ld_out, void* stream) {
+    SQ_TRY(check_dims(rows, cols, "accumulator"));
+    if (kind != 0 && kind != 1) return fail(SQ_ERR_INVALID_ARGUMENT, "kind must be 0 (dgrad) or 1 (wgrad)");
+    if (num_groups < 1 || num_groups > 8) return fail(SQ_ERR_INVALID_ARGUMENT, "num_groups must be in [1, 8]");
+    if (!gscale || !oscale) return fail(SQ_ERR_INVALID_ARGUMENT, "a scale is NULL");
+    if (rows == 0 || cols == 0) return SQ_OK;
+    SQ_TRY(check_f32(acc, ld_acc, cols, "acc"));
+    SQ_TRY(check_f32(out, ld_out, cols, "out"));
+    if (kind == 1 && !group) return fail(SQ_ERR_INVALID_ARGUMENT, "group is NULL");
+    return hip_status(launch_dequant(acc, rows, cols, ld_acc, kind, group, gscale, oscale, num_groups, out, ld_out,
+                                     static_cast<hipStream_t>(stream)),
+                      "dequant");
+}
+
+}  // extern "C"

@@ -1,0 +1,92 @@
+// Internal declarations of libshiftquant (kernels and their launchers).
+// Not part of the public ABI; see include/shiftquant.h for that.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "shiftquant.h"
+
+namespace sq {
+
+// ---------------------------------------------------------------------------
+// Fold layout descriptor (int32 words in a caller-provided device buffer).
+//   [0] E      : appended regions in use (0 when no channel needs them)
+//   [1] D      : appended columns in use (a multiple of kFoldPad)
+//   [2] base   : q_fold column where the appended columns start
+//   [4 + r]    : start column (relative to base) of region r, r < kMaxRegions,
+//                regions in the order the dgrad K-loop visits them
+//   [kLayoutHeader + j] : channel copied into appended column j, -1 = zero
+// ---------------------------------------------------------------------------
+constexpr int kLayoutHeader = 16;
+constexpr int kMaxRegions = 8;
+constexpr int kFoldPad = 64;        // appended regions are padded to the GEMM K tile
+
+__host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// Host-side constants of one quantizer configuration.
+struct QuantCfg {
+    int bits;
+    int Q;             // 2^(bits-1) - 1
+    int num_groups;    // N_G
+    int T;             // largest shift with Q * 2^T <= 127
+    int E_max;         // max(0, N_G - 1 - T): appended regions in the worst case
+    int round_mode;
+    uint64_t seed;
+    uint64_t offset;
+};
+
+QuantCfg make_cfg(const sq_quant_params& p);
+
+// Worst-case appended columns for C channels and the layout size in words.
+int64_t fold_ext_max(int64_t C, const QuantCfg& c);
+__host__ __device__ inline int64_t fold_ext_base(int64_t C) { return round_up(C, kFoldPad); }
+
+// ---- quantizer (sq_quant.hip) ----
+hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
+hipError_t launch_colmax(const float* x, int64_t M, int64_t C, int64_t ld, uint32_t* rbits,
+                         hipStream_t s);
+hipError_t launch_finalize_grad(const uint32_t* rbits, int64_t C, const QuantCfg& cfg,
+                                uint8_t* group, sq_scale* scale, int32_t* layout, hipStream_t s);
+hipError_t launch_finalize_tensor(const uint32_t* rbits, int64_t C, int Q, sq_scale* scale,
+                                  hipStream_t s);
+// group == nullptr: every channel in group 0 with shift 0 (per-tensor mode).
+hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, const uint8_t* group,
+                           const sq_scale* scale, const QuantCfg& cfg,
+                           int8_t* q_fold, int64_t ld_fold, int8_t* q_t, int64_t ld_t,
+                           const int32_t* layout, hipStream_t s);
+
+// ---- GEMMs (sq_gemm.hip) ----
+struct GemmArgs {
+    int64_t Mg, Ng;                 // output rows / columns
+    const int8_t* A; int64_t lda;   // [Mg, lda], K contiguous
+    const int8_t* B; int64_t ldb;   // [Ng, ldb], K contiguous
+    int64_t K;
+    const int8_t* extA; int64_t ld_extA;   // appended K region (dgrad fold), may be null
+    const int8_t* extB; int64_t ld_extB;
+    const int32_t* layout;
+    int splits;                     // split-K factor over the main segment
+    int32_t* acc; int64_t ld_acc;   // int32 output (or split-K target)
+    float* out; int64_t ld_out;     // fp32 output
+    int atomic_acc;                 // split-K: atomically add into acc, no fp32 output
+    int epi_mode;                   // 0: dgrad scale, 1: wgrad per-row scale
+    const sq_scale* gs;
+    const sq_scale* os;
+    const uint8_t* group;
+    int num_groups;
+};
+
+hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
+hipError_t launch_gather_ext(const int8_t* wq_t, int64_t ld_w, int64_t C_in, const int32_t* layout,
+                             int8_t* wext, int64_t ld_ext, int64_t ext_max, hipStream_t s);
+hipError_t launch_zero_i32(int32_t* p, int64_t rows, int64_t cols, int64_t ld, hipStream_t s);
+hipError_t launch_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_t ld_acc, int kind,
+                          const uint8_t* group, const sq_scale* gs, const sq_scale* os,
+                          int num_groups, float* out, int64_t ld_out, hipStream_t s);
+int wgrad_splits(int64_t M, int64_t C_out, int64_t C_in);
+
+// ---- device helpers ----
+// 2^k as a float, exact for -126 <= k <= 127 (from its bit pattern).
+__device__ __forceinline__ float pow2f(int k) { return __uint_as_float((uint32_t)(k + 127) << 23); }
+
+}  // namespace sq

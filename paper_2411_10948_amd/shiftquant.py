@@ -1,0 +1,346 @@
+"""ctypes binding of libshiftquant (include/shiftquant.h).
+
+The functions named ``sq_*`` mirror the C entry points one to one and only
+marshal arguments: torch tensors supply device pointers, leading dimensions
+and the current HIP stream; every step of the path runs in the library's HIP
+kernels.  There is no fallback: if the library is not built this module
+fails to import.
+
+The convenience layer below them (``quantize_grad``, ``quantize_tensor``,
+``gemm_dgrad``, ``gemm_wgrad``, ``BackwardPlan``) allocates outputs and
+workspaces with torch and calls the ``sq_*`` functions.
+"""
+from __future__ import annotations
+
+import ctypes as ct
+import dataclasses
+import os
+from typing import Optional, Tuple
+
+# torch is imported before the library is loaded: torch ships the HIP runtime
+# (soname libamdhip64.so.7), and loading it first makes libshiftquant bind to
+# that same runtime, so torch's streams and allocations are valid in it.
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libshiftquant.so")
+
+SQ_OK = 0
+STATUS_NAMES = {0: "SQ_OK", 1: "SQ_ERR_INVALID_ARGUMENT", 2: "SQ_ERR_OVERFLOW_RISK",
+                3: "SQ_ERR_UNSUPPORTED", 4: "SQ_ERR_WORKSPACE_TOO_SMALL", 5: "SQ_ERR_HIP"}
+ROUND_NEAREST_EVEN = 0
+ROUND_STOCHASTIC = 1
+FLAG_NONFINITE = 1
+FLAG_ZERO = 2
+
+# Every symbol include/shiftquant.h declares.
+EXPORTS = (
+    "sq_grad_layout_size", "sq_quantize_grad_workspace_size", "sq_quantize_tensor_workspace_size",
+    "sq_gemm_dgrad_workspace_size", "sq_gemm_wgrad_workspace_size",
+    "sq_quantize_grad", "sq_quantize_tensor", "sq_gemm_dgrad", "sq_gemm_wgrad", "sq_dequant",
+    "sq_status_string", "sq_last_error",
+)
+
+
+class ShiftQuantError(RuntimeError):
+    def __init__(self, fn: str, status: int, message: str):
+        self.status = status
+        super().__init__(f"{fn}: {STATUS_NAMES.get(status, status)}: {message}")
+
+
+class Params(ct.Structure):
+    """sq_quant_params"""
+    _fields_ = [("bits", ct.c_int32), ("num_groups", ct.c_int32), ("round_mode", ct.c_int32),
+                ("reserved", ct.c_int32), ("seed", ct.c_uint64), ("offset", ct.c_uint64)]
+
+    @classmethod
+    def make(cls, bits: int, num_groups: int = 4, round_mode: int = ROUND_NEAREST_EVEN,
+             seed: int = 0, offset: int = 0) -> "Params":
+        return cls(bits, num_groups, round_mode, 0, seed, offset)
+
+
+_P = ct.c_void_p
+_I64 = ct.c_int64
+_SZ = ct.c_size_t
+_lib = None
+
+
+def load() -> ct.CDLL:
+    """Load libshiftquant.so (built in-tree by paper_2411_10948_amd.build)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2411_10948_amd.build`")
+    L = ct.CDLL(LIB_PATH)
+    pp = ct.POINTER(Params)
+    sig = {
+        "sq_grad_layout_size": [_I64, pp, ct.POINTER(_SZ), ct.POINTER(_I64)],
+        "sq_quantize_grad_workspace_size": [_I64, _I64, pp, ct.POINTER(_SZ)],
+        "sq_quantize_tensor_workspace_size": [_I64, _I64, ct.POINTER(_SZ)],
+        "sq_gemm_dgrad_workspace_size": [_I64, _I64, _I64, pp, ct.POINTER(_SZ)],
+        "sq_gemm_wgrad_workspace_size": [_I64, _I64, _I64, pp, ct.POINTER(_SZ)],
+        "sq_quantize_grad": [_P, _I64, _I64, _I64, pp, _P, _I64, _P, _I64, _P, _P, _P, _P, _SZ, _P],
+        "sq_quantize_tensor": [_P, _I64, _I64, _I64, ct.c_int32, ct.c_int32, _P, _I64, _P, _P, _SZ, _P],
+        "sq_gemm_dgrad": [_P, _I64, _P, _P, _P, _P, _I64, _P, _I64, _I64, _I64, pp, _P, _I64, _P, _I64,
+                          _P, _SZ, _P],
+        "sq_gemm_wgrad": [_P, _I64, _P, _P, _P, _I64, _P, _I64, _I64, _I64, pp, _P, _I64, _P, _I64, _P,
+                          _SZ, _P],
+        "sq_dequant": [_P, _I64, _I64, _I64, ct.c_int32, _P, _P, _P, ct.c_int32, _P, _I64, _P],
+    }
+    for name, args in sig.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = ct.c_int
+    L.sq_status_string.argtypes = [ct.c_int]
+    L.sq_status_string.restype = ct.c_char_p
+    L.sq_last_error.argtypes = []
+    L.sq_last_error.restype = ct.c_char_p
+    _lib = L
+    return L
+
+
+def sq_status_string(status: int) -> str:
+    return load().sq_status_string(status).decode()
+
+
+def sq_last_error() -> str:
+    return load().sq_last_error().decode()
+
+
+def _check(fn: str, status: int) -> None:
+    if status != SQ_OK:
+        raise ShiftQuantError(fn, status, sq_last_error())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ct.c_void_p(t.data_ptr())
+
+
+def _ld(t: Optional[torch.Tensor]) -> int:
+    if t is None:
+        return 0
+    if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1):
+        raise ValueError("expected a 2-D tensor with unit column stride")
+    return t.stride(0)
+
+
+def _stream(stream) -> ct.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ct.c_void_p(s.cuda_stream)
+
+
+def _ws_ptr(ws: Optional[torch.Tensor]):
+    return (None, 0) if ws is None else (ct.c_void_p(ws.data_ptr()), ws.numel() * ws.element_size())
+
+
+# ---------------------------------------------------------------------------
+# one-to-one wrappers of the C entry points
+# ---------------------------------------------------------------------------
+def sq_grad_layout_size(C_out: int, params: Params) -> Tuple[int, int]:
+    nb, ld = _SZ(0), _I64(0)
+    _check("sq_grad_layout_size", load().sq_grad_layout_size(C_out, ct.byref(params), ct.byref(nb), ct.byref(ld)))
+    return nb.value, ld.value
+
+
+def sq_quantize_grad_workspace_size(M: int, C_out: int, params: Params) -> int:
+    nb = _SZ(0)
+    _check("sq_quantize_grad_workspace_size",
+           load().sq_quantize_grad_workspace_size(M, C_out, ct.byref(params), ct.byref(nb)))
+    return nb.value
+
+
+def sq_quantize_tensor_workspace_size(rows: int, cols: int) -> int:
+    nb = _SZ(0)
+    _check("sq_quantize_tensor_workspace_size", load().sq_quantize_tensor_workspace_size(rows, cols, ct.byref(nb)))
+    return nb.value
+
+
+def sq_gemm_dgrad_workspace_size(M: int, C_out: int, C_in: int, params: Params) -> int:
+    nb = _SZ(0)
+    _check("sq_gemm_dgrad_workspace_size",
+           load().sq_gemm_dgrad_workspace_size(M, C_out, C_in, ct.byref(params), ct.byref(nb)))
+    return nb.value
+
+
+def sq_gemm_wgrad_workspace_size(M: int, C_out: int, C_in: int, params: Params) -> int:
+    nb = _SZ(0)
+    _check("sq_gemm_wgrad_workspace_size",
+           load().sq_gemm_wgrad_workspace_size(M, C_out, C_in, ct.byref(params), ct.byref(nb)))
+    return nb.value
+
+
+def sq_quantize_grad(dY, params, q_fold, q_t, group, scale, layout, workspace, stream=None) -> None:
+    M, C = dY.shape
+    ws, nws = _ws_ptr(workspace)
+    _check("sq_quantize_grad", load().sq_quantize_grad(
+        _ptr(dY), M, C, _ld(dY), ct.byref(params), _ptr(q_fold), _ld(q_fold), _ptr(q_t), _ld(q_t),
+        _ptr(group), _ptr(scale), _ptr(layout), ws, nws, _stream(stream)))
+
+
+def sq_quantize_tensor(T, bits, transpose, q, scale, workspace, stream=None) -> None:
+    rows, cols = T.shape
+    ws, nws = _ws_ptr(workspace)
+    _check("sq_quantize_tensor", load().sq_quantize_tensor(
+        _ptr(T), rows, cols, _ld(T), bits, int(transpose), _ptr(q), _ld(q), _ptr(scale), ws, nws,
+        _stream(stream)))
+
+
+def sq_gemm_dgrad(q_fold, layout, group, gscale, wq_t, wscale, M, C_out, C_in, params, acc, dX,
+                  workspace, stream=None) -> None:
+    ws, nws = _ws_ptr(workspace)
+    _check("sq_gemm_dgrad", load().sq_gemm_dgrad(
+        _ptr(q_fold), _ld(q_fold), _ptr(layout), _ptr(group), _ptr(gscale), _ptr(wq_t), _ld(wq_t),
+        _ptr(wscale), M, C_out, C_in, ct.byref(params), _ptr(acc), _ld(acc), _ptr(dX), _ld(dX),
+        ws, nws, _stream(stream)))
+
+
+def sq_gemm_wgrad(q_t, group, gscale, xq_t, xscale, M, C_out, C_in, params, acc, dW, workspace,
+                  stream=None) -> None:
+    ws, nws = _ws_ptr(workspace)
+    _check("sq_gemm_wgrad", load().sq_gemm_wgrad(
+        _ptr(q_t), _ld(q_t), _ptr(group), _ptr(gscale), _ptr(xq_t), _ld(xq_t), _ptr(xscale),
+        M, C_out, C_in, ct.byref(params), _ptr(acc), _ld(acc), _ptr(dW), _ld(dW), ws, nws,
+        _stream(stream)))
+
+
+def sq_dequant(acc, kind, group, gscale, oscale, num_groups, out, stream=None) -> None:
+    rows, cols = acc.shape
+    _check("sq_dequant", load().sq_dequant(
+        _ptr(acc), rows, cols, _ld(acc), kind, _ptr(group), _ptr(gscale), _ptr(oscale), num_groups,
+        _ptr(out), _ld(out), _stream(stream)))
+
+
+# ---------------------------------------------------------------------------
+# convenience layer (allocates with torch, then calls the wrappers above)
+# ---------------------------------------------------------------------------
+def round_up(x: int, m: int) -> int:
+    return (x + m - 1) // m * m
+
+
+def new_scale(device) -> torch.Tensor:
+    """Device storage for one sq_scale (r_max, inv, step, flags)."""
+    return torch.zeros(4, dtype=torch.float32, device=device)
+
+
+def scale_to_host(scale: torch.Tensor) -> dict:
+    s = scale.detach().cpu()
+    return {"r_max": s[0].item(), "inv": s[1].item(), "step": s[2].item(),
+            "flags": int(s.view(torch.int32)[3].item()),
+            "bits": s.view(torch.int32).tolist()}
+
+
+def _workspace(nbytes: int, device) -> Optional[torch.Tensor]:
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+@dataclasses.dataclass
+class GradCodes:
+    """Output of sq_quantize_grad for one gradient tensor."""
+    q_fold: torch.Tensor      # [M, ld_fold] int8, dgrad operand
+    q_t: torch.Tensor         # [C_out, ld_t] int8, codes transposed (wgrad operand)
+    group: torch.Tensor       # [C_out] uint8
+    scale: torch.Tensor       # sq_scale
+    layout: torch.Tensor      # fold descriptor (int32)
+    params: Params
+    M: int
+    C_out: int
+
+    def codes(self) -> torch.Tensor:
+        """The codes [M, C_out] themselves (a view of q_t, transposed)."""
+        return self.q_t[:, :self.M].t()
+
+
+def quantize_grad(dY: torch.Tensor, bits: int, num_groups: int = 4, round_mode: int = ROUND_NEAREST_EVEN,
+                  seed: int = 0, offset: int = 0, stream=None) -> GradCodes:
+    M, C = dY.shape
+    dev = dY.device
+    p = Params.make(bits, num_groups, round_mode, seed, offset)
+    lay_bytes, min_ld = sq_grad_layout_size(C, p)
+    q_fold = torch.zeros((max(M, 1), min_ld), dtype=torch.int8, device=dev)[:M]
+    q_t = torch.zeros((max(C, 1), round_up(max(M, 1), 16)), dtype=torch.int8, device=dev)[:C]
+    group = torch.empty(max(C, 1), dtype=torch.uint8, device=dev)[:C]
+    scale = new_scale(dev)
+    layout = torch.zeros(lay_bytes // 4, dtype=torch.int32, device=dev)
+    ws = _workspace(sq_quantize_grad_workspace_size(M, C, p), dev)
+    sq_quantize_grad(dY, p, q_fold, q_t, group, scale, layout, ws, stream)
+    return GradCodes(q_fold, q_t, group, scale, layout, p, M, C)
+
+
+def quantize_tensor(T: torch.Tensor, bits: int = 8, transpose: bool = True, stream=None):
+    rows, cols = T.shape
+    dev = T.device
+    if transpose:
+        q = torch.zeros((max(cols, 1), round_up(max(rows, 1), 16)), dtype=torch.int8, device=dev)[:cols]
+    else:
+        q = torch.zeros((max(rows, 1), round_up(max(cols, 1), 16)), dtype=torch.int8, device=dev)[:rows]
+    scale = new_scale(dev)
+    ws = _workspace(sq_quantize_tensor_workspace_size(rows, cols), dev)
+    sq_quantize_tensor(T, bits, transpose, q, scale, ws, stream)
+    return q, scale
+
+
+def gemm_dgrad(codes: GradCodes, wq_t: torch.Tensor, wscale: torch.Tensor, want_acc: bool = False,
+               want_out: bool = True, stream=None):
+    M, C_out, C_in = codes.M, codes.C_out, wq_t.shape[0]
+    dev = wq_t.device
+    acc = torch.empty((M, C_in), dtype=torch.int32, device=dev) if want_acc else None
+    dX = torch.empty((M, C_in), dtype=torch.float32, device=dev) if want_out else None
+    ws = _workspace(sq_gemm_dgrad_workspace_size(M, C_out, C_in, codes.params), dev)
+    sq_gemm_dgrad(codes.q_fold, codes.layout, codes.group, codes.scale, wq_t, wscale, M, C_out, C_in,
+                  codes.params, acc, dX, ws, stream)
+    return acc, dX
+
+
+def gemm_wgrad(codes: GradCodes, xq_t: torch.Tensor, xscale: torch.Tensor, want_acc: bool = False,
+               want_out: bool = True, stream=None):
+    M, C_out, C_in = codes.M, codes.C_out, xq_t.shape[0]
+    dev = xq_t.device
+    acc = torch.empty((C_out, C_in), dtype=torch.int32, device=dev) if want_acc else None
+    dW = torch.empty((C_out, C_in), dtype=torch.float32, device=dev) if want_out else None
+    ws = _workspace(sq_gemm_wgrad_workspace_size(M, C_out, C_in, codes.params), dev)
+    sq_gemm_wgrad(codes.q_t, codes.group, codes.scale, xq_t, xscale, M, C_out, C_in, codes.params,
+                  acc, dW, ws, stream)
+    return acc, dW
+
+
+class BackwardPlan:
+    """All buffers of one backward step (quantize dY -> dgrad -> wgrad) for a
+    fixed layer shape, allocated once; ``run`` enqueues the three calls and
+    allocates nothing."""
+
+    def __init__(self, M: int, C_out: int, C_in: int, params: Params, device="cuda",
+                 want_acc: bool = False):
+        self.M, self.C_out, self.C_in, self.params = M, C_out, C_in, params
+        dev = torch.device(device)
+        lay_bytes, min_ld = sq_grad_layout_size(C_out, params)
+        self.q_fold = torch.zeros((M, min_ld), dtype=torch.int8, device=dev)
+        self.q_t = torch.zeros((C_out, round_up(M, 16)), dtype=torch.int8, device=dev)
+        self.group = torch.empty(C_out, dtype=torch.uint8, device=dev)
+        self.scale = new_scale(dev)
+        self.layout = torch.zeros(lay_bytes // 4, dtype=torch.int32, device=dev)
+        self.ws_q = _workspace(sq_quantize_grad_workspace_size(M, C_out, params), dev)
+        self.ws_d = _workspace(sq_gemm_dgrad_workspace_size(M, C_out, C_in, params), dev)
+        self.ws_w = _workspace(sq_gemm_wgrad_workspace_size(M, C_out, C_in, params), dev)
+        self.dX = torch.empty((M, C_in), dtype=torch.float32, device=dev)
+        self.dW = torch.empty((C_out, C_in), dtype=torch.float32, device=dev)
+        self.acc_dX = torch.empty((M, C_in), dtype=torch.int32, device=dev) if want_acc else None
+        self.acc_dW = torch.empty((C_out, C_in), dtype=torch.int32, device=dev) if want_acc else None
+
+    def quantize(self, dY, stream=None):
+        sq_quantize_grad(dY, self.params, self.q_fold, self.q_t, self.group, self.scale, self.layout,
+                         self.ws_q, stream)
+
+    def dgrad(self, wq_t, wscale, stream=None):
+        sq_gemm_dgrad(self.q_fold, self.layout, self.group, self.scale, wq_t, wscale, self.M, self.C_out,
+                      self.C_in, self.params, self.acc_dX, self.dX, self.ws_d, stream)
+
+    def wgrad(self, xq_t, xscale, stream=None):
+        sq_gemm_wgrad(self.q_t, self.group, self.scale, xq_t, xscale, self.M, self.C_out, self.C_in,
+                      self.params, self.acc_dW, self.dW, self.ws_w, stream)
+
+    def run(self, dY, wq_t, wscale, xq_t, xscale, stream=None):
+        self.quantize(dY, stream)
+        self.dgrad(wq_t, wscale, stream)
+        self.wgrad(xq_t, xscale, stream)
+        return self.dX, self.dW

@@ -1,0 +1,156 @@
+"""C-ABI contract tests that need no GPU: the library loads, exports every
+symbol include/shiftquant.h declares, and rejects bad arguments synchronously
+(before any HIP call) with the documented status codes."""
+import ctypes as ct
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "shiftquant.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    return sorted(set(re.findall(r"^(?:sq_status|const char\*)\s+(sq_\w+)\s*\(", src, re.M)))
+
+
+@pytest.fixture(scope="module")
+def sq():
+    from paper_2411_10948_amd import shiftquant
+    if not os.path.exists(shiftquant.LIB_PATH):
+        from paper_2411_10948_amd import build
+        build.build()
+    return shiftquant
+
+
+def test_header_declares_the_five_calls():
+    names = _declared()
+    for n in ["sq_quantize_grad", "sq_quantize_tensor", "sq_gemm_dgrad", "sq_gemm_wgrad", "sq_dequant"]:
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(sq):
+    names = _declared()
+    out = subprocess.run(["nm", "-D", "--defined-only", sq.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(l.split()[-1] for l in out.splitlines() if " T " in l)
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+    assert sorted(sq.EXPORTS) == names
+    L = sq.load()
+    for n in names:
+        assert getattr(L, n) is not None
+
+
+def test_status_strings(sq):
+    for code, name in sq.STATUS_NAMES.items():
+        assert sq.sq_status_string(code) == name
+
+
+def _params(sq, bits=4, ng=4, mode=0):
+    return sq.Params.make(bits, ng, mode)
+
+
+def test_size_queries(sq):
+    p = _params(sq, 4, 4)
+    nb, ld = sq.sq_grad_layout_size(100, p)
+    assert nb == 16 * 4 and ld == 112          # b=4, N_G=4: every shift fits int8, no appended columns
+    p6 = _params(sq, 6, 4)
+    nb, ld = sq.sq_grad_layout_size(100, p6)  # b=6: one appended region of up to roundup(100, 64) columns
+    assert nb == (16 + 128) * 4 and ld == 128 + 128
+    p8 = _params(sq, 8, 4)
+    nb, ld = sq.sq_grad_layout_size(64, p8)   # b=8: three regions
+    assert ld == 64 + 3 * 64
+    assert sq.sq_gemm_dgrad_workspace_size(10, 100, 30, p) == 0
+    assert sq.sq_gemm_dgrad_workspace_size(10, 100, 30, p6) == 30 * 128 + (256 - (30 * 128) % 256) % 256
+    assert sq.sq_quantize_grad_workspace_size(10, 100, p) == 512
+    assert sq.sq_quantize_tensor_workspace_size(10, 3) == 256
+
+
+def _raw(sq):
+    return sq.load()
+
+
+def test_invalid_params_rejected(sq):
+    L = _raw(sq)
+    nb, ld = ct.c_size_t(0), ct.c_int64(0)
+    for bits, ng, mode in [(1, 4, 0), (9, 4, 0), (4, 0, 0), (4, 9, 0), (4, 4, 2)]:
+        p = sq.Params.make(bits, ng, mode)
+        assert L.sq_grad_layout_size(64, ct.byref(p), ct.byref(nb), ct.byref(ld)) == 1
+        assert sq.sq_last_error()
+    p = sq.Params.make(4, 4, 0)
+    p.reserved = 1
+    assert L.sq_grad_layout_size(64, ct.byref(p), ct.byref(nb), ct.byref(ld)) == 1
+    assert L.sq_grad_layout_size(64, None, ct.byref(nb), ct.byref(ld)) == 1
+
+
+def test_quantize_grad_validation_no_launch(sq):
+    L = _raw(sq)
+    p = sq.Params.make(4, 4, 0)
+    fake = ct.c_void_p(0x100000)   # 16-byte aligned, never dereferenced on the host
+    # NULL dY
+    assert L.sq_quantize_grad(None, 8, 8, 8, ct.byref(p), fake, 16, fake, 16, fake, fake, fake, fake, 4096,
+                              None) == 1
+    # ld_dY < C
+    assert L.sq_quantize_grad(fake, 8, 8, 4, ct.byref(p), fake, 16, fake, 16, fake, fake, fake, fake, 4096,
+                              None) == 1
+    # ld_fold not a multiple of 16
+    assert L.sq_quantize_grad(fake, 8, 8, 8, ct.byref(p), fake, 24, fake, 16, fake, fake, fake, fake, 4096,
+                              None) == 1
+    # misaligned code pointer
+    assert L.sq_quantize_grad(fake, 8, 8, 8, ct.byref(p), ct.c_void_p(0x100008), 16, fake, 16, fake, fake,
+                              fake, fake, 4096, None) == 1
+    # workspace too small
+    assert L.sq_quantize_grad(fake, 8, 8, 8, ct.byref(p), fake, 16, fake, 16, fake, fake, fake, fake, 16,
+                              None) == 4
+    # negative sizes
+    assert L.sq_quantize_grad(fake, -1, 8, 8, ct.byref(p), fake, 16, fake, 16, fake, fake, fake, fake, 4096,
+                              None) == 1
+    assert "workspace" in sq.sq_last_error() or "dimensions" in sq.sq_last_error()
+
+
+def test_overflow_risk_rejected(sq):
+    L = _raw(sq)
+    fake = ct.c_void_p(0x100000)
+    # dgrad: C_out * Q * 2^(N_G-1) * 128 >= 2^31 with b = 8, N_G = 8
+    p = sq.Params.make(8, 8, 0)
+    st = L.sq_gemm_dgrad(fake, 2048, fake, fake, fake, fake, 2048, fake, 4, 1100, 8, ct.byref(p), None, 0,
+                         fake, 8, fake, 1 << 30, None)
+    assert st == 2 and "overflow" in sq.sq_last_error()
+    # wgrad: M * Q * 128 >= 2^31 with b = 8
+    p = sq.Params.make(8, 4, 0)
+    st = L.sq_gemm_wgrad(fake, 1 << 18, fake, fake, fake, 1 << 18, fake, 140000, 4, 4, ct.byref(p), None, 0,
+                         fake, 4, fake, 1 << 30, None)
+    assert st == 2
+    # one row fewer than the bound is accepted by the range check (then fails on NULL scales)
+    st = L.sq_gemm_wgrad(fake, 1 << 18, fake, None, fake, 1 << 18, fake, 130000, 4, 4, ct.byref(p), None, 0,
+                         fake, 4, fake, 1 << 30, None)
+    assert st == 1
+
+
+def test_gemm_validation(sq):
+    L = _raw(sq)
+    fake = ct.c_void_p(0x100000)
+    p = sq.Params.make(4, 4, 0)
+    # both outputs NULL
+    assert L.sq_gemm_wgrad(fake, 64, fake, fake, fake, 64, fake, 64, 4, 4, ct.byref(p), None, 0, None, 0,
+                           fake, 0, None) == 1
+    # xq_t ld smaller than M
+    assert L.sq_gemm_wgrad(fake, 64, fake, fake, fake, 32, fake, 64, 4, 4, ct.byref(p), None, 0, fake, 4,
+                           fake, 0, None) == 1
+    # dgrad: wq_t ld smaller than C_out
+    assert L.sq_gemm_dgrad(fake, 64, fake, fake, fake, fake, 16, fake, 8, 40, 8, ct.byref(p), None, 0,
+                           fake, 8, fake, 0, None) == 1
+    # dequant: bad kind
+    assert L.sq_dequant(fake, 4, 4, 4, 7, fake, fake, fake, 4, fake, 4, None) == 1
+
+
+def test_python_binding_has_no_fallback(sq, monkeypatch, tmp_path):
+    # a missing library is an import-time error, never a silent CPU path
+    monkeypatch.setattr(sq, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(sq, "_lib", None)
+    with pytest.raises(ImportError):
+        sq.load()

@@ -1,0 +1,378 @@
+"""Parity of the HIP path (through the C-ABI) with the CPU oracle.
+
+Integers -- codes, group ids, scale bit patterns, int32 accumulators -- must
+match bit for bit; fp32 outputs within 1e-6 relative (the same IEEE
+operations run in the same order on both sides, so they are expected to be
+identical).  All inputs are seeded and synthetic.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2411_10948_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+RTOL = 1e-6
+
+
+@pytest.fixture(scope="module")
+def sq():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    from paper_2411_10948_amd import shiftquant
+    shiftquant.load()
+    return shiftquant
+
+
+def _qmax(bits):
+    return (1 << (bits - 1)) - 1
+
+
+def _T(bits):
+    Q, T = _qmax(bits), 0
+    while Q * (1 << (T + 1)) <= 127:
+        T += 1
+    return T
+
+
+def _f32bits(x):
+    return int(np.array([x], np.float32).view(np.uint32)[0])
+
+
+def _dev(a, ld_pad=0, misalign=0):
+    import torch
+    a = np.ascontiguousarray(a)
+    if ld_pad == 0 and misalign == 0:
+        return torch.from_numpy(a).cuda()
+    rows, cols = a.shape
+    buf = torch.zeros(rows * (cols + ld_pad) + misalign, dtype=torch.float32, device="cuda")
+    view = buf[misalign:misalign + rows * (cols + ld_pad)].view(rows, cols + ld_pad)[:, :cols]
+    view.copy_(torch.from_numpy(a).cuda())
+    return view
+
+
+def expected_layout(g, num_groups, bits, pad=64):
+    """The fold layout include/shiftquant.h documents, derived from the group ids."""
+    T = _T(bits)
+    sh = num_groups - 1 - g.astype(np.int64)
+    e = np.maximum(sh - T, 0)
+    E = int(e.max()) if e.size else 0
+    cols, starts = [], []
+    for r in range(E):
+        j = E - 1 - r
+        members = [int(c) for c in np.nonzero(e > j)[0]]
+        starts.append(len(cols))
+        cols += members + [-1] * ((-len(members)) % pad)
+    return E, cols, starts
+
+
+def check_quant(sq, codes, dY, bits, ng, mode, seed, offset):
+    q_ref, g_ref, s_ref, _ = oracle.quantize_grad(dY, bits, ng, mode, seed, offset)
+    M, C = dY.shape
+    q = codes.codes().cpu().numpy()
+    g = codes.group.cpu().numpy()
+    assert np.array_equal(g, g_ref), "group ids differ"
+    bad = np.argwhere(q != q_ref)
+    assert bad.size == 0, f"{len(bad)} codes differ, first at {bad[:5].tolist()}"
+    s = sq.scale_to_host(codes.scale)
+    assert s["bits"][0] == _f32bits(s_ref["r_max"])
+    assert s["bits"][1] == _f32bits(s_ref["inv0"])
+    assert s["bits"][2] == _f32bits(s_ref["d0"])
+    assert s["flags"] == s_ref["flags"]
+    # shift-folded dgrad operand and its appended columns
+    T = _T(bits)
+    t = np.minimum(ng - 1 - g_ref.astype(np.int64), T)
+    qf = codes.q_fold.cpu().numpy()
+    if M:
+        assert np.array_equal(qf[:, :C].astype(np.int64), q_ref.astype(np.int64) << t[None, :])
+    lay = codes.layout.cpu().numpy()
+    E, cols, starts = expected_layout(g_ref, ng, bits)
+    assert lay[0] == E and lay[1] == len(cols)
+    assert list(lay[16:16 + len(cols)]) == cols
+    assert list(lay[4:4 + E]) == starts
+    if M and cols:
+        base = int(lay[2])
+        ext = qf[:, base:base + len(cols)].astype(np.int64)
+        for j, ch in enumerate(cols):
+            want = (q_ref[:, ch].astype(np.int64) << t[ch]) if ch >= 0 else np.zeros(M, np.int64)
+            assert np.array_equal(ext[:, j], want), f"appended column {j} (channel {ch})"
+    return q_ref, g_ref, s_ref
+
+
+def check_layer(sq, dY, W, X, bits, ng, mode=0, seed=0, offset=0, dgrad_rows=None, wgrad_rows=None,
+                want_acc=True):
+    import torch
+    M, C_out = dY.shape
+    C_in = W.shape[1]
+    codes = sq.quantize_grad(_dev(dY), bits, ng, mode, seed, offset)
+    wq_t, ws = sq.quantize_tensor(_dev(W), 8, transpose=True)
+    xq_t, xs = sq.quantize_tensor(_dev(X), 8, transpose=True)
+    acc_d, dX = sq.gemm_dgrad(codes, wq_t, ws, want_acc=want_acc)
+    acc_w, dW = sq.gemm_wgrad(codes, xq_t, xs, want_acc=want_acc)
+    torch.cuda.synchronize()
+    q_ref, g_ref, s_ref = check_quant(sq, codes, dY, bits, ng, mode, seed, offset)
+
+    wq_ref, ws_ref = oracle.quantize_tensor(W, 8)
+    xq_ref, xs_ref = oracle.quantize_tensor(X, 8)
+    assert np.array_equal(wq_t[:, :C_out].t().cpu().numpy(), wq_ref)
+    assert np.array_equal(xq_t[:, :M].t().cpu().numpy(), xq_ref)
+    for got, ref in ((ws, ws_ref), (xs, xs_ref)):
+        h = sq.scale_to_host(got)
+        assert h["bits"][:3] == [_f32bits(ref["r_max"]), _f32bits(ref["inv0"]), _f32bits(ref["d0"])]
+        assert h["flags"] == ref["flags"]
+
+    rows_d = np.arange(M) if dgrad_rows is None else np.asarray(dgrad_rows)
+    rows_w = np.arange(C_out) if wgrad_rows is None else np.asarray(wgrad_rows)
+    A_ref = oracle.dgrad(q_ref, g_ref, ng, wq_ref, None if dgrad_rows is None else rows_d)
+    B_ref = oracle.wgrad(q_ref, xq_ref, None if wgrad_rows is None else rows_w)
+    dX_ref = oracle.dequant_dgrad(A_ref, s_ref["d0"], ws_ref["d0"], ng)
+    dW_ref = oracle.dequant_wgrad(B_ref, g_ref[rows_w], s_ref["d0"], xs_ref["d0"])
+
+    rows_d_t = torch.as_tensor(rows_d, device="cuda", dtype=torch.long)
+    rows_w_t = torch.as_tensor(rows_w, device="cuda", dtype=torch.long)
+    if want_acc:
+        assert np.array_equal(acc_d.index_select(0, rows_d_t).cpu().numpy(), A_ref), "dgrad int32 differs"
+        assert np.array_equal(acc_w.index_select(0, rows_w_t).cpu().numpy(), B_ref), "wgrad int32 differs"
+    dXg = dX.index_select(0, rows_d_t).cpu().numpy()
+    dWg = dW.index_select(0, rows_w_t).cpu().numpy()
+    np.testing.assert_allclose(dXg, dX_ref, rtol=RTOL, atol=0)
+    np.testing.assert_allclose(dWg, dW_ref, rtol=RTOL, atol=0)
+    return {"codes": codes, "dX": dX, "dW": dW, "acc_d": acc_d, "acc_w": acc_w,
+            "exact_dX": bool(np.array_equal(dXg.view(np.uint32), dX_ref.view(np.uint32))),
+            "exact_dW": bool(np.array_equal(dWg.view(np.uint32), dW_ref.view(np.uint32)))}
+
+
+def _grad(M, C, seed, s=2.0, frac=0.03, factor=100.0, dist="normal"):
+    return workloads.make_grad(M, C, seed=seed, sigma_s=s, outlier_frac=frac, outlier_factor=factor, dist=dist)
+
+
+# ---------------------------------------------------------------------------
+# quantizer
+# ---------------------------------------------------------------------------
+QUANT_SHAPES = [(1, 1), (1, 7), (5, 3), (64, 64), (129, 67), (300, 130), (257, 96), (1000, 257), (130, 1024)]
+
+
+@pytest.mark.parametrize("shape", QUANT_SHAPES, ids=[f"{m}x{c}" for m, c in QUANT_SHAPES])
+@pytest.mark.parametrize("bits,ng", [(4, 4), (6, 4), (8, 4), (2, 8), (5, 1), (7, 3)])
+@pytest.mark.parametrize("mode", [0, 1])
+def test_quantize_grad_parity(sq, shape, bits, ng, mode):
+    import torch
+    M, C = shape
+    dY = _grad(M, C, seed=M * 7 + C + bits)
+    codes = sq.quantize_grad(_dev(dY), bits, ng, mode, seed=11, offset=5)
+    torch.cuda.synchronize()
+    check_quant(sq, codes, dY, bits, ng, mode, 11, 5)
+
+
+@pytest.mark.parametrize("ld_pad,misalign", [(3, 0), (4, 0), (0, 1), (5, 3)])
+@pytest.mark.parametrize("mode", [0, 1])
+def test_quantize_grad_strided_input(sq, ld_pad, misalign, mode):
+    import torch
+    dY = _grad(200, 77, seed=3)
+    codes = sq.quantize_grad(_dev(dY, ld_pad, misalign), 6, 4, mode, seed=2, offset=9)
+    torch.cuda.synchronize()
+    check_quant(sq, codes, dY, 6, 4, mode, 2, 9)
+
+
+def test_quantize_degenerate_tensors(sq):
+    import torch
+    cases = {
+        "zeros": np.zeros((70, 33), np.float32),
+        "tiny": np.full((70, 33), 2.0 ** -100, np.float32),
+        "at_threshold": np.full((70, 33), 2.0 ** -96, np.float32),
+        "single": np.array([[-3.5]], np.float32),
+    }
+    nan = _grad(70, 33, seed=1)
+    nan[17, 5] = np.nan
+    cases["nan"] = nan
+    inf = _grad(70, 33, seed=2)
+    inf[69, 32] = -np.inf
+    cases["inf"] = inf
+    huge = _grad(70, 33, seed=4)
+    huge[0, 0] = 3.0e38
+    cases["huge"] = huge
+    subn = _grad(70, 33, seed=5) * np.float32(1e-35)
+    cases["subnormal_scale"] = subn.astype(np.float32)
+    for name, dY in cases.items():
+        for mode in (0, 1):
+            codes = sq.quantize_grad(_dev(dY), 4, 4, mode, seed=1, offset=1)
+            torch.cuda.synchronize()
+            check_quant(sq, codes, dY, 4, 4, mode, 1, 1)
+    # empty token dimension
+    codes = sq.quantize_grad(torch.zeros((0, 8), device="cuda"), 4, 4)
+    torch.cuda.synchronize()
+    s = sq.scale_to_host(codes.scale)
+    assert s["flags"] == sq.FLAG_ZERO
+    assert np.all(codes.group.cpu().numpy() == 3)
+
+
+def test_stochastic_rounding_streams(sq):
+    import torch
+    dY = _grad(64, 40, seed=9)
+    x = _dev(dY)
+    a = sq.quantize_grad(x, 4, 4, 1, seed=3, offset=10).codes().clone()
+    b = sq.quantize_grad(x, 4, 4, 1, seed=3, offset=10).codes().clone()
+    c = sq.quantize_grad(x, 4, 4, 1, seed=3, offset=11).codes().clone()
+    d = sq.quantize_grad(x, 4, 4, 1, seed=4, offset=10).codes().clone()
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    assert not torch.equal(a, c) and not torch.equal(a, d)
+
+
+@pytest.mark.parametrize("transpose", [0, 1])
+@pytest.mark.parametrize("shape", [(1, 1), (33, 17), (300, 129), (64, 1000)])
+@pytest.mark.parametrize("bits", [8, 4])
+def test_quantize_tensor_parity(sq, transpose, shape, bits):
+    import torch
+    rng = np.random.default_rng(shape[0] + shape[1])
+    T = (rng.standard_normal(shape) * 0.02).astype(np.float32)
+    q, s = sq.quantize_tensor(_dev(T), bits, transpose=bool(transpose))
+    torch.cuda.synchronize()
+    q_ref, s_ref = oracle.quantize_tensor(T, bits)
+    got = q[:, :shape[0]].t() if transpose else q[:, :shape[1]]
+    assert np.array_equal(got.cpu().numpy(), q_ref)
+    h = sq.scale_to_host(s)
+    assert h["bits"][:3] == [_f32bits(s_ref["r_max"]), _f32bits(s_ref["inv0"]), _f32bits(s_ref["d0"])]
+
+
+# ---------------------------------------------------------------------------
+# GEMMs on small layers (several tiles, ragged tails, every fold case)
+# ---------------------------------------------------------------------------
+LAYERS = [(1, 1, 1), (7, 5, 3), (130, 67, 45), (256, 256, 256), (300, 200, 129), (513, 130, 260),
+          (64, 1100, 40)]
+
+
+@pytest.mark.parametrize("layer", LAYERS, ids=[f"{m}x{co}x{ci}" for m, co, ci in LAYERS])
+@pytest.mark.parametrize("bits,ng", [(4, 4), (6, 4), (8, 4), (7, 3), (2, 8), (5, 1)])
+def test_layer_parity(sq, layer, bits, ng):
+    M, C_out, C_in = layer
+    rng = np.random.default_rng(M + C_out + C_in + bits)
+    dY = _grad(M, C_out, seed=M + bits, s=2.5)
+    W = (rng.standard_normal((C_out, C_in)) * 0.02).astype(np.float32)
+    X = rng.standard_normal((M, C_in)).astype(np.float32)
+    mode = 1 if (M + bits) % 2 else 0
+    check_layer(sq, dY, W, X, bits, ng, mode=mode, seed=7, offset=3)
+
+
+def test_fp32_only_outputs_match_with_acc(sq):
+    import torch
+    M, C_out, C_in = 300, 200, 129
+    rng = np.random.default_rng(1)
+    dY = _grad(M, C_out, seed=1)
+    W = (rng.standard_normal((C_out, C_in)) * 0.02).astype(np.float32)
+    X = rng.standard_normal((M, C_in)).astype(np.float32)
+    codes = sq.quantize_grad(_dev(dY), 6, 4)
+    wq_t, ws = sq.quantize_tensor(_dev(W), 8)
+    xq_t, xs = sq.quantize_tensor(_dev(X), 8)
+    a1, dX1 = sq.gemm_dgrad(codes, wq_t, ws, want_acc=True)
+    _, dX2 = sq.gemm_dgrad(codes, wq_t, ws, want_acc=False)
+    b1, dW1 = sq.gemm_wgrad(codes, xq_t, xs, want_acc=True)
+    _, dW2 = sq.gemm_wgrad(codes, xq_t, xs, want_acc=False)
+    b3, dW3 = sq.gemm_wgrad(codes, xq_t, xs, want_acc=True, want_out=False)
+    torch.cuda.synchronize()
+    assert torch.equal(dX1, dX2) and torch.equal(dW1, dW2) and torch.equal(b1, b3) and dW3 is None
+    # standalone dequantization of the accumulators gives the fused outputs
+    outd = torch.empty_like(dX1)
+    sq.sq_dequant(a1, 0, None, codes.scale, ws, 4, outd)
+    outw = torch.empty_like(dW1)
+    sq.sq_dequant(b1, 1, codes.group, codes.scale, xs, 4, outw)
+    torch.cuda.synchronize()
+    assert torch.equal(outd, dX1) and torch.equal(outw, dW1)
+
+
+def test_wgrad_split_k(sq):
+    # long token dimension, small output: the wgrad splits K over many blocks
+    M, C_out, C_in = 20000, 64, 96
+    rng = np.random.default_rng(5)
+    dY = _grad(M, C_out, seed=5)
+    W = (rng.standard_normal((C_out, C_in)) * 0.05).astype(np.float32)
+    X = np.maximum(rng.standard_normal((M, C_in)), 0).astype(np.float32)
+    assert sq.sq_gemm_wgrad_workspace_size(M, C_out, C_in, sq.Params.make(4)) > 0
+    check_layer(sq, dY, W, X, 4, 4, dgrad_rows=[0, 1, 5000, 19999])
+    check_layer(sq, dY, W, X, 4, 4, dgrad_rows=[3, 19998], want_acc=False)
+
+
+def test_degenerate_layers(sq):
+    rng = np.random.default_rng(2)
+    W = (rng.standard_normal((40, 24)) * 0.02).astype(np.float32)
+    X = rng.standard_normal((50, 24)).astype(np.float32)
+    zeros = np.zeros((50, 40), np.float32)
+    r = check_layer(sq, zeros, W, X, 4, 4)
+    assert not r["dX"].any() and not r["dW"].any()
+    nan = _grad(50, 40, seed=3)
+    nan[3, 3] = np.nan
+    r = check_layer(sq, nan, W, X, 6, 4)
+    assert not r["dX"].any()
+    Wz = np.zeros_like(W)
+    check_layer(sq, _grad(50, 40, seed=4), Wz, X, 4, 4)
+
+
+# ---------------------------------------------------------------------------
+# The five layer workloads: reduced token counts (full oracle) ...
+# ---------------------------------------------------------------------------
+REDUCED = {"linear_256": 256, "resnet18_conv3x3": 3136, "resnet50_conv1x1": 1000,
+           "mlp_up_768x3072": 600, "linear_4096x11008_sr": 200}
+
+
+@pytest.mark.parametrize("name", workloads.WORKLOAD_ORDER)
+def test_workload_reduced(sq, name):
+    wl = workloads.WORKLOADS[name]
+    d = workloads.make_inputs(name, M=REDUCED[name])
+    M = d["M"]
+    dgrad_rows = None
+    wgrad_rows = None
+    if wl.C_out * wl.C_in * M > 2e9:
+        dgrad_rows = np.unique(np.r_[0, 1, M // 2, M - 2, M - 1, np.arange(64, M, 97)])
+        rng = np.random.default_rng(1)
+        wgrad_rows = np.unique(np.r_[0, wl.C_out - 1, rng.integers(0, wl.C_out, 24)])
+    r = check_layer(sq, d["dY"], d["W"], d["X"], wl.bits, wl.num_groups, wl.round_mode, wl.sr_seed,
+                    wl.sr_offset, dgrad_rows, wgrad_rows)
+    assert r["exact_dX"] and r["exact_dW"]
+
+
+# ... and full size, in the launch configuration the benchmark times, with
+# every code compared and sampled GEMM rows computed by the oracle.
+@pytest.mark.parametrize("name", workloads.WORKLOAD_ORDER)
+def test_workload_full_size(sq, name):
+    import torch
+    wl = workloads.WORKLOADS[name]
+    d = workloads.make_inputs(name)
+    M, C_out, C_in = d["M"], wl.C_out, wl.C_in
+    print(f"[full-size parity] {name} M={M} C_out={C_out} C_in={C_in}", flush=True)
+    p = sq.Params.make(wl.bits, wl.num_groups, wl.round_mode, wl.sr_seed, wl.sr_offset)
+    plan = sq.BackwardPlan(M, C_out, C_in, p, want_acc=True)
+    dY = _dev(d["dY"])
+    wq_t, ws = sq.quantize_tensor(_dev(d["W"]), 8)
+    xq_t, xs = sq.quantize_tensor(_dev(d["X"]), 8)
+    plan.run(dY, wq_t, ws, xq_t, xs)
+    torch.cuda.synchronize()
+
+    q_ref, g_ref, s_ref, _ = oracle.quantize_grad(d["dY"], wl.bits, wl.num_groups, wl.round_mode,
+                                                  wl.sr_seed, wl.sr_offset)
+    q = plan.q_t[:, :M].t().cpu().numpy()
+    assert np.array_equal(plan.group.cpu().numpy(), g_ref)
+    assert np.array_equal(q, q_ref)
+    wq_ref, ws_ref = oracle.quantize_tensor(d["W"], 8)
+    xq_ref, xs_ref = oracle.quantize_tensor(d["X"], 8)
+    assert np.array_equal(wq_t[:, :C_out].t().cpu().numpy(), wq_ref)
+    assert np.array_equal(xq_t[:, :M].t().cpu().numpy(), xq_ref)
+
+    rng = np.random.default_rng(0)
+    n_d = 24 if C_out * C_in > 1e7 else 96
+    rows_d = np.unique(np.r_[0, M - 1, M - 2, (M // 128) * 128, rng.integers(0, M, n_d)])
+    outliers = np.nonzero(g_ref < wl.num_groups - 1)[0]
+    rows_w = np.unique(np.r_[0, C_out - 1, outliers[:8], rng.integers(0, C_out, 8)])
+    A_ref = oracle.dgrad(q_ref, g_ref, wl.num_groups, wq_ref, rows_d)
+    B_ref = oracle.wgrad(q_ref, xq_ref, rows_w)
+    dX_ref = oracle.dequant_dgrad(A_ref, s_ref["d0"], ws_ref["d0"], wl.num_groups)
+    dW_ref = oracle.dequant_wgrad(B_ref, g_ref[rows_w], s_ref["d0"], xs_ref["d0"])
+    rd = torch.as_tensor(rows_d, device="cuda")
+    rw = torch.as_tensor(rows_w, device="cuda")
+    assert np.array_equal(plan.acc_dX.index_select(0, rd).cpu().numpy(), A_ref)
+    assert np.array_equal(plan.acc_dW.index_select(0, rw).cpu().numpy(), B_ref)
+    np.testing.assert_allclose(plan.dX.index_select(0, rd).cpu().numpy(), dX_ref, rtol=RTOL, atol=0)
+    np.testing.assert_allclose(plan.dW.index_select(0, rw).cpu().numpy(), dW_ref, rtol=RTOL, atol=0)
+    # properties that hold at any size, checked on the whole outputs
+    assert torch.isfinite(plan.dX).all() and torch.isfinite(plan.dW).all()
+    assert plan.q_t[:, :M].abs().max().item() == (1 << (wl.bits - 1)) - 1
