@@ -1,6 +1,7 @@
 // extern "C" entry points of libshiftquant: synchronous argument checks,
 // workspace carving and stream-ordered kernel launches.  The semantics of
 // every call are documented in include/shiftquant.h.
+#include <algorithm>
 #include <cstdint>
 #include <cstring>
 #include <string>
@@ -83,7 +84,8 @@ sq_status check_dims(int64_t rows, int64_t cols, const char* what) {
     return SQ_OK;
 }
 
-size_t rbits_bytes(int64_t C) { return (size_t)round_up(C > 0 ? C * 4 : 4, 256); }
+// quantizer scratch: slab maxima [slabs, C] followed by the channel ranges [C]
+size_t quant_ws_bytes(int64_t M, int64_t C) { return (size_t)round_up(std::max<int64_t>(colmax_workspace_words(M, C), 1) * 4, 256); }
 
 #define SQ_TRY(expr)                      \
     do {                                  \
@@ -126,14 +128,14 @@ sq_status sq_quantize_grad_workspace_size(int64_t M, int64_t C_out, const sq_qua
     SQ_TRY(check_params(p));
     SQ_TRY(check_dims(M, C_out, "gradient"));
     if (!bytes) return fail(SQ_ERR_INVALID_ARGUMENT, "bytes is NULL");
-    *bytes = rbits_bytes(C_out);
+    *bytes = quant_ws_bytes(M, C_out);
     return SQ_OK;
 }
 
 sq_status sq_quantize_tensor_workspace_size(int64_t rows, int64_t cols, size_t* bytes) {
     SQ_TRY(check_dims(rows, cols, "tensor"));
     if (!bytes) return fail(SQ_ERR_INVALID_ARGUMENT, "bytes is NULL");
-    *bytes = rbits_bytes(cols);
+    *bytes = quant_ws_bytes(rows, cols);
     return SQ_OK;
 }
 
@@ -155,7 +157,7 @@ sq_status sq_gemm_wgrad_workspace_size(int64_t M, int64_t C_out, int64_t C_in, c
     SQ_TRY(check_dims(C_in, C_in, "activation"));
     if (!bytes) return fail(SQ_ERR_INVALID_ARGUMENT, "bytes is NULL");
     const int splits = (M > 0 && C_out > 0 && C_in > 0) ? wgrad_splits(M, C_out, C_in) : 1;
-    *bytes = splits > 1 ? (size_t)round_up(C_out * C_in * 4, 256) : 0;
+    *bytes = splits > 1 ? (size_t)round_up((int64_t)splits * C_out * C_in * 4, 256) : 0;
     return SQ_OK;
 }
 
@@ -175,14 +177,15 @@ sq_status sq_quantize_grad(const float* dY, int64_t M, int64_t C_out, int64_t ld
     if (q_fold && M > 0) SQ_TRY(check_codes(q_fold, ld_fold, min_ld_fold, "q_fold"));
     if (q_t && C_out > 0) SQ_TRY(check_codes(q_t, ld_t, M > 0 ? M : 1, "q_t"));
     if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
-    if (workspace_bytes < rbits_bytes(C_out)) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+    if (workspace_bytes < quant_ws_bytes(M, C_out)) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
 
     const QuantCfg cfg = make_cfg(*p);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    uint32_t* rbits = static_cast<uint32_t*>(workspace);
-    SQ_TRY(hip_status(launch_fill_u32(rbits, C_out, 0u, s), "fill"));
-    SQ_TRY(hip_status(launch_colmax(dY, M, C_out, ld_dY, rbits, s), "colmax"));
-    SQ_TRY(hip_status(launch_finalize_grad(rbits, C_out, cfg, group, scale, layout, s), "finalize"));
+    uint32_t* partial = static_cast<uint32_t*>(workspace);
+    int64_t slabs = 0;
+    SQ_TRY(hip_status(launch_colmax(dY, M, C_out, ld_dY, partial, &slabs, s), "colmax"));
+    uint32_t* rbits = partial + slabs * C_out;
+    SQ_TRY(hip_status(launch_finalize_grad(partial, slabs, C_out, cfg, rbits, group, scale, layout, s), "finalize"));
     SQ_TRY(hip_status(launch_quantize(dY, M, C_out, ld_dY, group, scale, cfg, q_fold, ld_fold, q_t, ld_t,
                                       layout, s),
                       "quantize"));
@@ -201,7 +204,7 @@ sq_status sq_quantize_tensor(const float* T, int64_t rows, int64_t cols, int64_t
     }
     if (!scale || !aligned(scale, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "scale is NULL or misaligned");
     if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
-    if (workspace_bytes < rbits_bytes(cols)) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+    if (workspace_bytes < quant_ws_bytes(rows, cols)) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
 
     sq_quant_params p{};
     p.bits = bits;
@@ -209,10 +212,10 @@ sq_status sq_quantize_tensor(const float* T, int64_t rows, int64_t cols, int64_t
     p.round_mode = SQ_ROUND_NEAREST_EVEN;
     const QuantCfg cfg = make_cfg(p);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    uint32_t* rbits = static_cast<uint32_t*>(workspace);
-    SQ_TRY(hip_status(launch_fill_u32(rbits, cols, 0u, s), "fill"));
-    SQ_TRY(hip_status(launch_colmax(T, rows, cols, ld, rbits, s), "colmax"));
-    SQ_TRY(hip_status(launch_finalize_tensor(rbits, cols, cfg.Q, scale, s), "finalize"));
+    uint32_t* partial = static_cast<uint32_t*>(workspace);
+    int64_t slabs = 0;
+    SQ_TRY(hip_status(launch_colmax(T, rows, cols, ld, partial, &slabs, s), "colmax"));
+    SQ_TRY(hip_status(launch_finalize_tensor(partial, slabs, cols, cfg.Q, scale, s), "finalize"));
     SQ_TRY(hip_status(launch_quantize(T, rows, cols, ld, nullptr, scale, cfg, transpose ? nullptr : q, ld_q,
                                       transpose ? q : nullptr, ld_q, nullptr, s),
                       "quantize"));
@@ -265,7 +268,6 @@ sq_status sq_gemm_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* la
     a.splits = 1;
     a.acc = acc; a.ld_acc = ld_acc;
     a.out = dX; a.ld_out = ld_dX;
-    a.atomic_acc = 0;
     a.epi_mode = 0;
     a.gs = gscale; a.os = wscale; a.group = group; a.num_groups = cfg.num_groups;
     return hip_status(launch_gemm(a, s), "gemm_dgrad");
@@ -310,24 +312,16 @@ sq_status sq_gemm_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, c
         a.out = dW; a.ld_out = ld_dW;
         return hip_status(launch_gemm(a, s), "gemm_wgrad");
     }
-    int32_t* target = acc;
-    int64_t ld_target = ld_acc;
-    if (!target) {
-        if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
-        if (workspace_bytes < need) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
-        target = static_cast<int32_t*>(workspace);
-        ld_target = C_in;
-    }
-    SQ_TRY(hip_status(launch_zero_i32(target, C_out, C_in, ld_target, s), "zero"));
-    a.splits = splits;
-    a.acc = target; a.ld_acc = ld_target;
-    a.atomic_acc = 1;
-    SQ_TRY(hip_status(launch_gemm(a, s), "gemm_wgrad"));
-    if (dW)
-        SQ_TRY(hip_status(launch_dequant(target, C_out, C_in, ld_target, 1, group, gscale, xscale, cfg.num_groups, dW,
-                                         ld_dW, s),
-                          "dequant"));
-    return SQ_OK;
+    if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
+    if (workspace_bytes < need) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+    int32_t* ws = static_cast<int32_t*>(workspace);
+    GemmArgs g = a;
+    g.splits = splits;
+    g.part = ws;
+    SQ_TRY(hip_status(launch_gemm(g, s), "gemm_wgrad"));
+    a.acc = acc; a.ld_acc = ld_acc;
+    a.out = dW; a.ld_out = ld_dW;
+    return hip_status(launch_splitk_reduce(ws, splits, a, s), "splitk_reduce");
 }
 
 sq_status sq_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_t ld_acc, int32_t kind,

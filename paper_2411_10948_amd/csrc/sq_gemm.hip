@@ -160,13 +160,14 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm_i8(GemmArgs p, int tiles_n
 
     // ---- epilogue ----
     float base = 0.0f, alpha = 0.0f;
-    if (p.out) {
+    if (p.out && !p.part) {
         const sq_scale gs = *p.gs, os = *p.os;
         base = __fmul_rn(gs.step, os.step);
         alpha = __fmul_rn(base, pow2f(-(p.num_groups - 1)));
     }
     const bool vec_acc = p.acc && ((p.ld_acc & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.acc) & 15) == 0);
     const bool vec_out = p.out && ((p.ld_out & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.out) & 15) == 0);
+    const bool vec_part = p.part && ((p.Ng & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.part) & 15) == 0);
 #pragma unroll
     for (int wi = 0; wi < 2; ++wi) {
         const int64_t ii = m0 + wm * 64 + wi * 32 + (lane & 31);
@@ -183,11 +184,16 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm_i8(GemmArgs p, int tiles_n
                 const int v2 = acc[wi][wj][a4 * 4 + 2], v3 = acc[wi][wj][a4 * 4 + 3];
                 const int vv[4] = {v0, v1, v2, v3};
                 const bool full = jj + 4 <= p.Ng;
-                if (p.atomic_acc) {
-                    int32_t* dst = p.acc + ii * p.ld_acc + jj;
+                if (p.part) {
+                    // split-K: this split's partial tile, dense [splits, Mg, Ng]
+                    int32_t* dst = p.part + (int64_t)blockIdx.y * p.Mg * p.Ng + ii * p.Ng + jj;
+                    if (vec_part && full) {
+                        *reinterpret_cast<int4*>(dst) = make_int4(v0, v1, v2, v3);
+                    } else {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (jj + e < p.Ng) atomicAdd(dst + e, vv[e]);
+                        for (int e = 0; e < 4; ++e)
+                            if (jj + e < p.Ng) dst[e] = vv[e];
+                    }
                     continue;
                 }
                 if (p.acc) {
@@ -231,9 +237,62 @@ __global__ void k_gather_ext(const int8_t* __restrict__ wq_t, int64_t ld_w, int6
         }
 }
 
-__global__ void k_zero_i32(int32_t* __restrict__ p, int64_t rows, int64_t cols, int64_t ld) {
-    for (int64_t r = blockIdx.x; r < rows; r += gridDim.x)
-        for (int64_t c = threadIdx.x; c < cols; c += blockDim.x) p[r * ld + c] = 0;
+// Sum of the split-K partial tiles ws [splits, Mg, Ng] (int32 addition is
+// exact and order-free), then the same epilogue as the GEMM.
+__global__ void k_splitk_reduce(const int32_t* __restrict__ ws, int splits, int64_t Mg, int64_t Ng,
+                                int32_t* __restrict__ acc, int64_t ld_acc, float* __restrict__ out, int64_t ld_out,
+                                int epi_mode, const uint8_t* __restrict__ group, const sq_scale* __restrict__ gs,
+                                const sq_scale* __restrict__ os, int num_groups) {
+    const int64_t plane = Mg * Ng;
+    float base = 0.0f, alpha = 0.0f;
+    if (out) {
+        base = __fmul_rn(gs->step, os->step);
+        alpha = __fmul_rn(base, pow2f(-(num_groups - 1)));
+    }
+    const bool vec = ((Ng & 3) == 0);
+    const int64_t n_items = vec ? plane / 4 : plane;
+    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < n_items;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        if (vec) {
+            const int64_t e = q * 4;
+            int4 a[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) a[u] = make_int4(0, 0, 0, 0);
+            int s = 0;
+            for (; s + 4 <= splits; s += 4) {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int4 v = *reinterpret_cast<const int4*>(ws + (int64_t)(s + u) * plane + e);
+                    a[u].x += v.x; a[u].y += v.y; a[u].z += v.z; a[u].w += v.w;
+                }
+            }
+            for (; s < splits; ++s) {
+                const int4 v = *reinterpret_cast<const int4*>(ws + (int64_t)s * plane + e);
+                a[0].x += v.x; a[0].y += v.y; a[0].z += v.z; a[0].w += v.w;
+            }
+            const int t[4] = {a[0].x + a[1].x + a[2].x + a[3].x, a[0].y + a[1].y + a[2].y + a[3].y,
+                              a[0].z + a[1].z + a[2].z + a[3].z, a[0].w + a[1].w + a[2].w + a[3].w};
+            const int64_t i = e / Ng, j = e % Ng;
+            if (acc) {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) acc[i * ld_acc + j + u] = t[u];
+            }
+            if (out) {
+                const float sc = epi_mode == 1 ? __fmul_rn(base, pow2f(-(int)group[i])) : alpha;
+#pragma unroll
+                for (int u = 0; u < 4; ++u) out[i * ld_out + j + u] = __fmul_rn((float)t[u], sc);
+            }
+        } else {
+            int t = 0;
+            for (int s = 0; s < splits; ++s) t += ws[(int64_t)s * plane + q];
+            const int64_t i = q / Ng, j = q % Ng;
+            if (acc) acc[i * ld_acc + j] = t;
+            if (out) {
+                const float sc = epi_mode == 1 ? __fmul_rn(base, pow2f(-(int)group[i])) : alpha;
+                out[i * ld_out + j] = __fmul_rn((float)t, sc);
+            }
+        }
+    }
 }
 
 __global__ void k_dequant(const int32_t* __restrict__ acc, int64_t rows, int64_t cols, int64_t ld_acc, int kind,
@@ -271,6 +330,7 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     const int64_t per = splits > 1 ? (ktiles + splits - 1) / splits : std::max<int64_t>(ktiles, 1);
     const int64_t k_per_split = per * BK;
     if (splits > 1) splits = (int)((ktiles + per - 1) / per);
+    if (splits != std::max(1, a.splits)) return hipErrorInvalidValue;   // wgrad_splits() avoids this
     dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)splits);
     hipLaunchKernelGGL(k_gemm_i8, grid, dim3(kThreads), 0, s, a, (int)tiles_n, k_per_split);
     return hipGetLastError();
@@ -284,10 +344,12 @@ hipError_t launch_gather_ext(const int8_t* wq_t, int64_t ld_w, int64_t C_in, con
     return hipGetLastError();
 }
 
-hipError_t launch_zero_i32(int32_t* p, int64_t rows, int64_t cols, int64_t ld, hipStream_t s) {
-    if (rows <= 0 || cols <= 0) return hipSuccess;
-    const unsigned blocks = (unsigned)std::min<int64_t>(rows, 4096);
-    hipLaunchKernelGGL(k_zero_i32, dim3(blocks), dim3(256), 0, s, p, rows, cols, ld);
+hipError_t launch_splitk_reduce(const int32_t* ws, int splits, const GemmArgs& a, hipStream_t s) {
+    if (a.Mg <= 0 || a.Ng <= 0) return hipSuccess;
+    const int64_t items = (a.Ng & 3) == 0 ? a.Mg * a.Ng / 4 : a.Mg * a.Ng;
+    const unsigned blocks = (unsigned)std::min<int64_t>((items + 255) / 256, 2048);
+    hipLaunchKernelGGL(k_splitk_reduce, dim3(blocks), dim3(256), 0, s, ws, splits, a.Mg, a.Ng, a.acc, a.ld_acc,
+                       a.out, a.ld_out, a.epi_mode, a.group, a.gs, a.os, a.num_groups);
     return hipGetLastError();
 }
 

@@ -43,12 +43,22 @@ int64_t fold_ext_max(int64_t C, const QuantCfg& c);
 __host__ __device__ inline int64_t fold_ext_base(int64_t C) { return round_up(C, kFoldPad); }
 
 // ---- quantizer (sq_quant.hip) ----
-hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
-hipError_t launch_colmax(const float* x, int64_t M, int64_t C, int64_t ld, uint32_t* rbits,
+// First-level abs-max: rows cut into `slabs`, chunks of 4 * tpr channels.
+struct ColmaxPlan {
+    int vec;
+    int tpr;
+    int64_t chunks;
+    int64_t slabs;
+    int64_t rows_per_slab;
+};
+ColmaxPlan colmax_plan(int64_t M, int64_t C, bool vec);
+// uint32 words of scratch for the slab maxima and the channel ranges
+int64_t colmax_workspace_words(int64_t M, int64_t C);
+hipError_t launch_colmax(const float* x, int64_t M, int64_t C, int64_t ld, uint32_t* partial, int64_t* slabs,
                          hipStream_t s);
-hipError_t launch_finalize_grad(const uint32_t* rbits, int64_t C, const QuantCfg& cfg,
-                                uint8_t* group, sq_scale* scale, int32_t* layout, hipStream_t s);
-hipError_t launch_finalize_tensor(const uint32_t* rbits, int64_t C, int Q, sq_scale* scale,
+hipError_t launch_finalize_grad(const uint32_t* partial, int64_t slabs, int64_t C, const QuantCfg& cfg,
+                                uint32_t* rbits, uint8_t* group, sq_scale* scale, int32_t* layout, hipStream_t s);
+hipError_t launch_finalize_tensor(const uint32_t* partial, int64_t slabs, int64_t C, int Q, sq_scale* scale,
                                   hipStream_t s);
 // group == nullptr: every channel in group 0 with shift 0 (per-tensor mode).
 hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, const uint8_t* group,
@@ -66,9 +76,9 @@ struct GemmArgs {
     const int8_t* extB; int64_t ld_extB;
     const int32_t* layout;
     int splits;                     // split-K factor over the main segment
-    int32_t* acc; int64_t ld_acc;   // int32 output (or split-K target)
+    int32_t* acc; int64_t ld_acc;   // int32 output
     float* out; int64_t ld_out;     // fp32 output
-    int atomic_acc;                 // split-K: atomically add into acc, no fp32 output
+    int32_t* part;                  // split-K: partial tiles [splits, Mg, Ng] instead of acc/out
     int epi_mode;                   // 0: dgrad scale, 1: wgrad per-row scale
     const sq_scale* gs;
     const sq_scale* os;
@@ -79,7 +89,7 @@ struct GemmArgs {
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gather_ext(const int8_t* wq_t, int64_t ld_w, int64_t C_in, const int32_t* layout,
                              int8_t* wext, int64_t ld_ext, int64_t ext_max, hipStream_t s);
-hipError_t launch_zero_i32(int32_t* p, int64_t rows, int64_t cols, int64_t ld, hipStream_t s);
+hipError_t launch_splitk_reduce(const int32_t* ws, int splits, const GemmArgs& a, hipStream_t s);
 hipError_t launch_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_t ld_acc, int kind,
                           const uint8_t* group, const sq_scale* gs, const sq_scale* os,
                           int num_groups, float* out, int64_t ld_out, hipStream_t s);

@@ -3,9 +3,10 @@
 // Three stream-ordered passes (the tensor range r_max is global, so the
 // gradient is read twice):
 //   k_colmax    per-channel abs-max r_c (Sec. 3.1) as unsigned bit patterns,
-//               coalesced float4 row loads, one atomicMax per channel per block
-//   k_finalize  one block: r_max, group ids (power-of-two thresholds,
-//               Sec. 3.1), scales, flags, and the fold layout for the dgrad
+//               coalesced float4 row loads, one maximum per channel per slab
+//   k_finalize  one block: combines the slab maxima into r_c and r_max, group
+//               ids (power-of-two thresholds, Sec. 3.1), scales, flags, and
+//               the fold layout for the dgrad
 //   k_quantize  scale, round (ties-to-even or Philox stochastic rounding,
 //               App. B Eq. "sq"), clamp, write the shift-folded dgrad operand
 //               row-major and the codes transposed (LDS 4x4-byte transposes)
@@ -71,24 +72,23 @@ __device__ __forceinline__ int quant_one(float x, float s, float Qf, uint32_t u2
 }
 
 // ---------------------------------------------------------------------------
-__global__ void k_fill_u32(uint32_t* __restrict__ p, int64_t n, uint32_t v) {
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x)
-        p[i] = v;
-}
+// ---------------------------------------------------------------------------
+// Per-channel abs-max, first level.  The rows are cut into slabs; block
+// (chunk, slab) reduces its slab for the chunk's channels and stores the
+// slab maxima to partial[slab * C + c] (plain stores: same-address atomics
+// from many blocks serialise, so the slabs are combined by the finalize
+// kernel instead).  Thread (rl, tc) covers VEC channels starting at
+// (chunk * tpr + tc) * VEC and rows rl, rl + kColThreads / tpr, ...
+// ---------------------------------------------------------------------------
+constexpr int kColThreads = 512;
 
-// ---------------------------------------------------------------------------
-// Per-channel abs-max.  Thread (rl, tc) of a block covers VEC channels
-// starting at (blockIdx.x * tpr + tc) * VEC and rows rl, rl + 256/tpr, ...
-// of the block's row slab.
-// ---------------------------------------------------------------------------
 template <int VEC>
-__global__ __launch_bounds__(kBlock) void k_colmax(const float* __restrict__ x, int64_t M, int64_t C,
-                                                   int64_t ld, int tpr, int64_t rows_per_slab,
-                                                   uint32_t* __restrict__ rbits) {
-    __shared__ uint32_t red[kBlock * VEC];
+__global__ __launch_bounds__(kColThreads) void k_colmax(const float* __restrict__ x, int64_t M, int64_t C,
+                                                        int64_t ld, int tpr, int64_t rows_per_slab,
+                                                        uint32_t* __restrict__ partial) {
+    __shared__ uint32_t red[kColThreads * VEC];
     const int tid = threadIdx.x;
-    const int nrl = kBlock / tpr;
+    const int nrl = kColThreads / tpr;
     const int rl = tid / tpr, tc = tid % tpr;
     const int64_t c0 = ((int64_t)blockIdx.x * tpr + tc) * VEC;
     const int64_t m_begin = (int64_t)blockIdx.y * rows_per_slab;
@@ -137,10 +137,26 @@ __global__ __launch_bounds__(kBlock) void k_colmax(const float* __restrict__ x, 
         for (int r = 1; r < nrl; ++r)
 #pragma unroll
             for (int j = 0; j < VEC; ++j) best[j] = max(best[j], red[(r * tpr + tc) * VEC + j]);
+        uint32_t* dst = partial + (int64_t)blockIdx.y * C + c0;
 #pragma unroll
         for (int j = 0; j < VEC; ++j)
-            if (c0 + j < C && best[j] != 0u) atomicMax(rbits + c0 + j, best[j]);
+            if (c0 + j < C) dst[j] = best[j];
     }
+}
+
+// max over the S slab maxima of channel c (8 loads in flight per thread)
+__device__ __forceinline__ uint32_t reduce_slabs(const uint32_t* __restrict__ partial, int64_t S, int64_t C,
+                                                 int64_t c) {
+    uint32_t a[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+    int64_t s = 0;
+    for (; s + 8 <= S; s += 8) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) a[u] = max(a[u], partial[(s + u) * C + c]);
+    }
+    for (; s < S; ++s) a[0] = max(a[0], partial[s * C + c]);
+#pragma unroll
+    for (int u = 1; u < 8; ++u) a[0] = max(a[0], a[u]);
+    return a[0];
 }
 
 // ---------------------------------------------------------------------------
@@ -193,18 +209,42 @@ __device__ __forceinline__ int excess_of(int g, const QuantCfg& cfg) {
 }
 
 // ---------------------------------------------------------------------------
-// Finalize for the gradient quantizer (one block of 1024 threads).
+// Finalize for the gradient quantizer (one block).  Thread tid owns the
+// channels c = tid + k * kFinThreads; for k < kFinRegs their ranges and
+// excess shifts stay in registers, beyond that they are re-read from rbits
+// (written by the same thread).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void k_finalize_grad(const uint32_t* __restrict__ rbits, int64_t C,
-                                                        QuantCfg cfg, uint8_t* __restrict__ group,
-                                                        sq_scale* __restrict__ scale,
-                                                        int32_t* __restrict__ layout) {
+constexpr int kFinThreads = 1024, kFinRegs = 16;
+
+__global__ __launch_bounds__(kFinThreads) void k_finalize_grad(const uint32_t* __restrict__ partial, int64_t S,
+                                                               int64_t C, QuantCfg cfg,
+                                                               uint32_t* __restrict__ rbits,
+                                                               uint8_t* __restrict__ group,
+                                                               sq_scale* __restrict__ scale,
+                                                               int32_t* __restrict__ layout) {
     __shared__ uint32_t shu[16];
     __shared__ int shi[16];
-    const int tid = threadIdx.x, nt = blockDim.x;
+    const int tid = threadIdx.x;
 
+    // channel ranges and r_max
+    uint32_t rr[kFinRegs];
     uint32_t mb = 0u;
-    for (int64_t c = tid; c < C; c += nt) mb = max(mb, rbits[c]);
+#pragma unroll
+    for (int k = 0; k < kFinRegs; ++k) {
+        const int64_t c = tid + (int64_t)k * kFinThreads;
+        uint32_t r = 0u;
+        if (c < C) {
+            r = reduce_slabs(partial, S, C, c);
+            rbits[c] = r;
+        }
+        rr[k] = r;
+        mb = max(mb, r);
+    }
+    for (int64_t c = tid + (int64_t)kFinRegs * kFinThreads; c < C; c += kFinThreads) {
+        const uint32_t r = reduce_slabs(partial, S, C, c);
+        rbits[c] = r;
+        mb = max(mb, r);
+    }
     mb = block_max_u32(mb, shu);
     const float r_max = __uint_as_float(mb);
     uint32_t flags = 0u;
@@ -221,9 +261,22 @@ __global__ __launch_bounds__(1024) void k_finalize_grad(const uint32_t* __restri
         *scale = s;
     }
 
-    // group ids and the largest excess shift
+    // group ids and excess shifts
+    uint8_t ee[kFinRegs];
     int emax = 0;
-    for (int64_t c = tid; c < C; c += nt) {
+#pragma unroll
+    for (int k = 0; k < kFinRegs; ++k) {
+        const int64_t c = tid + (int64_t)k * kFinThreads;
+        int e = 0;
+        if (c < C) {
+            const int g = flags ? cfg.num_groups - 1 : group_of(__uint_as_float(rr[k]), r_max, cfg.num_groups);
+            group[c] = (uint8_t)g;
+            e = excess_of(g, cfg);
+        }
+        ee[k] = (uint8_t)e;
+        emax = max(emax, e);
+    }
+    for (int64_t c = tid + (int64_t)kFinRegs * kFinThreads; c < C; c += kFinThreads) {
         const int g = flags ? cfg.num_groups - 1 : group_of(__uint_as_float(rbits[c]), r_max, cfg.num_groups);
         group[c] = (uint8_t)g;
         emax = max(emax, excess_of(g, cfg));
@@ -238,17 +291,30 @@ __global__ __launch_bounds__(1024) void k_finalize_grad(const uint32_t* __restri
     for (int r = 0; r < E; ++r) {
         const int j = E - 1 - r;
         int written = 0;
-        for (int64_t c_base = 0; c_base < C; c_base += nt) {
+#pragma unroll
+        for (int k = 0; k < kFinRegs; ++k) {
+            const int64_t c_base = (int64_t)k * kFinThreads;
+            if (c_base < C) {      // uniform across the block
+                const int64_t c = c_base + tid;
+                const bool member = c < C && (int)ee[k] > j;
+                int chunk_total = 0;
+                const int pos = block_excl_scan_flag(member, shi, &chunk_total);
+                if (member) ext[start + written + pos] = (int32_t)c;
+                written += chunk_total;
+            }
+        }
+        for (int64_t c_base = (int64_t)kFinRegs * kFinThreads; c_base < C; c_base += kFinThreads) {
             const int64_t c = c_base + tid;
             bool member = false;
-            if (c < C) member = excess_of(group_of(__uint_as_float(rbits[c]), r_max, cfg.num_groups), cfg) > j;
+            if (c < C)
+                member = excess_of(group_of(__uint_as_float(rbits[c]), r_max, cfg.num_groups), cfg) > j;
             int chunk_total = 0;
             const int pos = block_excl_scan_flag(member, shi, &chunk_total);
             if (member) ext[start + written + pos] = (int32_t)c;
             written += chunk_total;
         }
         const int padded = (int)round_up(written, kFoldPad);
-        for (int i = written + tid; i < padded; i += nt) ext[start + i] = -1;
+        for (int i = written + tid; i < padded; i += kFinThreads) ext[start + i] = -1;
         if (tid == 0) layout[4 + r] = start;
         start += padded;
     }
@@ -262,13 +328,14 @@ __global__ __launch_bounds__(1024) void k_finalize_grad(const uint32_t* __restri
 }
 
 // ---------------------------------------------------------------------------
-// Finalize for per-tensor quantization (one block).
+// Finalize for per-tensor quantization (one block): the maximum of all slab
+// maxima is the tensor's absolute maximum.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void k_finalize_tensor(const uint32_t* __restrict__ rbits, int64_t C,
-                                                          int Q, sq_scale* __restrict__ scale) {
+__global__ __launch_bounds__(kFinThreads) void k_finalize_tensor(const uint32_t* __restrict__ partial, int64_t S,
+                                                                 int64_t C, int Q, sq_scale* __restrict__ scale) {
     __shared__ uint32_t shu[16];
     uint32_t mb = 0u;
-    for (int64_t c = threadIdx.x; c < C; c += blockDim.x) mb = max(mb, rbits[c]);
+    for (int64_t c = threadIdx.x; c < C; c += kFinThreads) mb = max(mb, reduce_slabs(partial, S, C, c));
     mb = block_max_u32(mb, shu);
     if (threadIdx.x == 0) {
         const float a = __uint_as_float(mb);
@@ -446,45 +513,57 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
-hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s) {
-    if (n <= 0) return hipSuccess;
-    const int64_t blocks = std::min<int64_t>((n + kBlock - 1) / kBlock, 1024);
-    hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)blocks), dim3(kBlock), 0, s, p, n, v);
-    return hipGetLastError();
-}
-
-hipError_t launch_colmax(const float* x, int64_t M, int64_t C, int64_t ld, uint32_t* rbits, hipStream_t s) {
-    if (M <= 0 || C <= 0) return hipSuccess;
-    const bool vec = ((ld & 3) == 0) && ((reinterpret_cast<uintptr_t>(x) & 15) == 0);
+ColmaxPlan colmax_plan(int64_t M, int64_t C, bool vec) {
+    ColmaxPlan p{};
     const int VEC = vec ? 4 : 1;
     const int64_t units = (C + VEC - 1) / VEC;
     int tpr = 1;
-    while (tpr < units && tpr < kBlock) tpr <<= 1;
-    const int nrl = kBlock / tpr;
-    const int64_t chunks = (units + tpr - 1) / tpr;
-    // about 2048 blocks in total, each slab at least 4 row-passes deep
-    int64_t slabs = std::max<int64_t>(1, 2048 / chunks);
+    while (tpr < units && tpr < 64) tpr <<= 1;
+    const int nrl = kColThreads / tpr;
+    p.vec = VEC;
+    p.tpr = tpr;
+    p.chunks = std::max<int64_t>(1, (units + tpr - 1) / tpr);
+    // about 512 blocks (two per CU), each slab at least 4 row passes deep
+    int64_t slabs = std::max<int64_t>(1, 512 / p.chunks);
     const int64_t min_rows = 4 * (int64_t)nrl;
     slabs = std::min<int64_t>(slabs, std::max<int64_t>(1, (M + min_rows - 1) / min_rows));
     slabs = std::min<int64_t>(slabs, 65535);
-    const int64_t rows_per_slab = (M + slabs - 1) / slabs;
-    slabs = (M + rows_per_slab - 1) / rows_per_slab;
-    dim3 grid((unsigned)chunks, (unsigned)slabs);
+    p.rows_per_slab = std::max<int64_t>(1, (M + slabs - 1) / slabs);
+    p.slabs = M > 0 ? (M + p.rows_per_slab - 1) / p.rows_per_slab : 0;
+    return p;
+}
+
+int64_t colmax_workspace_words(int64_t M, int64_t C) {
+    // worst case over both vector widths: partial maxima + channel ranges
+    const ColmaxPlan a = colmax_plan(M, C, true), b = colmax_plan(M, C, false);
+    return std::max(a.slabs, b.slabs) * C + C;
+}
+
+hipError_t launch_colmax(const float* x, int64_t M, int64_t C, int64_t ld, uint32_t* partial, int64_t* slabs,
+                         hipStream_t s) {
+    *slabs = 0;
+    if (M <= 0 || C <= 0) return hipSuccess;
+    const bool vec = ((ld & 3) == 0) && ((reinterpret_cast<uintptr_t>(x) & 15) == 0);
+    const ColmaxPlan p = colmax_plan(M, C, vec);
+    *slabs = p.slabs;
+    dim3 grid((unsigned)p.chunks, (unsigned)p.slabs);
     if (vec)
-        hipLaunchKernelGGL(k_colmax<4>, grid, dim3(kBlock), 0, s, x, M, C, ld, tpr, rows_per_slab, rbits);
+        hipLaunchKernelGGL(k_colmax<4>, grid, dim3(kColThreads), 0, s, x, M, C, ld, p.tpr, p.rows_per_slab, partial);
     else
-        hipLaunchKernelGGL(k_colmax<1>, grid, dim3(kBlock), 0, s, x, M, C, ld, tpr, rows_per_slab, rbits);
+        hipLaunchKernelGGL(k_colmax<1>, grid, dim3(kColThreads), 0, s, x, M, C, ld, p.tpr, p.rows_per_slab, partial);
     return hipGetLastError();
 }
 
-hipError_t launch_finalize_grad(const uint32_t* rbits, int64_t C, const QuantCfg& cfg, uint8_t* group,
-                                sq_scale* scale, int32_t* layout, hipStream_t s) {
-    hipLaunchKernelGGL(k_finalize_grad, dim3(1), dim3(1024), 0, s, rbits, C, cfg, group, scale, layout);
+hipError_t launch_finalize_grad(const uint32_t* partial, int64_t slabs, int64_t C, const QuantCfg& cfg,
+                                uint32_t* rbits, uint8_t* group, sq_scale* scale, int32_t* layout, hipStream_t s) {
+    hipLaunchKernelGGL(k_finalize_grad, dim3(1), dim3(kFinThreads), 0, s, partial, slabs, C, cfg, rbits, group,
+                       scale, layout);
     return hipGetLastError();
 }
 
-hipError_t launch_finalize_tensor(const uint32_t* rbits, int64_t C, int Q, sq_scale* scale, hipStream_t s) {
-    hipLaunchKernelGGL(k_finalize_tensor, dim3(1), dim3(1024), 0, s, rbits, C, Q, scale);
+hipError_t launch_finalize_tensor(const uint32_t* partial, int64_t slabs, int64_t C, int Q, sq_scale* scale,
+                                  hipStream_t s) {
+    hipLaunchKernelGGL(k_finalize_tensor, dim3(1), dim3(kFinThreads), 0, s, partial, slabs, C, Q, scale);
     return hipGetLastError();
 }
 

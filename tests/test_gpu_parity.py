@@ -360,7 +360,7 @@ def test_workload_full_size(sq, name):
 
     rng = np.random.default_rng(0)
     n_d = 24 if C_out * C_in > 1e7 else 96
-    rows_d = np.unique(np.r_[0, M - 1, M - 2, (M // 128) * 128, rng.integers(0, M, n_d)])
+    rows_d = np.unique(np.r_[0, M - 1, M - 2, min(M - 1, (M // 128) * 128), rng.integers(0, M, n_d)])
     outliers = np.nonzero(g_ref < wl.num_groups - 1)[0]
     rows_w = np.unique(np.r_[0, C_out - 1, outliers[:8], rng.integers(0, C_out, 8)])
     A_ref = oracle.dgrad(q_ref, g_ref, wl.num_groups, wq_ref, rows_d)
