@@ -119,26 +119,33 @@ def main(argv=None):
     torch.cuda.synchronize()
 
     K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    # Timed region: K whole steps on one stream, bracketed by two events only
+    # (an event recorded between kernels costs a bubble of several us).
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
-    for k in range(K):
-        e = ev[k]
-        e[0].record(stream)
-        plan.quantize(dY, stream)
-        e[1].record(stream)
-        plan.dgrad(wq_t, ws, stream)
-        e[2].record(stream)
-        plan.wgrad(xq_t, xs, stream)
-        e[3].record(stream)
+    for _ in range(K):
+        plan.run(dY, wq_t, ws, xq_t, xs, stream)
     stop.record(stream)
     torch.cuda.synchronize()
-    total_ms = start.elapsed_time(stop)
-    t_quant = sum(e[0].elapsed_time(e[1]) for e in ev) / K
-    t_dgrad = sum(e[1].elapsed_time(e[2]) for e in ev) / K
-    t_wgrad = sum(e[2].elapsed_time(e[3]) for e in ev) / K
-    ms_step = total_ms / K
+    ms_step = start.elapsed_time(stop) / K
+
+    # Per-call averages: each call launched K times back to back between two
+    # events on the same stream (the kernels of the dominant call are what the
+    # roofline entry reports).
+    def per_call(fn):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(K):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / K
+
+    t_quant = per_call(lambda: plan.quantize(dY, stream))
+    t_dgrad = per_call(lambda: plan.dgrad(wq_t, ws, stream))
+    t_wgrad = per_call(lambda: plan.wgrad(xq_t, xs, stream))
     ops = 4 * M * C_out * C_in
     value = ops / (ms_step * 1e-3) / 1e12
 

@@ -33,11 +33,9 @@ struct U4 { uint32_t x, y, z, w; };
 __device__ __forceinline__ U4 philox4x32_10(U4 c, uint32_t k0, uint32_t k1) {
 #pragma unroll
     for (int r = 0; r < 10; ++r) {
-        const uint32_t lo0 = 0xD2511F53u * c.x;
-        const uint32_t hi0 = __umulhi(0xD2511F53u, c.x);
-        const uint32_t lo1 = 0xCD9E8D57u * c.z;
-        const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z);
-        c = U4{hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0};
+        const uint64_t p0 = (uint64_t)0xD2511F53u * c.x;   // one 32x32->64 product each
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.z;
+        c = U4{(uint32_t)(p1 >> 32) ^ c.y ^ k0, (uint32_t)p1, (uint32_t)(p0 >> 32) ^ c.w ^ k1, (uint32_t)p0};
         k0 += 0x9E3779B9u;
         k1 += 0xBB67AE85u;
     }
@@ -228,22 +226,58 @@ __global__ __launch_bounds__(kFinThreads) void k_finalize_grad(const uint32_t* _
 
     // channel ranges and r_max
     uint32_t rr[kFinRegs];
-    uint32_t mb = 0u;
 #pragma unroll
-    for (int k = 0; k < kFinRegs; ++k) {
-        const int64_t c = tid + (int64_t)k * kFinThreads;
-        uint32_t r = 0u;
-        if (c < C) {
-            r = reduce_slabs(partial, S, C, c);
-            rbits[c] = r;
+    for (int k = 0; k < kFinRegs; ++k) rr[k] = 0u;
+    uint32_t mb = 0u;
+    if (C < kFinThreads) {
+        // few channels, many slabs: W channels x L slab lanes, then combine
+        // the lanes through LDS
+        __shared__ uint32_t lanes[kFinThreads];
+        int W = 1;
+        while (W < C) W <<= 1;
+        const int L = kFinThreads / W;
+        const int cl = tid % W, lane = tid / W;
+        uint32_t a[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+        if (cl < C) {
+            int64_t sl = lane;
+            for (; sl + 7 * (int64_t)L < S; sl += 8 * (int64_t)L) {
+#pragma unroll
+                for (int u = 0; u < 8; ++u) a[u] = max(a[u], partial[(sl + u * (int64_t)L) * C + cl]);
+            }
+            for (; sl < S; sl += L) a[0] = max(a[0], partial[sl * C + cl]);
         }
-        rr[k] = r;
-        mb = max(mb, r);
-    }
-    for (int64_t c = tid + (int64_t)kFinRegs * kFinThreads; c < C; c += kFinThreads) {
-        const uint32_t r = reduce_slabs(partial, S, C, c);
-        rbits[c] = r;
-        mb = max(mb, r);
+#pragma unroll
+        for (int u = 1; u < 8; ++u) a[0] = max(a[0], a[u]);
+        lanes[tid] = a[0];
+        __syncthreads();
+        if (tid < C) {
+            uint32_t r = 0u;
+            for (int l = 0; l < L; ++l) r = max(r, lanes[l * W + tid]);
+            rr[0] = r;
+            rbits[tid] = r;
+            mb = r;
+        }
+    } else {
+        // many channels, few slabs: independent loads across the channels a
+        // thread owns
+        for (int64_t sl = 0; sl < S; ++sl) {
+#pragma unroll
+            for (int k = 0; k < kFinRegs; ++k) {
+                const int64_t c = tid + (int64_t)k * kFinThreads;
+                if (c < C) rr[k] = max(rr[k], partial[sl * C + c]);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < kFinRegs; ++k) {
+            const int64_t c = tid + (int64_t)k * kFinThreads;
+            if (c < C) rbits[c] = rr[k];
+            mb = max(mb, rr[k]);
+        }
+        for (int64_t c = tid + (int64_t)kFinRegs * kFinThreads; c < C; c += kFinThreads) {
+            const uint32_t r = reduce_slabs(partial, S, C, c);
+            rbits[c] = r;
+            mb = max(mb, r);
+        }
     }
     mb = block_max_u32(mb, shu);
     const float r_max = __uint_as_float(mb);
