@@ -215,7 +215,8 @@ sq_status sq_quantize_tensor(const float* T, int64_t rows, int64_t cols, int64_t
     uint32_t* partial = static_cast<uint32_t*>(workspace);
     int64_t slabs = 0;
     SQ_TRY(hip_status(launch_colmax(T, rows, cols, ld, partial, &slabs, s), "colmax"));
-    SQ_TRY(hip_status(launch_finalize_tensor(partial, slabs, cols, cfg.Q, scale, s), "finalize"));
+    SQ_TRY(hip_status(launch_finalize_tensor(partial, slabs, cols, cfg.Q, partial + slabs * cols, scale, s),
+                      "finalize"));
     SQ_TRY(hip_status(launch_quantize(T, rows, cols, ld, nullptr, scale, cfg, transpose ? nullptr : q, ld_q,
                                       transpose ? q : nullptr, ld_q, nullptr, s),
                       "quantize"));

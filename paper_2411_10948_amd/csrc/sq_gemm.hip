@@ -1,15 +1,16 @@
 // Integer GEMMs of the ShiftQuant backward pass for gfx950.
 //
-// One kernel serves both products as C[i, j] = sum_k A[i, k] * B[j, k] with
-// both operands K-contiguous int8:
+// One kernel template serves both products as C[i, j] = sum_k A[i, k] * B[j, k]
+// with both operands K-contiguous int8:
 //   dgrad: A = shift-folded gradient codes [M, C_out(+appended)],
 //          B = W^T codes [C_in, C_out]              -> dX [M, C_in]
 //   wgrad: A = transposed gradient codes [C_out, M],
 //          B = X^T codes [C_in, M]                   -> dW [C_out, C_in]
-// int32 accumulation on the matrix cores (v_mfma_i32_32x32x32_i8, 32x32
-// outputs, K = 32 per instruction), 128x128 block tiles of four 64x64 wave
-// tiles, K tiles of 64 bytes double-buffered in LDS.  The dequantization of
-// Eq. "dq_mm_f" is fused into the epilogue.
+// int32 accumulation on the matrix cores (v_mfma_i32_32x32x32_i8 or
+// v_mfma_i32_16x16x64_i8), block tiles of WM x WN waves, K tiles of BK bytes
+// double-buffered in LDS (rows padded by 16 bytes, which keeps the 16-byte
+// fragment reads free of bank conflicts), and the dequantization of
+// Eq. "dq_mm_f" fused into the epilogue.
 //
 // ShiftMM (Sec. 3.2) shifts every product by the shift of its inner index
 // before accumulation.  The shifts that fit int8 are folded into the
@@ -25,12 +26,33 @@ namespace sq {
 
 namespace {
 
-constexpr int BM = 128, BN = 128, BK = 64;
-constexpr int LS = BK + 16;   // LDS row stride in bytes: conflict-free 16-byte reads
-constexpr int kThreads = 256;
-
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
+
+// Tile configuration: BM x BN outputs per block, WM x WN waves, BK bytes of
+// K per LDS stage, MF = 32 (32x32x32 MFMA) or 16 (16x16x64 MFMA).
+template <int BM_, int BN_, int BK_, int WM_, int WN_, int MF_>
+struct TileCfg {
+    static constexpr int BM = BM_, BN = BN_, BK = BK_, WM = WM_, WN = WN_, MF = MF_;
+    static constexpr int kThreads = 64 * WM * WN;
+    static constexpr int TM = BM / WM, TN = BN / WN;      // wave tile
+    static constexpr int FM = TM / MF, FN = TN / MF;      // MFMA blocks per wave
+    static constexpr int KS = MF == 32 ? 32 : 64;         // K bytes per MFMA
+    static constexpr int NACC = MF == 32 ? 16 : 4;        // int32 results per lane per MFMA
+    static constexpr int LS = BK + 16;                    // LDS row stride in bytes
+    static constexpr int CPR = BK / 16;                   // 16-byte chunks per row
+    static constexpr int LA = BM * CPR / kThreads;        // chunks per thread per stage
+    static constexpr int LB = BN * CPR / kThreads;
+    static constexpr int kSmem = 2 * (BM + BN) * LS;
+    static_assert(MF == 32 || MF == 16, "MFMA shape");
+    static_assert(TM % MF == 0 && TN % MF == 0, "wave tile must hold whole MFMA blocks");
+    static_assert(BK % KS == 0, "K tile must hold whole MFMA steps");
+    static_assert(LA * kThreads == BM * CPR && LB * kThreads == BN * CPR, "even load split");
+};
+
+// The configurations the library launches.
+using CfgSmall = TileCfg<128, 128, 64, 2, 2, 32>;   // small/skinny outputs, split-K
+using CfgLarge = TileCfg<256, 256, 64, 4, 2, 16>;   // large products (matrix-core bound)
 
 // Zero the bytes of a 16-byte chunk at positions >= nvalid (0 < nvalid < 16).
 __device__ __forceinline__ uint4 mask_tail(uint4 v, int nvalid) {
@@ -44,14 +66,52 @@ __device__ __forceinline__ uint4 mask_tail(uint4 v, int nvalid) {
     return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-__global__ __launch_bounds__(kThreads, 2) void k_gemm_i8(GemmArgs p, int tiles_n, int64_t k_per_split) {
-    __shared__ __attribute__((aligned(16))) int8_t sA[2][BM * LS];
-    __shared__ __attribute__((aligned(16))) int8_t sB[2][BN * LS];
+// Blocks are dispatched to the 8 XCDs of the chip round-robin.  Give each XCD
+// a contiguous range of tiles, then walk that range in groups of kGroupM tile
+// rows so neighbouring blocks share operand panels in their XCD's L2.
+constexpr int64_t kXcds = 8, kGroupM = 8;
+
+__device__ __forceinline__ void tile_coords(int64_t b, int64_t tiles_m, int64_t tiles_n, int64_t& tm, int64_t& tn) {
+    const int64_t nt = tiles_m * tiles_n;
+    const int64_t x = b % kXcds, i = b / kXcds, q = nt / kXcds, r = nt % kXcds;
+    const int64_t t = x * q + min(x, r) + i;
+    const int64_t per_group = kGroupM * tiles_n;
+    const int64_t first_m = (t / per_group) * kGroupM;
+    const int64_t gsz = min(tiles_m - first_m, kGroupM);
+    const int64_t w = t % per_group;
+    tm = first_m + w % gsz;
+    tn = w / gsz;
+}
+
+template <int MF>
+struct Mfma;
+template <>
+struct Mfma<32> {
+    typedef v16i acc_t;
+    static __device__ __forceinline__ acc_t run(v4i a, v4i b, acc_t c) {
+        return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
+    }
+};
+template <>
+struct Mfma<16> {
+    typedef v4i acc_t;
+    static __device__ __forceinline__ acc_t run(v4i a, v4i b, acc_t c) {
+        return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+    }
+};
+
+template <class T>
+__global__ __launch_bounds__(T::kThreads) void k_gemm(GemmArgs p, int64_t tiles_m, int64_t tiles_n,
+                                                      int64_t k_per_split) {
+    __shared__ __attribute__((aligned(16))) int8_t smem[T::kSmem];
+    using MF = Mfma<T::MF>;
+    using acc_t = typename MF::acc_t;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-    const int64_t tile = blockIdx.x;
-    const int64_t m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
+    const int wm = wave / T::WN, wn = wave % T::WN;
+    int64_t tm, tn;
+    tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
+    const int64_t m0 = tm * T::BM, n0 = tn * T::BN;
 
     // K tiles: appended regions first (dgrad fold), then this split's slice
     // of the main segment.
@@ -59,81 +119,94 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm_i8(GemmArgs p, int tiles_n
     const int32_t* rstart = nullptr;
     if (p.extA) {
         E = p.layout[0];
-        n_ext = p.layout[1] / BK;
+        n_ext = p.layout[1] / T::BK;
         rstart = p.layout + 4;
     }
     const int64_t kbeg = (int64_t)blockIdx.y * k_per_split;
     const int64_t kend = min(p.K, kbeg + k_per_split);
-    const int n_main = kend > kbeg ? (int)((kend - kbeg + BK - 1) / BK) : 0;
+    const int n_main = kend > kbeg ? (int)((kend - kbeg + T::BK - 1) / T::BK) : 0;
     const int n_tiles = n_ext + n_main;
 
-    v16i acc[2][2];
+    acc_t acc[T::FM][T::FN];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < T::FM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < T::FN; ++j)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
+            for (int r = 0; r < T::NACC; ++r) acc[i][j][r] = 0;
 
-    uint4 ra[2], rb[2];
+    uint4 ra[T::LA], rb[T::LB];
 
     auto load = [&](int t) {
         const int8_t *Ab, *Bb;
         int64_t la, lb, k0, klim;
         if (t < n_ext) {
             Ab = p.extA; la = p.ld_extA; Bb = p.extB; lb = p.ld_extB;
-            k0 = (int64_t)t * BK; klim = (int64_t)n_ext * BK;
+            k0 = (int64_t)t * T::BK; klim = (int64_t)n_ext * T::BK;
         } else {
             Ab = p.A; la = p.lda; Bb = p.B; lb = p.ldb;
-            k0 = kbeg + (int64_t)(t - n_ext) * BK; klim = kend;
+            k0 = kbeg + (int64_t)(t - n_ext) * T::BK; klim = kend;
         }
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int id = tid + i * kThreads;
-            const int row = id >> 2, c16 = (id & 3) * 16;
-            const int64_t kk = k0 + c16;
-            uint4 va = make_uint4(0u, 0u, 0u, 0u), vb = make_uint4(0u, 0u, 0u, 0u);
-            if (kk < klim) {
-                const int64_t gm = m0 + row, gn = n0 + row;
-                if (gm < p.Mg) va = *reinterpret_cast<const uint4*>(Ab + gm * la + kk);
-                if (gn < p.Ng) vb = *reinterpret_cast<const uint4*>(Bb + gn * lb + kk);
-                if (kk + 16 > klim) {
-                    va = mask_tail(va, (int)(klim - kk));
-                    vb = mask_tail(vb, (int)(klim - kk));
-                }
+        for (int i = 0; i < T::LA; ++i) {
+            const int id = tid + i * T::kThreads;
+            const int row = id / T::CPR, c16 = (id % T::CPR) * 16;
+            const int64_t kk = k0 + c16, gm = m0 + row;
+            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            if (kk < klim && gm < p.Mg) {
+                v = *reinterpret_cast<const uint4*>(Ab + gm * la + kk);
+                if (kk + 16 > klim) v = mask_tail(v, (int)(klim - kk));
             }
-            ra[i] = va;
-            rb[i] = vb;
+            ra[i] = v;
+        }
+#pragma unroll
+        for (int i = 0; i < T::LB; ++i) {
+            const int id = tid + i * T::kThreads;
+            const int row = id / T::CPR, c16 = (id % T::CPR) * 16;
+            const int64_t kk = k0 + c16, gn = n0 + row;
+            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            if (kk < klim && gn < p.Ng) {
+                v = *reinterpret_cast<const uint4*>(Bb + gn * lb + kk);
+                if (kk + 16 > klim) v = mask_tail(v, (int)(klim - kk));
+            }
+            rb[i] = v;
         }
     };
     auto store = [&](int buf) {
+        int8_t* sA = smem + buf * (T::BM + T::BN) * T::LS;
+        int8_t* sB = sA + T::BM * T::LS;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int id = tid + i * kThreads;
-            const int row = id >> 2, c16 = (id & 3) * 16;
-            *reinterpret_cast<uint4*>(&sA[buf][row * LS + c16]) = ra[i];
-            *reinterpret_cast<uint4*>(&sB[buf][row * LS + c16]) = rb[i];
+        for (int i = 0; i < T::LA; ++i) {
+            const int id = tid + i * T::kThreads;
+            *reinterpret_cast<uint4*>(&sA[(id / T::CPR) * T::LS + (id % T::CPR) * 16]) = ra[i];
+        }
+#pragma unroll
+        for (int i = 0; i < T::LB; ++i) {
+            const int id = tid + i * T::kThreads;
+            *reinterpret_cast<uint4*>(&sB[(id / T::CPR) * T::LS + (id % T::CPR) * 16]) = rb[i];
         }
     };
     auto compute = [&](int buf) {
+        const int8_t* sA = smem + buf * (T::BM + T::BN) * T::LS;
+        const int8_t* sB = sA + T::BM * T::LS;
+        const int lrow = lane % T::MF, lk = (lane / T::MF) * 16;
 #pragma unroll
-        for (int ks = 0; ks < BK / 32; ++ks) {
-            v4i a[2], b[2];
-            const int kb = ks * 32 + (lane >> 5) * 16;
+        for (int ks = 0; ks < T::BK / T::KS; ++ks) {
+            v4i a[T::FM], b[T::FN];
 #pragma unroll
-            for (int wi = 0; wi < 2; ++wi)
-                a[wi] = *reinterpret_cast<const v4i*>(&sA[buf][(wm * 64 + wi * 32 + (lane & 31)) * LS + kb]);
+            for (int i = 0; i < T::FM; ++i)
+                a[i] = *reinterpret_cast<const v4i*>(
+                    &sA[(wm * T::TM + i * T::MF + lrow) * T::LS + ks * T::KS + lk]);
 #pragma unroll
-            for (int wj = 0; wj < 2; ++wj)
-                b[wj] = *reinterpret_cast<const v4i*>(&sB[buf][(wn * 64 + wj * 32 + (lane & 31)) * LS + kb]);
+            for (int j = 0; j < T::FN; ++j)
+                b[j] = *reinterpret_cast<const v4i*>(
+                    &sB[(wn * T::TN + j * T::MF + lrow) * T::LS + ks * T::KS + lk]);
             // The B tile feeds the matrix-core A operand, so each lane's
-            // results run along the output row (4 consecutive columns per
-            // register quartet).
+            // results run along an output row (4 consecutive columns).
 #pragma unroll
-            for (int wi = 0; wi < 2; ++wi)
+            for (int i = 0; i < T::FM; ++i)
 #pragma unroll
-                for (int wj = 0; wj < 2; ++wj)
-                    acc[wi][wj] = __builtin_amdgcn_mfma_i32_32x32x32_i8(b[wj], a[wi], acc[wi][wj], 0, 0, 0);
+                for (int j = 0; j < T::FN; ++j) acc[i][j] = MF::run(b[j], a[i], acc[i][j]);
         }
     };
 
@@ -144,12 +217,12 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm_i8(GemmArgs p, int tiles_n
         int next_region = 0;
         for (int t = 0; t < n_tiles; ++t) {
             if (t + 1 < n_tiles) load(t + 1);
-            if (next_region < E && t < n_ext && (int64_t)t * BK == rstart[next_region]) {
+            if (next_region < E && t < n_ext && (int64_t)t * T::BK == rstart[next_region]) {
                 // Horner step: the accumulated regions weigh twice the next one
 #pragma unroll
-                for (int i = 0; i < 2; ++i)
+                for (int i = 0; i < T::FM; ++i)
 #pragma unroll
-                    for (int j = 0; j < 2; ++j) acc[i][j] = acc[i][j] + acc[i][j];
+                    for (int j = 0; j < T::FN; ++j) acc[i][j] = acc[i][j] + acc[i][j];
                 ++next_region;
             }
             compute(t & 1);
@@ -168,24 +241,265 @@ __global__ __launch_bounds__(kThreads, 2) void k_gemm_i8(GemmArgs p, int tiles_n
     const bool vec_acc = p.acc && ((p.ld_acc & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.acc) & 15) == 0);
     const bool vec_out = p.out && ((p.ld_out & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.out) & 15) == 0);
     const bool vec_part = p.part && ((p.Ng & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.part) & 15) == 0);
+    constexpr int kQuads = T::NACC / 4;   // groups of 4 consecutive columns per lane and MFMA block
 #pragma unroll
-    for (int wi = 0; wi < 2; ++wi) {
-        const int64_t ii = m0 + wm * 64 + wi * 32 + (lane & 31);
+    for (int i = 0; i < T::FM; ++i) {
+        const int64_t ii = m0 + wm * T::TM + i * T::MF + lane % T::MF;
         if (ii >= p.Mg) continue;
         float sc = alpha;
-        if (p.out && p.epi_mode == 1) sc = __fmul_rn(base, pow2f(-(int)p.group[ii]));
+        if (p.out && !p.part && p.epi_mode == 1) sc = __fmul_rn(base, pow2f(-(int)p.group[ii]));
 #pragma unroll
-        for (int wj = 0; wj < 2; ++wj) {
+        for (int j = 0; j < T::FN; ++j) {
 #pragma unroll
-            for (int a4 = 0; a4 < 4; ++a4) {
-                const int64_t jj = n0 + wn * 64 + wj * 32 + a4 * 8 + (lane >> 5) * 4;
+            for (int q = 0; q < kQuads; ++q) {
+                // 32x32: register quartet q covers columns 8q + 4 * (lane / 32) + 0..3
+                // 16x16: columns 4 * (lane / 16) + 0..3
+                const int64_t jj = n0 + wn * T::TN + j * T::MF +
+                                   (T::MF == 32 ? q * 8 + (lane / 32) * 4 : (lane / 16) * 4);
                 if (jj >= p.Ng) continue;
-                const int v0 = acc[wi][wj][a4 * 4 + 0], v1 = acc[wi][wj][a4 * 4 + 1];
-                const int v2 = acc[wi][wj][a4 * 4 + 2], v3 = acc[wi][wj][a4 * 4 + 3];
+                const int v0 = acc[i][j][q * 4 + 0], v1 = acc[i][j][q * 4 + 1];
+                const int v2 = acc[i][j][q * 4 + 2], v3 = acc[i][j][q * 4 + 3];
                 const int vv[4] = {v0, v1, v2, v3};
                 const bool full = jj + 4 <= p.Ng;
                 if (p.part) {
                     // split-K: this split's partial tile, dense [splits, Mg, Ng]
+                    int32_t* dst = p.part + (int64_t)blockIdx.y * p.Mg * p.Ng + ii * p.Ng + jj;
+                    if (vec_part && full) {
+                        *reinterpret_cast<int4*>(dst) = make_int4(v0, v1, v2, v3);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (jj + e < p.Ng) dst[e] = vv[e];
+                    }
+                    continue;
+                }
+                if (p.acc) {
+                    int32_t* dst = p.acc + ii * p.ld_acc + jj;
+                    if (vec_acc && full) {
+                        *reinterpret_cast<int4*>(dst) = make_int4(v0, v1, v2, v3);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (jj + e < p.Ng) dst[e] = vv[e];
+                    }
+                }
+                if (p.out) {
+                    float* dst = p.out + ii * p.ld_out + jj;
+                    const float f0 = __fmul_rn((float)v0, sc), f1 = __fmul_rn((float)v1, sc);
+                    const float f2 = __fmul_rn((float)v2, sc), f3 = __fmul_rn((float)v3, sc);
+                    if (vec_out && full) {
+                        *reinterpret_cast<float4*>(dst) = make_float4(f0, f1, f2, f3);
+                    } else {
+                        const float ff[4] = {f0, f1, f2, f3};
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (jj + e < p.Ng) dst[e] = ff[e];
+                    }
+                }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Pipelined variant for K-aligned operands: 64-byte K tiles move from global
+// memory straight into a ring of STAGES LDS buffers with the gfx950 direct
+// loads (global_load_lds_dwordx4, 16 bytes per lane), so STAGES - 1 tiles are
+// in flight without holding registers.  Each wave instruction fills 1 KB of
+// LDS = 16 rows x 64 bytes in lane order; the 16-byte chunk c of row r is
+// stored at chunk c ^ swz(r), which keeps the fragment reads conflict-free.
+// Synchronisation is explicit: a wave waits (vmcnt) for its own loads of
+// tile t, a barrier publishes them to the block, and a stage is refilled only
+// after the barrier that follows every wave's reads of it.
+// Requirements (checked by the launcher): every K segment a multiple of 64,
+// lda/ldb multiples of 16, 16-byte aligned operands.
+// ---------------------------------------------------------------------------
+template <int BM_, int BN_, int WM_, int WN_, int MF_, int STAGES_>
+struct PipeCfg {
+    static constexpr int BM = BM_, BN = BN_, BK = 64, WM = WM_, WN = WN_, MF = MF_, STAGES = STAGES_;
+    static constexpr int kThreads = 64 * WM * WN, kWaves = WM * WN;
+    static constexpr int TM = BM / WM, TN = BN / WN;
+    static constexpr int FM = TM / MF, FN = TN / MF;
+    static constexpr int KS = MF == 32 ? 32 : 64;
+    static constexpr int NACC = MF == 32 ? 16 : 4;
+    static constexpr int kStage = (BM + BN) * BK;         // bytes per stage
+    static constexpr int IA = BM / 16 / kWaves;           // A load instructions per wave per stage
+    static constexpr int IB = BN / 16 / kWaves;
+    static constexpr int kLoads = IA + IB;
+    static constexpr int kSmem = STAGES * kStage;
+    static_assert(IA * 16 * kWaves == BM && IB * 16 * kWaves == BN, "rows split evenly over waves");
+    static_assert(TM % MF == 0 && TN % MF == 0, "wave tile must hold whole MFMA blocks");
+    static_assert(STAGES >= 2 && (STAGES - 2) * kLoads <= 63, "vmcnt range");
+};
+
+using PipeLarge = PipeCfg<256, 256, 4, 2, 16, 4>;   // 128 KB of LDS, one block per CU
+using PipeSmall = PipeCfg<128, 128, 2, 2, 16, 4>;   // 64 KB of LDS
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef const __attribute__((address_space(1))) void gbl_void_t;
+
+// chunk swizzle of a 64-byte LDS row (conflict-free for 8- and 16-lane phases)
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 2)) & 3; }
+
+// s_waitcnt vmcnt(n) leaving the other counters unconstrained (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0x7F | (0x3 << 14) | (0x0 << 8)); }
+
+template <class T>
+__global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t tiles_m, int64_t tiles_n,
+                                                           int64_t k_per_split) {
+    __shared__ __attribute__((aligned(1024))) int8_t smem[T::kSmem];
+    using MF = Mfma<T::MF>;
+    using acc_t = typename MF::acc_t;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / T::WN, wn = wave % T::WN;
+    int64_t tm, tn;
+    tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
+    const int64_t m0 = tm * T::BM, n0 = tn * T::BN;
+
+    int n_ext = 0, E = 0;
+    const int32_t* rstart = nullptr;
+    if (p.extA) {
+        E = p.layout[0];
+        n_ext = p.layout[1] / T::BK;
+        rstart = p.layout + 4;
+    }
+    const int64_t kbeg = (int64_t)blockIdx.y * k_per_split;
+    const int64_t kend = min(p.K, kbeg + k_per_split);
+    const int n_main = kend > kbeg ? (int)((kend - kbeg) / T::BK) : 0;
+    const int n_tiles = n_ext + n_main;
+
+    // Per-lane source rows and chunk offsets of this wave's load
+    // instructions: row r of the instruction's 16, logical chunk
+    // (lane % 4) ^ swz(r).  Rows past the end of an operand read its last row
+    // (their results are never stored).  Both K segments share them.
+    int64_t rowA[T::IA], rowB[T::IB];
+    int chA[T::IA], chB[T::IB];
+    const int lr = lane >> 2;
+#pragma unroll
+    for (int i = 0; i < T::IA; ++i) {
+        const int r = (i * T::kWaves + wave) * 16 + lr;
+        rowA[i] = min(m0 + r, p.Mg - 1);
+        chA[i] = 16 * ((lane & 3) ^ swz(r));
+    }
+#pragma unroll
+    for (int i = 0; i < T::IB; ++i) {
+        const int r = (i * T::kWaves + wave) * 16 + lr;
+        rowB[i] = min(n0 + r, p.Ng - 1);
+        chB[i] = 16 * ((lane & 3) ^ swz(r));
+    }
+
+    auto issue = [&](int t) {
+        int8_t* st = smem + (t % T::STAGES) * T::kStage;
+        const bool ext = t < n_ext;
+        const int8_t* Ab = ext ? p.extA : p.A;
+        const int8_t* Bb = ext ? p.extB : p.B;
+        const int64_t la = ext ? p.ld_extA : p.lda, lb = ext ? p.ld_extB : p.ldb;
+        const int64_t k0 = ext ? (int64_t)t * T::BK : kbeg + (int64_t)(t - n_ext) * T::BK;
+#pragma unroll
+        for (int i = 0; i < T::IA; ++i)
+            __builtin_amdgcn_global_load_lds((gbl_void_t*)(Ab + rowA[i] * la + chA[i] + k0),
+                                             (lds_void_t*)(st + (i * T::kWaves + wave) * 1024), 16, 0, 0);
+#pragma unroll
+        for (int i = 0; i < T::IB; ++i)
+            __builtin_amdgcn_global_load_lds((gbl_void_t*)(Bb + rowB[i] * lb + chB[i] + k0),
+                                             (lds_void_t*)(st + T::BM * T::BK + (i * T::kWaves + wave) * 1024),
+                                             16, 0, 0);
+    };
+
+    acc_t acc[T::FM][T::FN];
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+            for (int r = 0; r < T::NACC; ++r) acc[i][j][r] = 0;
+
+    auto compute = [&](int t) {
+        const int8_t* sA = smem + (t % T::STAGES) * T::kStage;
+        const int8_t* sB = sA + T::BM * T::BK;
+        const int lrow = lane % T::MF, lc = lane / T::MF;
+#pragma unroll
+        for (int ks = 0; ks < T::BK / T::KS; ++ks) {
+            const int c = ks * (T::KS / 16) + lc;   // logical 16-byte chunk of this lane
+            v4i a[T::FM], b[T::FN];
+#pragma unroll
+            for (int i = 0; i < T::FM; ++i) {
+                const int r = wm * T::TM + i * T::MF + lrow;
+                a[i] = *reinterpret_cast<const v4i*>(&sA[r * T::BK + 16 * (c ^ swz(r))]);
+            }
+#pragma unroll
+            for (int j = 0; j < T::FN; ++j) {
+                const int r = wn * T::TN + j * T::MF + lrow;
+                b[j] = *reinterpret_cast<const v4i*>(&sB[r * T::BK + 16 * (c ^ swz(r))]);
+            }
+#pragma unroll
+            for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+                for (int j = 0; j < T::FN; ++j) acc[i][j] = MF::run(b[j], a[i], acc[i][j]);
+        }
+    };
+
+    if (n_tiles > 0) {
+#pragma unroll
+        for (int s = 0; s < T::STAGES - 1; ++s)
+            if (s < n_tiles) issue(s);
+        int next_region = 0;
+        for (int t = 0; t < n_tiles; ++t) {
+            // this wave's loads of tile t are done once at most
+            // min(STAGES - 2, n_tiles - 1 - t) later tiles remain in flight
+            const int later = min(T::STAGES - 2, n_tiles - 1 - t);
+            if (later >= T::STAGES - 2) wait_vm<(T::STAGES - 2) * T::kLoads>();
+            else if (later == 1) wait_vm<T::kLoads>();
+            else wait_vm<0>();
+            __builtin_amdgcn_s_barrier();   // tile t is in LDS for every wave; stage (t-1) is free
+            if (t + T::STAGES - 1 < n_tiles) issue(t + T::STAGES - 1);
+            if (next_region < E && t < n_ext && (int64_t)t * T::BK == rstart[next_region]) {
+                // Horner step: the accumulated regions weigh twice the next one
+#pragma unroll
+                for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < T::FN; ++j) acc[i][j] = acc[i][j] + acc[i][j];
+                ++next_region;
+            }
+            compute(t);
+            wait_lgkm0();   // every LDS read of this stage has returned before the next barrier
+        }
+    }
+
+    // ---- epilogue (same as the register-staged kernel) ----
+    float base = 0.0f, alpha = 0.0f;
+    if (p.out && !p.part) {
+        const sq_scale gs = *p.gs, os = *p.os;
+        base = __fmul_rn(gs.step, os.step);
+        alpha = __fmul_rn(base, pow2f(-(p.num_groups - 1)));
+    }
+    const bool vec_acc = p.acc && ((p.ld_acc & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.acc) & 15) == 0);
+    const bool vec_out = p.out && ((p.ld_out & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.out) & 15) == 0);
+    const bool vec_part = p.part && ((p.Ng & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.part) & 15) == 0);
+    constexpr int kQuads = T::NACC / 4;
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i) {
+        const int64_t ii = m0 + wm * T::TM + i * T::MF + lane % T::MF;
+        if (ii >= p.Mg) continue;
+        float sc = alpha;
+        if (p.out && !p.part && p.epi_mode == 1) sc = __fmul_rn(base, pow2f(-(int)p.group[ii]));
+#pragma unroll
+        for (int j = 0; j < T::FN; ++j) {
+#pragma unroll
+            for (int q = 0; q < kQuads; ++q) {
+                const int64_t jj = n0 + wn * T::TN + j * T::MF +
+                                   (T::MF == 32 ? q * 8 + (lane / 32) * 4 : (lane / 16) * 4);
+                if (jj >= p.Ng) continue;
+                const int v0 = acc[i][j][q * 4 + 0], v1 = acc[i][j][q * 4 + 1];
+                const int v2 = acc[i][j][q * 4 + 2], v3 = acc[i][j][q * 4 + 3];
+                const int vv[4] = {v0, v1, v2, v3};
+                const bool full = jj + 4 <= p.Ng;
+                if (p.part) {
                     int32_t* dst = p.part + (int64_t)blockIdx.y * p.Mg * p.Ng + ii * p.Ng + jj;
                     if (vec_part && full) {
                         *reinterpret_cast<int4*>(dst) = make_int4(v0, v1, v2, v3);
@@ -308,13 +622,52 @@ __global__ void k_dequant(const int32_t* __restrict__ acc, int64_t rows, int64_t
     }
 }
 
+// Launch one configuration.  k_per_split is a multiple of T::BK.
+template <class T>
+hipError_t launch_cfg(const GemmArgs& a, int splits, int64_t k_per_split, hipStream_t s) {
+    const int64_t tiles_m = (a.Mg + T::BM - 1) / T::BM, tiles_n = (a.Ng + T::BN - 1) / T::BN;
+    if (tiles_m * tiles_n > 0x7FFFFFFF || splits > 65535) return hipErrorInvalidValue;
+    if (a.extA && (kFoldPad % T::BK) != 0) return hipErrorInvalidValue;   // regions must start on K tiles
+    dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)splits);
+    hipLaunchKernelGGL(k_gemm<T>, grid, dim3(T::kThreads), 0, s, a, tiles_m, tiles_n, k_per_split);
+    return hipGetLastError();
+}
+
+template <class T>
+hipError_t launch_pipe(const GemmArgs& a, int splits, int64_t k_per_split, hipStream_t s) {
+    const int64_t tiles_m = (a.Mg + T::BM - 1) / T::BM, tiles_n = (a.Ng + T::BN - 1) / T::BN;
+    if (tiles_m * tiles_n > 0x7FFFFFFF || splits > 65535) return hipErrorInvalidValue;
+    dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)splits);
+    hipLaunchKernelGGL(k_gemm_pipe<T>, grid, dim3(T::kThreads), 0, s, a, tiles_m, tiles_n, k_per_split);
+    return hipGetLastError();
+}
+
+// The direct-load pipeline needs 64-byte K tiles that never cross the end of a
+// segment and 16-byte aligned rows.
+bool pipe_ok(const GemmArgs& a) {
+    auto al16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+    if (a.K % 64 != 0 || a.lda % 16 != 0 || a.ldb % 16 != 0 || !al16(a.A) || !al16(a.B)) return false;
+    if (a.extA && (a.ld_extA % 16 != 0 || a.ld_extB % 16 != 0 || !al16(a.extA) || !al16(a.extB))) return false;
+    return true;
+}
+
+// Large tiles only where the product fills the chip with them.
+bool use_large(const GemmArgs& a) {
+    const int64_t tiles = ((a.Mg + CfgLarge::BM - 1) / CfgLarge::BM) * ((a.Ng + CfgLarge::BN - 1) / CfgLarge::BN);
+    return a.splits <= 1 && a.K >= 1024 && tiles >= 256;
+}
+
 }  // namespace
 
 int wgrad_splits(int64_t M, int64_t C_out, int64_t C_in) {
-    const int64_t tiles = ((C_out + BM - 1) / BM) * ((C_in + BN - 1) / BN);
-    const int64_t ktiles = (M + BK - 1) / BK;
+    using T = CfgSmall;
+    GemmArgs probe{};
+    probe.Mg = C_out; probe.Ng = C_in; probe.K = M; probe.splits = 1;
+    if (use_large(probe)) return 1;
+    const int64_t tiles = ((C_out + T::BM - 1) / T::BM) * ((C_in + T::BN - 1) / T::BN);
+    const int64_t ktiles = (M + T::BK - 1) / T::BK;
     int64_t splits = (512 + tiles - 1) / tiles;
-    splits = min(splits, std::max<int64_t>(1, ktiles / 8));
+    splits = std::min(splits, std::max<int64_t>(1, ktiles / 8));
     splits = std::max<int64_t>(1, std::min<int64_t>(splits, 65535));
     // no empty splits
     const int64_t per = (ktiles + splits - 1) / splits;
@@ -323,17 +676,18 @@ int wgrad_splits(int64_t M, int64_t C_out, int64_t C_in) {
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     if (a.Mg <= 0 || a.Ng <= 0) return hipSuccess;
-    const int64_t tiles_m = (a.Mg + BM - 1) / BM, tiles_n = (a.Ng + BN - 1) / BN;
-    if (tiles_m * tiles_n > 0x7FFFFFFF) return hipErrorInvalidValue;
-    const int64_t ktiles = (a.K + BK - 1) / BK;
+    const bool pipe = pipe_ok(a);
+    if (use_large(a)) {
+        const int64_t ktiles = (a.K + 63) / 64;
+        const int64_t kps = std::max<int64_t>(ktiles, 1) * 64;
+        return pipe ? launch_pipe<PipeLarge>(a, 1, kps, s) : launch_cfg<CfgLarge>(a, 1, kps, s);
+    }
+    using T = CfgSmall;
+    const int64_t ktiles = (a.K + T::BK - 1) / T::BK;
     int splits = std::max(1, a.splits);
     const int64_t per = splits > 1 ? (ktiles + splits - 1) / splits : std::max<int64_t>(ktiles, 1);
-    const int64_t k_per_split = per * BK;
-    if (splits > 1) splits = (int)((ktiles + per - 1) / per);
-    if (splits != std::max(1, a.splits)) return hipErrorInvalidValue;   // wgrad_splits() avoids this
-    dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)splits);
-    hipLaunchKernelGGL(k_gemm_i8, grid, dim3(kThreads), 0, s, a, (int)tiles_n, k_per_split);
-    return hipGetLastError();
+    if (splits > 1 && (ktiles + per - 1) / per != splits) return hipErrorInvalidValue;   // wgrad_splits() avoids this
+    return pipe ? launch_pipe<PipeSmall>(a, splits, per * 64, s) : launch_cfg<T>(a, splits, per * T::BK, s);
 }
 
 hipError_t launch_gather_ext(const int8_t* wq_t, int64_t ld_w, int64_t C_in, const int32_t* layout,

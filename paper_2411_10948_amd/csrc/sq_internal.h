@@ -52,14 +52,15 @@ struct ColmaxPlan {
     int64_t rows_per_slab;
 };
 ColmaxPlan colmax_plan(int64_t M, int64_t C, bool vec);
-// uint32 words of scratch for the slab maxima and the channel ranges
+// uint32 words of scratch: slab maxima, then the channel ranges and the
+// per-block maxima of the second reduction level (rbits = partial + slabs * C)
 int64_t colmax_workspace_words(int64_t M, int64_t C);
 hipError_t launch_colmax(const float* x, int64_t M, int64_t C, int64_t ld, uint32_t* partial, int64_t* slabs,
                          hipStream_t s);
 hipError_t launch_finalize_grad(const uint32_t* partial, int64_t slabs, int64_t C, const QuantCfg& cfg,
                                 uint32_t* rbits, uint8_t* group, sq_scale* scale, int32_t* layout, hipStream_t s);
-hipError_t launch_finalize_tensor(const uint32_t* partial, int64_t slabs, int64_t C, int Q, sq_scale* scale,
-                                  hipStream_t s);
+hipError_t launch_finalize_tensor(const uint32_t* partial, int64_t slabs, int64_t C, int Q, uint32_t* rbits,
+                                  sq_scale* scale, hipStream_t s);
 // group == nullptr: every channel in group 0 with shift 0 (per-tensor mode).
 hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, const uint8_t* group,
                            const sq_scale* scale, const QuantCfg& cfg,
