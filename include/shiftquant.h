@@ -97,7 +97,9 @@ typedef struct {
  *   *layout_bytes : size of the device buffer `layout`
  *   *min_ld_fold  : smallest admissible ld_fold for q_fold (a multiple of 16);
  *                   q_fold rows hold C_out main columns followed, from column
- *                   roundup(C_out, 64), by the appended columns of the fold. */
+ *                   roundup(C_out, 64), by the appended columns of the fold:
+ *                   none when N_G - 1 <= T (see sq_quantize_grad), else at
+ *                   most roundup(C_out, 64) + 64 (N_G - 1). */
 sq_status sq_grad_layout_size(int64_t C_out, const sq_quant_params* p,
                               size_t* layout_bytes, int64_t* min_ld_fold);
 
@@ -128,13 +130,19 @@ sq_status sq_gemm_wgrad_workspace_size(int64_t M, int64_t C_out, int64_t C_in,
  * Inputs : dY [M, ld_dY] fp32 (M >= 0, C_out >= 0, ld_dY >= C_out).
  * Outputs (any of q_fold / q_t may be NULL to skip it):
  *   q_fold [M, ld_fold] int8, the dgrad operand with the shifts of
- *          ShiftMM folded in: column c holds code * 2^t_c with
- *          t_c = min(N_G - 1 - g_c, T), T the largest shift with Q 2^T <= 127.
- *          When some channel needs more than T (b >= 6 at N_G = 4), its
- *          column is appended again after column roundup(C_out, 64), as
- *          described by `layout`; sq_gemm_dgrad adds those columns with
- *          the remaining powers of two.  Columns in [C_out, roundup(C_out,
- *          64)) and beyond the appended ones are left unwritten.
+ *          ShiftMM folded in.  The shifts sh_c = N_G - 1 - g_c are cut into
+ *          windows [B, B + T] of T + 1 values, T the largest shift with
+ *          Q 2^T <= 127, and each channel is stored once, as
+ *          code << (sh_c - B) for its window's base B (this fits int8).  The
+ *          window holding the most channels (lowest B on ties) uses the
+ *          channel's own column c.  Every other non-empty window is a region
+ *          of appended columns from column roundup(C_out, 64): its channels
+ *          in ascending order, padded to a multiple of 64 columns; column c
+ *          of such a channel holds 0.  When N_G - 1 <= T (b <= 5 at N_G = 4)
+ *          there is one window and nothing is appended.  `layout` records
+ *          the windows, and sq_gemm_dgrad applies their bases as left shifts
+ *          of its accumulator.  Columns in [C_out, roundup(C_out, 64)) and
+ *          the padding of appended regions are left unwritten.
  *   q_t    [C_out, ld_t] int8 (ld_t >= M), the codes themselves, transposed:
  *          q_t[c, m] = code(m, c); this is the wgrad operand.
  *   group  [C_out] uint8, g_c.
@@ -177,8 +185,9 @@ sq_status sq_quantize_tensor(const float* T, int64_t rows, int64_t cols, int64_t
  *   dX[n, k]  = fl(float(acc[n, k]) * alpha),
  *   alpha     = fl(fl(gscale.step * wscale.step) * 2^-(N_G - 1)).
  * Sec. 3.2 shifts every product before it is accumulated; here the shift of
- * each inner index c is folded into the int8 operand (q_fold), and shifts
- * beyond int8 range are added through the appended columns of `layout`.
+ * each inner index c is folded into the int8 operand (q_fold) up to its
+ * window's base B, and the bases are applied once per window to the int32
+ * accumulator, which visits the windows in descending B (Horner's rule).
  * Inputs : q_fold, ld_fold, layout, group, gscale from sq_quantize_grad with
  *          the same M, C_out and p; wq_t [C_in, ld_w] int8 = W^T codes
  *          (ld_w >= C_out); wscale its sq_scale.

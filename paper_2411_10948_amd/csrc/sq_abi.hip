@@ -18,14 +18,16 @@ QuantCfg make_cfg(const sq_quant_params& p) {
     int T = 0;
     while (c.Q * (1 << (T + 1)) <= 127) ++T;
     c.T = T;
-    c.E_max = p.num_groups - 1 - T > 0 ? p.num_groups - 1 - T : 0;
     c.round_mode = p.round_mode;
     c.seed = p.seed;
     c.offset = p.offset;
     return c;
 }
 
-int64_t fold_ext_max(int64_t C, const QuantCfg& c) { return (int64_t)c.E_max * round_up(C, kFoldPad); }
+int64_t fold_ext_max(int64_t C, const QuantCfg& c) {
+    if (c.num_groups - 1 <= c.T) return 0;   // one window holds every shift
+    return round_up(C, kFoldPad) + (int64_t)kFoldPad * (c.num_groups - 1);
+}
 
 }  // namespace sq
 
@@ -119,7 +121,7 @@ sq_status sq_grad_layout_size(int64_t C_out, const sq_quant_params* p, size_t* l
     if (!layout_bytes || !min_ld_fold) return fail(SQ_ERR_INVALID_ARGUMENT, "output pointer is NULL");
     const QuantCfg cfg = make_cfg(*p);
     const int64_t ext = fold_ext_max(C_out, cfg);
-    *layout_bytes = (size_t)(kLayoutHeader + ext) * sizeof(int32_t);
+    *layout_bytes = (size_t)fold_layout_words(C_out, cfg) * sizeof(int32_t);
     *min_ld_fold = ext > 0 ? fold_ext_base(C_out) + ext : round_up(C_out > 0 ? C_out : 1, 16);
     return SQ_OK;
 }
@@ -185,9 +187,11 @@ sq_status sq_quantize_grad(const float* dY, int64_t M, int64_t C_out, int64_t ld
     int64_t slabs = 0;
     SQ_TRY(hip_status(launch_colmax(dY, M, C_out, ld_dY, partial, &slabs, s), "colmax"));
     uint32_t* rbits = partial + slabs * C_out;
-    SQ_TRY(hip_status(launch_finalize_grad(partial, slabs, C_out, cfg, rbits, group, scale, layout, s), "finalize"));
+    const int64_t ext_max = fold_ext_max(C_out, cfg);
+    SQ_TRY(hip_status(launch_finalize_grad(partial, slabs, C_out, cfg, rbits, group, scale, layout, ext_max, s),
+                      "finalize"));
     SQ_TRY(hip_status(launch_quantize(dY, M, C_out, ld_dY, group, scale, cfg, q_fold, ld_fold, q_t, ld_t,
-                                      layout, s),
+                                      layout + kLayoutHeader + ext_max, s),
                       "quantize"));
     return SQ_OK;
 }
@@ -259,12 +263,12 @@ sq_status sq_gemm_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* la
     a.A = q_fold; a.lda = ld_fold;
     a.B = wq_t; a.ldb = ld_w;
     a.K = C_out;
+    a.layout = layout;
     if (ext_max > 0) {
         int8_t* wext = static_cast<int8_t*>(workspace);
         SQ_TRY(hip_status(launch_gather_ext(wq_t, ld_w, C_in, layout, wext, ext_max, ext_max, s), "gather"));
         a.extA = q_fold + fold_ext_base(C_out); a.ld_extA = ld_fold;
         a.extB = wext; a.ld_extB = ext_max;
-        a.layout = layout;
     }
     a.splits = 1;
     a.acc = acc; a.ld_acc = ld_acc;

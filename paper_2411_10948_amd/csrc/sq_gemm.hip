@@ -13,11 +13,13 @@
 // Eq. "dq_mm_f" fused into the epilogue.
 //
 // ShiftMM (Sec. 3.2) shifts every product by the shift of its inner index
-// before accumulation.  The shifts that fit int8 are folded into the
-// gradient codes by the quantizer; channels that need more are appended as
-// extra K regions that this kernel visits first, doubling the accumulator at
-// the start of each region (Horner's rule), so the result equals
-// sum_c code * w << (N_G - 1 - g_c) exactly.
+// before accumulation.  The quantizer stores each channel's code already
+// shifted within a window of shifts that fits int8; channels of the windows
+// other than the main one sit in appended K columns.  This kernel visits the
+// windows in descending order and shifts the accumulator left by the
+// difference of window bases at each window start and by the last base at the
+// end (Horner's rule), so the result equals sum_c code * w << (N_G - 1 - g_c)
+// exactly.
 #include <algorithm>
 
 #include "sq_internal.h"
@@ -100,6 +102,46 @@ struct Mfma<16> {
     }
 };
 
+// The dgrad's flat K sequence (fold layout in sq_internal.h): appended
+// columns [0, H), the main segment, appended columns [H, D).  Tile t is
+// appended when it lies outside the main segment's n_main tiles.
+struct FoldView {
+    int n_ext = 0, h_tiles = 0, fshift = 0, bk = 64;
+    __device__ bool is_ext(int t, int n_main) const { return t < h_tiles || t >= h_tiles + n_main; }
+    __device__ int64_t ext_col(int t, int n_main) const { return (int64_t)(t < h_tiles ? t : t - n_main) * bk; }
+};
+
+__device__ __forceinline__ FoldView fold_view(const GemmArgs& p, int bk) {
+    FoldView v;
+    v.bk = bk;
+    if (p.layout) {
+        v.n_ext = p.extA ? p.layout[kLayD] / bk : 0;
+        v.h_tiles = p.layout[kLayH] / bk;
+        v.fshift = p.layout[kLayF];
+    }
+    return v;
+}
+
+// Region starts of the flat K sequence, in order; at each one the
+// accumulator is shifted left by the base difference to the region before
+// (Horner's rule).  col is the flat K column of the next start.
+struct HornerSteps {
+    int next = 1, nr = 1;
+    int64_t col = INT64_MAX;
+    __device__ explicit HornerSteps(const GemmArgs& p) {
+        if (p.layout) {
+            nr = p.layout[kLayNR];
+            if (nr > 1) col = p.layout[kLayStart + 1];
+        }
+    }
+    __device__ int advance(const GemmArgs& p) {
+        const int sft = p.layout[kLayShift + next];
+        ++next;
+        col = next < nr ? p.layout[kLayStart + next] : INT64_MAX;
+        return sft;
+    }
+};
+
 template <class T>
 __global__ __launch_bounds__(T::kThreads) void k_gemm(GemmArgs p, int64_t tiles_m, int64_t tiles_n,
                                                       int64_t k_per_split) {
@@ -113,19 +155,13 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm(GemmArgs p, int64_t tiles_
     tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
     const int64_t m0 = tm * T::BM, n0 = tn * T::BN;
 
-    // K tiles: appended regions first (dgrad fold), then this split's slice
-    // of the main segment.
-    int n_ext = 0, E = 0;
-    const int32_t* rstart = nullptr;
-    if (p.extA) {
-        E = p.layout[0];
-        n_ext = p.layout[1] / T::BK;
-        rstart = p.layout + 4;
-    }
+    // K tiles: this split's slice of the main segment, with the appended
+    // fold columns (dgrad) around it.
+    const FoldView fv = fold_view(p, T::BK);
     const int64_t kbeg = (int64_t)blockIdx.y * k_per_split;
     const int64_t kend = min(p.K, kbeg + k_per_split);
     const int n_main = kend > kbeg ? (int)((kend - kbeg + T::BK - 1) / T::BK) : 0;
-    const int n_tiles = n_ext + n_main;
+    const int n_tiles = fv.n_ext + n_main;
 
     acc_t acc[T::FM][T::FN];
 #pragma unroll
@@ -140,12 +176,12 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm(GemmArgs p, int64_t tiles_
     auto load = [&](int t) {
         const int8_t *Ab, *Bb;
         int64_t la, lb, k0, klim;
-        if (t < n_ext) {
+        if (fv.is_ext(t, n_main)) {
             Ab = p.extA; la = p.ld_extA; Bb = p.extB; lb = p.ld_extB;
-            k0 = (int64_t)t * T::BK; klim = (int64_t)n_ext * T::BK;
+            k0 = fv.ext_col(t, n_main); klim = (int64_t)fv.n_ext * T::BK;
         } else {
             Ab = p.A; la = p.lda; Bb = p.B; lb = p.ldb;
-            k0 = kbeg + (int64_t)(t - n_ext) * T::BK; klim = kend;
+            k0 = kbeg + (int64_t)(t - fv.h_tiles) * T::BK; klim = kend;
         }
 #pragma unroll
         for (int i = 0; i < T::LA; ++i) {
@@ -214,21 +250,27 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm(GemmArgs p, int64_t tiles_
         load(0);
         store(0);
         __syncthreads();
-        int next_region = 0;
+        HornerSteps hs(p);
         for (int t = 0; t < n_tiles; ++t) {
             if (t + 1 < n_tiles) load(t + 1);
-            if (next_region < E && t < n_ext && (int64_t)t * T::BK == rstart[next_region]) {
-                // Horner step: the accumulated regions weigh twice the next one
+            if ((int64_t)t * T::BK == hs.col) {
+                const int sft = hs.advance(p);
 #pragma unroll
                 for (int i = 0; i < T::FM; ++i)
 #pragma unroll
-                    for (int j = 0; j < T::FN; ++j) acc[i][j] = acc[i][j] + acc[i][j];
-                ++next_region;
+                    for (int j = 0; j < T::FN; ++j) acc[i][j] = acc[i][j] << sft;
             }
             compute(t & 1);
             if (t + 1 < n_tiles) store((t + 1) & 1);
             __syncthreads();
         }
+    }
+
+    if (fv.fshift) {
+#pragma unroll
+        for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+            for (int j = 0; j < T::FN; ++j) acc[i][j] = acc[i][j] << fv.fshift;
     }
 
     // ---- epilogue ----
@@ -361,17 +403,11 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
     tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
     const int64_t m0 = tm * T::BM, n0 = tn * T::BN;
 
-    int n_ext = 0, E = 0;
-    const int32_t* rstart = nullptr;
-    if (p.extA) {
-        E = p.layout[0];
-        n_ext = p.layout[1] / T::BK;
-        rstart = p.layout + 4;
-    }
+    const FoldView fv = fold_view(p, T::BK);
     const int64_t kbeg = (int64_t)blockIdx.y * k_per_split;
     const int64_t kend = min(p.K, kbeg + k_per_split);
     const int n_main = kend > kbeg ? (int)((kend - kbeg) / T::BK) : 0;
-    const int n_tiles = n_ext + n_main;
+    const int n_tiles = fv.n_ext + n_main;
 
     // Per-lane source rows and chunk offsets of this wave's load
     // instructions: row r of the instruction's 16, logical chunk
@@ -395,11 +431,11 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
 
     auto issue = [&](int t) {
         int8_t* st = smem + (t % T::STAGES) * T::kStage;
-        const bool ext = t < n_ext;
+        const bool ext = fv.is_ext(t, n_main);
         const int8_t* Ab = ext ? p.extA : p.A;
         const int8_t* Bb = ext ? p.extB : p.B;
         const int64_t la = ext ? p.ld_extA : p.lda, lb = ext ? p.ld_extB : p.ldb;
-        const int64_t k0 = ext ? (int64_t)t * T::BK : kbeg + (int64_t)(t - n_ext) * T::BK;
+        const int64_t k0 = ext ? fv.ext_col(t, n_main) : kbeg + (int64_t)(t - fv.h_tiles) * T::BK;
 #pragma unroll
         for (int i = 0; i < T::IA; ++i)
             __builtin_amdgcn_global_load_lds((gbl_void_t*)(Ab + rowA[i] * la + chA[i] + k0),
@@ -448,7 +484,7 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
 #pragma unroll
         for (int s = 0; s < T::STAGES - 1; ++s)
             if (s < n_tiles) issue(s);
-        int next_region = 0;
+        HornerSteps hs(p);
         for (int t = 0; t < n_tiles; ++t) {
             // this wave's loads of tile t are done once at most
             // min(STAGES - 2, n_tiles - 1 - t) later tiles remain in flight
@@ -458,17 +494,23 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
             else wait_vm<0>();
             __builtin_amdgcn_s_barrier();   // tile t is in LDS for every wave; stage (t-1) is free
             if (t + T::STAGES - 1 < n_tiles) issue(t + T::STAGES - 1);
-            if (next_region < E && t < n_ext && (int64_t)t * T::BK == rstart[next_region]) {
-                // Horner step: the accumulated regions weigh twice the next one
+            if ((int64_t)t * T::BK == hs.col) {
+                const int sft = hs.advance(p);
 #pragma unroll
                 for (int i = 0; i < T::FM; ++i)
 #pragma unroll
-                    for (int j = 0; j < T::FN; ++j) acc[i][j] = acc[i][j] + acc[i][j];
-                ++next_region;
+                    for (int j = 0; j < T::FN; ++j) acc[i][j] = acc[i][j] << sft;
             }
             compute(t);
             wait_lgkm0();   // every LDS read of this stage has returned before the next barrier
         }
+    }
+
+    if (fv.fshift) {
+#pragma unroll
+        for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+            for (int j = 0; j < T::FN; ++j) acc[i][j] = acc[i][j] << fv.fshift;
     }
 
     // ---- epilogue (same as the register-staged kernel) ----
@@ -627,7 +669,7 @@ template <class T>
 hipError_t launch_cfg(const GemmArgs& a, int splits, int64_t k_per_split, hipStream_t s) {
     const int64_t tiles_m = (a.Mg + T::BM - 1) / T::BM, tiles_n = (a.Ng + T::BN - 1) / T::BN;
     if (tiles_m * tiles_n > 0x7FFFFFFF || splits > 65535) return hipErrorInvalidValue;
-    if (a.extA && (kFoldPad % T::BK) != 0) return hipErrorInvalidValue;   // regions must start on K tiles
+    if (a.layout && T::BK != kFoldPad) return hipErrorInvalidValue;   // fold regions are whole K tiles
     dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)splits);
     hipLaunchKernelGGL(k_gemm<T>, grid, dim3(T::kThreads), 0, s, a, tiles_m, tiles_n, k_per_split);
     return hipGetLastError();

@@ -11,16 +11,33 @@ namespace sq {
 
 // ---------------------------------------------------------------------------
 // Fold layout descriptor (int32 words in a caller-provided device buffer).
-//   [0] E      : appended regions in use (0 when no channel needs them)
-//   [1] D      : appended columns in use (a multiple of kFoldPad)
-//   [2] base   : q_fold column where the appended columns start
-//   [4 + r]    : start column (relative to base) of region r, r < kMaxRegions,
-//                regions in the order the dgrad K-loop visits them
-//   [kLayoutHeader + j] : channel copied into appended column j, -1 = zero
+//
+// ShiftMM needs sum_c code_c * w_c * 2^sh_c with sh_c = N_G - 1 - g_c.  The
+// shifts are cut into windows of T + 1 consecutive values (T: the largest
+// shift with Q * 2^T <= 127); a channel of window [B, B + T] is stored once,
+// as code << (sh_c - B), which fits int8.  The window holding the most
+// channels stays in the channel's own column of q_fold (the main columns);
+// every other window is a compacted region of appended columns.  The dgrad
+// visits the regions in descending B as one flat K sequence -- appended
+// columns [0, H), the main columns [0, base), appended columns [H, D) -- and
+// shifts the accumulator left by B_prev - B at each region start and by the
+// last B at the end (Horner's rule), which gives the sum exactly.
+//   [0] NR     regions (1..kMaxRegions; the main columns are one of them)
+//   [1] D      appended columns in use (a multiple of kFoldPad)
+//   [2] base   q_fold column of appended column 0 (= roundup(C, kFoldPad))
+//   [3] F      final left shift of the accumulator
+//   [4] H      appended columns visited before the main columns
+//   [8 + r]    flat K column where region r starts (r < NR; INT32_MAX after)
+//   [16 + r]   left shift of the accumulator before region r (0 for r = 0)
+//   [kLayoutHeader + j], j < ext_max: channel of appended column j, -1 = pad
+//   [kLayoutHeader + ext_max + c], c < C: channel descriptor
+//              ((pos + 1) << 4) | t: code << t sits in main column c when
+//              pos = -1, else in appended column pos (main column c is 0)
 // ---------------------------------------------------------------------------
-constexpr int kLayoutHeader = 16;
+constexpr int kLayoutHeader = 32;
 constexpr int kMaxRegions = 8;
-constexpr int kFoldPad = 64;        // appended regions are padded to the GEMM K tile
+constexpr int kFoldPad = 64;        // regions are padded to the GEMM K tile
+constexpr int kLayNR = 0, kLayD = 1, kLayBase = 2, kLayF = 3, kLayH = 4, kLayStart = 8, kLayShift = 16;
 
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
@@ -30,7 +47,6 @@ struct QuantCfg {
     int Q;             // 2^(bits-1) - 1
     int num_groups;    // N_G
     int T;             // largest shift with Q * 2^T <= 127
-    int E_max;         // max(0, N_G - 1 - T): appended regions in the worst case
     int round_mode;
     uint64_t seed;
     uint64_t offset;
@@ -38,9 +54,13 @@ struct QuantCfg {
 
 QuantCfg make_cfg(const sq_quant_params& p);
 
-// Worst-case appended columns for C channels and the layout size in words.
+// Worst-case appended columns for C channels: 0 when every shift fits one
+// window, else the non-main channels (< C) plus the padding of at most N_G - 1
+// appended regions.
 int64_t fold_ext_max(int64_t C, const QuantCfg& c);
 __host__ __device__ inline int64_t fold_ext_base(int64_t C) { return round_up(C, kFoldPad); }
+// Layout words for C channels: header, appended-column list, channel descriptors.
+inline int64_t fold_layout_words(int64_t C, const QuantCfg& c) { return kLayoutHeader + fold_ext_max(C, c) + C; }
 
 // ---- quantizer (sq_quant.hip) ----
 // First-level abs-max: rows cut into `slabs`, chunks of 4 * tpr channels.
@@ -58,14 +78,16 @@ int64_t colmax_workspace_words(int64_t M, int64_t C);
 hipError_t launch_colmax(const float* x, int64_t M, int64_t C, int64_t ld, uint32_t* partial, int64_t* slabs,
                          hipStream_t s);
 hipError_t launch_finalize_grad(const uint32_t* partial, int64_t slabs, int64_t C, const QuantCfg& cfg,
-                                uint32_t* rbits, uint8_t* group, sq_scale* scale, int32_t* layout, hipStream_t s);
+                                uint32_t* rbits, uint8_t* group, sq_scale* scale, int32_t* layout,
+                                int64_t ext_max, hipStream_t s);
 hipError_t launch_finalize_tensor(const uint32_t* partial, int64_t slabs, int64_t C, int Q, uint32_t* rbits,
                                   sq_scale* scale, hipStream_t s);
-// group == nullptr: every channel in group 0 with shift 0 (per-tensor mode).
+// group == nullptr: every channel in group 0 with shift 0 (per-tensor mode);
+// desc: the channel descriptors of the fold layout (nullptr: all main, t = 0).
 hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, const uint8_t* group,
                            const sq_scale* scale, const QuantCfg& cfg,
                            int8_t* q_fold, int64_t ld_fold, int8_t* q_t, int64_t ld_t,
-                           const int32_t* layout, hipStream_t s);
+                           const int32_t* desc, hipStream_t s);
 
 // ---- GEMMs (sq_gemm.hip) ----
 struct GemmArgs {
@@ -73,9 +95,9 @@ struct GemmArgs {
     const int8_t* A; int64_t lda;   // [Mg, lda], K contiguous
     const int8_t* B; int64_t ldb;   // [Ng, ldb], K contiguous
     int64_t K;
-    const int8_t* extA; int64_t ld_extA;   // appended K region (dgrad fold), may be null
+    const int8_t* extA; int64_t ld_extA;   // appended K columns (dgrad fold), may be null
     const int8_t* extB; int64_t ld_extB;
-    const int32_t* layout;
+    const int32_t* layout;          // fold layout (dgrad), may be null
     int splits;                     // split-K factor over the main segment
     int32_t* acc; int64_t ld_acc;   // int32 output
     float* out; int64_t ld_out;     // fp32 output

@@ -259,11 +259,6 @@ __device__ __forceinline__ int group_of(float r_c, float r_max, int num_groups) 
     return num_groups - 1;
 }
 
-__device__ __forceinline__ int excess_of(int g, const QuantCfg& cfg) {
-    const int sh = cfg.num_groups - 1 - g;
-    return sh > cfg.T ? sh - cfg.T : 0;
-}
-
 __device__ __forceinline__ sq_scale make_scale(uint32_t mb, float Qf) {
     const float r_max = __uint_as_float(mb);
     uint32_t flags = 0u;
@@ -277,77 +272,196 @@ __device__ __forceinline__ sq_scale make_scale(uint32_t mb, float Qf) {
     return s;
 }
 
+// Shift windows of the fold (the layout is documented in sq_internal.h),
+// computed by one thread from the number of channels at each shift.
+struct FoldPlan {
+    int nr, main_r, D, H, F;
+    int win_of[kMaxRegions];      // region of each shift value
+    int base[kMaxRegions];        // lowest shift of each region
+    int cnt[kMaxRegions];         // channels of each region
+    int ext_start[kMaxRegions];   // first appended column (non-main regions)
+    int flat[kMaxRegions];        // first flat K column
+    int run[kMaxRegions];         // channels ranked so far
+};
+
+__device__ void make_fold_plan(const int* n, int S, int T, int64_t C, FoldPlan& P) {
+    auto count = [&](int lo, int hi) {
+        int c = 0;
+        for (int s = lo; s <= hi; ++s) c += n[s];
+        return c;
+    };
+    // the window [B, B + T] holding the most channels stays in the main columns
+    int bstar = 0, best = -1;
+    for (int B = 0; B <= max(0, S - T); ++B) {
+        const int c = count(B, min(S, B + T));
+        if (c > best) { best = c; bstar = B; }
+    }
+    P.nr = 0;
+    auto add = [&](int lo, int hi) {
+        const int r = P.nr++;
+        P.base[r] = lo;
+        P.cnt[r] = count(lo, hi);
+        for (int s = lo; s <= hi; ++s) P.win_of[s] = r;
+    };
+    // descending base: windows above the main one (highest first), the main
+    // window, then the windows below it; empty windows are dropped
+    int top = bstar + T + 1;
+    while (top + T + 1 <= S) top += T + 1;
+    for (int lo = top; lo > bstar + T; lo -= T + 1)
+        if (count(lo, min(S, lo + T)) > 0) add(lo, min(S, lo + T));
+    P.main_r = P.nr;
+    add(bstar, min(S, bstar + T));
+    for (int hi = bstar - 1; hi >= 0;) {
+        const int lo = max(0, hi - T);
+        if (count(lo, hi) > 0) add(lo, hi);
+        hi = lo - 1;
+    }
+    int flat = 0, ext = 0;
+    P.H = 0;
+    for (int r = 0; r < P.nr; ++r) {
+        P.flat[r] = flat;
+        P.run[r] = 0;
+        if (r == P.main_r) {
+            P.ext_start[r] = -1;
+            P.H = ext;
+            flat += (int)round_up(C, kFoldPad);
+        } else {
+            P.ext_start[r] = ext;
+            ext += (int)round_up(P.cnt[r], kFoldPad);
+            flat += (int)round_up(P.cnt[r], kFoldPad);
+        }
+    }
+    P.D = ext;
+    P.F = P.base[P.nr - 1];
+}
+
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
 // ---------------------------------------------------------------------------
-// Finalize for the gradient quantizer (one block).  With C < kFinThreads the
-// slab maxima are combined here; otherwise k_colmax_reduce has written rbits
-// and one maximum per block.  Thread tid owns the contiguous channels
-// [tid * R, tid * R + R), R = ceil(C / kFinThreads), so each fold region's
-// channel list comes out of a single block-wide scan.
+// Finalize for the gradient quantizer (one block): r_max, scales and flags,
+// the group of every channel (channel c handled by thread c mod kFinThreads),
+// the shift windows of the fold, and each channel's place in q_fold.  The
+// appended columns of a region list its channels in ascending order; a
+// channel's rank comes from wave ballots plus per-wave totals in LDS.
 // ---------------------------------------------------------------------------
+constexpr int kFinWaves = kFinThreads / 64;
+
 __global__ __launch_bounds__(kFinThreads) void k_finalize_grad(const uint32_t* __restrict__ partial, int64_t S,
                                                                int64_t C, QuantCfg cfg,
-                                                               uint32_t* __restrict__ rbits,
+                                                               const uint32_t* __restrict__ rbits,
                                                                const uint32_t* __restrict__ bmax, int64_t nb,
                                                                uint8_t* __restrict__ group,
                                                                sq_scale* __restrict__ scale,
-                                                               int32_t* __restrict__ layout) {
+                                                               int32_t* __restrict__ layout, int64_t ext_max) {
     __shared__ uint32_t shu[16];
-    __shared__ int shi[16];
+    __shared__ int wtot[kFinWaves][kMaxRegions];
     __shared__ uint32_t lanes[kFinThreads];
-    const int tid = threadIdx.x;
+    __shared__ FoldPlan P;
+    __shared__ int nsh[kMaxRegions];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int Sh = cfg.num_groups - 1;   // largest shift
 
-    uint32_t mb = 0u;
+    uint32_t mb = 0u, r_small = 0u;
     if (C < kFinThreads) {
-        const uint32_t r = small_channel_ranges(partial, S, C, lanes);
-        if (tid < C) rbits[tid] = r;   // read back below by the same thread
-        mb = r;
+        r_small = small_channel_ranges(partial, S, C, lanes);
+        mb = r_small;
     } else {
         for (int64_t i = tid; i < nb; i += kFinThreads) mb = max(mb, bmax[i]);
     }
     mb = block_max_u32(mb, shu);
     const sq_scale sc = make_scale(mb, (float)cfg.Q);
     if (tid == 0) *scale = sc;
-    const float r_max = sc.r_max;
     const bool flagged = sc.flags != 0u;
 
-    const int64_t R = (C + kFinThreads - 1) / kFinThreads;
-    const int64_t c_lo = min(C, (int64_t)tid * R), c_hi = min(C, c_lo + R);
-    auto group_at = [&](int64_t c) {
-        return flagged ? cfg.num_groups - 1 : group_of(__uint_as_float(rbits[c]), r_max, cfg.num_groups);
-    };
-
-    int emax = 0;
-    for (int64_t c = c_lo; c < c_hi; ++c) {
-        const int g = group_at(c);
+    // groups and the number of channels at each shift
+    int hist[kMaxRegions];
+#pragma unroll
+    for (int s = 0; s < kMaxRegions; ++s) hist[s] = 0;
+    for (int64_t c = tid; c < C; c += kFinThreads) {
+        const uint32_t rb = C < kFinThreads ? r_small : rbits[c];
+        const int g = flagged ? Sh : group_of(__uint_as_float(rb), sc.r_max, cfg.num_groups);
         group[c] = (uint8_t)g;
-        emax = max(emax, excess_of(g, cfg));
+#pragma unroll
+        for (int s = 0; s < kMaxRegions; ++s) hist[s] += (Sh - g) == s;
     }
-    const int E = (int)block_max_u32((uint32_t)emax, shu);
+#pragma unroll
+    for (int s = 0; s < kMaxRegions; ++s) {
+        const int v = wave_sum(hist[s]);
+        if (lane == 0) wtot[wave][s] = v;
+    }
+    __syncthreads();
+    if (tid < kMaxRegions) {
+        int v = 0;
+        for (int w = 0; w < kFinWaves; ++w) v += wtot[w][tid];
+        nsh[tid] = v;
+    }
+    __syncthreads();
+    if (tid == 0) make_fold_plan(nsh, Sh, cfg.T, C, P);
+    __syncthreads();
 
-    // Appended regions, in the order the dgrad visits them: region r holds,
-    // in ascending order, the channels whose excess exceeds j = E - 1 - r,
-    // padded with -1 to a multiple of kFoldPad columns.
+    // place of every channel: descriptor ((pos + 1) << 4) | t, and the
+    // appended-column list
     int32_t* ext = layout + kLayoutHeader;
-    int start = 0;
-    for (int r = 0; r < E; ++r) {
-        const int j = E - 1 - r;
-        int cnt = 0;
-        for (int64_t c = c_lo; c < c_hi; ++c) cnt += excess_of(group_at(c), cfg) > j;
-        int total = 0;
-        int pos = start + block_excl_scan(cnt, shi, &total);
-        for (int64_t c = c_lo; c < c_hi; ++c)
-            if (excess_of(group_at(c), cfg) > j) ext[pos++] = (int32_t)c;
-        const int padded = (int)round_up(total, kFoldPad);
-        for (int i = total + tid; i < padded; i += kFinThreads) ext[start + i] = -1;
-        if (tid == 0) layout[4 + r] = start;
-        start += padded;
+    int32_t* desc = ext + ext_max;
+    const int nr = P.nr, main_r = P.main_r;
+    const uint64_t below = (1ull << lane) - 1ull;
+    for (int64_t c0 = 0; c0 < C; c0 += kFinThreads) {
+        const int64_t c = c0 + tid;
+        int r = main_r, t = 0;
+        if (c < C) {
+            const int sh = Sh - (int)group[c];   // written by this thread above
+            r = P.win_of[sh];
+            t = sh - P.base[r];
+        }
+        const bool is_ext = c < C && r != main_r;
+        int rank = 0;
+        for (int q = 0; q < nr; ++q) {
+            const uint64_t m = __ballot(is_ext && r == q);
+            if (is_ext && r == q) rank = __popcll(m & below);
+            if (lane == 0) wtot[wave][q] = __popcll(m);
+        }
+        __syncthreads();
+        int pos = -1;
+        if (is_ext) {
+            int before = P.run[r];
+            for (int w = 0; w < wave; ++w) before += wtot[w][r];
+            pos = P.ext_start[r] + before + rank;
+        }
+        __syncthreads();   // every thread has read run[] for this round
+        if (tid < nr) {
+            int tot = 0;
+            for (int w = 0; w < kFinWaves; ++w) tot += wtot[w][tid];
+            P.run[tid] += tot;
+        }
+        if (c < C) {
+            desc[c] = ((pos + 1) << 4) | t;
+            if (is_ext) ext[pos] = (int32_t)c;
+        }
+        __syncthreads();   // run[] updated and wtot free for the next round
     }
-    if (tid == 0) {
-        layout[0] = E;
-        layout[1] = start;
-        layout[2] = (int32_t)fold_ext_base(C);
-        layout[3] = 0;
-        for (int r = E; r < kMaxRegions; ++r) layout[4 + r] = start;
+    for (int r = 0; r < nr; ++r) {
+        if (r == main_r) continue;
+        const int padded = (int)round_up(P.cnt[r], kFoldPad);
+        for (int i = P.cnt[r] + tid; i < padded; i += kFinThreads) ext[P.ext_start[r] + i] = -1;
+    }
+    if (tid < kLayoutHeader) {
+        int v = 0;
+        if (tid == kLayNR) v = nr;
+        else if (tid == kLayD) v = P.D;
+        else if (tid == kLayBase) v = (int)fold_ext_base(C);
+        else if (tid == kLayF) v = P.F;
+        else if (tid == kLayH) v = P.H;
+        else if (tid >= kLayStart && tid < kLayStart + kMaxRegions)
+            v = tid - kLayStart < nr ? P.flat[tid - kLayStart] : 0x7FFFFFFF;
+        else if (tid >= kLayShift && tid < kLayShift + kMaxRegions) {
+            const int r = tid - kLayShift;
+            v = (r > 0 && r < nr) ? P.base[r - 1] - P.base[r] : 0;
+        }
+        layout[tid] = v;
     }
 }
 
@@ -384,7 +498,7 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
                                                      const sq_scale* __restrict__ scale, QuantCfg cfg, int tc4n,
                                                      int8_t* __restrict__ q_fold, int64_t ld_fold,
                                                      int8_t* __restrict__ q_t, int64_t ld_t,
-                                                     const int32_t* __restrict__ layout) {
+                                                     const int32_t* __restrict__ desc, int64_t ext_base) {
     const int tid = threadIdx.x;
     const int tc4 = tid & (tc4n - 1), tr = tid / tc4n;
     const int rows_per_tile = kQR * (kBlock / tc4n);
@@ -396,13 +510,15 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
     const float Qf = (float)cfg.Q;
 
     float s[4];
-    int t[4];
+    int t[4], pos[4];   // fold: code << t in main column c (pos < 0) or appended column pos
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         const int64_t c = c0 + j;
         const int g = (group && c < C) ? (int)group[c] : 0;
         s[j] = __fmul_rn(sc.inv, pow2f(g));
-        t[j] = group ? min(cfg.num_groups - 1 - g, cfg.T) : 0;
+        const int d = (desc && c < C) ? desc[c] : 0;
+        t[j] = d & 15;
+        pos[j] = (d >> 4) - 1;
     }
     const bool sr_vec = SR && ((C & 3) == 0);   // 4 channels share one Philox block
 
@@ -455,16 +571,20 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
                     colw[j][i / 4] |= (uint32_t)(uint8_t)code[j] << (8 * (i % 4));
                 }
                 if (q_fold && m < M) {
-                    int8_t* dst = q_fold + m * ld_fold + c0;
+                    int8_t* row = q_fold + m * ld_fold;
+                    uint32_t word = 0u;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const uint32_t f = (uint32_t)(uint8_t)(code[j] * (1 << t[j]));
+                        if (pos[j] < 0) word |= f << (8 * j);
+                        else if (c0 + j < C) row[ext_base + pos[j]] = (int8_t)f;
+                    }
                     if (c0 + 4 <= C) {
-                        *reinterpret_cast<uint32_t*>(dst) = ((uint32_t)(uint8_t)(code[0] * (1 << t[0]))) |
-                                                            ((uint32_t)(uint8_t)(code[1] * (1 << t[1])) << 8) |
-                                                            ((uint32_t)(uint8_t)(code[2] * (1 << t[2])) << 16) |
-                                                            ((uint32_t)(uint8_t)(code[3] * (1 << t[3])) << 24);
+                        *reinterpret_cast<uint32_t*>(row + c0) = word;
                     } else {
 #pragma unroll
                         for (int j = 0; j < 4; ++j)
-                            if (c0 + j < C) dst[j] = (int8_t)(code[j] * (1 << t[j]));
+                            if (c0 + j < C) row[c0 + j] = (int8_t)(word >> (8 * j));
                     }
                 }
             }
@@ -480,31 +600,6 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
                             dst[i] = (int8_t)(colw[j][i / 4] >> (8 * (i % 4)));
                     }
                 }
-            }
-        }
-
-        // Appended fold columns (dgrad operand only), written by the blocks of
-        // the first channel tile for their rows.
-        if (q_fold && layout && blockIdx.x == 0) {
-            const int D = layout[1];
-            const int64_t base = layout[2];
-            const int32_t* ext = layout + kLayoutHeader;
-            const int64_t m_tile = rt * rows_per_tile;
-            const int64_t n_el = (int64_t)rows_per_tile * D;
-            for (int64_t idx = tid; idx < n_el; idx += kBlock) {
-                const int64_t rr = idx / D, j = idx % D;
-                const int64_t m = m_tile + rr;
-                if (m >= M) continue;
-                const int ch = ext[j];
-                int val = 0;
-                if (ch >= 0 && !zero) {
-                    const int g = (int)group[ch];
-                    const float sc_ch = __fmul_rn(sc.inv, pow2f(g));
-                    const uint32_t u = SR ? sr_uniform24((uint64_t)(m * C + ch), cfg) : 0u;
-                    const int tt = min(cfg.num_groups - 1 - g, cfg.T);
-                    val = quant_one<SR>(x[m * ld + ch], sc_ch, Qf, u) * (1 << tt);
-                }
-                q_fold[m * ld_fold + base + j] = (int8_t)val;
             }
         }
     }
@@ -567,12 +662,13 @@ static hipError_t launch_reduce(const uint32_t* partial, int64_t slabs, int64_t 
 }
 
 hipError_t launch_finalize_grad(const uint32_t* partial, int64_t slabs, int64_t C, const QuantCfg& cfg,
-                                uint32_t* rbits, uint8_t* group, sq_scale* scale, int32_t* layout, hipStream_t s) {
+                                uint32_t* rbits, uint8_t* group, sq_scale* scale, int32_t* layout,
+                                int64_t ext_max, hipStream_t s) {
     uint32_t* bmax = rbits + C;
     const hipError_t e = launch_reduce(partial, slabs, C, rbits, bmax, s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_finalize_grad, dim3(1), dim3(kFinThreads), 0, s, partial, slabs, C, cfg, rbits, bmax,
-                       colmax_reduce_blocks(C), group, scale, layout);
+                       colmax_reduce_blocks(C), group, scale, layout, ext_max);
     return hipGetLastError();
 }
 
@@ -588,7 +684,7 @@ hipError_t launch_finalize_tensor(const uint32_t* partial, int64_t slabs, int64_
 
 hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, const uint8_t* group,
                            const sq_scale* scale, const QuantCfg& cfg, int8_t* q_fold, int64_t ld_fold,
-                           int8_t* q_t, int64_t ld_t, const int32_t* layout, hipStream_t s) {
+                           int8_t* q_t, int64_t ld_t, const int32_t* desc, hipStream_t s) {
     if (M <= 0 || C <= 0) return hipSuccess;
     const bool vec = ((ld & 3) == 0) && ((reinterpret_cast<uintptr_t>(x) & 15) == 0);
     const bool sr = cfg.round_mode == SQ_ROUND_STOCHASTIC;
@@ -599,16 +695,16 @@ hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, con
               (unsigned)std::min<int64_t>((M + rows_per_tile - 1) / rows_per_tile, 65535));
     if (vec && sr)
         hipLaunchKernelGGL((k_quantize<4, true>), grid, dim3(kBlock), 0, s, x, M, C, ld, group, scale, cfg, tc4n,
-                           q_fold, ld_fold, q_t, ld_t, layout);
+                           q_fold, ld_fold, q_t, ld_t, desc, fold_ext_base(C));
     else if (vec)
         hipLaunchKernelGGL((k_quantize<4, false>), grid, dim3(kBlock), 0, s, x, M, C, ld, group, scale, cfg, tc4n,
-                           q_fold, ld_fold, q_t, ld_t, layout);
+                           q_fold, ld_fold, q_t, ld_t, desc, fold_ext_base(C));
     else if (sr)
         hipLaunchKernelGGL((k_quantize<1, true>), grid, dim3(kBlock), 0, s, x, M, C, ld, group, scale, cfg, tc4n,
-                           q_fold, ld_fold, q_t, ld_t, layout);
+                           q_fold, ld_fold, q_t, ld_t, desc, fold_ext_base(C));
     else
         hipLaunchKernelGGL((k_quantize<1, false>), grid, dim3(kBlock), 0, s, x, M, C, ld, group, scale, cfg, tc4n,
-                           q_fold, ld_fold, q_t, ld_t, layout);
+                           q_fold, ld_fold, q_t, ld_t, desc, fold_ext_base(C));
     return hipGetLastError();
 }
 

@@ -56,16 +56,17 @@ def _params(sq, bits=4, ng=4, mode=0):
 
 def test_size_queries(sq):
     p = _params(sq, 4, 4)
+    # layout words: 32 header + appended-column list + one descriptor per channel
     nb, ld = sq.sq_grad_layout_size(100, p)
-    assert nb == 16 * 4 and ld == 112          # b=4, N_G=4: every shift fits int8, no appended columns
+    assert nb == (32 + 100) * 4 and ld == 112  # b=4, N_G=4: every shift fits one window, nothing appended
     p6 = _params(sq, 6, 4)
-    nb, ld = sq.sq_grad_layout_size(100, p6)  # b=6: one appended region of up to roundup(100, 64) columns
-    assert nb == (16 + 128) * 4 and ld == 128 + 128
+    nb, ld = sq.sq_grad_layout_size(100, p6)  # b=6: at most roundup(100, 64) + 64 * 3 appended columns
+    assert nb == (32 + 320 + 100) * 4 and ld == 128 + 320
     p8 = _params(sq, 8, 4)
-    nb, ld = sq.sq_grad_layout_size(64, p8)   # b=8: three regions
-    assert ld == 64 + 3 * 64
+    nb, ld = sq.sq_grad_layout_size(64, p8)   # b=8: one window per shift
+    assert nb == (32 + 256 + 64) * 4 and ld == 64 + 256
     assert sq.sq_gemm_dgrad_workspace_size(10, 100, 30, p) == 0
-    assert sq.sq_gemm_dgrad_workspace_size(10, 100, 30, p6) == 30 * 128 + (256 - (30 * 128) % 256) % 256
+    assert sq.sq_gemm_dgrad_workspace_size(10, 100, 30, p6) == 30 * 320 + (256 - (30 * 320) % 256) % 256
     assert sq.sq_quantize_grad_workspace_size(10, 100, p) == 1024   # one slab of maxima + ranges
     assert sq.sq_quantize_tensor_workspace_size(10, 3) == 256
 

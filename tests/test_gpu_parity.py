@@ -52,22 +52,85 @@ def _dev(a, ld_pad=0, misalign=0):
     return view
 
 
-def expected_layout(g, num_groups, bits, pad=64):
-    """The fold layout include/shiftquant.h documents, derived from the group ids."""
-    T = _T(bits)
-    sh = num_groups - 1 - g.astype(np.int64)
-    e = np.maximum(sh - T, 0)
-    E = int(e.max()) if e.size else 0
-    cols, starts = [], []
-    for r in range(E):
-        j = E - 1 - r
-        members = [int(c) for c in np.nonzero(e > j)[0]]
-        starts.append(len(cols))
-        cols += members + [-1] * ((-len(members)) % pad)
-    return E, cols, starts
+def expected_fold(g, num_groups, bits, pad=64):
+    """The fold of the dgrad operand as include/shiftquant.h documents it.
+
+    Shifts sh = N_G - 1 - g are cut into windows [B, B + T]; the window with
+    the most channels (lowest B on ties) keeps the channels' own columns, the
+    other non-empty windows become appended regions, visited in descending B.
+    Returns the regions (base, members, is_main) in visiting order, the
+    appended-column list, and per channel (t, pos).
+    """
+    T, S = _T(bits), num_groups - 1
+    sh = S - g.astype(np.int64)
+    n = np.bincount(sh, minlength=S + 1) if sh.size else np.zeros(S + 1, np.int64)
+    best, bstar = -1, 0
+    for B in range(0, max(0, S - T) + 1):
+        c = int(n[B:min(S, B + T) + 1].sum())
+        if c > best:
+            best, bstar = c, B
+    wins = [(lo, min(S, lo + T), False) for lo in range(bstar + T + 1, S + 1, T + 1)][::-1]
+    wins.append((bstar, min(S, bstar + T), True))
+    hi = bstar - 1
+    while hi >= 0:
+        lo = max(0, hi - T)
+        wins.append((lo, hi, False))
+        hi = lo - 1
+    regions = []
+    for lo, hi, is_main in wins:
+        members = [int(c) for c in np.nonzero((sh >= lo) & (sh <= hi))[0]]
+        if members or is_main:
+            regions.append((lo, members, is_main))
+    cols, t, pos = [], np.zeros(sh.size, np.int64), np.full(sh.size, -1, np.int64)
+    for base, members, is_main in regions:
+        for c in members:
+            t[c] = sh[c] - base
+        if not is_main:
+            for c in members:
+                pos[c] = len(cols)
+                cols.append(c)
+            cols += [-1] * ((-len(members)) % pad)
+    return regions, cols, t, pos
 
 
-def check_quant(sq, codes, dY, bits, ng, mode, seed, offset):
+def check_fold(codes, q_ref, g_ref, bits, ng, rows=None):
+    """Layout words and the shift-folded operand (all rows, or the given ones)."""
+    C = q_ref.shape[1]
+    regions, cols, t, pos = expected_fold(g_ref, ng, bits)
+    lay = codes.layout.cpu().numpy()
+    ext_max = len(lay) - 32 - C
+    base_col = (C + 63) // 64 * 64
+    nr = len(regions)
+    main_r = [i for i, r in enumerate(regions) if r[2]][0]
+    flat, starts = 0, []
+    for base, members, is_main in regions:
+        starts.append(flat)
+        flat += base_col if is_main else (len(members) + 63) // 64 * 64
+    H = sum((len(r[1]) + 63) // 64 * 64 for r in regions[:main_r])
+    assert lay[0] == nr and lay[1] == len(cols) and lay[2] == base_col, lay[:8]
+    assert lay[3] == regions[-1][0] and lay[4] == H, lay[:8]
+    assert list(lay[8:8 + nr]) == starts
+    assert list(lay[16:16 + nr]) == [0] + [regions[i - 1][0] - regions[i][0] for i in range(1, nr)]
+    assert len(cols) <= ext_max
+    assert list(lay[32:32 + len(cols)]) == cols
+    assert np.array_equal(lay[32 + ext_max:32 + ext_max + C], ((pos + 1) << 4) | t)
+    if q_ref.shape[0] == 0:
+        return
+    if rows is None:
+        qf = codes.q_fold.cpu().numpy().astype(np.int64)
+        shifted = q_ref.astype(np.int64) << t[None, :]
+    else:
+        import torch
+        qf = codes.q_fold.index_select(0, torch.as_tensor(rows, device="cuda")).cpu().numpy().astype(np.int64)
+        shifted = q_ref[rows].astype(np.int64) << t[None, :]
+    main = pos < 0
+    assert np.array_equal(qf[:, :C][:, main], shifted[:, main]), "main fold columns"
+    assert not qf[:, :C][:, ~main].any(), "main columns of appended channels must be 0"
+    for c in np.nonzero(~main)[0]:
+        assert np.array_equal(qf[:, base_col + pos[c]], shifted[:, c]), f"appended column of channel {c}"
+
+
+def check_quant(sq, codes, dY, bits, ng, mode, seed, offset, fold_rows=None):
     q_ref, g_ref, s_ref, _ = oracle.quantize_grad(dY, bits, ng, mode, seed, offset)
     M, C = dY.shape
     q = codes.codes().cpu().numpy()
@@ -80,28 +143,12 @@ def check_quant(sq, codes, dY, bits, ng, mode, seed, offset):
     assert s["bits"][1] == _f32bits(s_ref["inv0"])
     assert s["bits"][2] == _f32bits(s_ref["d0"])
     assert s["flags"] == s_ref["flags"]
-    # shift-folded dgrad operand and its appended columns
-    T = _T(bits)
-    t = np.minimum(ng - 1 - g_ref.astype(np.int64), T)
-    qf = codes.q_fold.cpu().numpy()
-    if M:
-        assert np.array_equal(qf[:, :C].astype(np.int64), q_ref.astype(np.int64) << t[None, :])
-    lay = codes.layout.cpu().numpy()
-    E, cols, starts = expected_layout(g_ref, ng, bits)
-    assert lay[0] == E and lay[1] == len(cols)
-    assert list(lay[16:16 + len(cols)]) == cols
-    assert list(lay[4:4 + E]) == starts
-    if M and cols:
-        base = int(lay[2])
-        ext = qf[:, base:base + len(cols)].astype(np.int64)
-        for j, ch in enumerate(cols):
-            want = (q_ref[:, ch].astype(np.int64) << t[ch]) if ch >= 0 else np.zeros(M, np.int64)
-            assert np.array_equal(ext[:, j], want), f"appended column {j} (channel {ch})"
+    check_fold(codes, q_ref, g_ref, bits, ng, fold_rows)
     return q_ref, g_ref, s_ref
 
 
 def check_layer(sq, dY, W, X, bits, ng, mode=0, seed=0, offset=0, dgrad_rows=None, wgrad_rows=None,
-                want_acc=True):
+                want_acc=True, fold_rows=None):
     import torch
     M, C_out = dY.shape
     C_in = W.shape[1]
@@ -111,7 +158,7 @@ def check_layer(sq, dY, W, X, bits, ng, mode=0, seed=0, offset=0, dgrad_rows=Non
     acc_d, dX = sq.gemm_dgrad(codes, wq_t, ws, want_acc=want_acc)
     acc_w, dW = sq.gemm_wgrad(codes, xq_t, xs, want_acc=want_acc)
     torch.cuda.synchronize()
-    q_ref, g_ref, s_ref = check_quant(sq, codes, dY, bits, ng, mode, seed, offset)
+    q_ref, g_ref, s_ref = check_quant(sq, codes, dY, bits, ng, mode, seed, offset, fold_rows)
 
     wq_ref, ws_ref = oracle.quantize_tensor(W, 8)
     xq_ref, xs_ref = oracle.quantize_tensor(X, 8)
@@ -255,6 +302,69 @@ def test_layer_parity(sq, layer, bits, ng):
     check_layer(sq, dY, W, X, bits, ng, mode=mode, seed=7, offset=3)
 
 
+def _grouped_grad(M, groups, seed):
+    """dY whose channel c has range exactly 0.75 * 2^-groups[c], so that (with a
+    channel in group 0) its ShiftQuant group is groups[c]."""
+    rng = np.random.default_rng(seed)
+    scale = 0.75 * np.exp2(-np.asarray(groups, np.float64))
+    dY = rng.uniform(-1.0, 1.0, (M, len(groups))) * scale[None, :]
+    hit = rng.integers(0, M, len(groups))
+    dY[hit, np.arange(len(groups))] = scale * np.where(rng.random(len(groups)) < 0.5, -1.0, 1.0)
+    return dY.astype(np.float32)
+
+
+def _group_pattern(name, C, ng, seed):
+    rng = np.random.default_rng(seed)
+    last = ng - 1
+    if name == "all_g0":
+        g = np.zeros(C, np.int64)
+    elif name == "mostly_g0":
+        g = np.where(rng.random(C) < 0.8, 0, last)
+    elif name == "middle":
+        g = np.where(rng.random(C) < 0.7, min(1, last), rng.integers(0, ng, C))
+    elif name == "bimodal":
+        g = np.where(rng.random(C) < 0.5, 0, last)
+    else:   # spread
+        g = rng.integers(0, ng, C)
+    g[0] = 0
+    return g
+
+
+FOLD_PATTERNS = ["all_g0", "mostly_g0", "middle", "bimodal", "spread"]
+
+
+@pytest.mark.parametrize("layer", [(200, 130, 70), (256, 192, 128)], ids=["ragged", "aligned"])
+@pytest.mark.parametrize("pattern", FOLD_PATTERNS)
+@pytest.mark.parametrize("bits,ng", [(6, 4), (8, 4), (7, 3), (2, 8), (3, 8), (8, 6)])
+def test_fold_windows(sq, layer, pattern, bits, ng):
+    # channel groups forced so that the main window sits at the bottom, in the
+    # middle or at the top of the shift range, with appended windows above,
+    # below or on both sides
+    M, C_out, C_in = layer
+    g = _group_pattern(pattern, C_out, ng, seed=C_out + bits)
+    dY = _grouped_grad(M, g, seed=M + ng)
+    q_ref, g_ref, _, _ = oracle.quantize_grad(dY, bits, ng, 0, 0, 0)
+    assert np.array_equal(g_ref, g)
+    rng = np.random.default_rng(bits * 10 + ng)
+    W = (rng.standard_normal((C_out, C_in)) * 0.02).astype(np.float32)
+    X = rng.standard_normal((M, C_in)).astype(np.float32)
+    check_layer(sq, dY, W, X, bits, ng, mode=(M + bits) % 2)
+
+
+@pytest.mark.parametrize("pattern", ["mostly_g0", "spread"])
+def test_fold_windows_large_tiles(sq, pattern):
+    # the same on the large-tile pipelined GEMM (K >= 1024, >= 256 output tiles)
+    M, C_out, C_in, bits, ng = 4096, 1024, 4096, 6, 4
+    g = _group_pattern(pattern, C_out, ng, seed=3)
+    dY = _grouped_grad(M, g, seed=4)
+    rng = np.random.default_rng(6)
+    W = (rng.standard_normal((C_out, C_in)) * 0.02).astype(np.float32)
+    X = rng.standard_normal((M, C_in)).astype(np.float32)
+    rows_d = np.unique(np.r_[0, 255, 256, M - 1, rng.integers(0, M, 20)])
+    rows_w = np.unique(np.r_[0, C_out - 1, rng.integers(0, C_out, 10)])
+    check_layer(sq, dY, W, X, bits, ng, dgrad_rows=rows_d, wgrad_rows=rows_w, fold_rows=rows_d)
+
+
 def test_fp32_only_outputs_match_with_acc(sq):
     import torch
     M, C_out, C_in = 300, 200, 129
@@ -353,6 +463,8 @@ def test_workload_full_size(sq, name):
     q = plan.q_t[:, :M].t().cpu().numpy()
     assert np.array_equal(plan.group.cpu().numpy(), g_ref)
     assert np.array_equal(q, q_ref)
+    fold_rows = np.unique(np.r_[0, M - 1, np.random.default_rng(2).integers(0, M, 64)])
+    check_fold(plan, q_ref, g_ref, wl.bits, wl.num_groups, fold_rows)
     wq_ref, ws_ref = oracle.quantize_tensor(d["W"], 8)
     xq_ref, xs_ref = oracle.quantize_tensor(d["X"], 8)
     assert np.array_equal(wq_t[:, :C_out].t().cpu().numpy(), wq_ref)
