@@ -29,6 +29,9 @@ HIPCC_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-mcode-object-version=5",
     "-Wall",
+    # every symbol resolved at link time (a kernel whose host stub went
+    # missing must fail the build, not the first launch)
+    "-Wl,--no-undefined",
 ]
 
 

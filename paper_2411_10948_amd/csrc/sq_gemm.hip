@@ -21,6 +21,7 @@
 // end (Horner's rule), so the result equals sum_c code * w << (N_G - 1 - g_c)
 // exactly.
 #include <algorithm>
+#include <type_traits>
 
 #include "sq_internal.h"
 
@@ -124,20 +125,33 @@ __device__ __forceinline__ FoldView fold_view(const GemmArgs& p, int bk) {
 
 // Region starts of the flat K sequence, in order; at each one the
 // accumulator is shifted left by the base difference to the region before
-// (Horner's rule).  col is the flat K column of the next start.
+// (Horner's rule).  The schedule is read once into registers, so the K loop
+// itself touches no memory but its operand tiles.  col is the flat K column
+// of the next start.
 struct HornerSteps {
     int next = 1, nr = 1;
     int64_t col = INT64_MAX;
+    uint32_t shifts = 0u;                                          // 4 bits per region
+    int s1 = 0, s2 = 0, s3 = 0, s4 = 0, s5 = 0, s6 = 0, s7 = 0;   // region starts
     __device__ explicit HornerSteps(const GemmArgs& p) {
+        static_assert(kMaxRegions == 8, "one start per region after the first");
         if (p.layout) {
-            nr = p.layout[kLayNR];
-            if (nr > 1) col = p.layout[kLayStart + 1];
+            const int32_t* L = p.layout;
+            nr = L[kLayNR];
+            s1 = L[kLayStart + 1]; s2 = L[kLayStart + 2]; s3 = L[kLayStart + 3]; s4 = L[kLayStart + 4];
+            s5 = L[kLayStart + 5]; s6 = L[kLayStart + 6]; s7 = L[kLayStart + 7];
+#pragma unroll
+            for (int r = 1; r < kMaxRegions; ++r) shifts |= (uint32_t)(L[kLayShift + r] & 15) << (4 * r);
+            if (nr > 1) col = s1;
         }
     }
-    __device__ int advance(const GemmArgs& p) {
-        const int sft = p.layout[kLayShift + next];
+    __device__ int start_of(int r) const {
+        return r == 1 ? s1 : r == 2 ? s2 : r == 3 ? s3 : r == 4 ? s4 : r == 5 ? s5 : r == 6 ? s6 : s7;
+    }
+    __device__ int advance() {
+        const int sft = (int)((shifts >> (4 * next)) & 15u);
         ++next;
-        col = next < nr ? p.layout[kLayStart + next] : INT64_MAX;
+        col = next < nr ? (int64_t)start_of(next) : INT64_MAX;
         return sft;
     }
 };
@@ -254,7 +268,7 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm(GemmArgs p, int64_t tiles_
         for (int t = 0; t < n_tiles; ++t) {
             if (t + 1 < n_tiles) load(t + 1);
             if ((int64_t)t * T::BK == hs.col) {
-                const int sft = hs.advance(p);
+                const int sft = hs.advance();
 #pragma unroll
                 for (int i = 0; i < T::FM; ++i)
 #pragma unroll
@@ -346,15 +360,21 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm(GemmArgs p, int64_t tiles_
 // ---------------------------------------------------------------------------
 // Pipelined variant for K-aligned operands: 64-byte K tiles move from global
 // memory straight into a ring of STAGES LDS buffers with the gfx950 direct
-// loads (global_load_lds_dwordx4, 16 bytes per lane), so STAGES - 1 tiles are
-// in flight without holding registers.  Each wave instruction fills 1 KB of
+// loads (buffer_load_dwordx4 ... lds, 16 bytes per lane, a fixed per-lane
+// offset and a scalar K offset), so STAGES - 1 tiles are in flight without
+// holding registers or address arithmetic.  Each wave instruction fills 1 KB of
 // LDS = 16 rows x 64 bytes in lane order; the 16-byte chunk c of row r is
 // stored at chunk c ^ swz(r), which keeps the fragment reads conflict-free.
 // Synchronisation is explicit: a wave waits (vmcnt) for its own loads of
 // tile t, a barrier publishes them to the block, and a stage is refilled only
-// after the barrier that follows every wave's reads of it.
+// after the barrier that follows every wave's reads of it.  The MFMA operands
+// are double-buffered in registers: the LDS reads of tile t + 1 are issued
+// before the MFMAs of tile t, so they complete while the matrix cores work.
+// HORNER = false compiles out the accumulator shifts of the fold (wgrad, and
+// dgrads whose fold has one window), which lets the accumulators live in the
+// matrix-core registers for the whole loop.
 // Requirements (checked by the launcher): every K segment a multiple of 64,
-// lda/ldb multiples of 16, 16-byte aligned operands.
+// lda/ldb multiples of 16, 16-byte aligned operands, offsets below 2^31.
 // ---------------------------------------------------------------------------
 template <int BM_, int BN_, int WM_, int WN_, int MF_, int STAGES_>
 struct PipeCfg {
@@ -363,6 +383,7 @@ struct PipeCfg {
     static constexpr int TM = BM / WM, TN = BN / WN;
     static constexpr int FM = TM / MF, FN = TN / MF;
     static constexpr int KS = MF == 32 ? 32 : 64;
+    static constexpr int KSTEPS = BK / KS;                // MFMA k-steps per K tile
     static constexpr int NACC = MF == 32 ? 16 : 4;
     static constexpr int kStage = (BM + BN) * BK;         // bytes per stage
     static constexpr int IA = BM / 16 / kWaves;           // A load instructions per wave per stage
@@ -371,14 +392,14 @@ struct PipeCfg {
     static constexpr int kSmem = STAGES * kStage;
     static_assert(IA * 16 * kWaves == BM && IB * 16 * kWaves == BN, "rows split evenly over waves");
     static_assert(TM % MF == 0 && TN % MF == 0, "wave tile must hold whole MFMA blocks");
-    static_assert(STAGES >= 2 && (STAGES - 2) * kLoads <= 63, "vmcnt range");
+    static_assert(STAGES >= 3 && STAGES <= 4 && (STAGES - 2) * kLoads <= 63, "vmcnt range");
 };
 
 using PipeLarge = PipeCfg<256, 256, 4, 2, 16, 4>;   // 128 KB of LDS, one block per CU
+using PipeWide = PipeCfg<256, 256, 2, 2, 16, 4>;    // 4 waves of 128 x 128: half the LDS reads per MFMA
 using PipeSmall = PipeCfg<128, 128, 2, 2, 16, 4>;   // 64 KB of LDS
 
 typedef __attribute__((address_space(3))) void lds_void_t;
-typedef const __attribute__((address_space(1))) void gbl_void_t;
 
 // chunk swizzle of a 64-byte LDS row (conflict-free for 8- and 16-lane phases)
 __device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 2)) & 3; }
@@ -390,9 +411,10 @@ __device__ __forceinline__ void wait_vm() {
 }
 __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0x7F | (0x3 << 14) | (0x0 << 8)); }
 
-template <class T>
+template <class T, bool HORNER>
 __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t tiles_m, int64_t tiles_n,
                                                            int64_t k_per_split) {
+#if defined(__HIP_DEVICE_COMPILE__)   // buffer resources exist in the device pass only
     __shared__ __attribute__((aligned(1024))) int8_t smem[T::kSmem];
     using MF = Mfma<T::MF>;
     using acc_t = typename MF::acc_t;
@@ -409,42 +431,56 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
     const int n_main = kend > kbeg ? (int)((kend - kbeg) / T::BK) : 0;
     const int n_tiles = fv.n_ext + n_main;
 
-    // Per-lane source rows and chunk offsets of this wave's load
-    // instructions: row r of the instruction's 16, logical chunk
-    // (lane % 4) ^ swz(r).  Rows past the end of an operand read its last row
-    // (their results are never stored).  Both K segments share them.
-    int64_t rowA[T::IA], rowB[T::IB];
-    int chA[T::IA], chB[T::IB];
+    // Operand tiles come in with buffer loads straight to LDS: each lane's
+    // 32-bit byte offset (row of its load instruction, logical chunk
+    // (lane % 4) ^ swz(r)) is fixed for the whole K loop, and the K offset of
+    // the tile is a scalar.  Rows past the end of an operand read its last
+    // row (their results are never stored).  The launcher guarantees that
+    // every offset fits in 31 bits.
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
     const int lr = lane >> 2;
+    constexpr int kRsrcFlags = 0x00020000;   // raw byte buffer, gfx9 data format
+    auto rsrc = [&](const int8_t* base, int64_t rows, int64_t ld) {
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(base), (short)0, (int)min(rows * ld, (int64_t)0x7FFFFFFF),
+                                                 kRsrcFlags);
+    };
+    const __amdgpu_buffer_rsrc_t rA = rsrc(p.A, p.Mg, p.lda), rB = rsrc(p.B, p.Ng, p.ldb);
+    auto lane_off = [&](int i, int64_t first, int64_t rows, int64_t ld) {
+        const int r = (i * T::kWaves + wv) * 16 + lr;
+        return (uint32_t)(min(first + r, rows - 1) * ld + 16 * ((lane & 3) ^ swz(r)));
+    };
+    uint32_t offA[T::IA], offB[T::IB];
 #pragma unroll
-    for (int i = 0; i < T::IA; ++i) {
-        const int r = (i * T::kWaves + wave) * 16 + lr;
-        rowA[i] = min(m0 + r, p.Mg - 1);
-        chA[i] = 16 * ((lane & 3) ^ swz(r));
-    }
+    for (int i = 0; i < T::IA; ++i) offA[i] = lane_off(i, m0, p.Mg, p.lda);
 #pragma unroll
-    for (int i = 0; i < T::IB; ++i) {
-        const int r = (i * T::kWaves + wave) * 16 + lr;
-        rowB[i] = min(n0 + r, p.Ng - 1);
-        chB[i] = 16 * ((lane & 3) ^ swz(r));
-    }
+    for (int i = 0; i < T::IB; ++i) offB[i] = lane_off(i, n0, p.Ng, p.ldb);
 
     auto issue = [&](int t) {
         int8_t* st = smem + (t % T::STAGES) * T::kStage;
-        const bool ext = fv.is_ext(t, n_main);
-        const int8_t* Ab = ext ? p.extA : p.A;
-        const int8_t* Bb = ext ? p.extB : p.B;
-        const int64_t la = ext ? p.ld_extA : p.lda, lb = ext ? p.ld_extB : p.ldb;
-        const int64_t k0 = ext ? fv.ext_col(t, n_main) : kbeg + (int64_t)(t - fv.h_tiles) * T::BK;
+        if (HORNER && fv.is_ext(t, n_main)) {
+            // appended fold columns (a few tiles): offsets computed here
+            const __amdgpu_buffer_rsrc_t rAe = rsrc(p.extA, p.Mg, p.ld_extA), rBe = rsrc(p.extB, p.Ng, p.ld_extB);
+            const int k0 = (int)fv.ext_col(t, n_main);
+#pragma unroll
+            for (int i = 0; i < T::IA; ++i)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rAe, (lds_void_t*)(st + (i * T::kWaves + wv) * 1024), 16,
+                                                         lane_off(i, m0, p.Mg, p.ld_extA), k0, 0, 0);
+#pragma unroll
+            for (int i = 0; i < T::IB; ++i)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rBe, (lds_void_t*)(st + T::BM * T::BK + (i * T::kWaves + wv) * 1024), 16,
+                    lane_off(i, n0, p.Ng, p.ld_extB), k0, 0, 0);
+            return;
+        }
+        const int k0 = (int)(kbeg + (int64_t)(t - fv.h_tiles) * T::BK);
 #pragma unroll
         for (int i = 0; i < T::IA; ++i)
-            __builtin_amdgcn_global_load_lds((gbl_void_t*)(Ab + rowA[i] * la + chA[i] + k0),
-                                             (lds_void_t*)(st + (i * T::kWaves + wave) * 1024), 16, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void_t*)(st + (i * T::kWaves + wv) * 1024), 16, offA[i],
+                                                     k0, 0, 0);
 #pragma unroll
         for (int i = 0; i < T::IB; ++i)
-            __builtin_amdgcn_global_load_lds((gbl_void_t*)(Bb + rowB[i] * lb + chB[i] + k0),
-                                             (lds_void_t*)(st + T::BM * T::BK + (i * T::kWaves + wave) * 1024),
-                                             16, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_void_t*)(st + T::BM * T::BK + (i * T::kWaves + wv) * 1024),
+                                                     16, offB[i], k0, 0, 0);
     };
 
     acc_t acc[T::FM][T::FN];
@@ -455,65 +491,95 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
 #pragma unroll
             for (int r = 0; r < T::NACC; ++r) acc[i][j][r] = 0;
 
-    auto compute = [&](int t) {
+    // MFMA operands of one K tile, double-buffered (buffer index fixed at
+    // compile time by the two-step unrolled loop below)
+    v4i fa[2][T::KSTEPS][T::FM], fb[2][T::KSTEPS][T::FN];
+    const int lrow = lane % T::MF, lc = lane / T::MF;
+    auto read_frags = [&](int t, auto BUF) {
+        constexpr int buf = decltype(BUF)::value;
         const int8_t* sA = smem + (t % T::STAGES) * T::kStage;
         const int8_t* sB = sA + T::BM * T::BK;
-        const int lrow = lane % T::MF, lc = lane / T::MF;
 #pragma unroll
-        for (int ks = 0; ks < T::BK / T::KS; ++ks) {
+        for (int ks = 0; ks < T::KSTEPS; ++ks) {
             const int c = ks * (T::KS / 16) + lc;   // logical 16-byte chunk of this lane
-            v4i a[T::FM], b[T::FN];
 #pragma unroll
             for (int i = 0; i < T::FM; ++i) {
                 const int r = wm * T::TM + i * T::MF + lrow;
-                a[i] = *reinterpret_cast<const v4i*>(&sA[r * T::BK + 16 * (c ^ swz(r))]);
+                fa[buf][ks][i] = *reinterpret_cast<const v4i*>(&sA[r * T::BK + 16 * (c ^ swz(r))]);
             }
 #pragma unroll
             for (int j = 0; j < T::FN; ++j) {
                 const int r = wn * T::TN + j * T::MF + lrow;
-                b[j] = *reinterpret_cast<const v4i*>(&sB[r * T::BK + 16 * (c ^ swz(r))]);
+                fb[buf][ks][j] = *reinterpret_cast<const v4i*>(&sB[r * T::BK + 16 * (c ^ swz(r))]);
             }
+        }
+    };
+    auto mfmas = [&](auto BUF) {
+        constexpr int buf = decltype(BUF)::value;
+#pragma unroll
+        for (int ks = 0; ks < T::KSTEPS; ++ks)
 #pragma unroll
             for (int i = 0; i < T::FM; ++i)
 #pragma unroll
-                for (int j = 0; j < T::FN; ++j) acc[i][j] = MF::run(b[j], a[i], acc[i][j]);
+                for (int j = 0; j < T::FN; ++j) acc[i][j] = MF::run(fb[buf][ks][j], fa[buf][ks][i], acc[i][j]);
+    };
+    // this wave's loads of a tile are complete once at most `later` younger
+    // tiles remain in flight
+    auto wait_tile = [&](int later) {
+        if (later >= 2) wait_vm<2 * T::kLoads>();
+        else if (later == 1) wait_vm<T::kLoads>();
+        else wait_vm<0>();
+    };
+
+    HornerSteps hs(p);
+    // one K tile: publish tile t + 1, refill the stage tile t - 1 used, read
+    // tile t + 1's operands, then the MFMAs of tile t.  The reads are issued
+    // on the last tile too (of a stale stage, never used), which keeps the
+    // loop body free of branches around LDS reads, so the compiler's counter
+    // waits before the MFMAs leave the new reads in flight.
+    auto step = [&](int t, auto CUR, auto NXT) {
+        wait_tile(min(T::STAGES - 3, n_tiles - 2 - t));
+        __builtin_amdgcn_s_barrier();
+        if (t + T::STAGES - 1 < n_tiles) issue(t + T::STAGES - 1);
+        if (HORNER && (int64_t)t * T::BK == hs.col) {
+            const int sft = hs.advance();
+#pragma unroll
+            for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+                for (int j = 0; j < T::FN; ++j) acc[i][j] = acc[i][j] << sft;
         }
+        read_frags(t + 1, NXT);
+        mfmas(CUR);
+        // issue order: the LDS reads of the next tile spread between the
+        // MFMAs of this one (each group: a share of MFMAs, then one read), so
+        // the matrix cores start on operands that are already in registers
+        constexpr int kReads = T::KSTEPS * (T::FM + T::FN);
+        constexpr int kMfma = T::KSTEPS * T::FM * T::FN;
+        constexpr int kPer = kMfma / kReads;
+#pragma unroll
+        for (int g = 0; g < kReads; ++g) {
+            __builtin_amdgcn_sched_group_barrier(0x008, kPer, 0);   // MFMAs
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);      // one LDS read
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kPer * kReads, 0);
     };
 
     if (n_tiles > 0) {
 #pragma unroll
         for (int s = 0; s < T::STAGES - 1; ++s)
             if (s < n_tiles) issue(s);
-        HornerSteps hs(p);
-        for (int t = 0; t < n_tiles; ++t) {
-            // this wave's loads of tile t are done once at most
-            // min(STAGES - 2, n_tiles - 1 - t) later tiles remain in flight
-            const int later = min(T::STAGES - 2, n_tiles - 1 - t);
-            if (later >= T::STAGES - 2) wait_vm<(T::STAGES - 2) * T::kLoads>();
-            else if (later == 1) wait_vm<T::kLoads>();
-            else wait_vm<0>();
-            __builtin_amdgcn_s_barrier();   // tile t is in LDS for every wave; stage (t-1) is free
-            if (t + T::STAGES - 1 < n_tiles) issue(t + T::STAGES - 1);
-            if ((int64_t)t * T::BK == hs.col) {
-                const int sft = hs.advance(p);
-#pragma unroll
-                for (int i = 0; i < T::FM; ++i)
-#pragma unroll
-                    for (int j = 0; j < T::FN; ++j) acc[i][j] = acc[i][j] << sft;
-            }
-            compute(t);
-            wait_lgkm0();   // every LDS read of this stage has returned before the next barrier
+        wait_tile(min(T::STAGES - 2, n_tiles - 1));
+        __builtin_amdgcn_s_barrier();
+        read_frags(0, std::integral_constant<int, 0>());
+        for (int t = 0; t < n_tiles; t += 2) {
+            step(t, std::integral_constant<int, 0>(), std::integral_constant<int, 1>());
+            if (t + 1 < n_tiles) step(t + 1, std::integral_constant<int, 1>(), std::integral_constant<int, 0>());
         }
     }
 
-    if (fv.fshift) {
-#pragma unroll
-        for (int i = 0; i < T::FM; ++i)
-#pragma unroll
-            for (int j = 0; j < T::FN; ++j) acc[i][j] = acc[i][j] << fv.fshift;
-    }
-
-    // ---- epilogue (same as the register-staged kernel) ----
+    // ---- epilogue (as in the register-staged kernel; the fold's final shift
+    // is applied per element) ----
+    const int fsh = HORNER ? fv.fshift : 0;
     float base = 0.0f, alpha = 0.0f;
     if (p.out && !p.part) {
         const sq_scale gs = *p.gs, os = *p.os;
@@ -537,8 +603,8 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
                 const int64_t jj = n0 + wn * T::TN + j * T::MF +
                                    (T::MF == 32 ? q * 8 + (lane / 32) * 4 : (lane / 16) * 4);
                 if (jj >= p.Ng) continue;
-                const int v0 = acc[i][j][q * 4 + 0], v1 = acc[i][j][q * 4 + 1];
-                const int v2 = acc[i][j][q * 4 + 2], v3 = acc[i][j][q * 4 + 3];
+                const int v0 = acc[i][j][q * 4 + 0] << fsh, v1 = acc[i][j][q * 4 + 1] << fsh;
+                const int v2 = acc[i][j][q * 4 + 2] << fsh, v3 = acc[i][j][q * 4 + 3] << fsh;
                 const int vv[4] = {v0, v1, v2, v3};
                 const bool full = jj + 4 <= p.Ng;
                 if (p.part) {
@@ -578,6 +644,7 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
             }
         }
     }
+#endif
 }
 
 // Appended B columns of the dgrad fold: wext[k, j] = W^T code of the channel
@@ -675,21 +742,27 @@ hipError_t launch_cfg(const GemmArgs& a, int splits, int64_t k_per_split, hipStr
     return hipGetLastError();
 }
 
-template <class T>
+template <class T, bool HORNER>
 hipError_t launch_pipe(const GemmArgs& a, int splits, int64_t k_per_split, hipStream_t s) {
     const int64_t tiles_m = (a.Mg + T::BM - 1) / T::BM, tiles_n = (a.Ng + T::BN - 1) / T::BN;
     if (tiles_m * tiles_n > 0x7FFFFFFF || splits > 65535) return hipErrorInvalidValue;
     dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)splits);
-    hipLaunchKernelGGL(k_gemm_pipe<T>, grid, dim3(T::kThreads), 0, s, a, tiles_m, tiles_n, k_per_split);
+    hipLaunchKernelGGL((k_gemm_pipe<T, HORNER>), grid, dim3(T::kThreads), 0, s, a, tiles_m, tiles_n, k_per_split);
     return hipGetLastError();
 }
 
 // The direct-load pipeline needs 64-byte K tiles that never cross the end of a
-// segment and 16-byte aligned rows.
+// segment, 16-byte aligned rows, and byte offsets (rows * ld + K) that fit
+// the 31 bits of its buffer loads.
 bool pipe_ok(const GemmArgs& a) {
     auto al16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+    auto fits = [](int64_t rows, int64_t ld, int64_t cols) { return rows * ld + cols < ((int64_t)1 << 31); };
     if (a.K % 64 != 0 || a.lda % 16 != 0 || a.ldb % 16 != 0 || !al16(a.A) || !al16(a.B)) return false;
-    if (a.extA && (a.ld_extA % 16 != 0 || a.ld_extB % 16 != 0 || !al16(a.extA) || !al16(a.extB))) return false;
+    if (!fits(a.Mg, a.lda, a.K) || !fits(a.Ng, a.ldb, a.K)) return false;
+    if (a.extA) {
+        if (a.ld_extA % 16 != 0 || a.ld_extB % 16 != 0 || !al16(a.extA) || !al16(a.extB)) return false;
+        if (!fits(a.Mg, a.ld_extA, 0) || !fits(a.Ng, a.ld_extB, 0)) return false;
+    }
     return true;
 }
 
@@ -722,14 +795,17 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     if (use_large(a)) {
         const int64_t ktiles = (a.K + 63) / 64;
         const int64_t kps = std::max<int64_t>(ktiles, 1) * 64;
-        return pipe ? launch_pipe<PipeLarge>(a, 1, kps, s) : launch_cfg<CfgLarge>(a, 1, kps, s);
+        if (!pipe) return launch_cfg<CfgLarge>(a, 1, kps, s);
+        return a.extA ? launch_pipe<PipeLarge, true>(a, 1, kps, s) : launch_pipe<PipeLarge, false>(a, 1, kps, s);
     }
     using T = CfgSmall;
     const int64_t ktiles = (a.K + T::BK - 1) / T::BK;
     int splits = std::max(1, a.splits);
     const int64_t per = splits > 1 ? (ktiles + splits - 1) / splits : std::max<int64_t>(ktiles, 1);
     if (splits > 1 && (ktiles + per - 1) / per != splits) return hipErrorInvalidValue;   // wgrad_splits() avoids this
-    return pipe ? launch_pipe<PipeSmall>(a, splits, per * 64, s) : launch_cfg<T>(a, splits, per * T::BK, s);
+    if (!pipe) return launch_cfg<T>(a, splits, per * T::BK, s);
+    return a.extA ? launch_pipe<PipeSmall, true>(a, splits, per * 64, s)
+                  : launch_pipe<PipeSmall, false>(a, splits, per * 64, s);
 }
 
 hipError_t launch_gather_ext(const int8_t* wq_t, int64_t ld_w, int64_t C_in, const int32_t* layout,
