@@ -105,11 +105,17 @@ __global__ __launch_bounds__(kColThreads) void k_colmax(const float* __restrict_
         int64_t m = m_begin + rl;
         if constexpr (VEC == 4) {
             if (c0 + 4 <= C) {
-                for (; m + 7 * (int64_t)nrl < m_end; m += 8 * (int64_t)nrl) {
-                    float4 v[8];
+                // batches of 8 rows, the next batch in flight while one is reduced
+                const int64_t step = nrl;
+                auto load8 = [&](int64_t mm, float4 (&v)[8]) {
 #pragma unroll
-                    for (int u = 0; u < 8; ++u)
-                        v[u] = *reinterpret_cast<const float4*>(x + (m + u * (int64_t)nrl) * ld + c0);
+                    for (int u = 0; u < 8; ++u) {
+                        const int64_t row = mm + u * step;
+                        v[u] = row < m_end ? *reinterpret_cast<const float4*>(x + row * ld + c0)
+                                           : make_float4(0.f, 0.f, 0.f, 0.f);
+                    }
+                };
+                auto reduce8 = [&](const float4 (&v)[8]) {
 #pragma unroll
                     for (int u = 0; u < 8; ++u) {
                         best[0] = max(best[0], absbits(v[u].x));
@@ -117,14 +123,17 @@ __global__ __launch_bounds__(kColThreads) void k_colmax(const float* __restrict_
                         best[2] = max(best[2], absbits(v[u].z));
                         best[3] = max(best[3], absbits(v[u].w));
                     }
+                };
+                float4 va[8], vb[8];
+                if (m < m_end) load8(m, va);
+                for (; m < m_end; m += 16 * step) {
+                    if (m + 8 * step < m_end) load8(m + 8 * step, vb);
+                    reduce8(va);
+                    if (m + 8 * step >= m_end) break;
+                    if (m + 16 * step < m_end) load8(m + 16 * step, va);
+                    reduce8(vb);
                 }
-                for (; m < m_end; m += nrl) {
-                    const float4 v = *reinterpret_cast<const float4*>(x + m * ld + c0);
-                    best[0] = max(best[0], absbits(v.x));
-                    best[1] = max(best[1], absbits(v.y));
-                    best[2] = max(best[2], absbits(v.z));
-                    best[3] = max(best[3], absbits(v.w));
-                }
+                m = m_end;
             }
         }
         for (; m < m_end; m += nrl) {   // scalar path (and the ragged last vector)
@@ -218,33 +227,60 @@ __global__ __launch_bounds__(kRedThreads) void k_colmax_reduce(const uint32_t* _
     if (threadIdx.x == 0) bmax[blockIdx.x] = r;
 }
 
-// Channel ranges for fewer channels than threads: W channels x L slab lanes,
-// combined through LDS.  Thread tid < C returns r_{tid}; the others 0.
+// Channel ranges for fewer channels than threads: W channel units x L slab
+// lanes, combined through LDS (lanes holds 4 * kFinThreads words).  A unit is
+// 4 channels read as one 16-byte load when C is a multiple of 4, else 1.
+// Thread tid < C returns r_{tid}; the others 0.
 constexpr int kFinThreads = 1024;
 
 __device__ uint32_t small_channel_ranges(const uint32_t* __restrict__ partial, int64_t S, int64_t C,
                                          uint32_t* lanes) {
     const int tid = threadIdx.x;
+    const bool v4 = (C & 3) == 0;
+    const int units = v4 ? (int)(C / 4) : (int)C;
     int W = 1;
-    while (W < C) W <<= 1;
+    while (W < units) W <<= 1;
     const int L = kFinThreads / W;
     const int cl = tid % W, lane = tid / W;
-    uint32_t a[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
-    if (cl < C) {
-        int64_t sl = lane;
-        for (; sl + 7 * (int64_t)L < S; sl += 8 * (int64_t)L) {
+    uint32_t a[4] = {0u, 0u, 0u, 0u};
+    if (cl < units) {
+        if (v4) {
+            const uint32_t* base = partial + 4 * (int64_t)cl;
+            int64_t sl = lane;
+            for (; sl + 7 * (int64_t)L < S; sl += 8 * (int64_t)L) {
+                uint4 v[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) a[u] = max(a[u], partial[(sl + u * (int64_t)L) * C + cl]);
+                for (int u = 0; u < 8; ++u) v[u] = *reinterpret_cast<const uint4*>(base + (sl + u * (int64_t)L) * C);
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    a[0] = max(a[0], v[u].x); a[1] = max(a[1], v[u].y);
+                    a[2] = max(a[2], v[u].z); a[3] = max(a[3], v[u].w);
+                }
+            }
+            for (; sl < S; sl += L) {
+                const uint4 v = *reinterpret_cast<const uint4*>(base + sl * C);
+                a[0] = max(a[0], v.x); a[1] = max(a[1], v.y); a[2] = max(a[2], v.z); a[3] = max(a[3], v.w);
+            }
+        } else {
+            uint32_t b[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+            int64_t sl = lane;
+            for (; sl + 7 * (int64_t)L < S; sl += 8 * (int64_t)L) {
+#pragma unroll
+                for (int u = 0; u < 8; ++u) b[u] = max(b[u], partial[(sl + u * (int64_t)L) * C + cl]);
+            }
+            for (; sl < S; sl += L) b[0] = max(b[0], partial[sl * C + cl]);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) a[0] = max(a[0], b[u]);
         }
-        for (; sl < S; sl += L) a[0] = max(a[0], partial[sl * C + cl]);
     }
 #pragma unroll
-    for (int u = 1; u < 8; ++u) a[0] = max(a[0], a[u]);
-    lanes[tid] = a[0];
+    for (int k = 0; k < 4; ++k) lanes[4 * tid + k] = a[k];
     __syncthreads();
     uint32_t r = 0u;
-    if (tid < C)
-        for (int l = 0; l < L; ++l) r = max(r, lanes[l * W + tid]);
+    if (tid < C) {
+        const int q = v4 ? tid / 4 : tid, k = v4 ? tid % 4 : 0;
+        for (int l = 0; l < L; ++l) r = max(r, lanes[4 * (l * W + q) + k]);
+    }
     __syncthreads();
     return r;
 }
@@ -359,7 +395,7 @@ __global__ __launch_bounds__(kFinThreads) void k_finalize_grad(const uint32_t* _
                                                                int32_t* __restrict__ layout, int64_t ext_max) {
     __shared__ uint32_t shu[16];
     __shared__ int wtot[kFinWaves][kMaxRegions];
-    __shared__ uint32_t lanes[kFinThreads];
+    __shared__ uint32_t lanes[4 * kFinThreads];
     __shared__ FoldPlan P;
     __shared__ int nsh[kMaxRegions];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -376,6 +412,27 @@ __global__ __launch_bounds__(kFinThreads) void k_finalize_grad(const uint32_t* _
     const sq_scale sc = make_scale(mb, (float)cfg.Q);
     if (tid == 0) *scale = sc;
     const bool flagged = sc.flags != 0u;
+
+    int32_t* ext = layout + kLayoutHeader;
+    int32_t* desc = ext + ext_max;
+    if (ext_max == 0) {
+        // every shift fits int8 (N_G - 1 <= T): one window at base 0, the
+        // code of channel c stored as code << sh_c in its own column
+        for (int64_t c = tid; c < C; c += kFinThreads) {
+            const uint32_t rb = C < kFinThreads ? r_small : rbits[c];
+            const int g = flagged ? Sh : group_of(__uint_as_float(rb), sc.r_max, cfg.num_groups);
+            group[c] = (uint8_t)g;
+            desc[c] = Sh - g;
+        }
+        if (tid < kLayoutHeader) {
+            int v = 0;
+            if (tid == kLayNR) v = 1;
+            else if (tid == kLayBase) v = (int)fold_ext_base(C);
+            else if (tid > kLayStart && tid < kLayStart + kMaxRegions) v = 0x7FFFFFFF;
+            layout[tid] = v;
+        }
+        return;
+    }
 
     // groups and the number of channels at each shift
     int hist[kMaxRegions];
@@ -405,8 +462,6 @@ __global__ __launch_bounds__(kFinThreads) void k_finalize_grad(const uint32_t* _
 
     // place of every channel: descriptor ((pos + 1) << 4) | t, and the
     // appended-column list
-    int32_t* ext = layout + kLayoutHeader;
-    int32_t* desc = ext + ext_max;
     const int nr = P.nr, main_r = P.main_r;
     const uint64_t below = (1ull << lane) - 1ull;
     for (int64_t c0 = 0; c0 < C; c0 += kFinThreads) {
@@ -471,7 +526,7 @@ __global__ __launch_bounds__(kFinThreads) void k_finalize_tensor(const uint32_t*
                                                                  int64_t C, int Q, const uint32_t* __restrict__ bmax,
                                                                  int64_t nb, sq_scale* __restrict__ scale) {
     __shared__ uint32_t shu[16];
-    __shared__ uint32_t lanes[kFinThreads];
+    __shared__ uint32_t lanes[4 * kFinThreads];
     uint32_t mb = 0u;
     if (C < kFinThreads) mb = small_channel_ranges(partial, S, C, lanes);
     else
@@ -481,96 +536,97 @@ __global__ __launch_bounds__(kFinThreads) void k_finalize_tensor(const uint32_t*
 }
 
 // ---------------------------------------------------------------------------
-// Quantize.  Thread (tr, tc4) of a block handles 16 consecutive rows x 4
-// consecutive channels of a row tile: channels c0 = tile_c + 4 * tc4 and rows
-// m_base = tile_m + 16 * tr.  It writes the shift-folded codes of each row as
-// one 4-byte store into q_fold (a wave covers whole 128-byte lines) and the 16
-// codes of each of its channels as one 16-byte store into q_t, so the
-// transpose needs no LDS.  tc4n (a power of two <= 32) threads span the
-// channel tile; a row tile has 16 * kBlock / tc4n rows.
+// Quantize.  A block quantizes tiles of TR rows x TC channels (64 or 128 each,
+// smaller where the tensor would give too few tiles to fill the chip),
+// striding over the tiles; neighbouring
+// channel tiles of a row tile go to consecutive blocks.  Thread (rq, cq)
+// handles, in each pass over the tile, the 4 consecutive rows 4 rq .. 4 rq + 3
+// of the channel quad 4 cq .. 4 cq + 3: one 16-byte load per row, the row's 4
+// shift-folded codes as one 4-byte store into q_fold (a wave writes whole
+// row segments), and each channel's 4 codes as one word into an LDS tile
+// [channel][row], from which the block writes q_t as 16-byte chunks, so a
+// 128-row tile completes whole 128-byte lines of q_t.  Low register use keeps many
+// waves per SIMD in flight to hide the memory latency.
 // ---------------------------------------------------------------------------
 constexpr int kBlock = 256;
-constexpr int kQR = 16;   // rows per thread
 
-template <int VEC, bool SR>
+template <int TC, int kTR, int VEC, bool SR>
 __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x, int64_t M, int64_t C,
                                                      int64_t ld, const uint8_t* __restrict__ group,
-                                                     const sq_scale* __restrict__ scale, QuantCfg cfg, int tc4n,
+                                                     const sq_scale* __restrict__ scale, QuantCfg cfg,
                                                      int8_t* __restrict__ q_fold, int64_t ld_fold,
                                                      int8_t* __restrict__ q_t, int64_t ld_t,
                                                      const int32_t* __restrict__ desc, int64_t ext_base) {
-    const int tid = threadIdx.x;
-    const int tc4 = tid & (tc4n - 1), tr = tid / tc4n;
-    const int rows_per_tile = kQR * (kBlock / tc4n);
-    const int64_t c0 = (int64_t)blockIdx.x * 4 * tc4n + 4 * tc4;
-    const int64_t row_tiles = (M + rows_per_tile - 1) / rows_per_tile;
+    constexpr int QD = TC / 4;            // channel quads per tile
+    constexpr int RQ = kBlock / QD;       // row quads per pass
+    constexpr int RP = 4 * RQ;            // rows per pass
+    constexpr int PASSES = kTR / RP;
+    constexpr int TW = kTR / 4 + 1;       // LDS words per channel row (padded)
+    __shared__ uint32_t tq[TC * TW];
+    const int tid = threadIdx.x, cq = tid % QD, rq = tid / QD;
+    const int64_t ctiles = (C + TC - 1) / TC, rtiles = (M + kTR - 1) / kTR;
 
     const sq_scale sc = *scale;
     const bool zero = sc.flags != 0u;
     const float Qf = (float)cfg.Q;
-
-    float s[4];
-    int t[4], pos[4];   // fold: code << t in main column c (pos < 0) or appended column pos
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int64_t c = c0 + j;
-        const int g = (group && c < C) ? (int)group[c] : 0;
-        s[j] = __fmul_rn(sc.inv, pow2f(g));
-        const int d = (desc && c < C) ? desc[c] : 0;
-        t[j] = d & 15;
-        pos[j] = (d >> 4) - 1;
-    }
     const bool sr_vec = SR && ((C & 3) == 0);   // 4 channels share one Philox block
 
-    for (int64_t rt = blockIdx.y; rt < row_tiles; rt += gridDim.y) {
-        const int64_t m_base = rt * rows_per_tile + (int64_t)kQR * tr;
-        if (c0 < C && m_base < M) {
-            float v[kQR][4];
+    for (int64_t tile = blockIdx.x; tile < ctiles * rtiles; tile += gridDim.x) {
+        const int64_t ct = tile % ctiles, rt = tile / ctiles;
+        const int64_t c0 = ct * TC + 4 * cq, m_tile = rt * kTR;
+        const bool full_vec = VEC == 4 && c0 + 4 <= C;
+        float s[4];
+        int t[4], pos[4];   // fold: code << t in main column c (pos < 0) or appended column pos
 #pragma unroll
-            for (int i = 0; i < kQR; ++i) {
-                const int64_t m = m_base + i;
+        for (int j = 0; j < 4; ++j) {
+            const int64_t c = c0 + j;
+            const int g = (group && c < C) ? (int)group[c] : 0;
+            s[j] = __fmul_rn(sc.inv, pow2f(g));
+            const int d = (desc && c < C) ? desc[c] : 0;
+            t[j] = d & 15;
+            pos[j] = (d >> 4) - 1;
+        }
+#pragma unroll
+        for (int p = 0; p < PASSES; ++p) {
+            const int r0 = p * RP + 4 * rq;   // first of this thread's rows within the tile
+            float v[4][4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int64_t m = m_tile + r0 + i;
                 v[i][0] = v[i][1] = v[i][2] = v[i][3] = 0.f;
-                if (m < M) {
-                    bool done = false;
-                    if constexpr (VEC == 4) {
-                        if (c0 + 4 <= C) {
-                            const float4 f = *reinterpret_cast<const float4*>(x + m * ld + c0);
-                            v[i][0] = f.x; v[i][1] = f.y; v[i][2] = f.z; v[i][3] = f.w;
-                            done = true;
-                        }
-                    }
-                    if (!done) {
+                if (m < M && c0 < C) {
+                    if (full_vec) {
+                        const float4 f = *reinterpret_cast<const float4*>(x + m * ld + c0);
+                        v[i][0] = f.x; v[i][1] = f.y; v[i][2] = f.z; v[i][3] = f.w;
+                    } else {
 #pragma unroll
                         for (int j = 0; j < 4; ++j)
                             if (c0 + j < C) v[i][j] = x[m * ld + c0 + j];
                     }
                 }
             }
-            uint32_t colw[4][kQR / 4];   // channel j, rows 4w .. 4w + 3 packed little-endian
+            uint32_t colw[4] = {0u, 0u, 0u, 0u};   // channel j: rows r0 .. r0 + 3, little-endian
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-#pragma unroll
-                for (int w = 0; w < kQR / 4; ++w) colw[j][w] = 0u;
-#pragma unroll
-            for (int i = 0; i < kQR; ++i) {
-                const int64_t m = m_base + i;
+            for (int i = 0; i < 4; ++i) {
+                const int64_t m = m_tile + r0 + i;
                 uint32_t u[4] = {0u, 0u, 0u, 0u};
-                if (SR && m < M) {
+                if (SR && m < M && c0 < C) {
                     if (sr_vec) {
                         const U4 w = philox_block((uint64_t)(m * C + c0) >> 2, cfg);
                         u[0] = w.x >> 8; u[1] = w.y >> 8; u[2] = w.z >> 8; u[3] = w.w >> 8;
                     } else {
 #pragma unroll
-                        for (int j = 0; j < 4; ++j) u[j] = sr_uniform24((uint64_t)(m * C + c0 + j), cfg);
+                        for (int j = 0; j < 4; ++j)
+                            if (c0 + j < C) u[j] = sr_uniform24((uint64_t)(m * C + c0 + j), cfg);
                     }
                 }
                 int code[4];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     code[j] = (zero || m >= M || c0 + j >= C) ? 0 : quant_one<SR>(v[i][j], s[j], Qf, u[j]);
-                    colw[j][i / 4] |= (uint32_t)(uint8_t)code[j] << (8 * (i % 4));
+                    colw[j] |= (uint32_t)(uint8_t)code[j] << (8 * i);
                 }
-                if (q_fold && m < M) {
+                if (q_fold && m < M && c0 < C) {
                     int8_t* row = q_fold + m * ld_fold;
                     uint32_t word = 0u;
 #pragma unroll
@@ -590,17 +646,28 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
             }
             if (q_t) {
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    if (c0 + j >= C) continue;
-                    int8_t* dst = q_t + (c0 + j) * ld_t + m_base;
-                    if (m_base + kQR <= M) {
-                        *reinterpret_cast<uint4*>(dst) = make_uint4(colw[j][0], colw[j][1], colw[j][2], colw[j][3]);
+                for (int j = 0; j < 4; ++j) tq[(4 * cq + j) * TW + r0 / 4] = colw[j];
+            }
+        }
+        if (q_t) {
+            __syncthreads();
+            // channel row ch of the tile: kTR bytes = kTR / 16 chunks of 16 bytes
+            constexpr int CPR = kTR / 16;
+#pragma unroll
+            for (int id = tid; id < TC * CPR; id += kBlock) {
+                const int ch = id / CPR, part = id % CPR;
+                const int64_t c = ct * TC + ch, m = m_tile + 16 * part;
+                if (c < C && m < M) {
+                    const uint32_t* src = &tq[ch * TW + 4 * part];
+                    int8_t* dst = q_t + c * ld_t + m;
+                    if (m + 16 <= M) {
+                        *reinterpret_cast<uint4*>(dst) = make_uint4(src[0], src[1], src[2], src[3]);
                     } else {
-                        for (int i = 0; i < (int)(M - m_base); ++i)
-                            dst[i] = (int8_t)(colw[j][i / 4] >> (8 * (i % 4)));
+                        for (int i = 0; i < (int)(M - m); ++i) dst[i] = (int8_t)(src[i / 4] >> (8 * (i % 4)));
                     }
                 }
             }
+            __syncthreads();
         }
     }
 }
@@ -682,29 +749,38 @@ hipError_t launch_finalize_tensor(const uint32_t* partial, int64_t slabs, int64_
     return hipGetLastError();
 }
 
+constexpr int64_t kQuantMaxBlocks = 4096;   // grid-stride beyond this
+constexpr int64_t kQuantMinTiles = 1024;    // four blocks per CU
+
 hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, const uint8_t* group,
                            const sq_scale* scale, const QuantCfg& cfg, int8_t* q_fold, int64_t ld_fold,
                            int8_t* q_t, int64_t ld_t, const int32_t* desc, hipStream_t s) {
     if (M <= 0 || C <= 0) return hipSuccess;
     const bool vec = ((ld & 3) == 0) && ((reinterpret_cast<uintptr_t>(x) & 15) == 0);
     const bool sr = cfg.round_mode == SQ_ROUND_STOCHASTIC;
-    int tc4n = 1;
-    while (tc4n < 32 && 4 * tc4n < C) tc4n <<= 1;
-    const int64_t rows_per_tile = kQR * (kBlock / tc4n);
-    dim3 grid((unsigned)((C + 4 * tc4n - 1) / (4 * tc4n)),
-              (unsigned)std::min<int64_t>((M + rows_per_tile - 1) / rows_per_tile, 65535));
-    if (vec && sr)
-        hipLaunchKernelGGL((k_quantize<4, true>), grid, dim3(kBlock), 0, s, x, M, C, ld, group, scale, cfg, tc4n,
-                           q_fold, ld_fold, q_t, ld_t, desc, fold_ext_base(C));
-    else if (vec)
-        hipLaunchKernelGGL((k_quantize<4, false>), grid, dim3(kBlock), 0, s, x, M, C, ld, group, scale, cfg, tc4n,
-                           q_fold, ld_fold, q_t, ld_t, desc, fold_ext_base(C));
-    else if (sr)
-        hipLaunchKernelGGL((k_quantize<1, true>), grid, dim3(kBlock), 0, s, x, M, C, ld, group, scale, cfg, tc4n,
-                           q_fold, ld_fold, q_t, ld_t, desc, fold_ext_base(C));
-    else
-        hipLaunchKernelGGL((k_quantize<1, false>), grid, dim3(kBlock), 0, s, x, M, C, ld, group, scale, cfg, tc4n,
-                           q_fold, ld_fold, q_t, ld_t, desc, fold_ext_base(C));
+    // 128 x 128 tiles where the tensor gives enough of them to fill the chip
+    auto n_tiles = [&](int64_t tc, int64_t tr) { return ((C + tc - 1) / tc) * ((M + tr - 1) / tr); };
+    int tc = C <= 64 ? 64 : 128, tr = 128;
+    if (n_tiles(tc, tr) < kQuantMinTiles) tr = 64;
+    if (n_tiles(tc, tr) < kQuantMinTiles) tc = 64;
+    const dim3 grid((unsigned)std::min<int64_t>(n_tiles(tc, tr), kQuantMaxBlocks));
+    const int64_t eb = fold_ext_base(C);
+#define SQ_LAUNCH_QUANT(TC, TR)                                                                                  \
+    do {                                                                                                         \
+        if (vec && sr) hipLaunchKernelGGL((k_quantize<TC, TR, 4, true>), grid, dim3(kBlock), 0, s, x, M, C, ld,  \
+                                          group, scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb);              \
+        else if (vec) hipLaunchKernelGGL((k_quantize<TC, TR, 4, false>), grid, dim3(kBlock), 0, s, x, M, C, ld,  \
+                                         group, scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb);               \
+        else if (sr) hipLaunchKernelGGL((k_quantize<TC, TR, 1, true>), grid, dim3(kBlock), 0, s, x, M, C, ld,    \
+                                        group, scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb);                \
+        else hipLaunchKernelGGL((k_quantize<TC, TR, 1, false>), grid, dim3(kBlock), 0, s, x, M, C, ld, group,    \
+                                scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb);                               \
+    } while (0)
+    if (tc == 64 && tr == 64) SQ_LAUNCH_QUANT(64, 64);
+    else if (tc == 64) SQ_LAUNCH_QUANT(64, 128);
+    else if (tr == 64) SQ_LAUNCH_QUANT(128, 64);
+    else SQ_LAUNCH_QUANT(128, 128);
+#undef SQ_LAUNCH_QUANT
     return hipGetLastError();
 }
 
