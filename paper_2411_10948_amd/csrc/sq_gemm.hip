@@ -398,6 +398,7 @@ struct PipeCfg {
 using PipeLarge = PipeCfg<256, 256, 4, 2, 16, 4>;   // 128 KB of LDS, one block per CU
 using PipeWide = PipeCfg<256, 256, 2, 2, 16, 4>;    // 4 waves of 128 x 128: half the LDS reads per MFMA
 using PipeSmall = PipeCfg<128, 128, 2, 2, 16, 4>;   // 64 KB of LDS
+using PipeSkinny = PipeCfg<64, 192, 2, 2, 16, 4>;   // at most 64 output rows (wgrad of narrow layers)
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
@@ -661,60 +662,92 @@ __global__ void k_gather_ext(const int8_t* __restrict__ wq_t, int64_t ld_w, int6
 }
 
 // Sum of the split-K partial tiles ws [splits, Mg, Ng] (int32 addition is
-// exact and order-free), then the same epilogue as the GEMM.
-__global__ void k_splitk_reduce(const int32_t* __restrict__ ws, int splits, int64_t Mg, int64_t Ng,
-                                int32_t* __restrict__ acc, int64_t ld_acc, float* __restrict__ out, int64_t ld_out,
-                                int epi_mode, const uint8_t* __restrict__ group, const sq_scale* __restrict__ gs,
-                                const sq_scale* __restrict__ os, int num_groups) {
+// exact and order-free), then the same epilogue as the GEMM.  A block of
+// kRedThreads covers kRedThreads / lanes groups of 4 consecutive outputs; the
+// `lanes` threads of a group (a power of two, about a quarter of the splits,
+// at most 16) read every lanes-th split, and are combined in LDS.
+constexpr int kRedThreads = 256;
+
+__global__ __launch_bounds__(kRedThreads) void k_splitk_reduce(
+    const int32_t* __restrict__ ws, int splits, int lanes, int64_t Mg, int64_t Ng, int32_t* __restrict__ acc,
+    int64_t ld_acc, float* __restrict__ out, int64_t ld_out, int epi_mode, const uint8_t* __restrict__ group,
+    const sq_scale* __restrict__ gs, const sq_scale* __restrict__ os, int num_groups) {
+    __shared__ int4 part[kRedThreads];
     const int64_t plane = Mg * Ng;
+    const int items = kRedThreads / lanes;
+    const int it = threadIdx.x % items, sl = threadIdx.x / items;
+    const int64_t e = 4 * ((int64_t)blockIdx.x * items + it);   // outputs e .. e + 3 of the plane
+    const bool vec = (Ng & 3) == 0;
+    int4 sum = make_int4(0, 0, 0, 0);
+    if (e < plane) {
+        if (vec) {
+            int s = sl;
+            for (; s + 3 * lanes < splits; s += 4 * lanes) {
+                int4 v[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const int4*>(ws + (int64_t)(s + u * lanes) * plane + e);
+#pragma unroll
+                for (int u = 0; u < 4; ++u) { sum.x += v[u].x; sum.y += v[u].y; sum.z += v[u].z; sum.w += v[u].w; }
+            }
+            for (; s < splits; s += lanes) {
+                const int4 v = *reinterpret_cast<const int4*>(ws + (int64_t)s * plane + e);
+                sum.x += v.x; sum.y += v.y; sum.z += v.z; sum.w += v.w;
+            }
+        } else {
+            int t[4] = {0, 0, 0, 0};
+            for (int s = sl; s < splits; s += lanes)
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if (e + u < plane) t[u] += ws[(int64_t)s * plane + e + u];
+            sum = make_int4(t[0], t[1], t[2], t[3]);
+        }
+    }
+    if (lanes > 1) {
+        part[threadIdx.x] = sum;
+        __syncthreads();
+        if (sl != 0) return;
+        for (int l = 1; l < lanes; ++l) {
+            const int4 v = part[l * items + it];
+            sum.x += v.x; sum.y += v.y; sum.z += v.z; sum.w += v.w;
+        }
+    }
+    if (e >= plane) return;
     float base = 0.0f, alpha = 0.0f;
     if (out) {
         base = __fmul_rn(gs->step, os->step);
         alpha = __fmul_rn(base, pow2f(-(num_groups - 1)));
     }
-    const bool vec = ((Ng & 3) == 0);
-    const int64_t n_items = vec ? plane / 4 : plane;
-    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < n_items;
-         q += (int64_t)gridDim.x * blockDim.x) {
-        if (vec) {
-            const int64_t e = q * 4;
-            int4 a[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) a[u] = make_int4(0, 0, 0, 0);
-            int s = 0;
-            for (; s + 4 <= splits; s += 4) {
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const int4 v = *reinterpret_cast<const int4*>(ws + (int64_t)(s + u) * plane + e);
-                    a[u].x += v.x; a[u].y += v.y; a[u].z += v.z; a[u].w += v.w;
-                }
-            }
-            for (; s < splits; ++s) {
-                const int4 v = *reinterpret_cast<const int4*>(ws + (int64_t)s * plane + e);
-                a[0].x += v.x; a[0].y += v.y; a[0].z += v.z; a[0].w += v.w;
-            }
-            const int t[4] = {a[0].x + a[1].x + a[2].x + a[3].x, a[0].y + a[1].y + a[2].y + a[3].y,
-                              a[0].z + a[1].z + a[2].z + a[3].z, a[0].w + a[1].w + a[2].w + a[3].w};
-            const int64_t i = e / Ng, j = e % Ng;
-            if (acc) {
-#pragma unroll
-                for (int u = 0; u < 4; ++u) acc[i * ld_acc + j + u] = t[u];
-            }
-            if (out) {
-                const float sc = epi_mode == 1 ? __fmul_rn(base, pow2f(-(int)group[i])) : alpha;
-#pragma unroll
-                for (int u = 0; u < 4; ++u) out[i * ld_out + j + u] = __fmul_rn((float)t[u], sc);
-            }
-        } else {
-            int t = 0;
-            for (int s = 0; s < splits; ++s) t += ws[(int64_t)s * plane + q];
-            const int64_t i = q / Ng, j = q % Ng;
-            if (acc) acc[i * ld_acc + j] = t;
-            if (out) {
-                const float sc = epi_mode == 1 ? __fmul_rn(base, pow2f(-(int)group[i])) : alpha;
-                out[i * ld_out + j] = __fmul_rn((float)t, sc);
-            }
+    const int t[4] = {sum.x, sum.y, sum.z, sum.w};
+    int64_t i = e / Ng, j = e - i * Ng;   // a group of 4 spans two rows only when Ng % 4 != 0
+    if (vec) {
+        const float sc = out && epi_mode == 1 ? __fmul_rn(base, pow2f(-(int)group[i])) : alpha;
+        if (acc) {
+            int32_t* dst = acc + i * ld_acc + j;
+            if (((ld_acc & 3) == 0) && ((reinterpret_cast<uintptr_t>(acc) & 15) == 0))
+                *reinterpret_cast<int4*>(dst) = sum;
+            else
+                for (int u = 0; u < 4; ++u) dst[u] = t[u];
         }
+        if (out) {
+            float* dst = out + i * ld_out + j;
+            const float f[4] = {__fmul_rn((float)t[0], sc), __fmul_rn((float)t[1], sc), __fmul_rn((float)t[2], sc),
+                                __fmul_rn((float)t[3], sc)};
+            if (((ld_out & 3) == 0) && ((reinterpret_cast<uintptr_t>(out) & 15) == 0))
+                *reinterpret_cast<float4*>(dst) = make_float4(f[0], f[1], f[2], f[3]);
+            else
+                for (int u = 0; u < 4; ++u) dst[u] = f[u];
+        }
+        return;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        if (e + u >= plane) break;
+        if (acc) acc[i * ld_acc + j] = t[u];
+        if (out) {
+            const float sc = epi_mode == 1 ? __fmul_rn(base, pow2f(-(int)group[i])) : alpha;
+            out[i * ld_out + j] = __fmul_rn((float)t[u], sc);
+        }
+        if (++j == Ng) { j = 0; ++i; }
     }
 }
 
@@ -766,25 +799,35 @@ bool pipe_ok(const GemmArgs& a) {
     return true;
 }
 
-// Large tiles only where the product fills the chip with them.
-bool use_large(const GemmArgs& a) {
-    const int64_t tiles = ((a.Mg + CfgLarge::BM - 1) / CfgLarge::BM) * ((a.Ng + CfgLarge::BN - 1) / CfgLarge::BN);
-    return a.splits <= 1 && a.K >= 1024 && tiles >= 256;
+// Tile shape of a product: large tiles where there are enough of them to fill
+// most of the chip and K is long, a 64-row tile for products with at most 64
+// output rows, 128 x 128 otherwise.
+enum class Pick { kLarge, kSmall, kSkinny };
+
+int64_t tiles_of(const GemmArgs& a, int bm, int bn) { return ((a.Mg + bm - 1) / bm) * ((a.Ng + bn - 1) / bn); }
+
+Pick pick(const GemmArgs& a) {
+    if (a.splits <= 1 && a.K >= 1024 && tiles_of(a, PipeLarge::BM, PipeLarge::BN) >= 128) return Pick::kLarge;
+    if (a.Mg <= 64 && !a.extA) return Pick::kSkinny;
+    return Pick::kSmall;
 }
 
 }  // namespace
 
+// Split-K factor of the weight-gradient product: enough blocks for about two
+// per CU, at least 8 K tiles per split, no empty split.  The partial tiles do
+// not depend on the tile shape, so any kernel can consume this factor.
 int wgrad_splits(int64_t M, int64_t C_out, int64_t C_in) {
-    using T = CfgSmall;
     GemmArgs probe{};
     probe.Mg = C_out; probe.Ng = C_in; probe.K = M; probe.splits = 1;
-    if (use_large(probe)) return 1;
-    const int64_t tiles = ((C_out + T::BM - 1) / T::BM) * ((C_in + T::BN - 1) / T::BN);
-    const int64_t ktiles = (M + T::BK - 1) / T::BK;
+    const Pick p = pick(probe);
+    if (p == Pick::kLarge) return 1;
+    const int64_t tiles = p == Pick::kSkinny ? tiles_of(probe, PipeSkinny::BM, PipeSkinny::BN)
+                                             : tiles_of(probe, PipeSmall::BM, PipeSmall::BN);
+    const int64_t ktiles = (M + 63) / 64;
     int64_t splits = (512 + tiles - 1) / tiles;
     splits = std::min(splits, std::max<int64_t>(1, ktiles / 8));
     splits = std::max<int64_t>(1, std::min<int64_t>(splits, 65535));
-    // no empty splits
     const int64_t per = (ktiles + splits - 1) / splits;
     return (int)((ktiles + per - 1) / per);
 }
@@ -792,18 +835,19 @@ int wgrad_splits(int64_t M, int64_t C_out, int64_t C_in) {
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     if (a.Mg <= 0 || a.Ng <= 0) return hipSuccess;
     const bool pipe = pipe_ok(a);
-    if (use_large(a)) {
+    const Pick p = pick(a);
+    if (p == Pick::kLarge) {
         const int64_t ktiles = (a.K + 63) / 64;
         const int64_t kps = std::max<int64_t>(ktiles, 1) * 64;
         if (!pipe) return launch_cfg<CfgLarge>(a, 1, kps, s);
         return a.extA ? launch_pipe<PipeLarge, true>(a, 1, kps, s) : launch_pipe<PipeLarge, false>(a, 1, kps, s);
     }
-    using T = CfgSmall;
-    const int64_t ktiles = (a.K + T::BK - 1) / T::BK;
-    int splits = std::max(1, a.splits);
+    const int64_t ktiles = (a.K + 63) / 64;   // every configuration below has 64-byte K tiles
+    const int splits = std::max(1, a.splits);
     const int64_t per = splits > 1 ? (ktiles + splits - 1) / splits : std::max<int64_t>(ktiles, 1);
     if (splits > 1 && (ktiles + per - 1) / per != splits) return hipErrorInvalidValue;   // wgrad_splits() avoids this
-    if (!pipe) return launch_cfg<T>(a, splits, per * T::BK, s);
+    if (!pipe) return launch_cfg<CfgSmall>(a, splits, per * 64, s);
+    if (p == Pick::kSkinny) return launch_pipe<PipeSkinny, false>(a, splits, per * 64, s);
     return a.extA ? launch_pipe<PipeSmall, true>(a, splits, per * 64, s)
                   : launch_pipe<PipeSmall, false>(a, splits, per * 64, s);
 }
@@ -818,10 +862,14 @@ hipError_t launch_gather_ext(const int8_t* wq_t, int64_t ld_w, int64_t C_in, con
 
 hipError_t launch_splitk_reduce(const int32_t* ws, int splits, const GemmArgs& a, hipStream_t s) {
     if (a.Mg <= 0 || a.Ng <= 0) return hipSuccess;
-    const int64_t items = (a.Ng & 3) == 0 ? a.Mg * a.Ng / 4 : a.Mg * a.Ng;
-    const unsigned blocks = (unsigned)std::min<int64_t>((items + 255) / 256, 2048);
-    hipLaunchKernelGGL(k_splitk_reduce, dim3(blocks), dim3(256), 0, s, ws, splits, a.Mg, a.Ng, a.acc, a.ld_acc,
-                       a.out, a.ld_out, a.epi_mode, a.group, a.gs, a.os, a.num_groups);
+    int lanes = 1;
+    while (lanes < 16 && 4 * (2 * lanes) <= splits) lanes *= 2;
+    const int items = kRedThreads / lanes;
+    const int64_t groups = (a.Mg * a.Ng + 3) / 4;
+    const int64_t blocks = (groups + items - 1) / items;
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)blocks), dim3(kRedThreads), 0, s, ws, splits, lanes, a.Mg,
+                       a.Ng, a.acc, a.ld_acc, a.out, a.ld_out, a.epi_mode, a.group, a.gs, a.os, a.num_groups);
     return hipGetLastError();
 }
 

@@ -403,6 +403,18 @@ def test_wgrad_split_k(sq):
     check_layer(sq, dY, W, X, 4, 4, dgrad_rows=[3, 19998], want_acc=False)
 
 
+@pytest.mark.parametrize("shape", [(4096, 40, 200), (8192, 64, 197), (2048, 1, 64), (16384, 64, 576)])
+def test_wgrad_narrow_outputs(sq, shape):
+    # at most 64 output rows and a token count that is a multiple of 64: the
+    # 64-row tile with split-K, and the reduce with and without 4-aligned rows
+    M, C_out, C_in = shape
+    rng = np.random.default_rng(C_in)
+    dY = _grad(M, C_out, seed=C_out)
+    W = (rng.standard_normal((C_out, C_in)) * 0.05).astype(np.float32)
+    X = np.maximum(rng.standard_normal((M, C_in)), 0).astype(np.float32)
+    check_layer(sq, dY, W, X, 4, 4, dgrad_rows=[0, 1, M // 2, M - 1])
+
+
 def test_degenerate_layers(sq):
     rng = np.random.default_rng(2)
     W = (rng.standard_normal((40, 24)) * 0.02).astype(np.float32)
