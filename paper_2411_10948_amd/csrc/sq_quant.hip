@@ -320,55 +320,76 @@ struct FoldPlan {
     int run[kMaxRegions];         // channels ranked so far
 };
 
-__device__ void make_fold_plan(const int* n, int S, int T, int64_t C, FoldPlan& P) {
-    auto count = [&](int lo, int hi) {
-        int c = 0;
-        for (int s = lo; s <= hi; ++s) c += n[s];
-        return c;
-    };
-    // the window [B, B + T] holding the most channels stays in the main columns
+// The plan is computed by one thread in registers (every loop has a
+// compile-time bound of kMaxRegions shift values) and stored to LDS once.
+// Window of shift value s: key 0 for the main window [B*, B* + T], key j > 0
+// for [B* + j (T + 1), ...] above it, key -j for the j-th window below it
+// (its base clipped at 0).  Regions are the non-empty windows (and always the
+// main one) in descending key order, which is descending base.
+__device__ void make_fold_plan(const int* n_lds, int S, int T, int64_t C, FoldPlan& P) {
+    int n[kMaxRegions];
+#pragma unroll
+    for (int s = 0; s < kMaxRegions; ++s) n[s] = s <= S ? n_lds[s] : 0;
+    // the window [B, B + T] holding the most channels (lowest B on ties)
     int bstar = 0, best = -1;
-    for (int B = 0; B <= max(0, S - T); ++B) {
-        const int c = count(B, min(S, B + T));
+#pragma unroll
+    for (int B = 0; B < kMaxRegions; ++B) {
+        if (B > (S - T > 0 ? S - T : 0)) break;
+        int c = 0;
+#pragma unroll
+        for (int s = 0; s < kMaxRegions; ++s) c += (s >= B && s <= B + T) ? n[s] : 0;
         if (c > best) { best = c; bstar = B; }
     }
-    P.nr = 0;
-    auto add = [&](int lo, int hi) {
-        const int r = P.nr++;
-        P.base[r] = lo;
-        P.cnt[r] = count(lo, hi);
-        for (int s = lo; s <= hi; ++s) P.win_of[s] = r;
-    };
-    // descending base: windows above the main one (highest first), the main
-    // window, then the windows below it; empty windows are dropped
-    int top = bstar + T + 1;
-    while (top + T + 1 <= S) top += T + 1;
-    for (int lo = top; lo > bstar + T; lo -= T + 1)
-        if (count(lo, min(S, lo + T)) > 0) add(lo, min(S, lo + T));
-    P.main_r = P.nr;
-    add(bstar, min(S, bstar + T));
-    for (int hi = bstar - 1; hi >= 0;) {
-        const int lo = max(0, hi - T);
-        if (count(lo, hi) > 0) add(lo, hi);
-        hi = lo - 1;
+    auto key_of = [&](int s) { return s >= bstar ? (s - bstar) / (T + 1) : -1 - (bstar - 1 - s) / (T + 1); };
+    // channels per key, keys -7 .. 7
+    int kc[2 * kMaxRegions - 1];
+#pragma unroll
+    for (int k = 0; k < 2 * kMaxRegions - 1; ++k) kc[k] = 0;
+#pragma unroll
+    for (int s = 0; s < kMaxRegions; ++s) {
+        const int key = key_of(s) + (kMaxRegions - 1);
+#pragma unroll
+        for (int k = 0; k < 2 * kMaxRegions - 1; ++k) kc[k] += (k == key && s <= S) ? n[s] : 0;
     }
-    int flat = 0, ext = 0;
-    P.H = 0;
-    for (int r = 0; r < P.nr; ++r) {
+    // regions in descending key order
+    int nr = 0, main_r = 0, flat = 0, ext = 0, H = 0;
+    int region_of_key[2 * kMaxRegions - 1];
+#pragma unroll
+    for (int k = 2 * kMaxRegions - 2; k >= 0; --k) {
+        const int key = k - (kMaxRegions - 1);
+        region_of_key[k] = -1;
+        if (!(kc[k] > 0 || key == 0)) continue;
+        const int lo = key >= 0 ? bstar + key * (T + 1) : max(0, bstar + key * (T + 1));
+        const int r = nr++;
+        region_of_key[k] = r;
+        P.base[r] = lo;
+        P.cnt[r] = kc[k];
         P.flat[r] = flat;
         P.run[r] = 0;
-        if (r == P.main_r) {
+        if (key == 0) {
+            main_r = r;
             P.ext_start[r] = -1;
-            P.H = ext;
+            H = ext;
             flat += (int)round_up(C, kFoldPad);
         } else {
             P.ext_start[r] = ext;
-            ext += (int)round_up(P.cnt[r], kFoldPad);
-            flat += (int)round_up(P.cnt[r], kFoldPad);
+            ext += (int)round_up(kc[k], kFoldPad);
+            flat += (int)round_up(kc[k], kFoldPad);
         }
     }
+#pragma unroll
+    for (int s = 0; s < kMaxRegions; ++s) {
+        const int k = key_of(s) + (kMaxRegions - 1);
+        int r = 0;
+#pragma unroll
+        for (int kk = 0; kk < 2 * kMaxRegions - 1; ++kk) r = kk == k ? region_of_key[kk] : r;
+        P.win_of[s] = s <= S ? r : 0;
+    }
+    P.nr = nr;
+    P.main_r = main_r;
     P.D = ext;
-    P.F = P.base[P.nr - 1];
+    P.H = H;
+    P.F = P.base[nr - 1];
 }
 
 __device__ __forceinline__ int wave_sum(int v) {
@@ -385,6 +406,7 @@ __device__ __forceinline__ int wave_sum(int v) {
 // channel's rank comes from wave ballots plus per-wave totals in LDS.
 // ---------------------------------------------------------------------------
 constexpr int kFinWaves = kFinThreads / 64;
+constexpr int kChunk = 16;   // rounds of kFinThreads channels whose loads are batched
 
 __global__ __launch_bounds__(kFinThreads) void k_finalize_grad(const uint32_t* __restrict__ partial, int64_t S,
                                                                int64_t C, QuantCfg cfg,
@@ -394,7 +416,10 @@ __global__ __launch_bounds__(kFinThreads) void k_finalize_grad(const uint32_t* _
                                                                sq_scale* __restrict__ scale,
                                                                int32_t* __restrict__ layout, int64_t ext_max) {
     __shared__ uint32_t shu[16];
-    __shared__ int wtot[kFinWaves][kMaxRegions];
+    __shared__ int cnt[kChunk][kFinWaves][kMaxRegions];
+    __shared__ int pre[kChunk][kFinWaves][kMaxRegions];
+    __shared__ int tot[kChunk][kMaxRegions];
+    __shared__ int roundpre[kChunk][kMaxRegions];
     __shared__ uint32_t lanes[4 * kFinThreads];
     __shared__ FoldPlan P;
     __shared__ int nsh[kMaxRegions];
@@ -434,26 +459,40 @@ __global__ __launch_bounds__(kFinThreads) void k_finalize_grad(const uint32_t* _
         return;
     }
 
+    // Channel c = k * kFinThreads + tid is handled by this thread in round k;
+    // rounds are processed in chunks of kChunk with their loads batched.
+    const int64_t rounds = (C + kFinThreads - 1) / kFinThreads;
+
     // groups and the number of channels at each shift
     int hist[kMaxRegions];
 #pragma unroll
     for (int s = 0; s < kMaxRegions; ++s) hist[s] = 0;
-    for (int64_t c = tid; c < C; c += kFinThreads) {
-        const uint32_t rb = C < kFinThreads ? r_small : rbits[c];
-        const int g = flagged ? Sh : group_of(__uint_as_float(rb), sc.r_max, cfg.num_groups);
-        group[c] = (uint8_t)g;
+    for (int64_t k0 = 0; k0 < rounds; k0 += kChunk) {
+        uint32_t rb[kChunk];
 #pragma unroll
-        for (int s = 0; s < kMaxRegions; ++s) hist[s] += (Sh - g) == s;
+        for (int k = 0; k < kChunk; ++k) {
+            const int64_t c = (k0 + k) * kFinThreads + tid;
+            rb[k] = c < C ? (C < kFinThreads ? r_small : rbits[c]) : 0u;
+        }
+#pragma unroll
+        for (int k = 0; k < kChunk; ++k) {
+            const int64_t c = (k0 + k) * kFinThreads + tid;
+            if (c >= C) continue;
+            const int g = flagged ? Sh : group_of(__uint_as_float(rb[k]), sc.r_max, cfg.num_groups);
+            group[c] = (uint8_t)g;
+#pragma unroll
+            for (int s = 0; s < kMaxRegions; ++s) hist[s] += (Sh - g) == s;
+        }
     }
 #pragma unroll
     for (int s = 0; s < kMaxRegions; ++s) {
         const int v = wave_sum(hist[s]);
-        if (lane == 0) wtot[wave][s] = v;
+        if (lane == 0) cnt[0][wave][s] = v;
     }
     __syncthreads();
     if (tid < kMaxRegions) {
         int v = 0;
-        for (int w = 0; w < kFinWaves; ++w) v += wtot[w][tid];
+        for (int w = 0; w < kFinWaves; ++w) v += cnt[0][w][tid];
         nsh[tid] = v;
     }
     __syncthreads();
@@ -461,42 +500,72 @@ __global__ __launch_bounds__(kFinThreads) void k_finalize_grad(const uint32_t* _
     __syncthreads();
 
     // place of every channel: descriptor ((pos + 1) << 4) | t, and the
-    // appended-column list
+    // appended-column list.  Appended channels are ranked per round with wave
+    // ballots; cnt[k][w][q] counts those of region q in wave w of round k,
+    // and pre[k][w][q] is the number of region-q channels before that wave
+    // (earlier chunks, earlier rounds, earlier waves).
     const int nr = P.nr, main_r = P.main_r;
     const uint64_t below = (1ull << lane) - 1ull;
-    for (int64_t c0 = 0; c0 < C; c0 += kFinThreads) {
-        const int64_t c = c0 + tid;
-        int r = main_r, t = 0;
-        if (c < C) {
-            const int sh = Sh - (int)group[c];   // written by this thread above
-            r = P.win_of[sh];
-            t = sh - P.base[r];
+    for (int64_t k0 = 0; k0 < rounds; k0 += kChunk) {
+        uint8_t gk[kChunk];
+#pragma unroll
+        for (int k = 0; k < kChunk; ++k) {
+            const int64_t c = (k0 + k) * kFinThreads + tid;
+            gk[k] = c < C ? group[c] : (uint8_t)0;   // written by this thread above
         }
-        const bool is_ext = c < C && r != main_r;
-        int rank = 0;
-        for (int q = 0; q < nr; ++q) {
-            const uint64_t m = __ballot(is_ext && r == q);
-            if (is_ext && r == q) rank = __popcll(m & below);
-            if (lane == 0) wtot[wave][q] = __popcll(m);
+        int code_r[kChunk], rank[kChunk];
+#pragma unroll
+        for (int k = 0; k < kChunk; ++k) {
+            const int64_t c = (k0 + k) * kFinThreads + tid;
+            int r = main_r;
+            if (c < C) r = P.win_of[Sh - (int)gk[k]];
+            code_r[k] = r;
+            const bool is_ext = c < C && r != main_r;
+            rank[k] = 0;
+            if (k0 + k >= rounds) continue;   // uniform: no channel of this round exists
+            for (int q = 0; q < nr; ++q) {
+                const uint64_t m = __ballot(is_ext && r == q);
+                if (is_ext && r == q) rank[k] = __popcll(m & below);
+                if (lane == 0) cnt[k][wave][q] = __popcll(m);
+            }
         }
         __syncthreads();
-        int pos = -1;
-        if (is_ext) {
-            int before = P.run[r];
-            for (int w = 0; w < wave; ++w) before += wtot[w][r];
-            pos = P.ext_start[r] + before + rank;
+        // thread (k, q): exclusive prefix over the waves of round k
+        if (tid < kChunk * kMaxRegions) {
+            const int k = tid / kMaxRegions, q = tid % kMaxRegions;
+            int acc = 0;
+            if (q < nr && k0 + k < rounds)
+                for (int w = 0; w < kFinWaves; ++w) {
+                    pre[k][w][q] = acc;
+                    acc += cnt[k][w][q];
+                }
+            tot[k][q] = acc;
         }
-        __syncthreads();   // every thread has read run[] for this round
+        __syncthreads();
+        // thread q: prefix over the rounds, plus the channels of earlier chunks
         if (tid < nr) {
-            int tot = 0;
-            for (int w = 0; w < kFinWaves; ++w) tot += wtot[w][tid];
-            P.run[tid] += tot;
+            int acc = P.run[tid];
+            for (int k = 0; k < kChunk && k0 + k < rounds; ++k) {
+                roundpre[k][tid] = acc;
+                acc += tot[k][tid];
+            }
+            P.run[tid] = acc;
         }
-        if (c < C) {
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < kChunk; ++k) {
+            const int64_t c = (k0 + k) * kFinThreads + tid;
+            if (c >= C) continue;
+            const int r = code_r[k];
+            const int t = (Sh - (int)gk[k]) - P.base[r];
+            int pos = -1;
+            if (r != main_r) {
+                pos = P.ext_start[r] + roundpre[k][r] + pre[k][wave][r] + rank[k];
+                ext[pos] = (int32_t)c;
+            }
             desc[c] = ((pos + 1) << 4) | t;
-            if (is_ext) ext[pos] = (int32_t)c;
         }
-        __syncthreads();   // run[] updated and wtot free for the next round
+        __syncthreads();   // cnt / pre / roundpre free for the next chunk
     }
     for (int r = 0; r < nr; ++r) {
         if (r == main_r) continue;

@@ -351,6 +351,20 @@ def test_fold_windows(sq, layer, pattern, bits, ng):
     check_layer(sq, dY, W, X, bits, ng, mode=(M + bits) % 2)
 
 
+@pytest.mark.parametrize("bits,ng", [(6, 4), (8, 4)])
+def test_fold_windows_many_channels(sq, bits, ng):
+    # more than 16 * 1024 channels: the finalize kernel ranks appended
+    # channels over several chunks of rounds
+    M, C = 40, 20000
+    g = _group_pattern("spread", C, ng, seed=11)
+    dY = _grouped_grad(M, g, seed=12)
+    import torch
+    codes = sq.quantize_grad(_dev(dY), bits, ng, 0, 0, 0)
+    torch.cuda.synchronize()
+    q_ref, g_ref, _ = check_quant(sq, codes, dY, bits, ng, 0, 0, 0)
+    assert np.array_equal(g_ref, g)
+
+
 @pytest.mark.parametrize("pattern", ["mostly_g0", "spread"])
 def test_fold_windows_large_tiles(sq, pattern):
     # the same on the large-tile pipelined GEMM (K >= 1024, >= 256 output tiles)
