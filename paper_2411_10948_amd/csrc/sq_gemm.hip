@@ -799,32 +799,57 @@ bool pipe_ok(const GemmArgs& a) {
     return true;
 }
 
-// Tile shape of a product: large tiles where there are enough of them to fill
-// most of the chip and K is long, a 64-row tile for products with at most 64
-// output rows, 128 x 128 otherwise.
+// Tile shape of a product: large tiles where there are enough of them (alone,
+// or with K split into slices of at least 16 tiles) to fill most of the chip
+// and K is long, a 64-row tile for products with at most 64 output rows,
+// 128 x 128 otherwise.
 enum class Pick { kLarge, kSmall, kSkinny };
 
 int64_t tiles_of(const GemmArgs& a, int bm, int bn) { return ((a.Mg + bm - 1) / bm) * ((a.Ng + bn - 1) / bn); }
 
+constexpr int64_t kLargeFill = 128;      // large tiles per launch that count as filling the chip
+constexpr int64_t kCUs = 256;
+constexpr int64_t kMinSplitKTiles = 16;  // K tiles per split of a large-tile split-K
+
+// Split factor that brings large tiles of a short-and-narrow product with a
+// long K to at most one block per CU (0: large tiles do not suit this product).
+int64_t large_splits(const GemmArgs& a) {
+    const int64_t tiles = tiles_of(a, PipeLarge::BM, PipeLarge::BN);
+    if (tiles >= kLargeFill) return 1;
+    // split only dense tilings (most of each tile inside the product)
+    if (a.extA || 4 * a.Mg * a.Ng < 3 * tiles * PipeLarge::BM * PipeLarge::BN) return 0;
+    const int64_t ktiles = (a.K + 63) / 64;
+    int64_t s = std::min(kCUs / tiles, ktiles / kMinSplitKTiles);
+    if (s < 2) return 0;
+    const int64_t per = (ktiles + s - 1) / s;   // equal slices, none empty
+    s = (ktiles + per - 1) / per;
+    return s >= 2 && tiles * s >= kLargeFill ? s : 0;
+}
+
 Pick pick(const GemmArgs& a) {
-    if (a.splits <= 1 && a.K >= 1024 && tiles_of(a, PipeLarge::BM, PipeLarge::BN) >= 128) return Pick::kLarge;
+    const int64_t ls = a.K >= 1024 ? large_splits(a) : 0;
+    if (ls > 0 && std::max(a.splits, 1) == ls) return Pick::kLarge;
     if (a.Mg <= 64 && !a.extA) return Pick::kSkinny;
     return Pick::kSmall;
 }
 
 }  // namespace
 
-// Split-K factor of the weight-gradient product: enough blocks for about two
-// per CU, at least 8 K tiles per split, no empty split.  The partial tiles do
-// not depend on the tile shape, so any kernel can consume this factor.
+// Split-K factor of the weight-gradient product: large tiles with the split
+// that fills the chip where that works (large_splits), else enough smaller
+// tiles for about two blocks per CU with at least 8 K tiles per split and no
+// empty split.  The partial tiles do not depend on the tile shape.
 int wgrad_splits(int64_t M, int64_t C_out, int64_t C_in) {
     GemmArgs probe{};
     probe.Mg = C_out; probe.Ng = C_in; probe.K = M; probe.splits = 1;
-    const Pick p = pick(probe);
-    if (p == Pick::kLarge) return 1;
-    const int64_t tiles = p == Pick::kSkinny ? tiles_of(probe, PipeSkinny::BM, PipeSkinny::BN)
-                                             : tiles_of(probe, PipeSmall::BM, PipeSmall::BN);
     const int64_t ktiles = (M + 63) / 64;
+    if (M >= 1024) {
+        const int64_t ls = large_splits(probe);
+        if (ls > 0) return (int)ls;
+    }
+    const bool skinny = C_out <= 64;
+    const int64_t tiles = skinny ? tiles_of(probe, PipeSkinny::BM, PipeSkinny::BN)
+                                 : tiles_of(probe, PipeSmall::BM, PipeSmall::BN);
     int64_t splits = (512 + tiles - 1) / tiles;
     splits = std::min(splits, std::max<int64_t>(1, ktiles / 8));
     splits = std::max<int64_t>(1, std::min<int64_t>(splits, 65535));
@@ -836,16 +861,15 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     if (a.Mg <= 0 || a.Ng <= 0) return hipSuccess;
     const bool pipe = pipe_ok(a);
     const Pick p = pick(a);
-    if (p == Pick::kLarge) {
-        const int64_t ktiles = (a.K + 63) / 64;
-        const int64_t kps = std::max<int64_t>(ktiles, 1) * 64;
-        if (!pipe) return launch_cfg<CfgLarge>(a, 1, kps, s);
-        return a.extA ? launch_pipe<PipeLarge, true>(a, 1, kps, s) : launch_pipe<PipeLarge, false>(a, 1, kps, s);
-    }
-    const int64_t ktiles = (a.K + 63) / 64;   // every configuration below has 64-byte K tiles
+    const int64_t ktiles = (a.K + 63) / 64;   // every configuration has 64-byte K tiles
     const int splits = std::max(1, a.splits);
     const int64_t per = splits > 1 ? (ktiles + splits - 1) / splits : std::max<int64_t>(ktiles, 1);
     if (splits > 1 && (ktiles + per - 1) / per != splits) return hipErrorInvalidValue;   // wgrad_splits() avoids this
+    if (p == Pick::kLarge) {
+        if (!pipe) return launch_cfg<CfgLarge>(a, splits, per * 64, s);
+        return a.extA ? launch_pipe<PipeLarge, true>(a, splits, per * 64, s)
+                      : launch_pipe<PipeLarge, false>(a, splits, per * 64, s);
+    }
     if (!pipe) return launch_cfg<CfgSmall>(a, splits, per * 64, s);
     if (p == Pick::kSkinny) return launch_pipe<PipeSkinny, false>(a, splits, per * 64, s);
     return a.extA ? launch_pipe<PipeSmall, true>(a, splits, per * 64, s)

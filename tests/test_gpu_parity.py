@@ -417,6 +417,22 @@ def test_wgrad_split_k(sq):
     check_layer(sq, dY, W, X, 4, 4, dgrad_rows=[3, 19998], want_acc=False)
 
 
+@pytest.mark.parametrize("shape", [(4096, 1024, 2048), (4136, 1024, 2048), (5120, 1280, 1344)])
+def test_wgrad_large_tiles_split_k(sq, shape):
+    # few 256 x 256 output tiles and a long token dimension: the wgrad splits
+    # K over large tiles (4 or 5 slices); 4136 tokens leave a ragged last K
+    # tile, which takes the register-staged kernel
+    M, C_out, C_in = shape
+    rng = np.random.default_rng(M + C_in)
+    dY = _grad(M, C_out, seed=C_in)
+    W = (rng.standard_normal((C_out, C_in)) * 0.05).astype(np.float32)
+    X = np.maximum(rng.standard_normal((M, C_in)), 0).astype(np.float32)
+    assert sq.sq_gemm_wgrad_workspace_size(M, C_out, C_in, sq.Params.make(4)) > 0
+    check_layer(sq, dY, W, X, 4, 4, dgrad_rows=[0, 1, M // 2, M - 1],
+                wgrad_rows=[0, 1, 255, 256, C_out // 2, C_out - 1])
+    check_layer(sq, dY, W, X, 6, 4, dgrad_rows=[2, M - 2], wgrad_rows=[3, C_out - 2], want_acc=False)
+
+
 @pytest.mark.parametrize("shape", [(4096, 40, 200), (8192, 64, 197), (2048, 1, 64), (16384, 64, 576)])
 def test_wgrad_narrow_outputs(sq, shape):
     # at most 64 output rows and a token count that is a multiple of 64: the
