@@ -71,6 +71,9 @@ def _bind(L):
     L.sqo_quantize_tensor.restype = ct.c_int
     L.sqo_dgrad.argtypes = [P, i64, i64, P, ct.c_int, P, i64, P, i64, P]
     L.sqo_dgrad.restype = ct.c_int
+    L.sqo_conv_dgrad.argtypes = [P, i64, i64, i64, i64, P, ct.c_int, P, i64, ct.c_int, ct.c_int, ct.c_int,
+                                 ct.c_int, P, i64, P]
+    L.sqo_conv_dgrad.restype = ct.c_int
     L.sqo_wgrad.argtypes = [P, i64, i64, P, i64, P, i64, P]
     L.sqo_wgrad.restype = ct.c_int
     L.sqo_dequant_dgrad.argtypes = [P, i64, ct.c_float, ct.c_float, ct.c_int, P]
@@ -171,6 +174,35 @@ def dgrad(q: np.ndarray, g: np.ndarray, num_groups: int, wq: np.ndarray, rows=No
     if rc == 2:
         raise RangeError("dgrad accumulator leaves int32")
     assert rc == 0
+    return A
+
+
+def conv_dgrad(q: np.ndarray, g: np.ndarray, num_groups: int, wq: np.ndarray, N: int, H: int, W: int,
+               KH: int, KW: int, PH: int, PW: int, pix=None) -> np.ndarray:
+    """Input gradient of a stride-1 convolution, int32: the col2im of the
+    im2col'd ShiftMM dgrad (sqo_conv_dgrad).  q [N*Ho*Wo, C_out] codes of dY
+    (NHWC), wq [C_out, KH*KW*C_in] in (r, s, ci) column order; returns
+    A [N*H*W, C_in] (or the listed input pixels)."""
+    q = _c(q, np.int8)
+    g = _c(g, np.uint8)
+    wq = _c(wq, np.int8)
+    C_out = q.shape[1]
+    C_in = wq.shape[1] // (KH * KW)
+    assert wq.shape == (C_out, KH * KW * C_in) and g.shape[0] == C_out
+    Ho, Wo = H + 2 * PH - KH + 1, W + 2 * PW - KW + 1
+    assert q.shape[0] == N * Ho * Wo
+    if pix is None:
+        A = np.zeros((N * H * W, C_in), np.int32)
+        rc = lib().sqo_conv_dgrad(_p(q), N, H, W, C_out, _p(g), num_groups, _p(wq), C_in, KH, KW, PH, PW,
+                                  None, 0, _p(A))
+    else:
+        pix = _c(pix, np.int64)
+        A = np.zeros((pix.shape[0], C_in), np.int32)
+        rc = lib().sqo_conv_dgrad(_p(q), N, H, W, C_out, _p(g), num_groups, _p(wq), C_in, KH, KW, PH, PW,
+                                  _p(pix), pix.shape[0], _p(A))
+    if rc == 2:
+        raise RangeError("conv dgrad accumulator leaves int32")
+    assert rc == 0, rc
     return A
 
 

@@ -279,6 +279,59 @@ int sqo_dgrad(const int8_t* q, int64_t M, int64_t C_out, const uint8_t* g, int n
     return SQO_OK;
 }
 
+/* ---------------------------------------------------------------------------
+ * Loss propagation of a stride-1 convolution lowered to the GEMM of
+ * Eq. dq_mm_f by im2col (the ResNet layers of Sec. 5 are convolutions).  The
+ * forward conv reads, for output pixel (n, oh, ow), the input pixels
+ * (n, oh + r - PH, ow + s - PW) of the KH x KW window, and im2col orders a
+ * column row as (r, s, ci); W is [C_out, KH * KW * C_in] in that order.  The
+ * input gradient is the col2im (the adjoint of im2col) of the im2col'd dgrad:
+ *   A[(n, ih, iw), ci] = sum_{r, s} sum_co (q[(n, oh, ow), co] * wq[co, (r, s, ci)]) << sh_co
+ * with oh = ih + PH - r and ow = iw + PW - s, terms outside the Ho x Wo output
+ * grid being absent; sh_co = N_G - 1 - g_co as in sqo_dgrad.  q is the code
+ * matrix of dY [N * Ho * Wo, C_out] (NHWC), Ho = H + 2 PH - KH + 1 and
+ * Wo = W + 2 PW - KW + 1.  `pix` lists input pixels (n * H + ih) * W + iw
+ * (NULL = all N * H * W of them); A is [n_pix, C_in], accumulated in int64.
+ * ------------------------------------------------------------------------- */
+int sqo_conv_dgrad(const int8_t* q, int64_t N, int64_t H, int64_t W, int64_t C_out, const uint8_t* g,
+                   int num_groups, const int8_t* wq, int64_t C_in, int KH, int KW, int PH, int PW,
+                   const int64_t* pix, int64_t n_pix, int32_t* A)
+{
+    if (!q || !g || !wq || !A || num_groups < 1 || num_groups > 8) return SQO_ERR_ARG;
+    if (N < 0 || H < 1 || W < 1 || C_out < 0 || C_in < 0 || KH < 1 || KW < 1 || PH < 0 || PW < 0)
+        return SQO_ERR_ARG;
+    int64_t Ho = H + 2 * (int64_t)PH - KH + 1, Wo = W + 2 * (int64_t)PW - KW + 1;
+    if (Ho < 1 || Wo < 1) return SQO_ERR_ARG;
+    int64_t taps_ci = (int64_t)KH * KW * C_in;   /* columns of W */
+    int64_t np = pix ? n_pix : N * H * W;
+    for (int64_t i = 0; i < np; ++i) {
+        int64_t p = pix ? pix[i] : i;
+        if (p < 0 || p >= N * H * W) return SQO_ERR_ARG;
+        int64_t n = p / (H * W), ih = (p / W) % H, iw = p % W;
+        for (int64_t ci = 0; ci < C_in; ++ci) {
+            int64_t acc = 0;
+            for (int r = 0; r < KH; ++r) {
+                int64_t oh = ih + PH - r;
+                if (oh < 0 || oh >= Ho) continue;
+                for (int s = 0; s < KW; ++s) {
+                    int64_t ow = iw + PW - s;
+                    if (ow < 0 || ow >= Wo) continue;
+                    const int8_t* qrow = q + ((n * Ho + oh) * Wo + ow) * C_out;
+                    int64_t col = ((int64_t)r * KW + s) * C_in + ci;
+                    for (int64_t co = 0; co < C_out; ++co) {
+                        int shift = num_groups - 1 - (int)g[co];
+                        int64_t prod = (int64_t)qrow[co] * (int64_t)wq[co * taps_ci + col];
+                        acc += ((int64_t)1 << shift) * prod;
+                    }
+                }
+            }
+            if (acc > INT32_MAX || acc < INT32_MIN) return SQO_ERR_RANGE;
+            A[i * C_in + ci] = (int32_t)acc;
+        }
+    }
+    return SQO_OK;
+}
+
 /* Weight gradient (the third training GEMM, Fig. "MMs"): inner dimension is
  * the token index, so each output row c lies in one gradient group:
  *   B[c, k] = sum_m q[m, c] * xq[m, k]            (unshifted, R8)

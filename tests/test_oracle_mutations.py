@@ -45,6 +45,11 @@ MUTATIONS = [
      "float alpha = (d_grad * d_w) * pow2f(-num_groups);"),
     ("wgrad dequant sign", "float beta = (d_grad * d_x) * pow2f(-(int)g_rows[i]);",
      "float beta = (d_grad * d_x) * pow2f((int)g_rows[i]);"),
+    ("conv output row of a tap", "int64_t oh = ih + PH - r;", "int64_t oh = ih - PH + r;"),
+    ("conv tap order in the im2col column", "int64_t col = ((int64_t)r * KW + s) * C_in + ci;",
+     "int64_t col = ((int64_t)s * KH + r) * C_in + ci;"),
+    ("conv last output row dropped", "if (oh < 0 || oh >= Ho) continue;", "if (oh < 0 || oh >= Ho - 1) continue;"),
+    ("conv dropped shift", "acc += ((int64_t)1 << shift) * prod;", "acc += prod;"),
     ("int32 range check", "if (acc > INT32_MAX || acc < INT32_MIN) return SQO_ERR_RANGE;\n            A[i * C_in + k]",
      "A[i * C_in + k]"),
 ]
@@ -82,6 +87,9 @@ def _pin_calls():
         calls.append(lambda b=bits, n=ng: pins.test_dgrad_equals_shifted_matmul_and_group_gemms(b, n))
         calls.append(lambda b=bits, n=ng: pins.test_dgrad_dequant_equals_dequantized_product(b, n))
     calls.append(lambda: pins.test_shiftquant_variance_bound(4))
+    for case in pins.CONV_CASES:
+        calls.append(lambda c=case: pins.test_conv_dgrad_is_transpose_of_forward_conv(c))
+    calls.append(pins.test_conv_dgrad_1x1_is_dgrad_and_brute_force)
     return calls
 
 

@@ -441,3 +441,100 @@ def test_full_small_workload_consistency():
     xd = res["xq"].astype(np.float64) * np.float64(res["xscale"]["d0"])
     _close_to_product(res["dX"], dq @ wd, np.abs(dq) @ np.abs(wd))
     _close_to_product(res["dW"], dq.T @ xd, np.abs(dq).T @ np.abs(xd))
+
+
+# ---------------------------------------------------------------------------
+# Convolution lowered by im2col: the input gradient is the col2im of the dgrad
+# ---------------------------------------------------------------------------
+CONV_CASES = [  # N, H, W, C_out, C_in, KH, KW, PH, PW
+    (2, 5, 4, 3, 2, 3, 3, 1, 1),
+    (1, 6, 5, 4, 3, 3, 3, 0, 0),
+    (1, 4, 7, 2, 3, 1, 3, 0, 1),
+    (2, 5, 5, 3, 2, 5, 5, 2, 2),
+    (1, 4, 5, 2, 2, 2, 2, 0, 0),
+    (1, 3, 3, 5, 4, 1, 1, 0, 0),
+    (1, 2, 3, 2, 2, 3, 3, 2, 1),
+]
+
+
+def _conv_operands(N, H, W, C_out, C_in, KH, KW, PH, PW, seed):
+    rng = np.random.default_rng(seed)
+    Ho, Wo = H + 2 * PH - KH + 1, W + 2 * PW - KW + 1
+    ng = 4
+    q = rng.integers(-7, 8, (N * Ho * Wo, C_out)).astype(np.int8)
+    g = rng.integers(0, ng, C_out).astype(np.uint8)
+    wq = rng.integers(-127, 128, (C_out, KH * KW * C_in)).astype(np.int8)
+    return q, g, wq, ng, Ho, Wo
+
+
+def _forward_conv_jacobian(wq, N, H, W, C_out, C_in, KH, KW, PH, PW):
+    """Dense matrix J of the stride-1 forward convolution Y = conv(X, W), from
+    its definition Y[n, oh, ow, co] = sum_{r, s, ci} X[n, oh + r - PH,
+    ow + s - PW, ci] W[co, r, s, ci] (zero outside the input), with X and Y
+    flattened in NHWC order."""
+    Ho, Wo = H + 2 * PH - KH + 1, W + 2 * PW - KW + 1
+    J = np.zeros((N * Ho * Wo * C_out, N * H * W * C_in), np.int64)
+    w4 = wq.astype(np.int64).reshape(C_out, KH, KW, C_in)
+    for n in range(N):
+        for oh in range(Ho):
+            for ow in range(Wo):
+                for r in range(KH):
+                    for s in range(KW):
+                        ih, iw = oh + r - PH, ow + s - PW
+                        if not (0 <= ih < H and 0 <= iw < W):
+                            continue
+                        row = ((n * Ho + oh) * Wo + ow) * C_out
+                        col = ((n * H + ih) * W + iw) * C_in
+                        J[row:row + C_out, col:col + C_in] += w4[:, r, s, :]
+    return J
+
+
+@pytest.mark.parametrize("case", CONV_CASES, ids=[str(c) for c in CONV_CASES])
+def test_conv_dgrad_is_transpose_of_forward_conv(case):
+    # the gradient of a linear map is its transpose: dX = J^T dY', with dY'
+    # the codes left-shifted by their group shifts (App. D left-shift form)
+    N, H, W, C_out, C_in, KH, KW, PH, PW = case
+    q, g, wq, ng, Ho, Wo = _conv_operands(*case, seed=sum(case))
+    A = oracle.conv_dgrad(q, g, ng, wq, N, H, W, KH, KW, PH, PW)
+    J = _forward_conv_jacobian(wq, N, H, W, C_out, C_in, KH, KW, PH, PW)
+    shifted = q.astype(np.int64) << (ng - 1 - g.astype(np.int64))[None, :]
+    ref = (J.T @ shifted.reshape(-1)).reshape(N * H * W, C_in)
+    np.testing.assert_array_equal(A, ref)
+    pix = np.array([N * H * W - 1, 0, (N * H * W) // 2])
+    np.testing.assert_array_equal(oracle.conv_dgrad(q, g, ng, wq, N, H, W, KH, KW, PH, PW, pix), ref[pix])
+
+
+@pytest.mark.parametrize("case", CONV_CASES[:4], ids=[str(c) for c in CONV_CASES[:4]])
+def test_conv_dgrad_is_col2im_of_im2col_dgrad(case):
+    # the GEMM of the im2col'd layer (sqo_dgrad over columns (r, s, ci)),
+    # then col2im: every column entry added back to the input pixel it came from
+    N, H, W, C_out, C_in, KH, KW, PH, PW = case
+    q, g, wq, ng, Ho, Wo = _conv_operands(*case, seed=3 * sum(case))
+    A_col = oracle.dgrad(q, g, ng, wq).astype(np.int64).reshape(N, Ho, Wo, KH, KW, C_in)
+    dX = np.zeros((N, H + 2 * PH, W + 2 * PW, C_in), np.int64)
+    for r in range(KH):
+        for s in range(KW):
+            dX[:, r:r + Ho, s:s + Wo, :] += A_col[:, :, :, r, s, :]
+    ref = dX[:, PH:PH + H, PW:PW + W, :].reshape(N * H * W, C_in)
+    np.testing.assert_array_equal(oracle.conv_dgrad(q, g, ng, wq, N, H, W, KH, KW, PH, PW), ref)
+
+
+def test_conv_dgrad_1x1_is_dgrad_and_brute_force():
+    q, g, wq, ng, Ho, Wo = _conv_operands(2, 3, 4, 5, 6, 1, 1, 0, 0, seed=8)
+    np.testing.assert_array_equal(oracle.conv_dgrad(q, g, ng, wq, 2, 3, 4, 1, 1, 0, 0), oracle.dgrad(q, g, ng, wq))
+    # pure-Python loops over a 3x3 window with padding 1
+    N, H, W, C_out, C_in = 1, 3, 2, 2, 2
+    q, g, wq, ng, Ho, Wo = _conv_operands(N, H, W, C_out, C_in, 3, 3, 1, 1, seed=9)
+    A = oracle.conv_dgrad(q, g, ng, wq, N, H, W, 3, 3, 1, 1)
+    for ih in range(H):
+        for iw in range(W):
+            for ci in range(C_in):
+                ref = 0
+                for oh in range(Ho):
+                    for ow in range(Wo):
+                        r, s = ih - oh + 1, iw - ow + 1
+                        if 0 <= r < 3 and 0 <= s < 3:
+                            for co in range(C_out):
+                                ref += (int(q[oh * Wo + ow, co]) * int(wq[co, (r * 3 + s) * C_in + ci])
+                                        << (ng - 1 - int(g[co])))
+                assert A[ih * W + iw, ci] == ref
