@@ -25,6 +25,9 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 PEAK_INT8_TOPS = 5000.0      # MI355X dense int8 matrix-core peak
 DEFAULT_WORKLOAD = "resnet18_conv3x3"
+# the same conv layer with the input gradient taken by the implicit-im2col
+# conv dgrad (dX itself, NHWC, instead of the 9x larger im2col'd dX_col)
+FUSED_CONV = {"resnet18_conv3x3_fused": "resnet18_conv3x3"}
 KERNEL_SOURCES = ["paper_2411_10948_amd/csrc/sq_gemm.hip", "paper_2411_10948_amd/csrc/sq_quant.hip",
                   "paper_2411_10948_amd/csrc/sq_internal.h"]
 
@@ -54,24 +57,39 @@ def measured_traffic(workload: str, kernel: str):
         return None
 
 
-def cpu_baseline(inputs, wl, budget_s: float = 10.0):
-    """The CPU oracle (single-threaded C) on the first rows of the same layer."""
+def cpu_baseline(inputs, wl, budget_s: float = 10.0, conv=False):
+    """The CPU oracle (single-threaded C) on the first rows of the same layer
+    (whole images for the implicit-im2col conv step)."""
     import oracle
     dY, W, X = inputs["dY"], inputs["W"], inputs["X"]
     M = dY.shape[0]
+    hw = wl.conv_hw * wl.conv_hw
 
     def run(rows):
         t0 = time.perf_counter()
-        oracle.backward(dY[:rows], W, X[:rows], wl.bits, wl.num_groups, wl.round_mode, wl.sr_seed, wl.sr_offset)
+        if conv:
+            q, g, gs, _ = oracle.quantize_grad(dY[:rows], wl.bits, wl.num_groups, wl.round_mode, wl.sr_seed,
+                                               wl.sr_offset)
+            wq, ws = oracle.quantize_tensor(W, 8)
+            xq, xs = oracle.quantize_tensor(X[:rows], 8)
+            A = oracle.conv_dgrad(q, g, wl.num_groups, wq, rows // hw, wl.conv_hw, wl.conv_hw, 3, 3, 1, 1)
+            B = oracle.wgrad(q, xq)
+            oracle.dequant_dgrad(A, gs["d0"], ws["d0"], wl.num_groups)
+            oracle.dequant_wgrad(B, g, gs["d0"], xs["d0"])
+        else:
+            oracle.backward(dY[:rows], W, X[:rows], wl.bits, wl.num_groups, wl.round_mode, wl.sr_seed,
+                            wl.sr_offset)
         return time.perf_counter() - t0
 
-    rows = max(1, min(M, M // 256))
+    unit = hw if conv else 1
+    rows = max(unit, min(M, M // 256) // unit * unit)
     t = run(rows)
-    rows = int(min(M, max(rows, rows * budget_s / max(t, 1e-3))))
+    rows = int(min(M, max(rows, rows * budget_s / max(t, 1e-3)))) // unit * unit
     t = run(rows)
     ops = 4 * rows * wl.C_out * wl.C_in
+    what = "quantize+conv dgrad+wgrad+dequant" if conv else "quantize+dgrad+wgrad+dequant"
     return {"value": ops / t / 1e12, "unit": "TOPS", "cores": 1, "kind": "oracle",
-            "sample": f"oracle quantize+dgrad+wgrad+dequant on the first {rows} of {M} token rows "
+            "sample": f"oracle {what} on the first {rows} of {M} token rows "
                       f"({ops / 1e9:.2f} Gop in {t:.2f} s, 1 thread)"}
 
 
@@ -99,8 +117,9 @@ def main(argv=None):
         build.build()
     sq.load()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
-    wl = workloads.WORKLOADS[args.workload]
-    inputs = workloads.make_inputs(args.workload)
+    conv = args.workload in FUSED_CONV
+    wl = workloads.WORKLOADS[FUSED_CONV.get(args.workload, args.workload)]
+    inputs = workloads.make_inputs(wl.name)
     M, C_out, C_in = inputs["M"], wl.C_out, wl.C_in
     print(f"[bench] {args.workload}: M={M} C_out={C_out} C_in={C_in} b={wl.bits} N_G={wl.num_groups} "
           f"round={'SR' if wl.round_mode else 'RTN'}", file=sys.stderr, flush=True)
@@ -113,7 +132,11 @@ def main(argv=None):
     wq_t, ws = sq.quantize_tensor(W, 8, transpose=True)
     xq_t, xs = sq.quantize_tensor(X, 8, transpose=True)
     del W, X
-    plan = sq.BackwardPlan(M, C_out, C_in, params, device=dev)
+    if conv:
+        n_img = M // (wl.conv_hw * wl.conv_hw)
+        plan = sq.ConvBackwardPlan(n_img, wl.conv_hw, wl.conv_hw, C_out, wl.conv_cin, 3, 3, 1, 1, params, device=dev)
+    else:
+        plan = sq.BackwardPlan(M, C_out, C_in, params, device=dev)
     stream = torch.cuda.current_stream()
     if args.calibrate_copy:
         src = torch.empty(64 << 20, dtype=torch.float32, device=dev).fill_(1.0)
@@ -161,8 +184,10 @@ def main(argv=None):
     # algorithmic bytes / ops per launch (int8 operands read once, outputs written once)
     parts = {
         "sq_quantize_grad": {"ms": t_quant, "bytes": 5 * M * C_out, "ops": 0},
-        "sq_gemm_dgrad": {"ms": t_dgrad, "bytes": M * C_out + C_out * C_in + 4 * M * C_in,
-                          "ops": 2 * M * C_out * C_in},
+        # the conv dgrad writes dX [N*H*W, C_in / 9] (stride 1, same padding: N*H*W = M)
+        "sq_conv_dgrad" if conv else "sq_gemm_dgrad": {
+            "ms": t_dgrad, "bytes": M * C_out + C_out * C_in + 4 * M * (C_in // 9 if conv else C_in),
+            "ops": 2 * M * C_out * C_in},
         "sq_gemm_wgrad": {"ms": t_wgrad, "bytes": M * C_out + M * C_in + 4 * C_out * C_in,
                           "ops": 2 * M * C_out * C_in},
     }
@@ -197,6 +222,7 @@ def main(argv=None):
         "data": "synthetic",
         "config": {"workload": args.workload, "M": M, "C_out": C_out, "C_in": C_in, "bits": wl.bits,
                    "num_groups": wl.num_groups, "rounding": "stochastic" if wl.round_mode else "nearest-even",
+                   "dgrad_output": "dX [N,H,W,C] (implicit im2col + col2im)" if conv else "dX_col [M, C_in]",
                    "parallelism": "none"},
         "pct_int8_peak": 100.0 * value / PEAK_INT8_TOPS,
         "breakdown_ms": {k: v["ms"] for k, v in parts.items()},
@@ -204,7 +230,7 @@ def main(argv=None):
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a slice of the workload", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(inputs, wl)
+        out["cpu_baseline"] = cpu_baseline(inputs, wl, conv=conv)
     print(json.dumps(out), flush=True)
     return 0
 

@@ -227,6 +227,45 @@ sq_status sq_gemm_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, c
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * sq_conv_dgrad -- input gradient of a stride-1 convolution, im2col and
+ * col2im both implicit.
+ *
+ * The ResNet layers of Sec. 5 are convolutions that the GEMM of Eq. "dq_mm_f"
+ * serves through im2col: X_col [N Ho Wo, KH KW C_in] with columns in
+ * (r, s, ci) order, dX_col = dY . W, and dX = col2im(dX_col), col2im being
+ * the adjoint of im2col.  This call computes dX directly, without writing
+ * dX_col: with sh_c = N_G - 1 - g_c (0-indexed groups),
+ *   acc[(n, ih, iw), ci] = sum_{r < KH, s < KW} sum_c
+ *                          (code((n, ih + PH - r, iw + PW - s), c) * wq[c, (r, s, ci)]) << sh_c
+ * over the window taps whose output pixel lies inside the Ho x Wo grid,
+ * Ho = H + 2 PH - KH + 1, Wo = W + 2 PW - KW + 1, and
+ *   dX = fl(float(acc) * alpha), alpha as in sq_gemm_dgrad.
+ * The forward convolution this differentiates reads input pixel
+ * (n, oh + r - PH, ow + s - PW) at tap (r, s) of output pixel (n, oh, ow).
+ * Inputs : q_fold, ld_fold, layout, group, gscale from sq_quantize_grad of
+ *          dY [N Ho Wo, C_out] (NHWC pixel order); wq_t [KH KW C_in, ld_w]
+ *          int8 = W^T codes of W [C_out, KH KW C_in] (ld_w >= C_out);
+ *          wscale its sq_scale.  1 <= KH, KW <= 15, 0 <= PH < KH,
+ *          0 <= PW < KW, N H W < 2^31, N Ho Wo ld_fold < 2^31 bytes.
+ * Outputs (either may be NULL, not both): acc [N H W, ld_acc] int32,
+ *          dX [N H W, ld_dX] fp32 (NHWC).
+ * Workspace: sq_conv_dgrad_workspace_size bytes (the weights regathered in
+ *          the order of the implicit K sequence).
+ * Errors: SQ_ERR_INVALID_ARGUMENT; SQ_ERR_OVERFLOW_RISK when
+ *         KH KW C_out Q 2^(N_G-1) 128 >= 2^31; SQ_ERR_UNSUPPORTED beyond the
+ *         size limits above; SQ_ERR_WORKSPACE_TOO_SMALL; SQ_ERR_HIP.
+ * ------------------------------------------------------------------------- */
+sq_status sq_conv_dgrad_workspace_size(int64_t C_out, int64_t C_in, int32_t KH, int32_t KW,
+                                       const sq_quant_params* p, size_t* bytes);
+sq_status sq_conv_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* layout,
+                        const uint8_t* group, const sq_scale* gscale,
+                        const int8_t* wq_t, int64_t ld_w, const sq_scale* wscale,
+                        int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t C_in,
+                        int32_t KH, int32_t KW, int32_t PH, int32_t PW, const sq_quant_params* p,
+                        int32_t* acc, int64_t ld_acc, float* dX, int64_t ld_dX,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * sq_dequant -- int32 accumulator to fp32 (Eq. "dq_mm_f": the inverse
  * scales multiply the integer sum once, outside the accumulation).
  *   kind 0 (dgrad): out = fl(float(acc) * alpha), alpha as in sq_gemm_dgrad

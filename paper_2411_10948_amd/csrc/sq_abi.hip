@@ -278,6 +278,84 @@ sq_status sq_gemm_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* la
     return hip_status(launch_gemm(a, s), "gemm_dgrad");
 }
 
+static sq_status check_conv(int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t C_in, int32_t KH, int32_t KW,
+                            int32_t PH, int32_t PW) {
+    if (N < 0 || H < 1 || W < 1 || C_out < 0 || C_in < 0)
+        return fail(SQ_ERR_INVALID_ARGUMENT, "conv: need N >= 0, H, W >= 1, C_out, C_in >= 0");
+    if (KH < 1 || KW < 1 || KH > 15 || KW > 15 || PH < 0 || PW < 0 || PH >= KH || PW >= KW)
+        return fail(SQ_ERR_INVALID_ARGUMENT, "conv: need 1 <= KH, KW <= 15 and 0 <= PH < KH, 0 <= PW < KW");
+    if (H + 2 * (int64_t)PH - KH + 1 < 1 || W + 2 * (int64_t)PW - KW + 1 < 1)
+        return fail(SQ_ERR_INVALID_ARGUMENT, "conv: the window is larger than the padded input");
+    if (N * H * W > 0x7FFFFFFF) return fail(SQ_ERR_UNSUPPORTED, "conv: more than 2^31 - 1 input pixels");
+    return SQ_OK;
+}
+
+sq_status sq_conv_dgrad_workspace_size(int64_t C_out, int64_t C_in, int32_t KH, int32_t KW, const sq_quant_params* p,
+                                       size_t* bytes) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_dims(C_out, C_in, "conv weight"));
+    if (KH < 1 || KW < 1 || KH > 15 || KW > 15) return fail(SQ_ERR_INVALID_ARGUMENT, "conv: need 1 <= KH, KW <= 15");
+    if (!bytes) return fail(SQ_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    const QuantCfg cfg = make_cfg(*p);
+    *bytes = (size_t)round_up(C_in * conv_bc_ld(C_out, (int64_t)KH * KW, fold_ext_max(C_out, cfg)), 256);
+    return SQ_OK;
+}
+
+sq_status sq_conv_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* layout, const uint8_t* group,
+                        const sq_scale* gscale, const int8_t* wq_t, int64_t ld_w, const sq_scale* wscale, int64_t N,
+                        int64_t H, int64_t W, int64_t C_out, int64_t C_in, int32_t KH, int32_t KW, int32_t PH,
+                        int32_t PW, const sq_quant_params* p, int32_t* acc, int64_t ld_acc, float* dX,
+                        int64_t ld_dX, void* workspace, size_t workspace_bytes, void* stream) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_conv(N, H, W, C_out, C_in, KH, KW, PH, PW));
+    if (!acc && !dX) return fail(SQ_ERR_INVALID_ARGUMENT, "acc and dX are both NULL");
+    if (!layout || !gscale || !wscale) return fail(SQ_ERR_INVALID_ARGUMENT, "layout or a scale is NULL");
+    const QuantCfg cfg = make_cfg(*p);
+    const int64_t taps = (int64_t)KH * KW;
+    // worst case |acc| = KH * KW * C_out * Q * 2^(N_G-1) * 128 must stay below 2^31
+    const double bound = (double)taps * C_out * cfg.Q * (double)(1 << (cfg.num_groups - 1)) * 128.0;
+    if (bound >= 2147483648.0)
+        return fail(SQ_ERR_OVERFLOW_RISK,
+                    "KH * KW * C_out * Q * 2^(N_G-1) * 128 reaches 2^31: the int32 accumulator could overflow");
+    const int64_t pixels = N * H * W;
+    const int64_t Ho = H + 2 * (int64_t)PH - KH + 1, Wo = W + 2 * (int64_t)PW - KW + 1;
+    if (pixels == 0 || C_in == 0) return SQ_OK;
+    size_t lay_bytes = 0;
+    int64_t min_ld_fold = 0;
+    SQ_TRY(sq_grad_layout_size(C_out, p, &lay_bytes, &min_ld_fold));
+    SQ_TRY(check_codes(q_fold, ld_fold, min_ld_fold, "q_fold"));
+    SQ_TRY(check_codes(wq_t, ld_w, C_out > 0 ? C_out : 1, "wq_t"));
+    if (acc) SQ_TRY(check_f32(acc, ld_acc, C_in, "acc"));
+    if (dX) SQ_TRY(check_f32(dX, ld_dX, C_in, "dX"));
+    const int64_t ext_max = fold_ext_max(C_out, cfg);
+    size_t need = 0;
+    SQ_TRY(sq_conv_dgrad_workspace_size(C_out, C_in, KH, KW, p, &need));
+    if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
+    if (workspace_bytes < need) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+    if (N * Ho * Wo * ld_fold >= ((int64_t)1 << 31))
+        return fail(SQ_ERR_UNSUPPORTED, "conv: q_fold spans 2^31 bytes or more");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+
+    int8_t* bc = static_cast<int8_t*>(workspace);
+    const int64_t ld_bc = conv_bc_ld(C_out, taps, ext_max);
+    GemmArgs a{};
+    a.Mg = pixels; a.Ng = C_in;
+    a.A = q_fold; a.lda = ld_fold;
+    a.B = wq_t; a.ldb = ld_w;
+    a.K_used = C_out;
+    a.K = fold_ext_base(C_out);
+    a.layout = layout;
+    if (ext_max > 0) { a.extA = q_fold + fold_ext_base(C_out); a.ld_extA = ld_fold; }
+    a.splits = 1;
+    a.acc = acc; a.ld_acc = ld_acc;
+    a.out = dX; a.ld_out = ld_dX;
+    a.epi_mode = 0;
+    a.gs = gscale; a.os = wscale; a.group = group; a.num_groups = cfg.num_groups;
+    a.taps = (int)taps; a.cv_KW = KW; a.cv_PH = PH; a.cv_PW = PW;
+    a.cv_H = H; a.cv_W = W; a.cv_Ho = Ho; a.cv_Wo = Wo; a.a_rows = N * Ho * Wo;
+    return hip_status(launch_conv_dgrad(a, bc, ld_bc, s), "conv_dgrad");
+}
+
 sq_status sq_gemm_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, const sq_scale* gscale,
                         const int8_t* xq_t, int64_t ld_x, const sq_scale* xscale, int64_t M, int64_t C_out,
                         int64_t C_in, const sq_quant_params* p, int32_t* acc, int64_t ld_acc, float* dW,

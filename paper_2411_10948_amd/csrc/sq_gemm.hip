@@ -86,6 +86,17 @@ __device__ __forceinline__ void tile_coords(int64_t b, int64_t tiles_m, int64_t 
     tn = w / gsz;
 }
 
+// Position in the K sequence of the implicit-im2col convolution: flat fold
+// tile f, tap tau = r * KW + s of the window.
+struct TapCursor {
+    int f = 0, tau = 0, r = 0, s = 0;
+    __device__ void next(int taps, int kw) {
+        ++tau;
+        if (++s == kw) { s = 0; ++r; }
+        if (tau == taps) { tau = 0; r = 0; s = 0; ++f; }
+    }
+};
+
 template <int MF>
 struct Mfma;
 template <>
@@ -145,13 +156,13 @@ struct HornerSteps {
             if (nr > 1) col = s1;
         }
     }
-    __device__ int start_of(int r) const {
-        return r == 1 ? s1 : r == 2 ? s2 : r == 3 ? s3 : r == 4 ? s4 : r == 5 ? s5 : r == 6 ? s6 : s7;
-    }
+    // the starts are consumed in order: shift the queue instead of indexing
+    // it (an indexed member would be placed in scratch memory)
     __device__ int advance() {
         const int sft = (int)((shifts >> (4 * next)) & 15u);
         ++next;
-        col = next < nr ? (int64_t)start_of(next) : INT64_MAX;
+        col = next < nr ? (int64_t)s2 : INT64_MAX;
+        s2 = s3; s3 = s4; s4 = s5; s5 = s6; s6 = s7;
         return sft;
     }
 };
@@ -399,6 +410,7 @@ using PipeLarge = PipeCfg<256, 256, 4, 2, 16, 4>;   // 128 KB of LDS, one block 
 using PipeWide = PipeCfg<256, 256, 2, 2, 16, 4>;    // 4 waves of 128 x 128: half the LDS reads per MFMA
 using PipeSmall = PipeCfg<128, 128, 2, 2, 16, 4>;   // 64 KB of LDS
 using PipeSkinny = PipeCfg<64, 192, 2, 2, 16, 4>;   // at most 64 output rows (wgrad of narrow layers)
+using PipeNarrow = PipeCfg<256, 64, 4, 1, 16, 4>;   // at most 64 output columns (conv dgrad), 80 KB of LDS
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
@@ -412,7 +424,7 @@ __device__ __forceinline__ void wait_vm() {
 }
 __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0x7F | (0x3 << 14) | (0x0 << 8)); }
 
-template <class T, bool HORNER>
+template <class T, bool HORNER, bool CONV = false>
 __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t tiles_m, int64_t tiles_n,
                                                            int64_t k_per_split) {
 #if defined(__HIP_DEVICE_COMPILE__)   // buffer resources exist in the device pass only
@@ -430,7 +442,10 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
     const int64_t kbeg = (int64_t)blockIdx.y * k_per_split;
     const int64_t kend = min(p.K, kbeg + k_per_split);
     const int n_main = kend > kbeg ? (int)((kend - kbeg) / T::BK) : 0;
-    const int n_tiles = fv.n_ext + n_main;
+    // a convolution visits the flat fold sequence once per tap: tile t is
+    // flat tile t / taps of tap t % taps
+    const int taps = CONV ? p.taps : 1;
+    const int n_tiles = (fv.n_ext + n_main) * taps;
 
     // Operand tiles come in with buffer loads straight to LDS: each lane's
     // 32-bit byte offset (row of its load instruction, logical chunk
@@ -445,7 +460,7 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
         return __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(base), (short)0, (int)min(rows * ld, (int64_t)0x7FFFFFFF),
                                                  kRsrcFlags);
     };
-    const __amdgpu_buffer_rsrc_t rA = rsrc(p.A, p.Mg, p.lda), rB = rsrc(p.B, p.Ng, p.ldb);
+    const __amdgpu_buffer_rsrc_t rA = rsrc(p.A, CONV ? p.a_rows : p.Mg, p.lda), rB = rsrc(p.B, p.Ng, p.ldb);
     auto lane_off = [&](int i, int64_t first, int64_t rows, int64_t ld) {
         const int r = (i * T::kWaves + wv) * 16 + lr;
         return (uint32_t)(min(first + r, rows - 1) * ld + 16 * ((lane & 3) ^ swz(r)));
@@ -456,8 +471,51 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
 #pragma unroll
     for (int i = 0; i < T::IB; ++i) offB[i] = lane_off(i, n0, p.Ng, p.ldb);
 
+    // Convolution: the input pixel (n, ih, iw) of each of this lane's A rows;
+    // tap (r, s) reads output pixel (n, ih + PH - r, iw + PW - s) of q_fold,
+    // or, outside the output grid, an offset past the end of the buffer,
+    // which the buffer load's range check turns into zeros.
+    int cv_ih[CONV ? T::IA : 1], cv_iw[CONV ? T::IA : 1], cv_row0[CONV ? T::IA : 1];
+    uint32_t cv_chunk[CONV ? T::IA : 1];
+    if constexpr (CONV) {
+#pragma unroll
+        for (int i = 0; i < T::IA; ++i) {
+            const int r = (i * T::kWaves + wv) * 16 + lr;
+            const int64_t pix = min(m0 + r, p.Mg - 1);
+            const int64_t n = pix / (p.cv_H * p.cv_W), hw = pix - n * p.cv_H * p.cv_W;
+            cv_ih[i] = (int)(hw / p.cv_W);
+            cv_iw[i] = (int)(hw - (int64_t)cv_ih[i] * p.cv_W);
+            cv_row0[i] = (int)(n * p.cv_Ho * p.cv_Wo);
+            cv_chunk[i] = 16u * (uint32_t)((lane & 3) ^ swz(r));
+        }
+    }
+    auto conv_off = [&](int i, int tr, int ts) -> uint32_t {
+        const int oh = cv_ih[i] + p.cv_PH - tr, ow = cv_iw[i] + p.cv_PW - ts;
+        const bool ok = (uint32_t)oh < (uint32_t)p.cv_Ho && (uint32_t)ow < (uint32_t)p.cv_Wo;
+        return ok ? (uint32_t)((cv_row0[i] + oh * (int)p.cv_Wo + ow) * (int)p.lda) + cv_chunk[i] : 0x80000000u;
+    };
+
+    // (flat tile, tap) of the next tile to issue and of the next tile to
+    // compute; issue() and step() each visit t = 0, 1, 2, ... in order
+    TapCursor icur, hcur;
     auto issue = [&](int t) {
         int8_t* st = smem + (t % T::STAGES) * T::kStage;
+        if constexpr (CONV) {
+            const int f = icur.f, tr = icur.r, ts = icur.s;
+            icur.next(taps, p.cv_KW);
+            const bool ext = HORNER && fv.is_ext(f, n_main);
+            const int k0 = ext ? (int)fv.ext_col(f, n_main) : (f - fv.h_tiles) * T::BK;
+            const __amdgpu_buffer_rsrc_t ra = ext ? rsrc(p.extA, p.a_rows, p.ld_extA) : rA;
+#pragma unroll
+            for (int i = 0; i < T::IA; ++i)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void_t*)(st + (i * T::kWaves + wv) * 1024), 16,
+                                                         conv_off(i, tr, ts), k0, 0, 0);
+#pragma unroll
+            for (int i = 0; i < T::IB; ++i)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_void_t*)(st + T::BM * T::BK + (i * T::kWaves + wv) * 1024),
+                                                         16, offB[i], t * T::BK, 0, 0);
+            return;
+        }
         if (HORNER && fv.is_ext(t, n_main)) {
             // appended fold columns (a few tiles): offsets computed here
             const __amdgpu_buffer_rsrc_t rAe = rsrc(p.extA, p.Mg, p.ld_extA), rBe = rsrc(p.extB, p.Ng, p.ld_extB);
@@ -542,7 +600,9 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
         wait_tile(min(T::STAGES - 3, n_tiles - 2 - t));
         __builtin_amdgcn_s_barrier();
         if (t + T::STAGES - 1 < n_tiles) issue(t + T::STAGES - 1);
-        if (HORNER && (int64_t)t * T::BK == hs.col) {
+        const bool region_start = CONV ? hcur.tau == 0 && (int64_t)hcur.f * T::BK == hs.col : (int64_t)t * T::BK == hs.col;
+        if constexpr (CONV) hcur.next(taps, p.cv_KW);
+        if (HORNER && region_start) {
             const int sft = hs.advance();
 #pragma unroll
             for (int i = 0; i < T::FM; ++i)
@@ -644,6 +704,308 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
                 }
             }
         }
+    }
+#endif
+}
+
+// ---------------------------------------------------------------------------
+// Input gradient of a "same" stride-1 convolution (Ho = H, Wo = W) with the
+// rows of q_fold staged once per K chunk.  Tap (r, s) of input pixel p reads
+// q_fold row p + d, d = (PH - r) W + (PW - s), so the rows a tile of BM
+// pixels needs for all taps form the contiguous window [p0 - E, p0 + BM + E),
+// E = PH W + PW.  Per 64-column chunk of the fold's flat K sequence the block
+// loads that window and the chunk's weights of every tap into LDS once, then
+// runs one round of MFMAs per tap on rows of the window shifted by d.  A tap
+// whose output pixel lies outside the image (its row belongs to another image
+// row or image) adds nothing: that lane's operand fragment is cleared.  The
+// K order (chunk-major, tap-minor) and the Horner shifts at region starts are
+// those of the per-tap kernel.
+// ---------------------------------------------------------------------------
+constexpr int kHaloBM = 256, kHaloExtra = 128, kHaloWaves = 4, kHaloMaxTaps = 9;
+
+template <bool HORNER>
+__global__ __launch_bounds__(64 * kHaloWaves) void k_conv_halo(GemmArgs p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    constexpr int BM = kHaloBM, BN = 64, BK = 64, WR = kHaloBM + kHaloExtra;   // window rows
+    constexpr int kA = WR * BK;
+    __shared__ __attribute__((aligned(1024))) int8_t smem[kA + kHaloMaxTaps * BN * BK];
+    using MF = Mfma<16>;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    const int64_t m0 = (int64_t)blockIdx.x * BM, n0 = (int64_t)blockIdx.y * BN;
+    const int taps = p.taps, KW = p.cv_KW, H = (int)p.cv_H, W = (int)p.cv_W;
+    const int E = p.cv_PH * W + p.cv_PW;
+    const FoldView fv = fold_view(p, BK);
+    const int n_main = (int)(p.K / BK);
+    const int n_chunks = fv.n_ext + n_main;
+
+    constexpr int kRsrcFlags = 0x00020000;   // raw byte buffer, gfx9 data format
+    auto rsrc = [&](const int8_t* base, int64_t rows, int64_t ld) {
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(base), (short)0,
+                                                 (int)min(rows * ld, (int64_t)0x7FFFFFFF), kRsrcFlags);
+    };
+    const __amdgpu_buffer_rsrc_t rA = rsrc(p.A, p.a_rows, p.lda), rB = rsrc(p.B, p.Ng, p.ldb);
+    const int lr = lane >> 2;
+    // window rows: instruction i of this wave fills rows (i * waves + wv) * 16 .. + 15;
+    // rows before the tensor get an offset past the end of the buffer (zeros)
+    constexpr int kWin = WR / 16 / kHaloWaves;
+    uint32_t offW[kWin];
+#pragma unroll
+    for (int i = 0; i < kWin; ++i) {
+        const int w = (i * kHaloWaves + wv) * 16 + lr;
+        const int64_t g = m0 - E + w;
+        offW[i] = g >= 0 ? (uint32_t)(g * p.lda) + 16u * (uint32_t)((lane & 3) ^ swz(w)) : 0x80000000u;
+    }
+    // weights: this wave fills rows wv * 16 .. + 15 of each tap's 64-row block
+    const int brow = wv * 16 + lr;
+    const uint32_t offBw = (uint32_t)(min(n0 + brow, p.Ng - 1) * p.ldb);
+
+    // the input pixel of each of this lane's 4 accumulator rows (one per
+    // 16-row MFMA block of the wave's 64 rows)
+    const int lrow = lane % 16, lc = lane / 16;
+    int ih[4], iw[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t pix = min(m0 + wv * 64 + i * 16 + lrow, p.Mg - 1);
+        const int hw = (int)(pix % ((int64_t)H * W));
+        ih[i] = hw / W;
+        iw[i] = hw - ih[i] * W;
+    }
+
+    v4i acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+
+    HornerSteps hs(p);
+    for (int f = 0; f < n_chunks; ++f) {
+        // stage the chunk: the row window of q_fold and every tap's weights
+        const bool ext = HORNER && fv.is_ext(f, n_main);
+        const int kc = ext ? (int)fv.ext_col(f, n_main) : (f - fv.h_tiles) * BK;
+        const __amdgpu_buffer_rsrc_t ra = ext ? rsrc(p.extA, p.a_rows, p.ld_extA) : rA;
+        __syncthreads();   // the previous chunk's reads of LDS are done
+#pragma unroll
+        for (int i = 0; i < kWin; ++i)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void_t*)(smem + (i * kHaloWaves + wv) * 1024), 16,
+                                                     offW[i], kc, 0, 0);
+        for (int tau = 0; tau < taps; ++tau) {
+            const int row = tau * BN + brow;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rB, (lds_void_t*)(smem + kA + (tau * BN + wv * 16) * BK), 16,
+                offBw + 16u * (uint32_t)((lane & 3) ^ swz(row)), (f * taps + tau) * BK, 0, 0);
+        }
+        wait_vm<0>();
+        __syncthreads();
+        if (HORNER && (int64_t)f * BK == hs.col) {
+            const int sft = hs.advance();
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = acc[i][j] << sft;
+        }
+        for (int tau = 0, tr = 0, ts = 0; tau < taps; ++tau) {
+            const int d = (p.cv_PH - tr) * W + (p.cv_PW - ts);
+            v4i fa[4], fb[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int w = wv * 64 + i * 16 + lrow + E + d;
+                const v4i v = *reinterpret_cast<const v4i*>(&smem[w * BK + 16 * (lc ^ swz(w))]);
+                const int oh = ih[i] + p.cv_PH - tr, ow = iw[i] + p.cv_PW - ts;
+                const bool ok = (unsigned)oh < (unsigned)H && (unsigned)ow < (unsigned)W;
+                fa[i] = ok ? v : v4i{0, 0, 0, 0};
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = tau * BN + j * 16 + lrow;
+                fb[j] = *reinterpret_cast<const v4i*>(&smem[kA + r * BK + 16 * (lc ^ swz(r))]);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = MF::run(fb[j], fa[i], acc[i][j]);
+            if (++ts == KW) { ts = 0; ++tr; }
+        }
+    }
+
+    // epilogue: alpha = step_G * step_W * 2^-(N_G - 1), the fold's final shift
+    const int fsh = HORNER ? fv.fshift : 0;
+    float alpha = 0.0f;
+    if (p.out) {
+        const sq_scale gs = *p.gs, os = *p.os;
+        alpha = __fmul_rn(__fmul_rn(gs.step, os.step), pow2f(-(p.num_groups - 1)));
+    }
+    const bool vec_acc = p.acc && ((p.ld_acc & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.acc) & 15) == 0);
+    const bool vec_out = p.out && ((p.ld_out & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.out) & 15) == 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t ii = m0 + wv * 64 + i * 16 + lrow;
+        if (ii >= p.Mg) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t jj = n0 + j * 16 + lc * 4;
+            if (jj >= p.Ng) continue;
+            const int vv[4] = {acc[i][j][0] << fsh, acc[i][j][1] << fsh, acc[i][j][2] << fsh, acc[i][j][3] << fsh};
+            const bool full = jj + 4 <= p.Ng;
+            if (p.acc) {
+                int32_t* dst = p.acc + ii * p.ld_acc + jj;
+                if (vec_acc && full) *reinterpret_cast<int4*>(dst) = make_int4(vv[0], vv[1], vv[2], vv[3]);
+                else
+                    for (int e = 0; e < 4; ++e)
+                        if (jj + e < p.Ng) dst[e] = vv[e];
+            }
+            if (p.out) {
+                float* dst = p.out + ii * p.ld_out + jj;
+                const float ff[4] = {__fmul_rn((float)vv[0], alpha), __fmul_rn((float)vv[1], alpha),
+                                     __fmul_rn((float)vv[2], alpha), __fmul_rn((float)vv[3], alpha)};
+                if (vec_out && full) *reinterpret_cast<float4*>(dst) = make_float4(ff[0], ff[1], ff[2], ff[3]);
+                else
+                    for (int e = 0; e < 4; ++e)
+                        if (jj + e < p.Ng) dst[e] = ff[e];
+            }
+        }
+    }
+#endif
+}
+
+// ---------------------------------------------------------------------------
+// Streaming variant of the same-size convolution input gradient for one
+// 64-column K chunk (C_out <= 64, every shift in one window) and C_in <= 64.
+// Each block owns a contiguous range of input pixels and walks it in steps of
+// 64 rows.  The weights of every tap (rows (r, s, ci) of W^T, read straight
+// from wq_t) stay in LDS; the rows of q_fold flow through an LDS ring of
+// 64-row chunks, loaded kStreamPF steps ahead, and a step's outputs go out
+// with buffer stores while the next steps compute, so the output stream (the
+// bulk of the traffic) does not wait for loads.  A wave's loads and stores
+// complete in order on gfx9, so the wait for a chunk also covers the stores
+// issued before it: every wave issues the same number of loads and stores per
+// step (rows outside the tensor or the block take offsets past the end of the
+// buffer, which the range check drops), which keeps the vmcnt waits exact.
+// Code columns >= C_out (unwritten padding of q_fold) are cleared in the
+// operand registers.
+// ---------------------------------------------------------------------------
+constexpr int kStreamRing = 8, kStreamPF = 4, kStreamNW = 3;   // ring chunks, prefetch, chunks per step
+constexpr int kStreamBlocks = 512;
+
+// Hide a value from the optimizer, so that a memory instruction whose lanes
+// take different offsets stays one instruction (not one per branch of a select).
+template <class T>
+__device__ __forceinline__ void opaque(T& v) { asm volatile("" : "+v"(v)); }
+
+template <bool ACC>
+__global__ __launch_bounds__(256) void k_conv_stream(GemmArgs p, int64_t rows_per_block) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    constexpr int BK = 64, kRing = kStreamRing * 64 * BK;
+    constexpr int NS = ACC ? 8 : 4;   // stores per lane and step
+    static_assert(kStreamNW + kStreamPF <= kStreamRing && kStreamPF * (1 + NS) <= 63, "ring / vmcnt range");
+    __shared__ __attribute__((aligned(1024))) int8_t smem[kRing + kHaloMaxTaps * 64 * BK];
+    using MF = Mfma<16>;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int taps = p.taps, KW = p.cv_KW, H = (int)p.cv_H, W = (int)p.cv_W;
+    const int E = p.cv_PH * W + p.cv_PW;
+    const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
+    const int64_t r_end = min(p.Mg, r0 + rows_per_block);
+    const int steps = (int)((r_end - r0 + 63) / 64);
+    const int lr = lane >> 2, lrow = lane % 16, lc = lane / 16;
+    constexpr int kRsrcFlags = 0x00020000;
+    auto rsrc = [&](const void* base, int64_t bytes) {
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0,
+                                                 base ? (int)min(bytes, (int64_t)0x7FFFFFFF) : 0, kRsrcFlags);
+    };
+    const __amdgpu_buffer_rsrc_t rA = rsrc(p.A, p.a_rows * p.lda), rB = rsrc(p.B, (int64_t)taps * p.Ng * p.ldb);
+    const __amdgpu_buffer_rsrc_t rO = rsrc(p.out, p.Mg * p.ld_out * 4), rC = rsrc(p.acc, p.Mg * p.ld_acc * 4);
+
+    // scalars first: their loads share the vmcnt counter with the DMA below
+    float alpha = 0.0f;
+    if (p.out) {
+        const sq_scale gs = *p.gs, os = *p.os;
+        alpha = __fmul_rn(__fmul_rn(gs.step, os.step), pow2f(-(p.num_groups - 1)));
+    }
+    const int fsh = p.layout ? p.layout[kLayF] : 0;
+    __builtin_amdgcn_s_waitcnt(0);
+
+    // weights: LDS rows tau * 64 + ci <- W^T row tau * C_in + ci; wave wv loads ci = 16 wv .. + 15
+    {
+        const int ci = wv * 16 + lr;
+        const int64_t ci_c = min((int64_t)ci, p.Ng - 1);
+        for (int tau = 0; tau < taps; ++tau) {
+            const int row = tau * 64 + ci;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rB, (lds_void_t*)(smem + kRing + (tau * 64 + wv * 16) * BK), 16,
+                (uint32_t)(((int64_t)tau * p.Ng + ci_c) * p.ldb) + 16u * (uint32_t)((lane & 3) ^ swz(row)), 0, 0, 0);
+        }
+    }
+    // chunk j of q_fold rows: r0 - E + 64 j .. + 63, in ring slot j mod kStreamRing
+    auto load_chunk = [&](int j) {
+        const int wrow = 64 * j + wv * 16 + lr;             // row of the block's window
+        const int slot_row = wrow & (kStreamRing * 64 - 1);
+        const int64_t g = r0 - E + wrow;
+        uint32_t off = g >= 0 ? (uint32_t)(g * p.lda) + 16u * (uint32_t)((lane & 3) ^ swz(slot_row)) : 0x80000000u;
+        opaque(off);   // one load instruction whatever the lanes' offsets
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void_t*)(smem + (slot_row - lr) * BK), 16, off, 0, 0, 0);
+    };
+#pragma unroll
+    for (int j = 0; j < kStreamNW + kStreamPF - 1; ++j) load_chunk(j);
+
+    const int kvalid = (int)min((int64_t)16, max((int64_t)0, p.K_used - 16 * lc));   // code bytes < C_out
+    for (int k = 0; k < steps; ++k) {
+        load_chunk(k + kStreamNW - 1 + kStreamPF);
+        // chunk k + NW - 1 (issued kStreamPF steps back) has landed once only
+        // the younger operations remain: later chunks and the stores since
+        if (k == 0) wait_vm<kStreamPF>();
+        else if (k == 1) wait_vm<kStreamPF + NS>();
+        else if (k == 2) wait_vm<kStreamPF + 2 * NS>();
+        else if (k == 3) wait_vm<kStreamPF + 3 * NS>();
+        else wait_vm<kStreamPF + 4 * NS>();
+        __builtin_amdgcn_s_barrier();   // a plain barrier: the stores stay in flight
+
+        const int64_t pix = r0 + 64 * k + wv * 16 + lrow;   // this lane's output row
+        const int hw = (int)(min(pix, p.Mg - 1) % ((int64_t)H * W));
+        const int ih = hw / W, iw = hw - (hw / W) * W;
+        v4i acc[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[j] = v4i{0, 0, 0, 0};
+        for (int tau = 0, tr = 0, ts = 0; tau < taps; ++tau) {
+            const int d = (p.cv_PH - tr) * W + (p.cv_PW - ts);
+            const int w = (64 * k + wv * 16 + lrow + E + d) & (kStreamRing * 64 - 1);
+            v4i fa = *reinterpret_cast<const v4i*>(&smem[w * BK + 16 * (lc ^ swz(w))]);
+            const int oh = ih + p.cv_PH - tr, ow = iw + p.cv_PW - ts;
+            if (!((unsigned)oh < (unsigned)H && (unsigned)ow < (unsigned)W)) fa = v4i{0, 0, 0, 0};
+            if (kvalid < 16) {
+                const uint4 m = mask_tail(make_uint4(fa[0], fa[1], fa[2], fa[3]), kvalid);
+                fa = v4i{(int)m.x, (int)m.y, (int)m.z, (int)m.w};
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = tau * 64 + j * 16 + lrow;
+                const v4i fb = *reinterpret_cast<const v4i*>(&smem[kRing + r * BK + 16 * (lc ^ swz(r))]);
+                acc[j] = MF::run(fb, fa, acc[j]);
+            }
+            if (++ts == KW) { ts = 0; ++tr; }
+        }
+        // NS / 4 stores per column group: the fp32 output (a NULL output has
+        // an empty range) and, with ACC, the int32 accumulator
+        const bool row_ok = pix < r_end;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int col = j * 16 + lc * 4;
+            const bool ok = row_ok && col < p.Ng;
+            const int v0 = acc[j][0] << fsh, v1 = acc[j][1] << fsh, v2 = acc[j][2] << fsh, v3 = acc[j][3] << fsh;
+            typedef unsigned u4 __attribute__((ext_vector_type(4)));
+            const u4 fo = {__float_as_uint(__fmul_rn((float)v0, alpha)), __float_as_uint(__fmul_rn((float)v1, alpha)),
+                           __float_as_uint(__fmul_rn((float)v2, alpha)), __float_as_uint(__fmul_rn((float)v3, alpha))};
+            int oo = ok ? (int)((pix * p.ld_out + col) * 4) : (int)0x80000000;
+            opaque(oo);
+            __builtin_amdgcn_raw_buffer_store_b128(fo, rO, oo, 0, 0);
+            if constexpr (ACC) {
+                const u4 io = {(unsigned)v0, (unsigned)v1, (unsigned)v2, (unsigned)v3};
+                int oc = ok ? (int)((pix * p.ld_acc + col) * 4) : (int)0x80000000;
+                opaque(oc);
+                __builtin_amdgcn_raw_buffer_store_b128(io, rC, oc, 0, 0);
+            }
+        }
+        __builtin_amdgcn_s_barrier();   // the ring slots of this step may be refilled
     }
 #endif
 }
@@ -775,12 +1137,13 @@ hipError_t launch_cfg(const GemmArgs& a, int splits, int64_t k_per_split, hipStr
     return hipGetLastError();
 }
 
-template <class T, bool HORNER>
+template <class T, bool HORNER, bool CONV = false>
 hipError_t launch_pipe(const GemmArgs& a, int splits, int64_t k_per_split, hipStream_t s) {
     const int64_t tiles_m = (a.Mg + T::BM - 1) / T::BM, tiles_n = (a.Ng + T::BN - 1) / T::BN;
     if (tiles_m * tiles_n > 0x7FFFFFFF || splits > 65535) return hipErrorInvalidValue;
     dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)splits);
-    hipLaunchKernelGGL((k_gemm_pipe<T, HORNER>), grid, dim3(T::kThreads), 0, s, a, tiles_m, tiles_n, k_per_split);
+    hipLaunchKernelGGL((k_gemm_pipe<T, HORNER, CONV>), grid, dim3(T::kThreads), 0, s, a, tiles_m, tiles_n,
+                       k_per_split);
     return hipGetLastError();
 }
 
@@ -874,6 +1237,82 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     if (p == Pick::kSkinny) return launch_pipe<PipeSkinny, false>(a, splits, per * 64, s);
     return a.extA ? launch_pipe<PipeSmall, true>(a, splits, per * 64, s)
                   : launch_pipe<PipeSmall, false>(a, splits, per * 64, s);
+}
+
+// B operand of the conv dgrad: bc[ci, t * 64 + e] for K tile t = f * taps + tau
+// is column f * 64 + e of the fold's flat sequence (appended columns [0, H),
+// main columns, appended columns [H, D)) for weight column (tau, ci): the W^T
+// code of that column's channel, 0 for padding and for channels >= C_out.
+__global__ void k_conv_gather_w(const int8_t* __restrict__ wq_t, int64_t ld_w, int64_t C_out, int64_t C_in, int taps,
+                                const int32_t* __restrict__ layout, int8_t* __restrict__ bc, int64_t ld_bc) {
+    const int64_t H = layout[kLayH], D = layout[kLayD], base = layout[kLayBase];
+    const int32_t* ext = layout + kLayoutHeader;
+    const int64_t ncols = (int64_t)taps * (base + D);
+    for (int64_t ci = blockIdx.y; ci < C_in; ci += gridDim.y)
+        for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < ncols; j += (int64_t)gridDim.x * blockDim.x) {
+            const int64_t t = j / 64, f = t / taps, tau = t - f * taps;
+            const int64_t k = f * 64 + j % 64;
+            int64_t ch;
+            if (k < H) ch = ext[k];
+            else if (k < H + base) ch = k - H < C_out ? k - H : -1;
+            else ch = ext[k - base];
+            bc[ci * ld_bc + j] = ch >= 0 ? wq_t[(tau * C_in + ci) * ld_w + ch] : (int8_t)0;
+        }
+}
+
+hipError_t launch_conv_gather_w(const int8_t* wq_t, int64_t ld_w, int64_t C_out, int64_t C_in, int taps,
+                                const int32_t* layout, int8_t* bc, int64_t ld_bc, hipStream_t s) {
+    if (C_in <= 0 || C_out <= 0) return hipSuccess;
+    const dim3 grid((unsigned)std::min<int64_t>((ld_bc + 255) / 256, 64), (unsigned)std::min<int64_t>(C_in, 1024));
+    hipLaunchKernelGGL(k_conv_gather_w, grid, dim3(256), 0, s, wq_t, ld_w, C_out, C_in, taps, layout, bc, ld_bc);
+    return hipGetLastError();
+}
+
+// Conv dgrad: a.K is the main width of the fold (a multiple of 64), a.A /
+// a.extA the main and appended columns of q_fold ([a_rows, lda]), a.B / a.ldb
+// the W^T codes.  Same-size convolutions with one K chunk and a narrow output
+// stream (k_conv_stream, weights straight from W^T); the others gather the
+// weights into bc in the implicit GEMM's K order and take the window kernel
+// (same size, small window) or the per-tap pipelined kernel.
+hipError_t launch_conv_dgrad(const GemmArgs& a0, int8_t* bc, int64_t ld_bc, hipStream_t s) {
+    if (a0.Mg <= 0 || a0.Ng <= 0) return hipSuccess;
+    auto al16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+    auto fits = [](int64_t rows, int64_t ld) { return rows * ld < ((int64_t)1 << 31); };
+    if (a0.taps < 1 || a0.K % 64 != 0 || a0.lda % 16 != 0 || a0.ldb % 16 != 0 || !al16(a0.A) || !al16(a0.B) ||
+        !fits(a0.a_rows, a0.lda) || !fits((int64_t)a0.taps * a0.Ng, a0.ldb) || a0.Mg > 0x7FFFFFFF)
+        return hipErrorInvalidValue;
+    if (a0.extA && (a0.ld_extA != a0.lda || !al16(a0.extA))) return hipErrorInvalidValue;
+    const bool same = a0.cv_Ho == a0.cv_H && a0.cv_Wo == a0.cv_W;
+    auto small_out = [](const void* q, int64_t rows, int64_t ld) {
+        return !q || (((reinterpret_cast<uintptr_t>(q) & 15) == 0) && ld % 4 == 0 && rows * ld * 4 < ((int64_t)1 << 31));
+    };
+    if (same && !a0.extA && a0.K == 64 && a0.taps <= kHaloMaxTaps && (int64_t)a0.cv_PH * a0.cv_W + a0.cv_PW <= 64 &&
+        a0.Ng <= 64 && a0.Ng % 4 == 0 && small_out(a0.out, a0.Mg, a0.ld_out) && small_out(a0.acc, a0.Mg, a0.ld_acc)) {
+        const int64_t blocks = std::min<int64_t>(kStreamBlocks, (a0.Mg + 63) / 64);
+        const int64_t rows = (a0.Mg + blocks - 1) / blocks;
+        const dim3 grid((unsigned)((a0.Mg + rows - 1) / rows));
+        if (a0.acc) hipLaunchKernelGGL(k_conv_stream<true>, grid, dim3(256), 0, s, a0, rows);
+        else hipLaunchKernelGGL(k_conv_stream<false>, grid, dim3(256), 0, s, a0, rows);
+        return hipGetLastError();
+    }
+    // weights in the K order of the implicit GEMM
+    hipError_t e = launch_conv_gather_w(a0.B, a0.ldb, a0.K_used, a0.Ng, a0.taps, a0.layout, bc, ld_bc, s);
+    if (e != hipSuccess) return e;
+    GemmArgs a = a0;
+    a.B = bc;
+    a.ldb = ld_bc;
+    if (!fits(a.Ng, a.ldb)) return hipErrorInvalidValue;
+    const int64_t kps = a.K;
+    if (same && a.taps <= kHaloMaxTaps && 2 * ((int64_t)a.cv_PH * a.cv_W + a.cv_PW) <= kHaloExtra) {
+        const dim3 grid((unsigned)((a.Mg + kHaloBM - 1) / kHaloBM), (unsigned)((a.Ng + 63) / 64));
+        if (grid.y > 65535) return hipErrorInvalidValue;
+        if (a.extA) hipLaunchKernelGGL(k_conv_halo<true>, grid, dim3(64 * kHaloWaves), 0, s, a);
+        else hipLaunchKernelGGL(k_conv_halo<false>, grid, dim3(64 * kHaloWaves), 0, s, a);
+        return hipGetLastError();
+    }
+    if (a.Ng <= 64)
+        return a.extA ? launch_pipe<PipeNarrow, true, true>(a, 1, kps, s) : launch_pipe<PipeNarrow, false, true>(a, 1, kps, s);
+    return a.extA ? launch_pipe<PipeSmall, true, true>(a, 1, kps, s) : launch_pipe<PipeSmall, false, true>(a, 1, kps, s);
 }
 
 hipError_t launch_gather_ext(const int8_t* wq_t, int64_t ld_w, int64_t C_in, const int32_t* layout,

@@ -107,11 +107,30 @@ struct GemmArgs {
     const sq_scale* os;
     const uint8_t* group;
     int num_groups;
+    // Implicit-im2col convolution (conv dgrad), used when taps > 0: output
+    // row (n, ih, iw) of [Mg = N * H * W], and A = q_fold rows of the
+    // N * Ho * Wo output pixels (a_rows of them).  K visits every 64-column
+    // tile of the fold's flat sequence once per tap (r, s) of the KH x KW
+    // window, reading A row (n, ih + PH - r, iw + PW - s), or zeros where that
+    // pixel lies outside the Ho x Wo grid; B holds the matching weight columns.
+    int taps;
+    int cv_KW, cv_PH, cv_PW;
+    int64_t cv_H, cv_W, cv_Ho, cv_Wo, a_rows;
+    int64_t K_used;                 // code columns in use (C_out)
 };
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gather_ext(const int8_t* wq_t, int64_t ld_w, int64_t C_in, const int32_t* layout,
                              int8_t* wext, int64_t ld_ext, int64_t ext_max, hipStream_t s);
+// Conv dgrad: B operand [C_in, ld_bc] in the order of the conv K sequence;
+// conv_bc_ld(C_out, taps, ext_max) is its leading dimension, enough for any fold.
+inline int64_t conv_bc_ld(int64_t C_out, int64_t taps, int64_t ext_max) {
+    return round_up(taps * (round_up(C_out, kFoldPad) + ext_max), 64);
+}
+// Conv dgrad: a describes the product with a.B = wq_t (W^T codes [taps * C_in,
+// ld_w]); kernels that need the weights in the K order of the implicit GEMM
+// gather them into bc first.
+hipError_t launch_conv_dgrad(const GemmArgs& a, int8_t* bc, int64_t ld_bc, hipStream_t s);
 hipError_t launch_splitk_reduce(const int32_t* ws, int splits, const GemmArgs& a, hipStream_t s);
 hipError_t launch_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_t ld_acc, int kind,
                           const uint8_t* group, const sq_scale* gs, const sq_scale* os,

@@ -36,8 +36,8 @@ FLAG_ZERO = 2
 # Every symbol include/shiftquant.h declares.
 EXPORTS = (
     "sq_grad_layout_size", "sq_quantize_grad_workspace_size", "sq_quantize_tensor_workspace_size",
-    "sq_gemm_dgrad_workspace_size", "sq_gemm_wgrad_workspace_size",
-    "sq_quantize_grad", "sq_quantize_tensor", "sq_gemm_dgrad", "sq_gemm_wgrad", "sq_dequant",
+    "sq_gemm_dgrad_workspace_size", "sq_gemm_wgrad_workspace_size", "sq_conv_dgrad_workspace_size",
+    "sq_quantize_grad", "sq_quantize_tensor", "sq_gemm_dgrad", "sq_gemm_wgrad", "sq_conv_dgrad", "sq_dequant",
     "sq_status_string", "sq_last_error",
 )
 
@@ -87,6 +87,9 @@ def load() -> ct.CDLL:
         "sq_gemm_wgrad": [_P, _I64, _P, _P, _P, _I64, _P, _I64, _I64, _I64, pp, _P, _I64, _P, _I64, _P,
                           _SZ, _P],
         "sq_dequant": [_P, _I64, _I64, _I64, ct.c_int32, _P, _P, _P, ct.c_int32, _P, _I64, _P],
+        "sq_conv_dgrad_workspace_size": [_I64, _I64, ct.c_int32, ct.c_int32, pp, ct.POINTER(_SZ)],
+        "sq_conv_dgrad": [_P, _I64, _P, _P, _P, _P, _I64, _P, _I64, _I64, _I64, _I64, _I64, ct.c_int32,
+                          ct.c_int32, ct.c_int32, ct.c_int32, pp, _P, _I64, _P, _I64, _P, _SZ, _P],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -170,6 +173,13 @@ def sq_gemm_wgrad_workspace_size(M: int, C_out: int, C_in: int, params: Params) 
     return nb.value
 
 
+def sq_conv_dgrad_workspace_size(C_out: int, C_in: int, KH: int, KW: int, params: Params) -> int:
+    nb = _SZ(0)
+    _check("sq_conv_dgrad_workspace_size",
+           load().sq_conv_dgrad_workspace_size(C_out, C_in, KH, KW, ct.byref(params), ct.byref(nb)))
+    return nb.value
+
+
 def sq_quantize_grad(dY, params, q_fold, q_t, group, scale, layout, workspace, stream=None) -> None:
     M, C = dY.shape
     ws, nws = _ws_ptr(workspace)
@@ -193,6 +203,15 @@ def sq_gemm_dgrad(q_fold, layout, group, gscale, wq_t, wscale, M, C_out, C_in, p
         _ptr(q_fold), _ld(q_fold), _ptr(layout), _ptr(group), _ptr(gscale), _ptr(wq_t), _ld(wq_t),
         _ptr(wscale), M, C_out, C_in, ct.byref(params), _ptr(acc), _ld(acc), _ptr(dX), _ld(dX),
         ws, nws, _stream(stream)))
+
+
+def sq_conv_dgrad(q_fold, layout, group, gscale, wq_t, wscale, N, H, W, C_out, C_in, KH, KW, PH, PW, params,
+                  acc, dX, workspace, stream=None) -> None:
+    ws, nws = _ws_ptr(workspace)
+    _check("sq_conv_dgrad", load().sq_conv_dgrad(
+        _ptr(q_fold), _ld(q_fold), _ptr(layout), _ptr(group), _ptr(gscale), _ptr(wq_t), _ld(wq_t),
+        _ptr(wscale), N, H, W, C_out, C_in, KH, KW, PH, PW, ct.byref(params), _ptr(acc), _ld(acc),
+        _ptr(dX), _ld(dX), ws, nws, _stream(stream)))
 
 
 def sq_gemm_wgrad(q_t, group, gscale, xq_t, xscale, M, C_out, C_in, params, acc, dW, workspace,
@@ -292,6 +311,23 @@ def gemm_dgrad(codes: GradCodes, wq_t: torch.Tensor, wscale: torch.Tensor, want_
     return acc, dX
 
 
+def conv_dgrad(codes: GradCodes, wq_t: torch.Tensor, wscale: torch.Tensor, N: int, H: int, W: int,
+               KH: int, KW: int, PH: int, PW: int, want_acc: bool = False, want_out: bool = True, stream=None):
+    """Input gradient [N*H*W, C_in] (NHWC) of a stride-1 convolution whose output
+    gradient was quantized into `codes` ([N*Ho*Wo, C_out]); wq_t holds the W^T
+    codes of W [C_out, KH*KW*C_in] (columns in (r, s, ci) order)."""
+    C_out = codes.C_out
+    C_in = wq_t.shape[0] // (KH * KW)
+    assert wq_t.shape[0] == KH * KW * C_in
+    dev = wq_t.device
+    acc = torch.empty((N * H * W, C_in), dtype=torch.int32, device=dev) if want_acc else None
+    dX = torch.empty((N * H * W, C_in), dtype=torch.float32, device=dev) if want_out else None
+    ws = _workspace(sq_conv_dgrad_workspace_size(C_out, C_in, KH, KW, codes.params), dev)
+    sq_conv_dgrad(codes.q_fold, codes.layout, codes.group, codes.scale, wq_t, wscale, N, H, W, C_out, C_in,
+                  KH, KW, PH, PW, codes.params, acc, dX, ws, stream)
+    return acc, dX
+
+
 def gemm_wgrad(codes: GradCodes, xq_t: torch.Tensor, xscale: torch.Tensor, want_acc: bool = False,
                want_out: bool = True, stream=None):
     M, C_out, C_in = codes.M, codes.C_out, xq_t.shape[0]
@@ -344,3 +380,27 @@ class BackwardPlan:
         self.dgrad(wq_t, wscale, stream)
         self.wgrad(xq_t, xscale, stream)
         return self.dX, self.dW
+
+
+class ConvBackwardPlan(BackwardPlan):
+    """Backward step of a stride-1 convolution lowered by im2col, with the input
+    gradient taken by sq_conv_dgrad (implicit im2col and col2im: dX is
+    [N*H*W, C_in_ch], NHWC) and the weight gradient by sq_gemm_wgrad on the
+    im2col'd activations.  Buffers are allocated once; ``run`` allocates
+    nothing."""
+
+    def __init__(self, N: int, H: int, W: int, C_out: int, C_in_ch: int, KH: int, KW: int, PH: int, PW: int,
+                 params: Params, device="cuda", want_acc: bool = False):
+        Ho, Wo = H + 2 * PH - KH + 1, W + 2 * PW - KW + 1
+        super().__init__(N * Ho * Wo, C_out, KH * KW * C_in_ch, params, device, want_acc)
+        dev = torch.device(device)
+        self.geom = (N, H, W, KH, KW, PH, PW)
+        self.C_in_ch = C_in_ch
+        self.ws_d = _workspace(sq_conv_dgrad_workspace_size(C_out, C_in_ch, KH, KW, params), dev)
+        self.dX = torch.empty((N * H * W, C_in_ch), dtype=torch.float32, device=dev)
+        self.acc_dX = torch.empty((N * H * W, C_in_ch), dtype=torch.int32, device=dev) if want_acc else None
+
+    def dgrad(self, wq_t, wscale, stream=None):
+        N, H, W, KH, KW, PH, PW = self.geom
+        sq_conv_dgrad(self.q_fold, self.layout, self.group, self.scale, wq_t, wscale, N, H, W, self.C_out,
+                      self.C_in_ch, KH, KW, PH, PW, self.params, self.acc_dX, self.dX, self.ws_d, stream)

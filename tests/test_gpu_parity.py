@@ -445,6 +445,86 @@ def test_wgrad_narrow_outputs(sq, shape):
     check_layer(sq, dY, W, X, 4, 4, dgrad_rows=[0, 1, M // 2, M - 1])
 
 
+# ---------------------------------------------------------------------------
+# convolution input gradient with implicit im2col / col2im
+# ---------------------------------------------------------------------------
+CONV_GPU_CASES = [  # N, H, W, C_out, C_in, KH, KW, PH, PW, bits, N_G
+    (2, 9, 7, 64, 64, 3, 3, 1, 1, 4, 4),      # same-size 3x3: several tiles, ragged last tile
+    (1, 13, 11, 48, 40, 3, 3, 1, 1, 6, 4),    # fold with appended windows; C_out, C_in not multiples of 64
+    (1, 10, 12, 96, 160, 3, 3, 0, 1, 4, 4),   # unpadded rows, padded columns; C_in > 64
+    (2, 6, 5, 32, 24, 1, 1, 0, 0, 8, 3),      # 1 x 1 window
+    (1, 8, 8, 64, 64, 5, 5, 2, 2, 4, 4),      # 5 x 5 window
+    (1, 7, 9, 130, 64, 2, 3, 1, 0, 6, 4),     # even window height, one-sided padding
+    (3, 4, 4, 200, 72, 3, 3, 1, 1, 8, 4),     # 8-bit codes: several appended windows
+    (1, 5, 63, 64, 64, 3, 3, 1, 1, 4, 4),     # widest image whose row window is staged whole
+    (1, 4, 64, 64, 64, 3, 3, 1, 1, 4, 4),     # one column wider: per-tap loads
+    (2, 5, 6, 64, 32, 1, 3, 0, 1, 6, 4),      # 1 x 3 window
+]
+
+
+def _conv_layer(N, H, W, C_out, C_in, KH, KW, PH, PW, seed):
+    Ho, Wo = H + 2 * PH - KH + 1, W + 2 * PW - KW + 1
+    rng = np.random.default_rng(seed)
+    dY = _grad(N * Ho * Wo, C_out, seed=seed)
+    Wt = (rng.standard_normal((C_out, KH * KW * C_in)) * np.sqrt(2.0 / (KH * KW * C_in))).astype(np.float32)
+    return dY, Wt
+
+
+def check_conv(sq, case, pix=None, mode=0):
+    import torch
+    N, H, W, C_out, C_in, KH, KW, PH, PW, bits, ng = case
+    dY, Wt = _conv_layer(N, H, W, C_out, C_in, KH, KW, PH, PW, seed=sum(case))
+    codes = sq.quantize_grad(_dev(dY), bits, ng, mode, 7, 0)
+    wq_t, ws = sq.quantize_tensor(_dev(Wt), 8, transpose=True)
+    acc, dX = sq.conv_dgrad(codes, wq_t, ws, N, H, W, KH, KW, PH, PW, want_acc=True)
+    _, dX2 = sq.conv_dgrad(codes, wq_t, ws, N, H, W, KH, KW, PH, PW, want_acc=False)
+    torch.cuda.synchronize()
+    q_ref, g_ref, s_ref = check_quant(sq, codes, dY, bits, ng, mode, 7, 0, fold_rows=None if pix is None else [0])
+    wq_ref, ws_ref = oracle.quantize_tensor(Wt, 8)
+    A_ref = oracle.conv_dgrad(q_ref, g_ref, ng, wq_ref, N, H, W, KH, KW, PH, PW, pix)
+    dX_ref = oracle.dequant_dgrad(A_ref, s_ref["d0"], ws_ref["d0"], ng)
+    rows = torch.arange(N * H * W, device="cuda") if pix is None else torch.as_tensor(pix, device="cuda")
+    got = acc.index_select(0, rows).cpu().numpy()
+    bad = np.argwhere(got != A_ref)
+    assert bad.size == 0, f"{len(bad)} conv dgrad accumulators differ, first at {bad[:4].tolist()}"
+    np.testing.assert_allclose(dX.index_select(0, rows).cpu().numpy(), dX_ref, rtol=RTOL, atol=0)
+    assert torch.equal(dX, dX2)
+
+
+@pytest.mark.parametrize("case", CONV_GPU_CASES, ids=["x".join(map(str, c)) for c in CONV_GPU_CASES])
+def test_conv_dgrad_parity(sq, case):
+    check_conv(sq, case)
+
+
+def test_conv_dgrad_stochastic_codes(sq):
+    check_conv(sq, (1, 9, 9, 72, 64, 3, 3, 1, 1, 6, 4), mode=1)
+
+
+def test_conv_dgrad_full_resnet18_layer(sq):
+    # the full 64 x 56 x 56 x 64 layer; pixels sampled on image borders,
+    # corners, tile boundaries and interiors
+    N, H, W = 64, 56, 56
+    rng = np.random.default_rng(11)
+    picks = []
+    for n in (0, 1, 31, 63):
+        for ih, iw in ((0, 0), (0, 55), (55, 0), (55, 55), (0, 27), (27, 0), (55, 31), (13, 55), (28, 28)):
+            picks.append((n * H + ih) * W + iw)
+    picks += [255, 256, 511, 512, 3135, 3136] + list(rng.integers(0, N * H * W, 200))
+    check_conv(sq, (N, H, W, 64, 64, 3, 3, 1, 1, 4, 4), pix=np.array(sorted(set(int(p) for p in picks))))
+
+
+def test_conv_dgrad_rejects_bad_geometry(sq):
+    import torch
+    dY, Wt = _conv_layer(1, 5, 5, 16, 8, 3, 3, 1, 1, seed=1)
+    codes = sq.quantize_grad(_dev(dY), 4, 4)
+    wq_t, ws = sq.quantize_tensor(_dev(Wt), 8, transpose=True)
+    with pytest.raises(sq.ShiftQuantError):
+        sq.conv_dgrad(codes, wq_t, ws, 1, 5, 5, 3, 3, 3, 1)      # padding >= window
+    with pytest.raises(sq.ShiftQuantError):
+        sq.conv_dgrad(codes, wq_t, ws, 1, 1, 5, 3, 3, 0, 1)      # window taller than the input
+    torch.cuda.synchronize()
+
+
 def test_degenerate_layers(sq):
     rng = np.random.default_rng(2)
     W = (rng.standard_normal((40, 24)) * 0.02).astype(np.float32)
