@@ -937,11 +937,13 @@ __global__ __launch_bounds__(256) void k_conv_stream(GemmArgs p, int64_t rows_pe
         }
     }
     // chunk j of q_fold rows: r0 - E + 64 j .. + 63, in ring slot j mod kStreamRing
+    const int64_t win_rows = (r_end - r0) + 2 * E;   // rows of the block's window (chunks past it load nothing)
     auto load_chunk = [&](int j) {
         const int wrow = 64 * j + wv * 16 + lr;             // row of the block's window
         const int slot_row = wrow & (kStreamRing * 64 - 1);
         const int64_t g = r0 - E + wrow;
-        uint32_t off = g >= 0 ? (uint32_t)(g * p.lda) + 16u * (uint32_t)((lane & 3) ^ swz(slot_row)) : 0x80000000u;
+        uint32_t off = g >= 0 && wrow < win_rows ? (uint32_t)(g * p.lda) + 16u * (uint32_t)((lane & 3) ^ swz(slot_row))
+                                                 : 0x80000000u;
         opaque(off);   // one load instruction whatever the lanes' offsets
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void_t*)(smem + (slot_row - lr) * BK), 16, off, 0, 0, 0);
     };
