@@ -100,6 +100,12 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--bits", type=int, default=None, help="override the workload's gradient bits (variant runs)")
+    ap.add_argument("--num-groups", type=int, default=None, help="override the workload's N_G (variant runs)")
+    ap.add_argument("--rounding", choices=["rtn", "sr"], default=None,
+                    help="override the workload's rounding (variant runs)")
+    ap.add_argument("--dgrad", choices=["shiftmm", "grouped"], default="shiftmm",
+                    help="grouped: the GEMM-based comparison implementation of the dgrad (Sec. 3.2)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 256 MiB device-to-device copy first (reference for HBM byte counters)")
     args = ap.parse_args(argv)
@@ -119,6 +125,12 @@ def main(argv=None):
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     conv = args.workload in FUSED_CONV
     wl = workloads.WORKLOADS[FUSED_CONV.get(args.workload, args.workload)]
+    # parameter variants of the same layer (same tensors, other b / N_G / rounding)
+    import dataclasses
+    over = {k: v for k, v in (("bits", args.bits), ("num_groups", args.num_groups),
+                                ("round_mode", None if args.rounding is None else int(args.rounding == "sr")))
+            if v is not None}
+    wl = dataclasses.replace(wl, **over)
     inputs = workloads.make_inputs(wl.name)
     M, C_out, C_in = inputs["M"], wl.C_out, wl.C_in
     print(f"[bench] {args.workload}: M={M} C_out={C_out} C_in={C_in} b={wl.bits} N_G={wl.num_groups} "
@@ -136,7 +148,7 @@ def main(argv=None):
         n_img = M // (wl.conv_hw * wl.conv_hw)
         plan = sq.ConvBackwardPlan(n_img, wl.conv_hw, wl.conv_hw, C_out, wl.conv_cin, 3, 3, 1, 1, params, device=dev)
     else:
-        plan = sq.BackwardPlan(M, C_out, C_in, params, device=dev)
+        plan = sq.BackwardPlan(M, C_out, C_in, params, device=dev, grouped_dgrad=args.dgrad == "grouped")
     stream = torch.cuda.current_stream()
     if args.calibrate_copy:
         src = torch.empty(64 << 20, dtype=torch.float32, device=dev).fill_(1.0)
@@ -223,6 +235,7 @@ def main(argv=None):
         "config": {"workload": args.workload, "M": M, "C_out": C_out, "C_in": C_in, "bits": wl.bits,
                    "num_groups": wl.num_groups, "rounding": "stochastic" if wl.round_mode else "nearest-even",
                    "dgrad_output": "dX [N,H,W,C] (implicit im2col + col2im)" if conv else "dX_col [M, C_in]",
+                   "dgrad_impl": "shiftmm" if conv else args.dgrad,
                    "parallelism": "none"},
         "pct_int8_peak": 100.0 * value / PEAK_INT8_TOPS,
         "breakdown_ms": {k: v["ms"] for k, v in parts.items()},

@@ -227,6 +227,29 @@ sq_status sq_gemm_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, c
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * sq_gemm_dgrad_grouped -- the GEMM-based implementation of the same loss
+ * propagation, kept as a comparison for ShiftMM.
+ *
+ * Sec. 3.2 describes it in three steps: extract one pair of smaller matrices
+ * per group (memory rearrangement: the group's code columns and weight rows
+ * side by side), multiply each pair with a plain GEMM, then shift each
+ * product by N_G - 1 - g and sum.  The result is the accumulator and dX of
+ * sq_gemm_dgrad, bit for bit; only the cost differs.
+ * Inputs, outputs and errors as sq_gemm_dgrad; the workspace
+ * (sq_gemm_dgrad_grouped_workspace_size bytes, 256-byte aligned) holds the
+ * rearranged operands [M + C_in, C_out + 63 N_G] and N_G int32 products
+ * [M, C_in].  SQ_ERR_UNSUPPORTED when a rearranged operand spans 2^31 bytes.
+ * ------------------------------------------------------------------------- */
+sq_status sq_gemm_dgrad_grouped_workspace_size(int64_t M, int64_t C_out, int64_t C_in,
+                                               const sq_quant_params* p, size_t* bytes);
+sq_status sq_gemm_dgrad_grouped(const int8_t* q_fold, int64_t ld_fold, const int32_t* layout,
+                                const uint8_t* group, const sq_scale* gscale,
+                                const int8_t* wq_t, int64_t ld_w, const sq_scale* wscale,
+                                int64_t M, int64_t C_out, int64_t C_in, const sq_quant_params* p,
+                                int32_t* acc, int64_t ld_acc, float* dX, int64_t ld_dX,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * sq_conv_dgrad -- input gradient of a stride-1 convolution, im2col and
  * col2im both implicit.
  *

@@ -278,6 +278,87 @@ sq_status sq_gemm_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* la
     return hip_status(launch_gemm(a, s), "gemm_dgrad");
 }
 
+static int64_t grouped_ws_parts(int64_t M, int64_t C_out, int64_t C_in, const QuantCfg& cfg, int64_t* off_a,
+                                 int64_t* off_b, int64_t* off_p) {
+    const int64_t wmax = grouped_width(C_out, cfg.num_groups);
+    *off_a = round_up(4 * (16 + 2 * wmax), 256);
+    *off_b = *off_a + round_up(M * wmax, 256);
+    *off_p = *off_b + round_up(C_in * wmax, 256);
+    return *off_p + round_up((int64_t)cfg.num_groups * M * C_in * 4, 256);
+}
+
+sq_status sq_gemm_dgrad_grouped_workspace_size(int64_t M, int64_t C_out, int64_t C_in, const sq_quant_params* p,
+                                               size_t* bytes) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_dims(M, C_out, "gradient"));
+    SQ_TRY(check_dims(C_in, C_in, "weight"));
+    if (!bytes) return fail(SQ_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    int64_t a, b, c;
+    *bytes = (size_t)grouped_ws_parts(M, C_out, C_in, make_cfg(*p), &a, &b, &c);
+    return SQ_OK;
+}
+
+sq_status sq_gemm_dgrad_grouped(const int8_t* q_fold, int64_t ld_fold, const int32_t* layout, const uint8_t* group,
+                                const sq_scale* gscale, const int8_t* wq_t, int64_t ld_w, const sq_scale* wscale,
+                                int64_t M, int64_t C_out, int64_t C_in, const sq_quant_params* p, int32_t* acc,
+                                int64_t ld_acc, float* dX, int64_t ld_dX, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_dims(M, C_out, "gradient codes"));
+    SQ_TRY(check_dims(C_in, C_in, "weight codes"));
+    if (!acc && !dX) return fail(SQ_ERR_INVALID_ARGUMENT, "acc and dX are both NULL");
+    if (!layout || !gscale || !wscale) return fail(SQ_ERR_INVALID_ARGUMENT, "layout or a scale is NULL");
+    const QuantCfg cfg = make_cfg(*p);
+    const double bound = (double)C_out * cfg.Q * (double)(1 << (cfg.num_groups - 1)) * 128.0;
+    if (bound >= 2147483648.0)
+        return fail(SQ_ERR_OVERFLOW_RISK, "C_out * Q * 2^(N_G-1) * 128 reaches 2^31: the int32 accumulator could overflow");
+    if (M == 0 || C_in == 0) return SQ_OK;
+    size_t lay_bytes = 0;
+    int64_t min_ld_fold = 0;
+    SQ_TRY(sq_grad_layout_size(C_out, p, &lay_bytes, &min_ld_fold));
+    SQ_TRY(check_codes(q_fold, ld_fold, min_ld_fold, "q_fold"));
+    SQ_TRY(check_codes(wq_t, ld_w, C_out > 0 ? C_out : 1, "wq_t"));
+    if (acc) SQ_TRY(check_f32(acc, ld_acc, C_in, "acc"));
+    if (dX) SQ_TRY(check_f32(dX, ld_dX, C_in, "dX"));
+    int64_t off_a, off_b, off_p;
+    const int64_t need = grouped_ws_parts(M, C_out, C_in, cfg, &off_a, &off_b, &off_p);
+    if (!workspace || !aligned(workspace, 256)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or not 256-byte aligned");
+    if (workspace_bytes < (size_t)need) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+    if (M * grouped_width(C_out, cfg.num_groups) >= ((int64_t)1 << 31) ||
+        C_in * grouped_width(C_out, cfg.num_groups) >= ((int64_t)1 << 31))
+        return fail(SQ_ERR_UNSUPPORTED, "grouped dgrad: a rearranged operand spans 2^31 bytes or more");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    int8_t* ws = static_cast<int8_t*>(workspace);
+    int32_t* plan = reinterpret_cast<int32_t*>(ws);
+    int8_t* A_r = ws + off_a;
+    int8_t* B_r = ws + off_b;
+    int32_t* part = reinterpret_cast<int32_t*>(ws + off_p);
+    const int64_t wmax = grouped_width(C_out, cfg.num_groups);
+    const int32_t* desc = layout + kLayoutHeader + fold_ext_max(C_out, cfg);
+    // 1. memory rearrangement: the channels of each group side by side
+    SQ_TRY(hip_status(launch_group_plan(group, C_out, cfg.num_groups, desc, fold_ext_base(C_out), plan, wmax, s),
+                      "group_plan"));
+    // codes: q_fold column and fold shift per rearranged column; weights: the channel itself
+    SQ_TRY(hip_status(launch_gather_cols(q_fold, ld_fold, M, plan + 16 + wmax, wmax, A_r, wmax, s), "rearrange codes"));
+    SQ_TRY(hip_status(launch_gather_cols(wq_t, ld_w, C_in, plan + 16, wmax, B_r, wmax, s), "rearrange weights"));
+    // 2. one GEMM per group over its columns
+    for (int g = 0; g < cfg.num_groups; ++g) {
+        GemmArgs a{};
+        a.Mg = M; a.Ng = C_in;
+        a.A = A_r; a.lda = wmax;
+        a.B = B_r; a.ldb = wmax;
+        a.K = wmax;
+        a.kseg = plan + 2 * g;
+        a.splits = 1;
+        a.acc = part + (int64_t)g * M * C_in; a.ld_acc = C_in;
+        a.gs = gscale; a.os = wscale; a.group = group; a.num_groups = cfg.num_groups;
+        SQ_TRY(hip_status(launch_gemm(a, s), "group gemm"));
+    }
+    // 3. shift and sum
+    return hip_status(launch_group_combine(part, cfg.num_groups, M, C_in, acc, ld_acc, dX, ld_dX, gscale, wscale, s),
+                      "group_combine");
+}
+
 static sq_status check_conv(int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t C_in, int32_t KH, int32_t KW,
                             int32_t PH, int32_t PW) {
     if (N < 0 || H < 1 || W < 1 || C_out < 0 || C_in < 0)

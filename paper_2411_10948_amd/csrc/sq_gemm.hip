@@ -439,8 +439,10 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
     const int64_t m0 = tm * T::BM, n0 = tn * T::BN;
 
     const FoldView fv = fold_view(p, T::BK);
+    int64_t koff = 0, Kd = p.K;   // K range: [0, K), or a device-side segment
+    if (p.kseg) { koff = p.kseg[0]; Kd = p.kseg[1]; }
     const int64_t kbeg = (int64_t)blockIdx.y * k_per_split;
-    const int64_t kend = min(p.K, kbeg + k_per_split);
+    const int64_t kend = min(Kd, kbeg + k_per_split);
     const int n_main = kend > kbeg ? (int)((kend - kbeg) / T::BK) : 0;
     // a convolution visits the flat fold sequence once per tap: tile t is
     // flat tile t / taps of tap t % taps
@@ -531,7 +533,7 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
                     lane_off(i, n0, p.Ng, p.ld_extB), k0, 0, 0);
             return;
         }
-        const int k0 = (int)(kbeg + (int64_t)(t - fv.h_tiles) * T::BK);
+        const int k0 = (int)(koff + kbeg + (int64_t)(t - fv.h_tiles) * T::BK);
 #pragma unroll
         for (int i = 0; i < T::IA; ++i)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void_t*)(st + (i * T::kWaves + wv) * 1024), 16, offA[i],
@@ -1225,6 +1227,7 @@ int wgrad_splits(int64_t M, int64_t C_out, int64_t C_in) {
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     if (a.Mg <= 0 || a.Ng <= 0) return hipSuccess;
     const bool pipe = pipe_ok(a);
+    if (a.kseg && (!pipe || a.splits > 1 || a.layout)) return hipErrorInvalidValue;   // pipelined kernel only
     const Pick p = pick(a);
     const int64_t ktiles = (a.K + 63) / 64;   // every configuration has 64-byte K tiles
     const int splits = std::max(1, a.splits);
@@ -1315,6 +1318,167 @@ hipError_t launch_conv_dgrad(const GemmArgs& a0, int8_t* bc, int64_t ld_bc, hipS
     if (a.Ng <= 64)
         return a.extA ? launch_pipe<PipeNarrow, true, true>(a, 1, kps, s) : launch_pipe<PipeNarrow, false, true>(a, 1, kps, s);
     return a.extA ? launch_pipe<PipeSmall, true, true>(a, 1, kps, s) : launch_pipe<PipeSmall, false, true>(a, 1, kps, s);
+}
+
+// ---------------------------------------------------------------------------
+// GEMM-based implementation of ShiftQuant's loss propagation (Sec. 3.2), the
+// comparison for ShiftMM: extract one pair of smaller matrices per group
+// (memory rearrangement), multiply each pair with the GEMM, then shift the
+// products by N_G - 1 - g and sum them.
+// ---------------------------------------------------------------------------
+int64_t grouped_width(int64_t C_out, int num_groups) { return round_up(C_out + 63 * (int64_t)num_groups, 64); }
+
+// Group plan (one block): plan[2 g] = first rearranged column of group g
+// (64-aligned), plan[2 g + 1] = its padded width; perm[j] (from plan[16]) =
+// the channel at rearranged column j in ascending order within its group,
+// -1 for padding; then, from plan[16 + wmax], the q_fold column of that
+// channel's code and its fold shift t as (t << 24) | column (-1 for padding).
+constexpr int kPlanThreads = 1024;
+__global__ __launch_bounds__(kPlanThreads) void k_group_plan(const uint8_t* __restrict__ group, int64_t C, int ng,
+                                                             const int32_t* __restrict__ desc, int64_t base_col,
+                                                             int32_t* __restrict__ plan, int64_t wmax) {
+    __shared__ int cnt[kMaxRegions], off[kMaxRegions], run[kMaxRegions];
+    __shared__ int wcnt[kPlanThreads / 64][kMaxRegions];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int32_t* perm = plan + 16;
+    int32_t* acol = perm + wmax;
+    if (tid < kMaxRegions) { cnt[tid] = 0; run[tid] = 0; }
+    __syncthreads();
+    int local[kMaxRegions] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int64_t c = tid; c < C; c += kPlanThreads) {
+        const int g = group[c];
+#pragma unroll
+        for (int q = 0; q < kMaxRegions; ++q) local[q] += g == q;
+    }
+#pragma unroll
+    for (int q = 0; q < kMaxRegions; ++q) {
+        int v = local[q];
+        for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+        if (lane == 0 && v) atomicAdd(&cnt[q], v);
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int o = 0;
+        for (int q = 0; q < ng; ++q) {
+            off[q] = o;
+            const int w = (cnt[q] + 63) / 64 * 64;
+            plan[2 * q] = o;
+            plan[2 * q + 1] = w;
+            o += w;
+        }
+    }
+    __syncthreads();
+    for (int64_t j = tid; j < wmax; j += kPlanThreads) perm[j] = acol[j] = -1;
+    __syncthreads();
+    // ranks: rounds of kPlanThreads channels, wave ballots plus per-wave counts
+    const uint64_t below = (1ull << lane) - 1ull;
+    for (int64_t c0 = 0; c0 < C; c0 += kPlanThreads) {
+        const int64_t c = c0 + tid;
+        const int g = c < C ? (int)group[c] : -1;
+        int rank = 0;
+        for (int q = 0; q < ng; ++q) {
+            const uint64_t m = __ballot(g == q);
+            if (g == q) rank = __popcll(m & below);
+            if (lane == 0) wcnt[wave][q] = __popcll(m);
+        }
+        __syncthreads();
+        if (g >= 0) {
+            int before = run[g];
+            for (int w = 0; w < wave; ++w) before += wcnt[w][g];
+            const int j = off[g] + before + rank;
+            const int d = desc[c], t = d & 15, pos = (d >> 4) - 1;
+            perm[j] = (int32_t)c;
+            acol[j] = (t << 24) | (int32_t)(pos < 0 ? c : base_col + pos);
+        }
+        __syncthreads();
+        if (tid < ng) {
+            int tot = 0;
+            for (int w = 0; w < kPlanThreads / 64; ++w) tot += wcnt[w][tid];
+            run[tid] += tot;
+        }
+        __syncthreads();
+    }
+}
+
+hipError_t launch_group_plan(const uint8_t* group, int64_t C, int num_groups, const int32_t* desc, int64_t base_col,
+                             int32_t* plan, int64_t wmax, hipStream_t s) {
+    hipLaunchKernelGGL(k_group_plan, dim3(1), dim3(kPlanThreads), 0, s, group, C, num_groups, desc, base_col, plan,
+                       wmax);
+    return hipGetLastError();
+}
+
+// dst[r, j] = src[r, col_j] >> t_j with col[j] = (t << 24) | column (-1:
+// padding, 0), four output bytes per thread and 4 rows per block row.
+__global__ __launch_bounds__(256) void k_gather_cols(const int8_t* __restrict__ src, int64_t ld_src, int64_t rows,
+                                                     const int32_t* __restrict__ col, int64_t wmax,
+                                                     int8_t* __restrict__ dst, int64_t ld_dst) {
+    const int64_t j = ((int64_t)blockIdx.x * 64 + (threadIdx.x & 63)) * 4;
+    if (j >= wmax) return;
+    int sc[4], sh[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int v = col[j + e];
+        sc[e] = v < 0 ? -1 : (v & 0xFFFFFF);
+        sh[e] = v < 0 ? 0 : (v >> 24);
+    }
+    for (int64_t r = (int64_t)blockIdx.y * 4 + (threadIdx.x >> 6); r < rows; r += (int64_t)gridDim.y * 4) {
+        const int8_t* row = src + r * ld_src;
+        uint32_t w = 0u;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int8_t v = sc[e] >= 0 ? (int8_t)(row[sc[e]] >> sh[e]) : (int8_t)0;
+            w |= (uint32_t)(uint8_t)v << (8 * e);
+        }
+        *reinterpret_cast<uint32_t*>(dst + r * ld_dst + j) = w;
+    }
+}
+
+hipError_t launch_gather_cols(const int8_t* src, int64_t ld_src, int64_t rows, const int32_t* col, int64_t wmax,
+                              int8_t* dst, int64_t ld_dst, hipStream_t s) {
+    if (rows <= 0 || wmax <= 0) return hipSuccess;
+    if (wmax % 4 != 0 || ld_dst % 4 != 0) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((wmax / 4 + 63) / 64), (unsigned)std::min<int64_t>((rows + 3) / 4, 16384));
+    hipLaunchKernelGGL(k_gather_cols, grid, dim3(256), 0, s, src, ld_src, rows, col, wmax, dst, ld_dst);
+    return hipGetLastError();
+}
+
+// acc = sum_g part[g] << (N_G - 1 - g); out = fl(float(acc) * alpha); four
+// consecutive outputs per thread when N is a multiple of 4
+__global__ void k_group_combine(const int32_t* __restrict__ part, int ng, int64_t M, int64_t N,
+                                int32_t* __restrict__ acc, int64_t ld_acc, float* __restrict__ out, int64_t ld_out,
+                                const sq_scale* __restrict__ gs, const sq_scale* __restrict__ os) {
+    const float alpha = out ? __fmul_rn(__fmul_rn(gs->step, os->step), pow2f(-(ng - 1))) : 0.0f;
+    const int64_t total = M * N;
+    const int V = (N % 4 == 0) ? 4 : 1;
+    for (int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * V; i < total;
+         i += (int64_t)gridDim.x * blockDim.x * V) {
+        int32_t v[4] = {0, 0, 0, 0};
+        for (int g = 0; g < ng; ++g) {
+            if (V == 4) {
+                const int4 q = *reinterpret_cast<const int4*>(part + g * total + i);
+                const int s = ng - 1 - g;
+                v[0] += (int32_t)((uint32_t)q.x << s); v[1] += (int32_t)((uint32_t)q.y << s);
+                v[2] += (int32_t)((uint32_t)q.z << s); v[3] += (int32_t)((uint32_t)q.w << s);
+            } else {
+                v[0] += (int32_t)((uint32_t)part[g * total + i] << (ng - 1 - g));
+            }
+        }
+        for (int e = 0; e < V; ++e) {
+            const int64_t m = (i + e) / N, n = (i + e) - m * N;
+            if (acc) acc[m * ld_acc + n] = v[e];
+            if (out) out[m * ld_out + n] = __fmul_rn((float)v[e], alpha);
+        }
+    }
+}
+
+hipError_t launch_group_combine(const int32_t* part, int num_groups, int64_t M, int64_t N, int32_t* acc,
+                                int64_t ld_acc, float* out, int64_t ld_out, const sq_scale* gs, const sq_scale* os,
+                                hipStream_t s) {
+    if (M <= 0 || N <= 0) return hipSuccess;
+    const unsigned blocks = (unsigned)std::min<int64_t>((M * N + 255) / 256, 8192);
+    hipLaunchKernelGGL(k_group_combine, dim3(blocks), dim3(256), 0, s, part, num_groups, M, N, acc, ld_acc, out, ld_out,
+                       gs, os);
+    return hipGetLastError();
 }
 
 hipError_t launch_gather_ext(const int8_t* wq_t, int64_t ld_w, int64_t C_in, const int32_t* layout,

@@ -117,6 +117,9 @@ struct GemmArgs {
     int cv_KW, cv_PH, cv_PW;
     int64_t cv_H, cv_W, cv_Ho, cv_Wo, a_rows;
     int64_t K_used;                 // code columns in use (C_out)
+    // device {first K column, K columns} replacing [0, K) (the per-group
+    // GEMMs of the GEMM-based comparison), may be null
+    const int32_t* kseg;
 };
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
@@ -131,6 +134,16 @@ inline int64_t conv_bc_ld(int64_t C_out, int64_t taps, int64_t ext_max) {
 // ld_w]); kernels that need the weights in the K order of the implicit GEMM
 // gather them into bc first.
 hipError_t launch_conv_dgrad(const GemmArgs& a, int8_t* bc, int64_t ld_bc, hipStream_t s);
+// GEMM-based loss propagation (comparison for ShiftMM): group plan,
+// rearranged operands, per-group products, shift-and-sum.
+int64_t grouped_width(int64_t C_out, int num_groups);
+hipError_t launch_group_plan(const uint8_t* group, int64_t C, int num_groups, const int32_t* desc, int64_t base_col,
+                             int32_t* plan, int64_t wmax, hipStream_t s);
+hipError_t launch_gather_cols(const int8_t* src, int64_t ld_src, int64_t rows, const int32_t* col, int64_t wmax,
+                              int8_t* dst, int64_t ld_dst, hipStream_t s);
+hipError_t launch_group_combine(const int32_t* part, int num_groups, int64_t M, int64_t N, int32_t* acc,
+                                int64_t ld_acc, float* out, int64_t ld_out, const sq_scale* gs, const sq_scale* os,
+                                hipStream_t s);
 hipError_t launch_splitk_reduce(const int32_t* ws, int splits, const GemmArgs& a, hipStream_t s);
 hipError_t launch_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_t ld_acc, int kind,
                           const uint8_t* group, const sq_scale* gs, const sq_scale* os,

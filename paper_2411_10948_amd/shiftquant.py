@@ -37,7 +37,9 @@ FLAG_ZERO = 2
 EXPORTS = (
     "sq_grad_layout_size", "sq_quantize_grad_workspace_size", "sq_quantize_tensor_workspace_size",
     "sq_gemm_dgrad_workspace_size", "sq_gemm_wgrad_workspace_size", "sq_conv_dgrad_workspace_size",
+    "sq_gemm_dgrad_grouped_workspace_size",
     "sq_quantize_grad", "sq_quantize_tensor", "sq_gemm_dgrad", "sq_gemm_wgrad", "sq_conv_dgrad", "sq_dequant",
+    "sq_gemm_dgrad_grouped",
     "sq_status_string", "sq_last_error",
 )
 
@@ -88,6 +90,9 @@ def load() -> ct.CDLL:
                           _SZ, _P],
         "sq_dequant": [_P, _I64, _I64, _I64, ct.c_int32, _P, _P, _P, ct.c_int32, _P, _I64, _P],
         "sq_conv_dgrad_workspace_size": [_I64, _I64, ct.c_int32, ct.c_int32, pp, ct.POINTER(_SZ)],
+        "sq_gemm_dgrad_grouped_workspace_size": [_I64, _I64, _I64, pp, ct.POINTER(_SZ)],
+        "sq_gemm_dgrad_grouped": [_P, _I64, _P, _P, _P, _P, _I64, _P, _I64, _I64, _I64, pp, _P, _I64, _P, _I64,
+                                  _P, _SZ, _P],
         "sq_conv_dgrad": [_P, _I64, _P, _P, _P, _P, _I64, _P, _I64, _I64, _I64, _I64, _I64, ct.c_int32,
                           ct.c_int32, ct.c_int32, ct.c_int32, pp, _P, _I64, _P, _I64, _P, _SZ, _P],
     }
@@ -180,6 +185,13 @@ def sq_conv_dgrad_workspace_size(C_out: int, C_in: int, KH: int, KW: int, params
     return nb.value
 
 
+def sq_gemm_dgrad_grouped_workspace_size(M: int, C_out: int, C_in: int, params: Params) -> int:
+    nb = _SZ(0)
+    _check("sq_gemm_dgrad_grouped_workspace_size",
+           load().sq_gemm_dgrad_grouped_workspace_size(M, C_out, C_in, ct.byref(params), ct.byref(nb)))
+    return nb.value
+
+
 def sq_quantize_grad(dY, params, q_fold, q_t, group, scale, layout, workspace, stream=None) -> None:
     M, C = dY.shape
     ws, nws = _ws_ptr(workspace)
@@ -212,6 +224,15 @@ def sq_conv_dgrad(q_fold, layout, group, gscale, wq_t, wscale, N, H, W, C_out, C
         _ptr(q_fold), _ld(q_fold), _ptr(layout), _ptr(group), _ptr(gscale), _ptr(wq_t), _ld(wq_t),
         _ptr(wscale), N, H, W, C_out, C_in, KH, KW, PH, PW, ct.byref(params), _ptr(acc), _ld(acc),
         _ptr(dX), _ld(dX), ws, nws, _stream(stream)))
+
+
+def sq_gemm_dgrad_grouped(q_fold, layout, group, gscale, wq_t, wscale, M, C_out, C_in, params, acc, dX,
+                          workspace, stream=None) -> None:
+    ws, nws = _ws_ptr(workspace)
+    _check("sq_gemm_dgrad_grouped", load().sq_gemm_dgrad_grouped(
+        _ptr(q_fold), _ld(q_fold), _ptr(layout), _ptr(group), _ptr(gscale), _ptr(wq_t), _ld(wq_t),
+        _ptr(wscale), M, C_out, C_in, ct.byref(params), _ptr(acc), _ld(acc), _ptr(dX), _ld(dX),
+        ws, nws, _stream(stream)))
 
 
 def sq_gemm_wgrad(q_t, group, gscale, xq_t, xscale, M, C_out, C_in, params, acc, dW, workspace,
@@ -311,6 +332,19 @@ def gemm_dgrad(codes: GradCodes, wq_t: torch.Tensor, wscale: torch.Tensor, want_
     return acc, dX
 
 
+def gemm_dgrad_grouped(codes: GradCodes, wq_t: torch.Tensor, wscale: torch.Tensor, want_acc: bool = False,
+                       want_out: bool = True, stream=None):
+    """The GEMM-based comparison implementation of gemm_dgrad (same results)."""
+    M, C_out, C_in = codes.M, codes.C_out, wq_t.shape[0]
+    dev = wq_t.device
+    acc = torch.empty((M, C_in), dtype=torch.int32, device=dev) if want_acc else None
+    dX = torch.empty((M, C_in), dtype=torch.float32, device=dev) if want_out else None
+    ws = _workspace(sq_gemm_dgrad_grouped_workspace_size(M, C_out, C_in, codes.params), dev)
+    sq_gemm_dgrad_grouped(codes.q_fold, codes.layout, codes.group, codes.scale, wq_t, wscale, M, C_out, C_in,
+                          codes.params, acc, dX, ws, stream)
+    return acc, dX
+
+
 def conv_dgrad(codes: GradCodes, wq_t: torch.Tensor, wscale: torch.Tensor, N: int, H: int, W: int,
                KH: int, KW: int, PH: int, PW: int, want_acc: bool = False, want_out: bool = True, stream=None):
     """Input gradient [N*H*W, C_in] (NHWC) of a stride-1 convolution whose output
@@ -346,8 +380,9 @@ class BackwardPlan:
     allocates nothing."""
 
     def __init__(self, M: int, C_out: int, C_in: int, params: Params, device="cuda",
-                 want_acc: bool = False):
+                 want_acc: bool = False, grouped_dgrad: bool = False):
         self.M, self.C_out, self.C_in, self.params = M, C_out, C_in, params
+        self.grouped_dgrad = grouped_dgrad
         dev = torch.device(device)
         lay_bytes, min_ld = sq_grad_layout_size(C_out, params)
         self.q_fold = torch.zeros((M, min_ld), dtype=torch.int8, device=dev)
@@ -356,7 +391,8 @@ class BackwardPlan:
         self.scale = new_scale(dev)
         self.layout = torch.zeros(lay_bytes // 4, dtype=torch.int32, device=dev)
         self.ws_q = _workspace(sq_quantize_grad_workspace_size(M, C_out, params), dev)
-        self.ws_d = _workspace(sq_gemm_dgrad_workspace_size(M, C_out, C_in, params), dev)
+        self.ws_d = _workspace((sq_gemm_dgrad_grouped_workspace_size if grouped_dgrad else
+                                sq_gemm_dgrad_workspace_size)(M, C_out, C_in, params), dev)
         self.ws_w = _workspace(sq_gemm_wgrad_workspace_size(M, C_out, C_in, params), dev)
         self.dX = torch.empty((M, C_in), dtype=torch.float32, device=dev)
         self.dW = torch.empty((C_out, C_in), dtype=torch.float32, device=dev)
@@ -368,8 +404,9 @@ class BackwardPlan:
                          self.ws_q, stream)
 
     def dgrad(self, wq_t, wscale, stream=None):
-        sq_gemm_dgrad(self.q_fold, self.layout, self.group, self.scale, wq_t, wscale, self.M, self.C_out,
-                      self.C_in, self.params, self.acc_dX, self.dX, self.ws_d, stream)
+        fn = sq_gemm_dgrad_grouped if self.grouped_dgrad else sq_gemm_dgrad
+        fn(self.q_fold, self.layout, self.group, self.scale, wq_t, wscale, self.M, self.C_out, self.C_in,
+           self.params, self.acc_dX, self.dX, self.ws_d, stream)
 
     def wgrad(self, xq_t, xscale, stream=None):
         sq_gemm_wgrad(self.q_t, self.group, self.scale, xq_t, xscale, self.M, self.C_out, self.C_in,

@@ -525,6 +525,29 @@ def test_conv_dgrad_rejects_bad_geometry(sq):
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("bits,ng,shape", [(4, 4, (300, 200, 96)), (6, 4, (257, 130, 64)), (8, 6, (129, 300, 80)),
+                                           (5, 1, (64, 64, 64)), (6, 3, (1000, 1024, 256))])
+def test_dgrad_grouped_matches_shiftmm(sq, bits, ng, shape):
+    # the GEMM-based implementation (per-group sub-GEMMs after rearrangement,
+    # then shift and sum) gives the ShiftMM accumulator and dX bit for bit
+    import torch
+    M, C_out, C_in = shape
+    rng = np.random.default_rng(M + C_out)
+    dY = _grad(M, C_out, seed=C_in + bits, s=2.5)
+    W = (rng.standard_normal((C_out, C_in)) * 0.05).astype(np.float32)
+    codes = sq.quantize_grad(_dev(dY), bits, ng)
+    wq_t, ws = sq.quantize_tensor(_dev(W), 8, transpose=True)
+    a1, d1 = sq.gemm_dgrad(codes, wq_t, ws, want_acc=True)
+    a2, d2 = sq.gemm_dgrad_grouped(codes, wq_t, ws, want_acc=True)
+    torch.cuda.synchronize()
+    assert torch.equal(a1, a2) and torch.equal(d1, d2)
+    q_ref, g_ref, s_ref, _ = oracle.quantize_grad(dY, bits, ng)
+    wq_ref, _ = oracle.quantize_tensor(W, 8)
+    rows = np.unique(np.r_[0, M - 1, rng.integers(0, M, 8)])
+    A_ref = oracle.dgrad(q_ref, g_ref, ng, wq_ref, rows)
+    assert np.array_equal(a2.index_select(0, torch.as_tensor(rows, device="cuda")).cpu().numpy(), A_ref)
+
+
 def test_degenerate_layers(sq):
     rng = np.random.default_rng(2)
     W = (rng.standard_normal((40, 24)) * 0.02).astype(np.float32)
@@ -560,6 +583,33 @@ def test_workload_reduced(sq, name):
         wgrad_rows = np.unique(np.r_[0, wl.C_out - 1, rng.integers(0, wl.C_out, 24)])
     r = check_layer(sq, d["dY"], d["W"], d["X"], wl.bits, wl.num_groups, wl.round_mode, wl.sr_seed,
                     wl.sr_offset, dgrad_rows, wgrad_rows)
+    assert r["exact_dX"] and r["exact_dW"]
+
+
+# Parameter variants of the MLP layer (the bench's --bits / --num-groups /
+# --rounding runs): b in {4, 6, 8}, N_G in 1..6, both rounding modes.
+VARIANTS = [(b, g, 0) for b in (4, 6, 8) for g in range(1, 7)] + [(4, 4, 1), (6, 6, 1), (8, 3, 1), (8, 6, 1)]
+
+
+@pytest.mark.parametrize("bits,ng,mode", VARIANTS, ids=[f"b{b}-ng{g}-{'sr' if m else 'rtn'}" for b, g, m in VARIANTS])
+def test_parameter_variants(sq, bits, ng, mode):
+    d = workloads.make_inputs("mlp_up_768x3072", M=600)
+    M, C_out = d["M"], d["dY"].shape[1]
+    rng = np.random.default_rng(bits * 10 + ng)
+    dgrad_rows = np.unique(np.r_[0, M - 1, rng.integers(0, M, 12)])
+    wgrad_rows = np.unique(np.r_[0, C_out - 1, rng.integers(0, C_out, 12)])
+    r = check_layer(sq, d["dY"], d["W"], d["X"], bits, ng, mode, 3, 1, dgrad_rows, wgrad_rows)
+    assert r["exact_dX"] and r["exact_dW"]
+
+
+def test_parameter_variant_full_size(sq):
+    # the widest variant the benchmark runs: 8-bit codes in 6 groups, full MLP layer
+    d = workloads.make_inputs("mlp_up_768x3072")
+    M, C_out = d["M"], d["dY"].shape[1]
+    rng = np.random.default_rng(86)
+    dgrad_rows = np.unique(np.r_[0, M - 1, rng.integers(0, M, 16)])
+    wgrad_rows = np.unique(np.r_[0, C_out - 1, rng.integers(0, C_out, 8)])
+    r = check_layer(sq, d["dY"], d["W"], d["X"], 8, 6, 0, 0, 0, dgrad_rows, wgrad_rows, fold_rows=dgrad_rows)
     assert r["exact_dX"] and r["exact_dW"]
 
 
