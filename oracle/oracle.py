@@ -74,6 +74,10 @@ def _bind(L):
     L.sqo_conv_dgrad.argtypes = [P, i64, i64, i64, i64, P, ct.c_int, P, i64, ct.c_int, ct.c_int, ct.c_int,
                                  ct.c_int, P, i64, P]
     L.sqo_conv_dgrad.restype = ct.c_int
+    L.sqo_quantize_channels.argtypes = [P, i64, i64, i64, ct.c_int, ct.c_int, P, P]
+    L.sqo_quantize_channels.restype = ct.c_int
+    L.sqo_dequant_cols.argtypes = [P, i64, i64, ct.c_float, P, ct.c_int, P]
+    L.sqo_dequant_cols.restype = None
     L.sqo_wgrad.argtypes = [P, i64, i64, P, i64, P, i64, P]
     L.sqo_wgrad.restype = ct.c_int
     L.sqo_dequant_dgrad.argtypes = [P, i64, ct.c_float, ct.c_float, ct.c_int, P]
@@ -175,6 +179,30 @@ def dgrad(q: np.ndarray, g: np.ndarray, num_groups: int, wq: np.ndarray, rows=No
         raise RangeError("dgrad accumulator leaves int32")
     assert rc == 0
     return A
+
+
+def quantize_channels(T: np.ndarray, bits: int = 8, axis: int = 0):
+    """Per-channel symmetric quantization: one scale per row (axis 0) or
+    column (axis 1).  Returns (codes int8 [rows, cols], list of scale dicts)."""
+    T = _c(T, np.float32)
+    rows, cols = T.shape
+    q = np.zeros((rows, cols), np.int8)
+    n = rows if axis == 0 else cols
+    sc = (_Scale * max(n, 1))()
+    rc = lib().sqo_quantize_channels(_p(T), rows, cols, cols, bits, axis, _p(q), ct.cast(sc, ct.c_void_p))
+    assert rc == 0
+    return q, [_scale_dict(sc[i]) for i in range(n)]
+
+
+def dequant_cols(A: np.ndarray, d_a, d_w: np.ndarray, num_groups: int) -> np.ndarray:
+    """out[i, k] = fl(float(A[i, k]) * fl(fl(d_a * d_w[k]) * 2^-(N_G-1)))."""
+    A = _c(A, np.int32)
+    d_w = _c(d_w, np.float32)
+    n_rows, n_cols = A.shape
+    assert d_w.shape[0] == n_cols
+    out = np.zeros(A.shape, np.float32)
+    lib().sqo_dequant_cols(_p(A), n_rows, n_cols, float(d_a), _p(d_w), num_groups, _p(out))
+    return out
 
 
 def conv_dgrad(q: np.ndarray, g: np.ndarray, num_groups: int, wq: np.ndarray, N: int, H: int, W: int,

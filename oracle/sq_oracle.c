@@ -250,6 +250,62 @@ int sqo_quantize_tensor(const float* T, int64_t rows, int64_t cols, int64_t ld, 
 }
 
 /* ---------------------------------------------------------------------------
+ * Per-channel symmetric quantization of a weight matrix (Sec. 5.1: weights
+ * are quantized per output channel in the forward pass and per input channel
+ * in loss propagation).  axis 0: one scale per row of T, axis 1: one per
+ * column.  Each channel is quantized like a tensor of its own: amax over the
+ * channel, inv = fl(Q / amax), step = fl(amax / Q), code = clamp(rint(fl(x *
+ * inv)), -Q, Q); a channel whose amax is NaN/Inf or below 2^-96 gets its flag
+ * and all-zero codes.  q is [rows, cols]; scales has rows (axis 0) or cols
+ * (axis 1) entries.
+ * ------------------------------------------------------------------------- */
+int sqo_quantize_channels(const float* T, int64_t rows, int64_t cols, int64_t ld, int bits, int axis,
+                          int8_t* q, sqo_scale* scales)
+{
+    if (!T || !q || !scales || rows < 0 || cols < 0 || ld < cols || bits < 2 || bits > 8 || (axis != 0 && axis != 1))
+        return SQO_ERR_ARG;
+    const int32_t Q = qmax_of(bits);
+    int64_t nch = axis == 0 ? rows : cols, len = axis == 0 ? cols : rows;
+    for (int64_t ch = 0; ch < nch; ++ch) {
+        uint32_t amax = 0;
+        int nonfinite = 0;
+        for (int64_t e = 0; e < len; ++e) {
+            float x = axis == 0 ? T[ch * ld + e] : T[e * ld + ch];
+            uint32_t a = f2u(x) & 0x7FFFFFFFu;
+            if (a >= 0x7F800000u) nonfinite = 1;
+            if (a > amax) amax = a;
+        }
+        sqo_scale* sc = &scales[ch];
+        float a = u2f(amax);
+        sc->r_max = a;
+        sc->flags = nonfinite ? SQO_FLAG_NONFINITE : (a < pow2f(-96) ? SQO_FLAG_ZERO : 0u);
+        sc->inv0 = sc->flags ? 0.0f : (float)Q / a;
+        sc->d0 = sc->flags ? 0.0f : a / (float)Q;
+        for (int64_t e = 0; e < len; ++e) {
+            int64_t i = axis == 0 ? ch : e, j = axis == 0 ? e : ch;
+            float v = sc->flags ? 0.0f : rintf(T[i * ld + j] * sc->inv0);
+            if (v > (float)Q) v = (float)Q;
+            if (v < (float)-Q) v = (float)-Q;
+            q[i * cols + j] = (int8_t)(int32_t)v;
+        }
+    }
+    return SQO_OK;
+}
+
+/* Dequantization with one weight scale per output column (the forward pass
+ * with per-output-channel weights, or loss propagation with per-input-channel
+ * weights; Eq. dq_mm_f with S_W per channel):
+ *   gamma_k = fl(fl(d_a * d_w[k]) * 2^-(N_G-1)),   out[i, k] = fl(float(A[i, k]) * gamma_k). */
+void sqo_dequant_cols(const int32_t* A, int64_t n_rows, int64_t n_cols, float d_a, const float* d_w, int num_groups,
+                      float* out)
+{
+    for (int64_t k = 0; k < n_cols; ++k) {
+        float gamma = (d_a * d_w[k]) * pow2f(-(num_groups - 1));
+        for (int64_t i = 0; i < n_rows; ++i) out[i * n_cols + k] = (float)A[i * n_cols + k] * gamma;
+    }
+}
+
+/* ---------------------------------------------------------------------------
  * Loss propagation (Eq. dq_mm_f and App. D, left-shift form, R8):
  *   A[n, k] = sum_c  (q[n, c] * wq[c, k]) << (N_G - 1 - g_c)
  * ShiftMM (Sec. 3.2) shifts each product before it is accumulated; that is

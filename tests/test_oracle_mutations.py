@@ -50,6 +50,10 @@ MUTATIONS = [
      "int64_t col = ((int64_t)s * KH + r) * C_in + ci;"),
     ("conv last output row dropped", "if (oh < 0 || oh >= Ho) continue;", "if (oh < 0 || oh >= Ho - 1) continue;"),
     ("conv dropped shift", "acc += ((int64_t)1 << shift) * prod;", "acc += prod;"),
+    ("per-channel axis", "float x = axis == 0 ? T[ch * ld + e] : T[e * ld + ch];",
+     "float x = axis == 1 ? T[ch * ld + e] : T[e * ld + ch];"),
+    ("column dequant exponent", "float gamma = (d_a * d_w[k]) * pow2f(-(num_groups - 1));",
+     "float gamma = (d_a * d_w[k]) * pow2f(-num_groups);"),
     ("int32 range check", "if (acc > INT32_MAX || acc < INT32_MIN) return SQO_ERR_RANGE;\n            A[i * C_in + k]",
      "A[i * C_in + k]"),
 ]
@@ -90,6 +94,10 @@ def _pin_calls():
     for case in pins.CONV_CASES:
         calls.append(lambda c=case: pins.test_conv_dgrad_is_transpose_of_forward_conv(c))
     calls.append(pins.test_conv_dgrad_1x1_is_dgrad_and_brute_force)
+    for axis in (0, 1):
+        calls.append(lambda a=axis: pins.test_quantize_channels_is_per_tensor_per_channel(a, 8))
+    calls.append(pins.test_quantize_channels_degenerate_channels)
+    calls.append(lambda: pins.test_forward_equals_dequantized_product(4, 4))
     return calls
 
 

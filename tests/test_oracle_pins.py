@@ -538,3 +538,57 @@ def test_conv_dgrad_1x1_is_dgrad_and_brute_force():
                                 ref += (int(q[oh * Wo + ow, co]) * int(wq[co, (r * 3 + s) * C_in + ci])
                                         << (ng - 1 - int(g[co])))
                 assert A[ih * W + iw, ci] == ref
+
+
+# ---------------------------------------------------------------------------
+# Forward pass (Sec. 5.1): ShiftQuant on activations, per-channel weights
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("axis", [0, 1])
+@pytest.mark.parametrize("bits", [4, 8])
+def test_quantize_channels_is_per_tensor_per_channel(axis, bits):
+    rng = np.random.default_rng(40 + axis + bits)
+    T = (rng.standard_normal((9, 13)) * np.exp(rng.standard_normal((9, 1)))).astype(np.float32)
+    q, sc = oracle.quantize_channels(T, bits, axis)
+    for ch in range(T.shape[axis]):
+        part = T[ch:ch + 1, :] if axis == 0 else T[:, ch:ch + 1]
+        q1, s1 = oracle.quantize_tensor(part, bits)
+        got = q[ch:ch + 1, :] if axis == 0 else q[:, ch:ch + 1]
+        np.testing.assert_array_equal(got, q1)
+        assert sc[ch] == s1
+
+
+def test_quantize_channels_degenerate_channels():
+    T = np.ones((4, 5), np.float32)
+    T[1, :] = 0.0
+    T[2, 3] = np.nan
+    q, sc = oracle.quantize_channels(T, 8, 0)
+    assert sc[1]["flags"] == oracle.FLAG_ZERO and sc[2]["flags"] == oracle.FLAG_NONFINITE
+    assert sc[0]["flags"] == 0 and sc[3]["flags"] == 0
+    assert not q[1].any() and not q[2].any() and (q[0] == 127).all()
+    q, sc = oracle.quantize_channels(T, 8, 1)
+    assert sc[3]["flags"] == oracle.FLAG_NONFINITE and not q[:, 3].any()
+    assert sc[0]["flags"] == 0 and q[0, 0] == 127 and q[1, 0] == 0
+
+
+@pytest.mark.parametrize("bits,ng", [(4, 4), (6, 3), (8, 1)])
+def test_forward_equals_dequantized_product(bits, ng):
+    # Y = X W^T with X in ShiftQuant groups over its channels (the forward
+    # inner dimension) and W per output channel: the integer product is the
+    # ShiftMM sum over input channels, the column scale carries s_W[n]
+    rng = np.random.default_rng(bits * 3 + ng)
+    M, C_in, C_out = 37, 50, 23
+    X = _grad(M=M, C=C_in, seed=bits + ng, s=1.5)
+    W = (rng.standard_normal((C_out, C_in)) * np.exp(rng.standard_normal((C_out, 1)))).astype(np.float32)
+    xq, g, xs, _ = oracle.quantize_grad(X, bits, ng)
+    wq, wsc = oracle.quantize_channels(W, 8, 0)
+    A = oracle.dgrad(xq, g, ng, np.ascontiguousarray(wq.T))
+    sh = (ng - 1 - g.astype(np.int64))
+    np.testing.assert_array_equal(A, (xq.astype(np.int64) << sh[None, :]) @ wq.astype(np.int64).T)
+    d_w = np.array([s["d0"] for s in wsc], np.float32)
+    Y = oracle.dequant_cols(A, xs["d0"], d_w, ng)
+    xd = xq.astype(np.float64) * (np.float64(xs["d0"]) * np.exp2(-g.astype(np.float64)))[None, :]
+    wd = wq.astype(np.float64) * d_w.astype(np.float64)[:, None]
+    _close_to_product(Y, xd @ wd.T, np.abs(xd) @ np.abs(wd).T)
+    for i, k in [(0, 0), (M - 1, C_out - 1), (5, 7)]:
+        gamma = np.float32(np.float32(xs["d0"]) * d_w[k]) * np.float32(2.0 ** -(ng - 1))
+        assert Y[i, k] == np.float32(np.float32(A[i, k]) * gamma)
