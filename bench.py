@@ -93,6 +93,89 @@ def cpu_baseline(inputs, wl, budget_s: float = 10.0, conv=False):
                       f"({ops / 1e9:.2f} Gop in {t:.2f} s, 1 thread)"}
 
 
+def run_forward(args, torch, sq, wl, inputs):
+    """Forward pass of the same layer (Sec. 5.1): X quantized with ShiftQuant
+    (groups over its channels, the workload's b and N_G, round-half-even),
+    W per output channel (8-bit, untimed: in training the weights change once
+    per step), Y = X W^T as ShiftMM with per-column weight scales."""
+    dev = torch.device("cuda:0")
+    M, C_in, C_out = inputs["M"], wl.C_in, wl.C_out
+    X = torch.from_numpy(inputs["X"]).to(dev)
+    W = torch.from_numpy(inputs["W"]).to(dev)
+    params = sq.Params.make(wl.bits, wl.num_groups, 0)
+    wq, wsc = sq.quantize_channels(W, 8, 0, False)
+    del W
+    lay_bytes, min_ld = sq.sq_grad_layout_size(C_in, params)
+    xq = torch.zeros((M, min_ld), dtype=torch.int8, device=dev)
+    group = torch.empty(C_in, dtype=torch.uint8, device=dev)
+    xscale = sq.new_scale(dev)
+    layout = torch.zeros(lay_bytes // 4, dtype=torch.int32, device=dev)
+    ws_q = torch.empty(max(sq.sq_quantize_grad_workspace_size(M, C_in, params), 256), dtype=torch.uint8, device=dev)
+    ws_f = torch.empty(max(sq.sq_gemm_dgrad_workspace_size(M, C_in, C_out, params), 256), dtype=torch.uint8,
+                       device=dev)
+    Y = torch.empty((M, C_out), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def quant():
+        sq.sq_quantize_grad(X, params, xq, None, group, xscale, layout, ws_q, stream)
+
+    def fwd():
+        sq.sq_gemm_forward(xq, layout, group, xscale, wq, wsc, M, C_in, C_out, params, None, Y, ws_f, stream)
+
+    def timed(fn, K):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(K):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / K
+
+    for _ in range(args.warmup):
+        quant()
+        fwd()
+    step = lambda: (quant(), fwd())
+    ms_step = timed(step, args.steps)
+    t_q, t_f = timed(quant, args.steps), timed(fwd, args.steps)
+    ops = 2 * M * C_in * C_out
+    parts = {"sq_quantize_grad(X)": {"ms": t_q, "bytes": 5 * M * C_in, "ops": 0},
+             "sq_gemm_forward": {"ms": t_f, "bytes": M * C_in + C_in * C_out + 4 * M * C_out, "ops": ops}}
+    dom = max(parts, key=lambda k: parts[k]["ms"])
+    d = parts[dom]
+    if d["ops"] and d["ops"] / d["bytes"] > PEAK_INT8_TOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
+        roof = {"bound": "mfma", "achieved": d["ops"] / (d["ms"] * 1e-3) / 1e12, "peak": PEAK_INT8_TOPS,
+                "unit": "TOPS"}
+    else:
+        roof = {"bound": "hbm", "achieved": d["bytes"] / (d["ms"] * 1e-3) / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    roof.update({"frac": roof["achieved"] / roof["peak"], "traffic": None, "kernel": dom,
+                 "algorithmic_bytes": d["bytes"], "algorithmic_ops": d["ops"], "avg_ms": d["ms"]})
+    out = {"metric": "ShiftQuant forward TOPS (quantize X + ShiftMM forward GEMM)",
+           "value": ops / (ms_step * 1e-3) / 1e12, "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "int8", "data": "synthetic",
+           "config": {"workload": args.workload, "step": "forward", "M": M, "C_in": C_in, "C_out": C_out,
+                      "bits": wl.bits, "num_groups": wl.num_groups, "rounding": "nearest-even",
+                      "weights": "8-bit per output channel", "parallelism": "none"},
+           "breakdown_ms": {k: v["ms"] for k, v in parts.items()}, "roofline": roof}
+    if not args.no_cpu_baseline:
+        import numpy as np
+        import oracle
+        Xh, Wh = inputs["X"], inputs["W"]
+        rows = max(1, min(M, 64))
+        t0 = time.perf_counter()
+        xq_o, g_o, xs_o, _ = oracle.quantize_grad(Xh[:rows], wl.bits, wl.num_groups)
+        wq_o, wsc_o = oracle.quantize_channels(Wh, 8, 0)
+        A_o = oracle.dgrad(xq_o, g_o, wl.num_groups, np.ascontiguousarray(wq_o.T))
+        oracle.dequant_cols(A_o, xs_o["d0"], np.array([s["d0"] for s in wsc_o], np.float32), wl.num_groups)
+        t = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": 2 * rows * C_in * C_out / t / 1e12, "unit": "TOPS", "cores": 1,
+                               "kind": "oracle", "sample": f"oracle quantize X + forward product + dequant on the "
+                                                          f"first {rows} of {M} rows ({t:.2f} s, 1 thread)"}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -104,6 +187,8 @@ def main(argv=None):
     ap.add_argument("--num-groups", type=int, default=None, help="override the workload's N_G (variant runs)")
     ap.add_argument("--rounding", choices=["rtn", "sr"], default=None,
                     help="override the workload's rounding (variant runs)")
+    ap.add_argument("--step", choices=["backward", "forward"], default="backward",
+                    help="forward: quantize X with ShiftQuant + Y = X W^T (per-output-channel W)")
     ap.add_argument("--dgrad", choices=["shiftmm", "grouped"], default="shiftmm",
                     help="grouped: the GEMM-based comparison implementation of the dgrad (Sec. 3.2)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -135,6 +220,13 @@ def main(argv=None):
     M, C_out, C_in = inputs["M"], wl.C_out, wl.C_in
     print(f"[bench] {args.workload}: M={M} C_out={C_out} C_in={C_in} b={wl.bits} N_G={wl.num_groups} "
           f"round={'SR' if wl.round_mode else 'RTN'}", file=sys.stderr, flush=True)
+
+    if args.step == "forward":
+        if conv or wl.x_kind == "conv3x3_relu":
+            print("bench.py: --step forward runs the linear layers (the conv layers' inputs are im2col'd)",
+                  file=sys.stderr)
+            return 2
+        return run_forward(args, torch, sq, wl, inputs)
 
     dev = torch.device("cuda:0")
     dY = torch.from_numpy(inputs["dY"]).to(dev)

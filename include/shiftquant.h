@@ -178,6 +178,59 @@ sq_status sq_quantize_tensor(const float* T, int64_t rows, int64_t cols, int64_t
                              void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * sq_quantize_channels -- per-channel symmetric quantization of a weight
+ * matrix.
+ *
+ * Sec. 5.1 quantizes weights per output channel in the forward pass and per
+ * input channel in loss propagation.  Each channel is quantized like a
+ * tensor of its own (see sq_quantize_tensor): amax over the channel,
+ * inv = fl(Q / amax), step = fl(amax / Q),
+ * code = clamp(round_half_even(fl(T * inv)), -Q, Q); a channel whose amax is
+ * NaN/Inf or below 2^-96 gets SQ_FLAG_NONFINITE / SQ_FLAG_ZERO in its scale
+ * and all-zero codes.
+ * Input : T [rows, ld] fp32; axis 0: one scale per row (W [C_out, C_in] per
+ *         output channel), axis 1: one per column (per input channel).
+ * Output: q as in sq_quantize_tensor (transpose 0: [rows, ld_q], 1:
+ *         [cols, ld_q]); scales [rows] (axis 0) or [cols] (axis 1) sq_scale.
+ * Workspace: sq_quantize_channels_workspace_size bytes (0 for axis 0).
+ * Errors: SQ_ERR_INVALID_ARGUMENT, SQ_ERR_WORKSPACE_TOO_SMALL, SQ_ERR_HIP.
+ * ------------------------------------------------------------------------- */
+sq_status sq_quantize_channels_workspace_size(int64_t rows, int64_t cols, int32_t axis, size_t* bytes);
+sq_status sq_quantize_channels(const float* T, int64_t rows, int64_t cols, int64_t ld, int32_t bits,
+                               int32_t axis, int32_t transpose, int8_t* q, int64_t ld_q, sq_scale* scales,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * sq_gemm_forward -- forward pass Y = X . W^T with ShiftQuant activations
+ * and per-output-channel weights (Sec. 5.1; the first GEMM of Fig. "MMs").
+ *
+ * X is quantized by sq_quantize_grad (ShiftQuant groups over its channels,
+ * which are this product's inner dimension), so the product is ShiftMM as in
+ * sq_gemm_dgrad, with the weight scale taken per output column:
+ *   acc[m, n] = sum_c (code_X(m, c) * wq[n, c]) << (N_G - 1 - g_c)     (int32)
+ *   Y[m, n]   = fl(float(acc[m, n]) * gamma_n),
+ *   gamma_n   = fl(fl(xscale.step * wscales[n].step) * 2^-(N_G - 1)).
+ * The same call is loss propagation with per-input-channel weights: pass the
+ * gradient's codes as X, W^T codes as wq and their per-column scales.
+ * Inputs : xq_fold, ld_fold, layout, group, xscale from sq_quantize_grad of
+ *          X [M, C_in] with the same p; wq [C_out, ld_w] int8 W codes
+ *          (ld_w >= C_in) with wscales [C_out] from sq_quantize_channels
+ *          (axis 0, transpose 0).
+ * Outputs (either may be NULL, not both): acc [M, ld_acc] int32,
+ *          Y [M, ld_Y] fp32.
+ * Workspace: sq_gemm_dgrad_workspace_size(M, C_in, C_out, p) bytes.
+ * Errors: SQ_ERR_INVALID_ARGUMENT; SQ_ERR_OVERFLOW_RISK when
+ *         C_in * Q * 2^(N_G-1) * 128 >= 2^31; SQ_ERR_WORKSPACE_TOO_SMALL;
+ *         SQ_ERR_HIP.
+ * ------------------------------------------------------------------------- */
+sq_status sq_gemm_forward(const int8_t* xq_fold, int64_t ld_fold, const int32_t* layout,
+                          const uint8_t* group, const sq_scale* xscale,
+                          const int8_t* wq, int64_t ld_w, const sq_scale* wscales,
+                          int64_t M, int64_t C_in, int64_t C_out, const sq_quant_params* p,
+                          int32_t* acc, int64_t ld_acc, float* Y, int64_t ld_Y,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * sq_gemm_dgrad -- loss propagation dX = dY . W as ShiftMM.
  *
  * Eq. "dq_mm_f" and App. D (left-shift form): with 0-indexed groups,
@@ -294,6 +347,8 @@ sq_status sq_conv_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* la
  *   kind 0 (dgrad): out = fl(float(acc) * alpha), alpha as in sq_gemm_dgrad
  *   kind 1 (wgrad): out[r, :] = fl(float(acc[r, :]) * beta_r), beta_r as in
  *                   sq_gemm_wgrad with g_r = group[r]
+ *   kind 2 (per-column weight scales): out[:, c] = fl(float(acc[:, c]) * gamma_c),
+ *                   gamma_c as in sq_gemm_forward, oscale an array [cols]
  * Inputs : acc [rows, ld_acc] int32; group [rows] (kind 1 only); gscale and
  *          oscale (the W scale for kind 0, the X scale for kind 1).
  * Output : out [rows, ld_out] fp32.

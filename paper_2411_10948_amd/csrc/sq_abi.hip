@@ -278,6 +278,85 @@ sq_status sq_gemm_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* la
     return hip_status(launch_gemm(a, s), "gemm_dgrad");
 }
 
+sq_status sq_quantize_channels_workspace_size(int64_t rows, int64_t cols, int32_t axis, size_t* bytes) {
+    SQ_TRY(check_dims(rows, cols, "tensor"));
+    if (axis != 0 && axis != 1) return fail(SQ_ERR_INVALID_ARGUMENT, "axis must be 0 (rows) or 1 (columns)");
+    if (!bytes) return fail(SQ_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    *bytes = axis == 1 ? quant_ws_bytes(rows, cols) : 0;
+    return SQ_OK;
+}
+
+sq_status sq_quantize_channels(const float* T, int64_t rows, int64_t cols, int64_t ld, int32_t bits, int32_t axis,
+                               int32_t transpose, int8_t* q, int64_t ld_q, sq_scale* scales, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+    SQ_TRY(check_dims(rows, cols, "tensor"));
+    if (bits < 2 || bits > 8) return fail(SQ_ERR_INVALID_ARGUMENT, "bits must be in [2, 8]");
+    if (axis != 0 && axis != 1) return fail(SQ_ERR_INVALID_ARGUMENT, "axis must be 0 (rows) or 1 (columns)");
+    if (transpose != 0 && transpose != 1) return fail(SQ_ERR_INVALID_ARGUMENT, "transpose must be 0 or 1");
+    if (rows == 0 || cols == 0) return SQ_OK;
+    SQ_TRY(check_f32(T, ld, cols, "T"));
+    SQ_TRY(check_codes(q, ld_q, transpose ? rows : cols, "q"));
+    if (!scales || !aligned(scales, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "scales is NULL or misaligned");
+    size_t need = 0;
+    SQ_TRY(sq_quantize_channels_workspace_size(rows, cols, axis, &need));
+    if (need > 0) {
+        if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
+        if (workspace_bytes < need) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+    }
+    return hip_status(launch_quantize_channels(T, rows, cols, ld, bits, axis, transpose, q, ld_q, scales,
+                                               static_cast<uint32_t*>(workspace), static_cast<hipStream_t>(stream)),
+                      "quantize_channels");
+}
+
+sq_status sq_gemm_forward(const int8_t* xq_fold, int64_t ld_fold, const int32_t* layout, const uint8_t* group,
+                          const sq_scale* xscale, const int8_t* wq, int64_t ld_w, const sq_scale* wscales, int64_t M,
+                          int64_t C_in, int64_t C_out, const sq_quant_params* p, int32_t* acc, int64_t ld_acc,
+                          float* Y, int64_t ld_Y, void* workspace, size_t workspace_bytes, void* stream) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_dims(M, C_in, "activation codes"));
+    SQ_TRY(check_dims(C_out, C_out, "weight codes"));
+    if (!acc && !Y) return fail(SQ_ERR_INVALID_ARGUMENT, "acc and Y are both NULL");
+    if (!layout || !xscale || !wscales) return fail(SQ_ERR_INVALID_ARGUMENT, "layout or a scale is NULL");
+    const QuantCfg cfg = make_cfg(*p);
+    const double bound = (double)C_in * cfg.Q * (double)(1 << (cfg.num_groups - 1)) * 128.0;
+    if (bound >= 2147483648.0)
+        return fail(SQ_ERR_OVERFLOW_RISK, "C_in * Q * 2^(N_G-1) * 128 reaches 2^31: the int32 accumulator could overflow");
+    if (M == 0 || C_out == 0) return SQ_OK;
+    size_t lay_bytes = 0;
+    int64_t min_ld_fold = 0;
+    SQ_TRY(sq_grad_layout_size(C_in, p, &lay_bytes, &min_ld_fold));
+    SQ_TRY(check_codes(xq_fold, ld_fold, min_ld_fold, "xq_fold"));
+    SQ_TRY(check_codes(wq, ld_w, C_in > 0 ? C_in : 1, "wq"));
+    if (acc) SQ_TRY(check_f32(acc, ld_acc, C_out, "acc"));
+    if (Y) SQ_TRY(check_f32(Y, ld_Y, C_out, "Y"));
+    const int64_t ext_max = fold_ext_max(C_in, cfg);
+    size_t need = 0;
+    SQ_TRY(sq_gemm_dgrad_workspace_size(M, C_in, C_out, p, &need));
+    if (need > 0) {
+        if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
+        if (workspace_bytes < need) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    GemmArgs a{};
+    a.Mg = M; a.Ng = C_out;
+    a.A = xq_fold; a.lda = ld_fold;
+    a.B = wq; a.ldb = ld_w;
+    a.K = C_in;
+    a.layout = layout;
+    if (ext_max > 0) {
+        int8_t* wext = static_cast<int8_t*>(workspace);
+        SQ_TRY(hip_status(launch_gather_ext(wq, ld_w, C_out, layout, wext, ext_max, ext_max, s), "gather"));
+        a.extA = xq_fold + fold_ext_base(C_in); a.ld_extA = ld_fold;
+        a.extB = wext; a.ld_extB = ext_max;
+    }
+    a.splits = 1;
+    a.acc = acc; a.ld_acc = ld_acc;
+    a.out = Y; a.ld_out = ld_Y;
+    a.epi_mode = 2;
+    a.gs = xscale; a.os = wscales; a.group = group; a.num_groups = cfg.num_groups;
+    return hip_status(launch_gemm(a, s), "gemm_forward");
+}
+
 static int64_t grouped_ws_parts(int64_t M, int64_t C_out, int64_t C_in, const QuantCfg& cfg, int64_t* off_a,
                                  int64_t* off_b, int64_t* off_p) {
     const int64_t wmax = grouped_width(C_out, cfg.num_groups);
@@ -492,7 +571,7 @@ sq_status sq_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_t ld_
                      const uint8_t* group, const sq_scale* gscale, const sq_scale* oscale, int32_t num_groups,
                      float* out, int64_t ld_out, void* stream) {
     SQ_TRY(check_dims(rows, cols, "accumulator"));
-    if (kind != 0 && kind != 1) return fail(SQ_ERR_INVALID_ARGUMENT, "kind must be 0 (dgrad) or 1 (wgrad)");
+    if (kind < 0 || kind > 2) return fail(SQ_ERR_INVALID_ARGUMENT, "kind must be 0 (dgrad), 1 (wgrad) or 2 (per-column)");
     if (num_groups < 1 || num_groups > 8) return fail(SQ_ERR_INVALID_ARGUMENT, "num_groups must be in [1, 8]");
     if (!gscale || !oscale) return fail(SQ_ERR_INVALID_ARGUMENT, "a scale is NULL");
     if (rows == 0 || cols == 0) return SQ_OK;

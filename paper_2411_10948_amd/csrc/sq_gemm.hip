@@ -134,6 +134,12 @@ __device__ __forceinline__ FoldView fold_view(const GemmArgs& p, int bk) {
     return v;
 }
 
+// Output-column scale of epi_mode 2 (one weight scale per output column):
+// fl(fl(step_G * step_W[n]) * 2^-(N_G - 1)).
+__device__ __forceinline__ float col_scale(const GemmArgs& p, float gstep, int64_t n) {
+    return __fmul_rn(__fmul_rn(gstep, p.os[n].step), pow2f(-(p.num_groups - 1)));
+}
+
 // Region starts of the flat K sequence, in order; at each one the
 // accumulator is shifted left by the base difference to the region before
 // (Horner's rule).  The schedule is read once into registers, so the K loop
@@ -299,9 +305,10 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm(GemmArgs p, int64_t tiles_
     }
 
     // ---- epilogue ----
-    float base = 0.0f, alpha = 0.0f;
+    float base = 0.0f, alpha = 0.0f, gstep = 0.0f;
     if (p.out && !p.part) {
         const sq_scale gs = *p.gs, os = *p.os;
+        gstep = gs.step;
         base = __fmul_rn(gs.step, os.step);
         alpha = __fmul_rn(base, pow2f(-(p.num_groups - 1)));
     }
@@ -309,6 +316,17 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm(GemmArgs p, int64_t tiles_
     const bool vec_out = p.out && ((p.ld_out & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.out) & 15) == 0);
     const bool vec_part = p.part && ((p.Ng & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.part) & 15) == 0);
     constexpr int kQuads = T::NACC / 4;   // groups of 4 consecutive columns per lane and MFMA block
+    // epi_mode 2: this lane's output columns are the same for every row
+    float cs[T::FN][kQuads][4];
+#pragma unroll
+    for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+        for (int q = 0; q < kQuads; ++q) {
+            const int64_t jj = n0 + wn * T::TN + j * T::MF + (T::MF == 32 ? q * 8 + (lane / 32) * 4 : (lane / 16) * 4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                cs[j][q][e] = (p.epi_mode == 2 && p.out && !p.part && jj + e < p.Ng) ? col_scale(p, gstep, jj + e) : 0.0f;
+        }
 #pragma unroll
     for (int i = 0; i < T::FM; ++i) {
         const int64_t ii = m0 + wm * T::TM + i * T::MF + lane % T::MF;
@@ -352,8 +370,12 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm(GemmArgs p, int64_t tiles_
                 }
                 if (p.out) {
                     float* dst = p.out + ii * p.ld_out + jj;
-                    const float f0 = __fmul_rn((float)v0, sc), f1 = __fmul_rn((float)v1, sc);
-                    const float f2 = __fmul_rn((float)v2, sc), f3 = __fmul_rn((float)v3, sc);
+                    float s4[4] = {sc, sc, sc, sc};
+                    if (p.epi_mode == 2)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) s4[e] = cs[j][q][e];
+                    const float f0 = __fmul_rn((float)v0, s4[0]), f1 = __fmul_rn((float)v1, s4[1]);
+                    const float f2 = __fmul_rn((float)v2, s4[2]), f3 = __fmul_rn((float)v3, s4[3]);
                     if (vec_out && full) {
                         *reinterpret_cast<float4*>(dst) = make_float4(f0, f1, f2, f3);
                     } else {
@@ -643,9 +665,10 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
     // ---- epilogue (as in the register-staged kernel; the fold's final shift
     // is applied per element) ----
     const int fsh = HORNER ? fv.fshift : 0;
-    float base = 0.0f, alpha = 0.0f;
+    float base = 0.0f, alpha = 0.0f, gstep = 0.0f;
     if (p.out && !p.part) {
         const sq_scale gs = *p.gs, os = *p.os;
+        gstep = gs.step;
         base = __fmul_rn(gs.step, os.step);
         alpha = __fmul_rn(base, pow2f(-(p.num_groups - 1)));
     }
@@ -653,6 +676,17 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
     const bool vec_out = p.out && ((p.ld_out & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.out) & 15) == 0);
     const bool vec_part = p.part && ((p.Ng & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.part) & 15) == 0);
     constexpr int kQuads = T::NACC / 4;
+    // epi_mode 2: this lane's output columns are the same for every row
+    float cs[T::FN][kQuads][4];
+#pragma unroll
+    for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+        for (int q = 0; q < kQuads; ++q) {
+            const int64_t jj = n0 + wn * T::TN + j * T::MF + (T::MF == 32 ? q * 8 + (lane / 32) * 4 : (lane / 16) * 4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                cs[j][q][e] = (p.epi_mode == 2 && p.out && !p.part && jj + e < p.Ng) ? col_scale(p, gstep, jj + e) : 0.0f;
+        }
 #pragma unroll
     for (int i = 0; i < T::FM; ++i) {
         const int64_t ii = m0 + wm * T::TM + i * T::MF + lane % T::MF;
@@ -693,8 +727,12 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
                 }
                 if (p.out) {
                     float* dst = p.out + ii * p.ld_out + jj;
-                    const float f0 = __fmul_rn((float)v0, sc), f1 = __fmul_rn((float)v1, sc);
-                    const float f2 = __fmul_rn((float)v2, sc), f3 = __fmul_rn((float)v3, sc);
+                    float s4[4] = {sc, sc, sc, sc};
+                    if (p.epi_mode == 2)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) s4[e] = cs[j][q][e];
+                    const float f0 = __fmul_rn((float)v0, s4[0]), f1 = __fmul_rn((float)v1, s4[1]);
+                    const float f2 = __fmul_rn((float)v2, s4[2]), f3 = __fmul_rn((float)v3, s4[3]);
                     if (vec_out && full) {
                         *reinterpret_cast<float4*>(dst) = make_float4(f0, f1, f2, f3);
                     } else {
@@ -1125,8 +1163,10 @@ __global__ void k_dequant(const int32_t* __restrict__ acc, int64_t rows, int64_t
     const float alpha = __fmul_rn(base, pow2f(-(num_groups - 1)));
     for (int64_t r = blockIdx.x; r < rows; r += gridDim.x) {
         const float sc = kind == 1 ? __fmul_rn(base, pow2f(-(int)group[r])) : alpha;
-        for (int64_t c = threadIdx.x; c < cols; c += blockDim.x)
-            out[r * ld_out + c] = __fmul_rn((float)acc[r * ld_acc + c], sc);
+        for (int64_t c = threadIdx.x; c < cols; c += blockDim.x) {
+            const float s = kind == 2 ? __fmul_rn(__fmul_rn(gs->step, os[c].step), pow2f(-(num_groups - 1))) : sc;
+            out[r * ld_out + c] = __fmul_rn((float)acc[r * ld_acc + c], s);
+        }
     }
 }
 

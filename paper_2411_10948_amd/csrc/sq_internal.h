@@ -89,6 +89,12 @@ hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, con
                            int8_t* q_fold, int64_t ld_fold, int8_t* q_t, int64_t ld_t,
                            const int32_t* desc, hipStream_t s);
 
+// Per-channel weight quantization: axis 0 one scale per row, axis 1 one per
+// column (partial: colmax scratch, axis 1 only).
+hipError_t launch_quantize_channels(const float* x, int64_t rows, int64_t cols, int64_t ld, int bits, int axis,
+                                   int transpose, int8_t* q, int64_t ld_q, sq_scale* scales, uint32_t* partial,
+                                   hipStream_t s);
+
 // ---- GEMMs (sq_gemm.hip) ----
 struct GemmArgs {
     int64_t Mg, Ng;                 // output rows / columns
@@ -102,7 +108,7 @@ struct GemmArgs {
     int32_t* acc; int64_t ld_acc;   // int32 output
     float* out; int64_t ld_out;     // fp32 output
     int32_t* part;                  // split-K: partial tiles [splits, Mg, Ng] instead of acc/out
-    int epi_mode;                   // 0: dgrad scale, 1: wgrad per-row scale
+    int epi_mode;                   // 0: dgrad scale, 1: wgrad per-row scale, 2: per-column scales os[n]
     const sq_scale* gs;
     const sq_scale* os;
     const uint8_t* group;

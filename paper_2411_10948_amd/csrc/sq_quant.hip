@@ -744,6 +744,50 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
 }  // namespace
 
 // ---------------------------------------------------------------------------
+// Per-channel quantization of a weight matrix (one scale per row or per
+// column; the forward pass quantizes weights per output channel and loss
+// propagation per input channel, Sec. 5.1).  Weights are quantized once per
+// step, off the backward hot path, so these kernels are plain.
+// ---------------------------------------------------------------------------
+// column scales from the colmax slab maxima
+__global__ void k_channel_scales_cols(const uint32_t* __restrict__ partial, int64_t S, int64_t C, int Q,
+                                      sq_scale* __restrict__ scales) {
+    for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < C; c += (int64_t)gridDim.x * blockDim.x)
+        scales[c] = make_scale(reduce_slabs(partial, S, C, c), (float)Q);
+}
+
+// row scales: one wave per row
+__global__ void k_channel_scales_rows(const float* __restrict__ x, int64_t rows, int64_t cols, int64_t ld, int Q,
+                                      sq_scale* __restrict__ scales) {
+    const int lane = threadIdx.x & 63;
+    const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+    for (int64_t r = wave; r < rows; r += nwaves) {
+        uint32_t m = 0u;
+        for (int64_t c = lane; c < cols; c += 64) m = max(m, absbits(x[r * ld + c]));
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, o, 64));
+        if (lane == 0) scales[r] = make_scale(m, (float)Q);
+    }
+}
+
+// code = clamp(rint(fl(x * inv_ch)), -Q, Q), 0 in a flagged channel
+__global__ void k_quantize_channels(const float* __restrict__ x, int64_t rows, int64_t cols, int64_t ld, int axis,
+                                    const sq_scale* __restrict__ scales, int Q, int8_t* __restrict__ q, int64_t ld_q,
+                                    int transpose) {
+    const float Qf = (float)Q;
+    const int64_t n = rows * cols;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = transpose ? e % rows : e / cols, j = transpose ? e / rows : e % cols;
+        const sq_scale sc = scales[axis == 0 ? i : j];
+        int code = 0;
+        if (sc.flags == 0u) code = (int)fminf(fmaxf(rintf(__fmul_rn(x[i * ld + j], sc.inv)), -Qf), Qf);
+        if (transpose) q[j * ld_q + i] = (int8_t)code;
+        else q[i * ld_q + j] = (int8_t)code;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
 ColmaxPlan colmax_plan(int64_t M, int64_t C, bool vec) {
@@ -850,6 +894,28 @@ hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, con
     else if (tr == 64) SQ_LAUNCH_QUANT(128, 64);
     else SQ_LAUNCH_QUANT(128, 128);
 #undef SQ_LAUNCH_QUANT
+    return hipGetLastError();
+}
+
+hipError_t launch_quantize_channels(const float* x, int64_t rows, int64_t cols, int64_t ld, int bits, int axis,
+                                   int transpose, int8_t* q, int64_t ld_q, sq_scale* scales, uint32_t* partial,
+                                   hipStream_t s) {
+    if (rows <= 0 || cols <= 0) return hipSuccess;
+    const int Q = (1 << (bits - 1)) - 1;
+    if (axis == 1) {
+        int64_t slabs = 0;
+        const hipError_t e = launch_colmax(x, rows, cols, ld, partial, &slabs, s);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(k_channel_scales_cols, dim3((unsigned)std::min<int64_t>((cols + 255) / 256, 4096)), dim3(256),
+                           0, s, partial, slabs, cols, Q, scales);
+    } else {
+        hipLaunchKernelGGL(k_channel_scales_rows, dim3((unsigned)std::min<int64_t>((rows + 3) / 4, 8192)), dim3(256), 0,
+                           s, x, rows, cols, ld, Q, scales);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_quantize_channels, dim3((unsigned)std::min<int64_t>((rows * cols + 255) / 256, 16384)),
+                       dim3(256), 0, s, x, rows, cols, ld, axis, scales, Q, q, ld_q, transpose);
     return hipGetLastError();
 }
 

@@ -37,9 +37,9 @@ FLAG_ZERO = 2
 EXPORTS = (
     "sq_grad_layout_size", "sq_quantize_grad_workspace_size", "sq_quantize_tensor_workspace_size",
     "sq_gemm_dgrad_workspace_size", "sq_gemm_wgrad_workspace_size", "sq_conv_dgrad_workspace_size",
-    "sq_gemm_dgrad_grouped_workspace_size",
+    "sq_gemm_dgrad_grouped_workspace_size", "sq_quantize_channels_workspace_size",
     "sq_quantize_grad", "sq_quantize_tensor", "sq_gemm_dgrad", "sq_gemm_wgrad", "sq_conv_dgrad", "sq_dequant",
-    "sq_gemm_dgrad_grouped",
+    "sq_gemm_dgrad_grouped", "sq_quantize_channels", "sq_gemm_forward",
     "sq_status_string", "sq_last_error",
 )
 
@@ -91,6 +91,11 @@ def load() -> ct.CDLL:
         "sq_dequant": [_P, _I64, _I64, _I64, ct.c_int32, _P, _P, _P, ct.c_int32, _P, _I64, _P],
         "sq_conv_dgrad_workspace_size": [_I64, _I64, ct.c_int32, ct.c_int32, pp, ct.POINTER(_SZ)],
         "sq_gemm_dgrad_grouped_workspace_size": [_I64, _I64, _I64, pp, ct.POINTER(_SZ)],
+        "sq_quantize_channels_workspace_size": [_I64, _I64, ct.c_int32, ct.POINTER(_SZ)],
+        "sq_quantize_channels": [_P, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32, _P, _I64, _P, _P, _SZ,
+                                 _P],
+        "sq_gemm_forward": [_P, _I64, _P, _P, _P, _P, _I64, _P, _I64, _I64, _I64, pp, _P, _I64, _P, _I64, _P,
+                            _SZ, _P],
         "sq_gemm_dgrad_grouped": [_P, _I64, _P, _P, _P, _P, _I64, _P, _I64, _I64, _I64, pp, _P, _I64, _P, _I64,
                                   _P, _SZ, _P],
         "sq_conv_dgrad": [_P, _I64, _P, _P, _P, _P, _I64, _P, _I64, _I64, _I64, _I64, _I64, ct.c_int32,
@@ -190,6 +195,29 @@ def sq_gemm_dgrad_grouped_workspace_size(M: int, C_out: int, C_in: int, params: 
     _check("sq_gemm_dgrad_grouped_workspace_size",
            load().sq_gemm_dgrad_grouped_workspace_size(M, C_out, C_in, ct.byref(params), ct.byref(nb)))
     return nb.value
+
+
+def sq_quantize_channels_workspace_size(rows: int, cols: int, axis: int) -> int:
+    nb = _SZ(0)
+    _check("sq_quantize_channels_workspace_size",
+           load().sq_quantize_channels_workspace_size(rows, cols, axis, ct.byref(nb)))
+    return nb.value
+
+
+def sq_quantize_channels(T, bits, axis, transpose, q, scales, workspace, stream=None) -> None:
+    rows, cols = T.shape
+    ws, nws = _ws_ptr(workspace)
+    _check("sq_quantize_channels", load().sq_quantize_channels(
+        _ptr(T), rows, cols, _ld(T), bits, axis, int(transpose), _ptr(q), _ld(q), _ptr(scales), ws, nws,
+        _stream(stream)))
+
+
+def sq_gemm_forward(xq_fold, layout, group, xscale, wq, wscales, M, C_in, C_out, params, acc, Y, workspace,
+                    stream=None) -> None:
+    ws, nws = _ws_ptr(workspace)
+    _check("sq_gemm_forward", load().sq_gemm_forward(
+        _ptr(xq_fold), _ld(xq_fold), _ptr(layout), _ptr(group), _ptr(xscale), _ptr(wq), _ld(wq), _ptr(wscales),
+        M, C_in, C_out, ct.byref(params), _ptr(acc), _ld(acc), _ptr(Y), _ld(Y), ws, nws, _stream(stream)))
 
 
 def sq_quantize_grad(dY, params, q_fold, q_t, group, scale, layout, workspace, stream=None) -> None:
@@ -318,6 +346,35 @@ def quantize_tensor(T: torch.Tensor, bits: int = 8, transpose: bool = True, stre
     ws = _workspace(sq_quantize_tensor_workspace_size(rows, cols), dev)
     sq_quantize_tensor(T, bits, transpose, q, scale, ws, stream)
     return q, scale
+
+
+def quantize_channels(T: torch.Tensor, bits: int = 8, axis: int = 0, transpose: bool = False, stream=None):
+    """Per-channel codes of T: one scale per row (axis 0) or column (axis 1).
+    Returns (codes, scales [n, 4] float32 words = n sq_scale structs)."""
+    rows, cols = T.shape
+    dev = T.device
+    if transpose:
+        q = torch.zeros((max(cols, 1), round_up(max(rows, 1), 16)), dtype=torch.int8, device=dev)[:cols]
+    else:
+        q = torch.zeros((max(rows, 1), round_up(max(cols, 1), 16)), dtype=torch.int8, device=dev)[:rows]
+    n = rows if axis == 0 else cols
+    scales = torch.zeros((max(n, 1), 4), dtype=torch.float32, device=dev)
+    ws = _workspace(sq_quantize_channels_workspace_size(rows, cols, axis), dev)
+    sq_quantize_channels(T, bits, axis, transpose, q, scales, ws, stream)
+    return q, scales
+
+
+def gemm_forward(xcodes: GradCodes, wq: torch.Tensor, wscales: torch.Tensor, want_acc: bool = False,
+                 want_out: bool = True, stream=None):
+    """Y = X W^T: xcodes from quantize_grad(X), wq [C_out, C_in] per-output-channel codes."""
+    M, C_in, C_out = xcodes.M, xcodes.C_out, wq.shape[0]
+    dev = wq.device
+    acc = torch.empty((M, C_out), dtype=torch.int32, device=dev) if want_acc else None
+    Y = torch.empty((M, C_out), dtype=torch.float32, device=dev) if want_out else None
+    ws = _workspace(sq_gemm_dgrad_workspace_size(M, C_in, C_out, xcodes.params), dev)
+    sq_gemm_forward(xcodes.q_fold, xcodes.layout, xcodes.group, xcodes.scale, wq, wscales, M, C_in, C_out,
+                    xcodes.params, acc, Y, ws, stream)
+    return acc, Y
 
 
 def gemm_dgrad(codes: GradCodes, wq_t: torch.Tensor, wscale: torch.Tensor, want_acc: bool = False,

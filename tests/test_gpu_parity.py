@@ -548,6 +548,85 @@ def test_dgrad_grouped_matches_shiftmm(sq, bits, ng, shape):
     assert np.array_equal(a2.index_select(0, torch.as_tensor(rows, device="cuda")).cpu().numpy(), A_ref)
 
 
+# ---------------------------------------------------------------------------
+# forward pass: ShiftQuant activations, per-channel weights (Sec. 5.1)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("shape", [(1, 1), (7, 5), (64, 300), (257, 96), (1000, 33)])
+@pytest.mark.parametrize("axis", [0, 1])
+@pytest.mark.parametrize("transpose", [0, 1])
+def test_quantize_channels_parity(sq, shape, axis, transpose):
+    import torch
+    rows, cols = shape
+    rng = np.random.default_rng(rows * 3 + cols + axis)
+    T = (rng.standard_normal(shape) * np.exp(2 * rng.standard_normal((rows, 1)))).astype(np.float32)
+    if rows > 2 and cols > 2:
+        T[1, :] = 0.0            # a zero row
+        T[:, 2] = 0.0            # a zero column
+        T[rows - 1, cols - 1] = np.inf
+    q, scales = sq.quantize_channels(_dev(T), 4 if axis else 8, axis, bool(transpose))
+    torch.cuda.synchronize()
+    q_ref, s_ref = oracle.quantize_channels(T, 4 if axis else 8, axis)
+    got = q.cpu().numpy()
+    got = got[:, :rows].T if transpose else got[:, :cols]
+    assert np.array_equal(got, q_ref)
+    h = scales.cpu().numpy()
+    for ch, s in enumerate(s_ref):
+        assert list(h[ch, :3].view(np.uint32)) == [_f32bits(s["r_max"]), _f32bits(s["inv0"]), _f32bits(s["d0"])]
+        assert int(h[ch, 3:4].view(np.uint32)[0]) == s["flags"]
+
+
+FORWARD_CASES = [(200, 96, 64, 4, 4), (333, 130, 72, 6, 4), (129, 256, 300, 8, 6), (1000, 768, 512, 6, 3),
+                 (64, 64, 64, 4, 1), (4096, 1024, 1024, 4, 4)]
+
+
+@pytest.mark.parametrize("case", FORWARD_CASES, ids=["x".join(map(str, c)) for c in FORWARD_CASES])
+def test_forward_parity(sq, case):
+    # Y = X W^T: X in ShiftQuant groups over its channels, W per output channel
+    import torch
+    M, C_in, C_out, bits, ng = case
+    rng = np.random.default_rng(M + C_in)
+    X = _grad(M, C_in, seed=C_out, s=1.5)
+    W = (rng.standard_normal((C_out, C_in)) * np.exp(rng.standard_normal((C_out, 1)))).astype(np.float32)
+    xc = sq.quantize_grad(_dev(X), bits, ng)
+    wq, ws = sq.quantize_channels(_dev(W), 8, 0, False)
+    acc, Y = sq.gemm_forward(xc, wq, ws, want_acc=True)
+    torch.cuda.synchronize()
+    xq_ref, g_ref, xs_ref = check_quant(sq, xc, X, bits, ng, 0, 0, 0, fold_rows=[0, M - 1])
+    wq_ref, ws_ref = oracle.quantize_channels(W, 8, 0)
+    rows = np.arange(M) if M * C_in * C_out < 2e8 else np.unique(np.r_[0, M - 1, rng.integers(0, M, 20)])
+    A_ref = oracle.dgrad(xq_ref, g_ref, ng, np.ascontiguousarray(wq_ref.T), rows)
+    d_w = np.array([s["d0"] for s in ws_ref], np.float32)
+    Y_ref = oracle.dequant_cols(A_ref, xs_ref["d0"], d_w, ng)
+    rt = torch.as_tensor(rows, device="cuda")
+    assert np.array_equal(acc.index_select(0, rt).cpu().numpy(), A_ref)
+    np.testing.assert_allclose(Y.index_select(0, rt).cpu().numpy(), Y_ref, rtol=RTOL, atol=0)
+    # standalone dequantization (kind 2) of the accumulator gives the fused output
+    out = torch.empty_like(Y)
+    sq.sq_dequant(acc, 2, None, xc.scale, ws, ng, out)
+    torch.cuda.synchronize()
+    assert torch.equal(out, Y)
+
+
+def test_loss_propagation_per_input_channel_weights(sq):
+    # dX = dY W with W quantized per input channel: the forward call with the
+    # gradient's codes, W^T codes and their per-column scales
+    import torch
+    M, C_out, C_in, bits, ng = 700, 200, 160, 6, 4
+    rng = np.random.default_rng(12)
+    dY = _grad(M, C_out, seed=12)
+    W = (rng.standard_normal((C_out, C_in)) * np.exp(rng.standard_normal((1, C_in)))).astype(np.float32)
+    codes = sq.quantize_grad(_dev(dY), bits, ng)
+    wq_t, ws = sq.quantize_channels(_dev(W), 8, 1, True)      # [C_in, C_out], one scale per input channel
+    acc, dX = sq.gemm_forward(codes, wq_t, ws, want_acc=True)
+    torch.cuda.synchronize()
+    q_ref, g_ref, s_ref = check_quant(sq, codes, dY, bits, ng, 0, 0, 0)
+    wq_ref, ws_ref = oracle.quantize_channels(W, 8, 1)
+    A_ref = oracle.dgrad(q_ref, g_ref, ng, wq_ref)
+    dX_ref = oracle.dequant_cols(A_ref, s_ref["d0"], np.array([s["d0"] for s in ws_ref], np.float32), ng)
+    assert np.array_equal(acc.cpu().numpy(), A_ref)
+    np.testing.assert_allclose(dX.cpu().numpy(), dX_ref, rtol=RTOL, atol=0)
+
+
 def test_degenerate_layers(sq):
     rng = np.random.default_rng(2)
     W = (rng.standard_normal((40, 24)) * 0.02).astype(np.float32)
