@@ -122,10 +122,12 @@ sq_status sq_gemm_wgrad_workspace_size(int64_t M, int64_t C_out, int64_t C_in,
  *           the last group N_G - 1 also holding everything below
  *   v     = fl(dY[m, c] * fl(inv * 2^g_c)),  inv = fl(Q / r_max)
  *   code  = clamp(round(v), -Q, Q), round = ties-to-even or stochastic:
- *           floor(v) + [u24 < fl(v - floor(v)) * 2^24] with u24 the top 24
- *           bits of word (i mod 4) of Philox4x32-10(counter = (i / 4 as two
- *           32-bit words, offset as two words), key = seed as two words),
- *           i = m * C_out + c.
+ *           floor(v) + [u16 < fl(v - floor(v)) * 2^16] with u16 the 16-bit
+ *           half (i mod 2, low half first) of word (i / 2) mod 4 of
+ *           Philox4x32-10(counter = (i / 8 as two 32-bit words, offset as two
+ *           words), key = seed as two words), i = m * C_out + c.  One
+ *           Philox block serves 8 elements; the rounding bias is below 2^-16
+ *           of a step.
  *
  * Inputs : dY [M, ld_dY] fp32 (M >= 0, C_out >= 0, ld_dY >= C_out).
  * Outputs (any of q_fold / q_t may be NULL to skip it):

@@ -58,8 +58,8 @@ def _bind(L):
     i64 = ct.c_int64
     L.sqo_philox4x32_10.argtypes = [P, P, P]
     L.sqo_philox4x32_10.restype = None
-    L.sqo_sr_uniform24.argtypes = [ct.c_uint64, ct.c_uint64, ct.c_uint64]
-    L.sqo_sr_uniform24.restype = ct.c_uint32
+    L.sqo_sr_uniform16.argtypes = [ct.c_uint64, ct.c_uint64, ct.c_uint64]
+    L.sqo_sr_uniform16.restype = ct.c_uint32
     L.sqo_channel_range.argtypes = [P, i64, i64, i64, P, P]
     L.sqo_channel_range.restype = ct.c_int
     L.sqo_group_of.argtypes = [ct.c_float, ct.c_float, ct.c_int]
@@ -109,8 +109,8 @@ def philox4x32_10(counter, key) -> np.ndarray:
     return out
 
 
-def sr_uniform24(idx: int, seed: int, offset: int) -> int:
-    return int(lib().sqo_sr_uniform24(idx, seed, offset))
+def sr_uniform16(idx: int, seed: int, offset: int) -> int:
+    return int(lib().sqo_sr_uniform16(idx, seed, offset))
 
 
 def channel_range(x: np.ndarray):

@@ -25,7 +25,7 @@
  *  R5 scaling multiplies by the scale s = fl(Q / r_max) * 2^g, as App. B
  *     writes SR(X S) S^-1; the dequantization factor is fl(r_max / Q).
  *  R6 deterministic rounding is round-half-to-even; stochastic rounding draws
- *     its uniform from Philox4x32-10 (see sqo_quantize_grad).
+ *     a 16-bit uniform from Philox4x32-10 (see sqo_quantize_grad).
  *  R7 codes are clamped to [-Q, Q] after rounding.
  *  R8 the dgrad accumulator is the left-shift form of App. D (each group's
  *     product shifted left by N_G-1-g); the wgrad accumulator is unshifted and
@@ -88,18 +88,19 @@ void sqo_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t ou
     out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
 }
 
-/* The 24-bit uniform integer that stochastic rounding compares against for
- * the element with logical index idx = m * C + c: counter = (idx / 4 split
- * into two words, offset split into two words), key = seed split into two
- * words, word idx % 4 of the output, top 24 bits. */
-uint32_t sqo_sr_uniform24(uint64_t idx, uint64_t seed, uint64_t offset)
+/* The 16-bit uniform integer that stochastic rounding compares against for
+ * the element with logical index idx = m * C + c: one Philox block serves 8
+ * consecutive indices.  counter = (idx / 8 split into two words, offset
+ * split into two words), key = seed split into two words; the element takes
+ * 16-bit half (idx % 2) (low half first) of output word (idx / 2) % 4. */
+uint32_t sqo_sr_uniform16(uint64_t idx, uint64_t seed, uint64_t offset)
 {
-    uint64_t blk = idx >> 2;
+    uint64_t blk = idx >> 3;
     uint32_t ctr[4] = {(uint32_t)blk, (uint32_t)(blk >> 32), (uint32_t)offset, (uint32_t)(offset >> 32)};
     uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
     uint32_t w[4];
     sqo_philox4x32_10(ctr, key, w);
-    return w[idx & 3u] >> 8;
+    return (w[(idx >> 1) & 3u] >> (16u * (uint32_t)(idx & 1u))) & 0xFFFFu;
 }
 
 /* ---------------------------------------------------------------------------
@@ -149,8 +150,9 @@ static int check_qparams(int bits, int num_groups)
  *   v = fl(x * (s * 2^{g_c}))
  *   round_mode 0: q = clamp(round_half_even(v), -Q, Q)             (R6, R7)
  *   round_mode 1: l = floor(v), f = fl(v - l);  q = l + 1 with probability
- *     f (App. B Eq. sq), realised as [u24 < f * 2^24] with u24 from
- *     sqo_sr_uniform24(m * C + c, seed, offset); then clamp.
+ *     f (App. B Eq. sq), realised as [u16 < f * 2^16] with u16 from
+ *     sqo_sr_uniform16(m * C + c, seed, offset), so P(l + 1) = ceil(f 2^16) /
+ *     2^16 (a bias below 2^-16 steps); then clamp.
  * Outputs q [M, C] (row stride C), g [C], *scale.
  * ------------------------------------------------------------------------- */
 int sqo_quantize_grad(const float* dY, int64_t M, int64_t C, int64_t ld, int bits, int num_groups,
@@ -189,7 +191,7 @@ int sqo_quantize_grad(const float* dY, int64_t M, int64_t C, int64_t ld, int bit
     for (int64_t c = 0; c < C; ++c) g[c] = (uint8_t)sqo_group_of(r[c], r_max, num_groups);
     if (!r_out) free(r);
 
-    const float two24 = pow2f(24);
+    const float two16 = pow2f(16);
     for (int64_t m = 0; m < M; ++m) {
         for (int64_t c = 0; c < C; ++c) {
             float s_c = scale->inv0 * pow2f(g[c]);
@@ -200,8 +202,8 @@ int sqo_quantize_grad(const float* dY, int64_t M, int64_t C, int64_t ld, int bit
             } else {
                 float l = floorf(v);
                 float f = v - l;
-                uint32_t u = sqo_sr_uniform24((uint64_t)(m * C + c), seed, offset);
-                qf = ((float)u < f * two24) ? l + 1.0f : l;
+                uint32_t u = sqo_sr_uniform16((uint64_t)(m * C + c), seed, offset);
+                qf = ((float)u < f * two16) ? l + 1.0f : l;
             }
             if (qf > (float)Q) qf = (float)Q;
             if (qf < (float)-Q) qf = (float)-Q;

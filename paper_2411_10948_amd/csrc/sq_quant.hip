@@ -52,21 +52,23 @@ __device__ __forceinline__ uint32_t pick(const U4& w, int i) {
     return i == 0 ? w.x : (i == 1 ? w.y : (i == 2 ? w.z : w.w));
 }
 
-// The 24-bit uniform of the element with logical index idx = m * C + c.
-__device__ __forceinline__ uint32_t sr_uniform24(uint64_t idx, const QuantCfg& cfg) {
-    return pick(philox_block(idx >> 2, cfg), (int)(idx & 3u)) >> 8;
+// The 16-bit uniform of the element with logical index idx = m * C + c: one
+// Philox block per 8 consecutive indices, half idx % 2 (low first) of word
+// (idx / 2) % 4.
+__device__ __forceinline__ uint32_t sr_uniform16(uint64_t idx, const QuantCfg& cfg) {
+    return (pick(philox_block(idx >> 3, cfg), (int)((idx >> 1) & 3u)) >> (16u * (uint32_t)(idx & 1u))) & 0xFFFFu;
 }
 
-// One code: v = fl(x * s); round; clamp to [-Q, Q].  u24 is the 24-bit
+// One code: v = fl(x * s); round; clamp to [-Q, Q].  u16 is the 16-bit
 // uniform used only by stochastic rounding.
 template <bool SR>
-__device__ __forceinline__ int quant_one(float x, float s, float Qf, uint32_t u24) {
+__device__ __forceinline__ int quant_one(float x, float s, float Qf, uint32_t u16) {
     const float v = __fmul_rn(x, s);
     float qf;
     if (SR) {
         const float l = floorf(v);
         const float f = __fsub_rn(v, l);
-        qf = ((float)u24 < __fmul_rn(f, 16777216.0f)) ? __fadd_rn(l, 1.0f) : l;
+        qf = ((float)u16 < __fmul_rn(f, 65536.0f)) ? __fadd_rn(l, 1.0f) : l;
     } else {
         qf = rintf(v);
     }
@@ -638,7 +640,11 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
     const sq_scale sc = *scale;
     const bool zero = sc.flags != 0u;
     const float Qf = (float)cfg.Q;
-    const bool sr_vec = SR && ((C & 3) == 0);   // 4 channels share one Philox block
+    // C a multiple of 8: the channel quads 2k and 2k + 1 of a row share one
+    // Philox block; the two lanes (adjacent) each run it for two of their four
+    // rows and swap the halves the other needs
+    const bool sr_pair = SR && ((C & 7) == 0);
+    const int par = cq & 1;
 
     for (int64_t tile = blockIdx.x; tile < ctiles * rtiles; tile += gridDim.x) {
         const int64_t ct = tile % ctiles, rt = tile / ctiles;
@@ -675,18 +681,41 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
                 }
             }
             uint32_t colw[4] = {0u, 0u, 0u, 0u};   // channel j: rows r0 .. r0 + 3, little-endian
+            // this lane's two Philox words (its quad's 4 halves) for each of its 4 rows
+            uint32_t sw[4][2];
+            if (SR && sr_pair) {
+                const int64_t cpair = c0 & ~(int64_t)7;
+                uint32_t mine[2][4];
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int64_t m = m_tile + r0 + 2 * par + h;
+                    const U4 w = philox_block((uint64_t)(m * C + cpair) >> 3, cfg);
+                    mine[h][0] = w.x; mine[h][1] = w.y; mine[h][2] = w.z; mine[h][3] = w.w;
+                }
+                // own rows 2 par + h: words 2 par, 2 par + 1; the partner's rows
+                // come through a lane swap of the words 2 par, 2 par + 1 it computed
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+#pragma unroll
+                    for (int k = 0; k < 2; ++k) {
+                        const uint32_t give = mine[h][2 * (1 - par) + k];
+                        const uint32_t got = (uint32_t)__shfl_xor((int)give, 1, 64);
+                        sw[2 * par + h][k] = mine[h][2 * par + k];
+                        sw[2 * (1 - par) + h][k] = got;
+                    }
+            }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int64_t m = m_tile + r0 + i;
                 uint32_t u[4] = {0u, 0u, 0u, 0u};
                 if (SR && m < M && c0 < C) {
-                    if (sr_vec) {
-                        const U4 w = philox_block((uint64_t)(m * C + c0) >> 2, cfg);
-                        u[0] = w.x >> 8; u[1] = w.y >> 8; u[2] = w.z >> 8; u[3] = w.w >> 8;
+                    if (sr_pair) {
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) u[j] = (sw[i][j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
                     } else {
 #pragma unroll
                         for (int j = 0; j < 4; ++j)
-                            if (c0 + j < C) u[j] = sr_uniform24((uint64_t)(m * C + c0 + j), cfg);
+                            if (c0 + j < C) u[j] = sr_uniform16((uint64_t)(m * C + c0 + j), cfg);
                     }
                 }
                 int code[4];
@@ -873,7 +902,9 @@ hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, con
     const bool sr = cfg.round_mode == SQ_ROUND_STOCHASTIC;
     // 128 x 128 tiles where the tensor gives enough of them to fill the chip
     auto n_tiles = [&](int64_t tc, int64_t tr) { return ((C + tc - 1) / tc) * ((M + tr - 1) / tr); };
-    int tc = C <= 64 ? 64 : 128, tr = 128;
+    // stochastic rounding keeps the 64-channel tile: the Philox words of a
+    // 128-channel tile's passes need about 180 registers (2 waves per SIMD)
+    int tc = (C <= 64 || sr) ? 64 : 128, tr = 128;
     if (n_tiles(tc, tr) < kQuantMinTiles) tr = 64;
     if (n_tiles(tc, tr) < kQuantMinTiles) tc = 64;
     const dim3 grid((unsigned)std::min<int64_t>(n_tiles(tc, tr), kQuantMaxBlocks));

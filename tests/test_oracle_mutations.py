@@ -22,7 +22,9 @@ SRC = os.path.join(os.path.dirname(oracle.__file__), "sq_oracle.c")
 MUTATIONS = [
     ("philox multiplier", "(uint64_t)0xD2511F53u * x0", "(uint64_t)0xD2511F55u * x0"),
     ("philox key bump", "k1 += 0xBB67AE85u;", "k1 += 0xBB67AE84u;"),
-    ("philox word select", "return w[idx & 3u] >> 8;", "return w[(idx + 1) & 3u] >> 8;"),
+    ("philox word select", "return (w[(idx >> 1) & 3u] >> (16u * (uint32_t)(idx & 1u))) & 0xFFFFu;",
+     "return (w[(idx >> 1) & 3u] >> (16u * (uint32_t)((idx + 1) & 1u))) & 0xFFFFu;"),
+    ("SR threshold width", "const float two16 = pow2f(16);", "const float two16 = pow2f(15);"),
     ("abs mask", "uint32_t a = f2u(x[m * ld + c]) & 0x7FFFFFFFu;", "uint32_t a = f2u(x[m * ld + c]);"),
     ("threshold index", "float tau_next = r_max * pow2f(-(g + 1));", "float tau_next = r_max * pow2f(-g);"),
     ("threshold closedness", "if (r_c > tau_next) return g;", "if (r_c >= tau_next) return g;"),
@@ -31,8 +33,8 @@ MUTATIONS = [
     ("dropped group scale", "float s_c = scale->inv0 * pow2f(g[c]);", "float s_c = scale->inv0;"),
     ("truncation instead of rounding", "qf = rintf(v);", "qf = truncf(v);"),
     ("round half away", "qf = rintf(v);", "qf = roundf(v);"),
-    ("SR comparison direction", "qf = ((float)u < f * two24) ? l + 1.0f : l;",
-     "qf = ((float)u > f * two24) ? l + 1.0f : l;"),
+    ("SR comparison direction", "qf = ((float)u < f * two16) ? l + 1.0f : l;",
+     "qf = ((float)u > f * two16) ? l + 1.0f : l;"),
     ("SR uses ceil", "float l = floorf(v);", "float l = ceilf(v);"),
     ("zero threshold", "else if (r_max < pow2f(-96)) scale->flags = SQO_FLAG_ZERO;",
      "else if (r_max <= pow2f(-96)) scale->flags = SQO_FLAG_ZERO;"),

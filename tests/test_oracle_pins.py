@@ -43,21 +43,23 @@ def test_philox_known_answers():
 
 
 def test_sr_uniform_is_uniform_and_keyed():
-    # chi-square of the 24-bit draws over 64 equal bins (top 6 bits)
+    # chi-square of the 16-bit draws over 64 equal bins (top 6 bits)
     n = 1 << 16
-    u = np.array([oracle.sr_uniform24(i, 7, 3) for i in range(n)], dtype=np.uint32)
-    assert u.max() < (1 << 24)
-    counts = np.bincount(u >> 18, minlength=64)
+    u = np.array([oracle.sr_uniform16(i, 7, 3) for i in range(n)], dtype=np.uint32)
+    assert u.max() < (1 << 16)
+    counts = np.bincount(u >> 10, minlength=64)
     exp = n / 64
     chi2 = float(((counts - exp) ** 2 / exp).sum())
     # 63 degrees of freedom: p = 1e-4 quantile is about 113
     assert chi2 < 113, chi2
-    # the four words of one Philox block feed four consecutive indices
+    # the eight 16-bit halves of one Philox block feed eight consecutive
+    # indices, low half first
     w = oracle.philox4x32_10([5, 0, 3, 0], [7, 0])
-    assert [oracle.sr_uniform24(20 + j, 7, 3) for j in range(4)] == [int(x) >> 8 for x in w]
+    halves = [(int(w[j // 2]) >> (16 * (j % 2))) & 0xFFFF for j in range(8)]
+    assert [oracle.sr_uniform16(40 + j, 7, 3) for j in range(8)] == halves
     # different seed / offset give different streams
-    assert oracle.sr_uniform24(123, 7, 3) != oracle.sr_uniform24(123, 8, 3)
-    assert oracle.sr_uniform24(123, 7, 3) != oracle.sr_uniform24(123, 7, 4)
+    assert oracle.sr_uniform16(123, 7, 3) != oracle.sr_uniform16(123, 8, 3)
+    assert oracle.sr_uniform16(123, 7, 3) != oracle.sr_uniform16(123, 7, 4)
 
 
 # --------------------------------------------------------------------------
@@ -235,9 +237,10 @@ def test_stochastic_rounding_unbiased_and_variance():
     lo = np.floor(v)
     var_cf = (v - lo) * (lo + 1 - v) * step[None, :] ** 2        # (x - l)(u - x)
     assert np.all(var_cf <= step[None, :] ** 2 / 4 * (1 + 1e-12))  # Eq. varup
-    # unbiased: |mean - x| within 5 standard errors (+ the 2^-24 step bias bound)
+    # unbiased: |mean - x| within 5 standard errors (+ the 2^-16 step bias bound
+    # of 16-bit thresholds)
     se = np.sqrt(var_cf / S)
-    assert np.all(np.abs(mean - x) <= 5 * se + step[None, :] * (2.0 ** -23) + 1e-30)
+    assert np.all(np.abs(mean - x) <= 5 * se + step[None, :] * (2.0 ** -16) + 1e-30)
     # variance matches the closed form: in aggregate (sum over 256 elements of
     # Bernoulli variances, relative standard error about 1.2% at S = 1500)
     tot_emp = float((var_emp / step[None, :] ** 2).sum())
