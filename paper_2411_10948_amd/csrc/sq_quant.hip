@@ -215,15 +215,34 @@ __device__ int block_excl_scan(int v, int* sh, int* total) {
 // maximum in bmax[blockIdx.x].
 constexpr int kRedThreads = 256;
 
-__global__ __launch_bounds__(kRedThreads) void k_colmax_reduce(const uint32_t* __restrict__ partial, int64_t S,
-                                                               int64_t C, uint32_t* __restrict__ rbits,
-                                                               uint32_t* __restrict__ bmax) {
-    __shared__ uint32_t shu[kRedThreads / 64];
-    const int64_t c = (int64_t)blockIdx.x * kRedThreads + threadIdx.x;
-    uint32_t r = 0u;
+// kRedLanes threads per channel share its slabs (slab s goes to lane s mod
+// kRedLanes), combined in LDS: a block of kRedThreads channels uses
+// kRedLanes * kRedThreads threads.
+constexpr int kRedLanes = 4;
+__global__ __launch_bounds__(kRedThreads * kRedLanes) void k_colmax_reduce(const uint32_t* __restrict__ partial,
+                                                                           int64_t S, int64_t C,
+                                                                           uint32_t* __restrict__ rbits,
+                                                                           uint32_t* __restrict__ bmax) {
+    __shared__ uint32_t lanes[kRedLanes][kRedThreads];
+    __shared__ uint32_t shu[kRedThreads * kRedLanes / 64];
+    const int ch = threadIdx.x % kRedThreads, ln = threadIdx.x / kRedThreads;
+    const int64_t c = (int64_t)blockIdx.x * kRedThreads + ch;
+    uint32_t a[4] = {0u, 0u, 0u, 0u};
     if (c < C) {
-        r = reduce_slabs(partial, S, C, c);
-        rbits[c] = r;
+        int64_t s = ln;
+        for (; s + 3 * kRedLanes < S; s += 4 * kRedLanes) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) a[u] = max(a[u], partial[(s + u * kRedLanes) * C + c]);
+        }
+        for (; s < S; s += kRedLanes) a[0] = max(a[0], partial[s * C + c]);
+    }
+    lanes[ln][ch] = max(max(a[0], a[1]), max(a[2], a[3]));
+    __syncthreads();
+    uint32_t r = 0u;
+    if (ln == 0) {
+#pragma unroll
+        for (int l = 0; l < kRedLanes; ++l) r = max(r, lanes[l][ch]);
+        if (c < C) rbits[c] = r;
     }
     r = block_max_u32(r, shu);
     if (threadIdx.x == 0) bmax[blockIdx.x] = r;
@@ -591,6 +610,141 @@ __global__ __launch_bounds__(kFinThreads) void k_finalize_grad(const uint32_t* _
     }
 }
 
+// ---------------------------------------------------------------------------
+// Finalize for many channels (C >= kFinThreads), spread over the blocks of
+// the second reduction level (kRedThreads channels each) in two kernels:
+//   k_final_groups: r_max from the per-block maxima (every block), the group
+//     of each of its channels, and the block's count of channels per shift;
+//     with one fold window the descriptors and the header too;
+//   k_final_place:  every block plans the windows from the summed counts
+//     (the same plan everywhere), takes its region offsets from the counts
+//     of the blocks before it, and ranks its appended channels with wave
+//     ballots; block 0 writes the header and the region padding.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kRedThreads) void k_final_groups(const uint32_t* __restrict__ rbits,
+                                                               const uint32_t* __restrict__ bmax, int64_t nb,
+                                                               int64_t C, QuantCfg cfg, uint8_t* __restrict__ group,
+                                                               sq_scale* __restrict__ scale, int32_t* __restrict__ layout,
+                                                               int64_t ext_max, int32_t* __restrict__ hist) {
+    __shared__ uint32_t shu[kRedThreads / 64];
+    __shared__ int cnt[kMaxRegions];
+    const int tid = threadIdx.x;
+    uint32_t mb = 0u;
+    for (int64_t i = tid; i < nb; i += kRedThreads) mb = max(mb, bmax[i]);
+    mb = block_max_u32(mb, shu);
+    const sq_scale sc = make_scale(mb, (float)cfg.Q);
+    if (blockIdx.x == 0 && tid == 0) *scale = sc;
+    const int Sh = cfg.num_groups - 1;
+    const int64_t c = (int64_t)blockIdx.x * kRedThreads + tid;
+    int sh = -1;
+    if (c < C) {
+        const int g = sc.flags ? Sh : group_of(__uint_as_float(rbits[c]), sc.r_max, cfg.num_groups);
+        group[c] = (uint8_t)g;
+        sh = Sh - g;
+    }
+    if (ext_max == 0) {
+        // one window at base 0: the code of channel c is stored as code << sh_c in its own column
+        int32_t* desc = layout + kLayoutHeader;
+        if (c < C) desc[c] = sh;
+        if (blockIdx.x == 0 && tid < kLayoutHeader) {
+            int v = 0;
+            if (tid == kLayNR) v = 1;
+            else if (tid == kLayBase) v = (int)fold_ext_base(C);
+            else if (tid > kLayStart && tid < kLayStart + kMaxRegions) v = 0x7FFFFFFF;
+            layout[tid] = v;
+        }
+        return;
+    }
+    if (tid < kMaxRegions) cnt[tid] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kMaxRegions; ++q) {
+        const uint64_t m = __ballot(sh == q);
+        if ((tid & 63) == 0 && m) atomicAdd(&cnt[q], __popcll(m));
+    }
+    __syncthreads();
+    if (tid < kMaxRegions) hist[blockIdx.x * kMaxRegions + tid] = cnt[tid];
+}
+
+__global__ __launch_bounds__(kRedThreads) void k_final_place(const uint8_t* __restrict__ group,
+                                                              const int32_t* __restrict__ hist, int64_t nb, int64_t C,
+                                                              QuantCfg cfg, int32_t* __restrict__ layout,
+                                                              int64_t ext_max) {
+    __shared__ int tot[kMaxRegions], before[kMaxRegions];
+    __shared__ int wcnt[kRedThreads / 64][kMaxRegions];
+    __shared__ FoldPlan P;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int Sh = cfg.num_groups - 1;
+    // channels per shift: all blocks, and the blocks before this one (thread
+    // t sums shift t % 8 over the blocks b = t / 8 (mod 32), then LDS atomics)
+    if (tid < kMaxRegions) { tot[tid] = 0; before[tid] = 0; }
+    __syncthreads();
+    {
+        const int s = tid % kMaxRegions;
+        int vt = 0, vb = 0;
+        for (int64_t b = tid / kMaxRegions; b < nb; b += kRedThreads / kMaxRegions) {
+            const int h = hist[b * kMaxRegions + s];
+            vt += h;
+            vb += b < (int64_t)blockIdx.x ? h : 0;
+        }
+        if (vt) atomicAdd(&tot[s], vt);
+        if (vb) atomicAdd(&before[s], vb);
+    }
+    __syncthreads();
+    if (tid == 0) make_fold_plan(tot, Sh, cfg.T, C, P);
+    __syncthreads();
+    const int nr = P.nr, main_r = P.main_r;
+    int32_t* ext = layout + kLayoutHeader;
+    int32_t* desc = ext + ext_max;
+    const int64_t c = (int64_t)blockIdx.x * kRedThreads + tid;
+    const int sh = c < C ? Sh - (int)group[c] : 0;
+    const int r = c < C ? P.win_of[sh] : main_r;
+    const bool is_ext = c < C && r != main_r;
+    int rank = 0;
+    const uint64_t below = (1ull << lane) - 1ull;
+    for (int q = 0; q < nr; ++q) {
+        const uint64_t m = __ballot(is_ext && r == q);
+        if (is_ext && r == q) rank = __popcll(m & below);
+        if (lane == 0) wcnt[wave][q] = __popcll(m);
+    }
+    __syncthreads();
+    if (c < C) {
+        int pos = -1;
+        if (is_ext) {
+            // region offset: appended channels of region r in earlier blocks and waves
+            int off = 0;
+#pragma unroll
+            for (int s2 = 0; s2 < kMaxRegions; ++s2)
+                if (s2 <= Sh && P.win_of[s2] == r) off += before[s2];
+            for (int w = 0; w < wave; ++w) off += wcnt[w][r];
+            pos = P.ext_start[r] + off + rank;
+            ext[pos] = (int32_t)c;
+        }
+        desc[c] = ((pos + 1) << 4) | (sh - P.base[r]);
+    }
+    if (blockIdx.x != 0) return;
+    for (int q = 0; q < nr; ++q) {
+        if (q == main_r) continue;
+        const int padded = (int)round_up(P.cnt[q], kFoldPad);
+        for (int i = P.cnt[q] + tid; i < padded; i += kRedThreads) ext[P.ext_start[q] + i] = -1;
+    }
+    if (tid < kLayoutHeader) {
+        int v = 0;
+        if (tid == kLayNR) v = nr;
+        else if (tid == kLayD) v = P.D;
+        else if (tid == kLayBase) v = (int)fold_ext_base(C);
+        else if (tid == kLayF) v = P.F;
+        else if (tid == kLayH) v = P.H;
+        else if (tid >= kLayStart && tid < kLayStart + kMaxRegions)
+            v = tid - kLayStart < nr ? P.flat[tid - kLayStart] : 0x7FFFFFFF;
+        else if (tid >= kLayShift && tid < kLayShift + kMaxRegions) {
+            const int q = tid - kLayShift;
+            v = (q > 0 && q < nr) ? P.base[q - 1] - P.base[q] : 0;
+        }
+        layout[tid] = v;
+    }
+}
+
 // Finalize for per-tensor quantization (one block): the tensor's absolute
 // maximum is the maximum over all slab maxima.
 __global__ __launch_bounds__(kFinThreads) void k_finalize_tensor(const uint32_t* __restrict__ partial, int64_t S,
@@ -844,7 +998,7 @@ int64_t colmax_reduce_blocks(int64_t C) { return C >= kFinThreads ? (C + kRedThr
 int64_t colmax_workspace_words(int64_t M, int64_t C) {
     // worst case over both vector widths: slab maxima + channel ranges + block maxima
     const ColmaxPlan a = colmax_plan(M, C, true), b = colmax_plan(M, C, false);
-    return std::max(a.slabs, b.slabs) * C + C + colmax_reduce_blocks(C);
+    return std::max(a.slabs, b.slabs) * C + C + (1 + kMaxRegions) * colmax_reduce_blocks(C);
 }
 
 hipError_t launch_colmax(const float* x, int64_t M, int64_t C, int64_t ld, uint32_t* partial, int64_t* slabs,
@@ -866,7 +1020,8 @@ static hipError_t launch_reduce(const uint32_t* partial, int64_t slabs, int64_t 
                                 hipStream_t s) {
     const int64_t nb = colmax_reduce_blocks(C);
     if (nb == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_colmax_reduce, dim3((unsigned)nb), dim3(kRedThreads), 0, s, partial, slabs, C, rbits, bmax);
+    hipLaunchKernelGGL(k_colmax_reduce, dim3((unsigned)nb), dim3(kRedThreads * kRedLanes), 0, s, partial, slabs, C,
+                       rbits, bmax);
     return hipGetLastError();
 }
 
@@ -876,8 +1031,19 @@ hipError_t launch_finalize_grad(const uint32_t* partial, int64_t slabs, int64_t 
     uint32_t* bmax = rbits + C;
     const hipError_t e = launch_reduce(partial, slabs, C, rbits, bmax, s);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_finalize_grad, dim3(1), dim3(kFinThreads), 0, s, partial, slabs, C, cfg, rbits, bmax,
-                       colmax_reduce_blocks(C), group, scale, layout, ext_max);
+    const int64_t nb = colmax_reduce_blocks(C);
+    if (nb > 0) {
+        // many channels: groups and placement spread over nb blocks
+        int32_t* hist = reinterpret_cast<int32_t*>(bmax + nb);
+        hipLaunchKernelGGL(k_final_groups, dim3((unsigned)nb), dim3(kRedThreads), 0, s, rbits, bmax, nb, C, cfg, group,
+                           scale, layout, ext_max, hist);
+        if (ext_max > 0)
+            hipLaunchKernelGGL(k_final_place, dim3((unsigned)nb), dim3(kRedThreads), 0, s, group, hist, nb, C, cfg,
+                               layout, ext_max);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL(k_finalize_grad, dim3(1), dim3(kFinThreads), 0, s, partial, slabs, C, cfg, rbits, bmax, nb, group,
+                       scale, layout, ext_max);
     return hipGetLastError();
 }
 
