@@ -84,6 +84,10 @@ def _bind(L):
     L.sqo_dequant_dgrad.restype = None
     L.sqo_dequant_wgrad.argtypes = [P, i64, i64, P, ct.c_float, ct.c_float, P]
     L.sqo_dequant_wgrad.restype = None
+    L.sqo_l1bn_forward.argtypes = [P, i64, i64, ct.c_float, P, P, P, P, P, P, P, P, P, P, P]
+    L.sqo_l1bn_forward.restype = ct.c_int
+    L.sqo_l1bn_backward.argtypes = [P, P, ct.c_float, i64, i64, P, ct.c_float, P, P, P, P, i64, P, P, P]
+    L.sqo_l1bn_backward.restype = ct.c_int
     return L
 
 
@@ -284,3 +288,54 @@ def backward(dY, W, X, bits, num_groups, round_mode=0, seed=0, offset=0,
     dW = dequant_wgrad(B, g_rows, gs["d0"], xs["d0"])
     return {"q": q, "g": g, "gscale": gs, "wq": wq, "wscale": ws, "xq": xq, "xscale": xs,
             "A": A, "B": B, "dX": dX, "dW": dW}
+
+
+def l1bn_forward(xq: np.ndarray, x_step: float, gamma: np.ndarray, beta: np.ndarray) -> dict:
+    """L1BNQ forward (Sec. 4, App. E) of 8-bit codes xq [M, C] with step
+    x_step: y fp32 [M, C] and the per-channel state (mu / sigma codes, sign
+    and deviation sums, quantized gamma / beta, kappa) plus dev_max."""
+    xq = _c(xq, np.int8)
+    M, C = xq.shape
+    gamma = _c(gamma, np.float32)
+    beta = _c(beta, np.float32)
+    assert gamma.shape == (C,) and beta.shape == (C,)
+    n = max(C, 1)
+    y = np.zeros((M, C), np.float32)
+    mu = np.zeros(n, np.int32)
+    sigma = np.zeros(n, np.int32)
+    sign_sum = np.zeros(n, np.int32)
+    dev_sum = np.zeros(n, np.int64)
+    gq = np.zeros(n, np.float32)
+    bq = np.zeros(n, np.float32)
+    kappa = np.zeros(n, np.float32)
+    dev_max = ct.c_int64(0)
+    rc = lib().sqo_l1bn_forward(_p(xq), M, C, float(x_step), _p(gamma), _p(beta), _p(y), _p(mu), _p(sigma),
+                                _p(sign_sum), _p(dev_sum), _p(gq), _p(bq), _p(kappa), ct.byref(dev_max))
+    if rc:
+        raise ValueError(f"sqo_l1bn_forward failed ({rc})")
+    return {"y": y, "mu": mu[:C], "sigma": sigma[:C], "sign_sum": sign_sum[:C], "dev_sum": dev_sum[:C],
+            "gamma_q": gq[:C], "beta_q": bq[:C], "kappa": kappa[:C], "dev_max": int(dev_max.value),
+            "x_step": float(np.float32(x_step)), "M": M}
+
+
+def l1bn_backward(dy: np.ndarray, fwd: dict, xq: np.ndarray, bits: int = 8, num_groups: int = 4,
+                  round_mode: int = 0, seed: int = 0, offset: int = 0) -> dict:
+    """L1BNQ backward: ShiftQuant of dy, then dx, dgamma, dbeta from the
+    forward state `fwd` (as returned by l1bn_forward)."""
+    dy = _c(dy, np.float32)
+    xq = _c(xq, np.int8)
+    M, C = dy.shape
+    assert xq.shape == (M, C)
+    qg, grp, gs, _ = quantize_grad(dy, bits, num_groups, round_mode, seed, offset)
+    dx = np.zeros((M, C), np.float32)
+    n = max(C, 1)
+    dgamma = np.zeros(n, np.float32)
+    dbeta = np.zeros(n, np.float32)
+    f = {k: _c(fwd[k], np.int32) for k in ("mu", "sigma", "sign_sum")}
+    gq = _c(fwd["gamma_q"], np.float32)
+    rc = lib().sqo_l1bn_backward(_p(qg), _p(grp), float(gs["d0"]), M, C, _p(xq), float(fwd["x_step"]),
+                                 _p(f["mu"]), _p(f["sigma"]), _p(f["sign_sum"]), _p(gq), int(fwd["dev_max"]),
+                                 _p(dx), _p(dgamma), _p(dbeta))
+    if rc:
+        raise ValueError(f"sqo_l1bn_backward failed ({rc})")
+    return {"dx": dx, "dgamma": dgamma[:C], "dbeta": dbeta[:C], "qg": qg, "group": grp, "gscale": gs}

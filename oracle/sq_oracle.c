@@ -434,3 +434,143 @@ void sqo_dequant_wgrad(const int32_t* B, int64_t n_rows, int64_t C_in, const uin
         for (int64_t k = 0; k < C_in; ++k) out[i * C_in + k] = (float)B[i * C_in + k] * beta;
     }
 }
+
+/* ---------------------------------------------------------------------------
+ * Fully-quantized L1 batch normalization (L1BNQ), Sec. 4 (Fig. l1bnq) and
+ * App. E.  The paper draws the layer as a figure and states only the
+ * normalization equations, so this follows two readings:
+ *
+ *  R16 forward.  The layer's input is the 8-bit per-tensor code q of x (step
+ *      s_x); statistics are per channel c over the M rows (N*H*W) of the batch.
+ *      The mean is quantized onto the input's own grid,
+ *        m_c = round_half_even(S_c / M),  S_c = sum_m q[m, c],
+ *      so x - mu^q = s_x (q - m_c) exactly.  sigma is the L1 deviation
+ *      (App. E.1) taken as a mean, sigma_c = s_x A_c / M with
+ *      A_c = sum_m |q - m_c|, and is quantized per tensor to 8 bits under the
+ *      step max_c sigma_c / 127:
+ *        k_c = max(1, round_half_even(127 A_c / A_max)),  A_max = max_c A_c,
+ *      (s_x and M cancel in the ratio; the smallest code is kept at 1 so the
+ *      denominator of the quantized normalization of App. E.2 is never 0).
+ *      gamma and beta are quantized per tensor to 8 bits like W and X.  Then
+ *        kappa_c = fl32(gamma^q_c * 127 M / (A_max k_c))   (binary64),
+ *        y = fl(fl(kappa_c * (q - m_c)) + beta^q_c).
+ *      A_max = 0 (every channel constant): kappa = 0, k = 0, y = beta^q.
+ *  R17 backward.  The derivative of the L1 normalization (App. E.1's
+ *      derivation with sigma = mean |x - mu|, which brings in the signs
+ *      s = sgn(x - mu)), the quantizers of mu and sigma passed straight
+ *      through:  dx = (gamma / sigma)(g - mean g - mean(g xhat)(s - mean s)).
+ *      The incoming gradient is quantized with ShiftQuant (codes qg, channel
+ *      steps delta_c = d0 2^-g_c), so the channel sums are integers:
+ *        G1 = sum qg,  G2 = sum qg (q - m),  P = sum sgn(q - m).
+ *      With rho = 127 M / (A_max k) (xhat per code step) and
+ *      lambda = gamma^q rho / s_x (gamma^q / sigma^q), in binary64:
+ *        dbeta = delta G1,  dgamma = (delta G2) rho,  D = dgamma / M,
+ *        a = lambda delta,  b = -(lambda D),  e = lambda (D P / M - delta G1 / M),
+ *      each rounded once to binary32, and
+ *        dx = fl(fl(fl(a qg) + fl(b sgn(q - m))) + e).
+ *      A_max = 0: dgamma = 0 and dx = 0.
+ * ------------------------------------------------------------------------- */
+
+/* round_half_even(num / den) of integers, den > 0 */
+static int64_t div_round_even(int64_t num, int64_t den)
+{
+    int64_t q = num / den, r = num % den;
+    if (r < 0) { q -= 1; r += den; }          /* floor division, 0 <= r < den */
+    if (2 * r > den || (2 * r == den && (q & 1))) q += 1;
+    return q;
+}
+
+int sqo_l1bn_forward(const int8_t* q, int64_t M, int64_t C, float x_step, const float* gamma,
+                     const float* beta, float* y, int32_t* mu, int32_t* sigma, int32_t* sign_sum,
+                     int64_t* dev_sum, float* gamma_q, float* beta_q, float* kappa, int64_t* dev_max)
+{
+    if (!q || !gamma || !beta || !y || !mu || !sigma || !sign_sum || !dev_sum || !gamma_q || !beta_q ||
+        !kappa || !dev_max || M < 1 || C < 0)
+        return SQO_ERR_ARG;
+    (void)x_step;   /* cancels out of the normalized value */
+    int64_t amax = 0;
+    for (int64_t c = 0; c < C; ++c) {
+        int64_t S = 0;
+        for (int64_t m = 0; m < M; ++m) S += q[m * C + c];
+        int64_t mc = div_round_even(S, M);
+        int64_t A = 0, P = 0;
+        for (int64_t m = 0; m < M; ++m) {
+            int64_t d = (int64_t)q[m * C + c] - mc;
+            A += d < 0 ? -d : d;
+            P += (d > 0) - (d < 0);
+        }
+        mu[c] = (int32_t)mc;
+        dev_sum[c] = A;
+        sign_sum[c] = (int32_t)P;
+        if (A > amax) amax = A;
+    }
+    *dev_max = amax;
+    /* parameters: 8-bit per-tensor codes */
+    int8_t* gc = (int8_t*)malloc((size_t)(C > 0 ? C : 1));
+    int8_t* bc = (int8_t*)malloc((size_t)(C > 0 ? C : 1));
+    sqo_scale gs, bs;
+    if (!gc || !bc) { free(gc); free(bc); return SQO_ERR_ARG; }
+    sqo_quantize_tensor(gamma, 1, C, C, 8, gc, &gs);
+    sqo_quantize_tensor(beta, 1, C, C, 8, bc, &bs);
+    for (int64_t c = 0; c < C; ++c) {
+        gamma_q[c] = gs.d0 * (float)gc[c];
+        beta_q[c] = bs.d0 * (float)bc[c];
+        if (amax == 0) {
+            sigma[c] = 0;
+            kappa[c] = 0.0f;
+        } else {
+            int64_t k = div_round_even(127 * dev_sum[c], amax);
+            if (k < 1) k = 1;
+            sigma[c] = (int32_t)k;
+            double num = (double)gamma_q[c] * (127.0 * (double)M);
+            kappa[c] = (float)(num / ((double)amax * (double)k));
+        }
+    }
+    free(gc);
+    free(bc);
+    for (int64_t m = 0; m < M; ++m)
+        for (int64_t c = 0; c < C; ++c) {
+            float d = (float)((int32_t)q[m * C + c] - mu[c]);
+            y[m * C + c] = kappa[c] * d + beta_q[c];
+        }
+    return SQO_OK;
+}
+
+int sqo_l1bn_backward(const int8_t* qg, const uint8_t* grp, float d0, int64_t M, int64_t C, const int8_t* q,
+                      float x_step, const int32_t* mu, const int32_t* sigma, const int32_t* sign_sum,
+                      const float* gamma_q, int64_t dev_max, float* dx, float* dgamma, float* dbeta)
+{
+    if (!qg || !grp || !q || !mu || !sigma || !sign_sum || !gamma_q || !dx || !dgamma || !dbeta || M < 1 || C < 0)
+        return SQO_ERR_ARG;
+    for (int64_t c = 0; c < C; ++c) {
+        int64_t G1 = 0, G2 = 0;
+        for (int64_t m = 0; m < M; ++m) {
+            G1 += qg[m * C + c];
+            G2 += (int64_t)qg[m * C + c] * ((int64_t)q[m * C + c] - mu[c]);
+        }
+        const double delta = (double)(d0 * pow2f(-(int)grp[c]));
+        const double db = delta * (double)G1;
+        dbeta[c] = (float)db;
+        float a = 0.0f, b = 0.0f, e = 0.0f;
+        if (dev_max == 0) {
+            dgamma[c] = 0.0f;
+        } else {
+            const double rho = (127.0 * (double)M) / ((double)dev_max * (double)sigma[c]);
+            const double lambda = ((double)gamma_q[c] * rho) / (double)x_step;
+            const double dg = (delta * (double)G2) * rho;
+            const double D = dg / (double)M;
+            const double gbar = db / (double)M;
+            const double sbar = (double)sign_sum[c] / (double)M;
+            dgamma[c] = (float)dg;
+            a = (float)(lambda * delta);
+            b = (float)(-(lambda * D));
+            e = (float)(lambda * (D * sbar - gbar));
+        }
+        for (int64_t m = 0; m < M; ++m) {
+            int32_t d = (int32_t)q[m * C + c] - mu[c];
+            float s = (float)((d > 0) - (d < 0));
+            dx[m * C + c] = (a * (float)qg[m * C + c] + b * s) + e;
+        }
+    }
+    return SQO_OK;
+}

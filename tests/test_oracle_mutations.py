@@ -58,6 +58,17 @@ MUTATIONS = [
      "float gamma = (d_a * d_w[k]) * pow2f(-num_groups);"),
     ("int32 range check", "if (acc > INT32_MAX || acc < INT32_MIN) return SQO_ERR_RANGE;\n            A[i * C_in + k]",
      "A[i * C_in + k]"),
+    ("L1BN mean truncated", "int64_t mc = div_round_even(S, M);", "int64_t mc = S / M;"),
+    ("L1BN mean ties away", "if (2 * r > den || (2 * r == den && (q & 1))) q += 1;", "if (2 * r >= den) q += 1;"),
+    ("L1BN sigma code floor", "if (k < 1) k = 1;", "if (k < 0) k = 0;"),
+    ("L1BN kappa count", "double num = (double)gamma_q[c] * (127.0 * (double)M);",
+     "double num = (double)gamma_q[c] * (127.0 * (double)(M - 1));"),
+    ("L1BN sign-mean term", "e = (float)(lambda * (D * sbar - gbar));", "e = (float)(lambda * (-gbar));"),
+    ("L1BN sign term sign", "b = (float)(-(lambda * D));", "b = (float)(lambda * D);"),
+    ("L1BN dgamma xhat scale", "const double dg = (delta * (double)G2) * rho;", "const double dg = delta * (double)G2;"),
+    ("L1BN lambda step", "const double lambda = ((double)gamma_q[c] * rho) / (double)x_step;",
+     "const double lambda = ((double)gamma_q[c] * rho) * (double)x_step;"),
+    ("L1BN sign of deviation", "float s = (float)((d > 0) - (d < 0));", "float s = (float)((d < 0) - (d > 0));"),
 ]
 
 
@@ -100,6 +111,11 @@ def _pin_calls():
         calls.append(lambda a=axis: pins.test_quantize_channels_is_per_tensor_per_channel(a, 8))
     calls.append(pins.test_quantize_channels_degenerate_channels)
     calls.append(lambda: pins.test_forward_equals_dequantized_product(4, 4))
+    calls.append(pins.test_l1bn_forward_matches_textbook_when_statistics_are_exact)
+    calls.append(pins.test_l1bn_forward_statistics_bounds_random)
+    calls.append(lambda: pins.test_l1bn_backward_matches_autograd_when_statistics_are_exact(8, 4, 0))
+    calls.append(pins.test_l1bn_backward_is_shift_invariant_random)
+    calls.append(pins.test_l1bn_constant_channels)
     return calls
 
 

@@ -595,3 +595,184 @@ def test_forward_equals_dequantized_product(bits, ng):
     for i, k in [(0, 0), (M - 1, C_out - 1), (5, 7)]:
         gamma = np.float32(np.float32(xs["d0"]) * d_w[k]) * np.float32(2.0 ** -(ng - 1))
         assert Y[i, k] == np.float32(np.float32(A[i, k]) * gamma)
+
+
+# --------------------------------------------------------------------------
+# Fully-quantized L1 batch normalization (Sec. 4, App. E)
+# --------------------------------------------------------------------------
+def _l1bn_exact_codes(rng, C, triplets=64, unit=30):
+    """8-bit codes [3 * triplets, C] whose L1BNQ statistics are exact: every
+    triplet of a channel is mu + (2d, -d, -d) or mu - (2d, -d, -d), so the mean
+    is the integer mu (with a non-zero sign sum), and the deviation sums are
+    4 * unit * k with k = 127 for channel 0, so the 8-bit sigma codes are k
+    exactly."""
+    M = 3 * triplets
+    q = np.zeros((M, C), np.int64)
+    ks = [127] + list(rng.integers(1, 111, C - 1))
+    for c in range(C):
+        mu = 0 if c == 0 else int(rng.integers(-20, 21))
+        cap = 63 if c == 0 else (127 - 20) // 2
+        total = ks[c] * unit
+        d = np.zeros(triplets, np.int64)
+        while total > 0:                      # random composition under the cap
+            j = int(rng.integers(0, triplets))
+            if d[j] < cap:
+                d[j] += 1
+                total -= 1
+        col = []
+        for j in range(triplets):
+            s = 1 if rng.random() < 0.5 else -1
+            col += [mu + s * 2 * d[j], mu - s * d[j], mu - s * d[j]]
+        q[:, c] = rng.permutation(np.array(col))
+    assert np.abs(q).max() <= 127
+    return q.astype(np.int8), np.array(ks)
+
+
+def _l1bn_textbook(x, gamma, beta):
+    """L1 batch normalization in float64 with exact statistics (App. E.1 with
+    sigma the mean L1 deviation)."""
+    mu = x.mean(axis=0)
+    sigma = np.abs(x - mu).mean(axis=0)
+    return gamma * (x - mu) / sigma + beta, mu, sigma
+
+
+def test_l1bn_forward_matches_textbook_when_statistics_are_exact():
+    rng = np.random.default_rng(41)
+    C = 7
+    q, ks = _l1bn_exact_codes(rng, C)
+    x_step = np.float32(0.0173)
+    gamma = rng.normal(1.0, 0.3, C).astype(np.float32)
+    beta = rng.normal(0.0, 0.5, C).astype(np.float32)
+    f = oracle.l1bn_forward(q, x_step, gamma, beta)
+    # quantized parameters are the per-tensor 8-bit quantizer (App. E: every
+    # parameter of the layer is quantized)
+    for name, v in (("gamma_q", gamma), ("beta_q", beta)):
+        codes, sc = oracle.quantize_tensor(v[None, :], 8)
+        np.testing.assert_array_equal(f[name], (np.float32(sc["d0"]) * codes[0].astype(np.float32)))
+    x = q.astype(np.float64) * float(x_step)
+    y_tb, mu, sigma = _l1bn_textbook(x, f["gamma_q"].astype(np.float64), f["beta_q"].astype(np.float64))
+    np.testing.assert_array_equal(f["mu"], np.rint(mu / float(x_step)).astype(np.int32))
+    np.testing.assert_array_equal(f["sigma"], ks)
+    assert (f["sign_sum"] != 0).any()
+    mag = np.abs(f["gamma_q"].astype(np.float64) * (x - mu) / sigma) + np.abs(f["beta_q"])
+    assert np.all(np.abs(f["y"] - y_tb) <= 4 * 2.0 ** -24 * mag)
+
+
+def test_l1bn_forward_statistics_bounds_random():
+    # arbitrary codes: the mean code is the nearest integer to the batch mean
+    # (ties to even), sigma codes are within half a step of 127 A_c / A_max,
+    # and y is the normalization about the quantized mean within the sigma
+    # quantization error
+    rng = np.random.default_rng(42)
+    M, C = 300, 9
+    q = rng.integers(-127, 128, (M, C))
+    q[:, 3] = rng.integers(0, 6, M)           # narrow channel
+    q[:, 5] = -17
+    q[7, 5] = -16                             # near-constant channel: sigma code clamps to 1
+    q[:, 6] = np.where(np.arange(M) < M // 2, 4, 5)   # mean 4.5: tie, to 4
+    q[:, 8] = np.where(np.arange(M) < M // 2, 5, 6)   # mean 5.5: tie, to 6
+    q = q.astype(np.int8)
+    x_step = np.float32(0.031)
+    gamma = rng.normal(1.0, 0.3, C).astype(np.float32)
+    beta = rng.normal(0.0, 0.5, C).astype(np.float32)
+    f = oracle.l1bn_forward(q, x_step, gamma, beta)
+    qi = q.astype(np.float64)
+    mean = qi.mean(axis=0)
+    assert np.all(np.abs(mean - f["mu"]) <= 0.5)
+    ties = np.abs(np.abs(mean - f["mu"]) - 0.5) < 1e-12
+    assert ties[6] and ties[8] and f["mu"][6] == 4 and f["mu"][8] == 6
+    assert np.all(f["mu"][ties] % 2 == 0)
+    A = np.abs(qi - f["mu"]).sum(axis=0)
+    np.testing.assert_array_equal(f["dev_sum"], A.astype(np.int64))
+    assert f["dev_max"] == int(A.max())
+    ratio = 127 * A / A.max()
+    assert np.all((np.abs(f["sigma"] - ratio) <= 0.5) | ((f["sigma"] == 1) & (ratio < 0.5)))
+    assert f["sigma"][5] == 1
+    sgn = np.sign(qi - f["mu"]).sum(axis=0)
+    np.testing.assert_array_equal(f["sign_sum"], sgn.astype(np.int32))
+    # y against the float64 normalization with the quantized statistics
+    x = qi * float(x_step)
+    mu_q = f["mu"] * float(x_step)
+    sig_max = float(x_step) * A.max() / M
+    sig_q = sig_max * f["sigma"] / 127.0
+    y_ref = f["gamma_q"] * (x - mu_q) / sig_q + f["beta_q"]
+    mag = np.abs(f["gamma_q"] * (x - mu_q) / sig_q) + np.abs(f["beta_q"])
+    assert np.all(np.abs(f["y"] - y_ref) <= 4 * 2.0 ** -24 * mag)
+    # and sigma_q within half a code step of the mean deviation about mu_q
+    sig_dev = float(x_step) * A / M
+    assert np.all(np.abs(sig_q - sig_dev) <= sig_max / 254 * (1 + 1e-12) + (f["sigma"] == 1) * sig_max / 127)
+
+
+def _l1bn_autograd(x, gamma, beta, gbar):
+    torch = pytest.importorskip("torch")
+    xt = torch.tensor(x, dtype=torch.float64, requires_grad=True)
+    gt = torch.tensor(gamma, dtype=torch.float64, requires_grad=True)
+    bt = torch.tensor(beta, dtype=torch.float64, requires_grad=True)
+    mu = xt.mean(dim=0)
+    sigma = (xt - mu).abs().mean(dim=0)
+    y = gt * (xt - mu) / sigma + bt
+    y.backward(torch.tensor(gbar, dtype=torch.float64))
+    return xt.grad.numpy(), gt.grad.numpy(), bt.grad.numpy()
+
+
+@pytest.mark.parametrize("bits,ng,mode", [(8, 4, 0), (6, 4, 1), (8, 1, 0)])
+def test_l1bn_backward_matches_autograd_when_statistics_are_exact(bits, ng, mode):
+    # with exact statistics the layer is the textbook L1 normalization, so its
+    # input gradient is the float64 autograd one, fed the dequantized
+    # ShiftQuant gradient delta_c * qg
+    rng = np.random.default_rng(43 + bits + mode)
+    C = 6
+    q, _ = _l1bn_exact_codes(rng, C)
+    M = q.shape[0]
+    x_step = np.float32(0.0219)
+    gamma = rng.normal(1.0, 0.3, C).astype(np.float32)
+    beta = rng.normal(0.0, 0.5, C).astype(np.float32)
+    f = oracle.l1bn_forward(q, x_step, gamma, beta)
+    dy = (rng.normal(size=(M, C)) * np.exp(rng.normal(0, 1.5, C))).astype(np.float32)
+    b = oracle.l1bn_backward(dy, f, q, bits, ng, mode, seed=5, offset=1)
+    delta = np.float32(b["gscale"]["d0"]) * np.float32(2.0) ** (-b["group"].astype(np.float32))
+    gdeq = b["qg"].astype(np.float64) * delta.astype(np.float64)
+    x = q.astype(np.float64) * float(x_step)
+    dx_ref, dg_ref, db_ref = _l1bn_autograd(x, f["gamma_q"], f["beta_q"], gdeq)
+    _, mu, sigma = _l1bn_textbook(x, f["gamma_q"].astype(np.float64), f["beta_q"].astype(np.float64))
+    xhat = (x - mu) / sigma
+    lam = np.abs(f["gamma_q"] / sigma)
+    mag = lam * (np.abs(gdeq) + np.abs(gdeq.mean(0)) + 2 * np.abs((gdeq * xhat).mean(0)))
+    assert np.all(np.abs(b["dx"] - dx_ref) <= 1e-6 * mag + 1e-30)
+    np.testing.assert_allclose(b["dgamma"], dg_ref, rtol=1e-6, atol=1e-6 * np.abs(gdeq * xhat).sum(0).max())
+    np.testing.assert_allclose(b["dbeta"], db_ref, rtol=1e-6, atol=1e-6 * np.abs(gdeq).sum(0).max())
+
+
+def test_l1bn_backward_is_shift_invariant_random():
+    # the normalized output does not change when a channel is shifted by a
+    # constant, so the input gradient sums to zero over every channel
+    rng = np.random.default_rng(44)
+    M, C = 257, 5
+    q = rng.integers(-90, 120, (M, C)).astype(np.int8)
+    f = oracle.l1bn_forward(q, 0.02, rng.normal(1, 0.3, C), rng.normal(0, 0.5, C))
+    dy = rng.normal(size=(M, C)).astype(np.float32)
+    b = oracle.l1bn_backward(dy, f, q, 8, 4)
+    scale = np.abs(b["dx"]).sum(axis=0)
+    assert np.all(np.abs(b["dx"].astype(np.float64).sum(axis=0)) <= 1e-5 * scale)
+    assert np.abs(b["dx"]).max() > 0
+
+
+def test_l1bn_constant_channels():
+    # every channel constant: nothing to normalize, y = beta^q, no input gradient
+    M, C = 11, 4
+    q = np.tile(np.array([3, -5, 0, 127], np.int8), (M, 1))
+    gamma = np.array([1.0, 2.0, -1.0, 0.5], np.float32)
+    beta = np.array([0.25, -1.0, 0.0, 2.0], np.float32)
+    f = oracle.l1bn_forward(q, 0.1, gamma, beta)
+    assert f["dev_max"] == 0
+    np.testing.assert_array_equal(f["sigma"], 0)
+    np.testing.assert_array_equal(f["y"], np.tile(f["beta_q"], (M, 1)))
+    dy = np.linspace(-1, 1, M * C, dtype=np.float32).reshape(M, C)
+    b = oracle.l1bn_backward(dy, f, q, 8, 4)
+    np.testing.assert_array_equal(b["dx"], 0)
+    np.testing.assert_array_equal(b["dgamma"], 0)
+    delta = np.float32(b["gscale"]["d0"]) * np.float32(2.0) ** (-b["group"].astype(np.float32))
+    np.testing.assert_allclose(b["dbeta"], delta * b["qg"].astype(np.int64).sum(0), rtol=1e-7)
+    # one row: every channel constant as well
+    f1 = oracle.l1bn_forward(q[:1], 0.1, gamma, beta)
+    assert f1["dev_max"] == 0
