@@ -360,6 +360,123 @@ sq_status sq_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_t ld_
                      const uint8_t* group, const sq_scale* gscale, const sq_scale* oscale,
                      int32_t num_groups, float* out, int64_t ld_out, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * sq_quantize_grad_from_ranges -- sq_quantize_grad with the channel ranges
+ * supplied by the producer of dY.
+ *
+ * The quantizer's first step (r_c = max_m |dY[m, c]|, Sec. 3.1) reads all of
+ * dY once before the codes can be formed; a kernel that writes dY can take
+ * those maxima on the fly instead.  `ranges` holds them as partial maxima:
+ * ranges[s, c], s < range_slabs, is the bit pattern of max |dY[m, c]| over
+ * some subset of the rows (sign bit cleared, so NaN and Inf compare above
+ * every finite value), the subsets covering all M rows; r_c is the maximum
+ * over s.  Everything else -- outputs, layout, workspace
+ * (sq_quantize_grad_workspace_size), errors -- is as in sq_quantize_grad, and
+ * the results are identical when the ranges are exact.
+ * sq_l1bn_backward writes such ranges for its dx.
+ * ------------------------------------------------------------------------- */
+sq_status sq_quantize_grad_from_ranges(const float* dY, int64_t M, int64_t C_out, int64_t ld_dY,
+                                       const sq_quant_params* p, const uint32_t* ranges, int64_t range_slabs,
+                                       int8_t* q_fold, int64_t ld_fold,
+                                       int8_t* q_t, int64_t ld_t,
+                                       uint8_t* group, sq_scale* scale, int32_t* layout,
+                                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Fully-quantized L1 batch normalization (L1BNQ), Sec. 4 (Fig. l1bnq) and
+ * App. E.1 / E.2: input features, statistics and parameters are quantized,
+ * and the normalization divides by the L1 deviation instead of the standard
+ * deviation.
+ *
+ * Per-channel state written by sq_l1bn_forward and read by sq_l1bn_backward
+ * (device memory, one entry per channel):
+ *   mu       m_c = round_half_even(S_c / M), S_c = sum_m q[m, c]: the batch mean
+ *            quantized onto the input's own 8-bit grid (mu^q = s_x m_c)
+ *   sigma    k_c = max(1, round_half_even(127 A_c / A_max)): the L1 deviation
+ *            sigma_c = s_x A_c / M quantized per tensor to 8 bits under the
+ *            step max_c sigma_c / 127 (0 when the layer is flagged ZERO)
+ *   sign_sum P_c = sum_m sgn(q[m, c] - m_c)
+ *   gamma, beta  gamma^q_c, beta^q_c: the parameters quantized per tensor to
+ *            8 bits (as sq_quantize_tensor), dequantized
+ *   kappa    fl32(gamma^q_c 127 M / (A_max k_c)), evaluated in binary64
+ *   dev_sum  A_c = sum_m |q[m, c] - m_c|
+ * Layer state: rows M, dev_max A_max = max_c A_c, x_step s_x (the input's
+ * step), flags (SQ_FLAG_ZERO when A_max = 0: every channel constant), and the
+ * scales of gamma and beta.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+    int32_t mu;
+    int32_t sigma;
+    int32_t sign_sum;
+    float gamma;
+    float beta;
+    float kappa;
+    int64_t dev_sum;
+} sq_l1bn_channel;      /* 32 bytes */
+
+typedef struct {
+    int64_t rows;
+    int64_t dev_max;
+    float x_step;
+    uint32_t flags;
+    sq_scale gamma_scale;
+    sq_scale beta_scale;
+} sq_l1bn_layer;        /* 56 bytes */
+
+/* Partial-maximum slabs that sq_l1bn_backward writes to dx_ranges
+ * ([slabs, C] uint32) for M rows and C channels. */
+sq_status sq_l1bn_range_slabs(int64_t M, int64_t C, int64_t* slabs);
+sq_status sq_l1bn_forward_workspace_size(int64_t M, int64_t C, size_t* bytes);
+sq_status sq_l1bn_backward_workspace_size(int64_t M, int64_t C, const sq_quant_params* p, size_t* bytes);
+
+/* ---------------------------------------------------------------------------
+ * sq_l1bn_forward -- L1BNQ forward over a batch (training statistics).
+ *   y[m, c] = fl(fl(kappa_c (q[m, c] - m_c)) + beta^q_c),
+ * i.e. gamma^q (x^q - mu^q) / sigma^q + beta^q with x^q = s_x q (App. E.2's
+ * normalization with quantized statistics); with A_max = 0, y = beta^q.
+ * Inputs : xq [M, ld_x] int8, the 8-bit per-tensor codes of the layer input
+ *          (sq_quantize_tensor, bits 8), 16-byte aligned, ld_x % 16 == 0;
+ *          xscale its sq_scale (device); gamma, beta [C] fp32 (device).
+ *          1 <= M <= 2^24.
+ * Outputs: y [M, ld_y] fp32; chan [C] and layer (device) for the backward.
+ * Workspace: sq_l1bn_forward_workspace_size bytes.
+ * Errors: SQ_ERR_INVALID_ARGUMENT, SQ_ERR_UNSUPPORTED (M > 2^24),
+ *         SQ_ERR_WORKSPACE_TOO_SMALL, SQ_ERR_HIP.
+ * ------------------------------------------------------------------------- */
+sq_status sq_l1bn_forward(const int8_t* xq, int64_t M, int64_t C, int64_t ld_x, const sq_scale* xscale,
+                          const float* gamma, const float* beta, float* y, int64_t ld_y,
+                          sq_l1bn_channel* chan, sq_l1bn_layer* layer,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * sq_l1bn_backward -- L1BNQ backward.
+ * The incoming gradient dy is quantized with ShiftQuant (as sq_quantize_grad
+ * with params p; codes qg, groups g_c, channel steps delta_c = step 2^-g_c);
+ * the L1 normalization is differentiated exactly (App. E.1 with
+ * sigma = mean |x - mu|, which brings in s = sgn(x - mu)), the quantizers of
+ * mu and sigma passed straight through:
+ *   dx = (gamma^q / sigma^q)(g - mean g - mean(g xhat)(s - mean s)).
+ * With integer sums G1 = sum qg, G2 = sum qg (q - m), P = sign_sum,
+ * rho = 127 M / (A_max k), lambda = gamma^q rho / s_x, in binary64:
+ *   dbeta = delta G1,  dgamma = (delta G2) rho,  D = dgamma / M,
+ *   a = lambda delta,  b = -(lambda D),  e = lambda (D P / M - delta G1 / M),
+ * each rounded once to fp32, and dx = fl(fl(fl(a qg) + fl(b sgn(q - m))) + e).
+ * With A_max = 0: dgamma = 0 and dx = 0.
+ * Inputs : dy [M, ld_dy] fp32; p (b, N_G, rounding of the gradient codes);
+ *          xq, ld_x, chan, layer: the forward's input codes and state.
+ * Outputs: dx [M, ld_dx] fp32; dgamma, dbeta [C] fp32; group [C] and gscale:
+ *          the gradient quantizer's groups and scale; dx_ranges (may be NULL):
+ *          [sq_l1bn_range_slabs, C] partial maxima of |dx| per channel, the
+ *          input of sq_quantize_grad_from_ranges for the layer below.
+ * Workspace: sq_l1bn_backward_workspace_size bytes.
+ * Errors: as sq_l1bn_forward.
+ * ------------------------------------------------------------------------- */
+sq_status sq_l1bn_backward(const float* dy, int64_t M, int64_t C, int64_t ld_dy, const sq_quant_params* p,
+                           const int8_t* xq, int64_t ld_x, const sq_l1bn_channel* chan,
+                           const sq_l1bn_layer* layer, float* dx, int64_t ld_dx,
+                           float* dgamma, float* dbeta, uint8_t* group, sq_scale* gscale,
+                           uint32_t* dx_ranges, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Static description of a status code. */
 const char* sq_status_string(sq_status s);
 

@@ -12,7 +12,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libshiftquant.so")
-SOURCES = ["sq_abi.hip", "sq_quant.hip", "sq_gemm.hip"]
+SOURCES = ["sq_abi.hip", "sq_quant.hip", "sq_gemm.hip", "sq_l1bn.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

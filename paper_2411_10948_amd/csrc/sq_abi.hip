@@ -567,6 +567,170 @@ sq_status sq_gemm_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, c
     return hip_status(launch_splitk_reduce(ws, splits, a, s), "splitk_reduce");
 }
 
+sq_status sq_quantize_grad_from_ranges(const float* dY, int64_t M, int64_t C_out, int64_t ld_dY,
+                                       const sq_quant_params* p, const uint32_t* ranges, int64_t range_slabs,
+                                       int8_t* q_fold, int64_t ld_fold, int8_t* q_t, int64_t ld_t, uint8_t* group,
+                                       sq_scale* scale, int32_t* layout, void* workspace, size_t workspace_bytes,
+                                       void* stream) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_dims(M, C_out, "dY"));
+    if (M > 0 && C_out > 0) SQ_TRY(check_f32(dY, ld_dY, C_out, "dY"));
+    if (C_out > 0 && (!ranges || !aligned(ranges, 4)))
+        return fail(SQ_ERR_INVALID_ARGUMENT, "ranges is NULL or misaligned");
+    if (C_out > 0 && (range_slabs < 1 || range_slabs >= kMaxRows))
+        return fail(SQ_ERR_INVALID_ARGUMENT, "range_slabs must be >= 1");
+    if (!scale || !aligned(scale, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "scale is NULL or misaligned");
+    if (!layout || !aligned(layout, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "layout is NULL or misaligned");
+    if (C_out > 0 && !group) return fail(SQ_ERR_INVALID_ARGUMENT, "group is NULL");
+    size_t lay_bytes = 0;
+    int64_t min_ld_fold = 0;
+    SQ_TRY(sq_grad_layout_size(C_out, p, &lay_bytes, &min_ld_fold));
+    if (q_fold && M > 0) SQ_TRY(check_codes(q_fold, ld_fold, min_ld_fold, "q_fold"));
+    if (q_t && C_out > 0) SQ_TRY(check_codes(q_t, ld_t, M > 0 ? M : 1, "q_t"));
+    if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
+    if (workspace_bytes < quant_ws_bytes(M, C_out)) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+
+    const QuantCfg cfg = make_cfg(*p);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    uint32_t* rbits = static_cast<uint32_t*>(workspace);
+    const int64_t ext_max = fold_ext_max(C_out, cfg);
+    if (C_out > 0)
+        SQ_TRY(hip_status(launch_finalize_grad(ranges, range_slabs, C_out, cfg, rbits, group, scale, layout, ext_max, s),
+                          "finalize"));
+    SQ_TRY(hip_status(launch_quantize(dY, M, C_out, ld_dY, group, scale, cfg, q_fold, ld_fold, q_t, ld_t,
+                                      layout + kLayoutHeader + ext_max, s),
+                      "quantize"));
+    return SQ_OK;
+}
+
+// ---------------------------------------------------------------------------
+// L1BNQ
+// ---------------------------------------------------------------------------
+static_assert(sizeof(sq_l1bn_channel) == 32, "sq_l1bn_channel layout");
+static_assert(sizeof(sq_l1bn_layer) == 56, "sq_l1bn_layer layout");
+
+namespace {
+
+constexpr int64_t kBnMaxRows = (int64_t)1 << 24;
+
+sq_status check_bn_dims(int64_t M, int64_t C) {
+    if (M < 1 || C < 0 || C >= kMaxChannels) return fail(SQ_ERR_INVALID_ARGUMENT, "L1BNQ needs M >= 1 and C >= 0");
+    if (M > kBnMaxRows) return fail(SQ_ERR_UNSUPPORTED, "L1BNQ supports at most 2^24 rows");
+    return SQ_OK;
+}
+
+size_t bn_fwd_ws_bytes(int64_t M, int64_t C) {
+    return (size_t)round_up(std::max<int64_t>(l1bn_part_words(M, C), 1) * 4, 256);
+}
+
+// backward scratch: quantizer scratch | fold layout | gradient codes [M, ldc]
+// | column-sum partials | per-channel constants [C, 4]
+struct BnBwdWs {
+    size_t quant, layout, codes, part, coef, total;
+    int64_t ldc;
+};
+
+BnBwdWs bn_bwd_ws(int64_t M, int64_t C, const QuantCfg& cfg) {
+    BnBwdWs w{};
+    w.ldc = round_up(std::max<int64_t>(C, 1), 16);
+    w.quant = 0;
+    w.layout = w.quant + quant_ws_bytes(M, C);
+    w.codes = w.layout + (size_t)round_up(fold_layout_words(C, cfg) * 4, 256);
+    w.part = w.codes + (size_t)round_up(M * w.ldc, 256);
+    w.coef = w.part + (size_t)round_up(std::max<int64_t>(l1bn_part_words(M, C), 1) * 4, 256);
+    w.total = w.coef + (size_t)round_up(std::max<int64_t>(C, 1) * 16, 256);
+    return w;
+}
+
+}  // namespace
+
+sq_status sq_l1bn_range_slabs(int64_t M, int64_t C, int64_t* slabs) {
+    if (!slabs) return fail(SQ_ERR_INVALID_ARGUMENT, "slabs is NULL");
+    SQ_TRY(check_bn_dims(M, C));
+    *slabs = l1bn_range_slabs(M, C);
+    return SQ_OK;
+}
+
+sq_status sq_l1bn_forward_workspace_size(int64_t M, int64_t C, size_t* bytes) {
+    if (!bytes) return fail(SQ_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    SQ_TRY(check_bn_dims(M, C));
+    *bytes = bn_fwd_ws_bytes(M, C);
+    return SQ_OK;
+}
+
+sq_status sq_l1bn_backward_workspace_size(int64_t M, int64_t C, const sq_quant_params* p, size_t* bytes) {
+    if (!bytes) return fail(SQ_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_bn_dims(M, C));
+    *bytes = bn_bwd_ws(M, C, make_cfg(*p)).total;
+    return SQ_OK;
+}
+
+sq_status sq_l1bn_forward(const int8_t* xq, int64_t M, int64_t C, int64_t ld_x, const sq_scale* xscale,
+                          const float* gamma, const float* beta, float* y, int64_t ld_y, sq_l1bn_channel* chan,
+                          sq_l1bn_layer* layer, void* workspace, size_t workspace_bytes, void* stream) {
+    SQ_TRY(check_bn_dims(M, C));
+    if (!xscale || !aligned(xscale, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "xscale is NULL or misaligned");
+    if (!layer || !aligned(layer, 8)) return fail(SQ_ERR_INVALID_ARGUMENT, "layer is NULL or misaligned");
+    if (C > 0) {
+        SQ_TRY(check_codes(xq, ld_x, C, "xq"));
+        SQ_TRY(check_f32(y, ld_y, C, "y"));
+        if (!gamma || !beta || !aligned(gamma, 4) || !aligned(beta, 4))
+            return fail(SQ_ERR_INVALID_ARGUMENT, "gamma / beta NULL or misaligned");
+        if (!chan || !aligned(chan, 8)) return fail(SQ_ERR_INVALID_ARGUMENT, "chan is NULL or misaligned");
+    }
+    if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
+    if (workspace_bytes < bn_fwd_ws_bytes(M, C)) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (C == 0) return SQ_OK;
+    return hip_status(launch_l1bn_forward(xq, M, C, ld_x, xscale, gamma, beta, y, ld_y, chan, layer,
+                                          static_cast<int32_t*>(workspace), s),
+                      "l1bn forward");
+}
+
+sq_status sq_l1bn_backward(const float* dy, int64_t M, int64_t C, int64_t ld_dy, const sq_quant_params* p,
+                           const int8_t* xq, int64_t ld_x, const sq_l1bn_channel* chan, const sq_l1bn_layer* layer,
+                           float* dx, int64_t ld_dx, float* dgamma, float* dbeta, uint8_t* group, sq_scale* gscale,
+                           uint32_t* dx_ranges, void* workspace, size_t workspace_bytes, void* stream) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_bn_dims(M, C));
+    if (!layer || !aligned(layer, 8)) return fail(SQ_ERR_INVALID_ARGUMENT, "layer is NULL or misaligned");
+    if (!gscale || !aligned(gscale, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "gscale is NULL or misaligned");
+    if (C > 0) {
+        SQ_TRY(check_f32(dy, ld_dy, C, "dy"));
+        SQ_TRY(check_codes(xq, ld_x, C, "xq"));
+        SQ_TRY(check_f32(dx, ld_dx, C, "dx"));
+        if (!dgamma || !dbeta || !aligned(dgamma, 4) || !aligned(dbeta, 4))
+            return fail(SQ_ERR_INVALID_ARGUMENT, "dgamma / dbeta NULL or misaligned");
+        if (!chan || !aligned(chan, 8)) return fail(SQ_ERR_INVALID_ARGUMENT, "chan is NULL or misaligned");
+        if (!group) return fail(SQ_ERR_INVALID_ARGUMENT, "group is NULL");
+        if (dx_ranges && !aligned(dx_ranges, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "dx_ranges is misaligned");
+    }
+    if (!workspace || !aligned(workspace, 256))
+        return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or not 256-byte aligned");
+    const QuantCfg cfg = make_cfg(*p);
+    const BnBwdWs w = bn_bwd_ws(M, C, cfg);
+    if (workspace_bytes < w.total) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (C == 0) return SQ_OK;
+    char* base = static_cast<char*>(workspace);
+    uint32_t* partial = reinterpret_cast<uint32_t*>(base + w.quant);
+    int32_t* lay = reinterpret_cast<int32_t*>(base + w.layout);
+    int8_t* codes = reinterpret_cast<int8_t*>(base + w.codes);
+    int64_t slabs = 0;
+    SQ_TRY(hip_status(launch_colmax(dy, M, C, ld_dy, partial, &slabs, s), "colmax"));
+    const int64_t ext_max = fold_ext_max(C, cfg);
+    SQ_TRY(hip_status(launch_finalize_grad(partial, slabs, C, cfg, partial + slabs * C, group, gscale, lay, ext_max, s),
+                      "finalize"));
+    // canonical codes (no fold descriptor: every channel in its own column, unshifted)
+    SQ_TRY(hip_status(launch_quantize(dy, M, C, ld_dy, group, gscale, cfg, codes, w.ldc, nullptr, 0, nullptr, s),
+                      "quantize"));
+    return hip_status(launch_l1bn_backward(codes, w.ldc, xq, ld_x, M, C, chan, layer, group, gscale, dx, ld_dx, dgamma,
+                                           dbeta, dx_ranges, reinterpret_cast<int32_t*>(base + w.part),
+                                           reinterpret_cast<float*>(base + w.coef), s),
+                      "l1bn backward");
+}
+
 sq_status sq_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_t ld_acc, int32_t kind,
                      const uint8_t* group, const sq_scale* gscale, const sq_scale* oscale, int32_t num_groups,
                      float* out, int64_t ld_out, void* stream) {

@@ -156,6 +156,21 @@ hipError_t launch_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_
                           int num_groups, float* out, int64_t ld_out, hipStream_t s);
 int wgrad_splits(int64_t M, int64_t C_out, int64_t C_in);
 
+// ---- L1BNQ (sq_l1bn.hip) ----
+// Partial-maximum slabs of the backward's dx ranges; int32 partial words of
+// the column sums.
+int64_t l1bn_range_slabs(int64_t M, int64_t C);
+int64_t l1bn_part_words(int64_t M, int64_t C);
+hipError_t launch_l1bn_forward(const int8_t* xq, int64_t M, int64_t C, int64_t ld_x, const sq_scale* xs,
+                               const float* gamma, const float* beta, float* y, int64_t ld_y, sq_l1bn_channel* ch,
+                               sq_l1bn_layer* layer, int32_t* part, hipStream_t s);
+// After the gradient codes qg [M, ldg] are formed: sums, constants
+// (coef [C, 4] scratch), dx and its ranges.
+hipError_t launch_l1bn_backward(const int8_t* qg, int64_t ldg, const int8_t* xq, int64_t ld_x, int64_t M, int64_t C,
+                                const sq_l1bn_channel* ch, const sq_l1bn_layer* layer, const uint8_t* group,
+                                const sq_scale* gscale, float* dx, int64_t ld_dx, float* dgamma, float* dbeta,
+                                uint32_t* ranges, int32_t* part, float* coef, hipStream_t s);
+
 // ---- device helpers ----
 // 2^k as a float, exact for -126 <= k <= 127 (from its bit pattern).
 __device__ __forceinline__ float pow2f(int k) { return __uint_as_float((uint32_t)(k + 127) << 23); }

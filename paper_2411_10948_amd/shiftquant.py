@@ -40,6 +40,8 @@ EXPORTS = (
     "sq_gemm_dgrad_grouped_workspace_size", "sq_quantize_channels_workspace_size",
     "sq_quantize_grad", "sq_quantize_tensor", "sq_gemm_dgrad", "sq_gemm_wgrad", "sq_conv_dgrad", "sq_dequant",
     "sq_gemm_dgrad_grouped", "sq_quantize_channels", "sq_gemm_forward",
+    "sq_quantize_grad_from_ranges", "sq_l1bn_range_slabs", "sq_l1bn_forward_workspace_size",
+    "sq_l1bn_backward_workspace_size", "sq_l1bn_forward", "sq_l1bn_backward",
     "sq_status_string", "sq_last_error",
 )
 
@@ -100,6 +102,14 @@ def load() -> ct.CDLL:
                                   _P, _SZ, _P],
         "sq_conv_dgrad": [_P, _I64, _P, _P, _P, _P, _I64, _P, _I64, _I64, _I64, _I64, _I64, ct.c_int32,
                           ct.c_int32, ct.c_int32, ct.c_int32, pp, _P, _I64, _P, _I64, _P, _SZ, _P],
+        "sq_quantize_grad_from_ranges": [_P, _I64, _I64, _I64, pp, _P, _I64, _P, _I64, _P, _I64, _P, _P, _P, _P,
+                                         _SZ, _P],
+        "sq_l1bn_range_slabs": [_I64, _I64, ct.POINTER(_I64)],
+        "sq_l1bn_forward_workspace_size": [_I64, _I64, ct.POINTER(_SZ)],
+        "sq_l1bn_backward_workspace_size": [_I64, _I64, pp, ct.POINTER(_SZ)],
+        "sq_l1bn_forward": [_P, _I64, _I64, _I64, _P, _P, _P, _P, _I64, _P, _P, _P, _SZ, _P],
+        "sq_l1bn_backward": [_P, _I64, _I64, _I64, pp, _P, _I64, _P, _P, _P, _I64, _P, _P, _P, _P, _P, _P, _SZ,
+                             _P],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -226,6 +236,51 @@ def sq_quantize_grad(dY, params, q_fold, q_t, group, scale, layout, workspace, s
     _check("sq_quantize_grad", load().sq_quantize_grad(
         _ptr(dY), M, C, _ld(dY), ct.byref(params), _ptr(q_fold), _ld(q_fold), _ptr(q_t), _ld(q_t),
         _ptr(group), _ptr(scale), _ptr(layout), ws, nws, _stream(stream)))
+
+
+def sq_quantize_grad_from_ranges(dY, params, ranges, range_slabs, q_fold, q_t, group, scale, layout, workspace,
+                                 stream=None) -> None:
+    M, C = dY.shape
+    ws, nws = _ws_ptr(workspace)
+    _check("sq_quantize_grad_from_ranges", load().sq_quantize_grad_from_ranges(
+        _ptr(dY), M, C, _ld(dY), ct.byref(params), _ptr(ranges), range_slabs, _ptr(q_fold), _ld(q_fold),
+        _ptr(q_t), _ld(q_t), _ptr(group), _ptr(scale), _ptr(layout), ws, nws, _stream(stream)))
+
+
+def sq_l1bn_range_slabs(M: int, C: int) -> int:
+    n = _I64(0)
+    _check("sq_l1bn_range_slabs", load().sq_l1bn_range_slabs(M, C, ct.byref(n)))
+    return n.value
+
+
+def sq_l1bn_forward_workspace_size(M: int, C: int) -> int:
+    nb = _SZ(0)
+    _check("sq_l1bn_forward_workspace_size", load().sq_l1bn_forward_workspace_size(M, C, ct.byref(nb)))
+    return nb.value
+
+
+def sq_l1bn_backward_workspace_size(M: int, C: int, params: Params) -> int:
+    nb = _SZ(0)
+    _check("sq_l1bn_backward_workspace_size",
+           load().sq_l1bn_backward_workspace_size(M, C, ct.byref(params), ct.byref(nb)))
+    return nb.value
+
+
+def sq_l1bn_forward(xq, xscale, gamma, beta, y, chan, layer, workspace, stream=None) -> None:
+    M, C = xq.shape
+    ws, nws = _ws_ptr(workspace)
+    _check("sq_l1bn_forward", load().sq_l1bn_forward(
+        _ptr(xq), M, C, _ld(xq), _ptr(xscale), _ptr(gamma), _ptr(beta), _ptr(y), _ld(y), _ptr(chan), _ptr(layer),
+        ws, nws, _stream(stream)))
+
+
+def sq_l1bn_backward(dy, params, xq, chan, layer, dx, dgamma, dbeta, group, gscale, dx_ranges, workspace,
+                     stream=None) -> None:
+    M, C = dy.shape
+    ws, nws = _ws_ptr(workspace)
+    _check("sq_l1bn_backward", load().sq_l1bn_backward(
+        _ptr(dy), M, C, _ld(dy), ct.byref(params), _ptr(xq), _ld(xq), _ptr(chan), _ptr(layer), _ptr(dx), _ld(dx),
+        _ptr(dgamma), _ptr(dbeta), _ptr(group), _ptr(gscale), _ptr(dx_ranges), ws, nws, _stream(stream)))
 
 
 def sq_quantize_tensor(T, bits, transpose, q, scale, workspace, stream=None) -> None:
@@ -429,6 +484,87 @@ def gemm_wgrad(codes: GradCodes, xq_t: torch.Tensor, xscale: torch.Tensor, want_
     sq_gemm_wgrad(codes.q_t, codes.group, codes.scale, xq_t, xscale, M, C_out, C_in, codes.params,
                   acc, dW, ws, stream)
     return acc, dW
+
+
+def quantize_grad_from_ranges(dY: torch.Tensor, ranges: torch.Tensor, bits: int, num_groups: int = 4,
+                              round_mode: int = ROUND_NEAREST_EVEN, seed: int = 0, offset: int = 0,
+                              stream=None) -> GradCodes:
+    """quantize_grad with the channel ranges given as partial maxima
+    ranges [slabs, C] (uint32 bit patterns, as int32) from the producer of dY."""
+    M, C = dY.shape
+    dev = dY.device
+    p = Params.make(bits, num_groups, round_mode, seed, offset)
+    lay_bytes, min_ld = sq_grad_layout_size(C, p)
+    q_fold = torch.zeros((max(M, 1), min_ld), dtype=torch.int8, device=dev)[:M]
+    q_t = torch.zeros((max(C, 1), round_up(max(M, 1), 16)), dtype=torch.int8, device=dev)[:C]
+    group = torch.empty(max(C, 1), dtype=torch.uint8, device=dev)[:C]
+    scale = new_scale(dev)
+    layout = torch.zeros(lay_bytes // 4, dtype=torch.int32, device=dev)
+    ws = _workspace(sq_quantize_grad_workspace_size(M, C, p), dev)
+    sq_quantize_grad_from_ranges(dY, p, ranges, ranges.shape[0], q_fold, q_t, group, scale, layout, ws, stream)
+    return GradCodes(q_fold, q_t, group, scale, layout, p, M, C)
+
+
+# sq_l1bn_channel (32 bytes) and sq_l1bn_layer (56 bytes) as int32 words
+L1BN_CHANNEL_WORDS = 8
+L1BN_LAYER_WORDS = 14
+
+
+def l1bn_channels_to_host(chan: torch.Tensor) -> dict:
+    w = chan.view(-1, L1BN_CHANNEL_WORDS).cpu()
+    return {"mu": w[:, 0].numpy().copy(), "sigma": w[:, 1].numpy().copy(), "sign_sum": w[:, 2].numpy().copy(),
+            "gamma_q": w[:, 3].view(torch.float32).numpy().copy(), "beta_q": w[:, 4].view(torch.float32).numpy().copy(),
+            "kappa": w[:, 5].view(torch.float32).numpy().copy(),
+            "dev_sum": w[:, 6:8].contiguous().view(torch.int64).reshape(-1).numpy().copy()}
+
+
+def l1bn_layer_to_host(layer: torch.Tensor) -> dict:
+    w = layer.cpu()
+    i64 = w[0:4].view(torch.int64)
+    return {"rows": int(i64[0]), "dev_max": int(i64[1]), "x_step": float(w[4:5].view(torch.float32)[0]),
+            "flags": int(w[5])}
+
+
+class L1BNState:
+    """Forward state of an L1BNQ layer (device tensors)."""
+
+    def __init__(self, chan, layer, xq, M, C):
+        self.chan, self.layer, self.xq, self.M, self.C = chan, layer, xq, M, C
+
+
+def l1bn_forward(xq: torch.Tensor, xscale: torch.Tensor, gamma: torch.Tensor, beta: torch.Tensor,
+                 stream=None):
+    """L1BNQ forward of 8-bit codes xq [M, C] (ld a multiple of 16):
+    returns (y [M, C] fp32, L1BNState)."""
+    M, C = xq.shape
+    dev = xq.device
+    y = torch.empty((M, C), dtype=torch.float32, device=dev)
+    chan = torch.zeros(max(C, 1) * L1BN_CHANNEL_WORDS, dtype=torch.int32, device=dev)
+    layer = torch.zeros(16, dtype=torch.int32, device=dev)
+    ws = _workspace(sq_l1bn_forward_workspace_size(M, C), dev)
+    sq_l1bn_forward(xq, xscale, gamma, beta, y, chan, layer, ws, stream)
+    return y, L1BNState(chan, layer, xq, M, C)
+
+
+def l1bn_backward(dy: torch.Tensor, state: L1BNState, bits: int = 8, num_groups: int = 4,
+                  round_mode: int = ROUND_NEAREST_EVEN, seed: int = 0, offset: int = 0, want_ranges: bool = False,
+                  stream=None) -> dict:
+    """L1BNQ backward: dx, dgamma, dbeta, the gradient quantizer's group and
+    scale, and (want_ranges) the partial maxima of |dx| per channel."""
+    M, C = dy.shape
+    dev = dy.device
+    p = Params.make(bits, num_groups, round_mode, seed, offset)
+    dx = torch.empty((M, C), dtype=torch.float32, device=dev)
+    dgamma = torch.empty(max(C, 1), dtype=torch.float32, device=dev)[:C]
+    dbeta = torch.empty(max(C, 1), dtype=torch.float32, device=dev)[:C]
+    group = torch.empty(max(C, 1), dtype=torch.uint8, device=dev)[:C]
+    gscale = new_scale(dev)
+    ranges = None
+    if want_ranges:
+        ranges = torch.empty((sq_l1bn_range_slabs(M, C), max(C, 1)), dtype=torch.int32, device=dev)[:, :C]
+    ws = _workspace(sq_l1bn_backward_workspace_size(M, C, p), dev)
+    sq_l1bn_backward(dy, p, state.xq, state.chan, state.layer, dx, dgamma, dbeta, group, gscale, ranges, ws, stream)
+    return {"dx": dx, "dgamma": dgamma, "dbeta": dbeta, "group": group, "gscale": gscale, "ranges": ranges}
 
 
 class BackwardPlan:

@@ -155,3 +155,42 @@ def test_python_binding_has_no_fallback(sq, monkeypatch, tmp_path):
     monkeypatch.setattr(sq, "_lib", None)
     with pytest.raises(ImportError):
         sq.load()
+
+
+def test_l1bn_validation_no_launch(sq):
+    L = _raw(sq)
+    fake = ct.c_void_p(0x100000)
+    n = ct.c_int64(0)
+    nb = ct.c_size_t(0)
+    p = sq.Params.make(8, 4, 0)
+    # M must be in [1, 2^24]
+    assert L.sq_l1bn_range_slabs(0, 64, ct.byref(n)) == 1
+    assert L.sq_l1bn_range_slabs((1 << 24) + 1, 64, ct.byref(n)) == 3
+    assert L.sq_l1bn_range_slabs(200704, 64, ct.byref(n)) == 0 and 1 <= n.value <= 1024
+    assert L.sq_l1bn_forward_workspace_size(100, 64, ct.byref(nb)) == 0 and nb.value > 0
+    assert L.sq_l1bn_backward_workspace_size(100, 64, ct.byref(p), ct.byref(nb)) == 0 and nb.value >= 100 * 64
+    # forward: ld of the codes not a multiple of 16, NULL gamma, small workspace
+    assert L.sq_l1bn_forward(fake, 8, 8, 8, fake, fake, fake, fake, 8, fake, fake, fake, 4096, None) == 1
+    assert L.sq_l1bn_forward(fake, 8, 8, 16, fake, None, fake, fake, 8, fake, fake, fake, 4096, None) == 1
+    assert L.sq_l1bn_forward(fake, 8, 8, 16, fake, fake, fake, fake, 8, fake, fake, fake, 16, None) == 4
+    # backward: bad params, misaligned ranges, workspace not 256-byte aligned
+    bad = sq.Params.make(9, 4, 0)
+    assert L.sq_l1bn_backward(fake, 8, 8, 8, ct.byref(bad), fake, 16, fake, fake, fake, 8, fake, fake, fake,
+                              fake, None, fake, 1 << 20, None) == 1
+    assert L.sq_l1bn_backward(fake, 8, 8, 8, ct.byref(p), fake, 16, fake, fake, fake, 8, fake, fake, fake,
+                              fake, ct.c_void_p(0x100002), fake, 1 << 20, None) == 1
+    assert L.sq_l1bn_backward(fake, 8, 8, 8, ct.byref(p), fake, 16, fake, fake, fake, 8, fake, fake, fake,
+                              fake, None, ct.c_void_p(0x100010), 1 << 20, None) == 1
+
+
+def test_quantize_from_ranges_validation_no_launch(sq):
+    L = _raw(sq)
+    fake = ct.c_void_p(0x100000)
+    p = sq.Params.make(4, 4, 0)
+    # NULL ranges, zero slabs
+    assert L.sq_quantize_grad_from_ranges(fake, 8, 8, 8, ct.byref(p), None, 1, fake, 16, fake, 16, fake, fake,
+                                          fake, fake, 4096, None) == 1
+    assert L.sq_quantize_grad_from_ranges(fake, 8, 8, 8, ct.byref(p), fake, 0, fake, 16, fake, 16, fake, fake,
+                                          fake, fake, 4096, None) == 1
+    assert L.sq_quantize_grad_from_ranges(fake, 8, 8, 8, ct.byref(p), fake, 1, fake, 16, fake, 16, fake, fake,
+                                          fake, fake, 16, None) == 4
