@@ -176,6 +176,107 @@ def run_forward(args, torch, sq, wl, inputs):
     return 0
 
 
+def run_l1bn(args, torch, sq):
+    """Fully-quantized L1 batch normalization (Sec. 4), one training step of
+    the layer: the conv output X quantized to 8 bits per tensor, the L1BNQ
+    forward, and the L1BNQ backward (ShiftQuant of dy, dx, dgamma, dbeta and
+    the channel ranges of dx for the quantizer of the layer below).  HBM-bound:
+    the figure of merit is algorithmic GB/s (X read 4 B, y written 4 B, dy read
+    4 B, codes read 1 B, dx written 4 B per element)."""
+    from paper_2411_10948_amd import workloads
+    name = args.workload if args.workload in workloads.BN_WORKLOADS else "resnet18_bn_56x56x64"
+    w = workloads.BN_WORKLOADS[name]
+    inp = workloads.make_bn_inputs(name)
+    M, C = w.M, w.C
+    bits = args.bits or 8
+    ng = args.num_groups or 4
+    mode = int(args.rounding == "sr")
+    print(f"[bench] {name}: M={M} C={C} gradient b={bits} N_G={ng} round={'SR' if mode else 'RTN'}",
+          file=sys.stderr, flush=True)
+    dev = torch.device("cuda:0")
+    X = torch.from_numpy(inp["X"]).to(dev)
+    gamma = torch.from_numpy(inp["gamma"]).to(dev)
+    beta = torch.from_numpy(inp["beta"]).to(dev)
+    dy = torch.from_numpy(inp["dy"]).to(dev)
+    p = sq.Params.make(bits, ng, mode, 0, 0)
+    ldx = sq.round_up(C, 16)
+    xq = torch.zeros((M, ldx), dtype=torch.int8, device=dev)[:, :C]
+    xs = sq.new_scale(dev)
+    ws_x = torch.empty(max(sq.sq_quantize_tensor_workspace_size(M, C), 256), dtype=torch.uint8, device=dev)
+    y = torch.empty((M, C), dtype=torch.float32, device=dev)
+    chan = torch.zeros(C * sq.L1BN_CHANNEL_WORDS, dtype=torch.int32, device=dev)
+    layer = torch.zeros(16, dtype=torch.int32, device=dev)
+    ws_f = torch.empty(max(sq.sq_l1bn_forward_workspace_size(M, C), 256), dtype=torch.uint8, device=dev)
+    dx = torch.empty((M, C), dtype=torch.float32, device=dev)
+    dgamma = torch.empty(C, dtype=torch.float32, device=dev)
+    dbeta = torch.empty(C, dtype=torch.float32, device=dev)
+    group = torch.empty(C, dtype=torch.uint8, device=dev)
+    gscale = sq.new_scale(dev)
+    ranges = torch.empty((sq.sq_l1bn_range_slabs(M, C), C), dtype=torch.int32, device=dev)
+    ws_b = torch.empty(sq.sq_l1bn_backward_workspace_size(M, C, p), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def quant():
+        sq.sq_quantize_tensor(X, 8, False, xq, xs, ws_x, stream)
+
+    def fwd():
+        sq.sq_l1bn_forward(xq, xs, gamma, beta, y, chan, layer, ws_f, stream)
+
+    def bwd():
+        sq.sq_l1bn_backward(dy, p, xq, chan, layer, dx, dgamma, dbeta, group, gscale, ranges, ws_b, stream)
+
+    def step():
+        quant()
+        fwd()
+        bwd()
+
+    def timed(fn, K):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(K):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / K
+
+    for _ in range(args.warmup):
+        step()
+    ms_step = timed(step, args.steps)
+    parts = {"sq_quantize_tensor(X)": {"ms": timed(quant, args.steps), "bytes": 5 * M * C},
+             "sq_l1bn_forward": {"ms": timed(fwd, args.steps), "bytes": 5 * M * C},
+             "sq_l1bn_backward": {"ms": timed(bwd, args.steps), "bytes": 9 * M * C}}
+    total_bytes = 17 * M * C
+    dom = max(parts, key=lambda k: parts[k]["ms"])
+    d = parts[dom]
+    roof = {"bound": "hbm", "achieved": d["bytes"] / (d["ms"] * 1e-3) / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    roof.update({"frac": roof["achieved"] / roof["peak"], "traffic": None, "kernel": dom,
+                 "algorithmic_bytes": d["bytes"], "algorithmic_ops": 0, "avg_ms": d["ms"]})
+    value = total_bytes / (ms_step * 1e-3) / 1e9
+    out = {"metric": "L1BNQ training step (quantize X + forward + backward) algorithmic GB/s",
+           "value": value, "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": "int8", "data": "synthetic",
+           "config": {"workload": name, "step": "l1bn", "M": M, "C": C, "input_bits": 8, "grad_bits": bits,
+                      "num_groups": ng, "rounding": "stochastic" if mode else "nearest-even", "parallelism": "none"},
+           "pct_hbm_peak": 100.0 * value / PEAK_HBM_GBS,
+           "breakdown_ms": {k: v["ms"] for k, v in parts.items()}, "roofline": roof}
+    if not args.no_cpu_baseline:
+        import oracle
+        rows = min(M, 1 << 18)
+        Xh, dyh = inp["X"][:rows], inp["dy"][:rows]
+        t0 = time.perf_counter()
+        xq_o, xs_o = oracle.quantize_tensor(Xh, 8)
+        f = oracle.l1bn_forward(xq_o, xs_o["d0"], inp["gamma"], inp["beta"])
+        oracle.l1bn_backward(dyh, f, xq_o, bits, ng, mode)
+        t = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": 17 * rows * C / t / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+                               "sample": f"oracle quantize X + L1BNQ forward + backward on the first {rows} of {M} "
+                                         f"rows ({t:.2f} s, 1 thread)"}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -187,8 +288,10 @@ def main(argv=None):
     ap.add_argument("--num-groups", type=int, default=None, help="override the workload's N_G (variant runs)")
     ap.add_argument("--rounding", choices=["rtn", "sr"], default=None,
                     help="override the workload's rounding (variant runs)")
-    ap.add_argument("--step", choices=["backward", "forward"], default="backward",
-                    help="forward: quantize X with ShiftQuant + Y = X W^T (per-output-channel W)")
+    ap.add_argument("--step", choices=["backward", "forward", "l1bn"], default="backward",
+                    help="forward: quantize X with ShiftQuant + Y = X W^T (per-output-channel W); "
+                         "l1bn: the L1BNQ layer (workloads resnet18_bn_56x56x64, resnet50_bn_14x14x1024, "
+                         "transformer_bn_768)")
     ap.add_argument("--dgrad", choices=["shiftmm", "grouped"], default="shiftmm",
                     help="grouped: the GEMM-based comparison implementation of the dgrad (Sec. 3.2)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -208,6 +311,8 @@ def main(argv=None):
         build.build()
     sq.load()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.step == "l1bn":
+        return run_l1bn(args, torch, sq)
     conv = args.workload in FUSED_CONV
     wl = workloads.WORKLOADS[FUSED_CONV.get(args.workload, args.workload)]
     # parameter variants of the same layer (same tensors, other b / N_G / rounding)

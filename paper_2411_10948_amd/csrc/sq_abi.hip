@@ -635,7 +635,9 @@ BnBwdWs bn_bwd_ws(int64_t M, int64_t C, const QuantCfg& cfg) {
     w.ldc = round_up(std::max<int64_t>(C, 1), 16);
     w.quant = 0;
     w.layout = w.quant + quant_ws_bytes(M, C);
-    w.codes = w.layout + (size_t)round_up(fold_layout_words(C, cfg) * 4, 256);
+    // groups and scales only: the finalize runs without a fold plan (one
+    // window, descriptors for C channels)
+    w.codes = w.layout + (size_t)round_up((kLayoutHeader + C) * 4, 256);
     w.part = w.codes + (size_t)round_up(M * w.ldc, 256);
     w.coef = w.part + (size_t)round_up(std::max<int64_t>(l1bn_part_words(M, C), 1) * 4, 256);
     w.total = w.coef + (size_t)round_up(std::max<int64_t>(C, 1) * 16, 256);
@@ -719,8 +721,9 @@ sq_status sq_l1bn_backward(const float* dy, int64_t M, int64_t C, int64_t ld_dy,
     int8_t* codes = reinterpret_cast<int8_t*>(base + w.codes);
     int64_t slabs = 0;
     SQ_TRY(hip_status(launch_colmax(dy, M, C, ld_dy, partial, &slabs, s), "colmax"));
-    const int64_t ext_max = fold_ext_max(C, cfg);
-    SQ_TRY(hip_status(launch_finalize_grad(partial, slabs, C, cfg, partial + slabs * C, group, gscale, lay, ext_max, s),
+    // the groups and the scale do not depend on the fold (only the dgrad
+    // operand does), so the finalize skips the fold plan: ext_max = 0
+    SQ_TRY(hip_status(launch_finalize_grad(partial, slabs, C, cfg, partial + slabs * C, group, gscale, lay, 0, s),
                       "finalize"));
     // canonical codes (no fold descriptor: every channel in its own column, unshifted)
     SQ_TRY(hip_status(launch_quantize(dy, M, C, ld_dy, group, gscale, cfg, codes, w.ldc, nullptr, 0, nullptr, s),

@@ -35,7 +35,7 @@ namespace {
 
 constexpr int kBnThreads = 256;
 constexpr int kBnChunk = 16;                 // channels per thread (one 16-byte load)
-constexpr int kBnWaves = 16;                 // channels per reduction block (a wave each)
+constexpr int kBnWaves = 16;                 // waves of a channel-reduction block
 
 struct BnGeom {
     int64_t chunks;   // ceil(C / 16)
@@ -62,7 +62,6 @@ constexpr int64_t kSumBlocks = 512, kSumMinRows = 64;
 constexpr int64_t kApplyBlocks = 1024, kApplyMinRows = 64;
 
 BnGeom sum_geom(int64_t M, int64_t C) { return bn_geom(M, C, kSumBlocks, kSumMinRows); }
-BnGeom apply_geom(int64_t M, int64_t C) { return bn_geom(M, C, kApplyBlocks, kApplyMinRows); }
 
 __device__ __forceinline__ void unpack16(const int4 v, int (&out)[16]) {
     const uint32_t w[4] = {(uint32_t)v.x, (uint32_t)v.y, (uint32_t)v.z, (uint32_t)v.w};
@@ -94,13 +93,26 @@ __device__ __forceinline__ void block_colsum(int32_t* red, const int32_t (&acc)[
         for (int i = 0; i < 16; ++i) red[lane * width + cl * kBnChunk + i] = acc[i];
     }
     __syncthreads();
+    // every thread adds a strided subset of the lanes of one channel; the
+    // subsets' sums go through LDS once more (width <= 256 channels here:
+    // wider block columns have one lane, nothing to add)
     const int64_t cbase = (int64_t)blockIdx.y * width;
-    for (int k = threadIdx.x; k < width; k += kBnThreads) {
-        const int64_t c = cbase + k;
-        if (c >= C) continue;
+    if (g.lanes == 1) {
+        for (int k = threadIdx.x; k < width; k += kBnThreads)
+            if (cbase + k < C) part[(int64_t)blockIdx.x * C + cbase + k] = red[k];
+        return;
+    }
+    const int J = kBnThreads / width, k = threadIdx.x % width, j = threadIdx.x / width;
+    int32_t sub = 0;
+    if (j < J)
+        for (int l = j; l < g.lanes; l += J) sub += red[l * width + k];
+    __syncthreads();
+    if (j < J) red[j * width + k] = sub;
+    __syncthreads();
+    if (threadIdx.x < width && cbase + threadIdx.x < C) {
         int32_t s = 0;
-        for (int l = 0; l < g.lanes; ++l) s += red[l * width + k];
-        part[(int64_t)blockIdx.x * C + c] = s;
+        for (int i = 0; i < J; ++i) s += red[i * width + threadIdx.x];
+        part[(int64_t)blockIdx.x * C + cbase + threadIdx.x] = s;
     }
 }
 
@@ -123,7 +135,8 @@ __global__ __launch_bounds__(kBnThreads) void k_bn_colsum(const int8_t* __restri
     for (int i = 0; i < 16; ++i) {
         s0[i] = 0;
         s1[i] = 0;
-        mu[i] = (OP >= 1 && active && c0 + i < C) ? ch[c0 + i].mu : 0;
+        // clamped index, select after the load (no branch per channel)
+        mu[i] = OP >= 1 ? ch[std::min<int64_t>(c0 + i, C - 1)].mu : 0;
     }
     if (active) {
         constexpr int U = 4;   // rows in flight per thread
@@ -179,13 +192,10 @@ __global__ __launch_bounds__(kBnThreads) void k_bn_colsum(const int8_t* __restri
     if (OP >= 1) block_colsum(red, s1, active, lane, cl, g, C, part + g.nb * C);
 }
 
-__device__ __forceinline__ int64_t wave_sum64(int64_t v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
-}
-
-// Per-channel totals of the block partials, one wave per channel.
+// Per-channel totals of the block partials: a block of 16 waves takes 64
+// consecutive channels (one per lane, so every load is a coalesced 256-byte
+// row segment of the partials), the waves split the partial rows, and LDS
+// adds the 16 wave sums.
 //   OP 0: mean code.  OP 1: deviation and sign sums.
 //   OP 2: backward constants (a, b, e), dgamma, dbeta.
 template <int OP>
@@ -196,17 +206,38 @@ __global__ __launch_bounds__(64 * kBnWaves) void k_bn_chan(const int32_t* __rest
                                                            const sq_scale* __restrict__ gscale,
                                                            float* __restrict__ coef, float* __restrict__ dgamma,
                                                            float* __restrict__ dbeta) {
-    const int lane = threadIdx.x & 63;
-    const int64_t c = (int64_t)blockIdx.x * kBnWaves + (threadIdx.x >> 6);
-    if (c >= C) return;
+    __shared__ int64_t sh0[kBnWaves][64], sh1[kBnWaves][64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int64_t c = (int64_t)blockIdx.x * 64 + lane;
+    const int64_t cc = std::min<int64_t>(c, C - 1);
+    constexpr int U = 8;
     int64_t t0 = 0, t1 = 0;
-    for (int64_t b = lane; b < nb; b += 64) {
-        t0 += part[b * C + c];
-        if (OP >= 1) t1 += part[(nb + b) * C + c];
+    for (int64_t b0 = w; b0 < nb; b0 += (int64_t)kBnWaves * U) {
+        int32_t v0[U], v1[U];
+        // clamped row, select after the load: the loads issue back to back
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t b = std::min<int64_t>(b0 + (int64_t)kBnWaves * u, nb - 1);
+            v0[u] = part[b * C + cc];
+            v1[u] = OP >= 1 ? part[(nb + b) * C + cc] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const bool in = b0 + (int64_t)kBnWaves * u < nb;
+            t0 += in ? v0[u] : 0;
+            t1 += in ? v1[u] : 0;
+        }
     }
-    t0 = wave_sum64(t0);
-    if (OP >= 1) t1 = wave_sum64(t1);
-    if (lane != 0) return;
+    sh0[w][lane] = t0;
+    sh1[w][lane] = t1;
+    __syncthreads();
+    if (w != 0 || c >= C) return;
+    t0 = t1 = 0;
+#pragma unroll
+    for (int i = 0; i < kBnWaves; ++i) {
+        t0 += sh0[i][lane];
+        t1 += sh1[i][lane];
+    }
     if (OP == 0) {
         sq_l1bn_channel v{};
         v.mu = (int32_t)div_round_even(t0, M);
@@ -215,7 +246,7 @@ __global__ __launch_bounds__(64 * kBnWaves) void k_bn_chan(const int32_t* __rest
         ch[c].dev_sum = t0;
         ch[c].sign_sum = (int32_t)t1;
     } else {
-        const sq_l1bn_channel cc = ch[c];
+        const sq_l1bn_channel cv = ch[c];
         const sq_l1bn_layer L = *layer;
         const double delta = (double)__fmul_rn(gscale->step, pow2f(-(int)group[c]));
         const double db = delta * (double)t0;
@@ -224,21 +255,18 @@ __global__ __launch_bounds__(64 * kBnWaves) void k_bn_chan(const int32_t* __rest
         if (L.dev_max == 0) {
             dgamma[c] = 0.0f;
         } else {
-            const double rho = (127.0 * (double)M) / ((double)L.dev_max * (double)cc.sigma);
-            const double lambda = ((double)cc.gamma * rho) / (double)L.x_step;
+            const double rho = (127.0 * (double)M) / ((double)L.dev_max * (double)cv.sigma);
+            const double lambda = ((double)cv.gamma * rho) / (double)L.x_step;
             const double dg = (delta * (double)t1) * rho;
             const double D = dg / (double)M;
             const double gbar = db / (double)M;
-            const double sbar = (double)cc.sign_sum / (double)M;
+            const double sbar = (double)cv.sign_sum / (double)M;
             dgamma[c] = (float)dg;
             ca = (float)(lambda * delta);
             cb = (float)(-(lambda * D));
             ce = (float)(lambda * (D * sbar - gbar));
         }
-        coef[4 * c + 0] = ca;
-        coef[4 * c + 1] = cb;
-        coef[4 * c + 2] = ce;
-        coef[4 * c + 3] = 0.0f;
+        reinterpret_cast<float4*>(coef)[c] = make_float4(ca, cb, ce, 0.0f);
     }
 }
 
@@ -334,73 +362,115 @@ __global__ __launch_bounds__(kParThreads) void k_bn_params(sq_l1bn_channel* __re
 // a = input codes.  Backward: dx = fl(fl(fl(a qg) + fl(b sgn(q - m))) + e),
 // a = gradient codes, x = input codes; with `ranges`, each block also writes
 // the channel maxima of |dx| over its rows (bit patterns) to ranges[block, c].
+// A thread owns one channel quad of a row (a 4-byte code load, one float4
+// store), so a wave's loads and stores cover contiguous row segments.
+struct QuadGeom {
+    int64_t quads;    // ceil(C / 4)
+    int qis;          // quads per block column (<= 256)
+    int lanes;        // rows in flight per block
+    int64_t slabs, nb, rpb;
+};
+
+QuadGeom quad_geom(int64_t M, int64_t C) {
+    QuadGeom g{};
+    g.quads = (C + 3) / 4;
+    g.qis = (int)std::min<int64_t>(g.quads, kBnThreads);
+    g.lanes = kBnThreads / g.qis;
+    g.slabs = (g.quads + g.qis - 1) / g.qis;
+    g.nb = std::max<int64_t>(1, std::min<int64_t>(kApplyBlocks, (M + kApplyMinRows - 1) / kApplyMinRows));
+    g.rpb = (M + g.nb - 1) / g.nb;
+    g.nb = (M + g.rpb - 1) / g.rpb;
+    return g;
+}
+
+__device__ __forceinline__ void unpack4(uint32_t w, int (&out)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) out[i] = (int)(int8_t)(w >> (8 * i));
+}
+
 template <bool BWD>
 __global__ __launch_bounds__(kBnThreads) void k_bn_apply(const int8_t* __restrict__ a, int64_t lda,
                                                          const int8_t* __restrict__ x, int64_t ldx,
                                                          const sq_l1bn_channel* __restrict__ ch,
                                                          const float* __restrict__ coef, int64_t M, int64_t C,
-                                                         BnGeom g, float* __restrict__ out, int64_t ld_out,
+                                                         QuadGeom g, float* __restrict__ out, int64_t ld_out,
                                                          bool vec_out, uint32_t* __restrict__ ranges) {
-    __shared__ uint32_t red[BWD ? kBnThreads * kBnChunk : 1];
-    const int tid = threadIdx.x, cl = tid % g.cis, lane = tid / g.cis;
-    const int64_t chunk = (int64_t)blockIdx.y * g.cis + cl, c0 = chunk * kBnChunk;
-    const bool active = lane < g.lanes && chunk < g.chunks;
+    __shared__ uint32_t red[BWD ? kBnThreads * 4 : 1];
+    const int tid = threadIdx.x, cl = tid % g.qis, lane = tid / g.qis;
+    const int64_t quad = (int64_t)blockIdx.y * g.qis + cl, c0 = quad * 4;
+    const bool active = lane < g.lanes && quad < g.quads;
     const int64_t r0 = (int64_t)blockIdx.x * g.rpb, r1 = std::min<int64_t>(M, r0 + g.rpb);
-    const bool full = c0 + kBnChunk <= C && vec_out;
-    int mu[16];
-    float k0[16], k1[16], k2[16];
-    uint32_t rmax[16];
+    const bool full = c0 + 4 <= C && vec_out;
+    int mu[4];
+    float k0[4], k1[4], k2[4];
+    uint32_t rmax[4];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-        const bool ok = active && c0 + i < C;
-        mu[i] = ok ? ch[c0 + i].mu : 0;
+    for (int i = 0; i < 4; ++i) {
+        // clamped index, select after the load (no branch per channel)
+        const int64_t cc = std::min<int64_t>(c0 + i, C - 1);
+        const bool ok = c0 + i < C;
+        const sq_l1bn_channel v = ch[cc];
+        mu[i] = v.mu;
         if (BWD) {
-            k0[i] = ok ? coef[4 * (c0 + i) + 0] : 0.0f;
-            k1[i] = ok ? coef[4 * (c0 + i) + 1] : 0.0f;
-            k2[i] = ok ? coef[4 * (c0 + i) + 2] : 0.0f;
+            const float4 k = reinterpret_cast<const float4*>(coef)[cc];
+            k0[i] = ok ? k.x : 0.0f;
+            k1[i] = ok ? k.y : 0.0f;
+            k2[i] = ok ? k.z : 0.0f;
         } else {
-            k0[i] = ok ? ch[c0 + i].kappa : 0.0f;
-            k1[i] = ok ? ch[c0 + i].beta : 0.0f;
+            k0[i] = ok ? v.kappa : 0.0f;
+            k1[i] = ok ? v.beta : 0.0f;
             k2[i] = 0.0f;
         }
         rmax[i] = 0u;
     }
-    if (active) {
-        for (int64_t m = r0 + lane; m < r1; m += g.lanes) {
-            int qa[16], qx[16];
-            unpack16(*reinterpret_cast<const int4*>(a + m * lda + c0), qa);
-            if (BWD) unpack16(*reinterpret_cast<const int4*>(x + m * ldx + c0), qx);
-            float v[16];
+    auto row_out = [&](int64_t m, uint32_t wa, uint32_t wx) {
+        int qa[4], qx[4];
+        unpack4(wa, qa);
+        if (BWD) unpack4(wx, qx);
+        float v[4];
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                if (BWD) {
-                    const float s = (float)sgn(qx[i] - mu[i]);
-                    v[i] = __fadd_rn(__fadd_rn(__fmul_rn(k0[i], (float)qa[i]), __fmul_rn(k1[i], s)), k2[i]);
-                    rmax[i] = std::max(rmax[i], abs_bits(v[i]));
-                } else {
-                    v[i] = __fadd_rn(__fmul_rn(k0[i], (float)(qa[i] - mu[i])), k1[i]);
-                }
-            }
-            float* row = out + m * ld_out + c0;
-            if (full) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    reinterpret_cast<float4*>(row)[j] = make_float4(v[4 * j], v[4 * j + 1], v[4 * j + 2], v[4 * j + 3]);
+        for (int i = 0; i < 4; ++i) {
+            if (BWD) {
+                const float s = (float)sgn(qx[i] - mu[i]);
+                v[i] = __fadd_rn(__fadd_rn(__fmul_rn(k0[i], (float)qa[i]), __fmul_rn(k1[i], s)), k2[i]);
+                if (c0 + i < C) rmax[i] = std::max(rmax[i], abs_bits(v[i]));
             } else {
-#pragma unroll
-                for (int i = 0; i < 16; ++i)
-                    if (c0 + i < C) row[i] = v[i];
+                v[i] = __fadd_rn(__fmul_rn(k0[i], (float)(qa[i] - mu[i])), k1[i]);
             }
         }
+        float* row = out + m * ld_out + c0;
+        if (full) {
+            *reinterpret_cast<float4*>(row) = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (c0 + i < C) row[i] = v[i];
+        }
+    };
+    if (active) {
+        constexpr int U = 8;   // rows in flight per thread
+        int64_t m = r0 + lane;
+        for (; m + (U - 1) * (int64_t)g.lanes < r1; m += U * (int64_t)g.lanes) {
+            uint32_t wa[U], wx[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t mm = m + u * (int64_t)g.lanes;
+                wa[u] = *reinterpret_cast<const uint32_t*>(a + mm * lda + c0);
+                wx[u] = BWD ? *reinterpret_cast<const uint32_t*>(x + mm * ldx + c0) : 0u;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) row_out(m + u * (int64_t)g.lanes, wa[u], wx[u]);
+        }
+        for (; m < r1; m += g.lanes)
+            row_out(m, *reinterpret_cast<const uint32_t*>(a + m * lda + c0),
+                    BWD ? *reinterpret_cast<const uint32_t*>(x + m * ldx + c0) : 0u);
     }
     if (BWD && ranges) {
-        // bytes past C in the last chunk carry codes of no channel: their
-        // maxima are computed and never stored
-        const int width = g.cis * kBnChunk;
+        const int width = g.qis * 4;
         __syncthreads();
         if (active) {
 #pragma unroll
-            for (int i = 0; i < 16; ++i) red[lane * width + cl * kBnChunk + i] = rmax[i];
+            for (int i = 0; i < 4; ++i) red[lane * width + cl * 4 + i] = rmax[i];
         }
         __syncthreads();
         const int64_t cbase = (int64_t)blockIdx.y * width;
@@ -416,7 +486,7 @@ __global__ __launch_bounds__(kBnThreads) void k_bn_apply(const int8_t* __restric
 
 }  // namespace
 
-int64_t l1bn_range_slabs(int64_t M, int64_t C) { return M > 0 && C > 0 ? apply_geom(M, C).nb : 0; }
+int64_t l1bn_range_slabs(int64_t M, int64_t C) { return M > 0 && C > 0 ? quad_geom(M, C).nb : 0; }
 
 int64_t l1bn_part_words(int64_t M, int64_t C) { return 2 * sum_geom(M, C).nb * C; }
 
@@ -424,8 +494,9 @@ hipError_t launch_l1bn_forward(const int8_t* xq, int64_t M, int64_t C, int64_t l
                                const float* gamma, const float* beta, float* y, int64_t ld_y, sq_l1bn_channel* ch,
                                sq_l1bn_layer* layer, int32_t* part, hipStream_t s) {
     if (C <= 0) return hipSuccess;
-    const BnGeom gs = sum_geom(M, C), ga = apply_geom(M, C);
-    const dim3 sum_grid((unsigned)gs.nb, (unsigned)gs.slabs), chan_grid((unsigned)((C + kBnWaves - 1) / kBnWaves));
+    const BnGeom gs = sum_geom(M, C);
+    const QuadGeom ga = quad_geom(M, C);
+    const dim3 sum_grid((unsigned)gs.nb, (unsigned)gs.slabs), chan_grid((unsigned)((C + 63) / 64));
     hipLaunchKernelGGL(k_bn_colsum<0>, sum_grid, dim3(kBnThreads), 0, s, xq, ld_x, nullptr, 0, ch, M, C, gs, part);
     hipLaunchKernelGGL(k_bn_chan<0>, chan_grid, dim3(64 * kBnWaves), 0, s, part, gs.nb, M, C, ch, nullptr, nullptr,
                        nullptr, nullptr, nullptr, nullptr);
@@ -444,10 +515,11 @@ hipError_t launch_l1bn_backward(const int8_t* qg, int64_t ldg, const int8_t* xq,
                                 const sq_scale* gscale, float* dx, int64_t ld_dx, float* dgamma, float* dbeta,
                                 uint32_t* ranges, int32_t* part, float* coef, hipStream_t s) {
     if (C <= 0) return hipSuccess;
-    const BnGeom gs = sum_geom(M, C), ga = apply_geom(M, C);
+    const BnGeom gs = sum_geom(M, C);
+    const QuadGeom ga = quad_geom(M, C);
     hipLaunchKernelGGL(k_bn_colsum<2>, dim3((unsigned)gs.nb, (unsigned)gs.slabs), dim3(kBnThreads), 0, s, qg, ldg, xq,
                        ld_x, ch, M, C, gs, part);
-    hipLaunchKernelGGL(k_bn_chan<2>, dim3((unsigned)((C + kBnWaves - 1) / kBnWaves)), dim3(64 * kBnWaves), 0, s, part,
+    hipLaunchKernelGGL(k_bn_chan<2>, dim3((unsigned)((C + 63) / 64)), dim3(64 * kBnWaves), 0, s, part,
                        gs.nb, M, C, const_cast<sq_l1bn_channel*>(ch), layer, group, gscale, coef, dgamma, dbeta);
     const bool vec = (ld_dx % 4 == 0) && (reinterpret_cast<uintptr_t>(dx) % 16 == 0);
     hipLaunchKernelGGL(k_bn_apply<true>, dim3((unsigned)ga.nb, (unsigned)ga.slabs), dim3(kBnThreads), 0, s, qg, ldg,

@@ -162,3 +162,47 @@ def make_inputs(name: str, *, M: Optional[int] = None, seed: int = 0) -> dict:
     rw = _rng(seed, wl.index, TID_W)
     W = (rw.standard_normal(size=(wl.C_out, wl.C_in)) * wl.w_std).astype(np.float32)
     return {"dY": dY, "X": X, "W": W, "workload": wl, "M": M}
+
+
+# ---------------------------------------------------------------------------
+# L1BNQ layers (Sec. 4: 8-bit fully-quantized L1 batch normalization in the
+# ResNets and the Transformer of Sec. 5.1).  The layer's input is a conv (or
+# linear) output, so X is signed: z * sigma_c + mean_c with z ~ N(0, 1),
+# sigma_c ~ LogNormal(0, 0.5), mean_c ~ N(0, 0.5); gamma ~ N(1, 0.2),
+# beta ~ N(0, 0.2); the incoming gradient dy follows make_grad with
+# LogNormal(0, 1) channel scales and its default outlier channels.  Tensor ids continue after those above:
+# 5 = X, 6 = gamma / beta, 7 = dy base (via make_grad's ids with index + 100).
+# ---------------------------------------------------------------------------
+TID_BN_X, TID_BN_PARAM = 5, 6
+
+
+@dataclasses.dataclass(frozen=True)
+class BNWorkload:
+    name: str
+    index: int
+    M: int          # N * H * W rows
+    C: int          # channels
+    description: str
+
+
+BN_WORKLOADS = {w.name: w for w in [
+    BNWorkload("resnet18_bn_56x56x64", 10, 64 * 56 * 56, 64,
+               "ResNet-18 stage-1 batch norm, N=64, 56x56, 64 channels"),
+    BNWorkload("resnet50_bn_14x14x1024", 11, 64 * 14 * 14, 1024,
+               "ResNet-50 stage-3 batch norm, N=64, 14x14, 1024 channels"),
+    BNWorkload("transformer_bn_768", 12, 16384, 768,
+               "Transformer batch norm over 16384 tokens of width 768"),
+]}
+
+
+def make_bn_inputs(name: str, *, seed: int = 0) -> dict:
+    w = BN_WORKLOADS[name]
+    rx = _rng(seed, w.index, TID_BN_X)
+    sig = rx.lognormal(0.0, 0.5, w.C)
+    mean = rx.normal(0.0, 0.5, w.C)
+    X = (rx.standard_normal((w.M, w.C)) * sig + mean).astype(np.float32)
+    rp = _rng(seed, w.index, TID_BN_PARAM)
+    gamma = rp.normal(1.0, 0.2, w.C).astype(np.float32)
+    beta = rp.normal(0.0, 0.2, w.C).astype(np.float32)
+    dy = make_grad(w.M, w.C, seed=seed, index=w.index + 100, dist="normal", sigma_s=1.0)
+    return {"X": X, "gamma": gamma, "beta": beta, "dy": dy, "M": w.M, "C": w.C}
