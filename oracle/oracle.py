@@ -84,6 +84,8 @@ def _bind(L):
     L.sqo_dequant_dgrad.restype = None
     L.sqo_dequant_wgrad.argtypes = [P, i64, i64, P, ct.c_float, ct.c_float, P]
     L.sqo_dequant_wgrad.restype = None
+    L.sqo_conv_wgrad.argtypes = [P, i64, i64, i64, i64, P, i64, ct.c_int, ct.c_int, ct.c_int, ct.c_int, P]
+    L.sqo_conv_wgrad.restype = ct.c_int
     L.sqo_l1bn_forward.argtypes = [P, i64, i64, ct.c_float, P, P, P, P, P, P, P, P, P, P, P]
     L.sqo_l1bn_forward.restype = ct.c_int
     L.sqo_l1bn_backward.argtypes = [P, P, ct.c_float, i64, i64, P, ct.c_float, P, P, P, P, i64, P, P, P]
@@ -236,6 +238,21 @@ def conv_dgrad(q: np.ndarray, g: np.ndarray, num_groups: int, wq: np.ndarray, N:
         raise RangeError("conv dgrad accumulator leaves int32")
     assert rc == 0, rc
     return A
+
+
+def conv_wgrad(q: np.ndarray, xq: np.ndarray, N: int, H: int, W: int, KH: int, KW: int, PH: int,
+               PW: int) -> np.ndarray:
+    """Weight gradient of a stride-1 conv: B [C_out, KH*KW*C_in] int32 from
+    gradient codes q [N*Ho*Wo, C_out] and input codes xq [N*H*W, C_in]."""
+    q = _c(q, np.int8)
+    xq = _c(xq, np.int8)
+    C_out, C_in = q.shape[1], xq.shape[1]
+    B = np.zeros((C_out, KH * KW * C_in), np.int32)
+    rc = lib().sqo_conv_wgrad(_p(q), N, H, W, C_out, _p(xq), C_in, KH, KW, PH, PW, _p(B))
+    if rc == 2:
+        raise RangeError("conv wgrad accumulator leaves int32")
+    assert rc == 0, rc
+    return B
 
 
 def wgrad(q: np.ndarray, xq: np.ndarray, rows=None) -> np.ndarray:

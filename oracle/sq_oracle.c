@@ -574,3 +574,44 @@ int sqo_l1bn_backward(const int8_t* qg, const uint8_t* grp, float d0, int64_t M,
     }
     return SQO_OK;
 }
+
+/* ---------------------------------------------------------------------------
+ * Weight gradient of a stride-1 convolution (R14), written from the
+ * definition: with the forward conv Y[n, oh, ow, co] =
+ * sum_{r, s, ci} X[n, oh + r - PH, ow + s - PW, ci] W[co, r, s, ci] (zero
+ * outside the input), the gradient of <dY, Y> with respect to W is
+ *   B[co, (r KW + s) C_in + ci] = sum_{n, oh, ow} q[n, oh, ow, co] x[n, oh + r - PH, ow + s - PW, ci],
+ * i.e. the wgrad of the im2col'd layer (Fig. "MMs", third GEMM) without the
+ * im2col.  q [N Ho Wo, C_out] gradient codes, x [N H W, C_in] input codes,
+ * int64 accumulation, int32 result [C_out, KH KW C_in].
+ * ------------------------------------------------------------------------- */
+int sqo_conv_wgrad(const int8_t* q, int64_t N, int64_t H, int64_t W, int64_t C_out, const int8_t* x,
+                   int64_t C_in, int KH, int KW, int PH, int PW, int32_t* B)
+{
+    if (!q || !x || !B || N < 0 || H < 1 || W < 1 || C_out < 0 || C_in < 0 || KH < 1 || KW < 1 || PH < 0 ||
+        PW < 0)
+        return SQO_ERR_ARG;
+    int64_t Ho = H + 2 * (int64_t)PH - KH + 1, Wo = W + 2 * (int64_t)PW - KW + 1;
+    if (Ho < 1 || Wo < 1) return SQO_ERR_ARG;
+    int64_t cols = (int64_t)KH * KW * C_in;
+    for (int64_t co = 0; co < C_out; ++co)
+        for (int r = 0; r < KH; ++r)
+            for (int s = 0; s < KW; ++s)
+                for (int64_t ci = 0; ci < C_in; ++ci) {
+                    int64_t acc = 0;
+                    for (int64_t n = 0; n < N; ++n)
+                        for (int64_t oh = 0; oh < Ho; ++oh) {
+                            int64_t ih = oh + r - PH;
+                            if (ih < 0 || ih >= H) continue;
+                            for (int64_t ow = 0; ow < Wo; ++ow) {
+                                int64_t iw = ow + s - PW;
+                                if (iw < 0 || iw >= W) continue;
+                                acc += (int64_t)q[((n * Ho + oh) * Wo + ow) * C_out + co] *
+                                       (int64_t)x[((n * H + ih) * W + iw) * C_in + ci];
+                            }
+                        }
+                    if (acc > INT32_MAX || acc < INT32_MIN) return SQO_ERR_RANGE;
+                    B[co * cols + ((int64_t)r * KW + s) * C_in + ci] = (int32_t)acc;
+                }
+    return SQO_OK;
+}

@@ -69,6 +69,11 @@ MUTATIONS = [
     ("L1BN lambda step", "const double lambda = ((double)gamma_q[c] * rho) / (double)x_step;",
      "const double lambda = ((double)gamma_q[c] * rho) * (double)x_step;"),
     ("L1BN sign of deviation", "float s = (float)((d > 0) - (d < 0));", "float s = (float)((d < 0) - (d > 0));"),
+    ("conv wgrad input row of a tap", "int64_t ih = oh + r - PH;", "int64_t ih = oh - r + PH;"),
+    ("conv wgrad tap order", "B[co * cols + ((int64_t)r * KW + s) * C_in + ci] = (int32_t)acc;",
+     "B[co * cols + ((int64_t)s * KH + r) * C_in + ci] = (int32_t)acc;"),
+    ("conv wgrad last column dropped", "if (iw < 0 || iw >= W) continue;\n                                acc",
+     "if (iw < 0 || iw >= W - 1) continue;\n                                acc"),
 ]
 
 
@@ -111,6 +116,9 @@ def _pin_calls():
         calls.append(lambda a=axis: pins.test_quantize_channels_is_per_tensor_per_channel(a, 8))
     calls.append(pins.test_quantize_channels_degenerate_channels)
     calls.append(lambda: pins.test_forward_equals_dequantized_product(4, 4))
+    for case in pins.CONV_CASES[:4]:
+        calls.append(lambda c=case: pins.test_conv_wgrad_is_adjoint_of_forward_conv(c))
+    calls.append(pins.test_conv_wgrad_equals_wgrad_of_im2col)
     calls.append(pins.test_l1bn_forward_matches_textbook_when_statistics_are_exact)
     calls.append(pins.test_l1bn_forward_statistics_bounds_random)
     calls.append(lambda: pins.test_l1bn_backward_matches_autograd_when_statistics_are_exact(8, 4, 0))

@@ -776,3 +776,45 @@ def test_l1bn_constant_channels():
     # one row: every channel constant as well
     f1 = oracle.l1bn_forward(q[:1], 0.1, gamma, beta)
     assert f1["dev_max"] == 0
+
+
+def _im2col_codes(x, N, H, W, C_in, KH, KW, PH, PW):
+    """Explicit im2col of NHWC codes: row (n, oh, ow), columns (r, s, ci)."""
+    Ho, Wo = H + 2 * PH - KH + 1, W + 2 * PW - KW + 1
+    x4 = x.reshape(N, H, W, C_in)
+    xp = np.zeros((N, H + 2 * PH, W + 2 * PW, C_in), x.dtype)
+    xp[:, PH:PH + H, PW:PW + W, :] = x4
+    cols = [xp[:, r:r + Ho, s:s + Wo, :] for r in range(KH) for s in range(KW)]
+    return np.concatenate(cols, axis=3).reshape(N * Ho * Wo, KH * KW * C_in)
+
+
+@pytest.mark.parametrize("case", CONV_CASES, ids=[str(c) for c in CONV_CASES])
+def test_conv_wgrad_is_adjoint_of_forward_conv(case):
+    # <dW, V> = <dY, conv(X; V)> for every weight V: with V running over the
+    # unit weights, each entry of dW is the forward conv's response to it
+    N, H, W, C_out, C_in, KH, KW, PH, PW = case
+    rng = np.random.default_rng(sum(case) + 7)
+    Ho, Wo = H + 2 * PH - KH + 1, W + 2 * PW - KW + 1
+    q = rng.integers(-7, 8, (N * Ho * Wo, C_out)).astype(np.int8)
+    x = rng.integers(-127, 128, (N * H * W, C_in)).astype(np.int8)
+    B = oracle.conv_wgrad(q, x, N, H, W, KH, KW, PH, PW)
+    assert B.shape == (C_out, KH * KW * C_in)
+    xf = x.astype(np.int64).reshape(-1)
+    qf = q.astype(np.int64).reshape(-1)
+    for k in range(C_out * KH * KW * C_in):
+        V = np.zeros((C_out, KH * KW * C_in), np.int64)
+        V.reshape(-1)[k] = 1
+        J = _forward_conv_jacobian(V, N, H, W, C_out, C_in, KH, KW, PH, PW)
+        assert int(qf @ (J @ xf)) == int(B.reshape(-1)[k])
+
+
+def test_conv_wgrad_equals_wgrad_of_im2col():
+    # the implicit form equals the pinned wgrad of the explicitly im2col'd layer
+    for case in [(2, 7, 6, 5, 3, 3, 3, 1, 1), (1, 9, 8, 4, 6, 3, 3, 1, 1), (3, 5, 5, 2, 4, 1, 1, 0, 0)]:
+        N, H, W, C_out, C_in, KH, KW, PH, PW = case
+        rng = np.random.default_rng(sum(case))
+        Ho, Wo = H + 2 * PH - KH + 1, W + 2 * PW - KW + 1
+        q = rng.integers(-31, 32, (N * Ho * Wo, C_out)).astype(np.int8)
+        x = rng.integers(-127, 128, (N * H * W, C_in)).astype(np.int8)
+        cols = _im2col_codes(x, N, H, W, C_in, KH, KW, PH, PW)
+        np.testing.assert_array_equal(oracle.conv_wgrad(q, x, N, H, W, KH, KW, PH, PW), oracle.wgrad(q, cols))
