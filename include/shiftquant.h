@@ -361,6 +361,55 @@ sq_status sq_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_t ld_
                      int32_t num_groups, float* out, int64_t ld_out, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * Implicit-im2col weight gradient of a stride-1 convolution.
+ *
+ * The wgrad of the im2col'd conv layer (Fig. "MMs", third GEMM, on the conv
+ * layers of Sec. 5), computed without the im2col:
+ *   acc[co, (r KW + s) C_in + ci] = sum_{n, oh, ow} code(n, oh, ow, co)
+ *                                   xq(n, oh + r - PH, ow + s - PW, ci)
+ * (zero outside the input), with the epilogue of sq_gemm_wgrad
+ * (dW[co, :] = fl(float(acc[co, :]) * beta_co)).  Columns follow the (r, s, ci)
+ * order of W [C_out, KH KW C_in].
+ *
+ * Both operands live on a zero-padded pixel grid of Hp = H + 2 PH rows and
+ * Wp = roundup(W + 2 PW, 16) columns per image, where tap (r, s) is the
+ * constant shift r Wp + s of the pixel index.  The input codes are packed
+ * once per step (in training they come from the forward pass):
+ *   sq_conv_input_layout   -> rows (KW C_in) and ld of the packed input xs
+ *   sq_conv_pack_input     xq_t [C_in, ld_xq >= N H W] (sq_quantize_tensor,
+ *                          transpose 1) -> xs [rows, ld]: row s C_in + ci holds
+ *                          the padded grid of channel ci shifted by s; every
+ *                          byte of xs is written (zeros in the padding).
+ * sq_conv_wgrad takes the gradient codes q_t [C_out, ld_t >= N Ho Wo]
+ * (sq_quantize_grad's transposed codes), places them on the same grid in the
+ * workspace and runs one int8 GEMM whose B rows are the packed input at the
+ * taps' row offsets.
+ * Inputs : q_t, group, gscale as for sq_gemm_wgrad; xs, ld_xs from the pack
+ *          call; xscale the input codes' scale; stride 1, 0 <= PH < KH,
+ *          0 <= PW < KW, KH, KW <= 16.
+ * Outputs: acc [C_out, ld_acc] int32 and/or dW [C_out, ld_dW] fp32, each row
+ *          KH KW C_in wide.
+ * Workspace: sq_conv_wgrad_workspace_size bytes, 256-byte aligned.
+ * Errors: SQ_ERR_INVALID_ARGUMENT; SQ_ERR_OVERFLOW_RISK when
+ *         N Ho Wo Q 128 >= 2^31; SQ_ERR_UNSUPPORTED when a padded grid
+ *         exceeds 2^31 bytes; SQ_ERR_WORKSPACE_TOO_SMALL; SQ_ERR_HIP.
+ * ------------------------------------------------------------------------- */
+sq_status sq_conv_input_layout(int64_t N, int64_t H, int64_t W, int64_t C_in, int32_t KH, int32_t KW,
+                               int32_t PH, int32_t PW, int64_t* rows, int64_t* ld);
+sq_status sq_conv_pack_input(const int8_t* xq_t, int64_t ld_xq, int64_t N, int64_t H, int64_t W, int64_t C_in,
+                             int32_t KH, int32_t KW, int32_t PH, int32_t PW, int8_t* xs, int64_t ld_xs,
+                             void* stream);
+sq_status sq_conv_wgrad_workspace_size(int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t C_in,
+                                       int32_t KH, int32_t KW, int32_t PH, int32_t PW,
+                                       const sq_quant_params* p, size_t* bytes);
+sq_status sq_conv_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, const sq_scale* gscale,
+                        const int8_t* xs, int64_t ld_xs, const sq_scale* xscale,
+                        int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t C_in,
+                        int32_t KH, int32_t KW, int32_t PH, int32_t PW, const sq_quant_params* p,
+                        int32_t* acc, int64_t ld_acc, float* dW, int64_t ld_dW,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * sq_quantize_grad_from_ranges -- sq_quantize_grad with the channel ranges
  * supplied by the producer of dY.
  *

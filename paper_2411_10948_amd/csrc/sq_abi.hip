@@ -567,6 +567,140 @@ sq_status sq_gemm_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, c
     return hip_status(launch_splitk_reduce(ws, splits, a, s), "splitk_reduce");
 }
 
+// ---------------------------------------------------------------------------
+// Implicit-im2col conv wgrad
+// ---------------------------------------------------------------------------
+namespace {
+
+struct ConvGrid {
+    int64_t Ho, Wo, Hp, Wp, K, ld_q, rows_x, ld_x;
+};
+
+// padded pixel grid: Hp = H + 2 PH rows, Wp = roundup(W + 2 PW, 16) columns
+// per image; K = roundup(N Hp Wp, 64); the input copies extend (KH - 1) Wp
+// past K for the row shifts of the taps
+ConvGrid conv_grid(int64_t N, int64_t H, int64_t W, int64_t C_in, int KH, int KW, int PH, int PW) {
+    ConvGrid g{};
+    g.Ho = H + 2 * (int64_t)PH - KH + 1;
+    g.Wo = W + 2 * (int64_t)PW - KW + 1;
+    g.Hp = H + 2 * (int64_t)PH;
+    g.Wp = round_up(W + 2 * (int64_t)PW, 16);
+    g.K = round_up(std::max<int64_t>(N * g.Hp * g.Wp, 1), 64);
+    g.ld_q = g.K;
+    g.rows_x = (int64_t)KW * C_in;
+    g.ld_x = round_up(g.K + (int64_t)(KH - 1) * g.Wp, 16);
+    return g;
+}
+
+sq_status check_conv_geom(int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t C_in, int32_t KH, int32_t KW,
+                          int32_t PH, int32_t PW) {
+    if (N < 1 || H < 1 || W < 1 || C_out < 0 || C_in < 0 || KH < 1 || KW < 1 || PH < 0 || PW < 0 || KH > 16 ||
+        KW > 16 || PH >= KH || PW >= KW)
+        return fail(SQ_ERR_INVALID_ARGUMENT, "conv geometry out of range");
+    if (H + 2 * (int64_t)PH - KH + 1 < 1 || W + 2 * (int64_t)PW - KW + 1 < 1)
+        return fail(SQ_ERR_INVALID_ARGUMENT, "the window is larger than the padded input");
+    const ConvGrid g = conv_grid(N, H, W, C_in, KH, KW, PH, PW);
+    if (g.rows_x * g.ld_x >= ((int64_t)1 << 31) || std::max<int64_t>(C_out, 1) * g.ld_q >= ((int64_t)1 << 31))
+        return fail(SQ_ERR_UNSUPPORTED, "the padded code grids exceed 2^31 bytes");
+    return SQ_OK;
+}
+
+}  // namespace
+
+sq_status sq_conv_input_layout(int64_t N, int64_t H, int64_t W, int64_t C_in, int32_t KH, int32_t KW, int32_t PH,
+                               int32_t PW, int64_t* rows, int64_t* ld) {
+    if (!rows || !ld) return fail(SQ_ERR_INVALID_ARGUMENT, "rows / ld NULL");
+    SQ_TRY(check_conv_geom(N, H, W, 1, C_in, KH, KW, PH, PW));
+    const ConvGrid g = conv_grid(N, H, W, C_in, KH, KW, PH, PW);
+    *rows = g.rows_x;
+    *ld = g.ld_x;
+    return SQ_OK;
+}
+
+sq_status sq_conv_pack_input(const int8_t* xq_t, int64_t ld_xq, int64_t N, int64_t H, int64_t W, int64_t C_in,
+                             int32_t KH, int32_t KW, int32_t PH, int32_t PW, int8_t* xs, int64_t ld_xs,
+                             void* stream) {
+    SQ_TRY(check_conv_geom(N, H, W, 1, C_in, KH, KW, PH, PW));
+    const ConvGrid g = conv_grid(N, H, W, C_in, KH, KW, PH, PW);
+    if (C_in == 0) return SQ_OK;
+    SQ_TRY(check_codes(xq_t, ld_xq, N * H * W, "xq_t"));
+    SQ_TRY(check_codes(xs, ld_xs, g.ld_x, "xs"));
+    return hip_status(launch_grid_scatter(xq_t, ld_xq, C_in, KW, N, H, W, PH, PW, g.Hp, g.Wp, xs, ld_xs,
+                                          static_cast<hipStream_t>(stream)),
+                      "conv pack input");
+}
+
+sq_status sq_conv_wgrad_workspace_size(int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t C_in, int32_t KH,
+                                       int32_t KW, int32_t PH, int32_t PW, const sq_quant_params* p, size_t* bytes) {
+    if (!bytes) return fail(SQ_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_conv_geom(N, H, W, C_out, C_in, KH, KW, PH, PW));
+    const ConvGrid g = conv_grid(N, H, W, C_in, KH, KW, PH, PW);
+    const int64_t Ng = (int64_t)KH * KW * C_in;
+    const int splits = (C_out > 0 && Ng > 0) ? wgrad_splits(g.K, C_out, Ng) : 1;
+    size_t need = (size_t)round_up(std::max<int64_t>(C_out, 1) * g.ld_q, 256);
+    if (splits > 1) need += (size_t)splits * C_out * Ng * 4;
+    *bytes = need;
+    return SQ_OK;
+}
+
+sq_status sq_conv_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, const sq_scale* gscale,
+                        const int8_t* xs, int64_t ld_xs, const sq_scale* xscale, int64_t N, int64_t H, int64_t W,
+                        int64_t C_out, int64_t C_in, int32_t KH, int32_t KW, int32_t PH, int32_t PW,
+                        const sq_quant_params* p, int32_t* acc, int64_t ld_acc, float* dW, int64_t ld_dW,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_conv_geom(N, H, W, C_out, C_in, KH, KW, PH, PW));
+    if (!acc && !dW) return fail(SQ_ERR_INVALID_ARGUMENT, "acc and dW are both NULL");
+    if (!gscale || !xscale) return fail(SQ_ERR_INVALID_ARGUMENT, "a scale is NULL");
+    const QuantCfg cfg = make_cfg(*p);
+    const ConvGrid g = conv_grid(N, H, W, C_in, KH, KW, PH, PW);
+    const int64_t M = N * g.Ho * g.Wo, Ng = (int64_t)KH * KW * C_in;
+    if ((double)M * cfg.Q * 128.0 >= 2147483648.0)
+        return fail(SQ_ERR_OVERFLOW_RISK, "N Ho Wo * Q * 128 reaches 2^31: the int32 accumulator could overflow");
+    if (C_out == 0 || C_in == 0) return SQ_OK;
+    if (!group) return fail(SQ_ERR_INVALID_ARGUMENT, "group is NULL");
+    SQ_TRY(check_codes(q_t, ld_t, M, "q_t"));
+    SQ_TRY(check_codes(xs, ld_xs, g.ld_x, "xs"));
+    if (ld_xs != g.ld_x) return fail(SQ_ERR_INVALID_ARGUMENT, "ld_xs must be the one sq_conv_input_layout returns");
+    if (acc) SQ_TRY(check_f32(acc, ld_acc, Ng, "acc"));
+    if (dW) SQ_TRY(check_f32(dW, ld_dW, Ng, "dW"));
+    size_t need = 0;
+    SQ_TRY(sq_conv_wgrad_workspace_size(N, H, W, C_out, C_in, KH, KW, PH, PW, p, &need));
+    if (!workspace || !aligned(workspace, 256))
+        return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or not 256-byte aligned");
+    if (workspace_bytes < need) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // gradient codes onto the padded grid: output pixel (n, oh, ow) at
+    // n Hp Wp + oh Wp + ow, zeros elsewhere
+    int8_t* qp = static_cast<int8_t*>(workspace);
+    SQ_TRY(hip_status(launch_grid_scatter(q_t, ld_t, C_out, 1, N, g.Ho, g.Wo, 0, 0, g.Hp, g.Wp, qp, g.ld_q, s),
+                      "conv pack gradient"));
+    const int splits = wgrad_splits(g.K, C_out, Ng);
+    GemmArgs a{};
+    a.Mg = C_out; a.Ng = Ng;
+    a.A = qp; a.lda = g.ld_q;
+    a.B = xs; a.ldb = ld_xs;
+    a.K = g.K;
+    a.gs = gscale; a.os = xscale; a.group = group; a.num_groups = cfg.num_groups;
+    a.epi_mode = 1;
+    a.wg_KH = KH; a.wg_KW = KW; a.wg_Cin = C_in; a.wg_Wp = g.Wp;
+    if (splits <= 1) {
+        a.splits = 1;
+        a.acc = acc; a.ld_acc = ld_acc;
+        a.out = dW; a.ld_out = ld_dW;
+        return hip_status(launch_gemm(a, s), "conv wgrad");
+    }
+    int32_t* part = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + round_up(C_out * g.ld_q, 256));
+    GemmArgs gp = a;
+    gp.splits = splits;
+    gp.part = part;
+    SQ_TRY(hip_status(launch_gemm(gp, s), "conv wgrad"));
+    a.acc = acc; a.ld_acc = ld_acc;
+    a.out = dW; a.ld_out = ld_dW;
+    return hip_status(launch_splitk_reduce(part, splits, a, s), "splitk_reduce");
+}
+
 sq_status sq_quantize_grad_from_ranges(const float* dY, int64_t M, int64_t C_out, int64_t ld_dY,
                                        const sq_quant_params* p, const uint32_t* ranges, int64_t range_slabs,
                                        int8_t* q_fold, int64_t ld_fold, int8_t* q_t, int64_t ld_t, uint8_t* group,

@@ -484,7 +484,8 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
         return __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(base), (short)0, (int)min(rows * ld, (int64_t)0x7FFFFFFF),
                                                  kRsrcFlags);
     };
-    const __amdgpu_buffer_rsrc_t rA = rsrc(p.A, CONV ? p.a_rows : p.Mg, p.lda), rB = rsrc(p.B, p.Ng, p.ldb);
+    const __amdgpu_buffer_rsrc_t rA = rsrc(p.A, CONV ? p.a_rows : p.Mg, p.lda),
+                                 rB = rsrc(p.B, p.wg_KH ? p.wg_KW * p.wg_Cin : p.Ng, p.ldb);
     auto lane_off = [&](int i, int64_t first, int64_t rows, int64_t ld) {
         const int r = (i * T::kWaves + wv) * 16 + lr;
         return (uint32_t)(min(first + r, rows - 1) * ld + 16 * ((lane & 3) ^ swz(r)));
@@ -494,6 +495,17 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
     for (int i = 0; i < T::IA; ++i) offA[i] = lane_off(i, m0, p.Mg, p.lda);
 #pragma unroll
     for (int i = 0; i < T::IB; ++i) offB[i] = lane_off(i, n0, p.Ng, p.ldb);
+    if (p.wg_KH) {
+        // implicit-im2col conv wgrad: B row (tap, ci) is row s C_in + ci of
+        // the shifted input copies, r Wp bytes into its K range
+#pragma unroll
+        for (int i = 0; i < T::IB; ++i) {
+            const int r = (i * T::kWaves + wv) * 16 + lr;
+            const int64_t j = min(n0 + r, p.Ng - 1), tap = j / p.wg_Cin, ci = j - tap * p.wg_Cin;
+            const int64_t tr = tap / p.wg_KW, ts = tap - tr * p.wg_KW;
+            offB[i] = (uint32_t)((ts * p.wg_Cin + ci) * p.ldb + tr * p.wg_Wp + 16 * ((lane & 3) ^ swz(r)));
+        }
+    }
 
     // Convolution: the input pixel (n, ih, iw) of each of this lane's A rows;
     // tap (r, s) reads output pixel (n, ih + PH - r, iw + PW - s) of q_fold,
@@ -1268,6 +1280,10 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     if (a.Mg <= 0 || a.Ng <= 0) return hipSuccess;
     const bool pipe = pipe_ok(a);
     if (a.kseg && (!pipe || a.splits > 1 || a.layout)) return hipErrorInvalidValue;   // pipelined kernel only
+    if (a.wg_KH && (!pipe || a.extA || a.layout || a.kseg || a.wg_Cin <= 0 || a.wg_KW <= 0 || a.wg_Wp % 16 != 0 ||
+                    a.Ng != (int64_t)a.wg_KH * a.wg_KW * a.wg_Cin ||
+                    (int64_t)a.wg_KW * a.wg_Cin * a.ldb >= ((int64_t)1 << 31)))
+        return hipErrorInvalidValue;   // implicit-im2col wgrad: pipelined kernel, offsets in 31 bits
     const Pick p = pick(a);
     const int64_t ktiles = (a.K + 63) / 64;   // every configuration has 64-byte K tiles
     const int splits = std::max(1, a.splits);
@@ -1282,6 +1298,50 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     if (p == Pick::kSkinny) return launch_pipe<PipeSkinny, false>(a, splits, per * 64, s);
     return a.extA ? launch_pipe<PipeSmall, true>(a, splits, per * 64, s)
                   : launch_pipe<PipeSmall, false>(a, splits, per * 64, s);
+}
+
+// Padded pixel grids of the implicit-im2col conv wgrad: each thread writes
+// 16 consecutive bytes of an output row (one 16-byte store), reading the
+// pixels they map to one byte at a time.
+__global__ __launch_bounds__(256) void k_grid_scatter(const int8_t* __restrict__ in, int64_t ld_in, int64_t C,
+                                                      int64_t N, int64_t Hc, int64_t Wc, int64_t top, int64_t left,
+                                                      int64_t Hp, int64_t Wp, int8_t* __restrict__ out,
+                                                      int64_t ld_out, int64_t rows) {
+    const int64_t chunks = ld_out / 16, img = Hp * Wp;
+    for (int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; id < rows * chunks;
+         id += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t j = id / chunks, P0 = (id - j * chunks) * 16;
+        const int64_t sh = j / C, c = j - sh * C;
+        const int8_t* src = in + c * ld_in;
+        int64_t Q = P0 + sh;
+        int64_t n = Q / img, rem = Q - n * img, hp = rem / Wp, wp = rem - hp * Wp;
+        uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int64_t h = hp - top, x = wp - left;
+            if (n < N && h >= 0 && h < Hc && x >= 0 && x < Wc)
+                w[e >> 2] |= (uint32_t)(uint8_t)src[(n * Hc + h) * Wc + x] << (8 * (e & 3));
+            if (++wp == Wp) {
+                wp = 0;
+                if (++hp == Hp) {
+                    hp = 0;
+                    ++n;
+                }
+            }
+        }
+        *reinterpret_cast<uint4*>(out + j * ld_out + P0) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+}
+
+hipError_t launch_grid_scatter(const int8_t* in, int64_t ld_in, int64_t C, int copies, int64_t N, int64_t Hc,
+                               int64_t Wc, int64_t top, int64_t left, int64_t Hp, int64_t Wp, int8_t* out,
+                               int64_t ld_out, hipStream_t s) {
+    const int64_t rows = C * copies, work = rows * (ld_out / 16);
+    if (work <= 0) return hipSuccess;
+    const dim3 grid((unsigned)std::min<int64_t>((work + 255) / 256, 8192));
+    hipLaunchKernelGGL(k_grid_scatter, grid, dim3(256), 0, s, in, ld_in, C, N, Hc, Wc, top, left, Hp, Wp, out, ld_out,
+                       rows);
+    return hipGetLastError();
 }
 
 // B operand of the conv dgrad: bc[ci, t * 64 + e] for K tile t = f * taps + tau

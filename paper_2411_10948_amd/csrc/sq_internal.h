@@ -126,6 +126,12 @@ struct GemmArgs {
     // device {first K column, K columns} replacing [0, K) (the per-group
     // GEMMs of the GEMM-based comparison), may be null
     const int32_t* kseg;
+    // Implicit-im2col conv wgrad (wg_KH > 0): B row j = (r KW + s) C_in + ci
+    // is row s C_in + ci of B (the input codes on the padded pixel grid,
+    // pre-shifted by s), read from byte r Wp of its K range (the tap's row
+    // shift on a grid of width Wp, a multiple of 16); B has KW C_in rows.
+    int wg_KH, wg_KW;
+    int64_t wg_Cin, wg_Wp;
 };
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
@@ -155,6 +161,14 @@ hipError_t launch_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_
                           const uint8_t* group, const sq_scale* gs, const sq_scale* os,
                           int num_groups, float* out, int64_t ld_out, hipStream_t s);
 int wgrad_splits(int64_t M, int64_t C_out, int64_t C_in);
+
+// Padded pixel grids of the implicit-im2col conv wgrad (see sq_conv_wgrad):
+// out[j, P] for P < ld_out, j < copies * C: P + s (s = j / C) read as pixel
+// (n, hp - top, wp - left) of the content grid Hc x Wc inside the Hp x Wp grid
+// of image n, i.e. in[j % C, (n Hc + h) Wc + w], or 0 outside the content.
+hipError_t launch_grid_scatter(const int8_t* in, int64_t ld_in, int64_t C, int copies, int64_t N, int64_t Hc,
+                               int64_t Wc, int64_t top, int64_t left, int64_t Hp, int64_t Wp, int8_t* out,
+                               int64_t ld_out, hipStream_t s);
 
 // ---- L1BNQ (sq_l1bn.hip) ----
 // Partial-maximum slabs of the backward's dx ranges; int32 partial words of

@@ -42,6 +42,7 @@ EXPORTS = (
     "sq_gemm_dgrad_grouped", "sq_quantize_channels", "sq_gemm_forward",
     "sq_quantize_grad_from_ranges", "sq_l1bn_range_slabs", "sq_l1bn_forward_workspace_size",
     "sq_l1bn_backward_workspace_size", "sq_l1bn_forward", "sq_l1bn_backward",
+    "sq_conv_input_layout", "sq_conv_pack_input", "sq_conv_wgrad_workspace_size", "sq_conv_wgrad",
     "sq_status_string", "sq_last_error",
 )
 
@@ -105,6 +106,14 @@ def load() -> ct.CDLL:
         "sq_quantize_grad_from_ranges": [_P, _I64, _I64, _I64, pp, _P, _I64, _P, _I64, _P, _I64, _P, _P, _P, _P,
                                          _SZ, _P],
         "sq_l1bn_range_slabs": [_I64, _I64, ct.POINTER(_I64)],
+        "sq_conv_input_layout": [_I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32, ct.c_int32,
+                                 ct.POINTER(_I64), ct.POINTER(_I64)],
+        "sq_conv_pack_input": [_P, _I64, _I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32, ct.c_int32,
+                               _P, _I64, _P],
+        "sq_conv_wgrad_workspace_size": [_I64, _I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32,
+                                         ct.c_int32, pp, ct.POINTER(_SZ)],
+        "sq_conv_wgrad": [_P, _I64, _P, _P, _P, _I64, _P, _I64, _I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32,
+                          ct.c_int32, ct.c_int32, pp, _P, _I64, _P, _I64, _P, _SZ, _P],
         "sq_l1bn_forward_workspace_size": [_I64, _I64, ct.POINTER(_SZ)],
         "sq_l1bn_backward_workspace_size": [_I64, _I64, pp, ct.POINTER(_SZ)],
         "sq_l1bn_forward": [_P, _I64, _I64, _I64, _P, _P, _P, _P, _I64, _P, _P, _P, _SZ, _P],
@@ -245,6 +254,33 @@ def sq_quantize_grad_from_ranges(dY, params, ranges, range_slabs, q_fold, q_t, g
     _check("sq_quantize_grad_from_ranges", load().sq_quantize_grad_from_ranges(
         _ptr(dY), M, C, _ld(dY), ct.byref(params), _ptr(ranges), range_slabs, _ptr(q_fold), _ld(q_fold),
         _ptr(q_t), _ld(q_t), _ptr(group), _ptr(scale), _ptr(layout), ws, nws, _stream(stream)))
+
+
+def sq_conv_input_layout(N, H, W, C_in, KH, KW, PH, PW) -> Tuple[int, int]:
+    rows, ld = _I64(0), _I64(0)
+    _check("sq_conv_input_layout", load().sq_conv_input_layout(N, H, W, C_in, KH, KW, PH, PW, ct.byref(rows),
+                                                               ct.byref(ld)))
+    return rows.value, ld.value
+
+
+def sq_conv_pack_input(xq_t, N, H, W, C_in, KH, KW, PH, PW, xs, stream=None) -> None:
+    _check("sq_conv_pack_input", load().sq_conv_pack_input(_ptr(xq_t), _ld(xq_t), N, H, W, C_in, KH, KW, PH, PW,
+                                                           _ptr(xs), _ld(xs), _stream(stream)))
+
+
+def sq_conv_wgrad_workspace_size(N, H, W, C_out, C_in, KH, KW, PH, PW, params: Params) -> int:
+    nb = _SZ(0)
+    _check("sq_conv_wgrad_workspace_size", load().sq_conv_wgrad_workspace_size(
+        N, H, W, C_out, C_in, KH, KW, PH, PW, ct.byref(params), ct.byref(nb)))
+    return nb.value
+
+
+def sq_conv_wgrad(q_t, group, gscale, xs, xscale, N, H, W, C_out, C_in, KH, KW, PH, PW, params, acc, dW, workspace,
+                  stream=None) -> None:
+    ws, nws = _ws_ptr(workspace)
+    _check("sq_conv_wgrad", load().sq_conv_wgrad(
+        _ptr(q_t), _ld(q_t), _ptr(group), _ptr(gscale), _ptr(xs), _ld(xs), _ptr(xscale), N, H, W, C_out, C_in,
+        KH, KW, PH, PW, ct.byref(params), _ptr(acc), _ld(acc), _ptr(dW), _ld(dW), ws, nws, _stream(stream)))
 
 
 def sq_l1bn_range_slabs(M: int, C: int) -> int:
@@ -565,6 +601,30 @@ def l1bn_backward(dy: torch.Tensor, state: L1BNState, bits: int = 8, num_groups:
     ws = _workspace(sq_l1bn_backward_workspace_size(M, C, p), dev)
     sq_l1bn_backward(dy, p, state.xq, state.chan, state.layer, dx, dgamma, dbeta, group, gscale, ranges, ws, stream)
     return {"dx": dx, "dgamma": dgamma, "dbeta": dbeta, "group": group, "gscale": gscale, "ranges": ranges}
+
+
+def conv_pack_input(xq_t: torch.Tensor, N: int, H: int, W: int, KH: int, KW: int, PH: int, PW: int,
+                    stream=None) -> torch.Tensor:
+    """Input codes xq_t [C_in, >= N*H*W] packed for sq_conv_wgrad."""
+    C_in = xq_t.shape[0]
+    rows, ld = sq_conv_input_layout(N, H, W, C_in, KH, KW, PH, PW)
+    xs = torch.empty((max(rows, 1), ld), dtype=torch.int8, device=xq_t.device)[:rows]
+    sq_conv_pack_input(xq_t, N, H, W, C_in, KH, KW, PH, PW, xs, stream)
+    return xs
+
+
+def conv_wgrad(codes: "GradCodes", xs: torch.Tensor, xscale: torch.Tensor, N: int, H: int, W: int, C_in: int,
+               KH: int, KW: int, PH: int, PW: int, want_acc: bool = False, stream=None):
+    """Implicit-im2col conv wgrad: (dW [C_out, KH*KW*C_in] fp32, acc or None)."""
+    dev = codes.q_t.device
+    C_out = codes.C_out
+    Ng = KH * KW * C_in
+    dW = torch.empty((max(C_out, 1), Ng), dtype=torch.float32, device=dev)[:C_out]
+    acc = torch.empty((max(C_out, 1), Ng), dtype=torch.int32, device=dev)[:C_out] if want_acc else None
+    ws = _workspace(sq_conv_wgrad_workspace_size(N, H, W, C_out, C_in, KH, KW, PH, PW, codes.params), dev)
+    sq_conv_wgrad(codes.q_t, codes.group, codes.scale, xs, xscale, N, H, W, C_out, C_in, KH, KW, PH, PW,
+                  codes.params, acc, dW, ws, stream)
+    return dW, acc
 
 
 class BackwardPlan:
