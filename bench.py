@@ -24,7 +24,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 PEAK_INT8_TOPS = 5000.0      # MI355X dense int8 matrix-core peak
-DEFAULT_WORKLOAD = "resnet18_conv3x3"
+DEFAULT_WORKLOAD = "resnet18_conv3x3_fused"
 # the same conv layer with the input gradient taken by the implicit-im2col
 # conv dgrad (dX itself, NHWC, instead of the 9x larger im2col'd dX_col)
 FUSED_CONV = {"resnet18_conv3x3_fused": "resnet18_conv3x3"}
@@ -60,6 +60,7 @@ def measured_traffic(workload: str, kernel: str):
 def cpu_baseline(inputs, wl, budget_s: float = 10.0, conv=False):
     """The CPU oracle (single-threaded C) on the first rows of the same layer
     (whole images for the implicit-im2col conv step)."""
+    import numpy as np
     import oracle
     dY, W, X = inputs["dY"], inputs["W"], inputs["X"]
     M = dY.shape[0]
@@ -73,7 +74,9 @@ def cpu_baseline(inputs, wl, budget_s: float = 10.0, conv=False):
             wq, ws = oracle.quantize_tensor(W, 8)
             xq, xs = oracle.quantize_tensor(X[:rows], 8)
             A = oracle.conv_dgrad(q, g, wl.num_groups, wq, rows // hw, wl.conv_hw, wl.conv_hw, 3, 3, 1, 1)
-            B = oracle.wgrad(q, xq)
+            # the layer input is the centre tap of the im2col'd rows (pad 1)
+            xr = np.ascontiguousarray(xq[:, 4 * wl.conv_cin:5 * wl.conv_cin])
+            B = oracle.conv_wgrad(q, xr, rows // hw, wl.conv_hw, wl.conv_hw, 3, 3, 1, 1)
             oracle.dequant_dgrad(A, gs["d0"], ws["d0"], wl.num_groups)
             oracle.dequant_wgrad(B, g, gs["d0"], xs["d0"])
         else:
@@ -87,7 +90,7 @@ def cpu_baseline(inputs, wl, budget_s: float = 10.0, conv=False):
     rows = int(min(M, max(rows, rows * budget_s / max(t, 1e-3)))) // unit * unit
     t = run(rows)
     ops = 4 * rows * wl.C_out * wl.C_in
-    what = "quantize+conv dgrad+wgrad+dequant" if conv else "quantize+dgrad+wgrad+dequant"
+    what = "quantize+conv dgrad+conv wgrad+dequant" if conv else "quantize+dgrad+wgrad+dequant"
     return {"value": ops / t / 1e12, "unit": "TOPS", "cores": 1, "kind": "oracle",
             "sample": f"oracle {what} on the first {rows} of {M} token rows "
                       f"({ops / 1e9:.2f} Gop in {t:.2f} s, 1 thread)"}
@@ -292,6 +295,9 @@ def main(argv=None):
                     help="forward: quantize X with ShiftQuant + Y = X W^T (per-output-channel W); "
                          "l1bn: the L1BNQ layer (workloads resnet18_bn_56x56x64, resnet50_bn_14x14x1024, "
                          "transformer_bn_768)")
+    ap.add_argument("--conv-wgrad", choices=["implicit", "im2col"], default="implicit",
+                    help="weight gradient of the fused conv step: implicit im2col (sq_conv_wgrad) or the GEMM on "
+                         "the im2col'd activations")
     ap.add_argument("--dgrad", choices=["shiftmm", "grouped"], default="shiftmm",
                     help="grouped: the GEMM-based comparison implementation of the dgrad (Sec. 3.2)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -339,11 +345,23 @@ def main(argv=None):
     X = torch.from_numpy(inputs["X"]).to(dev)
     params = sq.Params.make(wl.bits, wl.num_groups, wl.round_mode, wl.sr_seed, wl.sr_offset)
     wq_t, ws = sq.quantize_tensor(W, 8, transpose=True)
-    xq_t, xs = sq.quantize_tensor(X, 8, transpose=True)
+    implicit = conv and args.conv_wgrad == "implicit"
+    if implicit:
+        # setup (untimed, as the im2col'd codes are): the layer input is the
+        # centre tap of the im2col'd rows (pad 1); its per-tensor scale equals
+        # the im2col'd tensor's (the im2col adds only zeros)
+        n_img = M // (wl.conv_hw * wl.conv_hw)
+        X = X[:, 4 * wl.conv_cin:5 * wl.conv_cin].contiguous()
+        xq_raw, xs = sq.quantize_tensor(X, 8, transpose=True)
+        xq_t = sq.conv_pack_input(xq_raw, n_img, wl.conv_hw, wl.conv_hw, 3, 3, 1, 1)
+        del xq_raw
+    else:
+        xq_t, xs = sq.quantize_tensor(X, 8, transpose=True)
     del W, X
     if conv:
         n_img = M // (wl.conv_hw * wl.conv_hw)
-        plan = sq.ConvBackwardPlan(n_img, wl.conv_hw, wl.conv_hw, C_out, wl.conv_cin, 3, 3, 1, 1, params, device=dev)
+        plan = sq.ConvBackwardPlan(n_img, wl.conv_hw, wl.conv_hw, C_out, wl.conv_cin, 3, 3, 1, 1, params, device=dev,
+                                   implicit_wgrad=implicit)
     else:
         plan = sq.BackwardPlan(M, C_out, C_in, params, device=dev, grouped_dgrad=args.dgrad == "grouped")
     stream = torch.cuda.current_stream()
@@ -397,8 +415,10 @@ def main(argv=None):
         "sq_conv_dgrad" if conv else "sq_gemm_dgrad": {
             "ms": t_dgrad, "bytes": M * C_out + C_out * C_in + 4 * M * (C_in // 9 if conv else C_in),
             "ops": 2 * M * C_out * C_in},
-        "sq_gemm_wgrad": {"ms": t_wgrad, "bytes": M * C_out + M * C_in + 4 * C_out * C_in,
-                          "ops": 2 * M * C_out * C_in},
+        # the implicit conv wgrad reads the layer input [N*H*W, C_in / 9] once
+        "sq_conv_wgrad" if implicit else "sq_gemm_wgrad": {
+            "ms": t_wgrad, "bytes": M * C_out + M * (C_in // 9 if implicit else C_in) + 4 * C_out * C_in,
+            "ops": 2 * M * C_out * C_in},
     }
     dom = max(parts, key=lambda k: parts[k]["ms"])
     d = parts[dom]
@@ -433,6 +453,8 @@ def main(argv=None):
                    "num_groups": wl.num_groups, "rounding": "stochastic" if wl.round_mode else "nearest-even",
                    "dgrad_output": "dX [N,H,W,C] (implicit im2col + col2im)" if conv else "dX_col [M, C_in]",
                    "dgrad_impl": "shiftmm" if conv else args.dgrad,
+                   "wgrad_impl": ("implicit im2col (sq_conv_wgrad)" if implicit else "GEMM on im2col'd X")
+                   if conv else "gemm",
                    "parallelism": "none"},
         "pct_int8_peak": 100.0 * value / PEAK_INT8_TOPS,
         "breakdown_ms": {k: v["ms"] for k, v in parts.items()},

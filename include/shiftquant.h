@@ -369,40 +369,53 @@ sq_status sq_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_t ld_
  *                                   xq(n, oh + r - PH, ow + s - PW, ci)
  * (zero outside the input), with the epilogue of sq_gemm_wgrad
  * (dW[co, :] = fl(float(acc[co, :]) * beta_co)).  Columns follow the (r, s, ci)
- * order of W [C_out, KH KW C_in].
+ * order of W [C_out, KH KW C_in].  Stride 1, 0 <= PH < KH, 0 <= PW < KW,
+ * KH, KW <= 16; Ho = H + 2 PH - KH + 1, Wo = W + 2 PW - KW + 1.
  *
- * Both operands live on a zero-padded pixel grid of Hp = H + 2 PH rows and
- * Wp = roundup(W + 2 PW, 16) columns per image, where tap (r, s) is the
- * constant shift r Wp + s of the pixel index.  The input codes are packed
- * once per step (in training they come from the forward pass):
- *   sq_conv_input_layout   -> rows (KW C_in) and ld of the packed input xs
- *   sq_conv_pack_input     xq_t [C_in, ld_xq >= N H W] (sq_quantize_tensor,
- *                          transpose 1) -> xs [rows, ld]: row s C_in + ci holds
- *                          the padded grid of channel ci shifted by s; every
- *                          byte of xs is written (zeros in the padding).
- * sq_conv_wgrad takes the gradient codes q_t [C_out, ld_t >= N Ho Wo]
- * (sq_quantize_grad's transposed codes), places them on the same grid in the
- * workspace and runs one int8 GEMM whose B rows are the packed input at the
- * taps' row offsets.
- * Inputs : q_t, group, gscale as for sq_gemm_wgrad; xs, ld_xs from the pack
- *          call; xscale the input codes' scale; stride 1, 0 <= PH < KH,
- *          0 <= PW < KW, KH, KW <= 16.
+ * Both operands live on a padded pixel grid of Hp = H + 2 PH rows and
+ * Wp = roundup(W + 2 PW, 16) columns per image, on which tap (r, s) is the
+ * constant shift r Wp + s of the pixel index:
+ *   q_tp [C_out, ld_tp >= q_ld]: gradient code (n, oh, ow, c) at column
+ *        n Hp Wp + oh Wp + ow of row c, every other column 0.
+ *   xs   [KW C_in, x_ld]: row s C_in + ci holds, at column P, the input code
+ *        of channel ci at grid position P + s (input pixel (n, ih, iw) sits at
+ *        n Hp Wp + (ih + PH) Wp + iw + PW), 0 in the padding.
+ * sq_conv_wgrad_layout gives x_rows = KW C_in, x_ld and q_ld.
+ * sq_conv_pack_input builds xs from the input codes xq_t [C_in, ld_xq >= N H W]
+ *   (sq_quantize_tensor, transpose 1) and writes every byte of xs; in training
+ *   the input codes come from the forward pass, once per step.
+ * sq_conv_pack_grad builds q_tp from transposed codes q_t [C_out, ld_t >= N Ho Wo]
+ *   and writes every byte of q_tp.
+ * sq_quantize_grad_conv is sq_quantize_grad for the conv's gradient
+ *   dY [N Ho Wo, ld_dY] (same codes, groups, scale, layout, q_fold, workspace)
+ *   that writes the transposed codes straight onto the padded grid: q_tp's
+ *   padding is never written, so the caller zero-fills that buffer once.
+ * sq_conv_wgrad runs one int8 GEMM (K = the padded grid, rounded up to 64)
+ *   whose B rows are xs at the taps' row offsets.
  * Outputs: acc [C_out, ld_acc] int32 and/or dW [C_out, ld_dW] fp32, each row
  *          KH KW C_in wide.
- * Workspace: sq_conv_wgrad_workspace_size bytes, 256-byte aligned.
+ * Workspace: sq_conv_wgrad_workspace_size bytes (split-K partials, may be 0).
  * Errors: SQ_ERR_INVALID_ARGUMENT; SQ_ERR_OVERFLOW_RISK when
  *         N Ho Wo Q 128 >= 2^31; SQ_ERR_UNSUPPORTED when a padded grid
  *         exceeds 2^31 bytes; SQ_ERR_WORKSPACE_TOO_SMALL; SQ_ERR_HIP.
  * ------------------------------------------------------------------------- */
-sq_status sq_conv_input_layout(int64_t N, int64_t H, int64_t W, int64_t C_in, int32_t KH, int32_t KW,
-                               int32_t PH, int32_t PW, int64_t* rows, int64_t* ld);
+sq_status sq_conv_wgrad_layout(int64_t N, int64_t H, int64_t W, int64_t C_in, int32_t KH, int32_t KW,
+                               int32_t PH, int32_t PW, int64_t* x_rows, int64_t* x_ld, int64_t* q_ld);
 sq_status sq_conv_pack_input(const int8_t* xq_t, int64_t ld_xq, int64_t N, int64_t H, int64_t W, int64_t C_in,
                              int32_t KH, int32_t KW, int32_t PH, int32_t PW, int8_t* xs, int64_t ld_xs,
                              void* stream);
+sq_status sq_conv_pack_grad(const int8_t* q_t, int64_t ld_t, int64_t N, int64_t H, int64_t W, int64_t C_out,
+                            int32_t KH, int32_t KW, int32_t PH, int32_t PW, int8_t* q_tp, int64_t ld_tp,
+                            void* stream);
+sq_status sq_quantize_grad_conv(const float* dY, int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t ld_dY,
+                                int32_t KH, int32_t KW, int32_t PH, int32_t PW, const sq_quant_params* p,
+                                int8_t* q_fold, int64_t ld_fold, int8_t* q_tp, int64_t ld_tp,
+                                uint8_t* group, sq_scale* scale, int32_t* layout,
+                                void* workspace, size_t workspace_bytes, void* stream);
 sq_status sq_conv_wgrad_workspace_size(int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t C_in,
                                        int32_t KH, int32_t KW, int32_t PH, int32_t PW,
                                        const sq_quant_params* p, size_t* bytes);
-sq_status sq_conv_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, const sq_scale* gscale,
+sq_status sq_conv_wgrad(const int8_t* q_tp, int64_t ld_tp, const uint8_t* group, const sq_scale* gscale,
                         const int8_t* xs, int64_t ld_xs, const sq_scale* xscale,
                         int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t C_in,
                         int32_t KH, int32_t KW, int32_t PH, int32_t PW, const sq_quant_params* p,

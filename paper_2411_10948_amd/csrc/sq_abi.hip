@@ -607,13 +607,14 @@ sq_status check_conv_geom(int64_t N, int64_t H, int64_t W, int64_t C_out, int64_
 
 }  // namespace
 
-sq_status sq_conv_input_layout(int64_t N, int64_t H, int64_t W, int64_t C_in, int32_t KH, int32_t KW, int32_t PH,
-                               int32_t PW, int64_t* rows, int64_t* ld) {
-    if (!rows || !ld) return fail(SQ_ERR_INVALID_ARGUMENT, "rows / ld NULL");
+sq_status sq_conv_wgrad_layout(int64_t N, int64_t H, int64_t W, int64_t C_in, int32_t KH, int32_t KW, int32_t PH,
+                               int32_t PW, int64_t* x_rows, int64_t* x_ld, int64_t* q_ld) {
+    if (!x_rows || !x_ld || !q_ld) return fail(SQ_ERR_INVALID_ARGUMENT, "an output pointer is NULL");
     SQ_TRY(check_conv_geom(N, H, W, 1, C_in, KH, KW, PH, PW));
     const ConvGrid g = conv_grid(N, H, W, C_in, KH, KW, PH, PW);
-    *rows = g.rows_x;
-    *ld = g.ld_x;
+    *x_rows = g.rows_x;
+    *x_ld = g.ld_x;
+    *q_ld = g.ld_q;
     return SQ_OK;
 }
 
@@ -630,6 +631,63 @@ sq_status sq_conv_pack_input(const int8_t* xq_t, int64_t ld_xq, int64_t N, int64
                       "conv pack input");
 }
 
+sq_status sq_conv_pack_grad(const int8_t* q_t, int64_t ld_t, int64_t N, int64_t H, int64_t W, int64_t C_out,
+                            int32_t KH, int32_t KW, int32_t PH, int32_t PW, int8_t* q_tp, int64_t ld_tp,
+                            void* stream) {
+    SQ_TRY(check_conv_geom(N, H, W, C_out, 1, KH, KW, PH, PW));
+    const ConvGrid g = conv_grid(N, H, W, 1, KH, KW, PH, PW);
+    if (C_out == 0) return SQ_OK;
+    SQ_TRY(check_codes(q_t, ld_t, N * g.Ho * g.Wo, "q_t"));
+    SQ_TRY(check_codes(q_tp, ld_tp, g.ld_q, "q_tp"));
+    return hip_status(launch_grid_scatter(q_t, ld_t, C_out, 1, N, g.Ho, g.Wo, 0, 0, g.Hp, g.Wp, q_tp, ld_tp,
+                                          static_cast<hipStream_t>(stream)),
+                      "conv pack gradient");
+}
+
+sq_status sq_quantize_grad_conv(const float* dY, int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t ld_dY,
+                                int32_t KH, int32_t KW, int32_t PH, int32_t PW, const sq_quant_params* p,
+                                int8_t* q_fold, int64_t ld_fold, int8_t* q_tp, int64_t ld_tp, uint8_t* group,
+                                sq_scale* scale, int32_t* layout, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_conv_geom(N, H, W, C_out, 1, KH, KW, PH, PW));
+    const ConvGrid g = conv_grid(N, H, W, 1, KH, KW, PH, PW);
+    const int64_t M = N * g.Ho * g.Wo;
+    SQ_TRY(check_dims(M, C_out, "dY"));
+    if (g.Hp * g.Wp >= ((int64_t)1 << 32) || M >= ((int64_t)1 << 32))
+        return fail(SQ_ERR_UNSUPPORTED, "the padded grid exceeds 2^32 pixels");
+    if (C_out > 0) SQ_TRY(check_f32(dY, ld_dY, C_out, "dY"));
+    if (!scale || !aligned(scale, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "scale is NULL or misaligned");
+    if (!layout || !aligned(layout, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "layout is NULL or misaligned");
+    if (C_out > 0 && !group) return fail(SQ_ERR_INVALID_ARGUMENT, "group is NULL");
+    size_t lay_bytes = 0;
+    int64_t min_ld_fold = 0;
+    SQ_TRY(sq_grad_layout_size(C_out, p, &lay_bytes, &min_ld_fold));
+    if (q_fold) SQ_TRY(check_codes(q_fold, ld_fold, min_ld_fold, "q_fold"));
+    if (C_out > 0) SQ_TRY(check_codes(q_tp, ld_tp, g.ld_q, "q_tp"));
+    if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
+    if (workspace_bytes < quant_ws_bytes(M, C_out)) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+
+    const QuantCfg cfg = make_cfg(*p);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    uint32_t* partial = static_cast<uint32_t*>(workspace);
+    int64_t slabs = 0;
+    SQ_TRY(hip_status(launch_colmax(dY, M, C_out, ld_dY, partial, &slabs, s), "colmax"));
+    const int64_t ext_max = fold_ext_max(C_out, cfg);
+    SQ_TRY(hip_status(launch_finalize_grad(partial, slabs, C_out, cfg, partial + slabs * C_out, group, scale, layout,
+                                           ext_max, s),
+                      "finalize"));
+    PadGrid pg;
+    pg.Wo = (uint32_t)g.Wo;
+    pg.HoWo = (uint32_t)(g.Ho * g.Wo);
+    pg.Wp = (uint32_t)g.Wp;
+    pg.HpWp = (uint32_t)(g.Hp * g.Wp);
+    SQ_TRY(hip_status(launch_quantize(dY, M, C_out, ld_dY, group, scale, cfg, q_fold, ld_fold, q_tp, ld_tp,
+                                      layout + kLayoutHeader + ext_max, s, pg),
+                      "quantize"));
+    return SQ_OK;
+}
+
 sq_status sq_conv_wgrad_workspace_size(int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t C_in, int32_t KH,
                                        int32_t KW, int32_t PH, int32_t PW, const sq_quant_params* p, size_t* bytes) {
     if (!bytes) return fail(SQ_ERR_INVALID_ARGUMENT, "bytes is NULL");
@@ -638,13 +696,11 @@ sq_status sq_conv_wgrad_workspace_size(int64_t N, int64_t H, int64_t W, int64_t 
     const ConvGrid g = conv_grid(N, H, W, C_in, KH, KW, PH, PW);
     const int64_t Ng = (int64_t)KH * KW * C_in;
     const int splits = (C_out > 0 && Ng > 0) ? wgrad_splits(g.K, C_out, Ng) : 1;
-    size_t need = (size_t)round_up(std::max<int64_t>(C_out, 1) * g.ld_q, 256);
-    if (splits > 1) need += (size_t)splits * C_out * Ng * 4;
-    *bytes = need;
+    *bytes = splits > 1 ? (size_t)splits * C_out * Ng * 4 : 0;
     return SQ_OK;
 }
 
-sq_status sq_conv_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, const sq_scale* gscale,
+sq_status sq_conv_wgrad(const int8_t* q_tp, int64_t ld_tp, const uint8_t* group, const sq_scale* gscale,
                         const int8_t* xs, int64_t ld_xs, const sq_scale* xscale, int64_t N, int64_t H, int64_t W,
                         int64_t C_out, int64_t C_in, int32_t KH, int32_t KW, int32_t PH, int32_t PW,
                         const sq_quant_params* p, int32_t* acc, int64_t ld_acc, float* dW, int64_t ld_dW,
@@ -660,26 +716,19 @@ sq_status sq_conv_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, c
         return fail(SQ_ERR_OVERFLOW_RISK, "N Ho Wo * Q * 128 reaches 2^31: the int32 accumulator could overflow");
     if (C_out == 0 || C_in == 0) return SQ_OK;
     if (!group) return fail(SQ_ERR_INVALID_ARGUMENT, "group is NULL");
-    SQ_TRY(check_codes(q_t, ld_t, M, "q_t"));
+    SQ_TRY(check_codes(q_tp, ld_tp, g.ld_q, "q_tp"));
     SQ_TRY(check_codes(xs, ld_xs, g.ld_x, "xs"));
-    if (ld_xs != g.ld_x) return fail(SQ_ERR_INVALID_ARGUMENT, "ld_xs must be the one sq_conv_input_layout returns");
+    if (ld_xs != g.ld_x) return fail(SQ_ERR_INVALID_ARGUMENT, "ld_xs must be the one sq_conv_wgrad_layout returns");
+    if ((int64_t)C_out * ld_tp >= ((int64_t)1 << 31)) return fail(SQ_ERR_UNSUPPORTED, "q_tp exceeds 2^31 bytes");
     if (acc) SQ_TRY(check_f32(acc, ld_acc, Ng, "acc"));
     if (dW) SQ_TRY(check_f32(dW, ld_dW, Ng, "dW"));
     size_t need = 0;
     SQ_TRY(sq_conv_wgrad_workspace_size(N, H, W, C_out, C_in, KH, KW, PH, PW, p, &need));
-    if (!workspace || !aligned(workspace, 256))
-        return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or not 256-byte aligned");
-    if (workspace_bytes < need) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
     hipStream_t s = static_cast<hipStream_t>(stream);
-    // gradient codes onto the padded grid: output pixel (n, oh, ow) at
-    // n Hp Wp + oh Wp + ow, zeros elsewhere
-    int8_t* qp = static_cast<int8_t*>(workspace);
-    SQ_TRY(hip_status(launch_grid_scatter(q_t, ld_t, C_out, 1, N, g.Ho, g.Wo, 0, 0, g.Hp, g.Wp, qp, g.ld_q, s),
-                      "conv pack gradient"));
     const int splits = wgrad_splits(g.K, C_out, Ng);
     GemmArgs a{};
     a.Mg = C_out; a.Ng = Ng;
-    a.A = qp; a.lda = g.ld_q;
+    a.A = q_tp; a.lda = ld_tp;
     a.B = xs; a.ldb = ld_xs;
     a.K = g.K;
     a.gs = gscale; a.os = xscale; a.group = group; a.num_groups = cfg.num_groups;
@@ -691,7 +740,9 @@ sq_status sq_conv_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, c
         a.out = dW; a.ld_out = ld_dW;
         return hip_status(launch_gemm(a, s), "conv wgrad");
     }
-    int32_t* part = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + round_up(C_out * g.ld_q, 256));
+    if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
+    if (workspace_bytes < need) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+    int32_t* part = static_cast<int32_t*>(workspace);
     GemmArgs gp = a;
     gp.splits = splits;
     gp.part = part;

@@ -456,14 +456,24 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / T::WN, wn = wave % T::WN;
+    // Split-K launches are one-dimensional: the tiles of one K split get block
+    // ids 8 apart, so they run on the same XCD at about the same time and
+    // share its L2 (operand rows common to the tiles are fetched once).
+    int64_t bt = blockIdx.x, split = blockIdx.y;
+    if (p.splits > 1) {
+        const int64_t nt = tiles_m * tiles_n, L = blockIdx.x, G = L / (8 * nt), rem = L - G * 8 * nt;
+        const int64_t Sg = min((int64_t)8, (int64_t)p.splits - 8 * G);
+        bt = rem / Sg;
+        split = 8 * G + rem % Sg;
+    }
     int64_t tm, tn;
-    tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
+    tile_coords(bt, tiles_m, tiles_n, tm, tn);
     const int64_t m0 = tm * T::BM, n0 = tn * T::BN;
 
     const FoldView fv = fold_view(p, T::BK);
     int64_t koff = 0, Kd = p.K;   // K range: [0, K), or a device-side segment
     if (p.kseg) { koff = p.kseg[0]; Kd = p.kseg[1]; }
-    const int64_t kbeg = (int64_t)blockIdx.y * k_per_split;
+    const int64_t kbeg = split * k_per_split;
     const int64_t kend = min(Kd, kbeg + k_per_split);
     const int n_main = kend > kbeg ? (int)((kend - kbeg) / T::BK) : 0;
     // a convolution visits the flat fold sequence once per tap: tile t is
@@ -717,7 +727,7 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
                 const int vv[4] = {v0, v1, v2, v3};
                 const bool full = jj + 4 <= p.Ng;
                 if (p.part) {
-                    int32_t* dst = p.part + (int64_t)blockIdx.y * p.Mg * p.Ng + ii * p.Ng + jj;
+                    int32_t* dst = p.part + split * p.Mg * p.Ng + ii * p.Ng + jj;
                     if (vec_part && full) {
                         *reinterpret_cast<int4*>(dst) = make_int4(v0, v1, v2, v3);
                     } else {
@@ -1196,8 +1206,11 @@ hipError_t launch_cfg(const GemmArgs& a, int splits, int64_t k_per_split, hipStr
 template <class T, bool HORNER, bool CONV = false>
 hipError_t launch_pipe(const GemmArgs& a, int splits, int64_t k_per_split, hipStream_t s) {
     const int64_t tiles_m = (a.Mg + T::BM - 1) / T::BM, tiles_n = (a.Ng + T::BN - 1) / T::BN;
-    if (tiles_m * tiles_n > 0x7FFFFFFF || splits > 65535) return hipErrorInvalidValue;
-    dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)splits);
+    if (tiles_m * tiles_n * splits > 0x7FFFFFFF || splits > 65535) return hipErrorInvalidValue;
+    // split-K: one-dimensional grid, decoded in the kernel (tiles of a split
+    // on one XCD); a.splits must equal splits for that decoding
+    if (splits > 1 && a.splits != splits) return hipErrorInvalidValue;
+    const dim3 grid = splits > 1 ? dim3((unsigned)(tiles_m * tiles_n * splits)) : dim3((unsigned)(tiles_m * tiles_n));
     hipLaunchKernelGGL((k_gemm_pipe<T, HORNER, CONV>), grid, dim3(T::kThreads), 0, s, a, tiles_m, tiles_n,
                        k_per_split);
     return hipGetLastError();
@@ -1256,7 +1269,7 @@ Pick pick(const GemmArgs& a) {
 
 // Split-K factor of the weight-gradient product: large tiles with the split
 // that fills the chip where that works (large_splits), else enough smaller
-// tiles for about two blocks per CU with at least 8 K tiles per split and no
+// tiles for about one block per CU with at least 8 K tiles per split and no
 // empty split.  The partial tiles do not depend on the tile shape.
 int wgrad_splits(int64_t M, int64_t C_out, int64_t C_in) {
     GemmArgs probe{};
@@ -1269,7 +1282,9 @@ int wgrad_splits(int64_t M, int64_t C_out, int64_t C_in) {
     const bool skinny = C_out <= 64;
     const int64_t tiles = skinny ? tiles_of(probe, PipeSkinny::BM, PipeSkinny::BN)
                                  : tiles_of(probe, PipeSmall::BM, PipeSmall::BN);
-    int64_t splits = (512 + tiles - 1) / tiles;
+    // about one block per CU: more splits only add partial tiles (measured on
+    // the ResNet layers: 256 blocks beat 512 and 768 slightly, 128 clearly)
+    int64_t splits = (256 + tiles - 1) / tiles;
     splits = std::min(splits, std::max<int64_t>(1, ktiles / 8));
     splits = std::max<int64_t>(1, std::min<int64_t>(splits, 65535));
     const int64_t per = (ktiles + splits - 1) / splits;

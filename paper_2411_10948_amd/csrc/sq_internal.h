@@ -82,12 +82,18 @@ hipError_t launch_finalize_grad(const uint32_t* partial, int64_t slabs, int64_t 
                                 int64_t ext_max, hipStream_t s);
 hipError_t launch_finalize_tensor(const uint32_t* partial, int64_t slabs, int64_t C, int Q, uint32_t* rbits,
                                   sq_scale* scale, hipStream_t s);
+// Padded pixel grid of the transposed codes (conv wgrad): row m = (n, oh, ow)
+// of an Ho x Wo output grid goes to column n HpWp + oh Wp + ow; Wo = 0: plain
+// (column m).  Every value below 2^32.
+struct PadGrid {
+    uint32_t Wo = 0, HoWo = 0, Wp = 0, HpWp = 0;
+};
 // group == nullptr: every channel in group 0 with shift 0 (per-tensor mode);
 // desc: the channel descriptors of the fold layout (nullptr: all main, t = 0).
 hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, const uint8_t* group,
                            const sq_scale* scale, const QuantCfg& cfg,
                            int8_t* q_fold, int64_t ld_fold, int8_t* q_t, int64_t ld_t,
-                           const int32_t* desc, hipStream_t s);
+                           const int32_t* desc, hipStream_t s, PadGrid pg = PadGrid());
 
 // Per-channel weight quantization: axis 0 one scale per row, axis 1 one per
 // column (partial: colmax scratch, axis 1 only).

@@ -781,7 +781,8 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
                                                      const sq_scale* __restrict__ scale, QuantCfg cfg,
                                                      int8_t* __restrict__ q_fold, int64_t ld_fold,
                                                      int8_t* __restrict__ q_t, int64_t ld_t,
-                                                     const int32_t* __restrict__ desc, int64_t ext_base) {
+                                                     const int32_t* __restrict__ desc, int64_t ext_base,
+                                                     PadGrid pg) {
     constexpr int QD = TC / 4;            // channel quads per tile
     constexpr int RQ = kBlock / QD;       // row quads per pass
     constexpr int RP = 4 * RQ;            // rows per pass
@@ -909,7 +910,29 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
             for (int id = tid; id < TC * CPR; id += kBlock) {
                 const int ch = id / CPR, part = id % CPR;
                 const int64_t c = ct * TC + ch, m = m_tile + 16 * part;
-                if (c < C && m < M) {
+                if (pg.Wo && c < C && m < M) {
+                    // padded pixel grid: pixel m = (n, oh, ow) at n HpWp + oh Wp + ow
+                    const uint32_t* src = &tq[ch * TW + 4 * part];
+                    int8_t* row = q_t + c * ld_t;
+                    if (pg.Wo % 8 == 0 && m + 16 <= M) {
+                        // 8-pixel halves never cross an image row
+#pragma unroll
+                        for (int h = 0; h < 2; ++h) {
+                            const uint32_t mh = (uint32_t)(m + 8 * h);
+                            const uint32_t n = mh / pg.HoWo, rem = mh - n * pg.HoWo, oh = rem / pg.Wo;
+                            const uint32_t ow = rem - oh * pg.Wo;
+                            const int64_t d = (int64_t)n * pg.HpWp + (int64_t)oh * pg.Wp + ow;
+                            *reinterpret_cast<uint2*>(row + d) = make_uint2(src[2 * h], src[2 * h + 1]);
+                        }
+                    } else {
+                        for (int i = 0; i < 16 && m + i < M; ++i) {
+                            const uint32_t mi = (uint32_t)(m + i);
+                            const uint32_t n = mi / pg.HoWo, rem = mi - n * pg.HoWo, oh = rem / pg.Wo;
+                            const uint32_t ow = rem - oh * pg.Wo;
+                            row[(int64_t)n * pg.HpWp + (int64_t)oh * pg.Wp + ow] = (int8_t)(src[i / 4] >> (8 * (i % 4)));
+                        }
+                    }
+                } else if (c < C && m < M) {
                     const uint32_t* src = &tq[ch * TW + 4 * part];
                     int8_t* dst = q_t + c * ld_t + m;
                     if (m + 16 <= M) {
@@ -1062,7 +1085,7 @@ constexpr int64_t kQuantMinTiles = 1024;    // four blocks per CU
 
 hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, const uint8_t* group,
                            const sq_scale* scale, const QuantCfg& cfg, int8_t* q_fold, int64_t ld_fold,
-                           int8_t* q_t, int64_t ld_t, const int32_t* desc, hipStream_t s) {
+                           int8_t* q_t, int64_t ld_t, const int32_t* desc, hipStream_t s, PadGrid pg) {
     if (M <= 0 || C <= 0) return hipSuccess;
     const bool vec = ((ld & 3) == 0) && ((reinterpret_cast<uintptr_t>(x) & 15) == 0);
     const bool sr = cfg.round_mode == SQ_ROUND_STOCHASTIC;
@@ -1078,13 +1101,13 @@ hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, con
 #define SQ_LAUNCH_QUANT(TC, TR)                                                                                  \
     do {                                                                                                         \
         if (vec && sr) hipLaunchKernelGGL((k_quantize<TC, TR, 4, true>), grid, dim3(kBlock), 0, s, x, M, C, ld,  \
-                                          group, scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb);              \
+                                          group, scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, pg);              \
         else if (vec) hipLaunchKernelGGL((k_quantize<TC, TR, 4, false>), grid, dim3(kBlock), 0, s, x, M, C, ld,  \
-                                         group, scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb);               \
+                                         group, scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, pg);               \
         else if (sr) hipLaunchKernelGGL((k_quantize<TC, TR, 1, true>), grid, dim3(kBlock), 0, s, x, M, C, ld,    \
-                                        group, scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb);                \
+                                        group, scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, pg);                \
         else hipLaunchKernelGGL((k_quantize<TC, TR, 1, false>), grid, dim3(kBlock), 0, s, x, M, C, ld, group,    \
-                                scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb);                               \
+                                scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, pg);                               \
     } while (0)
     if (tc == 64 && tr == 64) SQ_LAUNCH_QUANT(64, 64);
     else if (tc == 64) SQ_LAUNCH_QUANT(64, 128);

@@ -42,7 +42,8 @@ EXPORTS = (
     "sq_gemm_dgrad_grouped", "sq_quantize_channels", "sq_gemm_forward",
     "sq_quantize_grad_from_ranges", "sq_l1bn_range_slabs", "sq_l1bn_forward_workspace_size",
     "sq_l1bn_backward_workspace_size", "sq_l1bn_forward", "sq_l1bn_backward",
-    "sq_conv_input_layout", "sq_conv_pack_input", "sq_conv_wgrad_workspace_size", "sq_conv_wgrad",
+    "sq_conv_wgrad_layout", "sq_conv_pack_input", "sq_conv_pack_grad", "sq_quantize_grad_conv",
+    "sq_conv_wgrad_workspace_size", "sq_conv_wgrad",
     "sq_status_string", "sq_last_error",
 )
 
@@ -106,8 +107,12 @@ def load() -> ct.CDLL:
         "sq_quantize_grad_from_ranges": [_P, _I64, _I64, _I64, pp, _P, _I64, _P, _I64, _P, _I64, _P, _P, _P, _P,
                                          _SZ, _P],
         "sq_l1bn_range_slabs": [_I64, _I64, ct.POINTER(_I64)],
-        "sq_conv_input_layout": [_I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32, ct.c_int32,
-                                 ct.POINTER(_I64), ct.POINTER(_I64)],
+        "sq_conv_wgrad_layout": [_I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32, ct.c_int32,
+                                 ct.POINTER(_I64), ct.POINTER(_I64), ct.POINTER(_I64)],
+        "sq_conv_pack_grad": [_P, _I64, _I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32, ct.c_int32,
+                              _P, _I64, _P],
+        "sq_quantize_grad_conv": [_P, _I64, _I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32,
+                                  ct.c_int32, pp, _P, _I64, _P, _I64, _P, _P, _P, _P, _SZ, _P],
         "sq_conv_pack_input": [_P, _I64, _I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32, ct.c_int32,
                                _P, _I64, _P],
         "sq_conv_wgrad_workspace_size": [_I64, _I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32,
@@ -256,11 +261,26 @@ def sq_quantize_grad_from_ranges(dY, params, ranges, range_slabs, q_fold, q_t, g
         _ptr(q_t), _ld(q_t), _ptr(group), _ptr(scale), _ptr(layout), ws, nws, _stream(stream)))
 
 
-def sq_conv_input_layout(N, H, W, C_in, KH, KW, PH, PW) -> Tuple[int, int]:
-    rows, ld = _I64(0), _I64(0)
-    _check("sq_conv_input_layout", load().sq_conv_input_layout(N, H, W, C_in, KH, KW, PH, PW, ct.byref(rows),
-                                                               ct.byref(ld)))
-    return rows.value, ld.value
+def sq_conv_wgrad_layout(N, H, W, C_in, KH, KW, PH, PW) -> Tuple[int, int, int]:
+    """(x_rows, x_ld, q_ld) of the padded pixel grids of sq_conv_wgrad."""
+    rows, ld, qld = _I64(0), _I64(0), _I64(0)
+    _check("sq_conv_wgrad_layout", load().sq_conv_wgrad_layout(N, H, W, C_in, KH, KW, PH, PW, ct.byref(rows),
+                                                               ct.byref(ld), ct.byref(qld)))
+    return rows.value, ld.value, qld.value
+
+
+def sq_conv_pack_grad(q_t, N, H, W, C_out, KH, KW, PH, PW, q_tp, stream=None) -> None:
+    _check("sq_conv_pack_grad", load().sq_conv_pack_grad(_ptr(q_t), _ld(q_t), N, H, W, C_out, KH, KW, PH, PW,
+                                                         _ptr(q_tp), _ld(q_tp), _stream(stream)))
+
+
+def sq_quantize_grad_conv(dY, N, H, W, KH, KW, PH, PW, params, q_fold, q_tp, group, scale, layout, workspace,
+                          stream=None) -> None:
+    C = dY.shape[1]
+    ws, nws = _ws_ptr(workspace)
+    _check("sq_quantize_grad_conv", load().sq_quantize_grad_conv(
+        _ptr(dY), N, H, W, C, _ld(dY), KH, KW, PH, PW, ct.byref(params), _ptr(q_fold), _ld(q_fold), _ptr(q_tp),
+        _ld(q_tp), _ptr(group), _ptr(scale), _ptr(layout), ws, nws, _stream(stream)))
 
 
 def sq_conv_pack_input(xq_t, N, H, W, C_in, KH, KW, PH, PW, xs, stream=None) -> None:
@@ -607,22 +627,36 @@ def conv_pack_input(xq_t: torch.Tensor, N: int, H: int, W: int, KH: int, KW: int
                     stream=None) -> torch.Tensor:
     """Input codes xq_t [C_in, >= N*H*W] packed for sq_conv_wgrad."""
     C_in = xq_t.shape[0]
-    rows, ld = sq_conv_input_layout(N, H, W, C_in, KH, KW, PH, PW)
+    rows, ld, _ = sq_conv_wgrad_layout(N, H, W, C_in, KH, KW, PH, PW)
     xs = torch.empty((max(rows, 1), ld), dtype=torch.int8, device=xq_t.device)[:rows]
     sq_conv_pack_input(xq_t, N, H, W, C_in, KH, KW, PH, PW, xs, stream)
     return xs
 
 
+def conv_pack_grad(codes: "GradCodes", N: int, H: int, W: int, KH: int, KW: int, PH: int, PW: int,
+                   stream=None) -> torch.Tensor:
+    """The transposed gradient codes of `codes` on the padded pixel grid."""
+    _, _, qld = sq_conv_wgrad_layout(N, H, W, 1, KH, KW, PH, PW)
+    q_tp = torch.empty((max(codes.C_out, 1), qld), dtype=torch.int8, device=codes.q_t.device)[:codes.C_out]
+    sq_conv_pack_grad(codes.q_t, N, H, W, codes.C_out, KH, KW, PH, PW, q_tp, stream)
+    return q_tp
+
+
 def conv_wgrad(codes: "GradCodes", xs: torch.Tensor, xscale: torch.Tensor, N: int, H: int, W: int, C_in: int,
-               KH: int, KW: int, PH: int, PW: int, want_acc: bool = False, stream=None):
-    """Implicit-im2col conv wgrad: (dW [C_out, KH*KW*C_in] fp32, acc or None)."""
+               KH: int, KW: int, PH: int, PW: int, want_acc: bool = False, q_tp: Optional[torch.Tensor] = None,
+               stream=None):
+    """Implicit-im2col conv wgrad: (dW [C_out, KH*KW*C_in] fp32, acc or None).
+    q_tp: the padded gradient codes (sq_quantize_grad_conv); packed from
+    codes.q_t when not given."""
     dev = codes.q_t.device
     C_out = codes.C_out
+    if q_tp is None:
+        q_tp = conv_pack_grad(codes, N, H, W, KH, KW, PH, PW, stream)
     Ng = KH * KW * C_in
     dW = torch.empty((max(C_out, 1), Ng), dtype=torch.float32, device=dev)[:C_out]
     acc = torch.empty((max(C_out, 1), Ng), dtype=torch.int32, device=dev)[:C_out] if want_acc else None
     ws = _workspace(sq_conv_wgrad_workspace_size(N, H, W, C_out, C_in, KH, KW, PH, PW, codes.params), dev)
-    sq_conv_wgrad(codes.q_t, codes.group, codes.scale, xs, xscale, N, H, W, C_out, C_in, KH, KW, PH, PW,
+    sq_conv_wgrad(q_tp, codes.group, codes.scale, xs, xscale, N, H, W, C_out, C_in, KH, KW, PH, PW,
                   codes.params, acc, dW, ws, stream)
     return dW, acc
 
@@ -675,17 +709,26 @@ class BackwardPlan:
 class ConvBackwardPlan(BackwardPlan):
     """Backward step of a stride-1 convolution lowered by im2col, with the input
     gradient taken by sq_conv_dgrad (implicit im2col and col2im: dX is
-    [N*H*W, C_in_ch], NHWC) and the weight gradient by sq_gemm_wgrad on the
+    [N*H*W, C_in_ch], NHWC) and the weight gradient by sq_conv_wgrad on the
+    packed input codes (implicit_wgrad, the default: ``run`` takes the output
+    of conv_pack_input as its xq_t argument) or by sq_gemm_wgrad on the
     im2col'd activations.  Buffers are allocated once; ``run`` allocates
     nothing."""
 
     def __init__(self, N: int, H: int, W: int, C_out: int, C_in_ch: int, KH: int, KW: int, PH: int, PW: int,
-                 params: Params, device="cuda", want_acc: bool = False):
+                 params: Params, device="cuda", want_acc: bool = False, implicit_wgrad: bool = True):
         Ho, Wo = H + 2 * PH - KH + 1, W + 2 * PW - KW + 1
         super().__init__(N * Ho * Wo, C_out, KH * KW * C_in_ch, params, device, want_acc)
         dev = torch.device(device)
         self.geom = (N, H, W, KH, KW, PH, PW)
         self.C_in_ch = C_in_ch
+        self.implicit_wgrad = implicit_wgrad
+        if implicit_wgrad:
+            self.ws_w = _workspace(sq_conv_wgrad_workspace_size(N, H, W, C_out, C_in_ch, KH, KW, PH, PW, params), dev)
+            _, _, qld = sq_conv_wgrad_layout(N, H, W, C_in_ch, KH, KW, PH, PW)
+            # the quantizer never writes the padding of the grid: zero it once
+            self.q_tp = torch.zeros((C_out, qld), dtype=torch.int8, device=dev)
+            self.q_t = None
         self.ws_d = _workspace(sq_conv_dgrad_workspace_size(C_out, C_in_ch, KH, KW, params), dev)
         self.dX = torch.empty((N * H * W, C_in_ch), dtype=torch.float32, device=dev)
         self.acc_dX = torch.empty((N * H * W, C_in_ch), dtype=torch.int32, device=dev) if want_acc else None
@@ -694,3 +737,17 @@ class ConvBackwardPlan(BackwardPlan):
         N, H, W, KH, KW, PH, PW = self.geom
         sq_conv_dgrad(self.q_fold, self.layout, self.group, self.scale, wq_t, wscale, N, H, W, self.C_out,
                       self.C_in_ch, KH, KW, PH, PW, self.params, self.acc_dX, self.dX, self.ws_d, stream)
+
+    def quantize(self, dY, stream=None):
+        if not self.implicit_wgrad:
+            return super().quantize(dY, stream)
+        N, H, W, KH, KW, PH, PW = self.geom
+        sq_quantize_grad_conv(dY, N, H, W, KH, KW, PH, PW, self.params, self.q_fold, self.q_tp, self.group,
+                              self.scale, self.layout, self.ws_q, stream)
+
+    def wgrad(self, xq_t, xscale, stream=None):
+        if not self.implicit_wgrad:
+            return super().wgrad(xq_t, xscale, stream)
+        N, H, W, KH, KW, PH, PW = self.geom
+        sq_conv_wgrad(self.q_tp, self.group, self.scale, xq_t, xscale, N, H, W, self.C_out, self.C_in_ch, KH, KW,
+                      PH, PW, self.params, self.acc_dW, self.dW, self.ws_w, stream)

@@ -48,8 +48,20 @@ def _run(sq, dY, X, case, mode=0):
     xq_t, xs_scale = sq.quantize_tensor(_dev(X), 8, transpose=True)
     xs = sq.conv_pack_input(xq_t, N, H, W, KH, KW, PH, PW)
     dW, acc = sq.conv_wgrad(codes, xs, xs_scale, N, H, W, C_in, KH, KW, PH, PW, want_acc=True)
-    dW2, _ = sq.conv_wgrad(codes, xs, xs_scale, N, H, W, C_in, KH, KW, PH, PW, want_acc=False)
+    # the quantizer writing the padded codes directly (padding zero-filled once)
+    _, _, qld = sq.sq_conv_wgrad_layout(N, H, W, C_in, KH, KW, PH, PW)
+    q_tp = torch.zeros((C_out, qld), dtype=torch.int8, device="cuda")
+    q_fold = torch.zeros_like(codes.q_fold)
+    group = torch.empty_like(codes.group)
+    scale = sq.new_scale("cuda")
+    layout = torch.zeros_like(codes.layout)
+    ws = torch.empty(max(sq.sq_quantize_grad_workspace_size(dY.shape[0], C_out, codes.params), 256),
+                     dtype=torch.uint8, device="cuda")
+    sq.sq_quantize_grad_conv(_dev(dY), N, H, W, KH, KW, PH, PW, codes.params, q_fold, q_tp, group, scale, layout, ws)
+    dW2, _ = sq.conv_wgrad(codes, xs, xs_scale, N, H, W, C_in, KH, KW, PH, PW, want_acc=False, q_tp=q_tp)
     torch.cuda.synchronize()
+    assert torch.equal(q_fold, codes.q_fold) and torch.equal(group, codes.group) and torch.equal(scale, codes.scale)
+    assert torch.equal(q_tp, sq.conv_pack_grad(codes, N, H, W, KH, KW, PH, PW))
     assert torch.equal(dW, dW2)
     return codes, acc.cpu().numpy(), dW.cpu().numpy()
 
@@ -113,7 +125,7 @@ def test_conv_pack_input_layout(sq):
     xq_t[:, :N * H * W] = torch.from_numpy(xq.T.copy()).cuda()
     xs = sq.conv_pack_input(xq_t, N, H, W, KH, KW, PH, PW)
     torch.cuda.synchronize()
-    rows, ld = sq.sq_conv_input_layout(N, H, W, C_in, KH, KW, PH, PW)
+    rows, ld, _ = sq.sq_conv_wgrad_layout(N, H, W, C_in, KH, KW, PH, PW)
     Hp, Wp = H + 2 * PH, 16
     assert rows == KW * C_in and ld % 16 == 0
     got = xs.cpu().numpy()
