@@ -1006,8 +1006,10 @@ ColmaxPlan colmax_plan(int64_t M, int64_t C, bool vec) {
     p.vec = VEC;
     p.tpr = tpr;
     p.chunks = std::max<int64_t>(1, (units + tpr - 1) / tpr);
-    // about 1024 blocks (four per CU), each slab at least 8 row passes deep
-    int64_t slabs = std::max<int64_t>(1, 1024 / p.chunks);
+    // about 512 blocks (two per CU), each slab at least 8 row passes deep:
+    // fewer slab maxima for the finalize to reduce (1024 blocks cost the
+    // 64-channel conv gradient 3 us more, measured)
+    int64_t slabs = std::max<int64_t>(1, 512 / p.chunks);
     const int64_t min_rows = 8 * (int64_t)nrl;
     slabs = std::min<int64_t>(slabs, std::max<int64_t>(1, (M + min_rows - 1) / min_rows));
     slabs = std::min<int64_t>(slabs, 65535);
