@@ -361,6 +361,29 @@ sq_status sq_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_t ld_
                      int32_t num_groups, float* out, int64_t ld_out, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * sq_gemm_dgrad_ranged -- sq_gemm_dgrad that also writes the channel ranges
+ * of dX for the quantizer of the layer below.
+ *
+ * In a chain of layers dX is the next dY to be quantized, and the quantizer's
+ * first step is r_c = max_m |dY[m, c]| (Sec. 3.1).  Here the GEMM's epilogue
+ * takes those maxima from the values it stores:
+ *   dX_ranges[s, c] = bits of max |dX[m, c]| over rows m in [32 s, 32 s + 32),
+ * sign bit cleared, s < sq_gemm_dgrad_range_slabs(M) = ceil(M / 32); they are
+ * the `ranges` input of sq_quantize_grad_from_ranges.  The maxima come from
+ * the GEMM's epilogue when C_out is a multiple of 64 (and every operand's byte
+ * offsets fit in 31 bits); otherwise one extra pass over the stored dX takes
+ * them.  Arguments, outputs and errors as sq_gemm_dgrad, with dX required;
+ * SQ_ERR_UNSUPPORTED beyond 2^21 rows on the second path.
+ * ------------------------------------------------------------------------- */
+sq_status sq_gemm_dgrad_range_slabs(int64_t M, int64_t* slabs);
+sq_status sq_gemm_dgrad_ranged(const int8_t* q_fold, int64_t ld_fold, const int32_t* layout,
+                               const uint8_t* group, const sq_scale* gscale,
+                               const int8_t* wq_t, int64_t ld_w, const sq_scale* wscale,
+                               int64_t M, int64_t C_out, int64_t C_in, const sq_quant_params* p,
+                               int32_t* acc, int64_t ld_acc, float* dX, int64_t ld_dX, uint32_t* dX_ranges,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Implicit-im2col weight gradient of a stride-1 convolution.
  *
  * The wgrad of the im2col'd conv layer (Fig. "MMs", third GEMM, on the conv

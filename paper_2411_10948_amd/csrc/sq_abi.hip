@@ -227,10 +227,12 @@ sq_status sq_quantize_tensor(const float* T, int64_t rows, int64_t cols, int64_t
     return SQ_OK;
 }
 
-sq_status sq_gemm_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* layout, const uint8_t* group,
-                        const sq_scale* gscale, const int8_t* wq_t, int64_t ld_w, const sq_scale* wscale, int64_t M,
-                        int64_t C_out, int64_t C_in, const sq_quant_params* p, int32_t* acc, int64_t ld_acc,
-                        float* dX, int64_t ld_dX, void* workspace, size_t workspace_bytes, void* stream) {
+namespace {
+sq_status gemm_dgrad_impl(const int8_t* q_fold, int64_t ld_fold, const int32_t* layout, const uint8_t* group,
+                          const sq_scale* gscale, const int8_t* wq_t, int64_t ld_w, const sq_scale* wscale, int64_t M,
+                          int64_t C_out, int64_t C_in, const sq_quant_params* p, int32_t* acc, int64_t ld_acc,
+                          float* dX, int64_t ld_dX, uint32_t* ranges, void* workspace, size_t workspace_bytes,
+                          void* stream) {
     SQ_TRY(check_params(p));
     SQ_TRY(check_dims(M, C_out, "gradient codes"));
     SQ_TRY(check_dims(C_in, C_in, "weight codes"));
@@ -275,7 +277,42 @@ sq_status sq_gemm_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* la
     a.out = dX; a.ld_out = ld_dX;
     a.epi_mode = 0;
     a.gs = gscale; a.os = wscale; a.group = group; a.num_groups = cfg.num_groups;
+    if (ranges && !gemm_pipe_ok(a)) {
+        // the register-staged kernel (C_out not a multiple of 64, or operands
+        // past 31-bit offsets) stores dX, then one pass takes its slab maxima
+        if ((M + 31) / 32 > 65535) return fail(SQ_ERR_UNSUPPORTED, "dX ranges support at most 2^21 rows here");
+        SQ_TRY(hip_status(launch_gemm(a, s), "gemm_dgrad"));
+        return hip_status(launch_slab_colmax(dX, M, C_in, ld_dX, ranges, s), "dX ranges");
+    }
+    a.ranges = ranges;
     return hip_status(launch_gemm(a, s), "gemm_dgrad");
+}
+}  // namespace
+
+sq_status sq_gemm_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* layout, const uint8_t* group,
+                        const sq_scale* gscale, const int8_t* wq_t, int64_t ld_w, const sq_scale* wscale, int64_t M,
+                        int64_t C_out, int64_t C_in, const sq_quant_params* p, int32_t* acc, int64_t ld_acc,
+                        float* dX, int64_t ld_dX, void* workspace, size_t workspace_bytes, void* stream) {
+    return gemm_dgrad_impl(q_fold, ld_fold, layout, group, gscale, wq_t, ld_w, wscale, M, C_out, C_in, p, acc, ld_acc,
+                           dX, ld_dX, nullptr, workspace, workspace_bytes, stream);
+}
+
+sq_status sq_gemm_dgrad_range_slabs(int64_t M, int64_t* slabs) {
+    if (!slabs) return fail(SQ_ERR_INVALID_ARGUMENT, "slabs is NULL");
+    if (M < 0 || M >= kMaxRows) return fail(SQ_ERR_INVALID_ARGUMENT, "M out of range");
+    *slabs = (M + 31) / 32;
+    return SQ_OK;
+}
+
+sq_status sq_gemm_dgrad_ranged(const int8_t* q_fold, int64_t ld_fold, const int32_t* layout, const uint8_t* group,
+                               const sq_scale* gscale, const int8_t* wq_t, int64_t ld_w, const sq_scale* wscale,
+                               int64_t M, int64_t C_out, int64_t C_in, const sq_quant_params* p, int32_t* acc,
+                               int64_t ld_acc, float* dX, int64_t ld_dX, uint32_t* dX_ranges, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+    if (!dX) return fail(SQ_ERR_INVALID_ARGUMENT, "dX is NULL (the ranges are taken of dX)");
+    if (!dX_ranges || !aligned(dX_ranges, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "dX_ranges is NULL or misaligned");
+    return gemm_dgrad_impl(q_fold, ld_fold, layout, group, gscale, wq_t, ld_w, wscale, M, C_out, C_in, p, acc, ld_acc,
+                           dX, ld_dX, dX_ranges, workspace, workspace_bytes, stream);
 }
 
 sq_status sq_quantize_channels_workspace_size(int64_t rows, int64_t cols, int32_t axis, size_t* bytes) {

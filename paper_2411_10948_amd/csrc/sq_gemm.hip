@@ -446,7 +446,7 @@ __device__ __forceinline__ void wait_vm() {
 }
 __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0x7F | (0x3 << 14) | (0x0 << 8)); }
 
-template <class T, bool HORNER, bool CONV = false>
+template <class T, bool HORNER, bool CONV = false, bool RANGES = false>
 __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t tiles_m, int64_t tiles_n,
                                                            int64_t k_per_split) {
 #if defined(__HIP_DEVICE_COMPILE__)   // buffer resources exist in the device pass only
@@ -709,10 +709,18 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
             for (int e = 0; e < 4; ++e)
                 cs[j][q][e] = (p.epi_mode == 2 && p.out && !p.part && jj + e < p.Ng) ? col_scale(p, gstep, jj + e) : 0.0f;
         }
+    // RANGES: channel maxima of |out| per 32-row slab (two 16-row fragments;
+    // every wave's rows are whole slabs), bit patterns with the sign cleared
+    static_assert(!RANGES || (T::MF == 16 && T::TM % 32 == 0), "ranges need 16-row fragments and whole slabs");
+    uint32_t rm[RANGES ? T::FN : 1][4];
+#pragma unroll
+    for (int j = 0; j < (RANGES ? T::FN : 1); ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) rm[j][e] = 0u;
 #pragma unroll
     for (int i = 0; i < T::FM; ++i) {
         const int64_t ii = m0 + wm * T::TM + i * T::MF + lane % T::MF;
-        if (ii >= p.Mg) continue;
+        if (ii < p.Mg) {
         float sc = alpha;
         if (p.out && !p.part && p.epi_mode == 1) sc = __fmul_rn(base, pow2f(-(int)p.group[ii]));
 #pragma unroll
@@ -763,8 +771,43 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
                         for (int e = 0; e < 4; ++e)
                             if (jj + e < p.Ng) dst[e] = ff[e];
                     }
+                    if (RANGES) {
+                        const float ff[4] = {f0, f1, f2, f3};
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (jj + e < p.Ng)
+                                rm[RANGES ? j : 0][e] = max(rm[RANGES ? j : 0][e], __float_as_uint(ff[e]) & 0x7FFFFFFFu);
+                    }
                 }
             }
+        }
+        }
+        if (RANGES && (i & 1)) {
+            // end of a 32-row slab: maximum over the 16 lanes of each column
+            // group (same lane / 16), then the group's first lane writes
+            const int64_t slab = (m0 + wm * T::TM) / 32 + i / 2;
+#pragma unroll
+            for (int j = 0; j < (RANGES ? T::FN : 1); ++j)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    uint32_t v = rm[j][e];
+#pragma unroll
+                    for (int o = 1; o < 16; o <<= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, 64));
+                    rm[j][e] = v;
+                }
+            if ((lane & 15) == 0 && slab * 32 < p.Mg) {
+#pragma unroll
+                for (int j = 0; j < (RANGES ? T::FN : 1); ++j) {
+                    const int64_t jj = n0 + wn * T::TN + j * T::MF + (lane / 16) * 4;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (jj + e < p.Ng) p.ranges[slab * p.Ng + jj + e] = rm[j][e];
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < (RANGES ? T::FN : 1); ++j)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) rm[j][e] = 0u;
         }
     }
 #endif
@@ -1203,7 +1246,7 @@ hipError_t launch_cfg(const GemmArgs& a, int splits, int64_t k_per_split, hipStr
     return hipGetLastError();
 }
 
-template <class T, bool HORNER, bool CONV = false>
+template <class T, bool HORNER, bool CONV = false, bool RANGES = false>
 hipError_t launch_pipe(const GemmArgs& a, int splits, int64_t k_per_split, hipStream_t s) {
     const int64_t tiles_m = (a.Mg + T::BM - 1) / T::BM, tiles_n = (a.Ng + T::BN - 1) / T::BN;
     if (tiles_m * tiles_n * splits > 0x7FFFFFFF || splits > 65535) return hipErrorInvalidValue;
@@ -1211,7 +1254,7 @@ hipError_t launch_pipe(const GemmArgs& a, int splits, int64_t k_per_split, hipSt
     // on one XCD); a.splits must equal splits for that decoding
     if (splits > 1 && a.splits != splits) return hipErrorInvalidValue;
     const dim3 grid = splits > 1 ? dim3((unsigned)(tiles_m * tiles_n * splits)) : dim3((unsigned)(tiles_m * tiles_n));
-    hipLaunchKernelGGL((k_gemm_pipe<T, HORNER, CONV>), grid, dim3(T::kThreads), 0, s, a, tiles_m, tiles_n,
+    hipLaunchKernelGGL((k_gemm_pipe<T, HORNER, CONV, RANGES>), grid, dim3(T::kThreads), 0, s, a, tiles_m, tiles_n,
                        k_per_split);
     return hipGetLastError();
 }
@@ -1267,6 +1310,28 @@ Pick pick(const GemmArgs& a) {
 
 }  // namespace
 
+bool gemm_pipe_ok(const GemmArgs& a) { return pipe_ok(a); }
+
+// Channel maxima of |x| per 32-row slab (bit patterns), for products the
+// fused epilogue does not take: one thread per (slab, column), coalesced rows.
+__global__ __launch_bounds__(256) void k_slab_colmax(const float* __restrict__ x, int64_t M, int64_t N, int64_t ld,
+                                                     uint32_t* __restrict__ ranges) {
+    const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x, slab = blockIdx.y;
+    if (c >= N) return;
+    uint32_t mx = 0u;
+    for (int64_t m = slab * 32; m < min(M, slab * 32 + 32); ++m) mx = max(mx, __float_as_uint(x[m * ld + c]) & 0x7FFFFFFFu);
+    ranges[slab * N + c] = mx;
+}
+
+hipError_t launch_slab_colmax(const float* x, int64_t M, int64_t N, int64_t ld, uint32_t* ranges, hipStream_t s) {
+    const int64_t slabs = (M + 31) / 32;
+    if (slabs <= 0 || N <= 0) return hipSuccess;
+    if (slabs > 65535) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_slab_colmax, dim3((unsigned)((N + 255) / 256), (unsigned)slabs), dim3(256), 0, s, x, M, N, ld,
+                       ranges);
+    return hipGetLastError();
+}
+
 // Split-K factor of the weight-gradient product: large tiles with the split
 // that fills the chip where that works (large_splits), else enough smaller
 // tiles for about one block per CU with at least 8 K tiles per split and no
@@ -1304,6 +1369,16 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     const int splits = std::max(1, a.splits);
     const int64_t per = splits > 1 ? (ktiles + splits - 1) / splits : std::max<int64_t>(ktiles, 1);
     if (splits > 1 && (ktiles + per - 1) / per != splits) return hipErrorInvalidValue;   // wgrad_splits() avoids this
+    if (a.ranges) {
+        // dX with its channel maxima (producer-side ranges): pipelined kernel, no split
+        if (!pipe || splits > 1 || !a.out || a.part || a.wg_KH) return hipErrorInvalidValue;
+        if (p == Pick::kLarge)
+            return a.extA ? launch_pipe<PipeLarge, true, false, true>(a, 1, per * 64, s)
+                          : launch_pipe<PipeLarge, false, false, true>(a, 1, per * 64, s);
+        if (p == Pick::kSkinny) return launch_pipe<PipeSkinny, false, false, true>(a, 1, per * 64, s);
+        return a.extA ? launch_pipe<PipeSmall, true, false, true>(a, 1, per * 64, s)
+                      : launch_pipe<PipeSmall, false, false, true>(a, 1, per * 64, s);
+    }
     if (p == Pick::kLarge) {
         if (!pipe) return launch_cfg<CfgLarge>(a, splits, per * 64, s);
         return a.extA ? launch_pipe<PipeLarge, true>(a, splits, per * 64, s)

@@ -138,9 +138,16 @@ struct GemmArgs {
     // shift on a grid of width Wp, a multiple of 16); B has KW C_in rows.
     int wg_KH, wg_KW;
     int64_t wg_Cin, wg_Wp;
+    // with out: max |out| per 32-row slab and column, as bit patterns,
+    // [ceil(Mg / 32), Ng] (producer-side channel ranges of the next quantizer)
+    uint32_t* ranges;
 };
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
+// whether the direct-load pipelined kernel takes the product
+bool gemm_pipe_ok(const GemmArgs& a);
+// max |x| per 32-row slab and column (bit patterns): ranges [ceil(M / 32), N]
+hipError_t launch_slab_colmax(const float* x, int64_t M, int64_t N, int64_t ld, uint32_t* ranges, hipStream_t s);
 hipError_t launch_gather_ext(const int8_t* wq_t, int64_t ld_w, int64_t C_in, const int32_t* layout,
                              int8_t* wext, int64_t ld_ext, int64_t ext_max, hipStream_t s);
 // Conv dgrad: B operand [C_in, ld_bc] in the order of the conv K sequence;

@@ -43,7 +43,7 @@ EXPORTS = (
     "sq_quantize_grad_from_ranges", "sq_l1bn_range_slabs", "sq_l1bn_forward_workspace_size",
     "sq_l1bn_backward_workspace_size", "sq_l1bn_forward", "sq_l1bn_backward",
     "sq_conv_wgrad_layout", "sq_conv_pack_input", "sq_conv_pack_grad", "sq_quantize_grad_conv",
-    "sq_conv_wgrad_workspace_size", "sq_conv_wgrad",
+    "sq_conv_wgrad_workspace_size", "sq_conv_wgrad", "sq_gemm_dgrad_range_slabs", "sq_gemm_dgrad_ranged",
     "sq_status_string", "sq_last_error",
 )
 
@@ -107,6 +107,9 @@ def load() -> ct.CDLL:
         "sq_quantize_grad_from_ranges": [_P, _I64, _I64, _I64, pp, _P, _I64, _P, _I64, _P, _I64, _P, _P, _P, _P,
                                          _SZ, _P],
         "sq_l1bn_range_slabs": [_I64, _I64, ct.POINTER(_I64)],
+        "sq_gemm_dgrad_range_slabs": [_I64, ct.POINTER(_I64)],
+        "sq_gemm_dgrad_ranged": [_P, _I64, _P, _P, _P, _P, _I64, _P, _I64, _I64, _I64, pp, _P, _I64, _P, _I64, _P,
+                                 _P, _SZ, _P],
         "sq_conv_wgrad_layout": [_I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32, ct.c_int32,
                                  ct.POINTER(_I64), ct.POINTER(_I64), ct.POINTER(_I64)],
         "sq_conv_pack_grad": [_P, _I64, _I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32, ct.c_int32,
@@ -301,6 +304,21 @@ def sq_conv_wgrad(q_t, group, gscale, xs, xscale, N, H, W, C_out, C_in, KH, KW, 
     _check("sq_conv_wgrad", load().sq_conv_wgrad(
         _ptr(q_t), _ld(q_t), _ptr(group), _ptr(gscale), _ptr(xs), _ld(xs), _ptr(xscale), N, H, W, C_out, C_in,
         KH, KW, PH, PW, ct.byref(params), _ptr(acc), _ld(acc), _ptr(dW), _ld(dW), ws, nws, _stream(stream)))
+
+
+def sq_gemm_dgrad_range_slabs(M: int) -> int:
+    n = _I64(0)
+    _check("sq_gemm_dgrad_range_slabs", load().sq_gemm_dgrad_range_slabs(M, ct.byref(n)))
+    return n.value
+
+
+def sq_gemm_dgrad_ranged(q_fold, layout, group, gscale, wq_t, wscale, M, C_out, C_in, params, acc, dX, dX_ranges,
+                         workspace, stream=None) -> None:
+    ws, nws = _ws_ptr(workspace)
+    _check("sq_gemm_dgrad_ranged", load().sq_gemm_dgrad_ranged(
+        _ptr(q_fold), _ld(q_fold), _ptr(layout), _ptr(group), _ptr(gscale), _ptr(wq_t), _ld(wq_t), _ptr(wscale), M,
+        C_out, C_in, ct.byref(params), _ptr(acc), _ld(acc), _ptr(dX), _ld(dX), _ptr(dX_ranges), ws, nws,
+        _stream(stream)))
 
 
 def sq_l1bn_range_slabs(M: int, C: int) -> int:
