@@ -280,6 +280,70 @@ def run_l1bn(args, torch, sq):
     return 0
 
 
+def run_chain(args, torch, sq):
+    """Two layers of the Transformer MLP backward in sequence: the
+    down-projection (3072 -> 768) and then the up-projection (768 -> 3072),
+    whose output gradient is the down-projection's input gradient.  With
+    --fused-ranges the down-projection's dgrad also writes the channel ranges
+    of its dX and the up-projection's quantizer takes them instead of reading
+    dX once more for its abs-max; otherwise both quantizers run in full."""
+    from paper_2411_10948_amd import workloads
+    inp = workloads.make_chain_inputs()
+    M, d, f = inp["M"], inp["d_model"], inp["d_ff"]
+    dev = torch.device("cuda:0")
+    p = sq.Params.make(inp["bits"], inp["num_groups"], 0)
+    dY = torch.from_numpy(inp["dY_dn"]).to(dev)
+    wdn_t, wdn_s = sq.quantize_tensor(torch.from_numpy(inp["W_dn"]).to(dev), 8, transpose=True)
+    xdn_t, xdn_s = sq.quantize_tensor(torch.from_numpy(inp["X_dn"]).to(dev), 8, transpose=True)
+    wup_t, wup_s = sq.quantize_tensor(torch.from_numpy(inp["W_up"]).to(dev), 8, transpose=True)
+    xup_t, xup_s = sq.quantize_tensor(torch.from_numpy(inp["X_up"]).to(dev), 8, transpose=True)
+    fused = args.fused_ranges
+    dn = sq.BackwardPlan(M, d, f, p, device=dev, dx_ranges=fused)
+    up = sq.BackwardPlan(M, f, d, p, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        dn.run(dY, wdn_t, wdn_s, xdn_t, xdn_s, stream)
+        if fused:
+            up.quantize_from_ranges(dn.dX, dn.dX_ranges, stream)
+        else:
+            up.quantize(dn.dX, stream)
+        up.dgrad(wup_t, wup_s, stream)
+        up.wgrad(xup_t, xup_s, stream)
+
+    def timed(fn, K):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(K):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / K
+
+    for _ in range(args.warmup):
+        step()
+    ms = timed(step, args.steps)
+    t_qup = timed((lambda: up.quantize_from_ranges(dn.dX, dn.dX_ranges, stream)) if fused
+                  else (lambda: up.quantize(dn.dX, stream)), args.steps)
+    t_dgdn = timed(lambda: dn.dgrad(wdn_t, wdn_s, stream), args.steps)
+    ops = 2 * 4 * M * d * f
+    alg_q = 5 * M * f
+    out = {"metric": "ShiftQuant backward TOPS (quantize+dgrad+wgrad) and % of int8 MFMA peak",
+           "value": ops / (ms * 1e-3) / 1e12, "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "int8", "data": "synthetic",
+           "config": {"workload": "mlp_chain_down_up_768x3072", "step": "chain", "M": M, "d_model": d, "d_ff": f,
+                      "bits": inp["bits"], "num_groups": inp["num_groups"], "rounding": "nearest-even",
+                      "up_proj_ranges": "from the down-projection's dgrad epilogue" if fused else "abs-max pass",
+                      "parallelism": "none"},
+           "breakdown_ms": {"up-projection quantize": t_qup, "down-projection dgrad": t_dgdn},
+           "up_quantize_gbs": alg_q / (t_qup * 1e-3) / 1e9,
+           "up_quantize_frac_hbm": alg_q / (t_qup * 1e-3) / 1e9 / PEAK_HBM_GBS}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -291,7 +355,9 @@ def main(argv=None):
     ap.add_argument("--num-groups", type=int, default=None, help="override the workload's N_G (variant runs)")
     ap.add_argument("--rounding", choices=["rtn", "sr"], default=None,
                     help="override the workload's rounding (variant runs)")
-    ap.add_argument("--step", choices=["backward", "forward", "l1bn"], default="backward",
+    ap.add_argument("--fused-ranges", action="store_true",
+                    help="--step chain: the down-projection's dgrad writes the up-projection quantizer's ranges")
+    ap.add_argument("--step", choices=["backward", "forward", "l1bn", "chain"], default="backward",
                     help="forward: quantize X with ShiftQuant + Y = X W^T (per-output-channel W); "
                          "l1bn: the L1BNQ layer (workloads resnet18_bn_56x56x64, resnet50_bn_14x14x1024, "
                          "transformer_bn_768)")
@@ -319,6 +385,8 @@ def main(argv=None):
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.step == "l1bn":
         return run_l1bn(args, torch, sq)
+    if args.step == "chain":
+        return run_chain(args, torch, sq)
     conv = args.workload in FUSED_CONV
     wl = workloads.WORKLOADS[FUSED_CONV.get(args.workload, args.workload)]
     # parameter variants of the same layer (same tensors, other b / N_G / rounding)

@@ -446,6 +446,17 @@ __device__ __forceinline__ void wait_vm() {
 }
 __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0x7F | (0x3 << 14) | (0x0 << 8)); }
 
+// Maximum over the 16 lanes of a DPP row (lanes 16 r .. 16 r + 15), in every
+// lane of the row: swaps within quads (xor 1, xor 2), then the mirrors of
+// each 8-lane half and of the whole row.  Every lane of the wave must be active.
+__device__ __forceinline__ uint32_t row16_max(uint32_t v) {
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));    // quad_perm [1,0,3,2]
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));    // quad_perm [2,3,0,1]
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));   // row_half_mirror
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false));   // row_mirror
+    return v;
+}
+
 template <class T, bool HORNER, bool CONV = false, bool RANGES = false>
 __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t tiles_m, int64_t tiles_n,
                                                            int64_t k_per_split) {
@@ -789,12 +800,7 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
 #pragma unroll
             for (int j = 0; j < (RANGES ? T::FN : 1); ++j)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    uint32_t v = rm[j][e];
-#pragma unroll
-                    for (int o = 1; o < 16; o <<= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, 64));
-                    rm[j][e] = v;
-                }
+                for (int e = 0; e < 4; ++e) rm[j][e] = row16_max(rm[j][e]);
             if ((lane & 15) == 0 && slab * 32 < p.Mg) {
 #pragma unroll
                 for (int j = 0; j < (RANGES ? T::FN : 1); ++j) {

@@ -685,9 +685,13 @@ class BackwardPlan:
     allocates nothing."""
 
     def __init__(self, M: int, C_out: int, C_in: int, params: Params, device="cuda",
-                 want_acc: bool = False, grouped_dgrad: bool = False):
+                 want_acc: bool = False, grouped_dgrad: bool = False, dx_ranges: bool = False):
         self.M, self.C_out, self.C_in, self.params = M, C_out, C_in, params
         self.grouped_dgrad = grouped_dgrad
+        # dx_ranges: the dgrad also writes the channel ranges of dX (for the
+        # quantizer of the layer below, quantize_from_ranges)
+        self.dX_ranges = (torch.empty((sq_gemm_dgrad_range_slabs(M), C_in), dtype=torch.int32,
+                                      device=torch.device(device)) if dx_ranges else None)
         dev = torch.device(device)
         lay_bytes, min_ld = sq_grad_layout_size(C_out, params)
         self.q_fold = torch.zeros((M, min_ld), dtype=torch.int8, device=dev)
@@ -708,7 +712,15 @@ class BackwardPlan:
         sq_quantize_grad(dY, self.params, self.q_fold, self.q_t, self.group, self.scale, self.layout,
                          self.ws_q, stream)
 
+    def quantize_from_ranges(self, dY, ranges, stream=None):
+        sq_quantize_grad_from_ranges(dY, self.params, ranges, ranges.shape[0], self.q_fold, self.q_t, self.group,
+                                     self.scale, self.layout, self.ws_q, stream)
+
     def dgrad(self, wq_t, wscale, stream=None):
+        if self.dX_ranges is not None:
+            return sq_gemm_dgrad_ranged(self.q_fold, self.layout, self.group, self.scale, wq_t, wscale, self.M,
+                                        self.C_out, self.C_in, self.params, self.acc_dX, self.dX, self.dX_ranges,
+                                        self.ws_d, stream)
         fn = sq_gemm_dgrad_grouped if self.grouped_dgrad else sq_gemm_dgrad
         fn(self.q_fold, self.layout, self.group, self.scale, wq_t, wscale, self.M, self.C_out, self.C_in,
            self.params, self.acc_dX, self.dX, self.ws_d, stream)

@@ -206,3 +206,23 @@ def make_bn_inputs(name: str, *, seed: int = 0) -> dict:
     beta = rp.normal(0.0, 0.2, w.C).astype(np.float32)
     dy = make_grad(w.M, w.C, seed=seed, index=w.index + 100, dist="normal", sigma_s=1.0)
     return {"X": X, "gamma": gamma, "beta": beta, "dy": dy, "M": w.M, "C": w.C}
+
+
+# ---------------------------------------------------------------------------
+# Two-layer chain of the Transformer MLP: the down-projection (3072 -> 768)
+# backward produces, as its input gradient, the output gradient of the
+# up-projection (768 -> 3072, the mlp_up_768x3072 workload).  The chain's own
+# tensors: dY of the down-projection [16384, 768] (the MLP recipe: Student-t(3)
+# times LogNormal(0, 1.5) channel scales), its weight W_dn [768, 3072] ~
+# N(0, 0.02) and its input X_dn [16384, 3072] ~ N(0, 1) (tensor ids 8, 9, 10).
+# ---------------------------------------------------------------------------
+def make_chain_inputs(seed: int = 0) -> dict:
+    up = make_inputs("mlp_up_768x3072", seed=seed)
+    M = up["M"]
+    wl = up["workload"]
+    dy_dn = make_grad(M, wl.C_in, seed=seed, index=wl.index + 200, dist="student_t3", sigma_s=1.5,
+                      outlier_frac=0.0)
+    w_dn = (_rng(seed, wl.index, 9).standard_normal((wl.C_in, wl.C_out)) * 0.02).astype(np.float32)
+    x_dn = _rng(seed, wl.index, 10).standard_normal((M, wl.C_out)).astype(np.float32)
+    return {"dY_dn": dy_dn, "W_dn": w_dn, "X_dn": x_dn, "W_up": up["W"], "X_up": up["X"], "M": M,
+            "d_model": wl.C_in, "d_ff": wl.C_out, "bits": wl.bits, "num_groups": wl.num_groups}
