@@ -915,14 +915,21 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
                     const uint32_t* src = &tq[ch * TW + 4 * part];
                     int8_t* row = q_t + c * ld_t;
                     if (pg.Wo % 8 == 0 && m + 16 <= M) {
-                        // 8-pixel halves never cross an image row
-#pragma unroll
-                        for (int h = 0; h < 2; ++h) {
-                            const uint32_t mh = (uint32_t)(m + 8 * h);
-                            const uint32_t n = mh / pg.HoWo, rem = mh - n * pg.HoWo, oh = rem / pg.Wo;
-                            const uint32_t ow = rem - oh * pg.Wo;
-                            const int64_t d = (int64_t)n * pg.HpWp + (int64_t)oh * pg.Wp + ow;
-                            *reinterpret_cast<uint2*>(row + d) = make_uint2(src[2 * h], src[2 * h + 1]);
+                        const uint32_t m0 = (uint32_t)m;
+                        const uint32_t n = m0 / pg.HoWo, rem = m0 - n * pg.HoWo, oh = rem / pg.Wo;
+                        const uint32_t ow = rem - oh * pg.Wo;
+                        const int64_t d = (int64_t)n * pg.HpWp + (int64_t)oh * pg.Wp + ow;
+                        if (ow + 16 <= pg.Wo && (d & 15) == 0) {
+                            // the 16 pixels lie in one image row: one 16-byte store
+                            *reinterpret_cast<uint4*>(row + d) = make_uint4(src[0], src[1], src[2], src[3]);
+                        } else {
+                            // 8-pixel halves never cross an image row
+                            *reinterpret_cast<uint2*>(row + d) = make_uint2(src[0], src[1]);
+                            const uint32_t mh = m0 + 8;
+                            const uint32_t n1 = mh / pg.HoWo, rem1 = mh - n1 * pg.HoWo, oh1 = rem1 / pg.Wo;
+                            const uint32_t ow1 = rem1 - oh1 * pg.Wo;
+                            const int64_t d1 = (int64_t)n1 * pg.HpWp + (int64_t)oh1 * pg.Wp + ow1;
+                            *reinterpret_cast<uint2*>(row + d1) = make_uint2(src[2], src[3]);
                         }
                     } else {
                         for (int i = 0; i < 16 && m + i < M; ++i) {
