@@ -983,9 +983,11 @@ __global__ __launch_bounds__(64 * kHaloWaves) void k_conv_halo(GemmArgs p) {
 // Streaming variant of the same-size convolution input gradient for one
 // 64-column K chunk (C_out <= 64, every shift in one window) and C_in <= 64.
 // Each block owns a contiguous range of input pixels and walks it in steps of
-// 64 rows.  The weights of every tap (rows (r, s, ci) of W^T, read straight
-// from wq_t) stay in LDS; the rows of q_fold flow through an LDS ring of
-// 64-row chunks, loaded kStreamPF steps ahead, and a step's outputs go out
+// 128 rows (a wave takes rows 16 w .. and 64 + 16 w .. of the step, so each
+// weight fragment read feeds two MFMAs).  The weights of every tap (rows
+// (r, s, ci) of W^T, read straight from wq_t) stay in LDS; the rows of q_fold
+// flow through an LDS ring of 64-row chunks, two per step, loaded kStreamPF
+// steps ahead, and a step's outputs go out
 // with buffer stores while the next steps compute, so the output stream (the
 // bulk of the traffic) does not wait for loads.  A wave's loads and stores
 // complete in order on gfx9, so the wait for a chunk also covers the stores
@@ -995,7 +997,7 @@ __global__ __launch_bounds__(64 * kHaloWaves) void k_conv_halo(GemmArgs p) {
 // Code columns >= C_out (unwritten padding of q_fold) are cleared in the
 // operand registers.
 // ---------------------------------------------------------------------------
-constexpr int kStreamRing = 8, kStreamPF = 4, kStreamNW = 3;   // ring chunks, prefetch, chunks per step
+constexpr int kStreamRing = 8, kStreamPF = 2, kStreamNW = 4;   // ring chunks, prefetch steps, chunks per step
 constexpr int kStreamBlocks = 512;
 
 // Hide a value from the optimizer, so that a memory instruction whose lanes
@@ -1007,8 +1009,8 @@ template <bool ACC>
 __global__ __launch_bounds__(256) void k_conv_stream(GemmArgs p, int64_t rows_per_block) {
 #if defined(__HIP_DEVICE_COMPILE__)
     constexpr int BK = 64, kRing = kStreamRing * 64 * BK;
-    constexpr int NS = ACC ? 8 : 4;   // stores per lane and step
-    static_assert(kStreamNW + kStreamPF <= kStreamRing && kStreamPF * (1 + NS) <= 63, "ring / vmcnt range");
+    constexpr int NS = ACC ? 16 : 8;   // stores per lane and step
+    static_assert(kStreamNW + 2 * kStreamPF <= kStreamRing && 2 * NS + 4 <= 63, "ring / vmcnt range");
     __shared__ __attribute__((aligned(1024))) int8_t smem[kRing + kHaloMaxTaps * 64 * BK];
     using MF = Mfma<16>;
     const int tid = threadIdx.x, lane = tid & 63;
@@ -1017,7 +1019,7 @@ __global__ __launch_bounds__(256) void k_conv_stream(GemmArgs p, int64_t rows_pe
     const int E = p.cv_PH * W + p.cv_PW;
     const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
     const int64_t r_end = min(p.Mg, r0 + rows_per_block);
-    const int steps = (int)((r_end - r0 + 63) / 64);
+    const int steps = (int)((r_end - r0 + 127) / 128);
     const int lr = lane >> 2, lrow = lane % 16, lc = lane / 16;
     constexpr int kRsrcFlags = 0x00020000;
     auto rsrc = [&](const void* base, int64_t bytes) {
@@ -1058,64 +1060,84 @@ __global__ __launch_bounds__(256) void k_conv_stream(GemmArgs p, int64_t rows_pe
         opaque(off);   // one load instruction whatever the lanes' offsets
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void_t*)(smem + (slot_row - lr) * BK), 16, off, 0, 0, 0);
     };
+    // chunks 0 .. 2 PF + NW - 3 before the first step; step k loads chunks
+    // 2 k + NW + 2 PF - 2 and + 1 (past the window: loads of nothing, still counted)
 #pragma unroll
-    for (int j = 0; j < kStreamNW + kStreamPF - 1; ++j) load_chunk(j);
+    for (int j = 0; j < kStreamNW + 2 * kStreamPF - 2; ++j) load_chunk(j);
 
     const int kvalid = (int)min((int64_t)16, max((int64_t)0, p.K_used - 16 * lc));   // code bytes < C_out
     for (int k = 0; k < steps; ++k) {
-        load_chunk(k + kStreamNW - 1 + kStreamPF);
-        // chunk k + NW - 1 (issued kStreamPF steps back) has landed once only
-        // the younger operations remain: later chunks and the stores since
-        if (k == 0) wait_vm<kStreamPF>();
-        else if (k == 1) wait_vm<kStreamPF + NS>();
-        else if (k == 2) wait_vm<kStreamPF + 2 * NS>();
-        else if (k == 3) wait_vm<kStreamPF + 3 * NS>();
-        else wait_vm<kStreamPF + 4 * NS>();
+        load_chunk(2 * k + kStreamNW + 2 * kStreamPF - 2);
+        load_chunk(2 * k + kStreamNW + 2 * kStreamPF - 1);
+        // chunk 2 k + NW - 1, the last this step reads, was issued PF steps
+        // back (the prologue's last for k < PF); it has landed once only the
+        // younger operations remain: at most two loads per step since, and
+        // the stores of the steps in between
+        if (k == 0) wait_vm<4>();
+        else if (k == 1) wait_vm<NS + 4>();
+        else wait_vm<2 * NS + 4>();
         __builtin_amdgcn_s_barrier();   // a plain barrier: the stores stay in flight
 
-        const int64_t pix = r0 + 64 * k + wv * 16 + lrow;   // this lane's output row
-        const int hw = (int)(min(pix, p.Mg - 1) % ((int64_t)H * W));
-        const int ih = hw / W, iw = hw - (hw / W) * W;
-        v4i acc[4];
+        int64_t pix[2];
+        int ih[2], iw[2];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[j] = v4i{0, 0, 0, 0};
+        for (int h = 0; h < 2; ++h) {
+            pix[h] = r0 + 128 * k + 64 * h + wv * 16 + lrow;   // this lane's output rows
+            const int hw = (int)(min(pix[h], p.Mg - 1) % ((int64_t)H * W));
+            ih[h] = hw / W;
+            iw[h] = hw - ih[h] * W;
+        }
+        v4i acc[2][4];
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[h][j] = v4i{0, 0, 0, 0};
         for (int tau = 0, tr = 0, ts = 0; tau < taps; ++tau) {
             const int d = (p.cv_PH - tr) * W + (p.cv_PW - ts);
-            const int w = (64 * k + wv * 16 + lrow + E + d) & (kStreamRing * 64 - 1);
-            v4i fa = *reinterpret_cast<const v4i*>(&smem[w * BK + 16 * (lc ^ swz(w))]);
-            const int oh = ih + p.cv_PH - tr, ow = iw + p.cv_PW - ts;
-            if (!((unsigned)oh < (unsigned)H && (unsigned)ow < (unsigned)W)) fa = v4i{0, 0, 0, 0};
-            if (kvalid < 16) {
-                const uint4 m = mask_tail(make_uint4(fa[0], fa[1], fa[2], fa[3]), kvalid);
-                fa = v4i{(int)m.x, (int)m.y, (int)m.z, (int)m.w};
+            v4i fa[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int w = (128 * k + 64 * h + wv * 16 + lrow + E + d) & (kStreamRing * 64 - 1);
+                fa[h] = *reinterpret_cast<const v4i*>(&smem[w * BK + 16 * (lc ^ swz(w))]);
+                const int oh = ih[h] + p.cv_PH - tr, ow = iw[h] + p.cv_PW - ts;
+                if (!((unsigned)oh < (unsigned)H && (unsigned)ow < (unsigned)W)) fa[h] = v4i{0, 0, 0, 0};
+                if (kvalid < 16) {
+                    const uint4 m = mask_tail(make_uint4(fa[h][0], fa[h][1], fa[h][2], fa[h][3]), kvalid);
+                    fa[h] = v4i{(int)m.x, (int)m.y, (int)m.z, (int)m.w};
+                }
             }
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int r = tau * 64 + j * 16 + lrow;
                 const v4i fb = *reinterpret_cast<const v4i*>(&smem[kRing + r * BK + 16 * (lc ^ swz(r))]);
-                acc[j] = MF::run(fb, fa, acc[j]);
+#pragma unroll
+                for (int h = 0; h < 2; ++h) acc[h][j] = MF::run(fb, fa[h], acc[h][j]);
             }
             if (++ts == KW) { ts = 0; ++tr; }
         }
-        // NS / 4 stores per column group: the fp32 output (a NULL output has
-        // an empty range) and, with ACC, the int32 accumulator
-        const bool row_ok = pix < r_end;
+        // NS / 2 stores per row half: the fp32 output (a NULL output has an
+        // empty range) and, with ACC, the int32 accumulator
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int col = j * 16 + lc * 4;
-            const bool ok = row_ok && col < p.Ng;
-            const int v0 = acc[j][0] << fsh, v1 = acc[j][1] << fsh, v2 = acc[j][2] << fsh, v3 = acc[j][3] << fsh;
-            typedef unsigned u4 __attribute__((ext_vector_type(4)));
-            const u4 fo = {__float_as_uint(__fmul_rn((float)v0, alpha)), __float_as_uint(__fmul_rn((float)v1, alpha)),
-                           __float_as_uint(__fmul_rn((float)v2, alpha)), __float_as_uint(__fmul_rn((float)v3, alpha))};
-            int oo = ok ? (int)((pix * p.ld_out + col) * 4) : (int)0x80000000;
-            opaque(oo);
-            __builtin_amdgcn_raw_buffer_store_b128(fo, rO, oo, 0, 0);
-            if constexpr (ACC) {
-                const u4 io = {(unsigned)v0, (unsigned)v1, (unsigned)v2, (unsigned)v3};
-                int oc = ok ? (int)((pix * p.ld_acc + col) * 4) : (int)0x80000000;
-                opaque(oc);
-                __builtin_amdgcn_raw_buffer_store_b128(io, rC, oc, 0, 0);
+        for (int h = 0; h < 2; ++h) {
+            const bool row_ok = pix[h] < r_end;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int col = j * 16 + lc * 4;
+                const bool ok = row_ok && col < p.Ng;
+                const int v0 = acc[h][j][0] << fsh, v1 = acc[h][j][1] << fsh;
+                const int v2 = acc[h][j][2] << fsh, v3 = acc[h][j][3] << fsh;
+                typedef unsigned u4 __attribute__((ext_vector_type(4)));
+                const u4 fo = {__float_as_uint(__fmul_rn((float)v0, alpha)), __float_as_uint(__fmul_rn((float)v1, alpha)),
+                               __float_as_uint(__fmul_rn((float)v2, alpha)), __float_as_uint(__fmul_rn((float)v3, alpha))};
+                int oo = ok ? (int)((pix[h] * p.ld_out + col) * 4) : (int)0x80000000;
+                opaque(oo);
+                __builtin_amdgcn_raw_buffer_store_b128(fo, rO, oo, 0, 0);
+                if constexpr (ACC) {
+                    const u4 io = {(unsigned)v0, (unsigned)v1, (unsigned)v2, (unsigned)v3};
+                    int oc = ok ? (int)((pix[h] * p.ld_acc + col) * 4) : (int)0x80000000;
+                    opaque(oc);
+                    __builtin_amdgcn_raw_buffer_store_b128(io, rC, oc, 0, 0);
+                }
             }
         }
         __builtin_amdgcn_s_barrier();   // the ring slots of this step may be refilled
@@ -1489,8 +1511,8 @@ hipError_t launch_conv_dgrad(const GemmArgs& a0, int8_t* bc, int64_t ld_bc, hipS
     };
     if (same && !a0.extA && a0.K == 64 && a0.taps <= kHaloMaxTaps && (int64_t)a0.cv_PH * a0.cv_W + a0.cv_PW <= 64 &&
         a0.Ng <= 64 && a0.Ng % 4 == 0 && small_out(a0.out, a0.Mg, a0.ld_out) && small_out(a0.acc, a0.Mg, a0.ld_acc)) {
-        const int64_t blocks = std::min<int64_t>(kStreamBlocks, (a0.Mg + 63) / 64);
-        const int64_t rows = (a0.Mg + blocks - 1) / blocks;
+        // whole 128-row steps per block, at most kStreamBlocks blocks
+        const int64_t rows = round_up((a0.Mg + kStreamBlocks - 1) / kStreamBlocks, 128);
         const dim3 grid((unsigned)((a0.Mg + rows - 1) / rows));
         if (a0.acc) hipLaunchKernelGGL(k_conv_stream<true>, grid, dim3(256), 0, s, a0, rows);
         else hipLaunchKernelGGL(k_conv_stream<false>, grid, dim3(256), 0, s, a0, rows);
