@@ -194,3 +194,33 @@ def test_quantize_from_ranges_validation_no_launch(sq):
                                           fake, fake, 4096, None) == 1
     assert L.sq_quantize_grad_from_ranges(fake, 8, 8, 8, ct.byref(p), fake, 1, fake, 16, fake, 16, fake, fake,
                                           fake, fake, 16, None) == 4
+
+
+def test_conv_wgrad_and_ranged_dgrad_validation_no_launch(sq):
+    L = _raw(sq)
+    fake = ct.c_void_p(0x100000)
+    p = sq.Params.make(4, 4, 0)
+    rows, ld, qld = ct.c_int64(0), ct.c_int64(0), ct.c_int64(0)
+    # padded grid of the ResNet-18 layer: 58 rows x 64 columns per image
+    assert L.sq_conv_wgrad_layout(64, 56, 56, 64, 3, 3, 1, 1, ct.byref(rows), ct.byref(ld), ct.byref(qld)) == 0
+    assert rows.value == 3 * 64 and qld.value == 64 * 58 * 64 and ld.value == qld.value + 2 * 64
+    # padding >= window, window larger than the input
+    assert L.sq_conv_wgrad_layout(1, 5, 5, 8, 3, 3, 3, 1, ct.byref(rows), ct.byref(ld), ct.byref(qld)) == 1
+    assert L.sq_conv_wgrad_layout(1, 1, 5, 8, 3, 3, 0, 1, ct.byref(rows), ct.byref(ld), ct.byref(qld)) == 1
+    nb = ct.c_size_t(0)
+    assert L.sq_conv_wgrad_workspace_size(64, 56, 56, 64, 64, 3, 3, 1, 1, ct.byref(p), ct.byref(nb)) == 0
+    # wrong ld of the packed input, NULL outputs
+    assert L.sq_conv_wgrad(fake, qld.value, fake, fake, fake, ld.value + 16, fake, 64, 56, 56, 64, 64, 3, 3, 1, 1,
+                           ct.byref(p), fake, 576, fake, 576, fake, 1 << 30, None) == 1
+    assert L.sq_conv_wgrad(fake, qld.value, fake, fake, fake, ld.value, fake, 64, 56, 56, 64, 64, 3, 3, 1, 1,
+                           ct.byref(p), None, 0, None, 0, fake, 1 << 30, None) == 1
+    # quantize onto the padded grid: ld of the padded codes too small
+    assert L.sq_quantize_grad_conv(fake, 2, 8, 8, 64, 64, 3, 3, 1, 1, ct.byref(p), fake, 64, fake, 64, fake, fake,
+                                   fake, fake, 1 << 20, None) == 1
+    # ranged dgrad: slab count and required dX
+    n = ct.c_int64(0)
+    assert L.sq_gemm_dgrad_range_slabs(1000, ct.byref(n)) == 0 and n.value == 32
+    assert L.sq_gemm_dgrad_ranged(fake, 64, fake, fake, fake, fake, 64, fake, 64, 64, 64, ct.byref(p), None, 0,
+                                  None, 64, fake, fake, 0, None) == 1
+    assert L.sq_gemm_dgrad_ranged(fake, 64, fake, fake, fake, fake, 64, fake, 64, 64, 64, ct.byref(p), None, 0,
+                                  fake, 64, None, fake, 0, None) == 1
