@@ -437,19 +437,18 @@ using PipeNarrow = PipeCfg<256, 64, 4, 1, 16, 4>;   // at most 64 output columns
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 // chunk swizzle of a 64-byte LDS row (conflict-free for 8- and 16-lane phases)
-__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 2)) & 3; }
+[[maybe_unused]] __device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 2)) & 3; }
 
 // s_waitcnt vmcnt(n) leaving the other counters unconstrained (gfx9 encoding)
 template <int N>
 __device__ __forceinline__ void wait_vm() {
     __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
-__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0x7F | (0x3 << 14) | (0x0 << 8)); }
 
 // Maximum over the 16 lanes of a DPP row (lanes 16 r .. 16 r + 15), in every
 // lane of the row: swaps within quads (xor 1, xor 2), then the mirrors of
 // each 8-lane half and of the whole row.  Every lane of the wave must be active.
-__device__ __forceinline__ uint32_t row16_max(uint32_t v) {
+[[maybe_unused]] __device__ __forceinline__ uint32_t row16_max(uint32_t v) {
     v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));    // quad_perm [1,0,3,2]
     v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));    // quad_perm [2,3,0,1]
     v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));   // row_half_mirror
@@ -997,7 +996,7 @@ __global__ __launch_bounds__(64 * kHaloWaves) void k_conv_halo(GemmArgs p) {
 // Code columns >= C_out (unwritten padding of q_fold) are cleared in the
 // operand registers.
 // ---------------------------------------------------------------------------
-constexpr int kStreamRing = 8, kStreamPF = 2, kStreamNW = 4;   // ring chunks, prefetch steps, chunks per step
+[[maybe_unused]] constexpr int kStreamRing = 8, kStreamPF = 2, kStreamNW = 4;   // ring chunks, prefetch steps, chunks per step
 constexpr int kStreamBlocks = 512;
 
 // Hide a value from the optimizer, so that a memory instruction whose lanes

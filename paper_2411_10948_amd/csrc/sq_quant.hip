@@ -189,28 +189,6 @@ __device__ uint32_t block_max_u32(uint32_t v, uint32_t* sh) {
     return v;
 }
 
-// Exclusive prefix sum of v over the block (thread order), plus the total.
-__device__ int block_excl_scan(int v, int* sh, int* total) {
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    int x = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(x, o, 64);
-        if (lane >= o) x += y;
-    }
-    __syncthreads();
-    if (lane == 63) sh[w] = x;
-    __syncthreads();
-    int base = 0, tot = 0;
-    for (int i = 0; i < nw; ++i) {
-        if (i < w) base += sh[i];
-        tot += sh[i];
-    }
-    __syncthreads();
-    *total = tot;
-    return base + x - v;
-}
-
 // Second level for many channels: rbits[c] = max over slabs, and the block's
 // maximum in bmax[blockIdx.x].
 constexpr int kRedThreads = 256;
