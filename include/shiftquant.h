@@ -469,7 +469,7 @@ sq_status sq_quantize_grad_from_ranges(const float* dY, int64_t M, int64_t C_out
 
 /* ---------------------------------------------------------------------------
  * Fully-quantized L1 batch normalization (L1BNQ), Sec. 4 (Fig. l1bnq) and
- * App. E.1 / E.2: input features, statistics and parameters are quantized,
+ * App. C.1 / C.2: input features, statistics and parameters are quantized,
  * and the normalization divides by the L1 deviation instead of the standard
  * deviation.
  *
@@ -517,7 +517,7 @@ sq_status sq_l1bn_backward_workspace_size(int64_t M, int64_t C, const sq_quant_p
 /* ---------------------------------------------------------------------------
  * sq_l1bn_forward -- L1BNQ forward over a batch (training statistics).
  *   y[m, c] = fl(fl(kappa_c (q[m, c] - m_c)) + beta^q_c),
- * i.e. gamma^q (x^q - mu^q) / sigma^q + beta^q with x^q = s_x q (App. E.2's
+ * i.e. gamma^q (x^q - mu^q) / sigma^q + beta^q with x^q = s_x q (App. C.2's
  * normalization with quantized statistics); with A_max = 0, y = beta^q.
  * Inputs : xq [M, ld_x] int8, the 8-bit per-tensor codes of the layer input
  *          (sq_quantize_tensor, bits 8), 16-byte aligned, ld_x % 16 == 0;
@@ -537,7 +537,7 @@ sq_status sq_l1bn_forward(const int8_t* xq, int64_t M, int64_t C, int64_t ld_x, 
  * sq_l1bn_backward -- L1BNQ backward.
  * The incoming gradient dy is quantized with ShiftQuant (as sq_quantize_grad
  * with params p; codes qg, groups g_c, channel steps delta_c = step 2^-g_c);
- * the L1 normalization is differentiated exactly (App. E.1 with
+ * the L1 normalization is differentiated exactly (App. C.1 with
  * sigma = mean |x - mu|, which brings in s = sgn(x - mu)), the quantizers of
  * mu and sigma passed straight through:
  *   dx = (gamma^q / sigma^q)(g - mean g - mean(g xhat)(s - mean s)).

@@ -308,7 +308,7 @@ def backward(dY, W, X, bits, num_groups, round_mode=0, seed=0, offset=0,
 
 
 def l1bn_forward(xq: np.ndarray, x_step: float, gamma: np.ndarray, beta: np.ndarray) -> dict:
-    """L1BNQ forward (Sec. 4, App. E) of 8-bit codes xq [M, C] with step
+    """L1BNQ forward (Sec. 4, App. C) of 8-bit codes xq [M, C] with step
     x_step: y fp32 [M, C] and the per-channel state (mu / sigma codes, sign
     and deviation sums, quantized gamma / beta, kappa) plus dev_max."""
     xq = _c(xq, np.int8)

@@ -437,7 +437,7 @@ void sqo_dequant_wgrad(const int32_t* B, int64_t n_rows, int64_t C_in, const uin
 
 /* ---------------------------------------------------------------------------
  * Fully-quantized L1 batch normalization (L1BNQ), Sec. 4 (Fig. l1bnq) and
- * App. E.  The paper draws the layer as a figure and states only the
+ * App. C.  The paper draws the layer as a figure and states only the
  * normalization equations, so this follows two readings:
  *
  *  R16 forward.  The layer's input is the 8-bit per-tensor code q of x (step
@@ -445,17 +445,17 @@ void sqo_dequant_wgrad(const int32_t* B, int64_t n_rows, int64_t C_in, const uin
  *      The mean is quantized onto the input's own grid,
  *        m_c = round_half_even(S_c / M),  S_c = sum_m q[m, c],
  *      so x - mu^q = s_x (q - m_c) exactly.  sigma is the L1 deviation
- *      (App. E.1) taken as a mean, sigma_c = s_x A_c / M with
+ *      (App. C.1) taken as a mean, sigma_c = s_x A_c / M with
  *      A_c = sum_m |q - m_c|, and is quantized per tensor to 8 bits under the
  *      step max_c sigma_c / 127:
  *        k_c = max(1, round_half_even(127 A_c / A_max)),  A_max = max_c A_c,
  *      (s_x and M cancel in the ratio; the smallest code is kept at 1 so the
- *      denominator of the quantized normalization of App. E.2 is never 0).
+ *      denominator of the quantized normalization of App. C.2 is never 0).
  *      gamma and beta are quantized per tensor to 8 bits like W and X.  Then
  *        kappa_c = fl32(gamma^q_c * 127 M / (A_max k_c))   (binary64),
  *        y = fl(fl(kappa_c * (q - m_c)) + beta^q_c).
  *      A_max = 0 (every channel constant): kappa = 0, k = 0, y = beta^q.
- *  R17 backward.  The derivative of the L1 normalization (App. E.1's
+ *  R17 backward.  The derivative of the L1 normalization (App. C.1's
  *      derivation with sigma = mean |x - mu|, which brings in the signs
  *      s = sgn(x - mu)), the quantizers of mu and sigma passed straight
  *      through:  dx = (gamma / sigma)(g - mean g - mean(g xhat)(s - mean s)).

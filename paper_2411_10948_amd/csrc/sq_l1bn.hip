@@ -1,5 +1,5 @@
 // Fully-quantized L1 batch normalization (L1BNQ), Sec. 4 (Fig. l1bnq) and
-// App. E: forward and backward over 8-bit input codes [M, C] (M = N*H*W rows,
+// App. C: forward and backward over 8-bit input codes [M, C] (M = N*H*W rows,
 // channels contiguous).
 //
 // Every statistic is an integer sum over a channel's column, so the kernels

@@ -1,4 +1,4 @@
-"""Parity of the HIP L1BNQ layer (Sec. 4, App. E) and of the quantizer fed by
+"""Parity of the HIP L1BNQ layer (Sec. 4, App. C) and of the quantizer fed by
 producer-side channel ranges with the CPU oracle, through the C-ABI.
 
 Integer state (mean / sigma codes, sign and deviation sums, groups, scale

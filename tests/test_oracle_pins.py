@@ -598,7 +598,7 @@ def test_forward_equals_dequantized_product(bits, ng):
 
 
 # --------------------------------------------------------------------------
-# Fully-quantized L1 batch normalization (Sec. 4, App. E)
+# Fully-quantized L1 batch normalization (Sec. 4, App. C)
 # --------------------------------------------------------------------------
 def _l1bn_exact_codes(rng, C, triplets=64, unit=30):
     """8-bit codes [3 * triplets, C] whose L1BNQ statistics are exact: every
@@ -629,7 +629,7 @@ def _l1bn_exact_codes(rng, C, triplets=64, unit=30):
 
 
 def _l1bn_textbook(x, gamma, beta):
-    """L1 batch normalization in float64 with exact statistics (App. E.1 with
+    """L1 batch normalization in float64 with exact statistics (App. C.1 with
     sigma the mean L1 deviation)."""
     mu = x.mean(axis=0)
     sigma = np.abs(x - mu).mean(axis=0)
@@ -644,7 +644,7 @@ def test_l1bn_forward_matches_textbook_when_statistics_are_exact():
     gamma = rng.normal(1.0, 0.3, C).astype(np.float32)
     beta = rng.normal(0.0, 0.5, C).astype(np.float32)
     f = oracle.l1bn_forward(q, x_step, gamma, beta)
-    # quantized parameters are the per-tensor 8-bit quantizer (App. E: every
+    # quantized parameters are the per-tensor 8-bit quantizer (App. C: every
     # parameter of the layer is quantized)
     for name, v in (("gamma_q", gamma), ("beta_q", beta)):
         codes, sc = oracle.quantize_tensor(v[None, :], 8)
