@@ -370,8 +370,8 @@ def main(argv=None):
                     help="run one 256 MiB device-to-device copy first (reference for HBM byte counters)")
     args = ap.parse_args(argv)
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the ShiftQuant path is single-GPU, see DESIGN.md for how it would shard)", file=sys.stderr)
+        print(f"bench.py: measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the ShiftQuant path runs on one GPU; sharding over tokens is not built)", file=sys.stderr)
         return 2
 
     import torch
