@@ -47,7 +47,7 @@ typedef enum {
     SQ_OK = 0,
     SQ_ERR_INVALID_ARGUMENT = 1,   /* null pointer, bad size, stride or alignment  */
     SQ_ERR_OVERFLOW_RISK = 2,      /* the worst-case int32 accumulator would overflow */
-    SQ_ERR_UNSUPPORTED = 3,        /* valid request outside what this build supports */
+    SQ_ERR_UNSUPPORTED = 3,        /* valid request outside what the library supports */
     SQ_ERR_WORKSPACE_TOO_SMALL = 4,
     SQ_ERR_HIP = 5                 /* a HIP runtime call or kernel launch failed     */
 } sq_status;
