@@ -29,7 +29,8 @@ DEFAULT_WORKLOAD = "resnet18_conv3x3_fused"
 # conv dgrad (dX itself, NHWC, instead of the 9x larger im2col'd dX_col)
 FUSED_CONV = {"resnet18_conv3x3_fused": "resnet18_conv3x3"}
 KERNEL_SOURCES = ["paper_2411_10948_amd/csrc/sq_gemm.hip", "paper_2411_10948_amd/csrc/sq_quant.hip",
-                  "paper_2411_10948_amd/csrc/sq_internal.h", "paper_2411_10948_amd/csrc/sq_abi.hip"]
+                  "paper_2411_10948_amd/csrc/sq_internal.h", "paper_2411_10948_amd/csrc/sq_abi.hip",
+                  "paper_2411_10948_amd/build.py"]   # the compiler flags shape the kernels too
 
 
 def kernel_source_hash() -> str:

@@ -27,6 +27,10 @@ HIPCC_FLAGS = [
     "-fno-gpu-flush-denormals-to-zero",
     # never emit packed fp32 instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in VGPRs: with the accumulator-register form the
+    # compiler copied every accumulator into and out of AGPRs around each
+    # MFMA (four copies per 16x16x64 instruction in the streaming kernels)
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-mcode-object-version=5",
     "-Wall",
     # every symbol resolved at link time (a kernel whose host stub went

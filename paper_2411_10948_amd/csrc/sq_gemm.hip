@@ -994,7 +994,9 @@ __global__ __launch_bounds__(64 * kHaloWaves) void k_conv_halo(GemmArgs p) {
 // step (rows outside the tensor or the block take offsets past the end of the
 // buffer, which the range check drops), which keeps the vmcnt waits exact.
 // Code columns >= C_out (unwritten padding of q_fold) are cleared in the
-// operand registers.
+// operand registers (FULLK: all 64 columns hold codes, nothing to clear).
+// Taps that fall outside the image read a 16-byte zero slot of LDS instead
+// of their ring row.
 // ---------------------------------------------------------------------------
 [[maybe_unused]] constexpr int kStreamRing = 8, kStreamPF = 2, kStreamNW = 4;   // ring chunks, prefetch steps, chunks per step
 constexpr int kStreamBlocks = 512;
@@ -1004,16 +1006,19 @@ constexpr int kStreamBlocks = 512;
 template <class T>
 __device__ __forceinline__ void opaque(T& v) { asm volatile("" : "+v"(v)); }
 
-template <bool ACC>
+template <bool ACC, bool FULLK>
 __global__ __launch_bounds__(256) void k_conv_stream(GemmArgs p, int64_t rows_per_block) {
 #if defined(__HIP_DEVICE_COMPILE__)
     constexpr int BK = 64, kRing = kStreamRing * 64 * BK;
+    constexpr int kZero = kRing + kHaloMaxTaps * 64 * BK;   // 16 zero bytes
     constexpr int NS = ACC ? 16 : 8;   // stores per lane and step
     static_assert(kStreamNW + 2 * kStreamPF <= kStreamRing && 2 * NS + 4 <= 63, "ring / vmcnt range");
-    __shared__ __attribute__((aligned(1024))) int8_t smem[kRing + kHaloMaxTaps * 64 * BK];
+    __shared__ __attribute__((aligned(1024))) int8_t smem[kZero + 16];
     using MF = Mfma<16>;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    if (tid == 0) *reinterpret_cast<uint4*>(smem + kZero) = make_uint4(0u, 0u, 0u, 0u);
+    __syncthreads();
     const int taps = p.taps, KW = p.cv_KW, H = (int)p.cv_H, W = (int)p.cv_W;
     const int E = p.cv_PH * W + p.cv_PW;
     const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
@@ -1097,10 +1102,10 @@ __global__ __launch_bounds__(256) void k_conv_stream(GemmArgs p, int64_t rows_pe
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int w = (128 * k + 64 * h + wv * 16 + lrow + E + d) & (kStreamRing * 64 - 1);
-                fa[h] = *reinterpret_cast<const v4i*>(&smem[w * BK + 16 * (lc ^ swz(w))]);
                 const int oh = ih[h] + p.cv_PH - tr, ow = iw[h] + p.cv_PW - ts;
-                if (!((unsigned)oh < (unsigned)H && (unsigned)ow < (unsigned)W)) fa[h] = v4i{0, 0, 0, 0};
-                if (kvalid < 16) {
+                const bool inside = (unsigned)oh < (unsigned)H && (unsigned)ow < (unsigned)W;
+                fa[h] = *reinterpret_cast<const v4i*>(&smem[inside ? w * BK + 16 * (lc ^ swz(w)) : kZero]);
+                if (!FULLK && kvalid < 16) {
                     const uint4 m = mask_tail(make_uint4(fa[h][0], fa[h][1], fa[h][2], fa[h][3]), kvalid);
                     fa[h] = v4i{(int)m.x, (int)m.y, (int)m.z, (int)m.w};
                 }
@@ -1513,8 +1518,11 @@ hipError_t launch_conv_dgrad(const GemmArgs& a0, int8_t* bc, int64_t ld_bc, hipS
         // whole 128-row steps per block, at most kStreamBlocks blocks
         const int64_t rows = round_up((a0.Mg + kStreamBlocks - 1) / kStreamBlocks, 128);
         const dim3 grid((unsigned)((a0.Mg + rows - 1) / rows));
-        if (a0.acc) hipLaunchKernelGGL(k_conv_stream<true>, grid, dim3(256), 0, s, a0, rows);
-        else hipLaunchKernelGGL(k_conv_stream<false>, grid, dim3(256), 0, s, a0, rows);
+        const bool fullk = a0.K_used >= 64;   // every code column of the chunk is a channel
+        if (a0.acc && fullk) hipLaunchKernelGGL((k_conv_stream<true, true>), grid, dim3(256), 0, s, a0, rows);
+        else if (a0.acc) hipLaunchKernelGGL((k_conv_stream<true, false>), grid, dim3(256), 0, s, a0, rows);
+        else if (fullk) hipLaunchKernelGGL((k_conv_stream<false, true>), grid, dim3(256), 0, s, a0, rows);
+        else hipLaunchKernelGGL((k_conv_stream<false, false>), grid, dim3(256), 0, s, a0, rows);
         return hipGetLastError();
     }
     // weights in the K order of the implicit GEMM
