@@ -1070,6 +1070,21 @@ __global__ __launch_bounds__(256) void k_conv_stream(GemmArgs p, int64_t rows_pe
     for (int j = 0; j < kStreamNW + 2 * kStreamPF - 2; ++j) load_chunk(j);
 
     const int kvalid = (int)min((int64_t)16, max((int64_t)0, p.K_used - 16 * lc));   // code bytes < C_out
+    // image row and column of this lane's two output rows, advanced by 128
+    // pixels a step: (hw + 128 mod HW) < 2 HW, so one carry and one wrap
+    // suffice (rows past the tensor get a position too; they are not stored)
+    const uint32_t HW = (uint32_t)H * (uint32_t)W;
+    const uint32_t adv = 128u % HW, adv_h = adv / (uint32_t)W, adv_w = adv - adv_h * (uint32_t)W;
+    uint32_t ih[2], iw[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const uint32_t hw = (uint32_t)(r0 + 64 * h + wv * 16 + lrow) % HW;
+        ih[h] = hw / (uint32_t)W;
+        iw[h] = hw - ih[h] * (uint32_t)W;
+    }
+    // fp32 only: the fold's final shift goes into the scale, exactly
+    // ((float)(v << f) * a == (float)v * (a * 2^f) while neither overflows)
+    const float alpha_o = ACC ? alpha : __fmul_rn(alpha, pow2f(fsh));
     for (int k = 0; k < steps; ++k) {
         load_chunk(2 * k + kStreamNW + 2 * kStreamPF - 2);
         load_chunk(2 * k + kStreamNW + 2 * kStreamPF - 1);
@@ -1083,26 +1098,18 @@ __global__ __launch_bounds__(256) void k_conv_stream(GemmArgs p, int64_t rows_pe
         __builtin_amdgcn_s_barrier();   // a plain barrier: the stores stay in flight
 
         int64_t pix[2];
-        int ih[2], iw[2];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            pix[h] = r0 + 128 * k + 64 * h + wv * 16 + lrow;   // this lane's output rows
-            const int hw = (int)(min(pix[h], p.Mg - 1) % ((int64_t)H * W));
-            ih[h] = hw / W;
-            iw[h] = hw - ih[h] * W;
-        }
+        for (int h = 0; h < 2; ++h) pix[h] = r0 + 128 * k + 64 * h + wv * 16 + lrow;   // this lane's output rows
         v4i acc[2][4];
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) acc[h][j] = v4i{0, 0, 0, 0};
-        for (int tau = 0, tr = 0, ts = 0; tau < taps; ++tau) {
+        // one tap: its two A fragments (zero slot outside the image) times the
+        // tap's four weight fragments; the first tap starts from zero
+        auto tap = [&](int tau, int tr, int ts, auto FIRST) {
             const int d = (p.cv_PH - tr) * W + (p.cv_PW - ts);
             v4i fa[2];
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int w = (128 * k + 64 * h + wv * 16 + lrow + E + d) & (kStreamRing * 64 - 1);
-                const int oh = ih[h] + p.cv_PH - tr, ow = iw[h] + p.cv_PW - ts;
+                const int oh = (int)ih[h] + p.cv_PH - tr, ow = (int)iw[h] + p.cv_PW - ts;
                 const bool inside = (unsigned)oh < (unsigned)H && (unsigned)ow < (unsigned)W;
                 fa[h] = *reinterpret_cast<const v4i*>(&smem[inside ? w * BK + 16 * (lc ^ swz(w)) : kZero]);
                 if (!FULLK && kvalid < 16) {
@@ -1115,8 +1122,13 @@ __global__ __launch_bounds__(256) void k_conv_stream(GemmArgs p, int64_t rows_pe
                 const int r = tau * 64 + j * 16 + lrow;
                 const v4i fb = *reinterpret_cast<const v4i*>(&smem[kRing + r * BK + 16 * (lc ^ swz(r))]);
 #pragma unroll
-                for (int h = 0; h < 2; ++h) acc[h][j] = MF::run(fb, fa[h], acc[h][j]);
+                for (int h = 0; h < 2; ++h)
+                    acc[h][j] = MF::run(fb, fa[h], decltype(FIRST)::value ? v4i{0, 0, 0, 0} : acc[h][j]);
             }
+        };
+        tap(0, 0, 0, std::true_type());
+        for (int tau = 1, tr = KW == 1 ? 1 : 0, ts = KW == 1 ? 0 : 1; tau < taps; ++tau) {
+            tap(tau, tr, ts, std::false_type());
             if (++ts == KW) { ts = 0; ++tr; }
         }
         // NS / 2 stores per row half: the fp32 output (a NULL output has an
@@ -1128,21 +1140,31 @@ __global__ __launch_bounds__(256) void k_conv_stream(GemmArgs p, int64_t rows_pe
             for (int j = 0; j < 4; ++j) {
                 const int col = j * 16 + lc * 4;
                 const bool ok = row_ok && col < p.Ng;
-                const int v0 = acc[h][j][0] << fsh, v1 = acc[h][j][1] << fsh;
-                const int v2 = acc[h][j][2] << fsh, v3 = acc[h][j][3] << fsh;
+                // byte offsets below 2^31 (the output's size is checked on the host)
+                const uint32_t prow = (uint32_t)pix[h];
+                const int sh = ACC ? fsh : 0;
+                const int v0 = acc[h][j][0] << sh, v1 = acc[h][j][1] << sh;
+                const int v2 = acc[h][j][2] << sh, v3 = acc[h][j][3] << sh;
                 typedef unsigned u4 __attribute__((ext_vector_type(4)));
-                const u4 fo = {__float_as_uint(__fmul_rn((float)v0, alpha)), __float_as_uint(__fmul_rn((float)v1, alpha)),
-                               __float_as_uint(__fmul_rn((float)v2, alpha)), __float_as_uint(__fmul_rn((float)v3, alpha))};
-                int oo = ok ? (int)((pix[h] * p.ld_out + col) * 4) : (int)0x80000000;
+                const u4 fo = {__float_as_uint(__fmul_rn((float)v0, alpha_o)), __float_as_uint(__fmul_rn((float)v1, alpha_o)),
+                               __float_as_uint(__fmul_rn((float)v2, alpha_o)), __float_as_uint(__fmul_rn((float)v3, alpha_o))};
+                int oo = ok ? (int)((prow * (uint32_t)p.ld_out + (uint32_t)col) * 4u) : (int)0x80000000;
                 opaque(oo);
                 __builtin_amdgcn_raw_buffer_store_b128(fo, rO, oo, 0, 0);
                 if constexpr (ACC) {
                     const u4 io = {(unsigned)v0, (unsigned)v1, (unsigned)v2, (unsigned)v3};
-                    int oc = ok ? (int)((pix[h] * p.ld_acc + col) * 4) : (int)0x80000000;
+                    int oc = ok ? (int)((prow * (uint32_t)p.ld_acc + (uint32_t)col) * 4u) : (int)0x80000000;
                     opaque(oc);
                     __builtin_amdgcn_raw_buffer_store_b128(io, rC, oc, 0, 0);
                 }
             }
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            iw[h] += adv_w;
+            ih[h] += adv_h;
+            if (iw[h] >= (uint32_t)W) { iw[h] -= (uint32_t)W; ++ih[h]; }
+            if (ih[h] >= (uint32_t)H) ih[h] -= (uint32_t)H;
         }
         __builtin_amdgcn_s_barrier();   // the ring slots of this step may be refilled
     }
