@@ -30,6 +30,12 @@ WGRAD_CASES = [  # N, H, W, C_out, C_in, KH, KW, PH, PW, bits, N_G
     (3, 4, 4, 200, 72, 3, 3, 1, 1, 8, 4),     # 8-bit codes
     (1, 5, 16, 64, 64, 3, 3, 1, 1, 4, 4),     # padded width exactly 32
     (4, 14, 14, 256, 128, 3, 3, 1, 1, 4, 4),  # a ResNet stage-3 shape, large tiles
+    # 64 input channels, 3-wide windows, split K: the window kernel that
+    # reads one input copy and shifts in registers
+    (4, 14, 14, 64, 64, 3, 3, 1, 1, 4, 4),    # 2 K splits
+    (3, 20, 23, 40, 64, 3, 3, 1, 1, 6, 4),    # fewer than 64 output channels, 4 splits
+    (4, 12, 12, 64, 64, 5, 3, 2, 1, 4, 4),    # 5 tap rows per split (2 splits)
+    (2, 30, 30, 64, 64, 3, 3, 0, 0, 8, 4),    # unpadded rows and columns, 8-bit codes
 ]
 
 
