@@ -432,6 +432,7 @@ using PipeLarge = PipeCfg<256, 256, 4, 2, 16, 4>;   // 128 KB of LDS, one block 
 using PipeWide = PipeCfg<256, 256, 2, 2, 16, 4>;    // 4 waves of 128 x 128: half the LDS reads per MFMA
 using PipeSmall = PipeCfg<128, 128, 2, 2, 16, 4>;   // 64 KB of LDS
 using PipeSkinny = PipeCfg<64, 192, 2, 2, 16, 4>;   // at most 64 output rows (wgrad of narrow layers)
+using PipeTall = PipeCfg<128, 384, 2, 4, 16, 4>;    // 8 waves of 64 x 96: more tiles where 256 x 256 leaves CUs idle
 using PipeNarrow = PipeCfg<256, 64, 4, 1, 16, 4>;   // at most 64 output columns (conv dgrad), 80 KB of LDS
 
 typedef __attribute__((address_space(3))) void lds_void_t;
@@ -1332,7 +1333,7 @@ bool pipe_ok(const GemmArgs& a) {
 // or with K split into slices of at least 16 tiles) to fill most of the chip
 // and K is long, a 64-row tile for products with at most 64 output rows,
 // 128 x 128 otherwise.
-enum class Pick { kLarge, kSmall, kSkinny };
+enum class Pick { kLarge, kTall, kSmall, kSkinny };
 
 int64_t tiles_of(const GemmArgs& a, int bm, int bn) { return ((a.Mg + bm - 1) / bm) * ((a.Ng + bn - 1) / bn); }
 
@@ -1355,8 +1356,19 @@ int64_t large_splits(const GemmArgs& a) {
     return s >= 2 && tiles * s >= kLargeFill ? s : 0;
 }
 
+// An unsplit product whose 256 x 256 tiles leave CUs idle takes 128 x 384
+// tiles when those fill more CUs (at most one tile per CU, most of each tile
+// inside the product): the MLP layer's 16384 x 768 input gradient has 192
+// large tiles but 256 tall ones.
+bool tall_fits(const GemmArgs& a) {
+    const int64_t large = tiles_of(a, PipeLarge::BM, PipeLarge::BN), tall = tiles_of(a, PipeTall::BM, PipeTall::BN);
+    return large < kCUs && tall > large && tall <= kCUs &&
+           4 * a.Mg * a.Ng >= 3 * tall * PipeTall::BM * PipeTall::BN;
+}
+
 Pick pick(const GemmArgs& a) {
     const int64_t ls = a.K >= 1024 ? large_splits(a) : 0;
+    if (ls == 1 && a.splits <= 1 && tall_fits(a)) return Pick::kTall;
     if (ls > 0 && std::max(a.splits, 1) == ls) return Pick::kLarge;
     if (a.Mg <= 64 && !a.extA) return Pick::kSkinny;
     return Pick::kSmall;
@@ -1429,11 +1441,17 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
         if (p == Pick::kLarge)
             return a.extA ? launch_pipe<PipeLarge, true, false, true>(a, 1, per * 64, s)
                           : launch_pipe<PipeLarge, false, false, true>(a, 1, per * 64, s);
+        if (p == Pick::kTall)
+            return a.extA ? launch_pipe<PipeTall, true, false, true>(a, 1, per * 64, s)
+                          : launch_pipe<PipeTall, false, false, true>(a, 1, per * 64, s);
         if (p == Pick::kSkinny) return launch_pipe<PipeSkinny, false, false, true>(a, 1, per * 64, s);
         return a.extA ? launch_pipe<PipeSmall, true, false, true>(a, 1, per * 64, s)
                       : launch_pipe<PipeSmall, false, false, true>(a, 1, per * 64, s);
     }
-    if (p == Pick::kLarge) {
+    if (p == Pick::kTall && pipe)
+        return a.extA ? launch_pipe<PipeTall, true>(a, splits, per * 64, s)
+                      : launch_pipe<PipeTall, false>(a, splits, per * 64, s);
+    if (p == Pick::kLarge || p == Pick::kTall) {
         if (!pipe) return launch_cfg<CfgLarge>(a, splits, per * 64, s);
         return a.extA ? launch_pipe<PipeLarge, true>(a, splits, per * 64, s)
                       : launch_pipe<PipeLarge, false>(a, splits, per * 64, s);

@@ -379,6 +379,23 @@ def test_fold_windows_large_tiles(sq, pattern):
     check_layer(sq, dY, W, X, bits, ng, dgrad_rows=rows_d, wgrad_rows=rows_w, fold_rows=rows_d)
 
 
+@pytest.mark.parametrize("shape,bits", [((8000, 1024, 1536), 6), ((8000 - 77, 1024, 1536 - 40), 4)],
+                         ids=["8000x1024x1536-b6", "7923x1024x1496-b4"])
+def test_dgrad_tall_tiles(sq, shape, bits):
+    # 128 x 384 tiles: the 256 x 256 tiling would leave CUs idle (192 tiles),
+    # the tall one fills more of them; 6-bit codes take the appended fold
+    # windows, the second shape has ragged tiles in both directions
+    M, C_out, C_in = shape
+    g = _group_pattern("spread", C_out, 4, seed=8)
+    dY = _grouped_grad(M, g, seed=9)
+    rng = np.random.default_rng(10)
+    W = (rng.standard_normal((C_out, C_in)) * 0.02).astype(np.float32)
+    X = rng.standard_normal((M, C_in)).astype(np.float32)
+    rows_d = np.unique(np.r_[0, 127, 128, M - 2, M - 1, rng.integers(0, M, 24)])
+    rows_w = np.unique(np.r_[0, C_out - 1, rng.integers(0, C_out, 6)])
+    check_layer(sq, dY, W, X, bits, 4, dgrad_rows=rows_d, wgrad_rows=rows_w, fold_rows=rows_d)
+
+
 def test_fp32_only_outputs_match_with_acc(sq):
     import torch
     M, C_out, C_in = 300, 200, 129
