@@ -26,7 +26,8 @@ RANGE_CASES = [  # M, C_out, C_in, bits, N_G  (tile: large / small / skinny, fol
     (40, 128, 96, 4, 4),        # a single row tile of the skinny kind
     (4099, 768, 3072, 6, 4),    # the MLP chain's down-projection, large tiles
     (65, 64, 48, 8, 3),
-    (8000, 1024, 1536, 6, 4),   # 128 x 384 tiles (192 large tiles would leave CUs idle)
+    (8000, 1024, 1536, 6, 4),   # 128 x 384 tiles (192 large tiles would leave CUs idle), fold windows
+    (8000 - 40, 1024, 1536, 4, 4),   # the same tiles, one window, ragged rows
 ]
 
 
