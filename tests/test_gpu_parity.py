@@ -396,6 +396,20 @@ def test_dgrad_tall_tiles(sq, shape, bits):
     check_layer(sq, dY, W, X, bits, 4, dgrad_rows=rows_d, wgrad_rows=rows_w, fold_rows=rows_d)
 
 
+def test_wgrad_tall_tiles(sq):
+    # the weight gradient of a 2048 -> 4096 layer over 2048 tokens: 128 large
+    # tiles (no split), 192 tall ones; per-row group scales in the epilogue
+    M, C_out, C_in = 2048, 4096, 2048
+    g = _group_pattern("spread", C_out, 4, seed=11)
+    dY = _grouped_grad(M, g, seed=12)
+    rng = np.random.default_rng(13)
+    W = (rng.standard_normal((C_out, C_in)) * 0.02).astype(np.float32)
+    X = rng.standard_normal((M, C_in)).astype(np.float32)
+    rows_w = np.unique(np.r_[0, 127, 128, C_out - 1, np.nonzero(g < 3)[0][:6], rng.integers(0, C_out, 10)])
+    rows_d = np.unique(np.r_[0, M - 1, rng.integers(0, M, 6)])
+    check_layer(sq, dY, W, X, 6, 4, dgrad_rows=rows_d, wgrad_rows=rows_w)
+
+
 def test_fp32_only_outputs_match_with_acc(sq):
     import torch
     M, C_out, C_in = 300, 200, 129
