@@ -90,7 +90,22 @@ def _bind(L):
     L.sqo_l1bn_forward.restype = ct.c_int
     L.sqo_l1bn_backward.argtypes = [P, P, ct.c_float, i64, i64, P, ct.c_float, P, P, P, P, i64, P, P, P]
     L.sqo_l1bn_backward.restype = ct.c_int
+    L.sqo_set_threads.argtypes = [ct.c_int]
+    L.sqo_set_threads.restype = ct.c_int
+    L.sqo_max_threads.argtypes = []
+    L.sqo_max_threads.restype = ct.c_int
     return L
+
+
+def set_threads(n: int) -> int:
+    """Threads of the oracle's OpenMP loops (1 = plain serial loops).  The
+    results do not depend on it: each output is computed by one thread."""
+    return int(lib().sqo_set_threads(int(n)))
+
+
+def max_threads() -> int:
+    """Processors OpenMP sees on this host."""
+    return int(lib().sqo_max_threads())
 
 
 def _p(a: np.ndarray):

@@ -1,9 +1,12 @@
 /*
  * ShiftQuant backward path: CPU ORACLE.  TEST INFRASTRUCTURE ONLY.
  *
- * A plain, slow, single-threaded C implementation of what the GPU path
- * computes, written from "Towards Accurate and Efficient Sub-8-Bit Integer
- * Training" (arXiv 2411.10948).  Only the tests, the smoke check and the
+ * A plain, slow C implementation of what the GPU path computes, written
+ * from "Towards Accurate and Efficient Sub-8-Bit Integer Training" (arXiv
+ * 2411.10948).  The outer loops over independent outputs (channels, rows,
+ * output elements) carry OpenMP pragmas; every output is still computed by
+ * one thread in the plain loop order, so the results do not depend on the
+ * thread count (sqo_set_threads; one thread unless set).  Only the tests, the smoke check and the
  * benchmark's CPU-baseline leg may load it; the product library never does.
  * It shares no code, header or table with the HIP sources.
  *
@@ -35,6 +38,7 @@
  *     all-zero codes, every channel in the last group and zero scales.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -60,6 +64,11 @@ static float u2f(uint32_t u) { float f; memcpy(&f, &u, 4); return f; }
 static float pow2f(int k) { return u2f((uint32_t)(k + 127) << 23); }
 
 static int32_t qmax_of(int bits) { return (1 << (bits - 1)) - 1; }
+
+/* Thread count of the OpenMP loops (1 = the plain serial program). */
+static int g_threads = 1;
+int sqo_set_threads(int n) { g_threads = n > 0 ? n : 1; return g_threads; }
+int sqo_max_threads(void) { return omp_get_num_procs(); }
 
 /* ---------------------------------------------------------------------------
  * Philox4x32-10, Salmon, Moraes, Dror and Shaw, "Parallel random numbers: as
@@ -113,6 +122,7 @@ int sqo_channel_range(const float* x, int64_t M, int64_t C, int64_t ld, float* r
 {
     if (!x || !r || M < 0 || C < 0 || ld < C) return SQO_ERR_ARG;
     int nf = 0;
+#pragma omp parallel for num_threads(g_threads) reduction(|:nf) schedule(static)
     for (int64_t c = 0; c < C; ++c) {
         uint32_t best = 0;
         for (int64_t m = 0; m < M; ++m) {
@@ -192,6 +202,7 @@ int sqo_quantize_grad(const float* dY, int64_t M, int64_t C, int64_t ld, int bit
     if (!r_out) free(r);
 
     const float two16 = pow2f(16);
+#pragma omp parallel for num_threads(g_threads) schedule(static)
     for (int64_t m = 0; m < M; ++m) {
         for (int64_t c = 0; c < C; ++c) {
             float s_c = scale->inv0 * pow2f(g[c]);
@@ -320,9 +331,12 @@ int sqo_dgrad(const int8_t* q, int64_t M, int64_t C_out, const uint8_t* g, int n
 {
     if (!q || !g || !wq || !A || num_groups < 1 || num_groups > 8) return SQO_ERR_ARG;
     int64_t nr = rows ? n_rows : M;
+    for (int64_t i = 0; i < nr; ++i)
+        if (rows && (rows[i] < 0 || rows[i] >= M)) return SQO_ERR_ARG;
+    int err = SQO_OK;
+#pragma omp parallel for num_threads(g_threads) schedule(dynamic, 1)
     for (int64_t i = 0; i < nr; ++i) {
         int64_t n = rows ? rows[i] : i;
-        if (n < 0 || n >= M) return SQO_ERR_ARG;
         for (int64_t k = 0; k < C_in; ++k) {
             int64_t acc = 0;
             for (int64_t c = 0; c < C_out; ++c) {
@@ -330,11 +344,14 @@ int sqo_dgrad(const int8_t* q, int64_t M, int64_t C_out, const uint8_t* g, int n
                 int64_t prod = (int64_t)q[n * C_out + c] * (int64_t)wq[c * C_in + k];
                 acc += prod * ((int64_t)1 << shift);
             }
-            if (acc > INT32_MAX || acc < INT32_MIN) return SQO_ERR_RANGE;
+            if (acc > INT32_MAX || acc < INT32_MIN) {
+#pragma omp atomic write
+                err = SQO_ERR_RANGE;
+            }
             A[i * C_in + k] = (int32_t)acc;
         }
     }
-    return SQO_OK;
+    return err;
 }
 
 /* ---------------------------------------------------------------------------
@@ -362,9 +379,12 @@ int sqo_conv_dgrad(const int8_t* q, int64_t N, int64_t H, int64_t W, int64_t C_o
     if (Ho < 1 || Wo < 1) return SQO_ERR_ARG;
     int64_t taps_ci = (int64_t)KH * KW * C_in;   /* columns of W */
     int64_t np = pix ? n_pix : N * H * W;
+    for (int64_t i = 0; i < np; ++i)
+        if (pix && (pix[i] < 0 || pix[i] >= N * H * W)) return SQO_ERR_ARG;
+    int err = SQO_OK;
+#pragma omp parallel for num_threads(g_threads) schedule(dynamic, 16)
     for (int64_t i = 0; i < np; ++i) {
         int64_t p = pix ? pix[i] : i;
-        if (p < 0 || p >= N * H * W) return SQO_ERR_ARG;
         int64_t n = p / (H * W), ih = (p / W) % H, iw = p % W;
         for (int64_t ci = 0; ci < C_in; ++ci) {
             int64_t acc = 0;
@@ -383,11 +403,14 @@ int sqo_conv_dgrad(const int8_t* q, int64_t N, int64_t H, int64_t W, int64_t C_o
                     }
                 }
             }
-            if (acc > INT32_MAX || acc < INT32_MIN) return SQO_ERR_RANGE;
+            if (acc > INT32_MAX || acc < INT32_MIN) {
+#pragma omp atomic write
+                err = SQO_ERR_RANGE;
+            }
             A[i * C_in + ci] = (int32_t)acc;
         }
     }
-    return SQO_OK;
+    return err;
 }
 
 /* Weight gradient (the third training GEMM, Fig. "MMs"): inner dimension is
@@ -399,18 +422,24 @@ int sqo_wgrad(const int8_t* q, int64_t M, int64_t C_out, const int8_t* xq, int64
 {
     if (!q || !xq || !B) return SQO_ERR_ARG;
     int64_t nr = rows ? n_rows : C_out;
+    for (int64_t i = 0; i < nr; ++i)
+        if (rows && (rows[i] < 0 || rows[i] >= C_out)) return SQO_ERR_ARG;
+    int err = SQO_OK;
+#pragma omp parallel for num_threads(g_threads) collapse(2) schedule(dynamic, 16)
     for (int64_t i = 0; i < nr; ++i) {
-        int64_t c = rows ? rows[i] : i;
-        if (c < 0 || c >= C_out) return SQO_ERR_ARG;
         for (int64_t k = 0; k < C_in; ++k) {
+            int64_t c = rows ? rows[i] : i;
             int64_t acc = 0;
             for (int64_t m = 0; m < M; ++m)
                 acc += (int64_t)q[m * C_out + c] * (int64_t)xq[m * C_in + k];
-            if (acc > INT32_MAX || acc < INT32_MIN) return SQO_ERR_RANGE;
+            if (acc > INT32_MAX || acc < INT32_MIN) {
+#pragma omp atomic write
+                err = SQO_ERR_RANGE;
+            }
             B[i * C_in + k] = (int32_t)acc;
         }
     }
-    return SQO_OK;
+    return err;
 }
 
 /* Dequantization of the dgrad accumulator (Eq. dq_mm_f: the product of the two
@@ -420,6 +449,7 @@ int sqo_wgrad(const int8_t* q, int64_t M, int64_t C_out, const int8_t* xq, int64
 void sqo_dequant_dgrad(const int32_t* A, int64_t n, float d_grad, float d_w, int num_groups, float* out)
 {
     float alpha = (d_grad * d_w) * pow2f(-(num_groups - 1));
+#pragma omp parallel for num_threads(g_threads) schedule(static)
     for (int64_t i = 0; i < n; ++i) out[i] = (float)A[i] * alpha;
 }
 
@@ -429,6 +459,7 @@ void sqo_dequant_dgrad(const int32_t* A, int64_t n, float d_grad, float d_w, int
 void sqo_dequant_wgrad(const int32_t* B, int64_t n_rows, int64_t C_in, const uint8_t* g_rows,
                        float d_grad, float d_x, float* out)
 {
+#pragma omp parallel for num_threads(g_threads) schedule(static)
     for (int64_t i = 0; i < n_rows; ++i) {
         float beta = (d_grad * d_x) * pow2f(-(int)g_rows[i]);
         for (int64_t k = 0; k < C_in; ++k) out[i * C_in + k] = (float)B[i * C_in + k] * beta;
@@ -594,6 +625,8 @@ int sqo_conv_wgrad(const int8_t* q, int64_t N, int64_t H, int64_t W, int64_t C_o
     int64_t Ho = H + 2 * (int64_t)PH - KH + 1, Wo = W + 2 * (int64_t)PW - KW + 1;
     if (Ho < 1 || Wo < 1) return SQO_ERR_ARG;
     int64_t cols = (int64_t)KH * KW * C_in;
+    int err = SQO_OK;
+#pragma omp parallel for num_threads(g_threads) collapse(4) schedule(dynamic, 1)
     for (int64_t co = 0; co < C_out; ++co)
         for (int r = 0; r < KH; ++r)
             for (int s = 0; s < KW; ++s)
@@ -610,8 +643,11 @@ int sqo_conv_wgrad(const int8_t* q, int64_t N, int64_t H, int64_t W, int64_t C_o
                                        (int64_t)x[((n * H + ih) * W + iw) * C_in + ci];
                             }
                         }
-                    if (acc > INT32_MAX || acc < INT32_MIN) return SQO_ERR_RANGE;
+                    if (acc > INT32_MAX || acc < INT32_MIN) {
+#pragma omp atomic write
+                        err = SQO_ERR_RANGE;
+                    }
                     B[co * cols + ((int64_t)r * KW + s) * C_in + ci] = (int32_t)acc;
                 }
-    return SQO_OK;
+    return err;
 }

@@ -56,8 +56,9 @@ MUTATIONS = [
      "float x = axis == 1 ? T[ch * ld + e] : T[e * ld + ch];"),
     ("column dequant exponent", "float gamma = (d_a * d_w[k]) * pow2f(-(num_groups - 1));",
      "float gamma = (d_a * d_w[k]) * pow2f(-num_groups);"),
-    ("int32 range check", "if (acc > INT32_MAX || acc < INT32_MIN) return SQO_ERR_RANGE;\n            A[i * C_in + k]",
-     "A[i * C_in + k]"),
+    ("int32 range check", "            if (acc > INT32_MAX || acc < INT32_MIN) {\n#pragma omp atomic write\n"
+                          "                err = SQO_ERR_RANGE;\n            }\n            A[i * C_in + k]",
+     "            A[i * C_in + k]"),
     ("L1BN mean truncated", "int64_t mc = div_round_even(S, M);", "int64_t mc = S / M;"),
     ("L1BN mean ties away", "if (2 * r > den || (2 * r == den && (q & 1))) q += 1;", "if (2 * r >= den) q += 1;"),
     ("L1BN sigma code floor", "if (k < 1) k = 1;", "if (k < 0) k = 0;"),
