@@ -161,6 +161,28 @@ sq_status sq_quantize_grad(const float* dY, int64_t M, int64_t C_out, int64_t ld
                            void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * sq_quantize_grad_noalloc -- sq_quantize_grad without a workspace argument,
+ * for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc).
+ *
+ * Same arguments, results and errors as sq_quantize_grad, minus workspace /
+ * workspace_bytes.  Its scratch is a fixed 16 MiB device array inside the
+ * library (one copy per GPU, held until the process ends); the call itself
+ * allocates nothing.  A gradient whose quantizer scratch
+ * (sq_quantize_grad_workspace_size) exceeds 1 MiB (about 65,000 channels) is rejected with
+ * SQ_ERR_WORKSPACE_TOO_SMALL before any launch.  All calls on one GPU share
+ * that array: calls that overlap in time on one GPU (other streams, other
+ * host threads) race and must be serialized by the caller.  The first call
+ * on a device looks up its scratch address (hipGetSymbolAddress) with that
+ * device current.
+ * ------------------------------------------------------------------------- */
+sq_status sq_quantize_grad_noalloc(const float* dY, int64_t M, int64_t C_out, int64_t ld_dY,
+                                   const sq_quant_params* p,
+                                   int8_t* q_fold, int64_t ld_fold,
+                                   int8_t* q_t, int64_t ld_t,
+                                   uint8_t* group, sq_scale* scale, int32_t* layout, void* stream);
+
+/* ---------------------------------------------------------------------------
  * sq_quantize_tensor -- per-tensor symmetric quantization of W or X.
  *
  * The paper's INT8 baseline quantizes weights, activations and gradients per

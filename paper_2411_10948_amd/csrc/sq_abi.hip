@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "sq_internal.h"
@@ -95,6 +96,77 @@ size_t quant_ws_bytes(int64_t M, int64_t C) { return (size_t)round_up(std::max<i
         if (st__ != SQ_OK) return st__;   \
     } while (0)
 
+// Scratch of sq_quantize_grad_noalloc: a fixed device array instead of a
+// caller-provided workspace, for callers that cannot allocate.  Each GPU the
+// library runs on holds its own copy until the process ends; host code uses
+// the address hipGetSymbolAddress reports for the current device, never the
+// array's name.  Every call on one GPU shares it.
+constexpr size_t kNoAllocScratchBytes = (size_t)1 << 20;
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of this GPU's scratch, looked up once per device (with
+// that device current) and kept.
+sq_status noalloc_scratch(void** out) {
+    int dev = -1;
+    SQ_TRY(hip_status(hipGetDevice(&dev), "hipGetDevice"));
+    if (dev < 0 || dev >= kMaxDevices) return fail(SQ_ERR_UNSUPPORTED, "device index beyond the scratch table");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        SQ_TRY(hip_status(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)"));
+        if (!ptr || !aligned(ptr, 256)) return fail(SQ_ERR_HIP, "scratch symbol has no usable device address");
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return SQ_OK;
+}
+
+// argument checks of the gradient quantizer shared by both entry points
+// (everything but the workspace), made before any HIP call
+sq_status check_quantize_grad(const float* dY, int64_t M, int64_t C_out, int64_t ld_dY, const sq_quant_params* p,
+                              const int8_t* q_fold, int64_t ld_fold, const int8_t* q_t, int64_t ld_t,
+                              const uint8_t* group, const sq_scale* scale, const int32_t* layout) {
+    SQ_TRY(check_params(p));
+    SQ_TRY(check_dims(M, C_out, "dY"));
+    if (M > 0 && C_out > 0) SQ_TRY(check_f32(dY, ld_dY, C_out, "dY"));
+    if (!scale || !aligned(scale, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "scale is NULL or misaligned");
+    if (!layout || !aligned(layout, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "layout is NULL or misaligned");
+    if (C_out > 0 && !group) return fail(SQ_ERR_INVALID_ARGUMENT, "group is NULL");
+    size_t lay_bytes = 0;
+    int64_t min_ld_fold = 0;
+    SQ_TRY(sq_grad_layout_size(C_out, p, &lay_bytes, &min_ld_fold));
+    if (q_fold && M > 0) SQ_TRY(check_codes(q_fold, ld_fold, min_ld_fold, "q_fold"));
+    if (q_t && C_out > 0) SQ_TRY(check_codes(q_t, ld_t, M > 0 ? M : 1, "q_t"));
+    return SQ_OK;
+}
+
+// the gradient quantizer's launches, arguments already checked
+sq_status quantize_grad_impl(const float* dY, int64_t M, int64_t C_out, int64_t ld_dY, const sq_quant_params* p,
+                             int8_t* q_fold, int64_t ld_fold, int8_t* q_t, int64_t ld_t, uint8_t* group,
+                             sq_scale* scale, int32_t* layout, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+    if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
+    if (workspace_bytes < quant_ws_bytes(M, C_out)) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+
+    const QuantCfg cfg = make_cfg(*p);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    uint32_t* partial = static_cast<uint32_t*>(workspace);
+    int64_t slabs = 0;
+    SQ_TRY(hip_status(launch_colmax(dY, M, C_out, ld_dY, partial, &slabs, s), "colmax"));
+    uint32_t* rbits = partial + slabs * C_out;
+    const int64_t ext_max = fold_ext_max(C_out, cfg);
+    SQ_TRY(hip_status(launch_finalize_grad(partial, slabs, C_out, cfg, rbits, group, scale, layout, ext_max, s),
+                      "finalize"));
+    SQ_TRY(hip_status(launch_quantize(dY, M, C_out, ld_dY, group, scale, cfg, q_fold, ld_fold, q_t, ld_t,
+                                      layout + kLayoutHeader + ext_max, s),
+                      "quantize"));
+    return SQ_OK;
+}
+
 }  // namespace
 
 using namespace sq;
@@ -167,33 +239,25 @@ sq_status sq_quantize_grad(const float* dY, int64_t M, int64_t C_out, int64_t ld
                            int8_t* q_fold, int64_t ld_fold, int8_t* q_t, int64_t ld_t, uint8_t* group,
                            sq_scale* scale, int32_t* layout, void* workspace, size_t workspace_bytes,
                            void* stream) {
-    SQ_TRY(check_params(p));
-    SQ_TRY(check_dims(M, C_out, "dY"));
-    if (M > 0 && C_out > 0) SQ_TRY(check_f32(dY, ld_dY, C_out, "dY"));
-    if (!scale || !aligned(scale, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "scale is NULL or misaligned");
-    if (!layout || !aligned(layout, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "layout is NULL or misaligned");
-    if (C_out > 0 && !group) return fail(SQ_ERR_INVALID_ARGUMENT, "group is NULL");
-    size_t lay_bytes = 0;
-    int64_t min_ld_fold = 0;
-    SQ_TRY(sq_grad_layout_size(C_out, p, &lay_bytes, &min_ld_fold));
-    if (q_fold && M > 0) SQ_TRY(check_codes(q_fold, ld_fold, min_ld_fold, "q_fold"));
-    if (q_t && C_out > 0) SQ_TRY(check_codes(q_t, ld_t, M > 0 ? M : 1, "q_t"));
-    if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
-    if (workspace_bytes < quant_ws_bytes(M, C_out)) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+    SQ_TRY(check_quantize_grad(dY, M, C_out, ld_dY, p, q_fold, ld_fold, q_t, ld_t, group, scale, layout));
+    return quantize_grad_impl(dY, M, C_out, ld_dY, p, q_fold, ld_fold, q_t, ld_t, group, scale, layout, workspace,
+                              workspace_bytes, stream);
+}
 
-    const QuantCfg cfg = make_cfg(*p);
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    uint32_t* partial = static_cast<uint32_t*>(workspace);
-    int64_t slabs = 0;
-    SQ_TRY(hip_status(launch_colmax(dY, M, C_out, ld_dY, partial, &slabs, s), "colmax"));
-    uint32_t* rbits = partial + slabs * C_out;
-    const int64_t ext_max = fold_ext_max(C_out, cfg);
-    SQ_TRY(hip_status(launch_finalize_grad(partial, slabs, C_out, cfg, rbits, group, scale, layout, ext_max, s),
-                      "finalize"));
-    SQ_TRY(hip_status(launch_quantize(dY, M, C_out, ld_dY, group, scale, cfg, q_fold, ld_fold, q_t, ld_t,
-                                      layout + kLayoutHeader + ext_max, s),
-                      "quantize"));
-    return SQ_OK;
+sq_status sq_quantize_grad_noalloc(const float* dY, int64_t M, int64_t C_out, int64_t ld_dY,
+                                   const sq_quant_params* p, int8_t* q_fold, int64_t ld_fold, int8_t* q_t,
+                                   int64_t ld_t, uint8_t* group, sq_scale* scale, int32_t* layout, void* stream) {
+    SQ_TRY(check_quantize_grad(dY, M, C_out, ld_dY, p, q_fold, ld_fold, q_t, ld_t, group, scale, layout));
+    const size_t need = quant_ws_bytes(M, C_out);
+    if (need > kNoAllocScratchBytes)
+        return fail(SQ_ERR_WORKSPACE_TOO_SMALL,
+                    "sq_quantize_grad_noalloc: this gradient needs " + std::to_string(need) +
+                        " bytes of scratch, above the library's fixed " + std::to_string(kNoAllocScratchBytes) +
+                        "; call sq_quantize_grad with a workspace instead");
+    void* ws = nullptr;
+    SQ_TRY(noalloc_scratch(&ws));
+    return quantize_grad_impl(dY, M, C_out, ld_dY, p, q_fold, ld_fold, q_t, ld_t, group, scale, layout, ws,
+                              kNoAllocScratchBytes, stream);
 }
 
 sq_status sq_quantize_tensor(const float* T, int64_t rows, int64_t cols, int64_t ld, int32_t bits, int32_t transpose,

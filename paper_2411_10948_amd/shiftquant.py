@@ -44,7 +44,7 @@ EXPORTS = (
     "sq_l1bn_backward_workspace_size", "sq_l1bn_forward", "sq_l1bn_backward",
     "sq_conv_wgrad_layout", "sq_conv_pack_input", "sq_conv_pack_grad", "sq_quantize_grad_conv",
     "sq_conv_wgrad_workspace_size", "sq_conv_wgrad", "sq_gemm_dgrad_range_slabs", "sq_gemm_dgrad_ranged",
-    "sq_status_string", "sq_last_error",
+    "sq_quantize_grad_noalloc", "sq_status_string", "sq_last_error",
 )
 
 
@@ -87,6 +87,7 @@ def load() -> ct.CDLL:
         "sq_gemm_dgrad_workspace_size": [_I64, _I64, _I64, pp, ct.POINTER(_SZ)],
         "sq_gemm_wgrad_workspace_size": [_I64, _I64, _I64, pp, ct.POINTER(_SZ)],
         "sq_quantize_grad": [_P, _I64, _I64, _I64, pp, _P, _I64, _P, _I64, _P, _P, _P, _P, _SZ, _P],
+        "sq_quantize_grad_noalloc": [_P, _I64, _I64, _I64, pp, _P, _I64, _P, _I64, _P, _P, _P, _P],
         "sq_quantize_tensor": [_P, _I64, _I64, _I64, ct.c_int32, ct.c_int32, _P, _I64, _P, _P, _SZ, _P],
         "sq_gemm_dgrad": [_P, _I64, _P, _P, _P, _P, _I64, _P, _I64, _I64, _I64, pp, _P, _I64, _P, _I64,
                           _P, _SZ, _P],
@@ -253,6 +254,13 @@ def sq_quantize_grad(dY, params, q_fold, q_t, group, scale, layout, workspace, s
     _check("sq_quantize_grad", load().sq_quantize_grad(
         _ptr(dY), M, C, _ld(dY), ct.byref(params), _ptr(q_fold), _ld(q_fold), _ptr(q_t), _ld(q_t),
         _ptr(group), _ptr(scale), _ptr(layout), ws, nws, _stream(stream)))
+
+
+def sq_quantize_grad_noalloc(dY, params, q_fold, q_t, group, scale, layout, stream=None) -> None:
+    M, C = dY.shape
+    _check("sq_quantize_grad_noalloc", load().sq_quantize_grad_noalloc(
+        _ptr(dY), M, C, _ld(dY), ct.byref(params), _ptr(q_fold), _ld(q_fold), _ptr(q_t), _ld(q_t),
+        _ptr(group), _ptr(scale), _ptr(layout), _stream(stream)))
 
 
 def sq_quantize_grad_from_ranges(dY, params, ranges, range_slabs, q_fold, q_t, group, scale, layout, workspace,

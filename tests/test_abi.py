@@ -113,6 +113,26 @@ def test_quantize_grad_validation_no_launch(sq):
     assert "workspace" in sq.sq_last_error() or "dimensions" in sq.sq_last_error()
 
 
+def test_quantize_grad_noalloc_validation_no_launch(sq):
+    # the same synchronous checks as sq_quantize_grad, then the fixed-scratch
+    # limit, all before any HIP call
+    L = _raw(sq)
+    p = sq.Params.make(6, 4, 1)
+    fake = ct.c_void_p(0x100000)
+    assert L.sq_quantize_grad_noalloc(None, 8, 8, 8, ct.byref(p), fake, 16, fake, 16, fake, fake, fake, None) == 1
+    assert L.sq_quantize_grad_noalloc(fake, 8, 8, 4, ct.byref(p), fake, 16, fake, 16, fake, fake, fake, None) == 1
+    assert L.sq_quantize_grad_noalloc(fake, 8, 8, 8, ct.byref(p), fake, 24, fake, 16, fake, fake, fake, None) == 1
+    # a gradient whose quantizer scratch exceeds the fixed 1 MiB array
+    M, C = 1 << 16, 1 << 18
+    need = sq.sq_quantize_grad_workspace_size(M, C, p)
+    assert need > 1 << 20
+    _, ld = sq.sq_grad_layout_size(C, p)
+    st = L.sq_quantize_grad_noalloc(fake, M, C, C, ct.byref(p), fake, ld, fake, M, fake, fake, fake, None)
+    assert st == 4 and "sq_quantize_grad_noalloc" in sq.sq_last_error()
+    # the large linear layer's gradient fits
+    assert sq.sq_quantize_grad_workspace_size(8192, 11008, p) <= 1 << 20
+
+
 def test_overflow_risk_rejected(sq):
     L = _raw(sq)
     fake = ct.c_void_p(0x100000)
