@@ -426,6 +426,8 @@ def main(argv=None):
     ap.add_argument("--conv-wgrad", choices=["implicit", "im2col"], default="implicit",
                     help="weight gradient of the fused conv step: implicit im2col (sq_conv_wgrad) or the GEMM on "
                          "the im2col'd activations")
+    ap.add_argument("--layout", choices=["tiled", "rows"], default="tiled",
+                    help="code matrices of the linear layers: tile-major (default) or row-major")
     ap.add_argument("--dgrad", choices=["shiftmm", "grouped"], default="shiftmm",
                     help="grouped: the GEMM-based comparison implementation of the dgrad (Sec. 3.2)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -473,8 +475,12 @@ def main(argv=None):
     dY = torch.from_numpy(inputs["dY"]).to(dev)
     W = torch.from_numpy(inputs["W"]).to(dev)
     X = torch.from_numpy(inputs["X"]).to(dev)
-    params = sq.Params.make(wl.bits, wl.num_groups, wl.round_mode, wl.sr_seed, wl.sr_offset)
-    wq_t, ws = sq.quantize_tensor(W, 8, transpose=True)
+    # linear layers: tile-major code matrices (the GEMMs' K tiles are then
+    # contiguous 1 KB blocks); the conv kernels take row-major codes
+    tiled = not conv and args.dgrad == "shiftmm" and args.layout == "tiled"
+    params = sq.Params.make(wl.bits, wl.num_groups, wl.round_mode, wl.sr_seed, wl.sr_offset,
+                            sq.LAYOUT_TILED if tiled else sq.LAYOUT_ROWS)
+    wq_t, ws = sq.quantize_tensor(W, 8, transpose=True, tiled=tiled)
     implicit = conv and args.conv_wgrad == "implicit"
     if implicit:
         # setup (untimed, as the im2col'd codes are): the layer input is the
@@ -486,7 +492,7 @@ def main(argv=None):
         xq_t = sq.conv_pack_input(xq_raw, n_img, wl.conv_hw, wl.conv_hw, 3, 3, 1, 1)
         del xq_raw
     else:
-        xq_t, xs = sq.quantize_tensor(X, 8, transpose=True)
+        xq_t, xs = sq.quantize_tensor(X, 8, transpose=True, tiled=tiled)
     del W, X
     if conv:
         n_img = M // (wl.conv_hw * wl.conv_hw)
@@ -586,6 +592,7 @@ def main(argv=None):
                    "dgrad_impl": "shiftmm" if conv else args.dgrad,
                    "wgrad_impl": ("implicit im2col (sq_conv_wgrad)" if implicit else "GEMM on im2col'd X")
                    if conv else "gemm",
+                   "code_layout": "tile-major" if tiled else "row-major",
                    "parallelism": "none"},
         "pct_int8_peak": 100.0 * value / PEAK_INT8_TOPS,
         "breakdown_ms": {k: v["ms"] for k, v in parts.items()},

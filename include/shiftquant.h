@@ -65,12 +65,33 @@ enum {
     SQ_FLAG_ZERO = 2u              /* max |x| < 2^-96 (all-zero, tiny or empty tensor)  */
 };
 
+/* Layout of the int8 code matrices a call writes or reads (sq_quant_params.layout).
+ *   SQ_LAYOUT_ROWS  row-major: element (r, k) at r * ld + k.
+ *   SQ_LAYOUT_TILED tile-major: element (r, k) at
+ *                     ((r / 16) * (ld / 64) + k / 64) * 1024 + (r % 16) * 64 + k % 64,
+ *                   i.e. 16 x 64 tiles of 1 KB, the tiles of a 16-row group in
+ *                   order of k.  ld must be a multiple of 64 and the buffer
+ *                   must hold roundup(rows, 16) * ld bytes.  The GEMMs read
+ *                   one K tile of 16 rows as one contiguous 1 KB block, which
+ *                   keeps their operand streams sequential in HBM.  Writers fill
+ *                   the K padding up to the next multiple of 64 with zeros
+ *                   (q_fold columns [C_out, roundup(C_out, 64)), q_t and
+ *                   transposed tensor columns [rows, roundup(rows, 64))).
+ *                   Taken by sq_quantize_grad(_noalloc, _from_ranges),
+ *                   sq_gemm_dgrad(_ranged), sq_gemm_wgrad and sq_quantize_tensor
+ *                   (transpose = 2); the other calls that take sq_quant_params
+ *                   return SQ_ERR_UNSUPPORTED for it. */
+enum {
+    SQ_LAYOUT_ROWS = 0,
+    SQ_LAYOUT_TILED = 1
+};
+
 /* Quantizer parameters (host memory, read during the call only). */
 typedef struct {
     int32_t bits;         /* b in [2, 8]: codes lie in [-Q, Q], Q = 2^(b-1) - 1            */
     int32_t num_groups;   /* N_G in [1, 8] (the paper's default is 4, Sec. 5.1)            */
     int32_t round_mode;   /* SQ_ROUND_*                                                    */
-    int32_t reserved;     /* must be 0                                                     */
+    int32_t layout;       /* SQ_LAYOUT_*: layout of the int8 code matrices of the call     */
     uint64_t seed;        /* stochastic rounding: Philox key                               */
     uint64_t offset;      /* stochastic rounding: stream offset (e.g. the training step)   */
 } sq_quant_params;
@@ -144,7 +165,8 @@ sq_status sq_gemm_wgrad_workspace_size(int64_t M, int64_t C_out, int64_t C_in,
  *          there is one window and nothing is appended.  `layout` records
  *          the windows, and sq_gemm_dgrad applies their bases as left shifts
  *          of its accumulator.  Columns in [C_out, roundup(C_out, 64)) and
- *          the padding of appended regions are left unwritten.
+ *          the padding of appended regions are left unwritten (with
+ *          SQ_LAYOUT_TILED the former are written as zeros).
  *   q_t    [C_out, ld_t] int8 (ld_t >= M), the codes themselves, transposed:
  *          q_t[c, m] = code(m, c); this is the wgrad operand.
  *   group  [C_out] uint8, g_c.
@@ -192,6 +214,9 @@ sq_status sq_quantize_grad_noalloc(const float* dY, int64_t M, int64_t C_out, in
  * Input : T [rows, ld] fp32 (ld >= cols).
  * Output: transpose == 0: q [rows, ld_q] int8 (ld_q >= cols)
  *         transpose == 1: q [cols, ld_q] int8 (ld_q >= rows), q[j, i] = code(i, j)
+ *         transpose == 2: the same matrix tile-major (SQ_LAYOUT_TILED; ld_q a
+ *         multiple of 64, >= roundup(rows, 64); columns [rows, roundup(rows,
+ *         64)) written as zeros), the operand of the tile-major GEMMs
  *         (sq_gemm_dgrad takes W^T codes and sq_gemm_wgrad X^T codes, i.e.
  *         W [C_out, C_in] and X [M, C_in] quantized with transpose = 1).
  *         scale: one sq_scale.

@@ -9,6 +9,12 @@
 
 #include "sq_internal.h"
 
+#define SQ_TRY(expr)                      \
+    do {                                  \
+        const sq_status st__ = (expr);    \
+        if (st__ != SQ_OK) return st__;   \
+    } while (0)
+
 namespace sq {
 
 QuantCfg make_cfg(const sq_quant_params& p) {
@@ -60,7 +66,17 @@ sq_status check_params(const sq_quant_params* p) {
         return fail(SQ_ERR_INVALID_ARGUMENT, "num_groups must be in [1, 8]");
     if (p->round_mode != SQ_ROUND_NEAREST_EVEN && p->round_mode != SQ_ROUND_STOCHASTIC)
         return fail(SQ_ERR_INVALID_ARGUMENT, "round_mode must be SQ_ROUND_NEAREST_EVEN or SQ_ROUND_STOCHASTIC");
-    if (p->reserved != 0) return fail(SQ_ERR_INVALID_ARGUMENT, "reserved must be 0");
+    if (p->layout != SQ_LAYOUT_ROWS && p->layout != SQ_LAYOUT_TILED)
+        return fail(SQ_ERR_INVALID_ARGUMENT, "layout must be SQ_LAYOUT_ROWS or SQ_LAYOUT_TILED");
+    return SQ_OK;
+}
+
+bool tiled_of(const sq_quant_params* p) { return p->layout == SQ_LAYOUT_TILED; }
+
+// entry points that take row-major code matrices only
+sq_status rows_only(const sq_quant_params* p, const char* fn) {
+    if (p->layout != SQ_LAYOUT_ROWS)
+        return fail(SQ_ERR_UNSUPPORTED, std::string(fn) + " takes row-major codes only (SQ_LAYOUT_ROWS)");
     return SQ_OK;
 }
 
@@ -71,6 +87,15 @@ sq_status check_codes(const void* q, int64_t ld, int64_t min_ld, const char* nam
     if (ld < min_ld || ld % 16 != 0)
         return fail(SQ_ERR_INVALID_ARGUMENT, std::string("ld of ") + name + " must be a multiple of 16 and >= " +
                                                  std::to_string(min_ld));
+    return SQ_OK;
+}
+
+// the same for a code matrix in either layout; tile-major: ld a multiple of
+// 64 covering min_ld rounded up to 64 (the K padding the kernels write)
+sq_status check_codes_l(const void* q, int64_t ld, int64_t min_ld, bool tiled, const char* name) {
+    SQ_TRY(check_codes(q, ld, tiled ? round_up(min_ld, 64) : min_ld, name));
+    if (tiled && ld % 64 != 0)
+        return fail(SQ_ERR_INVALID_ARGUMENT, std::string("ld of ") + name + " must be a multiple of 64 (SQ_LAYOUT_TILED)");
     return SQ_OK;
 }
 
@@ -90,11 +115,6 @@ sq_status check_dims(int64_t rows, int64_t cols, const char* what) {
 // quantizer scratch: slab maxima [slabs, C] followed by the channel ranges [C]
 size_t quant_ws_bytes(int64_t M, int64_t C) { return (size_t)round_up(std::max<int64_t>(colmax_workspace_words(M, C), 1) * 4, 256); }
 
-#define SQ_TRY(expr)                      \
-    do {                                  \
-        const sq_status st__ = (expr);    \
-        if (st__ != SQ_OK) return st__;   \
-    } while (0)
 
 // Scratch of sq_quantize_grad_noalloc: a fixed device array instead of a
 // caller-provided workspace, for callers that cannot allocate.  Each GPU the
@@ -139,8 +159,8 @@ sq_status check_quantize_grad(const float* dY, int64_t M, int64_t C_out, int64_t
     size_t lay_bytes = 0;
     int64_t min_ld_fold = 0;
     SQ_TRY(sq_grad_layout_size(C_out, p, &lay_bytes, &min_ld_fold));
-    if (q_fold && M > 0) SQ_TRY(check_codes(q_fold, ld_fold, min_ld_fold, "q_fold"));
-    if (q_t && C_out > 0) SQ_TRY(check_codes(q_t, ld_t, M > 0 ? M : 1, "q_t"));
+    if (q_fold && M > 0) SQ_TRY(check_codes_l(q_fold, ld_fold, min_ld_fold, tiled_of(p), "q_fold"));
+    if (q_t && C_out > 0) SQ_TRY(check_codes_l(q_t, ld_t, M > 0 ? M : 1, tiled_of(p), "q_t"));
     return SQ_OK;
 }
 
@@ -162,7 +182,7 @@ sq_status quantize_grad_impl(const float* dY, int64_t M, int64_t C_out, int64_t 
     SQ_TRY(hip_status(launch_finalize_grad(partial, slabs, C_out, cfg, rbits, group, scale, layout, ext_max, s),
                       "finalize"));
     SQ_TRY(hip_status(launch_quantize(dY, M, C_out, ld_dY, group, scale, cfg, q_fold, ld_fold, q_t, ld_t,
-                                      layout + kLayoutHeader + ext_max, s),
+                                      layout + kLayoutHeader + ext_max, s, PadGrid(), tiled_of(p)),
                       "quantize"));
     return SQ_OK;
 }
@@ -220,7 +240,10 @@ sq_status sq_gemm_dgrad_workspace_size(int64_t M, int64_t C_out, int64_t C_in, c
     SQ_TRY(check_dims(C_in, C_in, "weight"));
     if (!bytes) return fail(SQ_ERR_INVALID_ARGUMENT, "bytes is NULL");
     const QuantCfg cfg = make_cfg(*p);
-    *bytes = (size_t)round_up(C_in * fold_ext_max(C_out, cfg), 256);
+    // gathered W^T columns of the appended windows [C_in, ext_max] (whole
+    // 16-row groups when tile-major)
+    const int64_t rows = tiled_of(p) ? round_up(C_in, 16) : C_in;
+    *bytes = (size_t)round_up(rows * fold_ext_max(C_out, cfg), 256);
     return SQ_OK;
 }
 
@@ -265,10 +288,10 @@ sq_status sq_quantize_tensor(const float* T, int64_t rows, int64_t cols, int64_t
                              void* stream) {
     SQ_TRY(check_dims(rows, cols, "tensor"));
     if (bits < 2 || bits > 8) return fail(SQ_ERR_INVALID_ARGUMENT, "bits must be in [2, 8]");
-    if (transpose != 0 && transpose != 1) return fail(SQ_ERR_INVALID_ARGUMENT, "transpose must be 0 or 1");
+    if (transpose < 0 || transpose > 2) return fail(SQ_ERR_INVALID_ARGUMENT, "transpose must be 0, 1 or 2");
     if (rows > 0 && cols > 0) {
         SQ_TRY(check_f32(T, ld, cols, "T"));
-        SQ_TRY(check_codes(q, ld_q, transpose ? rows : cols, "q"));
+        SQ_TRY(check_codes_l(q, ld_q, transpose ? rows : cols, transpose == 2, "q"));
     }
     if (!scale || !aligned(scale, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "scale is NULL or misaligned");
     if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
@@ -286,7 +309,7 @@ sq_status sq_quantize_tensor(const float* T, int64_t rows, int64_t cols, int64_t
     SQ_TRY(hip_status(launch_finalize_tensor(partial, slabs, cols, cfg.Q, partial + slabs * cols, scale, s),
                       "finalize"));
     SQ_TRY(hip_status(launch_quantize(T, rows, cols, ld, nullptr, scale, cfg, transpose ? nullptr : q, ld_q,
-                                      transpose ? q : nullptr, ld_q, nullptr, s),
+                                      transpose ? q : nullptr, ld_q, nullptr, s, PadGrid(), transpose == 2),
                       "quantize"));
     return SQ_OK;
 }
@@ -311,8 +334,9 @@ sq_status gemm_dgrad_impl(const int8_t* q_fold, int64_t ld_fold, const int32_t* 
     size_t lay_bytes = 0;
     int64_t min_ld_fold = 0;
     SQ_TRY(sq_grad_layout_size(C_out, p, &lay_bytes, &min_ld_fold));
-    SQ_TRY(check_codes(q_fold, ld_fold, min_ld_fold, "q_fold"));
-    SQ_TRY(check_codes(wq_t, ld_w, C_out > 0 ? C_out : 1, "wq_t"));
+    const bool tiled = tiled_of(p);
+    SQ_TRY(check_codes_l(q_fold, ld_fold, min_ld_fold, tiled, "q_fold"));
+    SQ_TRY(check_codes_l(wq_t, ld_w, C_out > 0 ? C_out : 1, tiled, "wq_t"));
     if (acc) SQ_TRY(check_f32(acc, ld_acc, C_in, "acc"));
     if (dX) SQ_TRY(check_f32(dX, ld_dX, C_in, "dX"));
     const int64_t ext_max = fold_ext_max(C_out, cfg);
@@ -328,14 +352,18 @@ sq_status gemm_dgrad_impl(const int8_t* q_fold, int64_t ld_fold, const int32_t* 
     a.Mg = M; a.Ng = C_in;
     a.A = q_fold; a.lda = ld_fold;
     a.B = wq_t; a.ldb = ld_w;
-    a.K = C_out;
+    // tile-major: K runs over the zero-padded main columns [0, roundup(C_out, 64))
+    a.K = tiled ? round_up(C_out, 64) : C_out;
+    a.tiled = tiled;
     a.layout = layout;
     if (ext_max > 0) {
         int8_t* wext = static_cast<int8_t*>(workspace);
-        SQ_TRY(hip_status(launch_gather_ext(wq_t, ld_w, C_in, layout, wext, ext_max, ext_max, s), "gather"));
-        a.extA = q_fold + fold_ext_base(C_out); a.ld_extA = ld_fold;
+        SQ_TRY(hip_status(launch_gather_ext(wq_t, ld_w, C_in, layout, wext, ext_max, ext_max, s, tiled), "gather"));
+        a.extA = tiled ? q_fold : q_fold + fold_ext_base(C_out); a.ld_extA = ld_fold;
+        a.ext_koff = tiled ? fold_ext_base(C_out) : 0;
         a.extB = wext; a.ld_extB = ext_max;
     }
+    if (tiled && !gemm_pipe_ok(a)) return fail(SQ_ERR_UNSUPPORTED, "tile-major operands past 31-bit offsets");
     a.splits = 1;
     a.acc = acc; a.ld_acc = ld_acc;
     a.out = dX; a.ld_out = ld_dX;
@@ -414,6 +442,7 @@ sq_status sq_gemm_forward(const int8_t* xq_fold, int64_t ld_fold, const int32_t*
                           int64_t C_in, int64_t C_out, const sq_quant_params* p, int32_t* acc, int64_t ld_acc,
                           float* Y, int64_t ld_Y, void* workspace, size_t workspace_bytes, void* stream) {
     SQ_TRY(check_params(p));
+    SQ_TRY(rows_only(p, "sq_gemm_forward"));
     SQ_TRY(check_dims(M, C_in, "activation codes"));
     SQ_TRY(check_dims(C_out, C_out, "weight codes"));
     if (!acc && !Y) return fail(SQ_ERR_INVALID_ARGUMENT, "acc and Y are both NULL");
@@ -484,6 +513,7 @@ sq_status sq_gemm_dgrad_grouped(const int8_t* q_fold, int64_t ld_fold, const int
                                 int64_t ld_acc, float* dX, int64_t ld_dX, void* workspace, size_t workspace_bytes,
                                 void* stream) {
     SQ_TRY(check_params(p));
+    SQ_TRY(rows_only(p, "sq_gemm_dgrad_grouped"));
     SQ_TRY(check_dims(M, C_out, "gradient codes"));
     SQ_TRY(check_dims(C_in, C_in, "weight codes"));
     if (!acc && !dX) return fail(SQ_ERR_INVALID_ARGUMENT, "acc and dX are both NULL");
@@ -496,8 +526,9 @@ sq_status sq_gemm_dgrad_grouped(const int8_t* q_fold, int64_t ld_fold, const int
     size_t lay_bytes = 0;
     int64_t min_ld_fold = 0;
     SQ_TRY(sq_grad_layout_size(C_out, p, &lay_bytes, &min_ld_fold));
-    SQ_TRY(check_codes(q_fold, ld_fold, min_ld_fold, "q_fold"));
-    SQ_TRY(check_codes(wq_t, ld_w, C_out > 0 ? C_out : 1, "wq_t"));
+    const bool tiled = tiled_of(p);
+    SQ_TRY(check_codes_l(q_fold, ld_fold, min_ld_fold, tiled, "q_fold"));
+    SQ_TRY(check_codes_l(wq_t, ld_w, C_out > 0 ? C_out : 1, tiled, "wq_t"));
     if (acc) SQ_TRY(check_f32(acc, ld_acc, C_in, "acc"));
     if (dX) SQ_TRY(check_f32(dX, ld_dX, C_in, "dX"));
     int64_t off_a, off_b, off_p;
@@ -568,6 +599,7 @@ sq_status sq_conv_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* la
                         int32_t PW, const sq_quant_params* p, int32_t* acc, int64_t ld_acc, float* dX,
                         int64_t ld_dX, void* workspace, size_t workspace_bytes, void* stream) {
     SQ_TRY(check_params(p));
+    SQ_TRY(rows_only(p, "sq_conv_dgrad"));
     SQ_TRY(check_conv(N, H, W, C_out, C_in, KH, KW, PH, PW));
     if (!acc && !dX) return fail(SQ_ERR_INVALID_ARGUMENT, "acc and dX are both NULL");
     if (!layout || !gscale || !wscale) return fail(SQ_ERR_INVALID_ARGUMENT, "layout or a scale is NULL");
@@ -584,8 +616,9 @@ sq_status sq_conv_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* la
     size_t lay_bytes = 0;
     int64_t min_ld_fold = 0;
     SQ_TRY(sq_grad_layout_size(C_out, p, &lay_bytes, &min_ld_fold));
-    SQ_TRY(check_codes(q_fold, ld_fold, min_ld_fold, "q_fold"));
-    SQ_TRY(check_codes(wq_t, ld_w, C_out > 0 ? C_out : 1, "wq_t"));
+    const bool tiled = tiled_of(p);
+    SQ_TRY(check_codes_l(q_fold, ld_fold, min_ld_fold, tiled, "q_fold"));
+    SQ_TRY(check_codes_l(wq_t, ld_w, C_out > 0 ? C_out : 1, tiled, "wq_t"));
     if (acc) SQ_TRY(check_f32(acc, ld_acc, C_in, "acc"));
     if (dX) SQ_TRY(check_f32(dX, ld_dX, C_in, "dX"));
     const int64_t ext_max = fold_ext_max(C_out, cfg);
@@ -632,9 +665,10 @@ sq_status sq_gemm_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, c
         return fail(SQ_ERR_OVERFLOW_RISK, "M * Q * 128 reaches 2^31: the int32 accumulator could overflow");
     if (C_out == 0 || C_in == 0) return SQ_OK;
     if (!group) return fail(SQ_ERR_INVALID_ARGUMENT, "group is NULL");
+    const bool tiled = tiled_of(p);
     if (M > 0) {
-        SQ_TRY(check_codes(q_t, ld_t, M, "q_t"));
-        SQ_TRY(check_codes(xq_t, ld_x, M, "xq_t"));
+        SQ_TRY(check_codes_l(q_t, ld_t, M, tiled, "q_t"));
+        SQ_TRY(check_codes_l(xq_t, ld_x, M, tiled, "xq_t"));
     }
     if (acc) SQ_TRY(check_f32(acc, ld_acc, C_in, "acc"));
     if (dW) SQ_TRY(check_f32(dW, ld_dW, C_in, "dW"));
@@ -647,7 +681,10 @@ sq_status sq_gemm_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, c
     a.Mg = C_out; a.Ng = C_in;
     a.A = q_t; a.lda = ld_t;
     a.B = xq_t; a.ldb = ld_x;
-    a.K = M;
+    // tile-major: K runs over the zero-padded token columns [0, roundup(M, 64))
+    a.K = tiled ? round_up(M, 64) : M;
+    a.tiled = tiled;
+    if (tiled && M > 0 && !gemm_pipe_ok(a)) return fail(SQ_ERR_UNSUPPORTED, "tile-major operands past 31-bit offsets");
     a.gs = gscale; a.os = xscale; a.group = group; a.num_groups = cfg.num_groups;
     a.epi_mode = 1;
     if (splits <= 1) {
@@ -751,6 +788,7 @@ sq_status sq_quantize_grad_conv(const float* dY, int64_t N, int64_t H, int64_t W
                                 sq_scale* scale, int32_t* layout, void* workspace, size_t workspace_bytes,
                                 void* stream) {
     SQ_TRY(check_params(p));
+    SQ_TRY(rows_only(p, "sq_quantize_grad_conv"));
     SQ_TRY(check_conv_geom(N, H, W, C_out, 1, KH, KW, PH, PW));
     const ConvGrid g = conv_grid(N, H, W, 1, KH, KW, PH, PW);
     const int64_t M = N * g.Ho * g.Wo;
@@ -807,6 +845,7 @@ sq_status sq_conv_wgrad(const int8_t* q_tp, int64_t ld_tp, const uint8_t* group,
                         const sq_quant_params* p, int32_t* acc, int64_t ld_acc, float* dW, int64_t ld_dW,
                         void* workspace, size_t workspace_bytes, void* stream) {
     SQ_TRY(check_params(p));
+    SQ_TRY(rows_only(p, "sq_conv_wgrad"));
     SQ_TRY(check_conv_geom(N, H, W, C_out, C_in, KH, KW, PH, PW));
     if (!acc && !dW) return fail(SQ_ERR_INVALID_ARGUMENT, "acc and dW are both NULL");
     if (!gscale || !xscale) return fail(SQ_ERR_INVALID_ARGUMENT, "a scale is NULL");
@@ -871,8 +910,8 @@ sq_status sq_quantize_grad_from_ranges(const float* dY, int64_t M, int64_t C_out
     size_t lay_bytes = 0;
     int64_t min_ld_fold = 0;
     SQ_TRY(sq_grad_layout_size(C_out, p, &lay_bytes, &min_ld_fold));
-    if (q_fold && M > 0) SQ_TRY(check_codes(q_fold, ld_fold, min_ld_fold, "q_fold"));
-    if (q_t && C_out > 0) SQ_TRY(check_codes(q_t, ld_t, M > 0 ? M : 1, "q_t"));
+    if (q_fold && M > 0) SQ_TRY(check_codes_l(q_fold, ld_fold, min_ld_fold, tiled_of(p), "q_fold"));
+    if (q_t && C_out > 0) SQ_TRY(check_codes_l(q_t, ld_t, M > 0 ? M : 1, tiled_of(p), "q_t"));
     if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
     if (workspace_bytes < quant_ws_bytes(M, C_out)) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
 
@@ -884,7 +923,7 @@ sq_status sq_quantize_grad_from_ranges(const float* dY, int64_t M, int64_t C_out
         SQ_TRY(hip_status(launch_finalize_grad(ranges, range_slabs, C_out, cfg, rbits, group, scale, layout, ext_max, s),
                           "finalize"));
     SQ_TRY(hip_status(launch_quantize(dY, M, C_out, ld_dY, group, scale, cfg, q_fold, ld_fold, q_t, ld_t,
-                                      layout + kLayoutHeader + ext_max, s),
+                                      layout + kLayoutHeader + ext_max, s, PadGrid(), tiled_of(p)),
                       "quantize"));
     return SQ_OK;
 }
@@ -981,6 +1020,7 @@ sq_status sq_l1bn_backward(const float* dy, int64_t M, int64_t C, int64_t ld_dy,
                            float* dx, int64_t ld_dx, float* dgamma, float* dbeta, uint8_t* group, sq_scale* gscale,
                            uint32_t* dx_ranges, void* workspace, size_t workspace_bytes, void* stream) {
     SQ_TRY(check_params(p));
+    SQ_TRY(rows_only(p, "sq_l1bn_backward"));
     SQ_TRY(check_bn_dims(M, C));
     if (!layer || !aligned(layer, 8)) return fail(SQ_ERR_INVALID_ARGUMENT, "layer is NULL or misaligned");
     if (!gscale || !aligned(gscale, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "gscale is NULL or misaligned");

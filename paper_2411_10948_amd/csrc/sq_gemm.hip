@@ -505,12 +505,21 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
         return __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(base), (short)0, (int)min(rows * ld, (int64_t)0x7FFFFFFF),
                                                  kRsrcFlags);
     };
-    const __amdgpu_buffer_rsrc_t rA = rsrc(p.A, CONV ? p.a_rows : p.Mg, p.lda),
-                                 rB = rsrc(p.B, p.wg_KH ? p.wg_KW * p.wg_Cin : p.Ng, p.ldb);
+    // tile-major operands (p.tiled) hold whole 16-row groups
+    const int64_t rows_a = CONV ? p.a_rows : (p.tiled ? round_up(p.Mg, 16) : p.Mg);
+    const int64_t rows_b = p.wg_KH ? p.wg_KW * p.wg_Cin : (p.tiled ? round_up(p.Ng, 16) : p.Ng);
+    const __amdgpu_buffer_rsrc_t rA = rsrc(p.A, rows_a, p.lda), rB = rsrc(p.B, rows_b, p.ldb);
+    // Row-major: row r at r ld.  Tile-major: the 16 rows of this load
+    // instruction form one contiguous 1 KB tile per K tile, and the K offset
+    // of a tile (scalar) is its index times 1 KB.
     auto lane_off = [&](int i, int64_t first, int64_t rows, int64_t ld) {
         const int r = (i * T::kWaves + wv) * 16 + lr;
-        return (uint32_t)(min(first + r, rows - 1) * ld + 16 * ((lane & 3) ^ swz(r)));
+        const int64_t rr = min(first + r, rows - 1);
+        const int chunk = 16 * ((lane & 3) ^ swz(r));
+        if (p.tiled) return (uint32_t)(tiled_off(rr, 0, ld) + chunk);
+        return (uint32_t)(rr * ld + chunk);
     };
+    auto kbytes = [&](int64_t col) { return (int)(p.tiled ? (col >> 6) << 10 : col); };
     uint32_t offA[T::IA], offB[T::IB];
 #pragma unroll
     for (int i = 0; i < T::IA; ++i) offA[i] = lane_off(i, m0, p.Mg, p.lda);
@@ -575,20 +584,22 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
         }
         if (HORNER && fv.is_ext(t, n_main)) {
             // appended fold columns (a few tiles): offsets computed here
-            const __amdgpu_buffer_rsrc_t rAe = rsrc(p.extA, p.Mg, p.ld_extA), rBe = rsrc(p.extB, p.Ng, p.ld_extB);
-            const int k0 = (int)fv.ext_col(t, n_main);
+            const __amdgpu_buffer_rsrc_t rAe = rsrc(p.extA, p.tiled ? round_up(p.Mg, 16) : p.Mg, p.ld_extA),
+                                         rBe = rsrc(p.extB, p.tiled ? round_up(p.Ng, 16) : p.Ng, p.ld_extB);
+            const int64_t col = fv.ext_col(t, n_main);
+            const int k0a = kbytes(p.ext_koff + col), k0b = kbytes(col);
 #pragma unroll
             for (int i = 0; i < T::IA; ++i)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(rAe, (lds_void_t*)(st + (i * T::kWaves + wv) * 1024), 16,
-                                                         lane_off(i, m0, p.Mg, p.ld_extA), k0, 0, 0);
+                                                         lane_off(i, m0, p.Mg, p.ld_extA), k0a, 0, 0);
 #pragma unroll
             for (int i = 0; i < T::IB; ++i)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(
                     rBe, (lds_void_t*)(st + T::BM * T::BK + (i * T::kWaves + wv) * 1024), 16,
-                    lane_off(i, n0, p.Ng, p.ld_extB), k0, 0, 0);
+                    lane_off(i, n0, p.Ng, p.ld_extB), k0b, 0, 0);
             return;
         }
-        const int k0 = (int)(koff + kbeg + (int64_t)(t - fv.h_tiles) * T::BK);
+        const int k0 = kbytes(koff + kbeg + (int64_t)(t - fv.h_tiles) * T::BK);
 #pragma unroll
         for (int i = 0; i < T::IA; ++i)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void_t*)(st + (i * T::kWaves + wv) * 1024), 16, offA[i],
@@ -1174,14 +1185,17 @@ __global__ __launch_bounds__(256) void k_conv_stream(GemmArgs p, int64_t rows_pe
 
 // Appended B columns of the dgrad fold: wext[k, j] = W^T code of the channel
 // the layout lists for appended column j (0 for padding).
+// Tile-major (tiled): both matrices in tiled_off order.
 __global__ void k_gather_ext(const int8_t* __restrict__ wq_t, int64_t ld_w, int64_t C_in,
-                             const int32_t* __restrict__ layout, int8_t* __restrict__ wext, int64_t ld_ext) {
+                             const int32_t* __restrict__ layout, int8_t* __restrict__ wext, int64_t ld_ext,
+                             int tiled) {
     const int D = layout[1];
     const int32_t* ext = layout + kLayoutHeader;
     for (int64_t k = blockIdx.x; k < C_in; k += gridDim.x)
         for (int j = threadIdx.x; j < D; j += blockDim.x) {
             const int ch = ext[j];
-            wext[k * ld_ext + j] = ch >= 0 ? wq_t[k * ld_w + ch] : (int8_t)0;
+            if (tiled) wext[tiled_off(k, j, ld_ext)] = ch >= 0 ? wq_t[tiled_off(k, ch, ld_w)] : (int8_t)0;
+            else wext[k * ld_ext + j] = ch >= 0 ? wq_t[k * ld_w + ch] : (int8_t)0;
         }
 }
 
@@ -1319,8 +1333,13 @@ hipError_t launch_pipe(const GemmArgs& a, int splits, int64_t k_per_split, hipSt
 // the 31 bits of its buffer loads.
 bool pipe_ok(const GemmArgs& a) {
     auto al16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
-    auto fits = [](int64_t rows, int64_t ld, int64_t cols) { return rows * ld + cols < ((int64_t)1 << 31); };
+    auto fits = [&](int64_t rows, int64_t ld, int64_t cols) {
+        return (a.tiled ? round_up(rows, 16) : rows) * ld + cols < ((int64_t)1 << 31);
+    };
     if (a.K % 64 != 0 || a.lda % 16 != 0 || a.ldb % 16 != 0 || !al16(a.A) || !al16(a.B)) return false;
+    if (a.tiled && (a.lda % 64 != 0 || a.ldb % 64 != 0 || (a.extA && (a.ld_extA % 64 || a.ld_extB % 64 ||
+                                                                     a.ext_koff % 64))))
+        return false;
     if (!fits(a.Mg, a.lda, a.K) || !fits(a.Ng, a.ldb, a.K)) return false;
     if (a.extA) {
         if (a.ld_extA % 16 != 0 || a.ld_extB % 16 != 0 || !al16(a.extA) || !al16(a.extB)) return false;
@@ -1425,6 +1444,8 @@ int wgrad_splits(int64_t M, int64_t C_out, int64_t C_in) {
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     if (a.Mg <= 0 || a.Ng <= 0) return hipSuccess;
     const bool pipe = pipe_ok(a);
+    // tile-major operands: the pipelined kernel only, no convolution
+    if (a.tiled && (!pipe || a.taps || a.wg_KH || a.kseg)) return hipErrorInvalidValue;
     if (a.kseg && (!pipe || a.splits > 1 || a.layout)) return hipErrorInvalidValue;   // pipelined kernel only
     if (a.wg_KH && (!pipe || a.extA || a.layout || a.kseg || a.wg_Cin <= 0 || a.wg_KW <= 0 || a.wg_Wp % 16 != 0 ||
                     a.Ng != (int64_t)a.wg_KH * a.wg_KW * a.wg_Cin ||
@@ -1747,10 +1768,12 @@ hipError_t launch_group_combine(const int32_t* part, int num_groups, int64_t M, 
 }
 
 hipError_t launch_gather_ext(const int8_t* wq_t, int64_t ld_w, int64_t C_in, const int32_t* layout,
-                             int8_t* wext, int64_t ld_ext, int64_t ext_max, hipStream_t s) {
+                             int8_t* wext, int64_t ld_ext, int64_t ext_max, hipStream_t s, bool tiled) {
     if (C_in <= 0 || ext_max <= 0) return hipSuccess;
+    if (tiled && (ld_w % 64 || ld_ext % 64)) return hipErrorInvalidValue;
     const unsigned blocks = (unsigned)std::min<int64_t>(C_in, 4096);
-    hipLaunchKernelGGL(k_gather_ext, dim3(blocks), dim3(64), 0, s, wq_t, ld_w, C_in, layout, wext, ld_ext);
+    hipLaunchKernelGGL(k_gather_ext, dim3(blocks), dim3(64), 0, s, wq_t, ld_w, C_in, layout, wext, ld_ext,
+                       (int)tiled);
     return hipGetLastError();
 }
 

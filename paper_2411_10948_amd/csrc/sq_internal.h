@@ -41,6 +41,16 @@ constexpr int kLayNR = 0, kLayD = 1, kLayBase = 2, kLayF = 3, kLayH = 4, kLaySta
 
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
+// Tile-major code matrix (SQ_LAYOUT_TILED): element (r, k) of a matrix with
+// leading dimension ld (a multiple of 64) sits in the 1 KB tile of rows
+// 16 (r / 16) .. + 15 and columns 64 (k / 64) .. + 63, the tiles of a row
+// group ordered by k, each tile row-major.  The GEMM's operand loads of one
+// K tile then read whole 1 KB blocks of memory instead of 64-byte pieces of
+// rows far apart.
+__host__ __device__ inline int64_t tiled_off(int64_t r, int64_t k, int64_t ld) {
+    return (((r >> 4) * (ld >> 6) + (k >> 6)) << 10) + ((r & 15) << 6) + (k & 63);
+}
+
 // Host-side constants of one quantizer configuration.
 struct QuantCfg {
     int bits;
@@ -90,10 +100,13 @@ struct PadGrid {
 };
 // group == nullptr: every channel in group 0 with shift 0 (per-tensor mode);
 // desc: the channel descriptors of the fold layout (nullptr: all main, t = 0).
+// tiled: q_fold and q_t tile-major (tiled_off), their K padding (q_fold
+// columns [C, roundup(C, 64)), q_t columns [M, roundup(M, 64))) written as
+// zeros; not with a padded pixel grid.
 hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, const uint8_t* group,
                            const sq_scale* scale, const QuantCfg& cfg,
                            int8_t* q_fold, int64_t ld_fold, int8_t* q_t, int64_t ld_t,
-                           const int32_t* desc, hipStream_t s, PadGrid pg = PadGrid());
+                           const int32_t* desc, hipStream_t s, PadGrid pg = PadGrid(), bool tiled = false);
 
 // Per-channel weight quantization: axis 0 one scale per row, axis 1 one per
 // column (partial: colmax scratch, axis 1 only).
@@ -141,6 +154,11 @@ struct GemmArgs {
     // with out: max |out| per 32-row slab and column, as bit patterns,
     // [ceil(Mg / 32), Ng] (producer-side channel ranges of the next quantizer)
     uint32_t* ranges;
+    // A, B, extA and extB tile-major (tiled_off; leading dimensions multiples
+    // of 64, K a multiple of 64); extA is then the whole fold matrix and its
+    // appended columns start at column ext_koff
+    int tiled;
+    int64_t ext_koff;
 };
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
@@ -149,7 +167,7 @@ bool gemm_pipe_ok(const GemmArgs& a);
 // max |x| per 32-row slab and column (bit patterns): ranges [ceil(M / 32), N]
 hipError_t launch_slab_colmax(const float* x, int64_t M, int64_t N, int64_t ld, uint32_t* ranges, hipStream_t s);
 hipError_t launch_gather_ext(const int8_t* wq_t, int64_t ld_w, int64_t C_in, const int32_t* layout,
-                             int8_t* wext, int64_t ld_ext, int64_t ext_max, hipStream_t s);
+                             int8_t* wext, int64_t ld_ext, int64_t ext_max, hipStream_t s, bool tiled = false);
 // Conv dgrad: B operand [C_in, ld_bc] in the order of the conv K sequence;
 // conv_bc_ld(C_out, taps, ext_max) is its leading dimension, enough for any fold.
 inline int64_t conv_bc_ld(int64_t C_out, int64_t taps, int64_t ext_max) {

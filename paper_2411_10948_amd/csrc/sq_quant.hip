@@ -760,7 +760,7 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
                                                      int8_t* __restrict__ q_fold, int64_t ld_fold,
                                                      int8_t* __restrict__ q_t, int64_t ld_t,
                                                      const int32_t* __restrict__ desc, int64_t ext_base,
-                                                     PadGrid pg) {
+                                                     PadGrid pg, int tiled) {
     constexpr int QD = TC / 4;            // channel quads per tile
     constexpr int RQ = kBlock / QD;       // row quads per pass
     constexpr int RP = 4 * RQ;            // rows per pass
@@ -860,7 +860,7 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
                     code[j] = (zero || m >= M || c0 + j >= C) ? 0 : quant_one<SR>(v[i][j], s[j], Qf, u[j]);
                     colw[j] |= (uint32_t)(uint8_t)code[j] << (8 * i);
                 }
-                if (q_fold && m < M && c0 < C) {
+                if (q_fold && m < M && c0 < C && !tiled) {
                     int8_t* row = q_fold + m * ld_fold;
                     uint32_t word = 0u;
 #pragma unroll
@@ -876,6 +876,17 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
                         for (int j = 0; j < 4; ++j)
                             if (c0 + j < C) row[c0 + j] = (int8_t)(word >> (8 * j));
                     }
+                } else if (q_fold && m < M && c0 < ext_base && tiled) {
+                    // tile-major: the quad's 4 bytes are contiguous; codes of
+                    // channels >= C (K padding of the main columns) are 0
+                    uint32_t word = 0u;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const uint32_t f = (uint32_t)(uint8_t)(code[j] * (1 << t[j]));
+                        if (pos[j] < 0) word |= f << (8 * j);
+                        else if (c0 + j < C) q_fold[tiled_off(m, ext_base + pos[j], ld_fold)] = (int8_t)f;
+                    }
+                    *reinterpret_cast<uint32_t*>(q_fold + tiled_off(m, c0, ld_fold)) = word;
                 }
             }
             if (q_t) {
@@ -914,6 +925,16 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
             for (int it = 0; it < TC * CPR / kBlock; ++it) {
                 const int ch = ch0 + it * (kBlock / CPR);
                 const int64_t c = ct * TC + ch;
+                if (tiled) {
+                    // tile-major: 16 codes of a channel row are contiguous;
+                    // rows past M hold 0 (K padding up to a multiple of 64)
+                    if (c < C && m < round_up(M, 64)) {
+                        const uint32_t* src = &tq[ch * TW + 4 * part];
+                        *reinterpret_cast<uint4*>(q_t + tiled_off(c, m, ld_t)) =
+                            make_uint4(src[0], src[1], src[2], src[3]);
+                    }
+                    continue;
+                }
                 if (c >= C || m >= M) continue;
                 const uint32_t* src = &tq[ch * TW + 4 * part];
                 int8_t* row = q_t + c * ld_t;
@@ -1082,8 +1103,9 @@ constexpr int64_t kQuantMinTiles = 1024;    // four blocks per CU
 
 hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, const uint8_t* group,
                            const sq_scale* scale, const QuantCfg& cfg, int8_t* q_fold, int64_t ld_fold,
-                           int8_t* q_t, int64_t ld_t, const int32_t* desc, hipStream_t s, PadGrid pg) {
+                           int8_t* q_t, int64_t ld_t, const int32_t* desc, hipStream_t s, PadGrid pg, bool tiled) {
     if (M <= 0 || C <= 0) return hipSuccess;
+    if (tiled && (pg.Wo || (q_fold && ld_fold % 64) || (q_t && ld_t % 64))) return hipErrorInvalidValue;
     const bool vec = ((ld & 3) == 0) && ((reinterpret_cast<uintptr_t>(x) & 15) == 0);
     const bool sr = cfg.round_mode == SQ_ROUND_STOCHASTIC;
     // 128 x 128 tiles where the tensor gives enough of them to fill the chip
@@ -1098,13 +1120,13 @@ hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, con
 #define SQ_LAUNCH_QUANT(TC, TR)                                                                                  \
     do {                                                                                                         \
         if (vec && sr) hipLaunchKernelGGL((k_quantize<TC, TR, 4, true>), grid, dim3(kBlock), 0, s, x, M, C, ld,  \
-                                          group, scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, pg);              \
+                                          group, scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, pg, (int)tiled);              \
         else if (vec) hipLaunchKernelGGL((k_quantize<TC, TR, 4, false>), grid, dim3(kBlock), 0, s, x, M, C, ld,  \
-                                         group, scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, pg);               \
+                                         group, scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, pg, (int)tiled);               \
         else if (sr) hipLaunchKernelGGL((k_quantize<TC, TR, 1, true>), grid, dim3(kBlock), 0, s, x, M, C, ld,    \
-                                        group, scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, pg);                \
+                                        group, scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, pg, (int)tiled);                \
         else hipLaunchKernelGGL((k_quantize<TC, TR, 1, false>), grid, dim3(kBlock), 0, s, x, M, C, ld, group,    \
-                                scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, pg);                               \
+                                scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, pg, (int)tiled);                               \
     } while (0)
     if (tc == 64 && tr == 64) SQ_LAUNCH_QUANT(64, 64);
     else if (tc == 64) SQ_LAUNCH_QUANT(64, 128);

@@ -28,6 +28,8 @@ LIB_PATH = os.path.join(_HERE, "libshiftquant.so")
 SQ_OK = 0
 STATUS_NAMES = {0: "SQ_OK", 1: "SQ_ERR_INVALID_ARGUMENT", 2: "SQ_ERR_OVERFLOW_RISK",
                 3: "SQ_ERR_UNSUPPORTED", 4: "SQ_ERR_WORKSPACE_TOO_SMALL", 5: "SQ_ERR_HIP"}
+LAYOUT_ROWS = 0
+LAYOUT_TILED = 1
 ROUND_NEAREST_EVEN = 0
 ROUND_STOCHASTIC = 1
 FLAG_NONFINITE = 1
@@ -57,12 +59,36 @@ class ShiftQuantError(RuntimeError):
 class Params(ct.Structure):
     """sq_quant_params"""
     _fields_ = [("bits", ct.c_int32), ("num_groups", ct.c_int32), ("round_mode", ct.c_int32),
-                ("reserved", ct.c_int32), ("seed", ct.c_uint64), ("offset", ct.c_uint64)]
+                ("layout", ct.c_int32), ("seed", ct.c_uint64), ("offset", ct.c_uint64)]
 
     @classmethod
     def make(cls, bits: int, num_groups: int = 4, round_mode: int = ROUND_NEAREST_EVEN,
-             seed: int = 0, offset: int = 0) -> "Params":
-        return cls(bits, num_groups, round_mode, 0, seed, offset)
+             seed: int = 0, offset: int = 0, layout: int = 0) -> "Params":
+        return cls(bits, num_groups, round_mode, layout, seed, offset)
+
+    @property
+    def tiled(self) -> bool:
+        return self.layout == LAYOUT_TILED
+
+
+def code_matrix(rows: int, cols: int, tiled: bool, device) -> torch.Tensor:
+    """A zero-filled int8 code matrix [rows, ld] for the given layout: ld a
+    multiple of 16 (row-major) or of 64 covering the K padding (tile-major,
+    storage for whole 16-row groups).  Returned as the first `rows` rows of
+    the allocation, so stride(0) is ld."""
+    if tiled:
+        ld = round_up(max(cols, 1), 64)
+        return torch.zeros((round_up(max(rows, 1), 16), ld), dtype=torch.int8, device=device)[:rows]
+    return torch.zeros((max(rows, 1), round_up(max(cols, 1), 16)), dtype=torch.int8, device=device)[:rows]
+
+
+def untile(t: torch.Tensor) -> torch.Tensor:
+    """Row-major copy [rows, ld] of a tile-major code matrix made by
+    code_matrix(..., tiled=True)."""
+    rows, ld = t.shape[0], t.stride(0)
+    r16 = round_up(max(rows, 1), 16)
+    full = t.as_strided((r16 // 16, ld // 64, 16, 64), (16 * ld, 1024, 64, 1))
+    return full.permute(0, 2, 1, 3).reshape(r16, ld)[:rows]
 
 
 _P = ct.c_void_p
@@ -441,7 +467,8 @@ def _workspace(nbytes: int, device) -> Optional[torch.Tensor]:
 
 @dataclasses.dataclass
 class GradCodes:
-    """Output of sq_quantize_grad for one gradient tensor."""
+    """Output of sq_quantize_grad for one gradient tensor (code matrices in the
+    layout params.layout names)."""
     q_fold: torch.Tensor      # [M, ld_fold] int8, dgrad operand
     q_t: torch.Tensor         # [C_out, ld_t] int8, codes transposed (wgrad operand)
     group: torch.Tensor       # [C_out] uint8
@@ -452,18 +479,23 @@ class GradCodes:
     C_out: int
 
     def codes(self) -> torch.Tensor:
-        """The codes [M, C_out] themselves (a view of q_t, transposed)."""
-        return self.q_t[:, :self.M].t()
+        """The codes [M, C_out] themselves (q_t transposed)."""
+        qt = untile(self.q_t) if self.params.tiled else self.q_t
+        return qt[:, :self.M].t()
+
+    def fold_rows(self) -> torch.Tensor:
+        """q_fold as a row-major [M, ld_fold] matrix (a copy when tile-major)."""
+        return untile(self.q_fold) if self.params.tiled else self.q_fold
 
 
 def quantize_grad(dY: torch.Tensor, bits: int, num_groups: int = 4, round_mode: int = ROUND_NEAREST_EVEN,
-                  seed: int = 0, offset: int = 0, stream=None) -> GradCodes:
+                  seed: int = 0, offset: int = 0, stream=None, tiled: bool = False) -> GradCodes:
     M, C = dY.shape
     dev = dY.device
-    p = Params.make(bits, num_groups, round_mode, seed, offset)
+    p = Params.make(bits, num_groups, round_mode, seed, offset, LAYOUT_TILED if tiled else LAYOUT_ROWS)
     lay_bytes, min_ld = sq_grad_layout_size(C, p)
-    q_fold = torch.zeros((max(M, 1), min_ld), dtype=torch.int8, device=dev)[:M]
-    q_t = torch.zeros((max(C, 1), round_up(max(M, 1), 16)), dtype=torch.int8, device=dev)[:C]
+    q_fold = code_matrix(M, min_ld, tiled, dev)
+    q_t = code_matrix(C, M, tiled, dev)
     group = torch.empty(max(C, 1), dtype=torch.uint8, device=dev)[:C]
     scale = new_scale(dev)
     layout = torch.zeros(lay_bytes // 4, dtype=torch.int32, device=dev)
@@ -472,16 +504,19 @@ def quantize_grad(dY: torch.Tensor, bits: int, num_groups: int = 4, round_mode: 
     return GradCodes(q_fold, q_t, group, scale, layout, p, M, C)
 
 
-def quantize_tensor(T: torch.Tensor, bits: int = 8, transpose: bool = True, stream=None):
+def quantize_tensor(T: torch.Tensor, bits: int = 8, transpose: bool = True, stream=None, tiled: bool = False):
+    """Per-tensor codes of T; transpose: [cols, rows] (the GEMM operand),
+    tiled: that matrix tile-major (transpose = 2 of the C call)."""
     rows, cols = T.shape
     dev = T.device
     if transpose:
-        q = torch.zeros((max(cols, 1), round_up(max(rows, 1), 16)), dtype=torch.int8, device=dev)[:cols]
+        q = code_matrix(cols, rows, tiled, dev)
     else:
-        q = torch.zeros((max(rows, 1), round_up(max(cols, 1), 16)), dtype=torch.int8, device=dev)[:rows]
+        assert not tiled, "tile-major codes are transposed"
+        q = code_matrix(rows, cols, False, dev)
     scale = new_scale(dev)
     ws = _workspace(sq_quantize_tensor_workspace_size(rows, cols), dev)
-    sq_quantize_tensor(T, bits, transpose, q, scale, ws, stream)
+    sq_quantize_tensor(T, bits, 2 if tiled else int(transpose), q, scale, ws, stream)
     return q, scale
 
 
@@ -570,15 +605,15 @@ def gemm_wgrad(codes: GradCodes, xq_t: torch.Tensor, xscale: torch.Tensor, want_
 
 def quantize_grad_from_ranges(dY: torch.Tensor, ranges: torch.Tensor, bits: int, num_groups: int = 4,
                               round_mode: int = ROUND_NEAREST_EVEN, seed: int = 0, offset: int = 0,
-                              stream=None) -> GradCodes:
+                              stream=None, tiled: bool = False) -> GradCodes:
     """quantize_grad with the channel ranges given as partial maxima
     ranges [slabs, C] (uint32 bit patterns, as int32) from the producer of dY."""
     M, C = dY.shape
     dev = dY.device
-    p = Params.make(bits, num_groups, round_mode, seed, offset)
+    p = Params.make(bits, num_groups, round_mode, seed, offset, LAYOUT_TILED if tiled else LAYOUT_ROWS)
     lay_bytes, min_ld = sq_grad_layout_size(C, p)
-    q_fold = torch.zeros((max(M, 1), min_ld), dtype=torch.int8, device=dev)[:M]
-    q_t = torch.zeros((max(C, 1), round_up(max(M, 1), 16)), dtype=torch.int8, device=dev)[:C]
+    q_fold = code_matrix(M, min_ld, tiled, dev)
+    q_t = code_matrix(C, M, tiled, dev)
     group = torch.empty(max(C, 1), dtype=torch.uint8, device=dev)[:C]
     scale = new_scale(dev)
     layout = torch.zeros(lay_bytes // 4, dtype=torch.int32, device=dev)
@@ -702,8 +737,10 @@ class BackwardPlan:
                                       device=torch.device(device)) if dx_ranges else None)
         dev = torch.device(device)
         lay_bytes, min_ld = sq_grad_layout_size(C_out, params)
-        self.q_fold = torch.zeros((M, min_ld), dtype=torch.int8, device=dev)
-        self.q_t = torch.zeros((C_out, round_up(M, 16)), dtype=torch.int8, device=dev)
+        # code matrices in the layout params.layout names (W^T and X^T codes
+        # passed to dgrad / wgrad must be in the same one)
+        self.q_fold = code_matrix(M, min_ld, params.tiled, dev)
+        self.q_t = code_matrix(C_out, M, params.tiled, dev)
         self.group = torch.empty(C_out, dtype=torch.uint8, device=dev)
         self.scale = new_scale(dev)
         self.layout = torch.zeros(lay_bytes // 4, dtype=torch.int32, device=dev)

@@ -83,7 +83,7 @@ def test_invalid_params_rejected(sq):
         assert L.sq_grad_layout_size(64, ct.byref(p), ct.byref(nb), ct.byref(ld)) == 1
         assert sq.sq_last_error()
     p = sq.Params.make(4, 4, 0)
-    p.reserved = 1
+    p.layout = 2
     assert L.sq_grad_layout_size(64, ct.byref(p), ct.byref(nb), ct.byref(ld)) == 1
     assert L.sq_grad_layout_size(64, None, ct.byref(nb), ct.byref(ld)) == 1
 

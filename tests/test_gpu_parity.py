@@ -116,12 +116,16 @@ def check_fold(codes, q_ref, g_ref, bits, ng, rows=None):
     assert np.array_equal(lay[32 + ext_max:32 + ext_max + C], ((pos + 1) << 4) | t)
     if q_ref.shape[0] == 0:
         return
+    fold = codes.q_fold
+    if codes.params.tiled:   # tile-major: compare the row-major matrix it encodes
+        from paper_2411_10948_amd import shiftquant
+        fold = shiftquant.untile(fold)
     if rows is None:
-        qf = codes.q_fold.cpu().numpy().astype(np.int64)
+        qf = fold.cpu().numpy().astype(np.int64)
         shifted = q_ref.astype(np.int64) << t[None, :]
     else:
         import torch
-        qf = codes.q_fold.index_select(0, torch.as_tensor(rows, device="cuda")).cpu().numpy().astype(np.int64)
+        qf = fold.index_select(0, torch.as_tensor(rows, device="cuda")).cpu().numpy().astype(np.int64)
         shifted = q_ref[rows].astype(np.int64) << t[None, :]
     main = pos < 0
     assert np.array_equal(qf[:, :C][:, main], shifted[:, main]), "main fold columns"
@@ -147,14 +151,19 @@ def check_quant(sq, codes, dY, bits, ng, mode, seed, offset, fold_rows=None):
     return q_ref, g_ref, s_ref
 
 
+def _rows(sq, t, tiled):
+    """A code matrix as row-major (a copy when tile-major)."""
+    return sq.untile(t) if tiled else t
+
+
 def check_layer(sq, dY, W, X, bits, ng, mode=0, seed=0, offset=0, dgrad_rows=None, wgrad_rows=None,
-                want_acc=True, fold_rows=None):
+                want_acc=True, fold_rows=None, tiled=False):
     import torch
     M, C_out = dY.shape
     C_in = W.shape[1]
-    codes = sq.quantize_grad(_dev(dY), bits, ng, mode, seed, offset)
-    wq_t, ws = sq.quantize_tensor(_dev(W), 8, transpose=True)
-    xq_t, xs = sq.quantize_tensor(_dev(X), 8, transpose=True)
+    codes = sq.quantize_grad(_dev(dY), bits, ng, mode, seed, offset, tiled=tiled)
+    wq_t, ws = sq.quantize_tensor(_dev(W), 8, transpose=True, tiled=tiled)
+    xq_t, xs = sq.quantize_tensor(_dev(X), 8, transpose=True, tiled=tiled)
     acc_d, dX = sq.gemm_dgrad(codes, wq_t, ws, want_acc=want_acc)
     acc_w, dW = sq.gemm_wgrad(codes, xq_t, xs, want_acc=want_acc)
     torch.cuda.synchronize()
@@ -162,8 +171,8 @@ def check_layer(sq, dY, W, X, bits, ng, mode=0, seed=0, offset=0, dgrad_rows=Non
 
     wq_ref, ws_ref = oracle.quantize_tensor(W, 8)
     xq_ref, xs_ref = oracle.quantize_tensor(X, 8)
-    assert np.array_equal(wq_t[:, :C_out].t().cpu().numpy(), wq_ref)
-    assert np.array_equal(xq_t[:, :M].t().cpu().numpy(), xq_ref)
+    assert np.array_equal(_rows(sq, wq_t, tiled)[:, :C_out].t().cpu().numpy(), wq_ref)
+    assert np.array_equal(_rows(sq, xq_t, tiled)[:, :M].t().cpu().numpy(), xq_ref)
     for got, ref in ((ws, ws_ref), (xs, xs_ref)):
         h = sq.scale_to_host(got)
         assert h["bits"][:3] == [_f32bits(ref["r_max"]), _f32bits(ref["inv0"]), _f32bits(ref["d0"])]
@@ -731,26 +740,27 @@ def test_workload_full_size(sq, name):
     wl = workloads.WORKLOADS[name]
     d = workloads.make_inputs(name)
     M, C_out, C_in = d["M"], wl.C_out, wl.C_in
-    print(f"[full-size parity] {name} M={M} C_out={C_out} C_in={C_in}", flush=True)
-    p = sq.Params.make(wl.bits, wl.num_groups, wl.round_mode, wl.sr_seed, wl.sr_offset)
+    # the launch configuration bench.py times: tile-major code matrices
+    print(f"[full-size parity] {name} M={M} C_out={C_out} C_in={C_in} (tile-major)", flush=True)
+    p = sq.Params.make(wl.bits, wl.num_groups, wl.round_mode, wl.sr_seed, wl.sr_offset, sq.LAYOUT_TILED)
     plan = sq.BackwardPlan(M, C_out, C_in, p, want_acc=True)
     dY = _dev(d["dY"])
-    wq_t, ws = sq.quantize_tensor(_dev(d["W"]), 8)
-    xq_t, xs = sq.quantize_tensor(_dev(d["X"]), 8)
+    wq_t, ws = sq.quantize_tensor(_dev(d["W"]), 8, tiled=True)
+    xq_t, xs = sq.quantize_tensor(_dev(d["X"]), 8, tiled=True)
     plan.run(dY, wq_t, ws, xq_t, xs)
     torch.cuda.synchronize()
 
     q_ref, g_ref, s_ref, _ = oracle.quantize_grad(d["dY"], wl.bits, wl.num_groups, wl.round_mode,
                                                   wl.sr_seed, wl.sr_offset)
-    q = plan.q_t[:, :M].t().cpu().numpy()
+    q = sq.untile(plan.q_t)[:, :M].t().cpu().numpy()
     assert np.array_equal(plan.group.cpu().numpy(), g_ref)
     assert np.array_equal(q, q_ref)
     fold_rows = np.unique(np.r_[0, M - 1, np.random.default_rng(2).integers(0, M, 64)])
     check_fold(plan, q_ref, g_ref, wl.bits, wl.num_groups, fold_rows)
     wq_ref, ws_ref = oracle.quantize_tensor(d["W"], 8)
     xq_ref, xs_ref = oracle.quantize_tensor(d["X"], 8)
-    assert np.array_equal(wq_t[:, :C_out].t().cpu().numpy(), wq_ref)
-    assert np.array_equal(xq_t[:, :M].t().cpu().numpy(), xq_ref)
+    assert np.array_equal(sq.untile(wq_t)[:, :C_out].t().cpu().numpy(), wq_ref)
+    assert np.array_equal(sq.untile(xq_t)[:, :M].t().cpu().numpy(), xq_ref)
 
     rng = np.random.default_rng(0)
     n_d = 24 if C_out * C_in > 1e7 else 96
@@ -769,4 +779,4 @@ def test_workload_full_size(sq, name):
     np.testing.assert_allclose(plan.dW.index_select(0, rw).cpu().numpy(), dW_ref, rtol=RTOL, atol=0)
     # properties that hold at any size, checked on the whole outputs
     assert torch.isfinite(plan.dX).all() and torch.isfinite(plan.dW).all()
-    assert plan.q_t[:, :M].abs().max().item() == (1 << (wl.bits - 1)) - 1
+    assert sq.untile(plan.q_t)[:, :M].abs().max().item() == (1 << (wl.bits - 1)) - 1
