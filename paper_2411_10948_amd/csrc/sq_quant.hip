@@ -76,6 +76,21 @@ __device__ __forceinline__ int quant_one(float x, float s, float Qf, uint32_t u1
     return (int)qf;
 }
 
+// The same code as a float (an exact integer in [-Q, Q]).
+template <bool SR>
+__device__ __forceinline__ float quant_onef(float x, float s, float Qf, uint32_t u16) {
+    const float v = __fmul_rn(x, s);
+    float qf;
+    if (SR) {
+        const float l = floorf(v);
+        const float f = __fsub_rn(v, l);
+        qf = ((float)u16 < __fmul_rn(f, 65536.0f)) ? __fadd_rn(l, 1.0f) : l;
+    } else {
+        qf = rintf(v);
+    }
+    return fminf(fmaxf(qf, -Qf), Qf);
+}
+
 __device__ __forceinline__ uint32_t absbits(float x) { return __float_as_uint(x) & 0x7FFFFFFFu; }
 
 // ---------------------------------------------------------------------------
@@ -963,6 +978,148 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
     }
 }
 
+// ---------------------------------------------------------------------------
+// Quantize, 8-channel form: the same codes and layouts as k_quantize for
+// 16-byte aligned inputs with C a multiple of 8 (no padded pixel grid).  A
+// thread quantizes 8 consecutive channels of 4 consecutive rows; the 8
+// elements of a row form one Philox block (indices m C + c0 .. + 7 with c0 a
+// multiple of 8), so each thread draws its own uniforms and no lane exchange
+// is needed.  Tiles of 128 rows x 64 channels; the codes of a tile are
+// transposed through LDS (4 rows per word) for q_t.  Each row's 8
+// shift-folded codes leave as one 8-byte store.
+// ---------------------------------------------------------------------------
+template <bool SR, bool TL>
+__global__ __launch_bounds__(kBlock) void k_quantize8(const float* __restrict__ x, int64_t M, int64_t C, int64_t ld,
+                                                      const uint8_t* __restrict__ group,
+                                                      const sq_scale* __restrict__ scale, QuantCfg cfg,
+                                                      int8_t* __restrict__ q_fold, int64_t ld_fold,
+                                                      int8_t* __restrict__ q_t, int64_t ld_t,
+                                                      const int32_t* __restrict__ desc, int64_t ext_base,
+                                                      int meta_vec) {
+    constexpr int TR = 128, TC = 64, TW = TR / 4 + 1;   // LDS words per channel row (padded)
+    __shared__ uint32_t tq[TC * TW];
+    const int tid = threadIdx.x, g8 = tid & 7, rq = tid >> 3;
+    const int64_t ctiles = (C + TC - 1) / TC, rtiles = (M + TR - 1) / TR;
+    const sq_scale sc = *scale;
+    const bool zero = sc.flags != 0u;
+    const float Qf = (float)cfg.Q;
+    // q_t rows written: the codes, and with the tile-major layout their zero
+    // padding up to a multiple of 64
+    const int64_t m_t = TL ? round_up(M, 64) : M;
+    auto at_fold = [&](int64_t m, int64_t k) { return TL ? tiled_off(m, k, ld_fold) : m * ld_fold + k; };
+
+    for (int64_t tile = blockIdx.x; tile < ctiles * rtiles; tile += gridDim.x) {
+        const int64_t ct = tile % ctiles, rt = tile / ctiles;
+        const int64_t c0 = ct * TC + 8 * g8, m0 = rt * TR + 4 * rq;
+        const bool cin = c0 < C;   // C % 8 == 0: all 8 channels or none
+        // per channel: scale, fold factor 2^t in its main column (0 for an
+        // appended channel, whose main column holds 0), appended position
+        uint32_t gw[2] = {0u, 0u};
+        int32_t dw[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        if (cin) {
+            if (meta_vec) {
+                if (group) {
+                    const uint2 g2 = *reinterpret_cast<const uint2*>(group + c0);
+                    gw[0] = g2.x; gw[1] = g2.y;
+                }
+                if (desc) {
+                    const int4 d0 = *reinterpret_cast<const int4*>(desc + c0);
+                    const int4 d1 = *reinterpret_cast<const int4*>(desc + c0 + 4);
+                    dw[0] = d0.x; dw[1] = d0.y; dw[2] = d0.z; dw[3] = d0.w;
+                    dw[4] = d1.x; dw[5] = d1.y; dw[6] = d1.z; dw[7] = d1.w;
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    if (group) gw[j >> 2] |= (uint32_t)group[c0 + j] << (8 * (j & 3));
+                    if (desc) dw[j] = desc[c0 + j];
+                }
+            }
+        }
+        float s[8], tf[8];
+        bool any_ext = false;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            s[j] = __fmul_rn(sc.inv, pow2f((int)((gw[j >> 2] >> (8 * (j & 3))) & 0xFFu)));
+            const int pos = (dw[j] >> 4) - 1;
+            tf[j] = pos < 0 ? pow2f(dw[j] & 15) : 0.0f;
+            any_ext |= pos >= 0;
+        }
+        // the bytes below are built as code + 128 (unsigned), then flipped
+        // back to two's complement with one xor per word
+        uint32_t colw[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};   // channel j, rows m0 .. m0 + 3
+        const bool rows_in = rt * TR + TR <= M;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int64_t m = m0 + i;
+            const bool ok = cin && !zero && (rows_in || m < M);
+            float v[8];
+            if (ok) {
+                const float4 a = *reinterpret_cast<const float4*>(x + m * ld + c0);
+                const float4 b = *reinterpret_cast<const float4*>(x + m * ld + c0 + 4);
+                v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+            } else {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) v[j] = 0.f;
+            }
+            U4 w{0u, 0u, 0u, 0u};
+            if (SR && ok) w = philox_block((uint64_t)(m * C + c0) >> 3, cfg);
+            uint32_t lo = 0u, hi = 0u;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const uint32_t u = SR ? (pick(w, j >> 1) >> (16 * (j & 1))) & 0xFFFFu : 0u;
+                const float q = ok ? quant_onef<SR>(v[j], s[j], Qf, u) : 0.0f;
+                colw[j] = __builtin_amdgcn_cvt_pk_u8_f32(__fadd_rn(q, 128.0f), i, colw[j]);
+                const float qf = __fadd_rn(__fmul_rn(q, tf[j]), 128.0f);
+                if (j < 4) lo = __builtin_amdgcn_cvt_pk_u8_f32(qf, j, lo);
+                else hi = __builtin_amdgcn_cvt_pk_u8_f32(qf, j - 4, hi);
+            }
+            if (q_fold && (rows_in || m < M)) {
+                if (cin) {
+                    if (any_ext) {
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) {
+                            const int pos = (dw[j] >> 4) - 1;
+                            if (pos >= 0) {
+                                const int code = (int)((colw[j] >> (8 * i)) & 0xFFu) - 128;
+                                q_fold[at_fold(m, ext_base + pos)] = (int8_t)(code * (1 << (dw[j] & 15)));
+                            }
+                        }
+                    }
+                    *reinterpret_cast<uint2*>(q_fold + at_fold(m, c0)) = make_uint2(lo ^ 0x80808080u, hi ^ 0x80808080u);
+                } else if (TL && c0 < ext_base) {
+                    // K padding of the main columns
+                    *reinterpret_cast<uint2*>(q_fold + at_fold(m, c0)) = make_uint2(0u, 0u);
+                }
+            }
+        }
+        if (q_t) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) tq[(8 * g8 + j) * TW + rq] = colw[j] ^ 0x80808080u;
+            __syncthreads();
+            // channel row ch of the tile, rows 32 part .. + 31 (two 16-byte chunks)
+            const int ch = tid >> 2, part = tid & 3;
+            const int64_t c = ct * TC + ch, mm = rt * TR + 32 * part;
+            if (c < C && mm < m_t) {
+                const uint32_t* src = &tq[ch * TW + 8 * part];
+                const uint4 a = make_uint4(src[0], src[1], src[2], src[3]);
+                const uint4 b = make_uint4(src[4], src[5], src[6], src[7]);
+                if (TL) {
+                    *reinterpret_cast<uint4*>(q_t + tiled_off(c, mm, ld_t)) = a;
+                    *reinterpret_cast<uint4*>(q_t + tiled_off(c, mm + 16, ld_t)) = b;
+                } else if (mm + 32 <= M) {
+                    *reinterpret_cast<uint4*>(q_t + c * ld_t + mm) = a;
+                    *reinterpret_cast<uint4*>(q_t + c * ld_t + mm + 16) = b;
+                } else {
+                    for (int r = 0; r < (int)(M - mm); ++r)
+                        q_t[c * ld_t + mm + r] = (int8_t)(src[r / 4] >> (8 * (r % 4)));
+                }
+            }
+            __syncthreads();
+        }
+    }
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -1115,8 +1272,24 @@ hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, con
     int tc = (C <= 64 || sr) ? 64 : 128, tr = 128;
     if (n_tiles(tc, tr) < kQuantMinTiles) tr = 64;
     if (n_tiles(tc, tr) < kQuantMinTiles) tc = 64;
-    const dim3 grid((unsigned)std::min<int64_t>(n_tiles(tc, tr), kQuantMaxBlocks));
     const int64_t eb = fold_ext_base(C);
+    if (vec && C % 8 == 0 && !pg.Wo) {
+        // 8-channel form: one Philox block per thread and row; the groups
+        // (8 bytes) and descriptors (2 x 16 bytes) of a thread's channels
+        // load as vectors when aligned
+        const int mv = ((reinterpret_cast<uintptr_t>(group) & 7) == 0 && (reinterpret_cast<uintptr_t>(desc) & 15) == 0);
+        const dim3 g8((unsigned)std::min<int64_t>(((C + 63) / 64) * ((M + 127) / 128), kQuantMaxBlocks));
+        if (sr && tiled) hipLaunchKernelGGL((k_quantize8<true, true>), g8, dim3(kBlock), 0, s, x, M, C, ld, group, scale,
+                                            cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, mv);
+        else if (sr) hipLaunchKernelGGL((k_quantize8<true, false>), g8, dim3(kBlock), 0, s, x, M, C, ld, group, scale,
+                                        cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, mv);
+        else if (tiled) hipLaunchKernelGGL((k_quantize8<false, true>), g8, dim3(kBlock), 0, s, x, M, C, ld, group,
+                                           scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, mv);
+        else hipLaunchKernelGGL((k_quantize8<false, false>), g8, dim3(kBlock), 0, s, x, M, C, ld, group, scale, cfg,
+                                q_fold, ld_fold, q_t, ld_t, desc, eb, mv);
+        return hipGetLastError();
+    }
+    const dim3 grid((unsigned)std::min<int64_t>(n_tiles(tc, tr), kQuantMaxBlocks));
 #define SQ_LAUNCH_QUANT(TC, TR)                                                                                  \
     do {                                                                                                         \
         if (vec && sr) hipLaunchKernelGGL((k_quantize<TC, TR, 4, true>), grid, dim3(kBlock), 0, s, x, M, C, ld,  \
