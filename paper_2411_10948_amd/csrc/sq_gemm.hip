@@ -622,6 +622,29 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
     // compile time by the two-step unrolled loop below)
     v4i fa[2][T::KSTEPS][T::FM], fb[2][T::KSTEPS][T::FN];
     const int lrow = lane % T::MF, lc = lane / T::MF;
+    // This lane's byte offset in a stage is fixed: r * BK + 16 (c ^ swz(r))
+    // depends on r only through r mod 8, which every 16-row fragment shares,
+    // so each fragment read is one base register plus a compile-time offset
+    // (fragment, operand, stage) once the loop is unrolled over the stages.
+    static_assert(T::KSTEPS == 1 && T::MF == 16 && T::TM % 8 == 0 && T::TN % 8 == 0, "fixed-offset fragment reads");
+    const int lane_base_a = [&] {
+        const int r = wm * T::TM + lrow;
+        return r * T::BK + 16 * (lc ^ swz(r));
+    }();
+    const int lane_base_b = [&] {
+        const int r = wn * T::TN + lrow;
+        return r * T::BK + 16 * (lc ^ swz(r));
+    }();
+    auto read_frags_at = [&](auto STG, auto BUF) {
+        constexpr int buf = decltype(BUF)::value, stg = decltype(STG)::value;
+#pragma unroll
+        for (int i = 0; i < T::FM; ++i)
+            fa[buf][0][i] = *reinterpret_cast<const v4i*>(smem + stg * T::kStage + lane_base_a + i * T::MF * T::BK);
+#pragma unroll
+        for (int j = 0; j < T::FN; ++j)
+            fb[buf][0][j] = *reinterpret_cast<const v4i*>(smem + stg * T::kStage + T::BM * T::BK + lane_base_b +
+                                                           j * T::MF * T::BK);
+    };
     auto read_frags = [&](int t, auto BUF) {
         constexpr int buf = decltype(BUF)::value;
         const int8_t* sA = smem + (t % T::STAGES) * T::kStage;
@@ -641,14 +664,16 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
             }
         }
     };
+    // B fragment outer: the first MFMAs of a tile need the A fragments and
+    // the first B fragment only, so they start before the later reads land
     auto mfmas = [&](auto BUF) {
         constexpr int buf = decltype(BUF)::value;
 #pragma unroll
         for (int ks = 0; ks < T::KSTEPS; ++ks)
 #pragma unroll
-            for (int i = 0; i < T::FM; ++i)
+            for (int j = 0; j < T::FN; ++j)
 #pragma unroll
-                for (int j = 0; j < T::FN; ++j) acc[i][j] = MF::run(fb[buf][ks][j], fa[buf][ks][i], acc[i][j]);
+                for (int i = 0; i < T::FM; ++i) acc[i][j] = MF::run(fb[buf][ks][j], fa[buf][ks][i], acc[i][j]);
     };
     // this wave's loads of a tile are complete once at most `later` younger
     // tiles remain in flight
@@ -664,7 +689,7 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
     // on the last tile too (of a stale stage, never used), which keeps the
     // loop body free of branches around LDS reads, so the compiler's counter
     // waits before the MFMAs leave the new reads in flight.
-    auto step = [&](int t, auto CUR, auto NXT) {
+    auto step = [&](int t, auto CUR, auto NXT, auto STG_NXT) {
         wait_tile(min(T::STAGES - 3, n_tiles - 2 - t));
         __builtin_amdgcn_s_barrier();
         if (t + T::STAGES - 1 < n_tiles) issue(t + T::STAGES - 1);
@@ -677,7 +702,7 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
 #pragma unroll
                 for (int j = 0; j < T::FN; ++j) acc[i][j] = acc[i][j] << sft;
         }
-        read_frags(t + 1, NXT);
+        read_frags_at(STG_NXT, NXT);
         mfmas(CUR);
         // issue order: the LDS reads of the next tile spread between the
         // MFMAs of this one (each group: a share of MFMAs, then one read), so
@@ -700,9 +725,17 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
         wait_tile(min(T::STAGES - 2, n_tiles - 1));
         __builtin_amdgcn_s_barrier();
         read_frags(0, std::integral_constant<int, 0>());
-        for (int t = 0; t < n_tiles; t += 2) {
-            step(t, std::integral_constant<int, 0>(), std::integral_constant<int, 1>());
-            if (t + 1 < n_tiles) step(t + 1, std::integral_constant<int, 1>(), std::integral_constant<int, 0>());
+        // unrolled over the 4 stages (tile t + 1 sits in stage (t + 1) % 4)
+        using I0 = std::integral_constant<int, 0>;
+        using I1 = std::integral_constant<int, 1>;
+        using I2 = std::integral_constant<int, 2>;
+        using I3 = std::integral_constant<int, 3>;
+        static_assert(T::STAGES == 4, "loop unrolled over 4 stages");
+        for (int t = 0; t < n_tiles; t += 4) {
+            step(t, I0(), I1(), I1());
+            if (t + 1 < n_tiles) step(t + 1, I1(), I0(), I2());
+            if (t + 2 < n_tiles) step(t + 2, I0(), I1(), I3());
+            if (t + 3 < n_tiles) step(t + 3, I1(), I0(), I0());
         }
     }
 
