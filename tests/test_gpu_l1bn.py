@@ -2,11 +2,11 @@
 producer-side channel ranges with the CPU oracle, through the C-ABI.
 
 Integer state (mean / sigma codes, sign and deviation sums, groups, scale
-bits, codes) must match bit for bit; fp32 outputs within 1e-6 of the
-magnitude of their terms (the same IEEE operations run in the same order on
-both sides, so they are expected to be identical).  Inputs are seeded and
-synthetic: post-ReLU or signed activations quantized to 8 bits, gradients
-with log-normal channel scales.
+bits, codes) and the fp32 outputs y, dx, dgamma and dbeta must match bit
+for bit (both sides run the same IEEE operations in the same order, with the
+binary64 channel constants rounded once).  Inputs are seeded and synthetic:
+post-ReLU or signed activations quantized to 8 bits, gradients with
+log-normal channel scales.
 """
 import numpy as np
 import pytest
@@ -65,8 +65,7 @@ def _check_against_oracle(sq, X, gamma, beta, dy, bits=8, ng=4, mode=0, seed=3, 
     assert lay["flags"] == (2 if f["dev_max"] == 0 else 0)
     np.testing.assert_array_equal(np.float32(lay["x_step"]), np.float32(xs_ref["d0"]))
     yd = y.cpu().numpy()
-    mag = np.abs(f["kappa"] * (xq_ref.astype(np.float32) - f["mu"])) + np.abs(f["beta_q"])
-    assert np.all(np.abs(yd - f["y"]) <= RTOL * mag), float(np.max(np.abs(yd - f["y"])))
+    _bits_equal(yd, f["y"], "y")
 
     r = oracle.l1bn_backward(dy, f, xq_ref, bits, ng, mode, seed, offset)
     np.testing.assert_array_equal(b["group"].cpu().numpy(), r["group"])
@@ -74,16 +73,25 @@ def _check_against_oracle(sq, X, gamma, beta, dy, bits=8, ng=4, mode=0, seed=3, 
     assert np.float32(gs["step"]) == np.float32(r["gscale"]["d0"])
     assert gs["flags"] == r["gscale"]["flags"]
     dx = b["dx"].cpu().numpy()
-    assert np.all(np.abs(dx - r["dx"]) <= RTOL * (np.abs(r["dx"]) + np.abs(dx).max(axis=0) * 1e-3 + 1e-30)), \
-        float(np.max(np.abs(dx - r["dx"])))
+    _bits_equal(dx, r["dx"], "dx")
     for k in ("dgamma", "dbeta"):
-        v = b[k].cpu().numpy()
-        np.testing.assert_allclose(v, r[k], rtol=RTOL, atol=RTOL * (np.abs(r[k]).max() + 1e-30), err_msg=k)
-    # producer-side ranges: their maximum over slabs is max |dx| of each channel
+        _bits_equal(b[k].cpu().numpy(), r[k], k)
+    # producer-side ranges: their maximum over slabs is max |dx| of each
+    # channel of the oracle's dx, and no slab exceeds it
     rg = b["ranges"].cpu().numpy().view(np.uint32)
     assert rg.shape == (sq.sq_l1bn_range_slabs(M, C), C)
-    np.testing.assert_array_equal(rg.max(axis=0), (dx.view(np.uint32) & 0x7FFFFFFF).max(axis=0))
-    return dx, b
+    ref_max = (np.ascontiguousarray(r["dx"]).view(np.uint32) & 0x7FFFFFFF).max(axis=0)
+    np.testing.assert_array_equal(rg.max(axis=0), ref_max)
+    return dx, b, r
+
+
+def _bits_equal(got, ref, name):
+    """fp32 arrays equal bit for bit (every NaN payload and signed zero)."""
+    g = np.ascontiguousarray(got, np.float32).view(np.uint32)
+    r = np.ascontiguousarray(ref, np.float32).view(np.uint32)
+    bad = np.argwhere(g != r)
+    assert bad.size == 0, (f"{name}: {len(bad)} values differ, first at {bad[:3].tolist()}: "
+                           f"{got.reshape(g.shape)[tuple(bad[0])]} vs {ref.reshape(r.shape)[tuple(bad[0])]}")
 
 
 L1BN_CASES = [
@@ -114,7 +122,7 @@ def test_l1bn_constant_channels(sq):
     gamma = rng.normal(1, 0.3, C).astype(np.float32)
     beta = rng.normal(0, 0.5, C).astype(np.float32)
     dy = rng.normal(size=(M, C)).astype(np.float32)
-    dx, b = _check_against_oracle(sq, X, gamma, beta, dy)
+    dx, b, _ = _check_against_oracle(sq, X, gamma, beta, dy)
     assert np.all(dx == 0)
 
 
@@ -127,16 +135,19 @@ def test_l1bn_resnet18_layer_full_size(sq):
 
 @pytest.mark.parametrize("bits,ng,mode", [(4, 4, 0), (6, 4, 1)])
 def test_quantize_from_producer_ranges_equals_quantize(sq, bits, ng, mode):
-    # the layer's dx with the ranges it wrote, quantized for the conv below,
-    # equals quantizing dx with the quantizer's own abs-max pass
+    # the layer's dx with the ranges it wrote, quantized for the conv below:
+    # codes, groups and scale equal the oracle's quantizer on the oracle's dx,
+    # and everything equals the quantizer's own abs-max pass
     import torch
+    from tests.test_gpu_parity import check_quant
     print(f"from ranges b={bits} mode={mode}", flush=True)
     X, gamma, beta, dy = _inputs(5003, 64, seed=bits + mode)
-    _, _, _, _, b = _run(sq, X, gamma, beta, dy)
+    dx_h, b, r = _check_against_oracle(sq, X, gamma, beta, dy)
     dx, ranges = b["dx"], b["ranges"]
     a = sq.quantize_grad(dx, bits, ng, mode, seed=4, offset=9)
     c = sq.quantize_grad_from_ranges(dx, ranges, bits, ng, mode, seed=4, offset=9)
     torch.cuda.synchronize()
+    check_quant(sq, c, r["dx"], bits, ng, mode, 4, 9)
     for name in ("q_fold", "q_t", "group", "layout"):
         assert torch.equal(getattr(a, name), getattr(c, name)), name
     assert torch.equal(a.scale, c.scale)
@@ -158,6 +169,8 @@ def test_quantize_from_ranges_arbitrary_slabs(sq):
     a = sq.quantize_grad(d, 6, 4)
     c = sq.quantize_grad_from_ranges(d, ranges, 6, 4)
     torch.cuda.synchronize()
+    from tests.test_gpu_parity import check_quant
+    check_quant(sq, c, dY, 6, 4, 0, 0, 0)   # against the oracle's quantizer of dY
     for name in ("q_fold", "q_t", "group", "layout"):
         assert torch.equal(getattr(a, name), getattr(c, name)), name
     assert torch.equal(a.scale, c.scale)

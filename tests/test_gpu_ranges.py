@@ -1,12 +1,14 @@
-"""Producer-side channel ranges from the loss-propagation GEMM (sq_gemm_dgrad_ranged):
-dX equals sq_gemm_dgrad's bit for bit, every 32-row slab maximum equals the
-maximum of |dX| over those rows (bit patterns), and quantizing dX with those
-ranges gives exactly the codes, groups, scale and layout of the quantizer's own
-abs-max pass.  Inputs are seeded and synthetic."""
+"""Producer-side channel ranges from the loss-propagation GEMM (sq_gemm_dgrad_ranged),
+anchored on the oracle: dX equals the oracle's dX bit for bit (and
+sq_gemm_dgrad's), every 32-row slab maximum equals the maximum of the oracle's
+|dX| over those rows (bit patterns), and quantizing dX with those ranges gives
+the oracle quantizer's codes, groups and scale on the oracle's dX (and exactly
+the quantizer's own abs-max pass).  Inputs are seeded and synthetic."""
 import numpy as np
 import pytest
 
-from tests.test_gpu_parity import _dev, _grad
+import oracle
+from tests.test_gpu_parity import _dev, _grad, check_quant
 
 pytestmark = pytest.mark.gpu
 
@@ -52,7 +54,13 @@ def test_dgrad_ranges(sq, case):
                             codes.params, None, dX, ranges, ws_d)
     torch.cuda.synchronize()
     assert torch.equal(dX, dX0)
-    xb = dX.cpu().numpy().view(np.uint32) & 0x7FFFFFFF
+    # the oracle's dX of the same layer
+    oracle.set_threads(16)
+    q_ref, g_ref, s_ref, _ = oracle.quantize_grad(dY, bits, ng)
+    wq_ref, ws_ref = oracle.quantize_tensor(Wt, 8)
+    dX_ref = oracle.dequant_dgrad(oracle.dgrad(q_ref, g_ref, ng, wq_ref), s_ref["d0"], ws_ref["d0"], ng)
+    np.testing.assert_array_equal(dX.cpu().numpy().view(np.uint32), dX_ref.view(np.uint32))
+    xb = dX_ref.view(np.uint32) & 0x7FFFFFFF
     pad = slabs * 32 - M
     ref = np.concatenate([xb, np.zeros((pad, C_in), np.uint32)]).reshape(slabs, 32, C_in).max(axis=1)
     np.testing.assert_array_equal(ranges.cpu().numpy().view(np.uint32), ref)
@@ -60,6 +68,7 @@ def test_dgrad_ranges(sq, case):
     a = sq.quantize_grad(dX, bits, ng)
     b = sq.quantize_grad_from_ranges(dX, ranges, bits, ng)
     torch.cuda.synchronize()
+    check_quant(sq, b, dX_ref, bits, ng, 0, 0, 0)
     for name in ("q_fold", "q_t", "group", "layout"):
         assert torch.equal(getattr(a, name), getattr(b, name)), name
     assert torch.equal(a.scale, b.scale)
