@@ -406,6 +406,73 @@ def summarize_steps(times, ops):
             "value_at_median": ops / (med * 1e-3) / 1e12}
 
 
+def run_conv_chain(args, torch, sq):
+    """Two ResNet-18 stage-1 conv layers backward in sequence (64 x 56 x 56,
+    64 -> 64 channels, 3x3, pad 1, 4-bit gradients): the upper layer's input
+    gradient is the lower layer's output gradient.  With --fused-ranges the
+    upper layer's conv dgrad also writes the channel ranges of its dX and the
+    lower layer's quantizer takes them instead of its own abs-max pass over dX."""
+    import numpy as np
+    from paper_2411_10948_amd import workloads
+    d = workloads.make_inputs("resnet18_conv3x3")
+    wl = d["workload"]
+    N, H, W, C = 64, 56, 56, 64
+    dev = torch.device("cuda:0")
+    p = sq.Params.make(wl.bits, wl.num_groups, wl.round_mode)
+    dY = torch.from_numpy(d["dY"]).to(dev)
+    W2 = torch.from_numpy(d["W"]).to(dev)
+    W1 = torch.flip(W2, dims=(0,)).contiguous()      # a second layer's weights (same distribution)
+    w2_t, w2_s = sq.quantize_tensor(W2, 8, transpose=True)
+    w1_t, w1_s = sq.quantize_tensor(W1, 8, transpose=True)
+    Xc = torch.from_numpy(np.ascontiguousarray(d["X"][:, 4 * C:5 * C])).to(dev)
+    xq_raw, xs = sq.quantize_tensor(Xc, 8, transpose=True)
+    xpk = sq.conv_pack_input(xq_raw, N, H, W, 3, 3, 1, 1)
+    del xq_raw, W1, W2
+    fused = args.fused_ranges
+    up = sq.ConvBackwardPlan(N, H, W, C, C, 3, 3, 1, 1, p, device=dev, dx_ranges=fused)
+    lo = sq.ConvBackwardPlan(N, H, W, C, C, 3, 3, 1, 1, p, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def quant_lo():
+        if fused:
+            lo.quantize_from_ranges(up.dX, up.dX_ranges, stream, range_slabs=up.range_slabs)
+        else:
+            lo.quantize(up.dX, stream)
+
+    def step():
+        up.run(dY, w2_t, w2_s, xpk, xs, stream)
+        quant_lo()
+        lo.dgrad(w1_t, w1_s, stream)
+        lo.wgrad(xpk, xs, stream)
+
+    def timed(fn, K):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(K):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / K
+
+    for _ in range(args.warmup):
+        step()
+    ms = timed(step, args.steps)
+    ops = 2 * 4 * (N * H * W) * C * 9 * C
+    out = {"metric": "ShiftQuant backward TOPS (quantize+dgrad+wgrad) and % of int8 MFMA peak",
+           "value": ops / (ms * 1e-3) / 1e12, "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "int8", "data": "synthetic",
+           "config": {"workload": "resnet18_conv3x3_chain", "step": "conv_chain", "layers": 2, "N": N, "H": H,
+                      "W": W, "C": C, "bits": wl.bits, "num_groups": wl.num_groups, "rounding": "nearest-even",
+                      "lower_quantizer_ranges": "from the upper layer's conv dgrad" if fused else "abs-max pass",
+                      "parallelism": "none"},
+           "breakdown_ms": {"upper conv dgrad": timed(lambda: up.dgrad(w2_t, w2_s, stream), args.steps),
+                            "lower quantize": timed(quant_lo, args.steps)}}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -418,8 +485,8 @@ def main(argv=None):
     ap.add_argument("--rounding", choices=["rtn", "sr"], default=None,
                     help="override the workload's rounding (variant runs)")
     ap.add_argument("--fused-ranges", action="store_true",
-                    help="--step chain: the down-projection's dgrad writes the up-projection quantizer's ranges")
-    ap.add_argument("--step", choices=["backward", "forward", "l1bn", "chain"], default="backward",
+                    help="--step chain / conv_chain: the upper layer's dgrad writes the lower quantizer's ranges")
+    ap.add_argument("--step", choices=["backward", "forward", "l1bn", "chain", "conv_chain"], default="backward",
                     help="forward: quantize X with ShiftQuant + Y = X W^T (per-output-channel W); "
                          "l1bn: the L1BNQ layer (workloads resnet18_bn_56x56x64, resnet50_bn_14x14x1024, "
                          "transformer_bn_768)")
@@ -451,6 +518,8 @@ def main(argv=None):
         return run_l1bn(args, torch, sq)
     if args.step == "chain":
         return run_chain(args, torch, sq)
+    if args.step == "conv_chain":
+        return run_conv_chain(args, torch, sq)
     conv = args.workload in FUSED_CONV
     wl = workloads.WORKLOADS[FUSED_CONV.get(args.workload, args.workload)]
     # parameter variants of the same layer (same tensors, other b / N_G / rounding)

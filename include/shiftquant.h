@@ -408,6 +408,34 @@ sq_status sq_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_t ld_
                      int32_t num_groups, float* out, int64_t ld_out, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * sq_conv_dgrad_ranged -- sq_conv_dgrad that also writes the channel ranges
+ * of dX for the quantizer of the layer below.
+ *
+ * Sec. 3.1's r_c = max_m |dY[m, c]| of the next layer's gradient, taken as
+ * the conv input gradient dX [N H W, C_in] is stored:
+ *   dX_ranges[s, c] = bits of max |dX[m, c]| over rows m in [s R, (s+1) R),
+ * sign bit cleared, s < *range_slabs = ceil(N H W / R), R = *range_rows.
+ * The streaming kernel (C_out <= 64 with one fold window, C_in <= 64 and a
+ * multiple of 4, same-size window of at most 9 taps) takes them per block of
+ * its own rows (R a multiple of 128, at most 512 slabs); the other conv
+ * kernels store dX and one pass takes 32-row slab maxima (R = 32).
+ * dX_ranges must hold sq_gemm_dgrad_range_slabs(N H W) x C_in words (the
+ * most either path writes).  *range_slabs and *range_rows (host memory) are
+ * set before the call returns, so the caller passes the slab count on to
+ * sq_quantize_grad_from_ranges / sq_quantize_grad_conv_from_ranges without a
+ * synchronization.  Arguments, outputs and errors as sq_conv_dgrad, with dX
+ * required; SQ_ERR_UNSUPPORTED beyond 2^21 input pixels.
+ * ------------------------------------------------------------------------- */
+sq_status sq_conv_dgrad_ranged(const int8_t* q_fold, int64_t ld_fold, const int32_t* layout,
+                               const uint8_t* group, const sq_scale* gscale,
+                               const int8_t* wq_t, int64_t ld_w, const sq_scale* wscale,
+                               int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t C_in,
+                               int32_t KH, int32_t KW, int32_t PH, int32_t PW, const sq_quant_params* p,
+                               int32_t* acc, int64_t ld_acc, float* dX, int64_t ld_dX,
+                               uint32_t* dX_ranges, int64_t* range_slabs, int64_t* range_rows,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * sq_gemm_dgrad_ranged -- sq_gemm_dgrad that also writes the channel ranges
  * of dX for the quantizer of the layer below.
  *
@@ -460,6 +488,9 @@ sq_status sq_gemm_dgrad_ranged(const int8_t* q_fold, int64_t ld_fold, const int3
  *   dY [N Ho Wo, ld_dY] (same codes, groups, scale, layout, q_fold, workspace)
  *   that writes the transposed codes straight onto the padded grid: q_tp's
  *   padding is never written, so the caller zero-fills that buffer once.
+ * sq_quantize_grad_conv_from_ranges is the same with the channel ranges
+ *   given as partial maxima (see sq_quantize_grad_from_ranges), e.g. the
+ *   dX_ranges of sq_conv_dgrad_ranged of the layer above.
  * sq_conv_wgrad runs one int8 GEMM (K = the padded grid, rounded up to 64)
  *   whose B rows are xs at the taps' row offsets.
  * Outputs: acc [C_out, ld_acc] int32 and/or dW [C_out, ld_dW] fp32, each row
@@ -482,6 +513,12 @@ sq_status sq_quantize_grad_conv(const float* dY, int64_t N, int64_t H, int64_t W
                                 int8_t* q_fold, int64_t ld_fold, int8_t* q_tp, int64_t ld_tp,
                                 uint8_t* group, sq_scale* scale, int32_t* layout,
                                 void* workspace, size_t workspace_bytes, void* stream);
+sq_status sq_quantize_grad_conv_from_ranges(const float* dY, int64_t N, int64_t H, int64_t W, int64_t C_out,
+                                            int64_t ld_dY, int32_t KH, int32_t KW, int32_t PH, int32_t PW,
+                                            const sq_quant_params* p, const uint32_t* ranges, int64_t range_slabs,
+                                            int8_t* q_fold, int64_t ld_fold, int8_t* q_tp, int64_t ld_tp,
+                                            uint8_t* group, sq_scale* scale, int32_t* layout,
+                                            void* workspace, size_t workspace_bytes, void* stream);
 sq_status sq_conv_wgrad_workspace_size(int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t C_in,
                                        int32_t KH, int32_t KW, int32_t PH, int32_t PW,
                                        const sq_quant_params* p, size_t* bytes);

@@ -593,11 +593,12 @@ sq_status sq_conv_dgrad_workspace_size(int64_t C_out, int64_t C_in, int32_t KH, 
     return SQ_OK;
 }
 
-sq_status sq_conv_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* layout, const uint8_t* group,
-                        const sq_scale* gscale, const int8_t* wq_t, int64_t ld_w, const sq_scale* wscale, int64_t N,
-                        int64_t H, int64_t W, int64_t C_out, int64_t C_in, int32_t KH, int32_t KW, int32_t PH,
-                        int32_t PW, const sq_quant_params* p, int32_t* acc, int64_t ld_acc, float* dX,
-                        int64_t ld_dX, void* workspace, size_t workspace_bytes, void* stream) {
+static sq_status conv_dgrad_impl(const int8_t* q_fold, int64_t ld_fold, const int32_t* layout, const uint8_t* group,
+                                 const sq_scale* gscale, const int8_t* wq_t, int64_t ld_w, const sq_scale* wscale,
+                                 int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t C_in, int32_t KH, int32_t KW,
+                                 int32_t PH, int32_t PW, const sq_quant_params* p, int32_t* acc, int64_t ld_acc,
+                                 float* dX, int64_t ld_dX, uint32_t* ranges, int64_t* range_rows, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
     SQ_TRY(check_params(p));
     SQ_TRY(rows_only(p, "sq_conv_dgrad"));
     SQ_TRY(check_conv(N, H, W, C_out, C_in, KH, KW, PH, PW));
@@ -647,7 +648,39 @@ sq_status sq_conv_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* la
     a.gs = gscale; a.os = wscale; a.group = group; a.num_groups = cfg.num_groups;
     a.taps = (int)taps; a.cv_KW = KW; a.cv_PH = PH; a.cv_PW = PW;
     a.cv_H = H; a.cv_W = W; a.cv_Ho = Ho; a.cv_Wo = Wo; a.a_rows = N * Ho * Wo;
-    return hip_status(launch_conv_dgrad(a, bc, ld_bc, s), "conv_dgrad");
+    a.ranges = ranges;
+    return hip_status(launch_conv_dgrad(a, bc, ld_bc, s, range_rows), "conv_dgrad");
+}
+
+sq_status sq_conv_dgrad(const int8_t* q_fold, int64_t ld_fold, const int32_t* layout, const uint8_t* group,
+                        const sq_scale* gscale, const int8_t* wq_t, int64_t ld_w, const sq_scale* wscale, int64_t N,
+                        int64_t H, int64_t W, int64_t C_out, int64_t C_in, int32_t KH, int32_t KW, int32_t PH,
+                        int32_t PW, const sq_quant_params* p, int32_t* acc, int64_t ld_acc, float* dX,
+                        int64_t ld_dX, void* workspace, size_t workspace_bytes, void* stream) {
+    return conv_dgrad_impl(q_fold, ld_fold, layout, group, gscale, wq_t, ld_w, wscale, N, H, W, C_out, C_in, KH, KW,
+                           PH, PW, p, acc, ld_acc, dX, ld_dX, nullptr, nullptr, workspace, workspace_bytes, stream);
+}
+
+sq_status sq_conv_dgrad_ranged(const int8_t* q_fold, int64_t ld_fold, const int32_t* layout, const uint8_t* group,
+                               const sq_scale* gscale, const int8_t* wq_t, int64_t ld_w, const sq_scale* wscale,
+                               int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t C_in, int32_t KH, int32_t KW,
+                               int32_t PH, int32_t PW, const sq_quant_params* p, int32_t* acc, int64_t ld_acc,
+                               float* dX, int64_t ld_dX, uint32_t* dX_ranges, int64_t* range_slabs,
+                               int64_t* range_rows, void* workspace, size_t workspace_bytes, void* stream) {
+    if (!dX) return fail(SQ_ERR_INVALID_ARGUMENT, "dX is NULL (the ranges are those of dX)");
+    if (!range_slabs || !range_rows) return fail(SQ_ERR_INVALID_ARGUMENT, "range_slabs or range_rows is NULL");
+    if (!dX_ranges || !aligned(dX_ranges, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "dX_ranges is NULL or misaligned");
+    const int64_t pixels = N * H * W;
+    if (pixels > 0 && (pixels + 31) / 32 > 65535)
+        return fail(SQ_ERR_UNSUPPORTED, "dX ranges support at most 2^21 input pixels here");
+    *range_slabs = 0;
+    *range_rows = 0;
+    int64_t rows = 0;
+    SQ_TRY(conv_dgrad_impl(q_fold, ld_fold, layout, group, gscale, wq_t, ld_w, wscale, N, H, W, C_out, C_in, KH, KW,
+                           PH, PW, p, acc, ld_acc, dX, ld_dX, dX_ranges, &rows, workspace, workspace_bytes, stream));
+    *range_rows = rows;
+    *range_slabs = rows > 0 ? (pixels + rows - 1) / rows : 0;
+    return SQ_OK;
 }
 
 sq_status sq_gemm_wgrad(const int8_t* q_t, int64_t ld_t, const uint8_t* group, const sq_scale* gscale,
@@ -782,11 +815,14 @@ sq_status sq_conv_pack_grad(const int8_t* q_t, int64_t ld_t, int64_t N, int64_t 
                       "conv pack gradient");
 }
 
-sq_status sq_quantize_grad_conv(const float* dY, int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t ld_dY,
-                                int32_t KH, int32_t KW, int32_t PH, int32_t PW, const sq_quant_params* p,
-                                int8_t* q_fold, int64_t ld_fold, int8_t* q_tp, int64_t ld_tp, uint8_t* group,
-                                sq_scale* scale, int32_t* layout, void* workspace, size_t workspace_bytes,
-                                void* stream) {
+// ranges == nullptr: the quantizer's own abs-max pass; else the channel
+// ranges as partial maxima [range_slabs, C_out] from the producer of dY
+static sq_status quantize_grad_conv_impl(const float* dY, int64_t N, int64_t H, int64_t W, int64_t C_out,
+                                         int64_t ld_dY, int32_t KH, int32_t KW, int32_t PH, int32_t PW,
+                                         const sq_quant_params* p, const uint32_t* ranges, int64_t range_slabs,
+                                         int8_t* q_fold, int64_t ld_fold, int8_t* q_tp, int64_t ld_tp,
+                                         uint8_t* group, sq_scale* scale, int32_t* layout, void* workspace,
+                                         size_t workspace_bytes, void* stream) {
     SQ_TRY(check_params(p));
     SQ_TRY(rows_only(p, "sq_quantize_grad_conv"));
     SQ_TRY(check_conv_geom(N, H, W, C_out, 1, KH, KW, PH, PW));
@@ -804,18 +840,27 @@ sq_status sq_quantize_grad_conv(const float* dY, int64_t N, int64_t H, int64_t W
     SQ_TRY(sq_grad_layout_size(C_out, p, &lay_bytes, &min_ld_fold));
     if (q_fold) SQ_TRY(check_codes(q_fold, ld_fold, min_ld_fold, "q_fold"));
     if (C_out > 0) SQ_TRY(check_codes(q_tp, ld_tp, g.ld_q, "q_tp"));
+    if (ranges && C_out > 0 && (!aligned(ranges, 4) || range_slabs < 1 || range_slabs >= kMaxRows))
+        return fail(SQ_ERR_INVALID_ARGUMENT, "ranges misaligned or range_slabs < 1");
     if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
     if (workspace_bytes < quant_ws_bytes(M, C_out)) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
 
     const QuantCfg cfg = make_cfg(*p);
     hipStream_t s = static_cast<hipStream_t>(stream);
     uint32_t* partial = static_cast<uint32_t*>(workspace);
-    int64_t slabs = 0;
-    SQ_TRY(hip_status(launch_colmax(dY, M, C_out, ld_dY, partial, &slabs, s), "colmax"));
     const int64_t ext_max = fold_ext_max(C_out, cfg);
-    SQ_TRY(hip_status(launch_finalize_grad(partial, slabs, C_out, cfg, partial + slabs * C_out, group, scale, layout,
-                                           ext_max, s),
-                      "finalize"));
+    if (ranges) {
+        if (C_out > 0)
+            SQ_TRY(hip_status(launch_finalize_grad(ranges, range_slabs, C_out, cfg, partial, group, scale, layout,
+                                                   ext_max, s),
+                              "finalize"));
+    } else {
+        int64_t slabs = 0;
+        SQ_TRY(hip_status(launch_colmax(dY, M, C_out, ld_dY, partial, &slabs, s), "colmax"));
+        SQ_TRY(hip_status(launch_finalize_grad(partial, slabs, C_out, cfg, partial + slabs * C_out, group, scale,
+                                               layout, ext_max, s),
+                          "finalize"));
+    }
     PadGrid pg;
     pg.Wo = (uint32_t)g.Wo;
     pg.HoWo = (uint32_t)(g.Ho * g.Wo);
@@ -825,6 +870,26 @@ sq_status sq_quantize_grad_conv(const float* dY, int64_t N, int64_t H, int64_t W
                                       layout + kLayoutHeader + ext_max, s, pg),
                       "quantize"));
     return SQ_OK;
+}
+
+sq_status sq_quantize_grad_conv(const float* dY, int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t ld_dY,
+                                int32_t KH, int32_t KW, int32_t PH, int32_t PW, const sq_quant_params* p,
+                                int8_t* q_fold, int64_t ld_fold, int8_t* q_tp, int64_t ld_tp, uint8_t* group,
+                                sq_scale* scale, int32_t* layout, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+    return quantize_grad_conv_impl(dY, N, H, W, C_out, ld_dY, KH, KW, PH, PW, p, nullptr, 0, q_fold, ld_fold, q_tp,
+                                   ld_tp, group, scale, layout, workspace, workspace_bytes, stream);
+}
+
+sq_status sq_quantize_grad_conv_from_ranges(const float* dY, int64_t N, int64_t H, int64_t W, int64_t C_out,
+                                            int64_t ld_dY, int32_t KH, int32_t KW, int32_t PH, int32_t PW,
+                                            const sq_quant_params* p, const uint32_t* ranges, int64_t range_slabs,
+                                            int8_t* q_fold, int64_t ld_fold, int8_t* q_tp, int64_t ld_tp,
+                                            uint8_t* group, sq_scale* scale, int32_t* layout, void* workspace,
+                                            size_t workspace_bytes, void* stream) {
+    if (C_out > 0 && !ranges) return fail(SQ_ERR_INVALID_ARGUMENT, "ranges is NULL");
+    return quantize_grad_conv_impl(dY, N, H, W, C_out, ld_dY, KH, KW, PH, PW, p, ranges, range_slabs, q_fold, ld_fold,
+                                   q_tp, ld_tp, group, scale, layout, workspace, workspace_bytes, stream);
 }
 
 sq_status sq_conv_wgrad_workspace_size(int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t C_in, int32_t KH,

@@ -1051,7 +1051,10 @@ constexpr int kStreamBlocks = 512;
 template <class T>
 __device__ __forceinline__ void opaque(T& v) { asm volatile("" : "+v"(v)); }
 
-template <bool ACC, bool FULLK>
+// RANGES: the block also writes max |dX| of each channel over its rows
+// (bit patterns, sign cleared) to row blockIdx.x of p.ranges [blocks, Ng]:
+// the producer-side channel ranges of the next layer's quantizer.
+template <bool ACC, bool FULLK, bool RANGES = false>
 __global__ __launch_bounds__(256) void k_conv_stream(GemmArgs p, int64_t rows_per_block) {
 #if defined(__HIP_DEVICE_COMPILE__)
     constexpr int BK = 64, kRing = kStreamRing * 64 * BK;
@@ -1130,6 +1133,11 @@ __global__ __launch_bounds__(256) void k_conv_stream(GemmArgs p, int64_t rows_pe
     // fp32 only: the fold's final shift goes into the scale, exactly
     // ((float)(v << f) * a == (float)v * (a * 2^f) while neither overflows)
     const float alpha_o = ACC ? alpha : __fmul_rn(alpha, pow2f(fsh));
+    uint32_t rmx[RANGES ? 4 : 1][4];   // this lane's maxima of |dX|, columns j * 16 + lc * 4 + e
+#pragma unroll
+    for (int j = 0; j < (RANGES ? 4 : 1); ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) rmx[j][e] = 0u;
     for (int k = 0; k < steps; ++k) {
         load_chunk(2 * k + kStreamNW + 2 * kStreamPF - 2);
         load_chunk(2 * k + kStreamNW + 2 * kStreamPF - 1);
@@ -1196,6 +1204,10 @@ __global__ __launch_bounds__(256) void k_conv_stream(GemmArgs p, int64_t rows_pe
                 int oo = ok ? (int)((prow * (uint32_t)p.ld_out + (uint32_t)col) * 4u) : (int)0x80000000;
                 opaque(oo);
                 __builtin_amdgcn_raw_buffer_store_b128(fo, rO, oo, 0, 0);
+                if constexpr (RANGES) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) rmx[j][e] = max(rmx[j][e], ok ? fo[e] & 0x7FFFFFFFu : 0u);
+                }
                 if constexpr (ACC) {
                     const u4 io = {(unsigned)v0, (unsigned)v1, (unsigned)v2, (unsigned)v3};
                     int oc = ok ? (int)((prow * (uint32_t)p.ld_acc + (uint32_t)col) * 4u) : (int)0x80000000;
@@ -1212,6 +1224,27 @@ __global__ __launch_bounds__(256) void k_conv_stream(GemmArgs p, int64_t rows_pe
             if (ih[h] >= (uint32_t)H) ih[h] -= (uint32_t)H;
         }
         __builtin_amdgcn_s_barrier();   // the ring slots of this step may be refilled
+    }
+    if constexpr (RANGES) {
+        // maximum over the 16 rows of a DPP row (same lc), then over the 4
+        // waves through LDS: the weight rows, no longer read after the last
+        // barrier and never a target of the ring's prefetches still in flight
+        uint32_t* red = reinterpret_cast<uint32_t*>(smem + kRing);   // [4 waves][64 columns]
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) rmx[j][e] = row16_max(rmx[j][e]);
+        if (lrow == 0) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) red[wv * 64 + j * 16 + lc * 4 + e] = rmx[j][e];
+        }
+        __syncthreads();
+        if (tid < 64 && tid < p.Ng) {
+            const uint32_t m = max(max(red[tid], red[64 + tid]), max(red[128 + tid], red[192 + tid]));
+            p.ranges[(int64_t)blockIdx.x * p.Ng + tid] = m;
+        }
     }
 #endif
 }
@@ -1595,8 +1628,9 @@ hipError_t launch_conv_gather_w(const int8_t* wq_t, int64_t ld_w, int64_t C_out,
 // stream (k_conv_stream, weights straight from W^T); the others gather the
 // weights into bc in the implicit GEMM's K order and take the window kernel
 // (same size, small window) or the per-tap pipelined kernel.
-hipError_t launch_conv_dgrad(const GemmArgs& a0, int8_t* bc, int64_t ld_bc, hipStream_t s) {
+hipError_t launch_conv_dgrad(const GemmArgs& a0, int8_t* bc, int64_t ld_bc, hipStream_t s, int64_t* range_rows) {
     if (a0.Mg <= 0 || a0.Ng <= 0) return hipSuccess;
+    if (a0.ranges && (!a0.out || !range_rows)) return hipErrorInvalidValue;
     auto al16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
     auto fits = [](int64_t rows, int64_t ld) { return rows * ld < ((int64_t)1 << 31); };
     if (a0.taps < 1 || a0.K % 64 != 0 || a0.lda % 16 != 0 || a0.ldb % 16 != 0 || !al16(a0.A) || !al16(a0.B) ||
@@ -1613,11 +1647,30 @@ hipError_t launch_conv_dgrad(const GemmArgs& a0, int8_t* bc, int64_t ld_bc, hipS
         const int64_t rows = round_up((a0.Mg + kStreamBlocks - 1) / kStreamBlocks, 128);
         const dim3 grid((unsigned)((a0.Mg + rows - 1) / rows));
         const bool fullk = a0.K_used >= 64;   // every code column of the chunk is a channel
+        if (a0.ranges) {
+            // channel maxima per block: one slab of `rows` rows each
+            *range_rows = rows;
+            if (a0.acc && fullk) hipLaunchKernelGGL((k_conv_stream<true, true, true>), grid, dim3(256), 0, s, a0, rows);
+            else if (a0.acc) hipLaunchKernelGGL((k_conv_stream<true, false, true>), grid, dim3(256), 0, s, a0, rows);
+            else if (fullk) hipLaunchKernelGGL((k_conv_stream<false, true, true>), grid, dim3(256), 0, s, a0, rows);
+            else hipLaunchKernelGGL((k_conv_stream<false, false, true>), grid, dim3(256), 0, s, a0, rows);
+            return hipGetLastError();
+        }
         if (a0.acc && fullk) hipLaunchKernelGGL((k_conv_stream<true, true>), grid, dim3(256), 0, s, a0, rows);
         else if (a0.acc) hipLaunchKernelGGL((k_conv_stream<true, false>), grid, dim3(256), 0, s, a0, rows);
         else if (fullk) hipLaunchKernelGGL((k_conv_stream<false, true>), grid, dim3(256), 0, s, a0, rows);
         else hipLaunchKernelGGL((k_conv_stream<false, false>), grid, dim3(256), 0, s, a0, rows);
         return hipGetLastError();
+    }
+    if (a0.ranges) {
+        // the other conv kernels store dX, then one pass takes 32-row slab maxima
+        if ((a0.Mg + 31) / 32 > 65535) return hipErrorInvalidValue;
+        GemmArgs b = a0;
+        b.ranges = nullptr;
+        const hipError_t e = launch_conv_dgrad(b, bc, ld_bc, s, nullptr);
+        if (e != hipSuccess) return e;
+        *range_rows = 32;
+        return launch_slab_colmax(a0.out, a0.Mg, a0.Ng, a0.ld_out, a0.ranges, s);
     }
     // weights in the K order of the implicit GEMM
     hipError_t e = launch_conv_gather_w(a0.B, a0.ldb, a0.K_used, a0.Ng, a0.taps, a0.layout, bc, ld_bc, s);

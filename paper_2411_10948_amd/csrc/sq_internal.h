@@ -176,7 +176,10 @@ inline int64_t conv_bc_ld(int64_t C_out, int64_t taps, int64_t ext_max) {
 // Conv dgrad: a describes the product with a.B = wq_t (W^T codes [taps * C_in,
 // ld_w]); kernels that need the weights in the K order of the implicit GEMM
 // gather them into bc first.
-hipError_t launch_conv_dgrad(const GemmArgs& a, int8_t* bc, int64_t ld_bc, hipStream_t s);
+// With a.ranges (and a.out): per-slab channel maxima of |dX|, slab s covering
+// rows [s R, (s + 1) R), R returned in *range_rows.
+hipError_t launch_conv_dgrad(const GemmArgs& a, int8_t* bc, int64_t ld_bc, hipStream_t s,
+                             int64_t* range_rows = nullptr);
 // GEMM-based loss propagation (comparison for ShiftMM): group plan,
 // rearranged operands, per-group products, shift-and-sum.
 int64_t grouped_width(int64_t C_out, int num_groups);

@@ -46,7 +46,8 @@ EXPORTS = (
     "sq_l1bn_backward_workspace_size", "sq_l1bn_forward", "sq_l1bn_backward",
     "sq_conv_wgrad_layout", "sq_conv_pack_input", "sq_conv_pack_grad", "sq_quantize_grad_conv",
     "sq_conv_wgrad_workspace_size", "sq_conv_wgrad", "sq_gemm_dgrad_range_slabs", "sq_gemm_dgrad_ranged",
-    "sq_quantize_grad_noalloc", "sq_status_string", "sq_last_error",
+    "sq_quantize_grad_noalloc", "sq_conv_dgrad_ranged", "sq_quantize_grad_conv_from_ranges",
+    "sq_status_string", "sq_last_error",
 )
 
 
@@ -135,6 +136,12 @@ def load() -> ct.CDLL:
                                          _SZ, _P],
         "sq_l1bn_range_slabs": [_I64, _I64, ct.POINTER(_I64)],
         "sq_gemm_dgrad_range_slabs": [_I64, ct.POINTER(_I64)],
+        "sq_conv_dgrad_ranged": [_P, _I64, _P, _P, _P, _P, _I64, _P, _I64, _I64, _I64, _I64, _I64, ct.c_int32,
+                                 ct.c_int32, ct.c_int32, ct.c_int32, pp, _P, _I64, _P, _I64, _P,
+                                 ct.POINTER(_I64), ct.POINTER(_I64), _P, _SZ, _P],
+        "sq_quantize_grad_conv_from_ranges": [_P, _I64, _I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32,
+                                              ct.c_int32, pp, _P, _I64, _P, _I64, _P, _I64, _P, _P, _P, _P, _SZ,
+                                              _P],
         "sq_gemm_dgrad_ranged": [_P, _I64, _P, _P, _P, _P, _I64, _P, _I64, _I64, _I64, pp, _P, _I64, _P, _I64, _P,
                                  _P, _SZ, _P],
         "sq_conv_wgrad_layout": [_I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32, ct.c_int32,
@@ -406,6 +413,28 @@ def sq_gemm_dgrad(q_fold, layout, group, gscale, wq_t, wscale, M, C_out, C_in, p
         _ptr(q_fold), _ld(q_fold), _ptr(layout), _ptr(group), _ptr(gscale), _ptr(wq_t), _ld(wq_t),
         _ptr(wscale), M, C_out, C_in, ct.byref(params), _ptr(acc), _ld(acc), _ptr(dX), _ld(dX),
         ws, nws, _stream(stream)))
+
+
+def sq_conv_dgrad_ranged(q_fold, layout, group, gscale, wq_t, wscale, N, H, W, C_out, C_in, KH, KW, PH, PW,
+                         params, acc, dX, dX_ranges, workspace, stream=None) -> Tuple[int, int]:
+    """sq_conv_dgrad plus the channel ranges of dX; returns (slabs, rows per slab)."""
+    ws, nws = _ws_ptr(workspace)
+    slabs, rows = _I64(0), _I64(0)
+    _check("sq_conv_dgrad_ranged", load().sq_conv_dgrad_ranged(
+        _ptr(q_fold), _ld(q_fold), _ptr(layout), _ptr(group), _ptr(gscale), _ptr(wq_t), _ld(wq_t),
+        _ptr(wscale), N, H, W, C_out, C_in, KH, KW, PH, PW, ct.byref(params), _ptr(acc), _ld(acc),
+        _ptr(dX), _ld(dX), _ptr(dX_ranges), ct.byref(slabs), ct.byref(rows), ws, nws, _stream(stream)))
+    return int(slabs.value), int(rows.value)
+
+
+def sq_quantize_grad_conv_from_ranges(dY, N, H, W, KH, KW, PH, PW, params, ranges, range_slabs, q_fold, q_tp, group,
+                                      scale, layout, workspace, stream=None) -> None:
+    C = dY.shape[1]
+    ws, nws = _ws_ptr(workspace)
+    _check("sq_quantize_grad_conv_from_ranges", load().sq_quantize_grad_conv_from_ranges(
+        _ptr(dY), N, H, W, C, _ld(dY), KH, KW, PH, PW, ct.byref(params), _ptr(ranges), range_slabs,
+        _ptr(q_fold), _ld(q_fold), _ptr(q_tp), _ld(q_tp), _ptr(group), _ptr(scale), _ptr(layout), ws, nws,
+        _stream(stream)))
 
 
 def sq_conv_dgrad(q_fold, layout, group, gscale, wq_t, wscale, N, H, W, C_out, C_in, KH, KW, PH, PW, params,
@@ -791,10 +820,17 @@ class ConvBackwardPlan(BackwardPlan):
     nothing."""
 
     def __init__(self, N: int, H: int, W: int, C_out: int, C_in_ch: int, KH: int, KW: int, PH: int, PW: int,
-                 params: Params, device="cuda", want_acc: bool = False, implicit_wgrad: bool = True):
+                 params: Params, device="cuda", want_acc: bool = False, implicit_wgrad: bool = True,
+                 dx_ranges: bool = False):
         Ho, Wo = H + 2 * PH - KH + 1, W + 2 * PW - KW + 1
         super().__init__(N * Ho * Wo, C_out, KH * KW * C_in_ch, params, device, want_acc)
         dev = torch.device(device)
+        # dx_ranges: the dgrad also writes the channel ranges of dX (for the
+        # quantizer of the layer below, quantize_from_ranges); range_slabs is
+        # the number of slab rows the last dgrad wrote
+        self.dX_ranges = (torch.empty((sq_gemm_dgrad_range_slabs(N * H * W), C_in_ch), dtype=torch.int32,
+                                      device=dev) if dx_ranges else None)
+        self.range_slabs, self.range_rows = 0, 0
         self.geom = (N, H, W, KH, KW, PH, PW)
         self.C_in_ch = C_in_ch
         self.implicit_wgrad = implicit_wgrad
@@ -810,6 +846,11 @@ class ConvBackwardPlan(BackwardPlan):
 
     def dgrad(self, wq_t, wscale, stream=None):
         N, H, W, KH, KW, PH, PW = self.geom
+        if self.dX_ranges is not None:
+            self.range_slabs, self.range_rows = sq_conv_dgrad_ranged(
+                self.q_fold, self.layout, self.group, self.scale, wq_t, wscale, N, H, W, self.C_out, self.C_in_ch,
+                KH, KW, PH, PW, self.params, self.acc_dX, self.dX, self.dX_ranges, self.ws_d, stream)
+            return
         sq_conv_dgrad(self.q_fold, self.layout, self.group, self.scale, wq_t, wscale, N, H, W, self.C_out,
                       self.C_in_ch, KH, KW, PH, PW, self.params, self.acc_dX, self.dX, self.ws_d, stream)
 
@@ -819,6 +860,17 @@ class ConvBackwardPlan(BackwardPlan):
         N, H, W, KH, KW, PH, PW = self.geom
         sq_quantize_grad_conv(dY, N, H, W, KH, KW, PH, PW, self.params, self.q_fold, self.q_tp, self.group,
                               self.scale, self.layout, self.ws_q, stream)
+
+    def quantize_from_ranges(self, dY, ranges, stream=None, range_slabs=None):
+        """Quantize dY with channel ranges from its producer (e.g. the
+        dX_ranges of the layer above's ranged dgrad)."""
+        slabs = ranges.shape[0] if range_slabs is None else range_slabs
+        if not self.implicit_wgrad:
+            return sq_quantize_grad_from_ranges(dY, self.params, ranges, slabs, self.q_fold, self.q_t, self.group,
+                                                self.scale, self.layout, self.ws_q, stream)
+        N, H, W, KH, KW, PH, PW = self.geom
+        sq_quantize_grad_conv_from_ranges(dY, N, H, W, KH, KW, PH, PW, self.params, ranges, slabs, self.q_fold,
+                                          self.q_tp, self.group, self.scale, self.layout, self.ws_q, stream)
 
     def wgrad(self, xq_t, xscale, stream=None):
         if not self.implicit_wgrad:
