@@ -426,8 +426,7 @@ def run_conv_chain(args, torch, sq):
     w1_t, w1_s = sq.quantize_tensor(W1, 8, transpose=True)
     Xc = torch.from_numpy(np.ascontiguousarray(d["X"][:, 4 * C:5 * C])).to(dev)
     xq_raw, xs = sq.quantize_tensor(Xc, 8, transpose=True)
-    xpk = sq.conv_pack_input(xq_raw, N, H, W, 3, 3, 1, 1)
-    del xq_raw, W1, W2
+    del W1, W2
     fused = args.fused_ranges
     up = sq.ConvBackwardPlan(N, H, W, C, C, 3, 3, 1, 1, p, device=dev, dx_ranges=fused)
     lo = sq.ConvBackwardPlan(N, H, W, C, C, 3, 3, 1, 1, p, device=dev)
@@ -440,10 +439,12 @@ def run_conv_chain(args, torch, sq):
             lo.quantize(up.dX, stream)
 
     def step():
-        up.run(dY, w2_t, w2_s, xpk, xs, stream)
+        # each layer packs its input codes onto its padded grid
+        up.run_packed(dY, w2_t, w2_s, xq_raw, xs, stream)
         quant_lo()
         lo.dgrad(w1_t, w1_s, stream)
-        lo.wgrad(xpk, xs, stream)
+        lo.pack_input(xq_raw, stream)
+        lo.wgrad(lo.x_grid, xs, stream)
 
     def timed(fn, K):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -552,14 +553,12 @@ def main(argv=None):
     wq_t, ws = sq.quantize_tensor(W, 8, transpose=True, tiled=tiled)
     implicit = conv and args.conv_wgrad == "implicit"
     if implicit:
-        # setup (untimed, as the im2col'd codes are): the layer input is the
-        # centre tap of the im2col'd rows (pad 1); its per-tensor scale equals
-        # the im2col'd tensor's (the im2col adds only zeros)
-        n_img = M // (wl.conv_hw * wl.conv_hw)
+        # the layer input is the centre tap of the im2col'd rows (pad 1); its
+        # per-tensor scale equals the im2col'd tensor's (the im2col adds only
+        # zeros).  Its codes come from the forward pass; the timed step packs
+        # them onto the padded grid (run_packed).
         X = X[:, 4 * wl.conv_cin:5 * wl.conv_cin].contiguous()
-        xq_raw, xs = sq.quantize_tensor(X, 8, transpose=True)
-        xq_t = sq.conv_pack_input(xq_raw, n_img, wl.conv_hw, wl.conv_hw, 3, 3, 1, 1)
-        del xq_raw
+        xq_t, xs = sq.quantize_tensor(X, 8, transpose=True)
     else:
         xq_t, xs = sq.quantize_tensor(X, 8, transpose=True, tiled=tiled)
     del W, X
@@ -578,19 +577,20 @@ def main(argv=None):
         torch.cuda.synchronize()
         del src, dst
 
+    run = plan.run_packed if implicit else plan.run
     for _ in range(args.warmup):
-        plan.run(dY, wq_t, ws, xq_t, xs, stream)
+        run(dY, wq_t, ws, xq_t, xs, stream)
     torch.cuda.synchronize()
 
     K = args.steps
-    per_step = per_step_times(torch, stream, lambda: plan.run(dY, wq_t, ws, xq_t, xs, stream), K)
+    per_step = per_step_times(torch, stream, lambda: run(dY, wq_t, ws, xq_t, xs, stream), K)
     # Timed region: K whole steps on one stream, bracketed by two events only
     # (an event recorded between kernels costs a bubble of several us).
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
     for _ in range(K):
-        plan.run(dY, wq_t, ws, xq_t, xs, stream)
+        run(dY, wq_t, ws, xq_t, xs, stream)
     stop.record(stream)
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(stop) / K
@@ -610,7 +610,11 @@ def main(argv=None):
 
     t_quant = per_call(lambda: plan.quantize(dY, stream))
     t_dgrad = per_call(lambda: plan.dgrad(wq_t, ws, stream))
-    t_wgrad = per_call(lambda: plan.wgrad(xq_t, xs, stream))
+    if implicit:
+        t_pack = per_call(lambda: plan.pack_input(xq_t, stream))
+        t_wgrad = per_call(lambda: plan.wgrad(plan.x_grid, xs, stream))
+    else:
+        t_wgrad = per_call(lambda: plan.wgrad(xq_t, xs, stream))
     ops = 4 * M * C_out * C_in
     value = ops / (ms_step * 1e-3) / 1e12
 
@@ -626,6 +630,9 @@ def main(argv=None):
             "ms": t_wgrad, "bytes": M * C_out + M * (C_in // 9 if implicit else C_in) + 4 * C_out * C_in,
             "ops": 2 * M * C_out * C_in},
     }
+    if implicit:
+        # the input codes [C_in / 9, N*H*W] read, the padded grid written
+        parts["sq_conv_pack_input"] = {"ms": t_pack, "bytes": M * (C_in // 9) + plan.x_grid.numel(), "ops": 0}
     dom = max(parts, key=lambda k: parts[k]["ms"])
     d = parts[dom]
     balance = PEAK_INT8_TOPS * 1e12 / (PEAK_HBM_GBS * 1e9)

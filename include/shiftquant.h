@@ -475,13 +475,15 @@ sq_status sq_gemm_dgrad_ranged(const int8_t* q_fold, int64_t ld_fold, const int3
  * constant shift r Wp + s of the pixel index:
  *   q_tp [C_out, ld_tp >= q_ld]: gradient code (n, oh, ow, c) at column
  *        n Hp Wp + oh Wp + ow of row c, every other column 0.
- *   xs   [KW C_in, x_ld]: row s C_in + ci holds, at column P, the input code
- *        of channel ci at grid position P + s (input pixel (n, ih, iw) sits at
- *        n Hp Wp + (ih + PH) Wp + iw + PW), 0 in the padding.
- * sq_conv_wgrad_layout gives x_rows = KW C_in, x_ld and q_ld.
+ *   xs   [C_in, ld_xs >= x_ld]: input pixel (n, ih, iw) of channel ci at
+ *        column n Hp Wp + (ih + PH) Wp + iw + PW of row ci, 0 in the padding
+ *        and in the x_ld - q_ld = (KH - 1) Wp + 64 columns past the grid, so
+ *        that tap (r, s) of grid position P reads column P + r Wp + s.
+ * sq_conv_wgrad_layout gives x_rows = C_in, x_ld and q_ld.
  * sq_conv_pack_input builds xs from the input codes xq_t [C_in, ld_xq >= N H W]
- *   (sq_quantize_tensor, transpose 1) and writes every byte of xs; in training
- *   the input codes come from the forward pass, once per step.
+ *   (sq_quantize_tensor, transpose 1) and writes every byte of xs (x_ld
+ *   columns); in training the input codes come from the forward pass, and
+ *   the pack runs once per step.
  * sq_conv_pack_grad builds q_tp from transposed codes q_t [C_out, ld_t >= N Ho Wo]
  *   and writes every byte of q_tp.
  * sq_quantize_grad_conv is sq_quantize_grad for the conv's gradient
@@ -491,8 +493,10 @@ sq_status sq_gemm_dgrad_ranged(const int8_t* q_fold, int64_t ld_fold, const int3
  * sq_quantize_grad_conv_from_ranges is the same with the channel ranges
  *   given as partial maxima (see sq_quantize_grad_from_ranges), e.g. the
  *   dX_ranges of sq_conv_dgrad_ranged of the layer above.
- * sq_conv_wgrad runs one int8 GEMM (K = the padded grid, rounded up to 64)
- *   whose B rows are xs at the taps' row offsets.
+ * sq_conv_wgrad runs the int8 product over the padded grid (K = N Hp Wp
+ *   rounded up to 64) with every tap read from the one copy of the input at
+ *   its shift r Wp + s (1 x 1 windows: a plain int8 GEMM of the two grids),
+ *   then, when K is split, the sum of the int32 partials.
  * Outputs: acc [C_out, ld_acc] int32 and/or dW [C_out, ld_dW] fp32, each row
  *          KH KW C_in wide.
  * Workspace: sq_conv_wgrad_workspace_size bytes (split-K partials, may be 0).

@@ -748,9 +748,10 @@ struct ConvGrid {
 };
 
 // padded pixel grid: Hp = H + 2 PH rows, Wp = roundup(W + 2 PW, 16) columns
-// per image; K = roundup(N Hp Wp, 64); the input copies extend (KH - 1) Wp
-// past K for the row shifts of the taps
+// per image; K = roundup(N Hp Wp, 64); the input grid extends (KH - 1) Wp + 64
+// zero columns past K for the shifts of the taps
 ConvGrid conv_grid(int64_t N, int64_t H, int64_t W, int64_t C_in, int KH, int KW, int PH, int PW) {
+    (void)KW;
     ConvGrid g{};
     g.Ho = H + 2 * (int64_t)PH - KH + 1;
     g.Wo = W + 2 * (int64_t)PW - KW + 1;
@@ -758,8 +759,8 @@ ConvGrid conv_grid(int64_t N, int64_t H, int64_t W, int64_t C_in, int KH, int KW
     g.Wp = round_up(W + 2 * (int64_t)PW, 16);
     g.K = round_up(std::max<int64_t>(N * g.Hp * g.Wp, 1), 64);
     g.ld_q = g.K;
-    g.rows_x = (int64_t)KW * C_in;
-    g.ld_x = round_up(g.K + (int64_t)(KH - 1) * g.Wp, 16);
+    g.rows_x = C_in;
+    g.ld_x = g.K + (int64_t)(KH - 1) * g.Wp + 64;
     return g;
 }
 
@@ -797,8 +798,8 @@ sq_status sq_conv_pack_input(const int8_t* xq_t, int64_t ld_xq, int64_t N, int64
     if (C_in == 0) return SQ_OK;
     SQ_TRY(check_codes(xq_t, ld_xq, N * H * W, "xq_t"));
     SQ_TRY(check_codes(xs, ld_xs, g.ld_x, "xs"));
-    return hip_status(launch_grid_scatter(xq_t, ld_xq, C_in, KW, N, H, W, PH, PW, g.Hp, g.Wp, xs, ld_xs,
-                                          static_cast<hipStream_t>(stream)),
+    return hip_status(launch_grid_pack(xq_t, ld_xq, C_in, N, H, W, PH, PW, g.Hp, g.Wp, xs, ld_xs,
+                                       static_cast<hipStream_t>(stream)),
                       "conv pack input");
 }
 
@@ -810,8 +811,8 @@ sq_status sq_conv_pack_grad(const int8_t* q_t, int64_t ld_t, int64_t N, int64_t 
     if (C_out == 0) return SQ_OK;
     SQ_TRY(check_codes(q_t, ld_t, N * g.Ho * g.Wo, "q_t"));
     SQ_TRY(check_codes(q_tp, ld_tp, g.ld_q, "q_tp"));
-    return hip_status(launch_grid_scatter(q_t, ld_t, C_out, 1, N, g.Ho, g.Wo, 0, 0, g.Hp, g.Wp, q_tp, ld_tp,
-                                          static_cast<hipStream_t>(stream)),
+    return hip_status(launch_grid_pack(q_t, ld_t, C_out, N, g.Ho, g.Wo, 0, 0, g.Hp, g.Wp, q_tp, ld_tp,
+                                       static_cast<hipStream_t>(stream)),
                       "conv pack gradient");
 }
 
@@ -892,6 +893,12 @@ sq_status sq_quantize_grad_conv_from_ranges(const float* dY, int64_t N, int64_t 
                                    q_tp, ld_tp, group, scale, layout, workspace, workspace_bytes, stream);
 }
 
+namespace {
+// 1 x 1 windows: the plain product of the two grids (no shifts), split as the
+// linear wgrad; otherwise the single-copy window kernel
+int conv_wgrad_splits_1x1(const ConvGrid& g, int64_t C_out, int64_t C_in) { return wgrad_splits(g.K, C_out, C_in); }
+}  // namespace
+
 sq_status sq_conv_wgrad_workspace_size(int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t C_in, int32_t KH,
                                        int32_t KW, int32_t PH, int32_t PW, const sq_quant_params* p, size_t* bytes) {
     if (!bytes) return fail(SQ_ERR_INVALID_ARGUMENT, "bytes is NULL");
@@ -899,7 +906,10 @@ sq_status sq_conv_wgrad_workspace_size(int64_t N, int64_t H, int64_t W, int64_t 
     SQ_TRY(check_conv_geom(N, H, W, C_out, C_in, KH, KW, PH, PW));
     const ConvGrid g = conv_grid(N, H, W, C_in, KH, KW, PH, PW);
     const int64_t Ng = (int64_t)KH * KW * C_in;
-    const int splits = (C_out > 0 && Ng > 0) ? wgrad_splits(g.K, C_out, Ng) : 1;
+    int splits = 1;
+    if (C_out > 0 && C_in > 0)
+        splits = (KH == 1 && KW == 1) ? conv_wgrad_splits_1x1(g, C_out, C_in)
+                                      : conv_wgrad_plan(g.K, C_out, C_in, KH, KW, g.Wp).splits;
     *bytes = splits > 1 ? (size_t)splits * C_out * Ng * 4 : 0;
     return SQ_OK;
 }
@@ -923,14 +933,20 @@ sq_status sq_conv_wgrad(const int8_t* q_tp, int64_t ld_tp, const uint8_t* group,
     if (!group) return fail(SQ_ERR_INVALID_ARGUMENT, "group is NULL");
     SQ_TRY(check_codes(q_tp, ld_tp, g.ld_q, "q_tp"));
     SQ_TRY(check_codes(xs, ld_xs, g.ld_x, "xs"));
-    if (ld_xs != g.ld_x) return fail(SQ_ERR_INVALID_ARGUMENT, "ld_xs must be the one sq_conv_wgrad_layout returns");
-    if ((int64_t)C_out * ld_tp >= ((int64_t)1 << 31)) return fail(SQ_ERR_UNSUPPORTED, "q_tp exceeds 2^31 bytes");
+    if ((int64_t)C_out * ld_tp >= ((int64_t)1 << 31) || (int64_t)C_in * ld_xs >= ((int64_t)1 << 31))
+        return fail(SQ_ERR_UNSUPPORTED, "a padded code grid exceeds 2^31 bytes");
     if (acc) SQ_TRY(check_f32(acc, ld_acc, Ng, "acc"));
     if (dW) SQ_TRY(check_f32(dW, ld_dW, Ng, "dW"));
     size_t need = 0;
     SQ_TRY(sq_conv_wgrad_workspace_size(N, H, W, C_out, C_in, KH, KW, PH, PW, p, &need));
+    if (need > 0) {
+        if (!workspace || !aligned(workspace, 16))
+            return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
+        if (workspace_bytes < need) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+    }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const int splits = wgrad_splits(g.K, C_out, Ng);
+    int32_t* part = static_cast<int32_t*>(workspace);
+    // the epilogue of the wgrad (one scale per output channel)
     GemmArgs a{};
     a.Mg = C_out; a.Ng = Ng;
     a.A = q_tp; a.lda = ld_tp;
@@ -938,22 +954,34 @@ sq_status sq_conv_wgrad(const int8_t* q_tp, int64_t ld_tp, const uint8_t* group,
     a.K = g.K;
     a.gs = gscale; a.os = xscale; a.group = group; a.num_groups = cfg.num_groups;
     a.epi_mode = 1;
-    a.wg_KH = KH; a.wg_KW = KW; a.wg_Cin = C_in; a.wg_Wp = g.Wp;
-    if (splits <= 1) {
-        a.splits = 1;
-        a.acc = acc; a.ld_acc = ld_acc;
-        a.out = dW; a.ld_out = ld_dW;
-        return hip_status(launch_gemm(a, s), "conv wgrad");
-    }
-    if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
-    if (workspace_bytes < need) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
-    int32_t* part = static_cast<int32_t*>(workspace);
-    GemmArgs gp = a;
-    gp.splits = splits;
-    gp.part = part;
-    SQ_TRY(hip_status(launch_gemm(gp, s), "conv wgrad"));
     a.acc = acc; a.ld_acc = ld_acc;
     a.out = dW; a.ld_out = ld_dW;
+    int splits = 1;
+    if (KH == 1 && KW == 1) {
+        splits = conv_wgrad_splits_1x1(g, C_out, C_in);
+        GemmArgs gp = a;
+        gp.splits = splits;
+        if (splits > 1) {
+            gp.part = part;
+            gp.acc = nullptr;
+            gp.out = nullptr;
+        }
+        SQ_TRY(hip_status(launch_gemm(gp, s), "conv wgrad"));
+    } else {
+        const ConvWgradPlan pl = conv_wgrad_plan(g.K, C_out, C_in, KH, KW, g.Wp);
+        splits = pl.splits;
+        ConvWgradArgs c{};
+        c.A = q_tp; c.lda = ld_tp;
+        c.X = xs; c.ldx = ld_xs;
+        c.C_out = C_out; c.C_in = C_in; c.Wp = g.Wp; c.ktiles = g.K / 64;
+        c.KH = KH; c.KW = KW;
+        c.part = splits > 1 ? part : nullptr;
+        c.acc = acc; c.ld_acc = ld_acc;
+        c.out = dW; c.ld_out = ld_dW;
+        c.group = group; c.gs = gscale; c.os = xscale;
+        SQ_TRY(hip_status(launch_conv_wgrad(c, pl, s), "conv wgrad"));
+    }
+    if (splits <= 1) return SQ_OK;
     return hip_status(launch_splitk_reduce(part, splits, a, s), "splitk_reduce");
 }
 

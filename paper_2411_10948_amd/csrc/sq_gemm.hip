@@ -507,7 +507,7 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
     };
     // tile-major operands (p.tiled) hold whole 16-row groups
     const int64_t rows_a = CONV ? p.a_rows : (p.tiled ? round_up(p.Mg, 16) : p.Mg);
-    const int64_t rows_b = p.wg_KH ? p.wg_KW * p.wg_Cin : (p.tiled ? round_up(p.Ng, 16) : p.Ng);
+    const int64_t rows_b = p.tiled ? round_up(p.Ng, 16) : p.Ng;
     const __amdgpu_buffer_rsrc_t rA = rsrc(p.A, rows_a, p.lda), rB = rsrc(p.B, rows_b, p.ldb);
     // Row-major: row r at r ld.  Tile-major: the 16 rows of this load
     // instruction form one contiguous 1 KB tile per K tile, and the K offset
@@ -525,18 +525,6 @@ __global__ __launch_bounds__(T::kThreads) void k_gemm_pipe(GemmArgs p, int64_t t
     for (int i = 0; i < T::IA; ++i) offA[i] = lane_off(i, m0, p.Mg, p.lda);
 #pragma unroll
     for (int i = 0; i < T::IB; ++i) offB[i] = lane_off(i, n0, p.Ng, p.ldb);
-    if (p.wg_KH) {
-        // implicit-im2col conv wgrad: B row (tap, ci) is row s C_in + ci of
-        // the shifted input copies, r Wp bytes into its K range
-#pragma unroll
-        for (int i = 0; i < T::IB; ++i) {
-            const int r = (i * T::kWaves + wv) * 16 + lr;
-            const int64_t j = min(n0 + r, p.Ng - 1), tap = j / p.wg_Cin, ci = j - tap * p.wg_Cin;
-            const int64_t tr = tap / p.wg_KW, ts = tap - tr * p.wg_KW;
-            offB[i] = (uint32_t)((ts * p.wg_Cin + ci) * p.ldb + tr * p.wg_Wp + 16 * ((lane & 3) ^ swz(r)));
-        }
-    }
-
     // Convolution: the input pixel (n, ih, iw) of each of this lane's A rows;
     // tap (r, s) reads output pixel (n, ih + PH - r, iw + PW - s) of q_fold,
     // or, outside the output grid, an offset past the end of the buffer,
@@ -1511,12 +1499,8 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     if (a.Mg <= 0 || a.Ng <= 0) return hipSuccess;
     const bool pipe = pipe_ok(a);
     // tile-major operands: the pipelined kernel only, no convolution
-    if (a.tiled && (!pipe || a.taps || a.wg_KH || a.kseg)) return hipErrorInvalidValue;
+    if (a.tiled && (!pipe || a.taps || a.kseg)) return hipErrorInvalidValue;
     if (a.kseg && (!pipe || a.splits > 1 || a.layout)) return hipErrorInvalidValue;   // pipelined kernel only
-    if (a.wg_KH && (!pipe || a.extA || a.layout || a.kseg || a.wg_Cin <= 0 || a.wg_KW <= 0 || a.wg_Wp % 16 != 0 ||
-                    a.Ng != (int64_t)a.wg_KH * a.wg_KW * a.wg_Cin ||
-                    (int64_t)a.wg_KW * a.wg_Cin * a.ldb >= ((int64_t)1 << 31)))
-        return hipErrorInvalidValue;   // implicit-im2col wgrad: pipelined kernel, offsets in 31 bits
     const Pick p = pick(a);
     const int64_t ktiles = (a.K + 63) / 64;   // every configuration has 64-byte K tiles
     const int splits = std::max(1, a.splits);
@@ -1524,7 +1508,7 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     if (splits > 1 && (ktiles + per - 1) / per != splits) return hipErrorInvalidValue;   // wgrad_splits() avoids this
     if (a.ranges) {
         // dX with its channel maxima (producer-side ranges): pipelined kernel, no split
-        if (!pipe || splits > 1 || !a.out || a.part || a.wg_KH) return hipErrorInvalidValue;
+        if (!pipe || splits > 1 || !a.out || a.part) return hipErrorInvalidValue;
         if (p == Pick::kLarge)
             return a.extA ? launch_pipe<PipeLarge, true, false, true>(a, 1, per * 64, s)
                           : launch_pipe<PipeLarge, false, false, true>(a, 1, per * 64, s);
@@ -1549,47 +1533,388 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
                   : launch_pipe<PipeSmall, false>(a, splits, per * 64, s);
 }
 
-// Padded pixel grids of the implicit-im2col conv wgrad: each thread writes
-// 16 consecutive bytes of an output row (one 16-byte store), reading the
-// pixels they map to one byte at a time.
-__global__ __launch_bounds__(256) void k_grid_scatter(const int8_t* __restrict__ in, int64_t ld_in, int64_t C,
-                                                      int64_t N, int64_t Hc, int64_t Wc, int64_t top, int64_t left,
-                                                      int64_t Hp, int64_t Wp, int8_t* __restrict__ out,
-                                                      int64_t ld_out, int64_t rows) {
+// Padded pixel grids of the conv wgrad: a thread writes one aligned 16-byte
+// chunk of an output row.  Its 16 grid positions lie in one grid row (Wp is a
+// multiple of 16), so they map to a run of consecutive source pixels: two
+// aligned 16-byte loads of the source row cover it, and v_alignbyte moves the
+// run into place; bytes outside the content are cleared.
+__global__ __launch_bounds__(256) void k_grid_pack(const int8_t* __restrict__ in, int64_t ld_in, int64_t N,
+                                                   int64_t Hc, int64_t Wc, int64_t top, int64_t left, int64_t Hp,
+                                                   int64_t Wp, int8_t* __restrict__ out, int64_t ld_out,
+                                                   int64_t rows) {
     const int64_t chunks = ld_out / 16, img = Hp * Wp;
     for (int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; id < rows * chunks;
          id += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t j = id / chunks, P0 = (id - j * chunks) * 16;
-        const int64_t sh = j / C, c = j - sh * C;
-        const int8_t* src = in + c * ld_in;
-        int64_t Q = P0 + sh;
-        int64_t n = Q / img, rem = Q - n * img, hp = rem / Wp, wp = rem - hp * Wp;
-        uint32_t w[4] = {0u, 0u, 0u, 0u};
+        const int64_t c = id / chunks, G0 = (id - c * chunks) * 16;
+        const int64_t n = G0 / img, rem = G0 - n * img, hp = rem / Wp, wp0 = rem - hp * Wp;
+        const int64_t ih = hp - top;
+        // grid bytes [e_lo, e_hi) of the chunk hold content pixels
+        const int64_t e_lo = max((int64_t)0, left - wp0), e_hi = min((int64_t)16, Wc + left - wp0);
+        uint32_t o[4] = {0u, 0u, 0u, 0u};
+        if (n < N && ih >= 0 && ih < Hc && e_lo < e_hi) {
+            const int8_t* src = in + c * ld_in;
+            // source index of grid byte 0 (before the row start when wp0 < left)
+            const int64_t lo = (n * Hc + ih) * Wc + wp0 - left;
+            const int64_t a16 = lo >= 0 ? (lo & ~(int64_t)15) : -16;
+            const int off = (int)(lo - a16);
+            uint32_t w[8];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            const int64_t h = hp - top, x = wp - left;
-            if (n < N && h >= 0 && h < Hc && x >= 0 && x < Wc)
-                w[e >> 2] |= (uint32_t)(uint8_t)src[(n * Hc + h) * Wc + x] << (8 * (e & 3));
-            if (++wp == Wp) {
-                wp = 0;
-                if (++hp == Hp) {
-                    hp = 0;
-                    ++n;
-                }
+            for (int h = 0; h < 2; ++h) {
+                const int64_t at = a16 + 16 * h;
+                uint4 v = make_uint4(0u, 0u, 0u, 0u);
+                if (at >= 0 && at + 16 <= ld_in) v = *reinterpret_cast<const uint4*>(src + at);
+                w[4 * h] = v.x; w[4 * h + 1] = v.y; w[4 * h + 2] = v.z; w[4 * h + 3] = v.w;
+            }
+            uint32_t sel[5];
+            switch (off >> 2) {
+                case 0: for (int i = 0; i < 5; ++i) sel[i] = w[i]; break;
+                case 1: for (int i = 0; i < 5; ++i) sel[i] = w[i + 1]; break;
+                case 2: for (int i = 0; i < 5; ++i) sel[i] = w[i + 2]; break;
+                default: for (int i = 0; i < 5; ++i) sel[i] = w[i + 3]; break;
+            }
+            const uint32_t b = (uint32_t)(off & 3);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int lo_i = (int)min((int64_t)4, max((int64_t)0, e_lo - 4 * i));
+                const int hi_i = (int)min((int64_t)4, max((int64_t)0, e_hi - 4 * i));
+                const uint32_t m = hi_i > lo_i ? (0xFFFFFFFFu >> (32 - 8 * (hi_i - lo_i))) << (8 * lo_i) : 0u;
+                o[i] = __builtin_amdgcn_alignbyte(sel[i + 1], sel[i], b) & m;
             }
         }
-        *reinterpret_cast<uint4*>(out + j * ld_out + P0) = make_uint4(w[0], w[1], w[2], w[3]);
+        *reinterpret_cast<uint4*>(out + c * ld_out + G0) = make_uint4(o[0], o[1], o[2], o[3]);
     }
 }
 
-hipError_t launch_grid_scatter(const int8_t* in, int64_t ld_in, int64_t C, int copies, int64_t N, int64_t Hc,
-                               int64_t Wc, int64_t top, int64_t left, int64_t Hp, int64_t Wp, int8_t* out,
-                               int64_t ld_out, hipStream_t s) {
-    const int64_t rows = C * copies, work = rows * (ld_out / 16);
+hipError_t launch_grid_pack(const int8_t* in, int64_t ld_in, int64_t C, int64_t N, int64_t Hc, int64_t Wc,
+                            int64_t top, int64_t left, int64_t Hp, int64_t Wp, int8_t* out, int64_t ld_out,
+                            hipStream_t s) {
+    if (ld_out % 16 || ld_in % 16 || Wp % 16) return hipErrorInvalidValue;
+    const int64_t work = C * (ld_out / 16);
     if (work <= 0) return hipSuccess;
-    const dim3 grid((unsigned)std::min<int64_t>((work + 255) / 256, 8192));
-    hipLaunchKernelGGL(k_grid_scatter, grid, dim3(256), 0, s, in, ld_in, C, N, Hc, Wc, top, left, Hp, Wp, out, ld_out,
-                       rows);
+    const dim3 grid((unsigned)std::min<int64_t>((work + 255) / 256, 16384));
+    hipLaunchKernelGGL(k_grid_pack, grid, dim3(256), 0, s, in, ld_in, N, Hc, Wc, top, left, Hp, Wp, out, ld_out, C);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Implicit-im2col weight gradient of a stride-1 convolution from one copy of
+// the input codes on the padded pixel grid:
+//   acc[co, (r KW + s) C_in + ci] = sum_P A[co, P] X[ci, P + r Wp + s],
+// the third product of the im2col'd conv layer (Fig. "MMs"), whose im2col
+// column of tap (r, s) is the grid shifted by r Wp + s bytes.
+// A block owns FM x 16 output channels, 16 input channels and RB rows of taps
+// (all KW columns of each) for one K split, and walks the split in chunks of
+// 16 K tiles: per chunk it stages 1 KB of each of its A rows and 1280 bytes
+// of each X row (the chunk and the halo of the row shifts) in a three-deep
+// LDS ring, with direct loads whose lane offsets are fixed and whose K offset
+// is a scalar.  Wave w of eight (two per SIMD; four for a runtime window)
+// takes K tiles w, w + 8 of a chunk; per tile it reads FM A fragments and, per tap row, the 16-byte
+// chunk of each X row plus the word after it, from which v_alignbyte forms
+// the KW byte-shifted B fragments: one X read feeds KW x FM MFMAs.  Chunk q of an
+// LDS row r sits at chunk (q & ~7) | ((q ^ r) & 7), so the 16 rows of a
+// fragment read fall in 8 distinct bank groups.  At the end the waves'
+// accumulators are summed in LDS and the block writes its tile: int32
+// partials of its K split, or the outputs with the epilogue of the wgrad
+// (dW[co, :] = fl(float(acc[co, :]) * fl(step_G step_X 2^-g_co))).
+// ---------------------------------------------------------------------------
+constexpr int kCwA = 1024, kCwX = 1280, kCwTiles = 16;
+constexpr int kCwHalo = kCwX - kCwA - 64;   // largest (RB - 1) Wp a chunk's X rows cover
+
+template <int FM, int KWC, int RBC>   // KWC / RBC: compile-time KW / tap rows, 0 = runtime (KW <= 16, RB <= 2)
+struct CwCfg {
+    // two waves per SIMD; the runtime-window variant (128 accumulator
+    // registers) keeps one
+    static constexpr int WAVES = KWC ? 8 : 4;
+    static constexpr int KWM = KWC ? KWC : 16;
+    static constexpr int RBM = RBC ? RBC : 2;
+    static constexpr int NX = KWM == 1 ? 0 : (KWM <= 5 ? 1 : 4);   // words read after each X chunk
+    static constexpr int kAbytes = 16 * FM * kCwA;
+    static constexpr int kStage = kAbytes + 16 * kCwX;
+    static constexpr int STAGES = FM == 1 && KWC ? 4 : 3;   // LDS ring depth (chunks)
+    static constexpr int kSmem = STAGES * kStage;
+    // DMA instructions per chunk: LA per wave for A; the NXI of the X rows
+    // go to waves i % T::WAVES, LXM at most per wave
+    static constexpr int LA = 16 * FM / WAVES, NXI = 16 * kCwX / 1024;
+    static constexpr int LXM = (NXI + WAVES - 1) / WAVES;
+    static_assert(LA * WAVES == 16 * FM && NXI * 1024 == 16 * kCwX, "whole DMA instructions");
+    static_assert(2 * (LA + LXM) <= 63, "vmcnt range");
+};
+
+__device__ __forceinline__ int cw_phys(int q, int r) { return (q & ~7) | ((q ^ r) & 7); }
+
+// s_waitcnt lgkmcnt(0) leaving vmcnt and expcnt unconstrained (gfx9 encoding)
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x3 << 14)); }
+
+template <int FM, int KWC, int RBC>
+__global__ __launch_bounds__((64 * CwCfg<FM, KWC, RBC>::WAVES)) void k_conv_wgrad(ConvWgradArgs p, ConvWgradPlan pl) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    using T = CwCfg<FM, KWC, RBC>;
+    __shared__ __attribute__((aligned(1024))) int8_t smem[T::kSmem];
+    using MF = Mfma<16>;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    // the tiles of one K split get block ids 8 apart: same XCD, shared L2
+    const int64_t nt = pl.tiles, L = blockIdx.x, G = L / (8 * nt), rem = L - G * 8 * nt;
+    const int64_t Sg = min((int64_t)8, (int64_t)pl.splits - 8 * G);
+    const int64_t bt = rem / Sg, split = 8 * G + rem % Sg;
+    const int tg = (int)(bt % pl.tap_groups);
+    const int64_t rest = bt / pl.tap_groups;
+    const int64_t ci0 = (rest % pl.tiles_ci) * 16, co0 = (rest / pl.tiles_ci) * (16 * FM);
+    const int KW = KWC ? KWC : p.KW;
+    const int r0 = tg * pl.rb;
+    const int nr = RBC ? RBC : min(pl.rb, p.KH - r0);
+    const int64_t c_beg = split * pl.per;
+    const int nch = (int)(min(pl.chunks, c_beg + pl.per) - c_beg);
+
+    constexpr int kRsrcFlags = 0x00020000;   // raw byte buffer, gfx9 data format
+    auto rsrc = [&](const int8_t* base, int64_t bytes) {
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(base), (short)0,
+                                                 (int)min(bytes, (int64_t)0x7FFFFFFF), kRsrcFlags);
+    };
+    const __amdgpu_buffer_rsrc_t rA = rsrc(p.A, p.C_out * p.lda), rX = rsrc(p.X, p.C_in * p.ldx);
+    // DMA: A instruction j of this wave fills LDS row w LA + j (1 KB); X
+    // instruction j fills bytes [1 KB i, 1 KB (i + 1)) of the X rows, i = w LX + j.
+    // Rows past C_out / C_in read the last row (never stored).
+    uint32_t offA[T::LA], offX[T::LXM];
+#pragma unroll
+    for (int j = 0; j < T::LA; ++j) {
+        const int row = w * T::LA + j;
+        const int64_t g = min(co0 + row, p.C_out - 1);
+        offA[j] = (uint32_t)(g * p.lda + 16 * cw_phys(lane, row & 15));
+    }
+    const int nxw = (T::NXI - w + T::WAVES - 1) / T::WAVES;   // X instructions of this wave
+#pragma unroll
+    for (int j = 0; j < T::LXM; ++j) {
+        const int i = min(w + T::WAVES * j, T::NXI - 1);
+        const int b = i * 1024 + 16 * lane, xr = b / kCwX, pc = (b - xr * kCwX) / 16;
+        const int64_t g = min(ci0 + xr, p.C_in - 1);
+        offX[j] = (uint32_t)(g * p.ldx + (int64_t)r0 * p.Wp + 16 * cw_phys(pc, xr & 15));
+    }
+    auto issue = [&](int c) {
+        int8_t* st = smem + (c % T::STAGES) * T::kStage;
+        const int k0 = (int)((c_beg + c) * kCwTiles * 64);
+#pragma unroll
+        for (int j = 0; j < T::LA; ++j)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void_t*)(st + (w * T::LA + j) * kCwA), 16, offA[j], k0,
+                                                     0, 0);
+#pragma unroll
+        for (int j = 0; j < T::LXM; ++j)
+            if (j < nxw)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rX, (lds_void_t*)(st + T::kAbytes + (w + T::WAVES * j) * 1024),
+                                                         16, offX[j], k0, 0, 0);
+    };
+    // this wave's loads of chunk c are complete once only those of the
+    // STAGES - 2 chunks issued after it remain
+    auto wait_chunk = [&](int later) {   // chunks issued after chunk c (0 .. STAGES - 2)
+        if (later <= 0) wait_vm<0>();
+        else if (later == 1) {
+            if (nxw == T::LXM) wait_vm<T::LA + T::LXM>();
+            else wait_vm<T::LA + T::LXM - 1>();
+        } else {
+            if (nxw == T::LXM) wait_vm<2 * (T::LA + T::LXM)>();
+            else wait_vm<2 * (T::LA + T::LXM - 1)>();
+        }
+    };
+
+    // fragment reads: lane (row lr, 16-byte K chunk lc) of K tile 4 u + w reads
+    // logical chunk 16 u + q0 of its row; cw_phys(16 u + q0) = 16 u + cw_phys(q0)
+    const int lr = lane & 15, lc = lane >> 4;
+    const int aoff = lr * kCwA + 16 * cw_phys(4 * w + lc, lr);
+    int xo0[T::RBM], xo1[T::RBM];
+#pragma unroll
+    for (int rr = 0; rr < T::RBM; ++rr) {
+        const int q0 = 4 * w + lc + rr * (int)(p.Wp / 16);
+        xo0[rr] = T::kAbytes + lr * kCwX + 16 * cw_phys(q0, lr);
+        xo1[rr] = T::kAbytes + lr * kCwX + 16 * cw_phys(q0 + 1, lr);
+    }
+
+    v4i acc[FM][T::RBM][T::KWM];
+#pragma unroll
+    for (int f = 0; f < FM; ++f)
+#pragma unroll
+        for (int rr = 0; rr < T::RBM; ++rr)
+#pragma unroll
+            for (int s = 0; s < T::KWM; ++s) acc[f][rr][s] = v4i{0, 0, 0, 0};
+
+    // One chunk: the wave's K tiles w + T::WAVES u.  FULL: every tile lies
+    // below K; else tiles past the end (last chunk) add nothing (A cleared).
+    constexpr int NU = kCwTiles / T::WAVES;
+    struct Frags {
+        v4i a[FM];
+        v4i x[T::RBM];
+        uint32_t nx[T::RBM][T::NX ? T::NX : 1];
+    };
+    auto load = [&](Frags& F, const int8_t* st, int u) {
+#pragma unroll
+        for (int f = 0; f < FM; ++f) F.a[f] = *reinterpret_cast<const v4i*>(st + aoff + f * 16 * kCwA + 64 * T::WAVES * u);
+#pragma unroll
+        for (int rr = 0; rr < T::RBM; ++rr) {
+            if (!RBC && rr >= nr) continue;
+            F.x[rr] = *reinterpret_cast<const v4i*>(st + xo0[rr] + 64 * T::WAVES * u);
+            if constexpr (T::NX == 1) {
+                F.nx[rr][0] = *reinterpret_cast<const uint32_t*>(st + xo1[rr] + 64 * T::WAVES * u);
+            } else if constexpr (T::NX == 4) {
+                const v4i y = *reinterpret_cast<const v4i*>(st + xo1[rr] + 64 * T::WAVES * u);
+                F.nx[rr][0] = (uint32_t)y.x; F.nx[rr][1] = (uint32_t)y.y;
+                F.nx[rr][2] = (uint32_t)y.z; F.nx[rr][3] = (uint32_t)y.w;
+            }
+        }
+    };
+    auto process = [&](Frags& F, bool valid) {
+        if (!valid)
+#pragma unroll
+            for (int f = 0; f < FM; ++f) F.a[f] = v4i{0, 0, 0, 0};
+#pragma unroll
+        for (int rr = 0; rr < T::RBM; ++rr) {
+            if (!RBC && rr >= nr) continue;
+            uint32_t wd[8] = {(uint32_t)F.x[rr].x, (uint32_t)F.x[rr].y, (uint32_t)F.x[rr].z, (uint32_t)F.x[rr].w,
+                              0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int i = 0; i < T::NX; ++i) wd[4 + i] = F.nx[rr][i];
+#pragma unroll
+            for (int s = 0; s < T::KWM; ++s) {
+                if (!KWC && s >= KW) continue;
+                const int d = s >> 2, sh = s & 3;
+                v4i b;
+                if (sh == 0) {
+                    b = v4i{(int)wd[d], (int)wd[d + 1], (int)wd[d + 2], (int)wd[d + 3]};
+                } else {
+                    b = v4i{(int)__builtin_amdgcn_alignbyte(wd[d + 1], wd[d], sh),
+                            (int)__builtin_amdgcn_alignbyte(wd[d + 2], wd[d + 1], sh),
+                            (int)__builtin_amdgcn_alignbyte(wd[d + 3], wd[d + 2], sh),
+                            (int)__builtin_amdgcn_alignbyte(wd[d + 4], wd[d + 3], sh)};
+                }
+#pragma unroll
+                for (int f = 0; f < FM; ++f) acc[f][rr][s] = MF::run(b, F.a[f], acc[f][rr][s]);
+            }
+        }
+    };
+    auto compute = [&](const int8_t* st, int64_t kt0, auto FULL) {
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+            Frags F;
+            load(F, st, u);
+            process(F, decltype(FULL)::value || kt0 + T::WAVES * u + w < p.ktiles);
+        }
+    };
+
+    // ring of STAGES chunks: chunk c + STAGES - 1 is issued once every wave
+    // has passed the barrier that follows its reads of chunk c - 1 (same stage)
+    for (int k = 0; k < T::STAGES - 1; ++k)
+        if (k < nch) issue(k);
+    for (int c = 0; c < nch; ++c) {
+        wait_chunk(min(T::STAGES - 2, nch - 1 - c));
+        wait_lgkm0();
+        __builtin_amdgcn_s_barrier();
+        if (c + T::STAGES - 1 < nch) issue(c + T::STAGES - 1);
+        const int64_t kt0 = (c_beg + c) * kCwTiles;
+        if (kt0 + kCwTiles <= p.ktiles) compute(smem + (c % T::STAGES) * T::kStage, kt0, std::true_type());
+        else compute(smem + (c % T::STAGES) * T::kStage, kt0, std::false_type());
+    }
+
+    // Sum the waves' accumulators through LDS, a pass of up to TP tiles
+    // (f, rr, s) at a time: each wave stores its 16 x 16 tiles as they sit
+    // in its lanes (lane l: output channel l % 16, input channels
+    // 4 (l / 16) .. + 3), one 1 KB row per tile; then item (tile, lane) of
+    // the pass adds the WAVES rows and writes the 4 outputs.
+    constexpr int NT = FM * T::RBM * T::KWM;
+    constexpr int TP = NT < T::kSmem / (T::WAVES * 1024) ? NT : T::kSmem / (T::WAVES * 1024);
+    static_assert(TP >= 1, "one tile per pass fits the ring");
+    const int64_t Ng = (int64_t)p.KH * KW * p.C_in;
+    const bool split_k = pl.splits > 1;
+    float base = 0.0f;
+    if (!split_k && p.out) base = __fmul_rn(p.gs->step, p.os->step);
+    const bool vec4 = (p.C_in & 3) == 0;
+    wait_lgkm0();
+    __syncthreads();
+#pragma unroll
+    for (int t0 = 0; t0 < NT; t0 += TP) {
+#pragma unroll
+        for (int tl = t0; tl < min(NT, t0 + TP); ++tl) {
+            const int f = tl / (T::RBM * T::KWM), rs = tl % (T::RBM * T::KWM), rr = rs / T::KWM, s = rs % T::KWM;
+            if ((!RBC && rr >= nr) || (!KWC && s >= KW)) continue;
+            *reinterpret_cast<v4i*>(smem + ((w * TP + (tl - t0)) * 64 + lane) * 16) = acc[f][rr][s];
+        }
+        __syncthreads();
+        const int nt = min(NT, t0 + TP) - t0;
+        for (int item = tid; item < nt * 64; item += 64 * T::WAVES) {
+            const int tl = t0 + item / 64, l = item % 64;
+            const int f = tl / (T::RBM * T::KWM), rs = tl % (T::RBM * T::KWM), rr = rs / T::KWM, s = rs % T::KWM;
+            if (rr >= nr || s >= KW) continue;
+            const int64_t co = co0 + f * 16 + (l & 15), ci = ci0 + 4 * (l >> 4);
+            if (co >= p.C_out || ci >= p.C_in) continue;
+            v4i sum = v4i{0, 0, 0, 0};
+#pragma unroll
+            for (int ww = 0; ww < T::WAVES; ++ww)
+                sum += *reinterpret_cast<const v4i*>(smem + ((ww * TP + (tl - t0)) * 64 + l) * 16);
+            const int nv = (int)min((int64_t)4, p.C_in - ci);
+            const int64_t j = ((int64_t)(r0 + rr) * KW + s) * p.C_in + ci;
+            const int vv[4] = {sum.x, sum.y, sum.z, sum.w};
+            if (split_k) {
+                int32_t* dst = p.part + ((int64_t)split * p.C_out + co) * Ng + j;
+                if (vec4) *reinterpret_cast<v4i*>(dst) = sum;
+                else
+                    for (int e = 0; e < nv; ++e) dst[e] = vv[e];
+                continue;
+            }
+            if (p.acc)
+                for (int e = 0; e < nv; ++e) p.acc[co * p.ld_acc + j + e] = vv[e];
+            if (p.out) {
+                const float sc = __fmul_rn(base, pow2f(-(int)p.group[co]));
+                for (int e = 0; e < nv; ++e) p.out[co * p.ld_out + j + e] = __fmul_rn((float)vv[e], sc);
+            }
+        }
+        __syncthreads();
+    }
+#endif
+}
+
+ConvWgradPlan conv_wgrad_plan(int64_t K, int64_t C_out, int64_t C_in, int KH, int KW, int64_t Wp) {
+    ConvWgradPlan pl;
+    pl.fm = C_out > 16 ? 2 : 1;
+    const bool three = KH == 3 && KW == 3 && 2 * Wp <= kCwHalo;
+    if (three) {
+        pl.kwc = 3;
+        pl.rbc = 3;
+        pl.rb = 3;
+    } else {
+        pl.fm = 1;   // runtime window: one fragment of output channels, at most 2 tap rows
+        pl.rb = (int)std::max<int64_t>(1, std::min<int64_t>({(int64_t)KH, 2, 1 + kCwHalo / Wp}));
+    }
+    pl.tap_groups = (KH + pl.rb - 1) / pl.rb;
+    pl.tiles_ci = (C_in + 15) / 16;
+    pl.tiles = (C_out + 16 * pl.fm - 1) / (16 * pl.fm) * pl.tiles_ci * pl.tap_groups;
+    const int64_t ktiles = (K + 63) / 64;
+    pl.chunks = (ktiles + kCwTiles - 1) / kCwTiles;
+    // about one block per CU; each split holds whole chunks and none is empty
+    int64_t splits = std::max<int64_t>(1, (256 + pl.tiles / 2) / pl.tiles);
+    splits = std::max<int64_t>(1, std::min(splits, pl.chunks));
+    const int64_t per = std::max<int64_t>(1, (pl.chunks + splits - 1) / splits);
+    pl.per = (int)per;
+    pl.splits = (int)std::max<int64_t>(1, (pl.chunks + per - 1) / per);
+    return pl;
+}
+
+hipError_t launch_conv_wgrad(const ConvWgradArgs& a, const ConvWgradPlan& pl, hipStream_t s) {
+    if (a.C_out <= 0 || a.C_in <= 0 || pl.chunks <= 0) return hipSuccess;
+    if (a.lda % 16 || a.ldx % 16 || a.Wp <= 0 || a.Wp % 16 || a.KH < 1 || a.KW < 1 || a.KW > 16 ||
+        (int64_t)(pl.rb - 1) * a.Wp > kCwHalo || (pl.kwc && (pl.kwc != a.KW || pl.rbc != a.KH)) ||
+        (!pl.kwc && (pl.fm != 1 || pl.rb > 2)))
+        return hipErrorInvalidValue;
+    if (pl.splits > 1 ? !a.part : (!a.acc && !a.out)) return hipErrorInvalidValue;
+    // every byte offset (row, chunk, row shift, halo) fits the 31-bit buffer range
+    const int64_t lim = (int64_t)1 << 31;
+    if (a.C_out * a.lda >= lim || a.C_in * a.ldx >= lim ||
+        a.C_in * a.ldx + pl.chunks * kCwTiles * 64 + (int64_t)a.KH * a.Wp + kCwX >= lim ||
+        a.C_out * a.lda + pl.chunks * kCwTiles * 64 + kCwA >= lim)
+        return hipErrorInvalidValue;
+    const dim3 grid((unsigned)(pl.tiles * pl.splits));
+    if (pl.kwc == 3 && pl.fm == 2)
+        hipLaunchKernelGGL((k_conv_wgrad<2, 3, 3>), grid, dim3(64 * CwCfg<2, 3, 3>::WAVES), 0, s, a, pl);
+    else if (pl.kwc == 3)
+        hipLaunchKernelGGL((k_conv_wgrad<1, 3, 3>), grid, dim3(64 * CwCfg<1, 3, 3>::WAVES), 0, s, a, pl);
+    else
+        hipLaunchKernelGGL((k_conv_wgrad<1, 0, 0>), grid, dim3(64 * CwCfg<1, 0, 0>::WAVES), 0, s, a, pl);
     return hipGetLastError();
 }
 

@@ -145,12 +145,6 @@ struct GemmArgs {
     // device {first K column, K columns} replacing [0, K) (the per-group
     // GEMMs of the GEMM-based comparison), may be null
     const int32_t* kseg;
-    // Implicit-im2col conv wgrad (wg_KH > 0): B row j = (r KW + s) C_in + ci
-    // is row s C_in + ci of B (the input codes on the padded pixel grid,
-    // pre-shifted by s), read from byte r Wp of its K range (the tap's row
-    // shift on a grid of width Wp, a multiple of 16); B has KW C_in rows.
-    int wg_KH, wg_KW;
-    int64_t wg_Cin, wg_Wp;
     // with out: max |out| per 32-row slab and column, as bit patterns,
     // [ceil(Mg / 32), Ng] (producer-side channel ranges of the next quantizer)
     uint32_t* ranges;
@@ -197,12 +191,41 @@ hipError_t launch_dequant(const int32_t* acc, int64_t rows, int64_t cols, int64_
 int wgrad_splits(int64_t M, int64_t C_out, int64_t C_in);
 
 // Padded pixel grids of the implicit-im2col conv wgrad (see sq_conv_wgrad):
-// out[j, P] for P < ld_out, j < copies * C: P + s (s = j / C) read as pixel
-// (n, hp - top, wp - left) of the content grid Hc x Wc inside the Hp x Wp grid
-// of image n, i.e. in[j % C, (n Hc + h) Wc + w], or 0 outside the content.
-hipError_t launch_grid_scatter(const int8_t* in, int64_t ld_in, int64_t C, int copies, int64_t N, int64_t Hc,
-                               int64_t Wc, int64_t top, int64_t left, int64_t Hp, int64_t Wp, int8_t* out,
-                               int64_t ld_out, hipStream_t s);
+// out[c, G] for G < ld_out (a multiple of 16), G = n Hp Wp + hp Wp + wp, is
+// pixel (n, hp - top, wp - left) of the content grid Hc x Wc of image n, i.e.
+// in[c, (n Hc + h) Wc + w], or 0 outside the content.  Wp and ld_in are
+// multiples of 16, in 16-byte aligned.
+hipError_t launch_grid_pack(const int8_t* in, int64_t ld_in, int64_t C, int64_t N, int64_t Hc, int64_t Wc,
+                            int64_t top, int64_t left, int64_t Hp, int64_t Wp, int8_t* out, int64_t ld_out,
+                            hipStream_t s);
+
+// Implicit-im2col conv wgrad from one copy of the input grid (k_conv_wgrad):
+// acc[co, (r KW + s) C_in + ci] = sum_P A[co, P] X[ci, P + r Wp + s] over
+// P < K (K a multiple of 64); X rows readable (zeros) through column
+// K + (KH - 1) Wp + 64.  The plan fixes the kernel variant, the tiles and the
+// K splits; splits > 1 write int32 partials [splits, C_out, KH KW C_in] to
+// `part`, which launch_splitk_reduce then sums with the epilogue.
+struct ConvWgradPlan {
+    int fm = 1, kwc = 0, rbc = 0;   // output-channel fragments per block, compile-time KW / tap rows (0: runtime)
+    int rb = 1, tap_groups = 1;     // tap rows per block and blocks along the window height
+    int64_t tiles_ci = 1, tiles = 1;
+    int64_t chunks = 0;             // 16-tile K chunks
+    int splits = 1, per = 1;        // K splits, chunks per split
+};
+ConvWgradPlan conv_wgrad_plan(int64_t K, int64_t C_out, int64_t C_in, int KH, int KW, int64_t Wp);
+struct ConvWgradArgs {
+    const int8_t* A; int64_t lda;   // gradient codes on the grid [C_out, lda]
+    const int8_t* X; int64_t ldx;   // input codes on the grid [C_in, ldx]
+    int64_t C_out, C_in, Wp, ktiles;
+    int KH, KW;
+    int32_t* part;                  // split K: partials [splits, C_out, KH KW C_in]
+    int32_t* acc; int64_t ld_acc;   // no split: int32 and / or fp32 outputs
+    float* out; int64_t ld_out;
+    const uint8_t* group;
+    const sq_scale* gs;
+    const sq_scale* os;
+};
+hipError_t launch_conv_wgrad(const ConvWgradArgs& a, const ConvWgradPlan& plan, hipStream_t s);
 
 // ---- L1BNQ (sq_l1bn.hip) ----
 // Partial-maximum slabs of the backward's dx ranges; int32 partial words of

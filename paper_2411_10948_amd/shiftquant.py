@@ -815,9 +815,10 @@ class ConvBackwardPlan(BackwardPlan):
     gradient taken by sq_conv_dgrad (implicit im2col and col2im: dX is
     [N*H*W, C_in_ch], NHWC) and the weight gradient by sq_conv_wgrad on the
     packed input codes (implicit_wgrad, the default: ``run`` takes the output
-    of conv_pack_input as its xq_t argument) or by sq_gemm_wgrad on the
-    im2col'd activations.  Buffers are allocated once; ``run`` allocates
-    nothing."""
+    of conv_pack_input as its xq_t argument, ``run_packed`` the input codes
+    xq_t [C_in, >= N*H*W] of sq_quantize_tensor, which it packs onto the
+    plan's grid first) or by sq_gemm_wgrad on the im2col'd activations.
+    Buffers are allocated once; ``run`` and ``run_packed`` allocate nothing."""
 
     def __init__(self, N: int, H: int, W: int, C_out: int, C_in_ch: int, KH: int, KW: int, PH: int, PW: int,
                  params: Params, device="cuda", want_acc: bool = False, implicit_wgrad: bool = True,
@@ -840,6 +841,9 @@ class ConvBackwardPlan(BackwardPlan):
             # the quantizer never writes the padding of the grid: zero it once
             self.q_tp = torch.zeros((C_out, qld), dtype=torch.int8, device=dev)
             self.q_t = None
+            # the input codes on the grid (written whole by pack_input)
+            xrows, xld, _ = sq_conv_wgrad_layout(N, H, W, C_in_ch, KH, KW, PH, PW)
+            self.x_grid = torch.empty((max(xrows, 1), xld), dtype=torch.int8, device=dev)[:xrows]
         self.ws_d = _workspace(sq_conv_dgrad_workspace_size(C_out, C_in_ch, KH, KW, params), dev)
         self.dX = torch.empty((N * H * W, C_in_ch), dtype=torch.float32, device=dev)
         self.acc_dX = torch.empty((N * H * W, C_in_ch), dtype=torch.int32, device=dev) if want_acc else None
@@ -871,6 +875,16 @@ class ConvBackwardPlan(BackwardPlan):
         N, H, W, KH, KW, PH, PW = self.geom
         sq_quantize_grad_conv_from_ranges(dY, N, H, W, KH, KW, PH, PW, self.params, ranges, slabs, self.q_fold,
                                           self.q_tp, self.group, self.scale, self.layout, self.ws_q, stream)
+
+    def pack_input(self, xq_t, stream=None):
+        """The input codes xq_t [C_in, >= N*H*W] onto the plan's padded grid."""
+        N, H, W, KH, KW, PH, PW = self.geom
+        sq_conv_pack_input(xq_t, N, H, W, self.C_in_ch, KH, KW, PH, PW, self.x_grid, stream)
+
+    def run_packed(self, dY, wq_t, wscale, xq_t, xscale, stream=None):
+        """The step from unpacked input codes: pack_input, then run."""
+        self.pack_input(xq_t, stream)
+        return self.run(dY, wq_t, wscale, self.x_grid, xscale, stream)
 
     def wgrad(self, xq_t, xscale, stream=None):
         if not self.implicit_wgrad:

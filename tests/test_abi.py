@@ -223,14 +223,15 @@ def test_conv_wgrad_and_ranged_dgrad_validation_no_launch(sq):
     rows, ld, qld = ct.c_int64(0), ct.c_int64(0), ct.c_int64(0)
     # padded grid of the ResNet-18 layer: 58 rows x 64 columns per image
     assert L.sq_conv_wgrad_layout(64, 56, 56, 64, 3, 3, 1, 1, ct.byref(rows), ct.byref(ld), ct.byref(qld)) == 0
-    assert rows.value == 3 * 64 and qld.value == 64 * 58 * 64 and ld.value == qld.value + 2 * 64
+    # one input copy: C_in rows, the grid plus (KH - 1) Wp + 64 zero columns
+    assert rows.value == 64 and qld.value == 64 * 58 * 64 and ld.value == qld.value + 2 * 64 + 64
     # padding >= window, window larger than the input
     assert L.sq_conv_wgrad_layout(1, 5, 5, 8, 3, 3, 3, 1, ct.byref(rows), ct.byref(ld), ct.byref(qld)) == 1
     assert L.sq_conv_wgrad_layout(1, 1, 5, 8, 3, 3, 0, 1, ct.byref(rows), ct.byref(ld), ct.byref(qld)) == 1
     nb = ct.c_size_t(0)
     assert L.sq_conv_wgrad_workspace_size(64, 56, 56, 64, 64, 3, 3, 1, 1, ct.byref(p), ct.byref(nb)) == 0
-    # wrong ld of the packed input, NULL outputs
-    assert L.sq_conv_wgrad(fake, qld.value, fake, fake, fake, ld.value + 16, fake, 64, 56, 56, 64, 64, 3, 3, 1, 1,
+    # too short a row of the packed input, NULL outputs
+    assert L.sq_conv_wgrad(fake, qld.value, fake, fake, fake, ld.value - 16, fake, 64, 56, 56, 64, 64, 3, 3, 1, 1,
                            ct.byref(p), fake, 576, fake, 576, fake, 1 << 30, None) == 1
     assert L.sq_conv_wgrad(fake, qld.value, fake, fake, fake, ld.value, fake, 64, 56, 56, 64, 64, 3, 3, 1, 1,
                            ct.byref(p), None, 0, None, 0, fake, 1 << 30, None) == 1

@@ -121,27 +121,38 @@ def test_conv_wgrad_full_resnet18_layer(sq):
     np.testing.assert_allclose(dW, dW_ref, rtol=RTOL, atol=0)
 
 
-def test_conv_pack_input_layout(sq):
-    # the packed input is the padded grid of each channel shifted by s, zeros elsewhere
+PACK_CASES = [  # N, H, W, C_in, KH, KW, PH, PW, ld_xq extra
+    (2, 5, 7, 3, 3, 3, 1, 1, 0),      # odd left padding, rows of 7 pixels
+    (3, 6, 16, 5, 3, 3, 1, 1, 16),    # a content row ends at a chunk edge
+    (1, 9, 30, 2, 5, 5, 2, 2, 32),    # 2-pixel padding, 3 chunks per grid row
+    (2, 4, 13, 4, 1, 1, 0, 0, 0),     # no padding, Wp = 16 > W
+    (1, 3, 33, 1, 3, 7, 0, 6, 48),    # padding wider than a word, Wp = 48
+]
+
+
+@pytest.mark.parametrize("case", PACK_CASES)
+def test_conv_pack_input_layout(sq, case):
+    # the packed input is the padded grid of each channel, zeros elsewhere
+    # (every byte of the row, through its leading dimension)
     import torch
-    N, H, W, C_in, KH, KW, PH, PW = 2, 5, 7, 3, 3, 3, 1, 1
-    rng = np.random.default_rng(3)
+    N, H, W, C_in, KH, KW, PH, PW, extra = case
+    rng = np.random.default_rng(sum(case))
     xq = rng.integers(-127, 128, (N * H * W, C_in)).astype(np.int8)
-    xq_t = torch.zeros((C_in, 80), dtype=torch.int8, device="cuda")
+    ld_xq = (N * H * W + 15) // 16 * 16 + extra
+    # bytes past N H W in each row are garbage the pack must not copy
+    xq_t = torch.from_numpy(rng.integers(-127, 128, (C_in, ld_xq)).astype(np.int8)).cuda()
     xq_t[:, :N * H * W] = torch.from_numpy(xq.T.copy()).cuda()
     xs = sq.conv_pack_input(xq_t, N, H, W, KH, KW, PH, PW)
     torch.cuda.synchronize()
-    rows, ld, _ = sq.sq_conv_wgrad_layout(N, H, W, C_in, KH, KW, PH, PW)
-    Hp, Wp = H + 2 * PH, 16
-    assert rows == KW * C_in and ld % 16 == 0
-    got = xs.cpu().numpy()
-    grid = np.zeros((C_in, ld + KW), np.int8)
+    rows, ld, qld = sq.sq_conv_wgrad_layout(N, H, W, C_in, KH, KW, PH, PW)
+    Hp, Wp = H + 2 * PH, (W + 2 * PW + 15) // 16 * 16
+    assert rows == C_in and ld % 16 == 0 and ld == qld + (KH - 1) * Wp + 64
+    grid = np.zeros((C_in, ld), np.int8)
     for n in range(N):
         for h in range(H):
             for w in range(W):
                 grid[:, n * Hp * Wp + (h + PH) * Wp + (w + PW)] = xq[(n * H + h) * W + w]
-    for s in range(KW):
-        np.testing.assert_array_equal(got[s * C_in:(s + 1) * C_in], grid[:, s:s + ld])
+    np.testing.assert_array_equal(xs.cpu().numpy(), grid)
 
 
 def test_conv_wgrad_rejects_bad_geometry(sq):
