@@ -1495,6 +1495,24 @@ int wgrad_splits(int64_t M, int64_t C_out, int64_t C_in) {
     return (int)((ktiles + per - 1) / per);
 }
 
+namespace {
+// The product restricted to output rows [r0, Mg) (r0 a multiple of 256):
+// every row-indexed pointer moves to row r0.
+GemmArgs rows_from(const GemmArgs& a, int64_t r0) {
+    GemmArgs b = a;
+    auto row_ptr = [&](const int8_t* base, int64_t ld) {
+        return a.tiled ? base + (r0 / 16) * (ld / 64) * 1024 : base + r0 * ld;
+    };
+    b.A = row_ptr(a.A, a.lda);
+    if (a.extA) b.extA = row_ptr(a.extA, a.ld_extA);
+    if (a.acc) b.acc = a.acc + r0 * a.ld_acc;
+    if (a.out) b.out = a.out + r0 * a.ld_out;
+    if (a.group && a.epi_mode == 1) b.group = a.group + r0;
+    b.Mg = a.Mg - r0;
+    return b;
+}
+}  // namespace
+
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     if (a.Mg <= 0 || a.Ng <= 0) return hipSuccess;
     const bool pipe = pipe_ok(a);
@@ -1502,6 +1520,22 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     if (a.tiled && (!pipe || a.taps || a.kseg)) return hipErrorInvalidValue;
     if (a.kseg && (!pipe || a.splits > 1 || a.layout)) return hipErrorInvalidValue;   // pipelined kernel only
     const Pick p = pick(a);
+    if (p == Pick::kLarge && pipe && a.splits <= 1 && !a.ranges && !a.part && !a.taps && !a.kseg) {
+        // A last round of large tiles that would leave a quarter or more of
+        // the CUs idle: the rows of the full rounds take the large tiles and
+        // the remaining rows one round of smaller tiles (two launches).
+        const int64_t tn = (a.Ng + PipeLarge::BN - 1) / PipeLarge::BN;
+        const int64_t tiles = tn * ((a.Mg + PipeLarge::BM - 1) / PipeLarge::BM);
+        const int64_t rounds = tiles / kCUs, rem = tiles - rounds * kCUs;
+        const int64_t rows_main = (rounds * kCUs / tn) * PipeLarge::BM;
+        if (rounds >= 1 && rem > 0 && 4 * rem <= 3 * kCUs && rows_main > 0 && rows_main < a.Mg) {
+            GemmArgs m = a;
+            m.Mg = rows_main;
+            const hipError_t e = launch_gemm(m, s);
+            if (e != hipSuccess) return e;
+            return launch_gemm(rows_from(a, rows_main), s);
+        }
+    }
     const int64_t ktiles = (a.K + 63) / 64;   // every configuration has 64-byte K tiles
     const int splits = std::max(1, a.splits);
     const int64_t per = splits > 1 ? (ktiles + splits - 1) / splits : std::max<int64_t>(ktiles, 1);

@@ -122,14 +122,16 @@ __global__ __launch_bounds__(kColThreads) void k_colmax(const float* __restrict_
         int64_t m = m_begin + rl;
         if constexpr (VEC == 4) {
             if (c0 + 4 <= C) {
-                // batches of 8 rows, the next batch in flight while one is reduced
+                // batches of 8 rows, the next batch in flight while one is
+                // reduced.  Rows past the slab re-read its last row (the
+                // maximum is unchanged): no branch between the loads, so the
+                // wait before a batch's reduction leaves the next batch in flight.
                 const int64_t step = nrl;
                 auto load8 = [&](int64_t mm, float4 (&v)[8]) {
 #pragma unroll
                     for (int u = 0; u < 8; ++u) {
-                        const int64_t row = mm + u * step;
-                        v[u] = row < m_end ? *reinterpret_cast<const float4*>(x + row * ld + c0)
-                                           : make_float4(0.f, 0.f, 0.f, 0.f);
+                        const int64_t row = min(mm + u * step, m_end - 1);
+                        v[u] = *reinterpret_cast<const float4*>(x + row * ld + c0);
                     }
                 };
                 auto reduce8 = [&](const float4 (&v)[8]) {
@@ -141,14 +143,15 @@ __global__ __launch_bounds__(kColThreads) void k_colmax(const float* __restrict_
                         best[3] = max(best[3], absbits(v[u].w));
                     }
                 };
-                float4 va[8], vb[8];
-                if (m < m_end) load8(m, va);
-                for (; m < m_end; m += 16 * step) {
-                    if (m + 8 * step < m_end) load8(m + 8 * step, vb);
-                    reduce8(va);
-                    if (m + 8 * step >= m_end) break;
-                    if (m + 16 * step < m_end) load8(m + 16 * step, va);
-                    reduce8(vb);
+                if (m < m_end) {
+                    float4 va[8], vb[8];
+                    load8(m, va);
+                    for (; m < m_end; m += 16 * step) {
+                        load8(m + 8 * step, vb);
+                        reduce8(va);
+                        load8(m + 16 * step, va);
+                        reduce8(vb);
+                    }
                 }
                 m = m_end;
             }
