@@ -653,8 +653,10 @@ sq_status sq_l1bn_backward(const float* dy, int64_t M, int64_t C, int64_t ld_dy,
 /* Static description of a status code. */
 const char* sq_status_string(sq_status s);
 
-/* Message of the last failed call on this thread ("" if none). */
+/* Message of the last failed call on this thread ("" if none);
+ * sq_last_error_string is the same function under a second name. */
 const char* sq_last_error(void);
+const char* sq_last_error_string(void);
 
 #ifdef __cplusplus
 }

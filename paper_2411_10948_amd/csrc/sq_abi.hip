@@ -206,6 +206,7 @@ const char* sq_status_string(sq_status s) {
 }
 
 const char* sq_last_error(void) { return g_last_error.c_str(); }
+const char* sq_last_error_string(void) { return g_last_error.c_str(); }
 
 sq_status sq_grad_layout_size(int64_t C_out, const sq_quant_params* p, size_t* layout_bytes, int64_t* min_ld_fold) {
     SQ_TRY(check_params(p));

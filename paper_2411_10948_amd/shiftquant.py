@@ -47,7 +47,7 @@ EXPORTS = (
     "sq_conv_wgrad_layout", "sq_conv_pack_input", "sq_conv_pack_grad", "sq_quantize_grad_conv",
     "sq_conv_wgrad_workspace_size", "sq_conv_wgrad", "sq_gemm_dgrad_range_slabs", "sq_gemm_dgrad_ranged",
     "sq_quantize_grad_noalloc", "sq_conv_dgrad_ranged", "sq_quantize_grad_conv_from_ranges",
-    "sq_status_string", "sq_last_error",
+    "sq_status_string", "sq_last_error", "sq_last_error_string",
 )
 
 
@@ -170,6 +170,8 @@ def load() -> ct.CDLL:
     L.sq_status_string.restype = ct.c_char_p
     L.sq_last_error.argtypes = []
     L.sq_last_error.restype = ct.c_char_p
+    L.sq_last_error_string.argtypes = []
+    L.sq_last_error_string.restype = ct.c_char_p
     _lib = L
     return L
 

@@ -82,6 +82,7 @@ def test_invalid_params_rejected(sq):
         p = sq.Params.make(bits, ng, mode)
         assert L.sq_grad_layout_size(64, ct.byref(p), ct.byref(nb), ct.byref(ld)) == 1
         assert sq.sq_last_error()
+        assert L.sq_last_error_string().decode() == sq.sq_last_error()
     p = sq.Params.make(4, 4, 0)
     p.layout = 2
     assert L.sq_grad_layout_size(64, ct.byref(p), ct.byref(nb), ct.byref(ld)) == 1
