@@ -998,7 +998,7 @@ __global__ __launch_bounds__(kBlock) void k_quantize8(const float* __restrict__ 
                                                       int8_t* __restrict__ q_fold, int64_t ld_fold,
                                                       int8_t* __restrict__ q_t, int64_t ld_t,
                                                       const int32_t* __restrict__ desc, int64_t ext_base,
-                                                      int meta_vec) {
+                                                      int meta_vec, PadGrid pg) {
     constexpr int TR = 128, TC = 64, TW = TR / 4 + 1;   // LDS words per channel row (padded)
     __shared__ uint32_t tq[TC * TW];
     const int tid = threadIdx.x, g8 = tid & 7, rq = tid >> 3;
@@ -1110,6 +1110,28 @@ __global__ __launch_bounds__(kBlock) void k_quantize8(const float* __restrict__ 
                 if (TL) {
                     *reinterpret_cast<uint4*>(q_t + tiled_off(c, mm, ld_t)) = a;
                     *reinterpret_cast<uint4*>(q_t + tiled_off(c, mm + 16, ld_t)) = b;
+                } else if (pg.Wo) {
+                    // padded pixel grid (Wo % 8 == 0): pixel m = (n, oh, ow) at
+                    // n HpWp + oh Wp + ow; the 4 groups of 8 pixels never cross an
+                    // image row, so each is one 8-byte store (16-byte stores of
+                    // aligned pairs, behind a branch, measured slower)
+                    const uint32_t m0 = (uint32_t)mm;
+                    uint32_t n = m0 / pg.HoWo, rem = m0 - n * pg.HoWo, oh = rem / pg.Wo, ow = rem - oh * pg.Wo;
+                    int8_t* row = q_t + c * ld_t;
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        if (mm + 8 * g < M)
+                            *reinterpret_cast<uint2*>(row + (int64_t)n * pg.HpWp + (int64_t)oh * pg.Wp + ow) =
+                                make_uint2(src[2 * g], src[2 * g + 1]);
+                        ow += 8;
+                        if (ow == pg.Wo) {
+                            ow = 0;
+                            if (++oh * pg.Wo == pg.HoWo) {
+                                oh = 0;
+                                ++n;
+                            }
+                        }
+                    }
                 } else if (mm + 32 <= M) {
                     *reinterpret_cast<uint4*>(q_t + c * ld_t + mm) = a;
                     *reinterpret_cast<uint4*>(q_t + c * ld_t + mm + 16) = b;
@@ -1276,20 +1298,20 @@ hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, con
     if (n_tiles(tc, tr) < kQuantMinTiles) tr = 64;
     if (n_tiles(tc, tr) < kQuantMinTiles) tc = 64;
     const int64_t eb = fold_ext_base(C);
-    if (vec && C % 8 == 0 && !pg.Wo) {
+    if (vec && C % 8 == 0 && (!pg.Wo || (pg.Wo % 8 == 0 && !tiled))) {
         // 8-channel form: one Philox block per thread and row; the groups
         // (8 bytes) and descriptors (2 x 16 bytes) of a thread's channels
         // load as vectors when aligned
         const int mv = ((reinterpret_cast<uintptr_t>(group) & 7) == 0 && (reinterpret_cast<uintptr_t>(desc) & 15) == 0);
         const dim3 g8((unsigned)std::min<int64_t>(((C + 63) / 64) * ((M + 127) / 128), kQuantMaxBlocks));
         if (sr && tiled) hipLaunchKernelGGL((k_quantize8<true, true>), g8, dim3(kBlock), 0, s, x, M, C, ld, group, scale,
-                                            cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, mv);
+                                            cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, mv, pg);
         else if (sr) hipLaunchKernelGGL((k_quantize8<true, false>), g8, dim3(kBlock), 0, s, x, M, C, ld, group, scale,
-                                        cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, mv);
+                                        cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, mv, pg);
         else if (tiled) hipLaunchKernelGGL((k_quantize8<false, true>), g8, dim3(kBlock), 0, s, x, M, C, ld, group,
-                                           scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, mv);
+                                           scale, cfg, q_fold, ld_fold, q_t, ld_t, desc, eb, mv, pg);
         else hipLaunchKernelGGL((k_quantize8<false, false>), g8, dim3(kBlock), 0, s, x, M, C, ld, group, scale, cfg,
-                                q_fold, ld_fold, q_t, ld_t, desc, eb, mv);
+                                q_fold, ld_fold, q_t, ld_t, desc, eb, mv, pg);
         return hipGetLastError();
     }
     const dim3 grid((unsigned)std::min<int64_t>(n_tiles(tc, tr), kQuantMaxBlocks));
