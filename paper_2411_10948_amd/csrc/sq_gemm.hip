@@ -1587,23 +1587,22 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
 // multiple of 16), so they map to a run of consecutive source pixels: two
 // aligned 16-byte loads of the source row cover it, and v_alignbyte moves the
 // run into place; bytes outside the content are cleared.
-__global__ __launch_bounds__(256) void k_grid_pack(const int8_t* __restrict__ in, int64_t ld_in, int64_t N,
-                                                   int64_t Hc, int64_t Wc, int64_t top, int64_t left, int64_t Hp,
-                                                   int64_t Wp, int8_t* __restrict__ out, int64_t ld_out,
-                                                   int64_t rows) {
-    const int64_t chunks = ld_out / 16, img = Hp * Wp;
-    for (int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; id < rows * chunks;
-         id += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t c = id / chunks, G0 = (id - c * chunks) * 16;
-        const int64_t n = G0 / img, rem = G0 - n * img, hp = rem / Wp, wp0 = rem - hp * Wp;
-        const int64_t ih = hp - top;
+__global__ __launch_bounds__(256) void k_grid_pack(const int8_t* __restrict__ in, int64_t ld_in, uint32_t N,
+                                                   uint32_t Hc, uint32_t Wc, uint32_t top, uint32_t left, uint32_t Hp,
+                                                   uint32_t Wp, int8_t* __restrict__ out, int64_t ld_out,
+                                                   uint32_t rows) {
+    // every index fits 32 bits (the launcher checks): no 64-bit divisions
+    const uint32_t chunks = (uint32_t)(ld_out / 16), img = Hp * Wp, total = rows * chunks;
+    for (uint32_t id = blockIdx.x * blockDim.x + threadIdx.x; id < total; id += gridDim.x * blockDim.x) {
+        const uint32_t c = id / chunks, G0 = (id - c * chunks) * 16;
+        const uint32_t n = G0 / img, rem = G0 - n * img, hp = rem / Wp, wp0 = rem - hp * Wp;
         // grid bytes [e_lo, e_hi) of the chunk hold content pixels
-        const int64_t e_lo = max((int64_t)0, left - wp0), e_hi = min((int64_t)16, Wc + left - wp0);
+        const int e_lo = (int)max(0, (int)left - (int)wp0), e_hi = (int)min(16, (int)(Wc + left) - (int)wp0);
         uint32_t o[4] = {0u, 0u, 0u, 0u};
-        if (n < N && ih >= 0 && ih < Hc && e_lo < e_hi) {
-            const int8_t* src = in + c * ld_in;
+        if (n < N && hp >= top && hp - top < Hc && e_lo < e_hi) {
+            const int8_t* src = in + (int64_t)c * ld_in;
             // source index of grid byte 0 (before the row start when wp0 < left)
-            const int64_t lo = (n * Hc + ih) * Wc + wp0 - left;
+            const int64_t lo = (int64_t)((n * Hc + (hp - top)) * Wc) + (int64_t)wp0 - (int64_t)left;
             const int64_t a16 = lo >= 0 ? (lo & ~(int64_t)15) : -16;
             const int off = (int)(lo - a16);
             uint32_t w[8];
@@ -1624,13 +1623,12 @@ __global__ __launch_bounds__(256) void k_grid_pack(const int8_t* __restrict__ in
             const uint32_t b = (uint32_t)(off & 3);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int lo_i = (int)min((int64_t)4, max((int64_t)0, e_lo - 4 * i));
-                const int hi_i = (int)min((int64_t)4, max((int64_t)0, e_hi - 4 * i));
+                const int lo_i = min(4, max(0, e_lo - 4 * i)), hi_i = min(4, max(0, e_hi - 4 * i));
                 const uint32_t m = hi_i > lo_i ? (0xFFFFFFFFu >> (32 - 8 * (hi_i - lo_i))) << (8 * lo_i) : 0u;
                 o[i] = __builtin_amdgcn_alignbyte(sel[i + 1], sel[i], b) & m;
             }
         }
-        *reinterpret_cast<uint4*>(out + c * ld_out + G0) = make_uint4(o[0], o[1], o[2], o[3]);
+        *reinterpret_cast<uint4*>(out + (int64_t)c * ld_out + G0) = make_uint4(o[0], o[1], o[2], o[3]);
     }
 }
 
@@ -1640,8 +1638,13 @@ hipError_t launch_grid_pack(const int8_t* in, int64_t ld_in, int64_t C, int64_t 
     if (ld_out % 16 || ld_in % 16 || Wp % 16) return hipErrorInvalidValue;
     const int64_t work = C * (ld_out / 16);
     if (work <= 0) return hipSuccess;
+    // 32-bit indices: chunks, grid positions and source pixels
+    const int64_t lim = (int64_t)1 << 31;
+    if (work >= lim || ld_out >= lim || N * Hp * Wp >= lim || N * Hc * Wc >= lim || C >= lim)
+        return hipErrorInvalidValue;
     const dim3 grid((unsigned)std::min<int64_t>((work + 255) / 256, 16384));
-    hipLaunchKernelGGL(k_grid_pack, grid, dim3(256), 0, s, in, ld_in, N, Hc, Wc, top, left, Hp, Wp, out, ld_out, C);
+    hipLaunchKernelGGL(k_grid_pack, grid, dim3(256), 0, s, in, ld_in, (uint32_t)N, (uint32_t)Hc, (uint32_t)Wc,
+                       (uint32_t)top, (uint32_t)left, (uint32_t)Hp, (uint32_t)Wp, out, ld_out, (uint32_t)C);
     return hipGetLastError();
 }
 
