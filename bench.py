@@ -474,6 +474,43 @@ def run_conv_chain(args, torch, sq):
     return 0
 
 
+def run_vendor_gemm(args, torch, wl, M):
+    """The vendor library's int8 GEMM (torch._int_mm, int32 output) on the
+    layer's two backward product shapes, for comparison with the ShiftQuant
+    GEMMs: dX = dY W as [M, C_out] x [C_out, C_in] and dW = dY^T X as
+    [C_out, M] x [M, C_in], second operand column-major (its faster layout).
+    Warm, back-to-back launches; random codes in [-31, 31]."""
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    shapes = {"dgrad": (M, wl.C_out, wl.C_in), "wgrad": (wl.C_out, M, wl.C_in)}
+    out = {}
+    for name, (m, k, n) in shapes.items():
+        a = torch.randint(-31, 32, (m, k), dtype=torch.int8, device=dev, generator=g)
+        b = torch.randint(-31, 32, (n, k), dtype=torch.int8, device=dev, generator=g).t()
+        for _ in range(args.warmup):
+            torch._int_mm(a, b)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            torch._int_mm(a, b)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        out[name] = {"ms": ms, "TOPS": 2.0 * m * n * k / ms / 1e9, "shape_mkn": [m, k, n]}
+        del a, b
+    total_ms = sum(v["ms"] for v in out.values())
+    ops = 4.0 * M * wl.C_out * wl.C_in
+    print(json.dumps({"metric": "vendor int8 GEMM (torch._int_mm) TOPS on the backward product shapes",
+                      "value": ops / total_ms / 1e9, "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
+                      "warmup": args.warmup, "ms_per_step": total_ms, "higher_is_better": True, "dtype": "int8",
+                      "data": "synthetic", "config": {"workload": wl.name, "M": M, "C_out": wl.C_out,
+                                                      "C_in": wl.C_in, "library": "hipBLASLt via torch._int_mm"},
+                      "per_product": out, "pct_int8_peak": 100.0 * ops / total_ms / 1e9 / PEAK_INT8_TOPS}))
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -487,8 +524,10 @@ def main(argv=None):
                     help="override the workload's rounding (variant runs)")
     ap.add_argument("--fused-ranges", action="store_true",
                     help="--step chain / conv_chain: the upper layer's dgrad writes the lower quantizer's ranges")
-    ap.add_argument("--step", choices=["backward", "forward", "l1bn", "chain", "conv_chain"], default="backward",
+    ap.add_argument("--step", choices=["backward", "forward", "l1bn", "chain", "conv_chain", "vendor_gemm"],
+                    default="backward",
                     help="forward: quantize X with ShiftQuant + Y = X W^T (per-output-channel W); "
+                         "vendor_gemm: the vendor int8 GEMM on the linear layer's two backward product shapes; "
                          "l1bn: the L1BNQ layer (workloads resnet18_bn_56x56x64, resnet50_bn_14x14x1024, "
                          "transformer_bn_768)")
     ap.add_argument("--conv-wgrad", choices=["implicit", "im2col"], default="implicit",
@@ -533,6 +572,12 @@ def main(argv=None):
     M, C_out, C_in = inputs["M"], wl.C_out, wl.C_in
     print(f"[bench] {args.workload}: M={M} C_out={C_out} C_in={C_in} b={wl.bits} N_G={wl.num_groups} "
           f"round={'SR' if wl.round_mode else 'RTN'}", file=sys.stderr, flush=True)
+
+    if args.step == "vendor_gemm":
+        if conv:
+            print("bench.py: --step vendor_gemm takes a linear workload", file=sys.stderr)
+            return 2
+        return run_vendor_gemm(args, torch, wl, M)
 
     if args.step == "forward":
         if conv or wl.x_kind == "conv3x3_relu":
