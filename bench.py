@@ -195,7 +195,8 @@ def run_forward(args, torch, sq, wl, inputs):
            "config": {"workload": args.workload, "step": "forward", "M": M, "C_in": C_in, "C_out": C_out,
                       "bits": wl.bits, "num_groups": wl.num_groups, "rounding": "nearest-even",
                       "weights": "8-bit per output channel", "parallelism": "none"},
-           "breakdown_ms": {k: v["ms"] for k, v in parts.items()}, "roofline": roof}
+           "breakdown_ms": {k: v["ms"] for k, v in parts.items()},
+        **({"forward_ms": forward_ms} if forward_ms else {}), "roofline": roof}
     if not args.no_cpu_baseline:
         import numpy as np
         import oracle
@@ -298,7 +299,8 @@ def run_l1bn(args, torch, sq):
            "config": {"workload": name, "step": "l1bn", "M": M, "C": C, "input_bits": 8, "grad_bits": bits,
                       "num_groups": ng, "rounding": "stochastic" if mode else "nearest-even", "parallelism": "none"},
            "pct_hbm_peak": 100.0 * value / PEAK_HBM_GBS,
-           "breakdown_ms": {k: v["ms"] for k, v in parts.items()}, "roofline": roof}
+           "breakdown_ms": {k: v["ms"] for k, v in parts.items()},
+        **({"forward_ms": forward_ms} if forward_ms else {}), "roofline": roof}
     if not args.no_cpu_baseline:
         import oracle
         rows = min(M, 1 << 18)
@@ -428,9 +430,15 @@ def run_conv_chain(args, torch, sq):
     xq_raw, xs = sq.quantize_tensor(Xc, 8, transpose=True)
     del W1, W2
     fused = args.fused_ranges
+    packed = args.conv_input == "pack"
     up = sq.ConvBackwardPlan(N, H, W, C, C, 3, 3, 1, 1, p, device=dev, dx_ranges=fused)
     lo = sq.ConvBackwardPlan(N, H, W, C, C, 3, 3, 1, 1, p, device=dev)
     stream = torch.cuda.current_stream()
+    if not packed:
+        # the forward pass's input quantizer writes each layer's grid
+        up.quantize_input(Xc, stream)
+        lo.quantize_input(Xc, stream)
+    del Xc
 
     def quant_lo():
         if fused:
@@ -439,12 +447,16 @@ def run_conv_chain(args, torch, sq):
             lo.quantize(up.dX, stream)
 
     def step():
-        # each layer packs its input codes onto its padded grid
-        up.run_packed(dY, w2_t, w2_s, xq_raw, xs, stream)
+        # --conv-input pack: each layer packs its input codes onto its grid
+        if packed:
+            up.run_packed(dY, w2_t, w2_s, xq_raw, xs, stream)
+        else:
+            up.run(dY, w2_t, w2_s, up.x_grid, up.x_scale, stream)
         quant_lo()
         lo.dgrad(w1_t, w1_s, stream)
-        lo.pack_input(xq_raw, stream)
-        lo.wgrad(lo.x_grid, xs, stream)
+        if packed:
+            lo.pack_input(xq_raw, stream)
+        lo.wgrad(lo.x_grid, xs if packed else lo.x_scale, stream)
 
     def timed(fn, K):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -467,6 +479,7 @@ def run_conv_chain(args, torch, sq):
            "config": {"workload": "resnet18_conv3x3_chain", "step": "conv_chain", "layers": 2, "N": N, "H": H,
                       "W": W, "C": C, "bits": wl.bits, "num_groups": wl.num_groups, "rounding": "nearest-even",
                       "lower_quantizer_ranges": "from the upper layer's conv dgrad" if fused else "abs-max pass",
+                      "conv_input_codes": "packed in the step" if packed else "on the grid from the forward quantizer",
                       "parallelism": "none"},
            "breakdown_ms": {"upper conv dgrad": timed(lambda: up.dgrad(w2_t, w2_s, stream), args.steps),
                             "lower quantize": timed(quant_lo, args.steps)}}
@@ -533,6 +546,10 @@ def main(argv=None):
     ap.add_argument("--conv-wgrad", choices=["implicit", "im2col"], default="implicit",
                     help="weight gradient of the fused conv step: implicit im2col (sq_conv_wgrad) or the GEMM on "
                          "the im2col'd activations")
+    ap.add_argument("--conv-input", choices=["grid", "pack"], default="grid",
+                    help="input codes of the implicit conv wgrad: written onto the padded grid by the forward "
+                         "pass's quantizer (sq_quantize_input_conv, untimed like the rest of the forward), or "
+                         "packed from sq_quantize_tensor's codes inside the timed step (sq_conv_pack_input)")
     ap.add_argument("--layout", choices=["tiled", "rows"], default="tiled",
                     help="code matrices of the linear layers: tile-major (default) or row-major")
     ap.add_argument("--dgrad", choices=["shiftmm", "grouped"], default="shiftmm",
@@ -597,16 +614,18 @@ def main(argv=None):
                             sq.LAYOUT_TILED if tiled else sq.LAYOUT_ROWS)
     wq_t, ws = sq.quantize_tensor(W, 8, transpose=True, tiled=tiled)
     implicit = conv and args.conv_wgrad == "implicit"
+    packed = implicit and args.conv_input == "pack"
     if implicit:
         # the layer input is the centre tap of the im2col'd rows (pad 1); its
         # per-tensor scale equals the im2col'd tensor's (the im2col adds only
-        # zeros).  Its codes come from the forward pass; the timed step packs
-        # them onto the padded grid (run_packed).
+        # zeros).  Its codes come from the forward pass: written onto the
+        # padded grid by the input quantizer (--conv-input grid), or as
+        # sq_quantize_tensor codes that the timed step packs (run_packed).
         X = X[:, 4 * wl.conv_cin:5 * wl.conv_cin].contiguous()
-        xq_t, xs = sq.quantize_tensor(X, 8, transpose=True)
+        xq_t, xs = sq.quantize_tensor(X, 8, transpose=True) if packed else (None, None)
     else:
         xq_t, xs = sq.quantize_tensor(X, 8, transpose=True, tiled=tiled)
-    del W, X
+    del W
     if conv:
         n_img = M // (wl.conv_hw * wl.conv_hw)
         plan = sq.ConvBackwardPlan(n_img, wl.conv_hw, wl.conv_hw, C_out, wl.conv_cin, 3, 3, 1, 1, params, device=dev,
@@ -614,6 +633,11 @@ def main(argv=None):
     else:
         plan = sq.BackwardPlan(M, C_out, C_in, params, device=dev, grouped_dgrad=args.dgrad == "grouped")
     stream = torch.cuda.current_stream()
+    if implicit and not packed:
+        plan.quantize_input(X, stream)     # the forward pass's quantizer of the layer input
+        xq_t, xs = plan.x_grid, plan.x_scale
+    else:
+        del X
     if args.calibrate_copy:
         src = torch.empty(64 << 20, dtype=torch.float32, device=dev).fill_(1.0)
         dst = torch.empty_like(src)
@@ -622,7 +646,7 @@ def main(argv=None):
         torch.cuda.synchronize()
         del src, dst
 
-    run = plan.run_packed if implicit else plan.run
+    run = plan.run_packed if packed else plan.run
     for _ in range(args.warmup):
         run(dY, wq_t, ws, xq_t, xs, stream)
     torch.cuda.synchronize()
@@ -655,11 +679,18 @@ def main(argv=None):
 
     t_quant = per_call(lambda: plan.quantize(dY, stream))
     t_dgrad = per_call(lambda: plan.dgrad(wq_t, ws, stream))
-    if implicit:
+    if packed:
         t_pack = per_call(lambda: plan.pack_input(xq_t, stream))
+        t_wgrad = per_call(lambda: plan.wgrad(plan.x_grid, xs, stream))
+    elif implicit:
         t_wgrad = per_call(lambda: plan.wgrad(plan.x_grid, xs, stream))
     else:
         t_wgrad = per_call(lambda: plan.wgrad(xq_t, xs, stream))
+    forward_ms = {}
+    if implicit and not packed:
+        # outside the step: the forward pass's input quantizer, for the record
+        forward_ms["sq_quantize_input_conv"] = per_call(lambda: plan.quantize_input(X, stream))
+        del X
     ops = 4 * M * C_out * C_in
     value = ops / (ms_step * 1e-3) / 1e12
 
@@ -675,7 +706,7 @@ def main(argv=None):
             "ms": t_wgrad, "bytes": M * C_out + M * (C_in // 9 if implicit else C_in) + 4 * C_out * C_in,
             "ops": 2 * M * C_out * C_in},
     }
-    if implicit:
+    if packed:
         # the input codes [C_in / 9, N*H*W] read, the padded grid written
         parts["sq_conv_pack_input"] = {"ms": t_pack, "bytes": M * (C_in // 9) + plan.x_grid.numel(), "ops": 0}
     dom = max(parts, key=lambda k: parts[k]["ms"])
@@ -713,10 +744,14 @@ def main(argv=None):
                    "dgrad_impl": "shiftmm" if conv else args.dgrad,
                    "wgrad_impl": ("implicit im2col (sq_conv_wgrad)" if implicit else "GEMM on im2col'd X")
                    if conv else "gemm",
+                   **({"conv_input_codes": "packed in the step (sq_conv_pack_input)" if packed else
+                       "on the padded grid from the forward quantizer (sq_quantize_input_conv)"}
+                      if implicit else {}),
                    "code_layout": "tile-major" if tiled else "row-major",
                    "parallelism": "none"},
         "pct_int8_peak": 100.0 * value / PEAK_INT8_TOPS,
         "breakdown_ms": {k: v["ms"] for k, v in parts.items()},
+        **({"forward_ms": forward_ms} if forward_ms else {}),
         "roofline": roof,
         "per_step": summarize_steps(per_step, ops),
     }

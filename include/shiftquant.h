@@ -486,6 +486,15 @@ sq_status sq_gemm_dgrad_ranged(const int8_t* q_fold, int64_t ld_fold, const int3
  *   the pack runs once per step.
  * sq_conv_pack_grad builds q_tp from transposed codes q_t [C_out, ld_t >= N Ho Wo]
  *   and writes every byte of q_tp.
+ * sq_quantize_input_conv is the forward pass's quantizer of the layer input
+ *   X [N H W, ld_X] (NHWC rows, fp32): the per-tensor b-bit codes of
+ *   sq_quantize_tensor (Sec. 5.1: activations quantized per tensor) written
+ *   straight onto the padded input grid xs, optionally also
+ *   row-major into xq [N H W, ld_xq >= C_in] (the forward's layout; NULL to
+ *   skip).  xs's padding is never written, so the caller zero-fills that
+ *   buffer once; then no pack is needed.  Workspace:
+ *   sq_quantize_tensor_workspace_size(N H W, C_in).  Errors as
+ *   sq_quantize_tensor, plus SQ_ERR_UNSUPPORTED beyond 2^32 grid pixels.
  * sq_quantize_grad_conv is sq_quantize_grad for the conv's gradient
  *   dY [N Ho Wo, ld_dY] (same codes, groups, scale, layout, q_fold, workspace)
  *   that writes the transposed codes straight onto the padded grid: q_tp's
@@ -512,6 +521,10 @@ sq_status sq_conv_pack_input(const int8_t* xq_t, int64_t ld_xq, int64_t N, int64
 sq_status sq_conv_pack_grad(const int8_t* q_t, int64_t ld_t, int64_t N, int64_t H, int64_t W, int64_t C_out,
                             int32_t KH, int32_t KW, int32_t PH, int32_t PW, int8_t* q_tp, int64_t ld_tp,
                             void* stream);
+sq_status sq_quantize_input_conv(const float* X, int64_t N, int64_t H, int64_t W, int64_t C_in, int64_t ld_X,
+                                 int32_t KH, int32_t KW, int32_t PH, int32_t PW, int32_t bits,
+                                 int8_t* xq, int64_t ld_xq, int8_t* xs, int64_t ld_xs, sq_scale* scale,
+                                 void* workspace, size_t workspace_bytes, void* stream);
 sq_status sq_quantize_grad_conv(const float* dY, int64_t N, int64_t H, int64_t W, int64_t C_out, int64_t ld_dY,
                                 int32_t KH, int32_t KW, int32_t PH, int32_t PW, const sq_quant_params* p,
                                 int8_t* q_fold, int64_t ld_fold, int8_t* q_tp, int64_t ld_tp,

@@ -817,6 +817,49 @@ sq_status sq_conv_pack_grad(const int8_t* q_t, int64_t ld_t, int64_t N, int64_t 
                       "conv pack gradient");
 }
 
+sq_status sq_quantize_input_conv(const float* X, int64_t N, int64_t H, int64_t W, int64_t C_in, int64_t ld_X,
+                                 int32_t KH, int32_t KW, int32_t PH, int32_t PW, int32_t bits, int8_t* xq,
+                                 int64_t ld_xq, int8_t* xs, int64_t ld_xs, sq_scale* scale, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+    SQ_TRY(check_conv_geom(N, H, W, 1, C_in, KH, KW, PH, PW));
+    if (bits < 2 || bits > 8) return fail(SQ_ERR_INVALID_ARGUMENT, "bits must be in [2, 8]");
+    const ConvGrid g = conv_grid(N, H, W, C_in, KH, KW, PH, PW);
+    const int64_t M = N * H * W;
+    SQ_TRY(check_dims(M, C_in, "X"));
+    if (g.Hp * g.Wp >= ((int64_t)1 << 32) || M >= ((int64_t)1 << 32))
+        return fail(SQ_ERR_UNSUPPORTED, "the padded grid exceeds 2^32 pixels");
+    if (C_in > 0) {
+        SQ_TRY(check_f32(X, ld_X, C_in, "X"));
+        SQ_TRY(check_codes(xs, ld_xs, g.ld_x, "xs"));
+        if (xq) SQ_TRY(check_codes(xq, ld_xq, C_in, "xq"));
+    }
+    if (!scale || !aligned(scale, 4)) return fail(SQ_ERR_INVALID_ARGUMENT, "scale is NULL or misaligned");
+    if (!workspace || !aligned(workspace, 16)) return fail(SQ_ERR_INVALID_ARGUMENT, "workspace is NULL or misaligned");
+    if (workspace_bytes < quant_ws_bytes(M, C_in)) return fail(SQ_ERR_WORKSPACE_TOO_SMALL, "workspace too small");
+
+    sq_quant_params p{};
+    p.bits = bits;
+    p.num_groups = 1;
+    p.round_mode = SQ_ROUND_NEAREST_EVEN;
+    const QuantCfg cfg = make_cfg(p);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    uint32_t* partial = static_cast<uint32_t*>(workspace);
+    int64_t slabs = 0;
+    SQ_TRY(hip_status(launch_colmax(X, M, C_in, ld_X, partial, &slabs, s), "colmax"));
+    SQ_TRY(hip_status(launch_finalize_tensor(partial, slabs, C_in, cfg.Q, partial + slabs * C_in, scale, s),
+                      "finalize"));
+    // input pixel (n, ih, iw) at grid column n Hp Wp + (ih + PH) Wp + iw + PW
+    PadGrid pg;
+    pg.Wo = (uint32_t)W;
+    pg.HoWo = (uint32_t)(H * W);
+    pg.Wp = (uint32_t)g.Wp;
+    pg.HpWp = (uint32_t)(g.Hp * g.Wp);
+    pg.off = (uint32_t)(PH * g.Wp + PW);
+    SQ_TRY(hip_status(launch_quantize(X, M, C_in, ld_X, nullptr, scale, cfg, xq, ld_xq, xs, ld_xs, nullptr, s, pg),
+                      "quantize"));
+    return SQ_OK;
+}
+
 // ranges == nullptr: the quantizer's own abs-max pass; else the channel
 // ranges as partial maxima [range_slabs, C_out] from the producer of dY
 static sq_status quantize_grad_conv_impl(const float* dY, int64_t N, int64_t H, int64_t W, int64_t C_out,

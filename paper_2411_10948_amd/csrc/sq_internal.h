@@ -95,8 +95,10 @@ hipError_t launch_finalize_tensor(const uint32_t* partial, int64_t slabs, int64_
 // Padded pixel grid of the transposed codes (conv wgrad): row m = (n, oh, ow)
 // of an Ho x Wo output grid goes to column n HpWp + oh Wp + ow; Wo = 0: plain
 // (column m).  Every value below 2^32.
+// Padded pixel grid of a transposed code matrix: pixel m = (n, oh, ow) of an
+// Ho x Wo image goes to column n HpWp + oh Wp + ow + off (Wo == 0: no grid).
 struct PadGrid {
-    uint32_t Wo = 0, HoWo = 0, Wp = 0, HpWp = 0;
+    uint32_t Wo = 0, HoWo = 0, Wp = 0, HpWp = 0, off = 0;
 };
 // group == nullptr: every channel in group 0 with shift 0 (per-tensor mode);
 // desc: the channel descriptors of the fold layout (nullptr: all main, t = 0).

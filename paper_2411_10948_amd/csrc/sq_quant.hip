@@ -925,18 +925,18 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
             // padded pixel grid: pixel m = (n, oh, ow) at n HpWp + oh Wp + ow;
             // 16 pixels in one image row as one 16-byte store, else two 8-byte
             // halves (which never cross an image row when Wo % 8 == 0)
-            const bool grid_fast = pg.Wo && pg.Wo % 8 == 0 && m + 16 <= M;
+            const bool grid_fast = pg.Wo && pg.Wo % 8 == 0 && (pg.off & 7) == 0 && m + 16 <= M;
             int64_t d0 = 0, d1 = 0;
             bool whole = false;
             if (grid_fast) {
                 const uint32_t m0 = (uint32_t)m;
                 const uint32_t n = m0 / pg.HoWo, rem = m0 - n * pg.HoWo, oh = rem / pg.Wo;
                 const uint32_t ow = rem - oh * pg.Wo;
-                d0 = (int64_t)n * pg.HpWp + (int64_t)oh * pg.Wp + ow;
+                d0 = (int64_t)n * pg.HpWp + (int64_t)oh * pg.Wp + ow + pg.off;
                 whole = ow + 16 <= pg.Wo && (d0 & 15) == 0;
                 const uint32_t mh = m0 + 8;
                 const uint32_t n1 = mh / pg.HoWo, rem1 = mh - n1 * pg.HoWo, oh1 = rem1 / pg.Wo;
-                d1 = (int64_t)n1 * pg.HpWp + (int64_t)oh1 * pg.Wp + (rem1 - oh1 * pg.Wo);
+                d1 = (int64_t)n1 * pg.HpWp + (int64_t)oh1 * pg.Wp + (rem1 - oh1 * pg.Wo) + pg.off;
             }
             // kept rolled: unrolled, the 64-channel tiles measured 1.5 us slower
 #pragma unroll 1
@@ -968,7 +968,8 @@ __global__ __launch_bounds__(kBlock) void k_quantize(const float* __restrict__ x
                         const uint32_t mi = (uint32_t)(m + i);
                         const uint32_t n = mi / pg.HoWo, rem = mi - n * pg.HoWo, oh = rem / pg.Wo;
                         const uint32_t ow = rem - oh * pg.Wo;
-                        row[(int64_t)n * pg.HpWp + (int64_t)oh * pg.Wp + ow] = (int8_t)(src[i / 4] >> (8 * (i % 4)));
+                        row[(int64_t)n * pg.HpWp + (int64_t)oh * pg.Wp + ow + pg.off] =
+                            (int8_t)(src[i / 4] >> (8 * (i % 4)));
                     }
                 } else if (m + 16 <= M) {
                     *reinterpret_cast<uint4*>(row + m) = make_uint4(src[0], src[1], src[2], src[3]);
@@ -1110,14 +1111,63 @@ __global__ __launch_bounds__(kBlock) void k_quantize8(const float* __restrict__ 
                 if (TL) {
                     *reinterpret_cast<uint4*>(q_t + tiled_off(c, mm, ld_t)) = a;
                     *reinterpret_cast<uint4*>(q_t + tiled_off(c, mm + 16, ld_t)) = b;
-                } else if (pg.Wo) {
-                    // padded pixel grid (Wo % 8 == 0): pixel m = (n, oh, ow) at
-                    // n HpWp + oh Wp + ow; the 4 groups of 8 pixels never cross an
-                    // image row, so each is one 8-byte store (16-byte stores of
-                    // aligned pairs, behind a branch, measured slower)
+                } else if (pg.Wo && (pg.off & 7) != 0) {
+                    // padded pixel grid at an offset that is not a multiple of 8
+                    // (a conv input: pixel (n, ih, iw) at n HpWp + (ih + PH) Wp +
+                    // iw + PW).  A group of 8 pixels then straddles two aligned
+                    // 8-byte words; each word that holds codes is written whole,
+                    // once, by the group whose last codes open it: its bytes
+                    // are that group's tail and the next group's head, or zeros
+                    // where the image row ends.  A row's first group also writes
+                    // the word before it (zeros, then its head).  The head of the
+                    // next tile's first group is quantized again here from x
+                    // (per-tensor codes, round to nearest: the same value).
+                    const int sa = 8 * (int)(pg.off & 7);
                     const uint32_t m0 = (uint32_t)mm;
                     uint32_t n = m0 / pg.HoWo, rem = m0 - n * pg.HoWo, oh = rem / pg.Wo, ow = rem - oh * pg.Wo;
                     int8_t* row = q_t + c * ld_t;
+                    auto word = [&](int w) {   // codes of 8 pixels: tile word pair w of this channel row
+                        return (uint64_t)tq[ch * TW + 2 * w] | ((uint64_t)tq[ch * TW + 2 * w + 1] << 32);
+                    };
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        if (mm + 8 * g < M) {
+                            const uint64_t cur = word(4 * part + g);
+                            uint64_t nxt = 0;
+                            if (ow + 8 < pg.Wo) {
+                                if (part < 3 || g < 3) {
+                                    nxt = word(4 * part + g + 1);
+                                } else if (!zero) {
+                                    const int64_t mn = mm + 8 * g + 8;
+                                    const float sn = __fmul_rn(sc.inv, pow2f(0));
+#pragma unroll
+                                    for (int k = 0; k < 8; ++k)
+                                        nxt |= (uint64_t)(uint8_t)quant_one<false>(x[(mn + k) * ld + c], sn, Qf, 0u)
+                                               << (8 * k);
+                                }
+                            }
+                            const int64_t d = (int64_t)n * pg.HpWp + (int64_t)oh * pg.Wp + ow + pg.off - sa / 8;
+                            if (ow == 0) *reinterpret_cast<uint64_t*>(row + d) = cur << sa;
+                            *reinterpret_cast<uint64_t*>(row + d + 8) = (cur >> (64 - sa)) | (nxt << sa);
+                        }
+                        ow += 8;
+                        if (ow == pg.Wo) {
+                            ow = 0;
+                            if (++oh * pg.Wo == pg.HoWo) {
+                                oh = 0;
+                                ++n;
+                            }
+                        }
+                    }
+                } else if (pg.Wo) {
+                    // padded pixel grid (Wo % 8 == 0, offset a multiple of 8):
+                    // pixel m = (n, oh, ow) at n HpWp + oh Wp + ow + off; the 4
+                    // groups of 8 pixels never cross an image row, so each is one
+                    // 8-byte store (16-byte stores of aligned pairs, behind a
+                    // branch, measured slower)
+                    const uint32_t m0 = (uint32_t)mm;
+                    uint32_t n = m0 / pg.HoWo, rem = m0 - n * pg.HoWo, oh = rem / pg.Wo, ow = rem - oh * pg.Wo;
+                    int8_t* row = q_t + c * ld_t + pg.off;
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
                         if (mm + 8 * g < M)
@@ -1298,7 +1348,12 @@ hipError_t launch_quantize(const float* x, int64_t M, int64_t C, int64_t ld, con
     if (n_tiles(tc, tr) < kQuantMinTiles) tr = 64;
     if (n_tiles(tc, tr) < kQuantMinTiles) tc = 64;
     const int64_t eb = fold_ext_base(C);
-    if (vec && C % 8 == 0 && (!pg.Wo || (pg.Wo % 8 == 0 && !tiled))) {
+    // a grid offset that is not a multiple of 8 takes the 8-channel kernel
+    // only for per-tensor round-to-nearest codes (it quantizes a few codes of
+    // the next tile again), else the byte stores of k_quantize
+    const bool grid8 = !pg.Wo || (pg.Wo % 8 == 0 && !tiled &&
+                                  ((pg.off & 7) == 0 || (!sr && !group && !desc)));
+    if (vec && C % 8 == 0 && grid8) {
         // 8-channel form: one Philox block per thread and row; the groups
         // (8 bytes) and descriptors (2 x 16 bytes) of a thread's channels
         // load as vectors when aligned

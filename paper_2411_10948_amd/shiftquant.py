@@ -44,7 +44,8 @@ EXPORTS = (
     "sq_gemm_dgrad_grouped", "sq_quantize_channels", "sq_gemm_forward",
     "sq_quantize_grad_from_ranges", "sq_l1bn_range_slabs", "sq_l1bn_forward_workspace_size",
     "sq_l1bn_backward_workspace_size", "sq_l1bn_forward", "sq_l1bn_backward",
-    "sq_conv_wgrad_layout", "sq_conv_pack_input", "sq_conv_pack_grad", "sq_quantize_grad_conv",
+    "sq_conv_wgrad_layout", "sq_conv_pack_input", "sq_conv_pack_grad", "sq_quantize_input_conv",
+    "sq_quantize_grad_conv",
     "sq_conv_wgrad_workspace_size", "sq_conv_wgrad", "sq_gemm_dgrad_range_slabs", "sq_gemm_dgrad_ranged",
     "sq_quantize_grad_noalloc", "sq_conv_dgrad_ranged", "sq_quantize_grad_conv_from_ranges",
     "sq_status_string", "sq_last_error", "sq_last_error_string",
@@ -152,6 +153,8 @@ def load() -> ct.CDLL:
                                   ct.c_int32, pp, _P, _I64, _P, _I64, _P, _P, _P, _P, _SZ, _P],
         "sq_conv_pack_input": [_P, _I64, _I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32, ct.c_int32,
                                _P, _I64, _P],
+        "sq_quantize_input_conv": [_P, _I64, _I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32, ct.c_int32,
+                                   ct.c_int32, _P, _I64, _P, _I64, _P, _P, _SZ, _P],
         "sq_conv_wgrad_workspace_size": [_I64, _I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32, ct.c_int32,
                                          ct.c_int32, pp, ct.POINTER(_SZ)],
         "sq_conv_wgrad": [_P, _I64, _P, _P, _P, _I64, _P, _I64, _I64, _I64, _I64, _I64, ct.c_int32, ct.c_int32,
@@ -332,6 +335,14 @@ def sq_quantize_grad_conv(dY, N, H, W, KH, KW, PH, PW, params, q_fold, q_tp, gro
 def sq_conv_pack_input(xq_t, N, H, W, C_in, KH, KW, PH, PW, xs, stream=None) -> None:
     _check("sq_conv_pack_input", load().sq_conv_pack_input(_ptr(xq_t), _ld(xq_t), N, H, W, C_in, KH, KW, PH, PW,
                                                            _ptr(xs), _ld(xs), _stream(stream)))
+
+
+def sq_quantize_input_conv(X, N, H, W, KH, KW, PH, PW, bits, xq, xs, scale, workspace, stream=None) -> None:
+    C = X.shape[1]
+    ws, nws = _ws_ptr(workspace)
+    _check("sq_quantize_input_conv", load().sq_quantize_input_conv(
+        _ptr(X), N, H, W, C, _ld(X), KH, KW, PH, PW, bits, _ptr(xq), _ld(xq) if xq is not None else 0, _ptr(xs),
+        _ld(xs), _ptr(scale), ws, nws, _stream(stream)))
 
 
 def sq_conv_wgrad_workspace_size(N, H, W, C_out, C_in, KH, KW, PH, PW, params: Params) -> int:
@@ -725,6 +736,23 @@ def conv_pack_input(xq_t: torch.Tensor, N: int, H: int, W: int, KH: int, KW: int
     return xs
 
 
+def quantize_input_conv(X: torch.Tensor, N: int, H: int, W: int, KH: int, KW: int, PH: int, PW: int,
+                        bits: int = 8, want_rows: bool = False, stream=None):
+    """Per-tensor codes of the conv input X [N*H*W, C_in] on the padded grid of
+    sq_conv_wgrad (a zero-filled buffer: the padding is never written), and,
+    with want_rows, row-major as well: (xs, xq or None, scale)."""
+    C_in = X.shape[1]
+    dev = X.device
+    rows, ld, _ = sq_conv_wgrad_layout(N, H, W, C_in, KH, KW, PH, PW)
+    xs = torch.zeros((max(rows, 1), ld), dtype=torch.int8, device=dev)[:rows]
+    xq = torch.empty((N * H * W, round_up(max(C_in, 1), 16)), dtype=torch.int8, device=dev)[:, :C_in] \
+        if want_rows else None
+    scale = new_scale(dev)
+    ws = _workspace(sq_quantize_tensor_workspace_size(N * H * W, C_in), dev)
+    sq_quantize_input_conv(X, N, H, W, KH, KW, PH, PW, bits, xq, xs, scale, ws, stream)
+    return xs, xq, scale
+
+
 def conv_pack_grad(codes: "GradCodes", N: int, H: int, W: int, KH: int, KW: int, PH: int, PW: int,
                    stream=None) -> torch.Tensor:
     """The transposed gradient codes of `codes` on the padded pixel grid."""
@@ -843,9 +871,13 @@ class ConvBackwardPlan(BackwardPlan):
             # the quantizer never writes the padding of the grid: zero it once
             self.q_tp = torch.zeros((C_out, qld), dtype=torch.int8, device=dev)
             self.q_t = None
-            # the input codes on the grid (written whole by pack_input)
+            # the input codes on the grid (written whole by pack_input; the
+            # input quantizer writes the pixels only, so the padding is zeroed
+            # once)
             xrows, xld, _ = sq_conv_wgrad_layout(N, H, W, C_in_ch, KH, KW, PH, PW)
-            self.x_grid = torch.empty((max(xrows, 1), xld), dtype=torch.int8, device=dev)[:xrows]
+            self.x_grid = torch.zeros((max(xrows, 1), xld), dtype=torch.int8, device=dev)[:xrows]
+            self.x_scale = new_scale(dev)
+            self.ws_x = _workspace(sq_quantize_tensor_workspace_size(N * H * W, C_in_ch), dev)
         self.ws_d = _workspace(sq_conv_dgrad_workspace_size(C_out, C_in_ch, KH, KW, params), dev)
         self.dX = torch.empty((N * H * W, C_in_ch), dtype=torch.float32, device=dev)
         self.acc_dX = torch.empty((N * H * W, C_in_ch), dtype=torch.int32, device=dev) if want_acc else None
@@ -882,6 +914,13 @@ class ConvBackwardPlan(BackwardPlan):
         """The input codes xq_t [C_in, >= N*H*W] onto the plan's padded grid."""
         N, H, W, KH, KW, PH, PW = self.geom
         sq_conv_pack_input(xq_t, N, H, W, self.C_in_ch, KH, KW, PH, PW, self.x_grid, stream)
+
+    def quantize_input(self, X, stream=None):
+        """The forward pass's input quantizer: per-tensor 8-bit codes of X
+        [N*H*W, C_in] straight onto the plan's grid (x_grid, x_scale), so the
+        step runs without pack_input."""
+        N, H, W, KH, KW, PH, PW = self.geom
+        sq_quantize_input_conv(X, N, H, W, KH, KW, PH, PW, 8, None, self.x_grid, self.x_scale, self.ws_x, stream)
 
     def run_packed(self, dY, wq_t, wscale, xq_t, xscale, stream=None):
         """The step from unpacked input codes: pack_input, then run."""
