@@ -175,12 +175,9 @@ sq_status quantize_grad_impl(const float* dY, int64_t M, int64_t C_out, int64_t 
     const QuantCfg cfg = make_cfg(*p);
     hipStream_t s = static_cast<hipStream_t>(stream);
     uint32_t* partial = static_cast<uint32_t*>(workspace);
-    int64_t slabs = 0;
-    SQ_TRY(hip_status(launch_colmax(dY, M, C_out, ld_dY, partial, &slabs, s), "colmax"));
-    uint32_t* rbits = partial + slabs * C_out;
     const int64_t ext_max = fold_ext_max(C_out, cfg);
-    SQ_TRY(hip_status(launch_finalize_grad(partial, slabs, C_out, cfg, rbits, group, scale, layout, ext_max, s),
-                      "finalize"));
+    SQ_TRY(hip_status(launch_colmax_finalize_grad(dY, M, C_out, ld_dY, cfg, partial, group, scale, layout, ext_max, s),
+                      "abs-max and finalize"));
     SQ_TRY(hip_status(launch_quantize(dY, M, C_out, ld_dY, group, scale, cfg, q_fold, ld_fold, q_t, ld_t,
                                       layout + kLayoutHeader + ext_max, s, PadGrid(), tiled_of(p)),
                       "quantize"));
@@ -900,11 +897,9 @@ static sq_status quantize_grad_conv_impl(const float* dY, int64_t N, int64_t H, 
                                                    ext_max, s),
                               "finalize"));
     } else {
-        int64_t slabs = 0;
-        SQ_TRY(hip_status(launch_colmax(dY, M, C_out, ld_dY, partial, &slabs, s), "colmax"));
-        SQ_TRY(hip_status(launch_finalize_grad(partial, slabs, C_out, cfg, partial + slabs * C_out, group, scale,
-                                               layout, ext_max, s),
-                          "finalize"));
+        SQ_TRY(hip_status(launch_colmax_finalize_grad(dY, M, C_out, ld_dY, cfg, partial, group, scale, layout,
+                                                      ext_max, s),
+                          "abs-max and finalize"));
     }
     PadGrid pg;
     pg.Wo = (uint32_t)g.Wo;

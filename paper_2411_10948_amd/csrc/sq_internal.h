@@ -83,13 +83,20 @@ struct ColmaxPlan {
 };
 ColmaxPlan colmax_plan(int64_t M, int64_t C, bool vec);
 // uint32 words of scratch: slab maxima, then the channel ranges and the
-// per-block maxima of the second reduction level (rbits = partial + slabs * C)
+// per-block maxima of the second reduction level (rbits = partial + slabs * C),
+// the second level's shift counts and the abs-max blocks' maxima
 int64_t colmax_workspace_words(int64_t M, int64_t C);
+// block_max (optional): the maximum of each abs-max block, *n_block_max of them
 hipError_t launch_colmax(const float* x, int64_t M, int64_t C, int64_t ld, uint32_t* partial, int64_t* slabs,
-                         hipStream_t s);
+                         hipStream_t s, uint32_t* block_max = nullptr, int64_t* n_block_max = nullptr);
 hipError_t launch_finalize_grad(const uint32_t* partial, int64_t slabs, int64_t C, const QuantCfg& cfg,
                                 uint32_t* rbits, uint8_t* group, sq_scale* scale, int32_t* layout,
                                 int64_t ext_max, hipStream_t s);
+// abs-max pass + finalize of the gradient quantizer over the scratch ws
+// (colmax_workspace_words(M, C) words)
+hipError_t launch_colmax_finalize_grad(const float* x, int64_t M, int64_t C, int64_t ld, const QuantCfg& cfg,
+                                       uint32_t* ws, uint8_t* group, sq_scale* scale, int32_t* layout,
+                                       int64_t ext_max, hipStream_t s);
 hipError_t launch_finalize_tensor(const uint32_t* partial, int64_t slabs, int64_t C, int Q, uint32_t* rbits,
                                   sq_scale* scale, hipStream_t s);
 // Padded pixel grid of the transposed codes (conv wgrad): row m = (n, oh, ow)

@@ -110,7 +110,8 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 template <int VEC, bool NT>
 __global__ __launch_bounds__(kColThreads) void k_colmax(const float* __restrict__ x, int64_t M, int64_t C,
                                                         int64_t ld, int tpr, int64_t rows_per_slab,
-                                                        uint32_t* __restrict__ partial) {
+                                                        uint32_t* __restrict__ partial,
+                                                        uint32_t* __restrict__ block_max) {
     __shared__ uint32_t red[kColThreads * VEC];
     const int tid = threadIdx.x;
     const int nrl = kColThreads / tpr;
@@ -182,6 +183,18 @@ __global__ __launch_bounds__(kColThreads) void k_colmax(const float* __restrict_
 #pragma unroll
         for (int j = 0; j < VEC; ++j)
             if (c0 + j < C) dst[j] = best[j];
+    }
+    // the block's maximum over its channels (the rl == 0 threads, tid < tpr,
+    // all in wave 0), so that r_max needs no pass over the channel ranges
+    if (block_max && tid < 64) {
+        uint32_t mb = 0u;
+        if (rl == 0 && c0 < C)
+#pragma unroll
+            for (int j = 0; j < VEC; ++j)
+                if (c0 + j < C) mb = max(mb, best[j]);
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) mb = max(mb, (uint32_t)__shfl_xor((int)mb, o, 64));
+        if (tid == 0) block_max[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = mb;
     }
 }
 
@@ -626,31 +639,25 @@ __global__ __launch_bounds__(kFinThreads) void k_finalize_grad(const uint32_t* _
 //     of the blocks before it, and ranks its appended channels with wave
 //     ballots; block 0 writes the header and the region padding.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kRedThreads) void k_final_groups(const uint32_t* __restrict__ rbits,
-                                                               const uint32_t* __restrict__ bmax, int64_t nb,
-                                                               int64_t C, QuantCfg cfg, uint8_t* __restrict__ group,
-                                                               sq_scale* __restrict__ scale, int32_t* __restrict__ layout,
-                                                               int64_t ext_max, int32_t* __restrict__ hist) {
-    __shared__ uint32_t shu[kRedThreads / 64];
-    __shared__ int cnt[kMaxRegions];
+// Groups of the block's channels (thread t < kRedThreads: channel
+// blockIdx.x * kRedThreads + t with range bits rb; the other threads pass
+// nothing), the descriptors and header with one fold window, else the
+// block's count of channels per shift.  Every thread of the block calls it.
+__device__ void final_groups_body(int64_t c, uint32_t rb, const sq_scale& sc, int64_t C, const QuantCfg& cfg,
+                                  uint8_t* __restrict__ group, int32_t* __restrict__ layout, int64_t ext_max,
+                                  int32_t* __restrict__ hist, int* cnt) {
     const int tid = threadIdx.x;
-    uint32_t mb = 0u;
-    for (int64_t i = tid; i < nb; i += kRedThreads) mb = max(mb, bmax[i]);
-    mb = block_max_u32(mb, shu);
-    const sq_scale sc = make_scale(mb, (float)cfg.Q);
-    if (blockIdx.x == 0 && tid == 0) *scale = sc;
     const int Sh = cfg.num_groups - 1;
-    const int64_t c = (int64_t)blockIdx.x * kRedThreads + tid;
     int sh = -1;
-    if (c < C) {
-        const int g = sc.flags ? Sh : group_of(__uint_as_float(rbits[c]), sc.r_max, cfg.num_groups);
+    if (tid < kRedThreads && c < C) {
+        const int g = sc.flags ? Sh : group_of(__uint_as_float(rb), sc.r_max, cfg.num_groups);
         group[c] = (uint8_t)g;
         sh = Sh - g;
     }
     if (ext_max == 0) {
         // one window at base 0: the code of channel c is stored as code << sh_c in its own column
         int32_t* desc = layout + kLayoutHeader;
-        if (c < C) desc[c] = sh;
+        if (tid < kRedThreads && c < C) desc[c] = sh;
         if (blockIdx.x == 0 && tid < kLayoutHeader) {
             int v = 0;
             if (tid == kLayNR) v = 1;
@@ -669,6 +676,60 @@ __global__ __launch_bounds__(kRedThreads) void k_final_groups(const uint32_t* __
     }
     __syncthreads();
     if (tid < kMaxRegions) hist[blockIdx.x * kMaxRegions + tid] = cnt[tid];
+}
+
+__global__ __launch_bounds__(kRedThreads) void k_final_groups(const uint32_t* __restrict__ rbits,
+                                                               const uint32_t* __restrict__ bmax, int64_t nb,
+                                                               int64_t C, QuantCfg cfg, uint8_t* __restrict__ group,
+                                                               sq_scale* __restrict__ scale, int32_t* __restrict__ layout,
+                                                               int64_t ext_max, int32_t* __restrict__ hist) {
+    __shared__ uint32_t shu[kRedThreads / 64];
+    __shared__ int cnt[kMaxRegions];
+    const int tid = threadIdx.x;
+    uint32_t mb = 0u;
+    for (int64_t i = tid; i < nb; i += kRedThreads) mb = max(mb, bmax[i]);
+    mb = block_max_u32(mb, shu);
+    const sq_scale sc = make_scale(mb, (float)cfg.Q);
+    if (blockIdx.x == 0 && tid == 0) *scale = sc;
+    const int64_t c = (int64_t)blockIdx.x * kRedThreads + tid;
+    final_groups_body(c, c < C ? rbits[c] : 0u, sc, C, cfg, group, layout, ext_max, hist, cnt);
+}
+
+// The same from the abs-max pass's outputs directly: r_max from its block
+// maxima, and each channel's range from its slab maxima (kRedLanes threads
+// per channel, as k_colmax_reduce), one launch fewer.
+__global__ __launch_bounds__(kRedThreads * kRedLanes) void k_final_groups_slabs(
+    const uint32_t* __restrict__ partial, int64_t S, const uint32_t* __restrict__ block_max, int64_t nbm, int64_t C,
+    QuantCfg cfg, uint8_t* __restrict__ group, sq_scale* __restrict__ scale, int32_t* __restrict__ layout,
+    int64_t ext_max, int32_t* __restrict__ hist) {
+    __shared__ uint32_t lanes[kRedLanes][kRedThreads];
+    __shared__ uint32_t shu[kRedThreads * kRedLanes / 64];
+    __shared__ int cnt[kMaxRegions];
+    const int tid = threadIdx.x;
+    const int ch = tid % kRedThreads, ln = tid / kRedThreads;
+    const int64_t c = (int64_t)blockIdx.x * kRedThreads + ch;
+    uint32_t a[4] = {0u, 0u, 0u, 0u};
+    if (c < C) {
+        int64_t s = ln;
+        for (; s + 3 * kRedLanes < S; s += 4 * kRedLanes) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) a[u] = max(a[u], partial[(s + u * kRedLanes) * C + c]);
+        }
+        for (; s < S; s += kRedLanes) a[0] = max(a[0], partial[s * C + c]);
+    }
+    uint32_t mb = 0u;
+    for (int64_t i = tid; i < nbm; i += kRedThreads * kRedLanes) mb = max(mb, block_max[i]);
+    mb = block_max_u32(mb, shu);
+    lanes[ln][ch] = max(max(a[0], a[1]), max(a[2], a[3]));
+    __syncthreads();
+    uint32_t rb = 0u;
+    if (ln == 0) {
+#pragma unroll
+        for (int l = 0; l < kRedLanes; ++l) rb = max(rb, lanes[l][ch]);
+    }
+    const sq_scale sc = make_scale(mb, (float)cfg.Q);
+    if (blockIdx.x == 0 && tid == 0) *scale = sc;
+    final_groups_body(c, rb, sc, C, cfg, group, layout, ext_max, hist, cnt);
 }
 
 __global__ __launch_bounds__(kRedThreads) void k_final_place(const uint8_t* __restrict__ group,
@@ -1278,18 +1339,25 @@ ColmaxPlan colmax_plan(int64_t M, int64_t C, bool vec) {
 int64_t colmax_reduce_blocks(int64_t C) { return C >= kFinThreads ? (C + kRedThreads - 1) / kRedThreads : 0; }
 
 int64_t colmax_workspace_words(int64_t M, int64_t C) {
-    // worst case over both vector widths: slab maxima + channel ranges + block maxima
-    const ColmaxPlan a = colmax_plan(M, C, true), b = colmax_plan(M, C, false);
-    return std::max(a.slabs, b.slabs) * C + C + (1 + kMaxRegions) * colmax_reduce_blocks(C);
+    // worst case over both vector widths: slab maxima, channel ranges, the
+    // second level's block maxima and shift counts, the abs-max blocks' maxima
+    int64_t w = 0;
+    for (const bool vec : {true, false}) {
+        const ColmaxPlan p = colmax_plan(M, C, vec);
+        w = std::max(w, p.slabs * C + C + (1 + kMaxRegions) * colmax_reduce_blocks(C) + p.chunks * p.slabs);
+    }
+    return w;
 }
 
 hipError_t launch_colmax(const float* x, int64_t M, int64_t C, int64_t ld, uint32_t* partial, int64_t* slabs,
-                         hipStream_t s) {
+                         hipStream_t s, uint32_t* block_max, int64_t* n_block_max) {
     *slabs = 0;
+    if (n_block_max) *n_block_max = 0;
     if (M <= 0 || C <= 0) return hipSuccess;
     const bool vec = ((ld & 3) == 0) && ((reinterpret_cast<uintptr_t>(x) & 15) == 0);
     const ColmaxPlan p = colmax_plan(M, C, vec);
     *slabs = p.slabs;
+    if (n_block_max) *n_block_max = p.chunks * p.slabs;
     dim3 grid((unsigned)p.chunks, (unsigned)p.slabs);
     // A tensor larger than the 256 MB last-level cache cannot stay there for
     // the quantize pass's second read; streaming it through without
@@ -1300,13 +1368,13 @@ hipError_t launch_colmax(const float* x, int64_t M, int64_t C, int64_t ld, uint3
     const bool nt = (uint64_t)M * (uint64_t)ld * sizeof(float) > kLastLevelCacheBytes;
     if (vec && nt)
         hipLaunchKernelGGL((k_colmax<4, true>), grid, dim3(kColThreads), 0, s, x, M, C, ld, p.tpr, p.rows_per_slab,
-                           partial);
+                           partial, block_max);
     else if (vec)
         hipLaunchKernelGGL((k_colmax<4, false>), grid, dim3(kColThreads), 0, s, x, M, C, ld, p.tpr, p.rows_per_slab,
-                           partial);
+                           partial, block_max);
     else
         hipLaunchKernelGGL((k_colmax<1, false>), grid, dim3(kColThreads), 0, s, x, M, C, ld, p.tpr, p.rows_per_slab,
-                           partial);
+                           partial, block_max);
     return hipGetLastError();
 }
 
@@ -1338,6 +1406,34 @@ hipError_t launch_finalize_grad(const uint32_t* partial, int64_t slabs, int64_t 
     }
     hipLaunchKernelGGL(k_finalize_grad, dim3(1), dim3(kFinThreads), 0, s, partial, slabs, C, cfg, rbits, bmax, nb, group,
                        scale, layout, ext_max);
+    return hipGetLastError();
+}
+
+hipError_t launch_colmax_finalize_grad(const float* x, int64_t M, int64_t C, int64_t ld, const QuantCfg& cfg,
+                                       uint32_t* ws, uint8_t* group, sq_scale* scale, int32_t* layout,
+                                       int64_t ext_max, hipStream_t s) {
+    const int64_t nb = colmax_reduce_blocks(C);
+    if (nb == 0 || M <= 0) {
+        int64_t slabs = 0;
+        hipError_t e = launch_colmax(x, M, C, ld, ws, &slabs, s);
+        if (e != hipSuccess) return e;
+        return launch_finalize_grad(ws, slabs, C, cfg, ws + slabs * C, group, scale, layout, ext_max, s);
+    }
+    // many channels: the abs-max pass also leaves its blocks' maxima, and the
+    // group kernel reduces the slab maxima itself (no k_colmax_reduce)
+    const ColmaxPlan p = colmax_plan(M, C, ((ld & 3) == 0) && ((reinterpret_cast<uintptr_t>(x) & 15) == 0));
+    uint32_t* rbits = ws + p.slabs * C;
+    int32_t* hist = reinterpret_cast<int32_t*>(rbits + C + nb);
+    uint32_t* bm = rbits + C + (1 + kMaxRegions) * nb;
+    int64_t slabs = 0, nbm = 0;
+    hipError_t e = launch_colmax(x, M, C, ld, ws, &slabs, s, bm, &nbm);
+    if (e != hipSuccess) return e;
+    if (slabs != p.slabs) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_final_groups_slabs, dim3((unsigned)nb), dim3(kRedThreads * kRedLanes), 0, s, ws, slabs, bm,
+                       nbm, C, cfg, group, scale, layout, ext_max, hist);
+    if (ext_max > 0)
+        hipLaunchKernelGGL(k_final_place, dim3((unsigned)nb), dim3(kRedThreads), 0, s, group, hist, nb, C, cfg,
+                           layout, ext_max);
     return hipGetLastError();
 }
 
