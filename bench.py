@@ -34,11 +34,25 @@ KERNEL_SOURCES = ["paper_2411_10948_amd/csrc/sq_gemm.hip", "paper_2411_10948_amd
                   "paper_2411_10948_amd/build.py"]   # the compiler flags shape the kernels too
 
 
-def kernel_source_hash() -> str:
+def _code_only(text: str) -> str:
+    """C++ source without comments and blank lines (comments do not change the kernels)."""
+    import re
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    lines = (re.sub(r"//.*$", "", line).rstrip() for line in text.splitlines())
+    return "\n".join(line for line in lines if line)
+
+
+def kernel_source_hash(read=None) -> str:
+    """Hash of the kernel sources' code and of the build script (its flags
+    shape the kernels too); read(rel) -> text overrides reading the files."""
     h = hashlib.sha256()
     for rel in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+        if read is None:
+            with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
+                text = f.read()
+        else:
+            text = read(rel)
+        h.update((text if rel.endswith(".py") else _code_only(text)).encode())
     return h.hexdigest()[:16]
 
 

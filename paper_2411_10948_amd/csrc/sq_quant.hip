@@ -4,11 +4,15 @@
 // read twice):
 //   k_colmax         per-channel abs-max r_c (Sec. 3.1) as unsigned bit
 //                    patterns: coalesced float4 row loads, one maximum per
-//                    channel per row slab (plain stores, no atomics)
-//   k_colmax_reduce  (many channels only) combines the slabs per channel and
-//                    leaves one maximum per block
-//   k_finalize       one block: r_max, group ids (power-of-two thresholds,
-//                    Sec. 3.1), scales, flags, and the fold layout for dgrad
+//                    channel per row slab (plain stores, no atomics) and one
+//                    per block
+//   finalize         r_max, group ids (power-of-two thresholds, Sec. 3.1),
+//                    scales, flags, and the fold layout for dgrad: one block
+//                    (k_finalize_grad) for few channels, else the group kernel
+//                    (k_final_groups_slabs, which also combines the slabs per
+//                    channel) and the placement kernel (k_final_place);
+//                    k_colmax_reduce + k_final_groups serve channel ranges
+//                    that come from the producer of dY
 //   k_quantize       scale, round (ties-to-even or Philox stochastic rounding,
 //                    App. B Eq. "sq"), clamp; writes the shift-folded dgrad
 //                    operand row-major and the codes transposed
