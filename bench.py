@@ -209,8 +209,7 @@ def run_forward(args, torch, sq, wl, inputs):
            "config": {"workload": args.workload, "step": "forward", "M": M, "C_in": C_in, "C_out": C_out,
                       "bits": wl.bits, "num_groups": wl.num_groups, "rounding": "nearest-even",
                       "weights": "8-bit per output channel", "parallelism": "none"},
-           "breakdown_ms": {k: v["ms"] for k, v in parts.items()},
-        **({"forward_ms": forward_ms} if forward_ms else {}), "roofline": roof}
+           "breakdown_ms": {k: v["ms"] for k, v in parts.items()}, "roofline": roof}
     if not args.no_cpu_baseline:
         import numpy as np
         import oracle
@@ -313,8 +312,7 @@ def run_l1bn(args, torch, sq):
            "config": {"workload": name, "step": "l1bn", "M": M, "C": C, "input_bits": 8, "grad_bits": bits,
                       "num_groups": ng, "rounding": "stochastic" if mode else "nearest-even", "parallelism": "none"},
            "pct_hbm_peak": 100.0 * value / PEAK_HBM_GBS,
-           "breakdown_ms": {k: v["ms"] for k, v in parts.items()},
-        **({"forward_ms": forward_ms} if forward_ms else {}), "roofline": roof}
+           "breakdown_ms": {k: v["ms"] for k, v in parts.items()}, "roofline": roof}
     if not args.no_cpu_baseline:
         import oracle
         rows = min(M, 1 << 18)
