@@ -75,6 +75,22 @@ def test_quantize_input_conv_parity(sq, case):
     assert torch.equal(xs, sq.conv_pack_input(xq_t, N, H, W, KH, KW, PH, PW))
 
 
+@pytest.mark.parametrize("ld_pad,misalign", [(8, 0), (3, 1)])
+def test_quantize_input_conv_strided_input(sq, ld_pad, misalign):
+    # X with a padded leading dimension (16-byte rows: the 8-channel kernel),
+    # and with an odd one at a 4-byte offset (the generic kernel's byte stores)
+    import torch
+    N, H, W, C_in, KH, KW, PH, PW = 2, 5, 24, 16, 3, 3, 1, 1
+    print(f"conv input quantizer, ld pad {ld_pad}, offset {misalign}", flush=True)
+    X = _input(N, H, W, C_in, 40 + ld_pad)
+    xs, xq, s = sq.quantize_input_conv(_dev(X, ld_pad, misalign), N, H, W, KH, KW, PH, PW, 8, want_rows=True)
+    torch.cuda.synchronize()
+    q_ref, _ = oracle.quantize_tensor(X, 8)
+    _, ld, _ = sq.sq_conv_wgrad_layout(N, H, W, C_in, KH, KW, PH, PW)
+    np.testing.assert_array_equal(xs.cpu().numpy(), _grid(q_ref, N, H, W, C_in, KH, PH, PW, ld))
+    np.testing.assert_array_equal(xq.cpu().numpy(), q_ref)
+
+
 def test_quantize_input_conv_zero_tensor(sq):
     # an all-zero input: zero codes, the scale's zero flag, the grid untouched
     import torch
