@@ -566,6 +566,8 @@ def main(argv=None):
                     help="code matrices of the linear layers: tile-major (default) or row-major")
     ap.add_argument("--dgrad", choices=["shiftmm", "grouped"], default="shiftmm",
                     help="grouped: the GEMM-based comparison implementation of the dgrad (Sec. 3.2)")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the step captured as a HIP graph and replayed (reported under 'graph')")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 256 MiB device-to-device copy first (reference for HBM byte counters)")
     args = ap.parse_args(argv)
@@ -676,6 +678,34 @@ def main(argv=None):
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(stop) / K
 
+    graph = None
+    if args.graph:
+        # the same step captured once as a HIP graph (the library allocates,
+        # clears and synchronizes nothing, so a step is capturable) and
+        # replayed K times between two events: the same kernels, launched by
+        # the runtime as one graph instead of one call at a time
+        cs = torch.cuda.Stream()
+        cs.wait_stream(stream)
+        with torch.cuda.stream(cs):
+            run(dY, wq_t, ws, xq_t, xs, cs)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cs):
+            run(dY, wq_t, ws, xq_t, xs, cs)
+        torch.cuda.synchronize()
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        start.record(stream)
+        for _ in range(K):
+            g.replay()
+        stop.record(stream)
+        torch.cuda.synchronize()
+        ms_graph = start.elapsed_time(stop) / K
+        graph = {"ms_per_step": ms_graph, "value": 4 * M * C_out * C_in / (ms_graph * 1e-3) / 1e12,
+                 "mode": "one step captured as a HIP graph, replayed K times between two events"}
+        del g
+
     # Per-call averages: each call launched K times back to back between two
     # events on the same stream (the kernels of the dominant call are what the
     # roofline entry reports).
@@ -764,6 +794,7 @@ def main(argv=None):
         "pct_int8_peak": 100.0 * value / PEAK_INT8_TOPS,
         "breakdown_ms": {k: v["ms"] for k, v in parts.items()},
         **({"forward_ms": forward_ms} if forward_ms else {}),
+        **({"graph": graph} if graph else {}),
         "roofline": roof,
         "per_step": summarize_steps(per_step, ops),
     }
