@@ -1738,10 +1738,14 @@ __global__ __launch_bounds__((64 * CwCfg<FM, KWC, RBC>::WAVES)) void k_conv_wgra
     using MF = Mfma<16>;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    // the tiles of one K split get block ids 8 apart: same XCD, shared L2
-    const int64_t nt = pl.tiles, L = blockIdx.x, G = L / (8 * nt), rem = L - G * 8 * nt;
-    const int64_t Sg = min((int64_t)8, (int64_t)pl.splits - 8 * G);
-    const int64_t bt = rem / Sg, split = 8 * G + rem % Sg;
+    // (split, tile) items split-major, XCD x (blocks L = x mod 8) taking the
+    // contiguous run after those of XCDs 0 .. x-1, as in k_gemm_pipe: the
+    // tiles of a K split share its L2 whatever the number of splits
+    const int64_t nt = pl.tiles, total = nt * pl.splits, L = blockIdx.x;
+    const int64_t xcd = L & 7, jj = L >> 3;
+    int64_t start = 0;
+    for (int64_t y = 0; y < xcd; ++y) start += (total - y + 7) >> 3;
+    const int64_t item = start + jj, split = item / nt, bt = item - split * nt;
     const int tg = (int)(bt % pl.tap_groups);
     const int64_t rest = bt / pl.tap_groups;
     const int64_t ci0 = (rest % pl.tiles_ci) * 16, co0 = (rest / pl.tiles_ci) * (16 * FM);
