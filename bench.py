@@ -500,39 +500,55 @@ def run_conv_chain(args, torch, sq):
 
 
 def run_vendor_gemm(args, torch, wl, M):
-    """The vendor library's int8 GEMM (torch._int_mm, int32 output) on the
-    layer's two backward product shapes, for comparison with the ShiftQuant
-    GEMMs: dX = dY W as [M, C_out] x [C_out, C_in] and dW = dY^T X as
-    [C_out, M] x [M, C_in], second operand column-major (its faster layout).
-    Warm, back-to-back launches; random codes in [-31, 31]."""
+    """The vendor library's GEMMs on the layer's two backward product shapes,
+    for comparison with the ShiftQuant GEMMs: dX = dY W as [M, C_out] x
+    [C_out, C_in] and dW = dY^T X as [C_out, M] x [M, C_in], second operand
+    column-major (its faster layout), in int8 (torch._int_mm, int32 output)
+    and, as the paper's floating-point comparison point, in fp16 and bf16
+    (torch.matmul, output in the same type).  Warm, back-to-back launches;
+    random codes in [-31, 31] (the same values in every type)."""
     dev = torch.device("cuda:0")
     g = torch.Generator(device=dev)
     g.manual_seed(0)
     shapes = {"dgrad": (M, wl.C_out, wl.C_in), "wgrad": (wl.C_out, M, wl.C_in)}
-    out = {}
-    for name, (m, k, n) in shapes.items():
-        a = torch.randint(-31, 32, (m, k), dtype=torch.int8, device=dev, generator=g)
-        b = torch.randint(-31, 32, (n, k), dtype=torch.int8, device=dev, generator=g).t()
+
+    def timed(fn):
         for _ in range(args.warmup):
-            torch._int_mm(a, b)
+            fn()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         for _ in range(args.steps):
-            torch._int_mm(a, b)
+            fn()
         e1.record()
         torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / args.steps
-        out[name] = {"ms": ms, "TOPS": 2.0 * m * n * k / ms / 1e9, "shape_mkn": [m, k, n]}
+        return e0.elapsed_time(e1) / args.steps
+
+    out = {}
+    for name, (m, k, n) in shapes.items():
+        a = torch.randint(-31, 32, (m, k), dtype=torch.int8, device=dev, generator=g)
+        b = torch.randint(-31, 32, (n, k), dtype=torch.int8, device=dev, generator=g)
+        ops = 2.0 * m * n * k
+        res = {"shape_mkn": [m, k, n]}
+        ms = timed(lambda: torch._int_mm(a, b.t()))
+        res["int8"] = {"ms": ms, "TOPS": ops / ms / 1e9}
+        for tname, dt in (("fp16", torch.float16), ("bf16", torch.bfloat16)):
+            af, bf = a.to(dt), b.to(dt)
+            ms = timed(lambda: torch.matmul(af, bf.t()))
+            res[tname] = {"ms": ms, "TFLOPS": ops / ms / 1e9}
+            del af, bf
+        out[name] = res
         del a, b
-    total_ms = sum(v["ms"] for v in out.values())
     ops = 4.0 * M * wl.C_out * wl.C_in
+    tot = {t: sum(v[t]["ms"] for v in out.values()) for t in ("int8", "fp16", "bf16")}
     print(json.dumps({"metric": "vendor int8 GEMM (torch._int_mm) TOPS on the backward product shapes",
-                      "value": ops / total_ms / 1e9, "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
-                      "warmup": args.warmup, "ms_per_step": total_ms, "higher_is_better": True, "dtype": "int8",
+                      "value": ops / tot["int8"] / 1e9, "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
+                      "warmup": args.warmup, "ms_per_step": tot["int8"], "higher_is_better": True, "dtype": "int8",
                       "data": "synthetic", "config": {"workload": wl.name, "M": M, "C_out": wl.C_out,
-                                                      "C_in": wl.C_in, "library": "hipBLASLt via torch._int_mm"},
-                      "per_product": out, "pct_int8_peak": 100.0 * ops / total_ms / 1e9 / PEAK_INT8_TOPS}))
+                                                      "C_in": wl.C_in, "library": "hipBLASLt via torch"},
+                      "fp16_ms_per_step": tot["fp16"], "fp16_TFLOPS": ops / tot["fp16"] / 1e9,
+                      "bf16_ms_per_step": tot["bf16"], "bf16_TFLOPS": ops / tot["bf16"] / 1e9,
+                      "per_product": out, "pct_int8_peak": 100.0 * ops / tot["int8"] / 1e9 / PEAK_INT8_TOPS}))
     return 0
 
 
@@ -552,7 +568,7 @@ def main(argv=None):
     ap.add_argument("--step", choices=["backward", "forward", "l1bn", "chain", "conv_chain", "vendor_gemm"],
                     default="backward",
                     help="forward: quantize X with ShiftQuant + Y = X W^T (per-output-channel W); "
-                         "vendor_gemm: the vendor int8 GEMM on the linear layer's two backward product shapes; "
+                         "vendor_gemm: the vendor int8, fp16 and bf16 GEMMs on the linear layer's two backward product shapes; "
                          "l1bn: the L1BNQ layer (workloads resnet18_bn_56x56x64, resnet50_bn_14x14x1024, "
                          "transformer_bn_768)")
     ap.add_argument("--conv-wgrad", choices=["implicit", "im2col"], default="implicit",
